@@ -1,0 +1,169 @@
+"""Seeded synthetic inputs shared by the tests, the benchmark and the smoke check.
+
+The heavy workloads are drawn by ``synth.c`` (compiled into ``_synth.so`` next
+to this file by :func:`build`); the small randomized edge-case traces are drawn
+here with numpy.  Nothing in this module computes energies: it only produces
+timestamps, power samples, interval bounds and operator keys.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SO = os.path.join(_HERE, "_synth.so")
+_lib = None
+
+
+def build() -> str:
+    """Compile synth.c into _synth.so with gcc (always recompiles)."""
+    src = os.path.join(_HERE, "synth.c")
+    tmp = _SO + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-o", tmp, src, "-lm"])
+    os.replace(tmp, _SO)
+    return _SO
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_SO):
+            build()
+        lib = ctypes.CDLL(_SO)
+        p = ctypes.c_void_p
+        lib.synth_shape.argtypes = [ctypes.c_int, p]
+        lib.synth_vocab.argtypes = [ctypes.c_int, ctypes.c_uint64, p]
+        lib.synth_structure.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_int, p, p, p, p, p]
+        lib.synth_power.argtypes = [ctypes.c_int, ctypes.c_uint64, ctypes.c_int, p, p, p, p, p, p]
+        lib.synth_mix64.argtypes = [ctypes.c_uint64]
+        lib.synth_mix64.restype = ctypes.c_uint64
+        _lib = lib
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def shape(cfg: int) -> dict:
+    """Sizes of workload ``cfg`` (1..5) per side."""
+    out = np.zeros(4, dtype=np.int64)
+    if _load().synth_shape(cfg, _ptr(out)) != 0:
+        raise ValueError(f"unknown workload {cfg}")
+    return {"n": int(out[0]), "m": int(out[1]), "K": int(out[2]), "streams": int(out[3])}
+
+
+N_SIDES = {1: 2, 2: 2, 3: 2, 4: 9, 5: 2}
+
+
+def vocab(cfg: int, seed: int = 0) -> np.ndarray:
+    sh = shape(cfg)
+    out = np.empty(sh["K"], dtype=np.uint64)
+    _load().synth_vocab(cfg, seed, _ptr(out))
+    return out
+
+
+def structure(cfg: int, seed: int = 0, side: int = 0) -> dict:
+    """Timestamps, interval bounds, keys and stream offsets of one side."""
+    sh = shape(cfg)
+    t = np.empty(sh["n"], dtype=np.float64)
+    s = np.empty(sh["m"], dtype=np.float64)
+    e = np.empty(sh["m"], dtype=np.float64)
+    key = np.empty(sh["m"], dtype=np.uint64)
+    off = np.empty(sh["streams"] + 1, dtype=np.int64)
+    rc = _load().synth_structure(cfg, seed, side, _ptr(t), _ptr(s), _ptr(e), _ptr(key), _ptr(off))
+    if rc != 0:
+        raise RuntimeError(f"synth_structure({cfg}) failed: {rc}")
+    return {"t": t, "s": s, "e": e, "key": key, "offsets": off}
+
+
+def power(cfg: int, st: dict, seed: int = 0, side: int = 0) -> np.ndarray:
+    """fp32 power samples of one side, drawn against the given structure."""
+    P = np.empty(st["t"].shape[0], dtype=np.float32)
+    rc = _load().synth_power(cfg, seed, side, _ptr(st["t"]), _ptr(st["s"]), _ptr(st["e"]),
+                             _ptr(st["key"]), _ptr(st["offsets"]), _ptr(P))
+    if rc != 0:
+        raise RuntimeError(f"synth_power({cfg}) failed: {rc}")
+    return P
+
+
+def trace(cfg: int, seed: int = 0, side: int = 0) -> dict:
+    st = structure(cfg, seed, side)
+    st["P"] = power(cfg, st, seed, side)
+    return st
+
+
+def sides(cfg: int, seed: int = 0, which=None) -> list:
+    """All sides of a workload; sides that share a structure share its arrays."""
+    which = list(range(N_SIDES[cfg])) if which is None else list(which)
+    out = []
+    base = None
+    for side in which:
+        if cfg == 5 or base is None:
+            st = structure(cfg, seed, side)
+            if cfg != 5:
+                base = st
+        else:
+            st = dict(base)
+        st = dict(st)
+        st["P"] = power(cfg, st, seed, side)
+        out.append(st)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# small randomized traces for edge cases (numpy)
+# ----------------------------------------------------------------------------
+
+def tiny_case(seed: int, n: int = 64, streams: int = 1, per_stream: int = 8,
+              snap: float = 0.3, zero_len: float = 0.1, outside: bool = True,
+              zero_power: float = 0.1, keys: int = 5, dyadic: bool = False) -> dict:
+    """A small random trace with the awkward cases the method has.
+
+    Intervals are sorted and non-overlapping within each stream; some bounds sit
+    exactly on sample times, some intervals have zero length, and (when
+    ``outside``) some start before the first sample or end after the last.
+    """
+    rng = np.random.default_rng(seed)
+    if dyadic:
+        steps = 2 ** rng.integers(0, 3, size=n - 1)  # 1, 2 or 4 ticks of 1/1024 s
+        t = np.concatenate([[0], np.cumsum(steps)]).astype(np.float64) / 1024.0
+        P = rng.integers(0, 1000, size=n).astype(np.float32)
+    else:
+        t = np.concatenate([[0.0], np.cumsum(rng.uniform(0.2, 1.8, size=n - 1))])
+        t += rng.uniform(-5, 5)
+        P = rng.uniform(0.0, 800.0, size=n).astype(np.float32)
+        P[rng.random(n) < zero_power] = 0.0
+    lo, hi = t[0], t[-1]
+    span = hi - lo
+    s_all, e_all, off = [], [], [0]
+    for _ in range(streams):
+        cnt = int(rng.integers(0, per_stream + 1))
+        a = lo - (0.1 * span if outside else 0.0)
+        b = hi + (0.1 * span if outside else 0.0)
+        cuts = np.sort(rng.uniform(a, b, size=2 * cnt))
+        if dyadic:
+            cuts = np.sort(np.round(cuts * 4096.0) / 4096.0)
+        if snap > 0 and cnt:
+            m = rng.random(2 * cnt) < snap
+            idx = np.clip(np.searchsorted(t, cuts), 0, n - 1)
+            cuts = np.where(m, t[idx], cuts)
+            cuts = np.sort(cuts)
+        s = cuts[0::2].copy()
+        e = cuts[1::2].copy()
+        if zero_len > 0 and cnt:
+            z = rng.random(cnt) < zero_len
+            e = np.where(z, s, e)
+        s_all.append(s)
+        e_all.append(e)
+        off.append(off[-1] + cnt)
+    s = np.concatenate(s_all) if s_all else np.zeros(0)
+    e = np.concatenate(e_all) if e_all else np.zeros(0)
+    key_vocab = rng.integers(0, 2**63, size=keys, dtype=np.int64).astype(np.uint64) * np.uint64(2) + \
+        rng.integers(0, 2, size=keys).astype(np.uint64)
+    key = key_vocab[rng.integers(0, keys, size=s.shape[0])] if s.shape[0] else np.zeros(0, np.uint64)
+    return {"t": t.astype(np.float64), "P": P, "s": s.astype(np.float64), "e": e.astype(np.float64),
+            "key": key.astype(np.uint64), "offsets": np.array(off, dtype=np.int64)}
