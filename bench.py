@@ -1,0 +1,239 @@
+#!/usr/bin/env python3
+"""Throughput of operator energy attribution + A/B diff on one MI355X.
+
+One step = the whole path over one A/B pair of the multi-stream workload
+(100,000,000 power samples at 1 MHz, 4 concurrent streams x 1,000,000
+operator intervals, 5,000 Zipf(1.2) keys): attribute side A, attribute side B
+(equal split of concurrent power, per-interval energies and sample indices,
+per-key count/sum/M2), then join and rank the top-100 excess-energy keys.
+Inputs are synthetic, seeded and resident in HBM before timing.
+
+Prints ONE JSON line.  `value` is operator intervals attributed per second
+(both sides); samples/s and the pipeline's algorithmic HBM GB/s ride along.
+`roofline` covers the dominant kernel (the interval-energy tile kernel),
+timed with HIP events on the call's stream; `cpu_baseline` is the CPU oracle
+timed on this host's cores over both sides of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E
+METRIC = "operator intervals attributed/sec + power samples/sec; achieved HBM GB/s"
+WORKLOAD = 3
+TOP_K = 100
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_hash() -> str:
+    h = hashlib.sha256()
+    with open(os.path.join(ROOT, "paper_2512_08365_amd", "csrc", "attr_tile.hip"), "rb") as f:
+        h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def counters_traffic(bytes_alg: float):
+    """HBM traffic of the tile kernel from the committed counter summary, if it
+    was taken on the current kernel source (else None)."""
+    path = os.path.join(ROOT, "profiles", "tile_kernel_counters.json")
+    try:
+        with open(path) as f:
+            d = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if d.get("source_hash") != source_hash():
+        return None
+    return d.get("traffic_bytes_per_launch")
+
+
+class Side:
+    """Device copies of one side plus preallocated outputs and workspace."""
+
+    def __init__(self, c, lib, N, torch, k_cap):
+        import numpy as np
+        self.n = int(c["t"].shape[0])
+        self.m = int(c["s"].shape[0])
+        self.off = [int(x) for x in c["offsets"]]
+        dev = "cuda"
+        self.t = torch.from_numpy(c["t"]).to(dev)
+        self.P = torch.from_numpy(c["P"]).to(dev)
+        self.s = torch.from_numpy(c["s"]).to(dev)
+        self.e = torch.from_numpy(c["e"]).to(dev)
+        self.key = torch.from_numpy(np.ascontiguousarray(c["key"]).view(np.int64)).to(dev)
+        self.energy = torch.empty(self.m, dtype=torch.float64, device=dev)
+        self.si = torch.empty(self.m, dtype=torch.int64, device=dev)
+        self.ei = torch.empty(self.m, dtype=torch.int64, device=dev)
+        self.kout = torch.empty(k_cap, dtype=torch.int64, device=dev)
+        self.ksum = torch.empty(k_cap, dtype=torch.float64, device=dev)
+        self.km2 = torch.empty(k_cap, dtype=torch.float64, device=dev)
+        self.kcnt = torch.empty(k_cap, dtype=torch.int64, device=dev)
+        self.k_cap = k_cap
+        self.offs = (ctypes.c_int64 * len(self.off))(*self.off)
+        self.opts = N.AttrOpts(len(self.off) - 1, N.MAG_EQUAL_SPLIT | N.MAG_TIME_KERNELS,
+                               ctypes.cast(self.offs, ctypes.c_void_p))
+        b = ctypes.c_size_t(0)
+        rc = lib.mag_attribute_workspace_size(self.n, self.m, k_cap, ctypes.byref(self.opts),
+                                              ctypes.byref(b))
+        assert rc == 0
+        self.ws = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
+        self.pio = N.IntervalOut(self.energy.data_ptr(), self.si.data_ptr(), self.ei.data_ptr())
+        self.ks = N.KeyStats(self.ksum.data_ptr(), self.km2.data_ptr(), self.kcnt.data_ptr(), k_cap, 0)
+        self.summ = N.Summary()
+
+    def attribute(self, lib, stream):
+        rc = lib.mag_attribute(self.t.data_ptr(), self.P.data_ptr(), self.n, self.s.data_ptr(),
+                               self.e.data_ptr(), self.key.data_ptr(), self.m,
+                               ctypes.byref(self.opts), ctypes.byref(self.pio), self.kout.data_ptr(),
+                               ctypes.byref(self.ks), ctypes.byref(self.summ), self.ws.data_ptr(),
+                               self.ws.numel(), stream)
+        if rc != 0:
+            raise RuntimeError(f"mag_attribute failed {rc}: {lib.mag_last_error().decode()}")
+        return self.summ.tile_kernel_ms
+
+
+def cpu_baseline(A, B):
+    """The oracle, as it stands, on both sides of the workload (one core)."""
+    import oracle
+    t0 = time.perf_counter()
+    tabs = []
+    for c in (A, B):
+        r = oracle.attribute(c["t"], c["P"], c["s"], c["e"], c["offsets"])
+        tabs.append(oracle.groupby(c["key"], r["energy"]))
+    oracle.diff(tabs[0], tabs[1], TOP_K)
+    dt = time.perf_counter() - t0
+    m = A["s"].shape[0] + B["s"].shape[0]
+    return {"value": m / dt, "unit": "intervals/s", "cores": 1, "kind": "oracle",
+            "sample": ("both sides of the benchmark workload (2 x 100,000,000 samples, "
+                       f"2 x 4,000,000 intervals), attribution + grouping + top-{TOP_K} diff, "
+                       f"{dt:.1f} s on one host core"),
+            "seconds": round(dt, 2),
+            "samples_per_s": (A["t"].shape[0] + B["t"].shape[0]) / dt}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
+              "(the multi-GPU sharding is design-only).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np  # noqa: F401
+    import torch
+
+    import paper_2512_08365_amd as mag
+    from paper_2512_08365_amd import _native as N
+    import synth
+
+    if not torch.cuda.is_available():
+        log("bench.py needs a GPU")
+        sys.exit(1)
+    lib = N.load()
+    log(f"[bench] {mag.version()} on {torch.cuda.get_device_name(0)}")
+    t0 = time.perf_counter()
+    A, B = synth.sides(WORKLOAD, args.seed)
+    log(f"[bench] generated workload in {time.perf_counter() - t0:.1f} s")
+    sh = synth.shape(WORKLOAD)
+    k_cap = 8192
+    sa = Side(A, lib, N, torch, k_cap)
+    sb = Side(B, lib, N, torch, k_cap)
+    torch.cuda.synchronize()
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    # diff buffers
+    dev = "cuda"
+    dcap = TOP_K
+    d_out = {k: torch.empty(dcap, dtype=dt, device=dev) for k, dt in
+             (("key", torch.int64), ("ratio", torch.float64), ("ea", torch.float64),
+              ("eb", torch.float64), ("ca", torch.int64), ("cb", torch.int64))}
+    b = ctypes.c_size_t(0)
+    lib.mag_diff_workspace_size(k_cap, k_cap, TOP_K, ctypes.byref(b))
+    d_ws = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
+    ro = N.RankOut(d_out["key"].data_ptr(), d_out["ratio"].data_ptr(), d_out["ea"].data_ptr(),
+                   d_out["eb"].data_ptr(), d_out["ca"].data_ptr(), d_out["cb"].data_ptr(), dcap,
+                   0, 0, 0, 0)
+
+    tile_ms = []
+
+    def step(record):
+        ta = sa.attribute(lib, stream)
+        tb = sb.attribute(lib, stream)
+        rc = lib.mag_diff(sa.kout.data_ptr(), ctypes.byref(sa.ks), sb.kout.data_ptr(),
+                          ctypes.byref(sb.ks), TOP_K, ctypes.byref(ro), d_ws.data_ptr(),
+                          d_ws.numel(), stream)
+        if rc != 0:
+            raise RuntimeError(f"mag_diff failed {rc}: {lib.mag_last_error().decode()}")
+        if record:
+            tile_ms.extend([ta, tb])
+
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(True)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    sec_per_step = dt / args.steps
+    log(f"[bench] {args.steps} steps in {dt:.3f} s -> {sec_per_step * 1e3:.3f} ms/step; "
+        f"keys A={sa.ks.n_keys} B={sb.ks.n_keys} joined={ro.n_join}")
+
+    n, m = sh["n"], sh["m"]
+    intervals = 2 * m
+    samples = 2 * n
+    bytes_step = 2 * (12 * n + 48 * m)  # algorithmic bytes of the step (see design notes)
+    tile_bytes = 12 * n + 40 * m        # per launch of the tile kernel
+    tile_avg_ms = sum(tile_ms) / len(tile_ms)
+    achieved = tile_bytes / (tile_avg_ms * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": intervals / sec_per_step,
+        "unit": "intervals/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": sec_per_step * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": ("multi-stream trace: 100,000,000 fp32 power samples at 1 MHz, "
+                                "4 concurrent streams x 1,000,000 intervals (equal split), "
+                                "5,000 Zipf(1.2) keys; A+B attribution + top-100 diff"),
+                   "n_samples_per_side": n, "n_intervals_per_side": m, "streams": 4,
+                   "keys": sh["K"], "top_k": TOP_K, "sides": 2, "seed": args.seed},
+        "samples_per_s": samples / sec_per_step,
+        "hbm_gbps_algorithmic": bytes_step / sec_per_step / 1e9,
+        "hbm_frac_algorithmic": bytes_step / sec_per_step / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"kernel": "k_tile (interval energies)", "bound": "hbm",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": counters_traffic(tile_bytes),
+                     "algorithmic_bytes_per_launch": tile_bytes,
+                     "avg_launch_ms": tile_avg_ms},
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on both sides ...")
+        result["cpu_baseline"] = cpu_baseline(A, B)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

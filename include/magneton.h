@@ -1,0 +1,211 @@
+/*
+ * magneton.h -- C ABI of the MI355X operator energy attribution library.
+ *
+ * The library implements the data-parallel core of differential energy
+ * debugging (Magneton, arXiv 2512.08365): a sampled power trace is integrated
+ * over operator/kernel execution intervals (Section 5.2, which asks for energy
+ * attributed to individual kernels lasting tens to hundreds of microseconds),
+ * the interval energies are aggregated per operator key (Section 4.1 makes
+ * the operator the unit of comparison; Section 2.1 ranks operators by energy),
+ * and the per-key energies of two systems running the same workload are
+ * joined and ranked by their relative difference (Section 6.1 flags operators
+ * whose energy differs by more than a threshold; Table "tab:energy-profiling"
+ * fixes the sign convention (value - reference) / reference).
+ *
+ * Conventions for every entry point:
+ *   - All array arguments are DEVICE pointers to caller-owned memory (for
+ *     example torch tensors on the current HIP device), unless documented as
+ *     host.  The library never allocates device memory and keeps no pointer
+ *     after a call returns.  Scratch memory is the caller's `workspace`.
+ *   - Work is enqueued on `stream`.  Entry points that return data-dependent
+ *     sizes or device-detected errors synchronize `stream` before returning.
+ *   - Return value: MAG_OK (0) or a negative MAG_E_* code.  No exception
+ *     crosses the ABI.  On error, device outputs are unspecified;
+ *     mag_last_error() gives a human-readable detail (thread-local).
+ *   - Energies are joules (fp64) when timestamps are seconds and power watts.
+ */
+#ifndef MAGNETON_H
+#define MAGNETON_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+#define MAG_OK 0
+#define MAG_E_NULL (-1)       /* a required pointer is NULL                          */
+#define MAG_E_SIZE (-2)       /* n_samples < 2, a negative count, k < 0               */
+#define MAG_E_CAPACITY (-3)   /* more distinct keys than the key table capacity       */
+#define MAG_E_WORKSPACE (-4)  /* workspace too small (or misaligned: 256 B required)  */
+#define MAG_E_TIMESTAMPS (-5) /* timestamps not finite or not strictly increasing     */
+#define MAG_E_POWER (-6)      /* a power sample is NaN, infinite or negative          */
+#define MAG_E_INTERVAL (-7)   /* start > end, non-finite bound, or a stream whose     */
+                              /* intervals are unsorted or overlap                    */
+#define MAG_E_STREAMS (-8)    /* bad n_streams or stream_offsets                      */
+#define MAG_E_STATE (-9)      /* streaming handle used out of order                   */
+#define MAG_E_HIP (-10)       /* a HIP runtime call failed                            */
+#define MAG_E_ALIGN (-11)     /* a device array is not aligned to its element size    */
+#define MAG_E_KEYS (-12)      /* a key table passed to mag_diff is not strictly       */
+                              /* ascending                                            */
+
+/* ----------------------------------------------------------------- flags */
+/* Split the power at each instant equally among the intervals active at that
+   instant (several concurrent streams).  Without it every interval receives
+   the full power over its span. */
+#define MAG_EQUAL_SPLIT 0x1u
+/* Skip the device-side input checks (sortedness, finiteness, signs). */
+#define MAG_SKIP_VALIDATE 0x2u
+/* Time the call on `stream` with HIP events and report it in mag_summary. */
+#define MAG_TIME_KERNELS 0x4u
+
+/* Most concurrent streams one call accepts. */
+#define MAG_MAX_STREAMS 32
+
+typedef struct mag_attr_opts {
+    int32_t n_streams;              /* >= 1; intervals are concatenated by stream   */
+    uint32_t flags;                 /* MAG_EQUAL_SPLIT | MAG_SKIP_VALIDATE |          */
+                                    /* MAG_TIME_KERNELS                               */
+    const int64_t* stream_offsets;  /* HOST int64[n_streams + 1]: stream a owns       */
+                                    /* intervals [offs[a], offs[a+1]); offs[0] = 0,   */
+                                    /* offs[n_streams] = n_intervals; NULL allowed    */
+                                    /* only when n_streams == 1                       */
+} mag_attr_opts;
+
+/* Per-interval outputs (device arrays of n_intervals entries; any may be NULL). */
+typedef struct mag_interval_out {
+    double* energy;     /* E_i, J                                                  */
+    int64_t* start_idx; /* lower_bound(timestamps, starts[i]) in [0, n_samples]     */
+    int64_t* end_idx;   /* lower_bound(timestamps, ends[i])   in [0, n_samples]     */
+} mag_interval_out;
+
+/* Per-key statistics (device arrays of `capacity` rows, ascending key order). */
+typedef struct mag_key_stats {
+    double* sum;      /* sum of E_i over the key's intervals                      */
+    double* m2;       /* sum of (E_i - mean)^2 over the key's intervals            */
+    int64_t* count;   /* number of intervals carrying the key                      */
+    int64_t capacity; /* rows available in each array (host value)                 */
+    int64_t n_keys;   /* rows filled (host value): output of mag_attribute, input  */
+                      /* of mag_diff                                               */
+} mag_key_stats;
+
+/* Whole-trace figures (host struct). */
+typedef struct mag_summary {
+    double trace_energy;      /* integral of the power over [t_0, t_{n-1}]          */
+    double idle_energy;       /* energy at instants where no interval is active     */
+    double attributed_energy; /* sum of all E_i                                     */
+    int64_t n_clipped;        /* intervals with start < t_0 or end > t_{n-1}        */
+    int64_t n_keys;           /* distinct keys (also when over capacity)            */
+    double tile_kernel_ms;    /* MAG_TIME_KERNELS: duration of the interval-energy  */
+                              /* kernel (HIP events on `stream`), else 0            */
+    double device_ms;         /* MAG_TIME_KERNELS: all device work of the call      */
+} mag_summary;
+
+/* Ranked join of two key tables (device arrays of `capacity` rows). */
+typedef struct mag_rank_out {
+    uint64_t* key;
+    double* ratio;    /* (E_B - E_A) / E_A; +inf when E_A = 0 < E_B; 0 when both 0  */
+    double* energy_a;
+    double* energy_b;
+    int64_t* count_a;
+    int64_t* count_b;
+    int64_t capacity; /* rows available (host), must be >= min(k, keys joined)      */
+    int64_t n_out;    /* rows written (host output)                                  */
+    int64_t n_only_a; /* keys present only in A (host output)                        */
+    int64_t n_only_b; /* keys present only in B (host output)                        */
+    int64_t n_join;   /* keys present in both (host output)                          */
+} mag_rank_out;
+
+/*
+ * mag_attribute_workspace_size -- bytes of device workspace mag_attribute needs
+ * for the given sizes, key-table capacity (0 when no per-key output is asked
+ * for) and options.  Host only; no device work.  Returns MAG_OK or
+ * MAG_E_SIZE / MAG_E_STREAMS / MAG_E_NULL.
+ */
+int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
+                                 const mag_attr_opts* opts, size_t* bytes);
+
+/*
+ * mag_attribute -- attribute the energy of a sampled power trace to operator
+ * intervals, and aggregate it per operator key.
+ *
+ * The paper asks for per-kernel energy from a microsecond-resolution power
+ * source (Section 5.2) and compares operators (Section 4.1); it does not give
+ * the integration rule.  This library's definition:
+ *   P^(x)  = piecewise-linear interpolant of (timestamps[j], power[j]) on
+ *            [t_0, t_{n-1}], zero outside;
+ *   m(x)   = number of intervals i with starts[i] <= x < ends[i];
+ *   E_i    = integral over [starts[i], ends[i]] of P^(x) / m(x)  (MAG_EQUAL_SPLIT)
+ *          = integral over [starts[i], ends[i]] of P^(x)          (otherwise).
+ * Per key: count, sum of E_i and M2 = sum of (E_i - mean)^2; rows ascending by
+ * unsigned key.  Every energy is computed as a sum of non-negative pieces (no
+ * difference of running totals), in fp64.
+ *
+ * Arguments (device arrays unless noted):
+ *   timestamps[n_samples] fp64, strictly increasing, finite (seconds)
+ *   power[n_samples]      fp32, finite, >= 0 (watts)
+ *   starts/ends[n_intervals] fp64, starts <= ends; within each stream sorted
+ *                          and non-overlapping (ends[i] <= starts[i+1])
+ *   op_keys[n_intervals]  uint64 operator key (any value); may be NULL when
+ *                          per_key is NULL
+ *   opts                  host; NULL means one stream with MAG_EQUAL_SPLIT
+ *   per_interval          host struct of device pointers; may be NULL
+ *   keys_out[capacity]    device uint64, ascending distinct keys; NULL iff
+ *                          per_key is NULL
+ *   per_key               host struct of device arrays; may be NULL to skip
+ *                          the grouping; n_keys is written back
+ *   summary               host struct; may be NULL
+ *   workspace             device, >= mag_attribute_workspace_size(...,
+ *                          per_key ? per_key->capacity : 0, opts) bytes,
+ *                          256-byte aligned; its contents are scratch
+ * Synchronizes `stream`.  Errors: MAG_E_NULL, MAG_E_SIZE, MAG_E_STREAMS,
+ * MAG_E_WORKSPACE, MAG_E_ALIGN (host-detected, before any device work);
+ * MAG_E_TIMESTAMPS, MAG_E_POWER, MAG_E_INTERVAL (device-detected, unless
+ * MAG_SKIP_VALIDATE); MAG_E_CAPACITY (n_keys and summary->n_keys still report
+ * the number of distinct keys; the key rows are unspecified); MAG_E_HIP.
+ */
+int mag_attribute(const double* timestamps, const float* power, int64_t n_samples,
+                  const double* starts, const double* ends, const uint64_t* op_keys,
+                  int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
+                  uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary, void* workspace,
+                  size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * mag_diff_workspace_size -- device workspace bytes for mag_diff.  Host only.
+ */
+int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_t* bytes);
+
+/*
+ * mag_diff -- join two per-key tables and rank the keys by relative energy
+ * difference (Section 6.1 compares the energy of matched operators; Table
+ * "tab:energy-profiling" uses (value - reference) / reference).
+ *   keysA[statsA->n_keys], keysB[statsB->n_keys]: strictly ascending uint64
+ *   (as produced by mag_attribute); statsA/statsB: host structs of device
+ *   arrays (sum and count are read).  Rows are the keys present in both
+ *   tables, r = (sum_B - sum_A) / sum_A (+inf if sum_A = 0 < sum_B, 0 if both
+ *   are 0), ordered by r descending then key ascending (unsigned); the first
+ *   min(k, joined) rows are written to out (device arrays, host counts).
+ * Synchronizes `stream`.  Errors: MAG_E_NULL, MAG_E_SIZE (k < 0 or a negative
+ * n_keys), MAG_E_CAPACITY (out->capacity < min(k, joined) possible rows, i.e.
+ * < min(k, n_keys_a)), MAG_E_WORKSPACE, MAG_E_KEYS, MAG_E_HIP.
+ */
+int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
+             size_t workspace_bytes, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* mag_strerror(int status);
+/* Detail of the last error on the calling thread ("" if none). */
+const char* mag_last_error(void);
+/* Library version string. */
+const char* mag_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MAGNETON_H */

@@ -1,0 +1,181 @@
+"""MI355X operator energy attribution and A/B energy comparison.
+
+Thin Python binding over libmagneton.so (C ABI in include/magneton.h).  Torch
+is used only to allocate device memory and to name the current HIP stream;
+every step of the computation runs in the library's HIP kernels.  There is no
+CPU fallback: if the library is missing, or the device is not a GPU, the calls
+raise.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _native as N
+
+__all__ = ["MagnetonError", "attribute", "diff", "workspace_size", "diff_workspace_size",
+           "version", "EQUAL_SPLIT", "SKIP_VALIDATE"]
+
+EQUAL_SPLIT = N.MAG_EQUAL_SPLIT
+SKIP_VALIDATE = N.MAG_SKIP_VALIDATE
+
+
+class MagnetonError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"[{code}] {msg}")
+        self.code = code
+
+
+def _lib():
+    return N.load()
+
+
+def _check(rc: int):
+    if rc != N.MAG_OK:
+        lib = _lib()
+        detail = lib.mag_last_error().decode() or lib.mag_strerror(rc).decode()
+        raise MagnetonError(rc, detail)
+
+
+def version() -> str:
+    return _lib().mag_version().decode()
+
+
+def _opts(n_streams: int, stream_offsets, flags: int):
+    o = N.AttrOpts()
+    o.n_streams = int(n_streams)
+    o.flags = int(flags)
+    keep = None
+    if stream_offsets is not None:
+        keep = (ctypes.c_int64 * len(stream_offsets))(*[int(x) for x in stream_offsets])
+        o.stream_offsets = ctypes.cast(keep, ctypes.c_void_p)
+    return o, keep
+
+
+def _dev_ptr(x, dtype, name):
+    if x is None:
+        return None
+    if not isinstance(x, torch.Tensor) or not x.is_cuda:
+        raise MagnetonError(N.MAG_E_NULL, f"{name} must be a GPU tensor")
+    if x.dtype != dtype:
+        raise MagnetonError(N.MAG_E_SIZE, f"{name} must be {dtype}, got {x.dtype}")
+    if not x.is_contiguous():
+        raise MagnetonError(N.MAG_E_SIZE, f"{name} must be contiguous")
+    return x.data_ptr()
+
+
+def workspace_size(n_samples: int, n_intervals: int, key_capacity: int = 0, n_streams: int = 1,
+                   stream_offsets=None, flags: int = EQUAL_SPLIT) -> int:
+    o, keep = _opts(n_streams, stream_offsets, flags)
+    b = ctypes.c_size_t(0)
+    _check(_lib().mag_attribute_workspace_size(n_samples, n_intervals, key_capacity,
+                                                ctypes.byref(o), ctypes.byref(b)))
+    return int(b.value)
+
+
+def diff_workspace_size(n_keys_a: int, n_keys_b: int, k: int) -> int:
+    b = ctypes.c_size_t(0)
+    _check(_lib().mag_diff_workspace_size(n_keys_a, n_keys_b, k, ctypes.byref(b)))
+    return int(b.value)
+
+
+def _stream_handle(device):
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
+              equal_split: bool = True, validate: bool = True, key_capacity: int | None = None,
+              indices: bool = True, workspace=None, out=None):
+    """Attribute the energy of a power trace to intervals and group it by key.
+
+    t: float64 [n] timestamps (s), P: float32 [n] power (W), s/e: float64 [m]
+    interval bounds, keys: int64 [m] (bits read as uint64) or None.
+    Returns (per_interval, per_key, summary): dicts of tensors / numbers.
+    """
+    lib = _lib()
+    n = int(t.shape[0])
+    m = int(s.shape[0])
+    dev = t.device
+    flags = (EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE)
+    o, keep = _opts(n_streams, stream_offsets, flags)
+    group = keys is not None
+    cap = int(key_capacity) if key_capacity is not None else max(1, m)
+    ws_bytes = workspace_size(n, m, cap if group else 0, n_streams, stream_offsets, flags)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    out = out or {}
+    energy = out.get("energy")
+    if energy is None:
+        energy = torch.empty(m, dtype=torch.float64, device=dev)
+    si = ei = None
+    if indices:
+        si = out.get("start_idx")
+        ei = out.get("end_idx")
+        if si is None:
+            si = torch.empty(m, dtype=torch.int64, device=dev)
+        if ei is None:
+            ei = torch.empty(m, dtype=torch.int64, device=dev)
+    pio = N.IntervalOut(_dev_ptr(energy, torch.float64, "energy"),
+                        _dev_ptr(si, torch.int64, "start_idx"), _dev_ptr(ei, torch.int64, "end_idx"))
+    ks = None
+    kout = ksum = km2 = kcnt = None
+    if group:
+        kout = torch.empty(cap, dtype=torch.int64, device=dev)
+        ksum = torch.empty(cap, dtype=torch.float64, device=dev)
+        km2 = torch.empty(cap, dtype=torch.float64, device=dev)
+        kcnt = torch.empty(cap, dtype=torch.int64, device=dev)
+        ks = N.KeyStats(ksum.data_ptr(), km2.data_ptr(), kcnt.data_ptr(), cap, 0)
+    summ = N.Summary()
+    rc = lib.mag_attribute(
+        _dev_ptr(t, torch.float64, "t"), _dev_ptr(P, torch.float32, "P"), n,
+        _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
+        _dev_ptr(keys, torch.int64, "keys") if group else None, m, ctypes.byref(o),
+        ctypes.byref(pio), kout.data_ptr() if group else None,
+        ctypes.byref(ks) if group else None, ctypes.byref(summ), workspace.data_ptr(),
+        workspace.numel(), _stream_handle(dev))
+    _check(rc)
+    per_interval = {"energy": energy}
+    if indices:
+        per_interval["start_idx"] = si
+        per_interval["end_idx"] = ei
+    per_key = None
+    if group:
+        nk = int(ks.n_keys)
+        per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+    summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
+               "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
+               "n_keys": int(summ.n_keys)}
+    return per_interval, per_key, summary
+
+
+def diff(a: dict, b: dict, k: int, workspace=None):
+    """Rank keys present in both per-key tables by (E_B - E_A)/E_A (descending,
+    ties by ascending key).  a/b: per-key dicts as returned by attribute()."""
+    lib = _lib()
+    dev = a["keys"].device
+    na, nb = int(a["keys"].shape[0]), int(b["keys"].shape[0])
+    ws_bytes = diff_workspace_size(na, nb, k)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    cap = max(1, min(int(k), na))
+    key = torch.empty(cap, dtype=torch.int64, device=dev)
+    ratio = torch.empty(cap, dtype=torch.float64, device=dev)
+    ea = torch.empty(cap, dtype=torch.float64, device=dev)
+    eb = torch.empty(cap, dtype=torch.float64, device=dev)
+    ca = torch.empty(cap, dtype=torch.int64, device=dev)
+    cb = torch.empty(cap, dtype=torch.int64, device=dev)
+    sa = N.KeyStats(_dev_ptr(a["sum"], torch.float64, "a.sum"), a["m2"].data_ptr() if "m2" in a else None,
+                    _dev_ptr(a["count"], torch.int64, "a.count"), na, na)
+    sb = N.KeyStats(_dev_ptr(b["sum"], torch.float64, "b.sum"), b["m2"].data_ptr() if "m2" in b else None,
+                    _dev_ptr(b["count"], torch.int64, "b.count"), nb, nb)
+    ro = N.RankOut(key.data_ptr(), ratio.data_ptr(), ea.data_ptr(), eb.data_ptr(), ca.data_ptr(),
+                   cb.data_ptr(), cap, 0, 0, 0, 0)
+    rc = lib.mag_diff(_dev_ptr(a["keys"], torch.int64, "a.keys"), ctypes.byref(sa),
+                      _dev_ptr(b["keys"], torch.int64, "b.keys"), ctypes.byref(sb), int(k),
+                      ctypes.byref(ro), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
+    _check(rc)
+    r = int(ro.n_out)
+    return {"key": key[:r], "ratio": ratio[:r], "energy_a": ea[:r], "energy_b": eb[:r],
+            "count_a": ca[:r], "count_b": cb[:r], "n_only_a": int(ro.n_only_a),
+            "n_only_b": int(ro.n_only_b), "n_join": int(ro.n_join)}

@@ -1,0 +1,96 @@
+"""ctypes view of libmagneton.so (declarations mirror include/magneton.h)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libmagneton.so")
+
+c_i64 = ctypes.c_int64
+c_vp = ctypes.c_void_p
+
+MAG_OK = 0
+MAG_E_NULL = -1
+MAG_E_SIZE = -2
+MAG_E_CAPACITY = -3
+MAG_E_WORKSPACE = -4
+MAG_E_TIMESTAMPS = -5
+MAG_E_POWER = -6
+MAG_E_INTERVAL = -7
+MAG_E_STREAMS = -8
+MAG_E_STATE = -9
+MAG_E_HIP = -10
+MAG_E_ALIGN = -11
+MAG_E_KEYS = -12
+
+MAG_EQUAL_SPLIT = 0x1
+MAG_SKIP_VALIDATE = 0x2
+MAG_TIME_KERNELS = 0x4
+MAG_MAX_STREAMS = 32
+
+# every symbol include/magneton.h declares
+EXPORTED = (
+    "mag_attribute_workspace_size", "mag_attribute", "mag_diff_workspace_size", "mag_diff",
+    "mag_strerror", "mag_last_error", "mag_version",
+)
+
+
+class AttrOpts(ctypes.Structure):
+    _fields_ = [("n_streams", ctypes.c_int32), ("flags", ctypes.c_uint32),
+                ("stream_offsets", c_vp)]
+
+
+class IntervalOut(ctypes.Structure):
+    _fields_ = [("energy", c_vp), ("start_idx", c_vp), ("end_idx", c_vp)]
+
+
+class KeyStats(ctypes.Structure):
+    _fields_ = [("sum", c_vp), ("m2", c_vp), ("count", c_vp), ("capacity", c_i64),
+                ("n_keys", c_i64)]
+
+
+class Summary(ctypes.Structure):
+    _fields_ = [("trace_energy", ctypes.c_double), ("idle_energy", ctypes.c_double),
+                ("attributed_energy", ctypes.c_double), ("n_clipped", c_i64), ("n_keys", c_i64),
+                ("tile_kernel_ms", ctypes.c_double), ("device_ms", ctypes.c_double)]
+
+
+class RankOut(ctypes.Structure):
+    _fields_ = [("key", c_vp), ("ratio", c_vp), ("energy_a", c_vp), ("energy_b", c_vp),
+                ("count_a", c_vp), ("count_b", c_vp), ("capacity", c_i64), ("n_out", c_i64),
+                ("n_only_a", c_i64), ("n_only_b", c_i64), ("n_join", c_i64)]
+
+
+_lib = None
+
+
+def load(path: str = LIB_PATH):
+    """Load the HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{path} is missing: build the HIP library first (python -c 'import __graft_entry__ as g; g.build()')")
+    lib = ctypes.CDLL(path)
+    P = ctypes.POINTER
+    lib.mag_attribute_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(AttrOpts), P(ctypes.c_size_t)]
+    lib.mag_attribute_workspace_size.restype = ctypes.c_int
+    lib.mag_attribute.argtypes = [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),
+                                  P(IntervalOut), c_vp, P(KeyStats), P(Summary), c_vp,
+                                  ctypes.c_size_t, c_vp]
+    lib.mag_attribute.restype = ctypes.c_int
+    lib.mag_diff_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
+    lib.mag_diff_workspace_size.restype = ctypes.c_int
+    lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,
+                             ctypes.c_size_t, c_vp]
+    lib.mag_diff.restype = ctypes.c_int
+    lib.mag_strerror.argtypes = [ctypes.c_int]
+    lib.mag_strerror.restype = ctypes.c_char_p
+    lib.mag_last_error.argtypes = []
+    lib.mag_last_error.restype = ctypes.c_char_p
+    lib.mag_version.argtypes = []
+    lib.mag_version.restype = ctypes.c_char_p
+    _lib = lib
+    return lib

@@ -1,0 +1,167 @@
+// mag_internal.hpp -- shared definitions of the HIP kernels and the host
+// orchestration of the attribution library (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/magneton.h"
+
+namespace mag {
+
+// ---------------------------------------------------------------- tiling
+// A tile is TILE consecutive sample segments [t_j, t_{j+1}] (TILE + 1 samples,
+// the last one shared with the next tile).  TILE_THREADS threads each own
+// SEG_PER_THREAD consecutive segments.  Interval endpoints that fall inside a
+// tile are processed in rounds of at most ROUND_EVENTS endpoints.
+constexpr int TILE = 2048;
+constexpr int TILE_THREADS = 256;
+constexpr int SEG_PER_THREAD = TILE / TILE_THREADS;  // 8
+constexpr int ROUND_EVENTS = 512;
+constexpr int MAX_STREAMS = MAG_MAX_STREAMS;
+constexpr int TILE_WGS_PER_CU = 3;  // resident tile workgroups per CU (LDS-limited)
+
+// group-by
+constexpr int AGG_THREADS = 256;
+constexpr int AGG_IDS = 4096;       // key ids per LDS table (count u32 + sum f64)
+constexpr int AGG_MAX_CHUNKS = 256; // interval chunks (partial tables)
+
+// device-side error bits
+enum : uint32_t {
+    ERR_TIMESTAMPS = 1u,
+    ERR_POWER = 2u,
+    ERR_INTERVAL = 4u,
+    ERR_KEYS = 8u,
+};
+
+// small device status block at the head of every workspace
+struct Status {
+    uint32_t err;
+    uint32_t n_inserted;  // distinct keys inserted into the hash table
+    uint32_t special;     // the all-ones key was seen (stored out of band)
+    uint32_t overflow;    // a key found no free slot
+    unsigned long long n_clipped;
+    uint32_t n_unique;    // rows of the compacted distinct-key list
+    uint32_t n_cand;      // diff: surviving candidates
+    uint32_t n_join;      // diff: keys present on both sides
+    uint32_t pad0;
+    double trace_energy;
+    double idle_energy;
+    double attributed_energy;
+    double bounds[2];     // t_0 and t_{n-1}
+};
+static_assert(sizeof(Status) <= 256, "status block");
+
+struct StreamSet {
+    int32_t S;
+    int32_t pad;
+    int64_t off[MAX_STREAMS + 1];
+};
+
+struct TileParams {
+    const double* t;    // sample g (global index) is t[g - base]
+    const float* P;
+    int64_t base;
+    int64_t nseg;       // segments of the whole trace (n_samples - 1)
+    int64_t n_total;    // samples of the whole trace
+    int64_t tile_begin; // global tile range of this launch
+    int64_t tile_end;
+    int64_t tiles_per_wg;
+    int64_t NT;         // tiles of the whole trace
+    const double* s;
+    const double* e;
+    StreamSet ss;
+    double* energy;
+    int64_t* start_idx;
+    int64_t* end_idx;
+    int64_t* cnt;       // [S][NT+1] endpoints <= tile start time, per stream
+    int64_t* cnt_fin;   // [S][NT+1] cursor of a workgroup after its last tile (at that tile's end)
+    double* head;       // [S][NT] in-tile energy of the interval active at tile start
+    double* tail;       // [S][NT] in-tile energy of the interval started in the tile, active at its end
+    double* tileW;      // [NT]
+    double* tileIdle;   // [NT]
+    Status* status;
+    int split;
+    int validate;
+};
+
+struct FixParams {
+    const double* s;
+    const double* e;
+    StreamSet ss;
+    int64_t NT;
+    int64_t n_total;
+    int64_t tile_begin;   // workgroup boundaries of the tile launch: tile_begin + w * tiles_per_wg
+    int64_t tiles_per_wg;
+    const int64_t* cnt;
+    const int64_t* cnt_fin;
+    const double* head;
+    const double* tail;
+    double* energy;
+    int64_t* start_idx;
+    int64_t* end_idx;
+    Status* status;
+    int validate;
+};
+
+struct GroupParams {
+    const uint64_t* keys;
+    const double* energy;
+    int64_t m;
+    uint32_t H;           // hash slots (power of two); slot H holds the all-ones key
+    int64_t cap;          // key rows available
+    int nchunks;
+    int64_t chunk;        // intervals per chunk
+    unsigned long long* table;  // [H]
+    uint32_t* slot;       // [m]
+    uint32_t* slot2id;    // [H+1]
+    uint64_t* ukey;       // [H+1]
+    uint32_t* uslot;      // [H+1]
+    double* mean;         // [cap]
+    uint32_t* pcnt;       // [nchunks][cap]
+    double* psum;         // [nchunks][cap]
+    double* pm2;          // [nchunks][cap]
+    uint64_t* keys_out;   // [cap]
+    double* sum_out;
+    double* m2_out;
+    int64_t* count_out;
+    Status* status;
+};
+
+struct DiffParams {
+    const uint64_t* ka;
+    const double* sa;
+    const int64_t* ca;
+    int64_t na;
+    const uint64_t* kb;
+    const double* sb;
+    const int64_t* cb;
+    int64_t nb;
+    int64_t k;
+    double* cand_r;
+    uint64_t* cand_key;
+    int32_t* cand_ia;
+    int32_t* cand_ib;
+    uint64_t* out_key;
+    double* out_ratio;
+    double* out_ea;
+    double* out_eb;
+    int64_t* out_ca;
+    int64_t* out_cb;
+    Status* status;
+};
+
+// launchers (return hipError_t of the launch)
+hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
+hipError_t launch_tile(const TileParams& p, int grid, hipStream_t stream);
+hipError_t launch_cross(const FixParams& p, hipStream_t stream);
+hipError_t launch_outside(const FixParams& p, hipStream_t stream);
+hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, Status* st,
+                          hipStream_t stream);
+hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
+hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream);
+hipError_t launch_diff(const DiffParams& p, hipStream_t stream);
+
+int device_cu_count();
+
+}  // namespace mag

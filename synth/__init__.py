@@ -22,7 +22,8 @@ def build() -> str:
     """Compile synth.c into _synth.so with gcc (always recompiles)."""
     src = os.path.join(_HERE, "synth.c")
     tmp = _SO + ".tmp"
-    subprocess.check_call(["gcc", "-O2", "-std=c99", "-fPIC", "-shared", "-o", tmp, src, "-lm"])
+    subprocess.check_call(["gcc", "-O2", "-std=gnu99", "-fopenmp", "-fPIC", "-shared", "-o", tmp, src,
+                           "-lm"])
     os.replace(tmp, _SO)
     return _SO
 

@@ -6,7 +6,9 @@
  * power samples, interval bounds and operator keys.
  *
  * Random numbers: splitmix64 (Steele, Lea & Flood 2014) seeds one
- * xoshiro256** stream (Blackman & Vigna 2018) per purpose.  Uniforms are the
+ * xoshiro256** stream (Blackman & Vigna 2018) per purpose and per block of
+ * 2^16 draws, so that blocks are drawn in parallel (OpenMP) and the result
+ * does not depend on the thread count.  Uniforms are the
  * top 53 bits; normals come from Box-Muller; lognormal(median, sigma) is
  * exp(ln(median) + sigma * Z); exponential(mean) is -mean * ln(1 - U); a
  * Zipf(s, K) rank is found by inverse CDF over the cumulative weights r^-s.
@@ -108,6 +110,15 @@ static void rng_for(rng_t* g, int cfg, int side, int purpose, uint64_t seed)
     uint64_t v = 0x4D41474E45544F4Eull ^ ((uint64_t)cfg << 16) ^ ((uint64_t)side << 8) ^
                  (uint64_t)purpose ^ (seed * 0x9E3779B97F4A7C15ull);
     rng_seed(g, synth_mix64(v));
+}
+
+/* the stream of block b of a purpose */
+#define BLK ((int64_t)1 << 16)
+static void rng_block(rng_t* g, int cfg, int side, int purpose, uint64_t seed, int64_t b)
+{
+    uint64_t v = 0x4D41474E45544F4Eull ^ ((uint64_t)cfg << 16) ^ ((uint64_t)side << 8) ^
+                 (uint64_t)purpose ^ (seed * 0x9E3779B97F4A7C15ull);
+    rng_seed(g, synth_mix64(synth_mix64(v) ^ (uint64_t)(b + 1) * 0xD1B54A32D192ED03ull));
 }
 
 enum {
@@ -223,6 +234,59 @@ static uint64_t decode_key(uint64_t salt, int op, int layer, int bucket)
 /* structure: timestamps, intervals, keys                               */
 /* ------------------------------------------------------------------ */
 
+/* out[i] = lognormal(median, sigma), drawn block-parallel */
+static void draw_lognormal(int cfg, int side, int purpose, uint64_t seed, int64_t m, double median,
+                           double sigma, double* out)
+{
+    int64_t nb = (m + BLK - 1) / BLK, b;
+#pragma omp parallel for schedule(static)
+    for (b = 0; b < nb; ++b) {
+        rng_t g;
+        int64_t i, hi = (b + 1) * BLK < m ? (b + 1) * BLK : m;
+        rng_block(&g, cfg, side, purpose, seed, b);
+        for (i = b * BLK; i < hi; ++i)
+            out[i] = lognormal(&g, median, sigma);
+    }
+}
+
+static void draw_expo(int cfg, int side, int purpose, uint64_t seed, int64_t m, double mean,
+                      double* out)
+{
+    int64_t nb = (m + BLK - 1) / BLK, b;
+#pragma omp parallel for schedule(static)
+    for (b = 0; b < nb; ++b) {
+        rng_t g;
+        int64_t i, hi = (b + 1) * BLK < m ? (b + 1) * BLK : m;
+        rng_block(&g, cfg, side, purpose, seed, b);
+        for (i = b * BLK; i < hi; ++i)
+            out[i] = expo(&g, mean);
+    }
+}
+
+/* keys by Zipf rank (zs > 0) or uniform rank (zs == 0) */
+static int draw_keys(int cfg, int side, int purpose, uint64_t seed, int64_t m, double zs,
+                     const uint64_t* vocab, int64_t K, uint64_t* key)
+{
+    zipf_t z = {0, 0};
+    int64_t nb = (m + BLK - 1) / BLK, b;
+    if (zs > 0 && zipf_init(&z, zs, K))
+        return -2;
+#pragma omp parallel for schedule(static)
+    for (b = 0; b < nb; ++b) {
+        rng_t g;
+        int64_t i, hi = (b + 1) * BLK < m ? (b + 1) * BLK : m;
+        rng_block(&g, cfg, side, purpose, seed, b);
+        for (i = b * BLK; i < hi; ++i) {
+            int64_t r = (zs > 0) ? zipf_draw(&z, &g) : (int64_t)(u01(&g) * (double)K);
+            if (r >= K)
+                r = K - 1;
+            key[i] = vocab[r];
+        }
+    }
+    free(z.cum);
+    return 0;
+}
+
 /*
  * synth_structure: fill t[n], s[m], e[m], key[m] and offsets[streams+1] of
  * workload cfg.  'side' selects an independent draw (workload 5's second
@@ -232,69 +296,67 @@ int synth_structure(int cfg, uint64_t seed, int side, double* t, double* s, doub
                     uint64_t* key, int64_t* offsets)
 {
     shape_t sh;
-    rng_t gt, gd, gg, gk;
     int64_t j, i;
     uint64_t* vocab;
-    zipf_t z = {0, 0};
+    int rc = 0;
     if (shape_of(cfg, &sh))
         return -1;
     if (cfg != 5)
         side = 0;
-    rng_for(&gt, cfg, side, PU_TIME, seed);
-    rng_for(&gd, cfg, side, PU_DUR, seed);
-    rng_for(&gg, cfg, side, PU_GAP, seed);
-    rng_for(&gk, cfg, side, PU_KEY, seed);
     vocab = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)sh.K);
     if (!vocab)
         return -2;
     make_vocab(cfg, seed, sh.K, vocab);
 
     /* timestamps */
-    for (j = 0; j < sh.n; ++j) {
-        switch (cfg) {
-        case 1:
-            t[j] = (j == 0) ? 0.0 : (double)j * 1e-3 + (u01(&gt) * 2.0 - 1.0) * 5e-5;
-            break;
-        case 2: t[j] = (double)j / 1e5; break;
-        case 3: t[j] = (double)j / 1e6; break;
-        case 4: t[j] = (double)j / 2e5; break;
-        default: t[j] = (double)j / 1e5; break;
+    if (cfg == 1) {
+        int64_t nb = (sh.n + BLK - 1) / BLK, b;
+#pragma omp parallel for schedule(static)
+        for (b = 0; b < nb; ++b) {
+            rng_t g;
+            int64_t hi = (b + 1) * BLK < sh.n ? (b + 1) * BLK : sh.n, jj;
+            rng_block(&g, cfg, side, PU_TIME, seed, b);
+            for (jj = b * BLK; jj < hi; ++jj) {
+                double jit = (u01(&g) * 2.0 - 1.0) * 5e-5;
+                t[jj] = (jj == 0) ? 0.0 : (double)jj * 1e-3 + jit;
+            }
         }
+    } else {
+        double rate = (cfg == 3) ? 1e6 : (cfg == 4) ? 2e5 : 1e5;
+#pragma omp parallel for schedule(static)
+        for (j = 0; j < sh.n; ++j)
+            t[j] = (double)j / rate;
     }
 
     offsets[0] = 0;
     if (cfg == 1 || cfg == 4 || cfg == 5) {
         double median = (cfg == 1) ? 3e-3 : (cfg == 4) ? 60e-6 : 40e-6;
         double sigma = (cfg == 1) ? 0.8 : 1.0;
-        double zs = (cfg == 1) ? 1.1 : 1.05;
+        double zs = (cfg == 1) ? 1.1 : (cfg == 4) ? 0.0 : 1.05;
         double cur = 0.0;
-        if (cfg != 4 && zipf_init(&z, zs, sh.K)) {
-            free(vocab);
-            return -2;
-        }
-        for (i = 0; i < sh.m; ++i) {
-            double d = lognormal(&gd, median, sigma);
+        draw_lognormal(cfg, side, PU_DUR, seed, sh.m, median, sigma, e);
+        for (i = 0; i < sh.m; ++i) { /* packed back to back from t = 0 */
             s[i] = cur;
-            e[i] = cur + d;
+            e[i] = cur + e[i];
             cur = e[i];
-            if (cfg == 4)
-                key[i] = vocab[(int64_t)(u01(&gk) * (double)sh.K)];
-            else
-                key[i] = vocab[zipf_draw(&z, &gk)];
         }
+        rc = draw_keys(cfg, side, PU_KEY, seed, sh.m, zs, vocab, sh.K, key);
         offsets[1] = sh.m;
     } else if (cfg == 2) {
         const int layers = 32, ops = 12, steps = 256;
-        uint64_t salt = rng_next(&gk);
+        rng_t gk;
+        uint64_t salt;
+        rng_for(&gk, cfg, side, PU_KEY, seed);
+        salt = rng_next(&gk);
+        draw_lognormal(cfg, side, PU_DUR, seed, sh.m, 20e-6, 1.0, e);
         i = 0;
         for (int st = 0; st < steps; ++st) {
             double cur = (double)st * 0.078125;
             for (int l = 0; l < layers; ++l) {
                 for (int o = 0; o < ops; ++o) {
-                    double d = lognormal(&gd, 20e-6, 1.0);
                     int bucket = (o == 4) ? st / 128 : 0;
                     s[i] = cur;
-                    e[i] = cur + d;
+                    e[i] = cur + e[i];
                     cur = e[i];
                     key[i] = decode_key(salt, o, l, bucket);
                     ++i;
@@ -302,28 +364,25 @@ int synth_structure(int cfg, uint64_t seed, int side, double* t, double* s, doub
             }
         }
         offsets[1] = sh.m;
-    } else { /* cfg 3: four streams, exponential gaps before each interval */
+    } else { /* cfg 3: four streams, an exponential gap before each interval */
         int64_t per = sh.m / sh.streams;
-        if (zipf_init(&z, 1.2, sh.K)) {
-            free(vocab);
-            return -2;
-        }
+        draw_lognormal(cfg, side, PU_DUR, seed, sh.m, 15e-6, 1.0, e);
+        draw_expo(cfg, side, PU_GAP, seed, sh.m, 73e-6, s);
         for (int a = 0; a < sh.streams; ++a) {
             double cur = 0.0;
             for (int64_t u = 0; u < per; ++u) {
                 i = (int64_t)a * per + u;
-                cur += expo(&gg, 73e-6);
+                cur += s[i];
                 s[i] = cur;
-                e[i] = cur + lognormal(&gd, 15e-6, 1.0);
+                e[i] = cur + e[i];
                 cur = e[i];
-                key[i] = vocab[zipf_draw(&z, &gk)];
             }
             offsets[a + 1] = (int64_t)(a + 1) * per;
         }
+        rc = draw_keys(cfg, side, PU_KEY, seed, sh.m, 1.2, vocab, sh.K, key);
     }
-    free(z.cum);
     free(vocab);
-    return 0;
+    return rc;
 }
 
 /* ------------------------------------------------------------------ */
@@ -357,13 +416,11 @@ typedef struct {
 static int keyindex_build(keyindex_t* ki, const uint64_t* vocab, int64_t K)
 {
     int64_t r;
-    uint64_t* pairs = (uint64_t*)malloc(sizeof(uint64_t) * 2 * (size_t)K);
     ki->keys = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)K);
     ki->rank = (int64_t*)malloc(sizeof(int64_t) * (size_t)K);
     ki->K = K;
-    if (!pairs || !ki->keys || !ki->rank)
+    if (!ki->keys || !ki->rank)
         return -1;
-    /* sort keys, then recover ranks by a search in the vocabulary order */
     for (r = 0; r < K; ++r)
         ki->keys[r] = vocab[r];
     qsort(ki->keys, (size_t)K, sizeof(uint64_t), cmp_u64);
@@ -378,7 +435,6 @@ static int keyindex_build(keyindex_t* ki, const uint64_t* vocab, int64_t K)
         }
         ki->rank[lo] = r;
     }
-    free(pairs);
     return 0;
 }
 
@@ -401,6 +457,44 @@ static void keyindex_free(keyindex_t* ki)
     free(ki->rank);
 }
 
+/* first interval of [lo, hi) whose end is after time x (ends are sorted) */
+static int64_t first_ending_after(const double* e, int64_t lo, int64_t hi, double x)
+{
+    while (lo < hi) {
+        int64_t mid = lo + (hi - lo) / 2;
+        if (e[mid] <= x)
+            lo = mid + 1;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+/* clamped random walk: P[0] = 400, P[j] = clamp(P[j-1] + 5 N(0,1), 100, hi) */
+static void random_walk(int cfg, int side, uint64_t seed, int64_t n, double hi, float* P)
+{
+    int64_t nb = (n + BLK - 1) / BLK, b, j;
+    double x = 400.0;
+#pragma omp parallel for schedule(static)
+    for (b = 0; b < nb; ++b) {
+        rng_t g;
+        int64_t jj, top = (b + 1) * BLK < n ? (b + 1) * BLK : n;
+        rng_block(&g, cfg, side, PU_POWER, seed, b);
+        for (jj = b * BLK; jj < top; ++jj)
+            P[jj] = (float)normal01(&g); /* the step, kept in the output for now */
+    }
+    for (j = 0; j < n; ++j) {
+        if (j > 0) {
+            x += 5.0 * (double)P[j];
+            if (x < 100.0)
+                x = 100.0;
+            if (x > hi)
+                x = hi;
+        }
+        P[j] = (float)x;
+    }
+}
+
 /*
  * synth_power: fill P[n] (W, fp32, >= 0) for the given side of workload cfg,
  * from the structure arrays produced by synth_structure for that side.
@@ -419,33 +513,19 @@ int synth_power(int cfg, uint64_t seed, int side, const double* t, const double*
                 const double* e, const uint64_t* key, const int64_t* offsets, float* P)
 {
     shape_t sh;
-    rng_t gn;
-    int64_t j;
     uint64_t* vocab = NULL;
     double* level = NULL;
     keyindex_t ki = {0, 0, 0};
     int rc = 0;
+    int64_t nb, b;
     if (shape_of(cfg, &sh))
         return -1;
-    rng_for(&gn, cfg, side, PU_NOISE, seed);
+    nb = (sh.n + BLK - 1) / BLK;
 
     if (cfg == 1 || cfg == 5) {
-        rng_t gw;
-        double x = 400.0, hi = (cfg == 1) ? 700.0 : 750.0;
-        rng_for(&gw, cfg, (cfg == 5) ? side : 0, PU_POWER, seed);
-        for (j = 0; j < sh.n; ++j) {
-            if (j > 0) {
-                x += 5.0 * normal01(&gw);
-                if (x < 100.0)
-                    x = 100.0;
-                if (x > hi)
-                    x = hi;
-            }
-            P[j] = (float)x;
-        }
+        random_walk(cfg, (cfg == 5) ? side : 0, seed, sh.n, (cfg == 1) ? 700.0 : 750.0, P);
         if (cfg == 1 && side == 1) {
             uint64_t chosen[3];
-            int64_t i = 0;
             vocab = (uint64_t*)malloc(sizeof(uint64_t) * (size_t)sh.K);
             if (!vocab)
                 return -2;
@@ -453,15 +533,22 @@ int synth_power(int cfg, uint64_t seed, int side, const double* t, const double*
             chosen[0] = vocab[0];
             chosen[1] = vocab[4];
             chosen[2] = vocab[19];
-            for (j = 0; j < sh.n; ++j) {
-                double v = (double)P[j];
-                while (i < sh.m && e[i] <= t[j])
-                    ++i;
-                if (i < sh.m && s[i] <= t[j] && t[j] < e[i] &&
-                    (key[i] == chosen[0] || key[i] == chosen[1] || key[i] == chosen[2]))
-                    v *= 1.15;
-                v += normal01(&gn);
-                P[j] = (float)(v < 0.0 ? 0.0 : v);
+#pragma omp parallel for schedule(static)
+            for (b = 0; b < nb; ++b) {
+                rng_t g;
+                int64_t j, top = (b + 1) * BLK < sh.n ? (b + 1) * BLK : sh.n;
+                int64_t i = first_ending_after(e, 0, sh.m, t[b * BLK]);
+                rng_block(&g, cfg, side, PU_NOISE, seed, b);
+                for (j = b * BLK; j < top; ++j) {
+                    double v = (double)P[j];
+                    while (i < sh.m && e[i] <= t[j])
+                        ++i;
+                    if (i < sh.m && s[i] <= t[j] && t[j] < e[i] &&
+                        (key[i] == chosen[0] || key[i] == chosen[1] || key[i] == chosen[2]))
+                        v *= 1.15;
+                    v += normal01(&g);
+                    P[j] = (float)(v < 0.0 ? 0.0 : v);
+                }
             }
         }
         free(vocab);
@@ -532,10 +619,14 @@ int synth_power(int cfg, uint64_t seed, int side, const double* t, const double*
                 level[r] *= mult[r];
             free(mult);
         }
-        {
-            int64_t i = 0;
-            int64_t cur_rank = -1, cur_i = -1;
-            for (j = 0; j < sh.n; ++j) {
+#pragma omp parallel for schedule(static)
+        for (b = 0; b < nb; ++b) {
+            rng_t g;
+            int64_t j, top = (b + 1) * BLK < sh.n ? (b + 1) * BLK : sh.n;
+            int64_t i = first_ending_after(e, 0, sh.m, t[b * BLK]);
+            int64_t cur_i = -1, cur_rank = -1;
+            rng_block(&g, cfg, side, PU_NOISE, seed, b);
+            for (j = b * BLK; j < top; ++j) {
                 double v = 100.0;
                 while (i < sh.m && e[i] <= t[j])
                     ++i;
@@ -547,13 +638,16 @@ int synth_power(int cfg, uint64_t seed, int side, const double* t, const double*
                     if (cur_rank >= 0)
                         v = level[cur_rank];
                 }
-                v += 20.0 * normal01(&gn);
+                v += 20.0 * normal01(&g);
                 P[j] = (float)(v < 0.0 ? 0.0 : v);
             }
         }
     } else { /* cfg 3 */
-        int64_t cursor[64];
-        int a, S = sh.streams;
+        int S = sh.streams;
+        if (S > 64) {
+            rc = -1;
+            goto done;
+        }
         per_key_uniform(cfg, 0, PU_KEYPARAM, seed, sh.K, 50.0, 160.0, level);
         if (side == 1) {
             double* mult = (double*)malloc(sizeof(double) * (size_t)sh.K);
@@ -567,35 +661,38 @@ int synth_power(int cfg, uint64_t seed, int side, const double* t, const double*
                 level[r] *= mult[r];
             free(mult);
         }
-        double cur_level[64];
-        if (S > 64) {
-            rc = -1;
-            goto done;
-        }
-        for (a = 0; a < S; ++a) {
-            cursor[a] = offsets[a];
-            cur_level[a] = (offsets[a] < offsets[a + 1])
-                               ? level[keyindex_find(&ki, key[offsets[a]])]
-                               : 0.0;
-        }
-        for (j = 0; j < sh.n; ++j) {
-            double v = 100.0;
+#pragma omp parallel for schedule(static)
+        for (b = 0; b < nb; ++b) {
+            rng_t g;
+            int64_t cursor[64], cur_i[64];
+            double cur_level[64];
+            int a;
+            int64_t j, top = (b + 1) * BLK < sh.n ? (b + 1) * BLK : sh.n;
+            rng_block(&g, cfg, side, PU_NOISE, seed, b);
             for (a = 0; a < S; ++a) {
-                int64_t i = cursor[a];
-                if (i < offsets[a + 1] && e[i] <= t[j]) {
+                cursor[a] = first_ending_after(e, offsets[a], offsets[a + 1], t[b * BLK]);
+                cur_i[a] = -1;
+                cur_level[a] = 0.0;
+            }
+            for (j = b * BLK; j < top; ++j) {
+                double v = 100.0;
+                for (a = 0; a < S; ++a) {
+                    int64_t i = cursor[a];
                     while (i < offsets[a + 1] && e[i] <= t[j])
                         ++i;
                     cursor[a] = i;
-                    if (i < offsets[a + 1]) {
-                        int64_t r = keyindex_find(&ki, key[i]);
-                        cur_level[a] = (r >= 0) ? level[r] : 0.0;
+                    if (i < offsets[a + 1] && s[i] <= t[j] && t[j] < e[i]) {
+                        if (i != cur_i[a]) {
+                            int64_t r = keyindex_find(&ki, key[i]);
+                            cur_i[a] = i;
+                            cur_level[a] = (r >= 0) ? level[r] : 0.0;
+                        }
+                        v += cur_level[a];
                     }
                 }
-                if (i < offsets[a + 1] && s[i] <= t[j] && t[j] < e[i])
-                    v += cur_level[a];
+                v += 20.0 * normal01(&g);
+                P[j] = (float)(v < 0.0 ? 0.0 : v);
             }
-            v += 20.0 * normal01(&gn);
-            P[j] = (float)(v < 0.0 ? 0.0 : v);
         }
     }
 done:

@@ -1,0 +1,93 @@
+"""The C-ABI library: it loads, exports every symbol include/*.h declares, and
+rejects bad arguments on the host before any device work (no GPU needed)."""
+import ctypes
+import glob
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    names = set()
+    for h in glob.glob(os.path.join(ROOT, "include", "*.h")):
+        text = open(h).read()
+        text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+        for mt in re.finditer(r"^[A-Za-z_][\w\s\*]*?\b(mag_\w+)\s*\(", text, flags=re.M):
+            names.add(mt.group(1))
+    return names
+
+
+def test_header_declares_the_entry_points():
+    names = _declared()
+    assert {"mag_attribute", "mag_diff", "mag_attribute_workspace_size",
+            "mag_diff_workspace_size", "mag_strerror", "mag_last_error"} <= names
+
+
+def test_library_exports_every_declared_symbol():
+    from paper_2512_08365_amd import _native
+    lib = _native.load()
+    for name in _declared():
+        assert hasattr(lib, name), name
+    assert set(_native.EXPORTED) == _declared()
+
+
+def test_host_side_errors_without_gpu():
+    from paper_2512_08365_amd import _native as N
+    lib = N.load()
+    b = ctypes.c_size_t(0)
+    assert lib.mag_attribute_workspace_size(1, 0, 0, None, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_attribute_workspace_size(10, -1, 0, None, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_attribute_workspace_size(10, 5, 0, None, None) == N.MAG_E_NULL
+    o = N.AttrOpts(2, N.MAG_EQUAL_SPLIT, None)
+    assert lib.mag_attribute_workspace_size(10, 5, 0, ctypes.byref(o), ctypes.byref(b)) == N.MAG_E_STREAMS
+    offs = (ctypes.c_int64 * 3)(0, 4, 3)
+    o = N.AttrOpts(2, N.MAG_EQUAL_SPLIT, ctypes.cast(offs, ctypes.c_void_p))
+    assert lib.mag_attribute_workspace_size(10, 3, 0, ctypes.byref(o), ctypes.byref(b)) == N.MAG_E_STREAMS
+    o = N.AttrOpts(33, N.MAG_EQUAL_SPLIT, None)
+    assert lib.mag_attribute_workspace_size(10, 3, 0, ctypes.byref(o), ctypes.byref(b)) == N.MAG_E_STREAMS
+    assert lib.mag_attribute_workspace_size(10, 3, 8, None, ctypes.byref(b)) == N.MAG_OK
+    assert b.value > 0
+    # NULL inputs and bad sizes are rejected before any HIP call
+    assert lib.mag_attribute(None, None, 10, None, None, None, 0, None, None, None, None, None,
+                             None, 0, None) == N.MAG_E_NULL
+    fake = ctypes.c_void_p(256)
+    assert lib.mag_attribute(fake, fake, 1, None, None, None, 0, None, None, None, None, None,
+                             fake, 0, None) == N.MAG_E_SIZE
+    assert lib.mag_attribute(fake, fake, 10, None, None, None, 3, None, None, None, None, None,
+                             fake, 0, None) == N.MAG_E_NULL
+    assert lib.mag_attribute(fake, fake, 10, fake, fake, None, 3, None, None, None, None, None,
+                             fake, 0, None) == N.MAG_E_WORKSPACE
+    assert b"workspace" in lib.mag_last_error()
+    ks = N.KeyStats(None, None, None, 0, 0)
+    assert lib.mag_attribute(fake, fake, 10, fake, fake, fake, 3, None, None, None,
+                             ctypes.byref(ks), None, fake, 1 << 30, None) == N.MAG_E_SIZE
+    assert lib.mag_diff(None, None, None, None, 3, None, None, 0, None) == N.MAG_E_NULL
+    sa = N.KeyStats(None, None, None, 0, 0)
+    ro = N.RankOut()
+    assert lib.mag_diff(None, ctypes.byref(sa), None, ctypes.byref(sa), -1, ctypes.byref(ro),
+                        None, 0, None) == N.MAG_E_SIZE
+    assert lib.mag_diff_workspace_size(5, 5, -1, ctypes.byref(b)) == N.MAG_E_SIZE
+    for code in range(-12, 1):
+        assert lib.mag_strerror(code)
+
+
+def test_product_has_no_cpu_fallback():
+    # the binding refuses CPU tensors instead of computing on the host
+    torch = pytest.importorskip("torch")
+    import paper_2512_08365_amd as mag
+    t = torch.linspace(0, 1, 10, dtype=torch.float64)
+    P = torch.ones(10, dtype=torch.float32)
+    s = torch.zeros(1, dtype=torch.float64)
+    with pytest.raises(mag.MagnetonError):
+        mag.attribute(t, P, s, s + 0.5)
+
+
+def test_product_does_not_import_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2512_08365_amd")
+    for path in glob.glob(os.path.join(pkg, "**", "*"), recursive=True):
+        if os.path.isfile(path) and path.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+            text = open(path).read()
+            assert "oracle" not in text.lower().replace("oracle-free", ""), path

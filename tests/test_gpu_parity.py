@@ -1,0 +1,222 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integer outputs (sample indices, key grouping, counts, top-k order) must be
+bit-exact; energies within 1e-9 relative; M2 within 1e-9 of the key's second
+moment (sum of E^2).  Sizes span many tiles, ragged tails, endpoint rounds and
+the degenerate cases of the method.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from gpu_util import (assert_energy_close, compare_attribution, log, run_gpu, run_oracle,
+                      to_gpu)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    import paper_2512_08365_amd as mag
+    mag.version()  # loads the HIP library or raises
+    yield
+
+
+# ---------------------------------------------------------------------------
+# small randomized cases
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("streams", [1, 2, 3, 4, 7])
+def test_tiny_fuzz(streams):
+    for seed in range(25):
+        c = synth.tiny_case(5000 * streams + seed, n=int(2 + (seed * 37) % 300), streams=streams,
+                            per_stream=int(seed % 13))
+        for split in (True, False):
+            compare_attribution(c, equal_split=split, label=f"tiny s{streams} seed{seed}")
+
+
+def test_dyadic_bit_exact():
+    for seed in range(10):
+        c = synth.tiny_case(77 + seed, n=200, streams=2, per_stream=20, dyadic=True)
+        o, g = run_oracle(c)
+        gi, gk, summ, _ = run_gpu(c)
+        assert np.array_equal(gi["energy"], o["energy"]), seed
+
+
+def _long_trace(seed, n, streams, per_stream, span_frac=0.02, outside=True):
+    """intervals whose lengths range from sub-sample to many tiles"""
+    rng = np.random.default_rng(seed)
+    t = np.concatenate([[0.0], np.cumsum(rng.uniform(0.5, 1.5, n - 1))]) * 1e-6
+    P = rng.uniform(50, 800, n).astype(np.float32)
+    s_all, e_all, off = [], [], [0]
+    lo, hi = t[0], t[-1]
+    for a in range(streams):
+        pad = 0.05 * (hi - lo) if outside else 0.0
+        cuts = np.sort(rng.uniform(lo - pad, hi + pad, 2 * per_stream))
+        s_all.append(cuts[0::2])
+        e_all.append(cuts[1::2])
+        off.append(off[-1] + per_stream)
+    s = np.concatenate(s_all)
+    e = np.concatenate(e_all)
+    key = rng.integers(0, 40, s.shape[0]).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    return {"t": t, "P": P, "s": s, "e": e, "key": key, "offsets": np.array(off, np.int64)}
+
+
+@pytest.mark.parametrize("streams", [1, 4])
+def test_intervals_spanning_many_tiles(streams):
+    for seed, (n, per) in enumerate([(20000, 3), (50001, 40), (100000, 400), (4097, 2000)]):
+        c = _long_trace(seed, n, streams, per)
+        compare_attribution(c, label=f"long s{streams} n{n} per{per}")
+
+
+def test_dense_endpoints_force_rounds():
+    # thousands of endpoints inside one tile (and inside single segments)
+    rng = np.random.default_rng(3)
+    n = 5000
+    t = np.arange(n, dtype=np.float64) * 1e-3
+    P = rng.uniform(100, 500, n).astype(np.float32)
+    for streams in (1, 3, 32):
+        s_all, e_all, off = [], [], [0]
+        for a in range(streams):
+            per = 3000 // streams
+            cuts = np.sort(rng.uniform(1.0, 1.3, 2 * per))   # ~300 samples, 6000 endpoints
+            s_all.append(cuts[0::2])
+            e_all.append(cuts[1::2])
+            off.append(off[-1] + per)
+        c = {"t": t, "P": P, "s": np.concatenate(s_all), "e": np.concatenate(e_all),
+             "key": rng.integers(0, 9, off[-1]).astype(np.uint64), "offsets": np.array(off)}
+        compare_attribution(c, label=f"dense s{streams}")
+    # all endpoints inside one sample segment
+    cuts = np.sort(rng.uniform(2.0001, 2.0009, 4000))
+    c = {"t": t, "P": P, "s": cuts[0::2], "e": cuts[1::2], "key": np.zeros(2000, np.uint64),
+         "offsets": np.array([0, 2000])}
+    compare_attribution(c, label="one segment")
+
+
+def test_degenerate_cases():
+    t = np.array([0.0, 1.0])
+    P = np.array([3.0, 5.0], np.float32)
+    cases = {
+        "two samples": (np.array([0.25]), np.array([0.75])),
+        "no intervals": (np.zeros(0), np.zeros(0)),
+        "zero length": (np.array([0.5, 0.5]), np.array([0.5, 0.7])),
+        "all before": (np.array([-3.0, -2.0]), np.array([-2.5, -1.0])),
+        "all after": (np.array([2.0, 3.0]), np.array([2.5, 4.0])),
+        "covers trace": (np.array([-1.0]), np.array([5.0])),
+        "on samples": (np.array([0.0]), np.array([1.0])),
+    }
+    for name, (s, e) in cases.items():
+        c = {"t": t, "P": P, "s": s, "e": e, "key": np.arange(s.shape[0]).astype(np.uint64),
+             "offsets": np.array([0, s.shape[0]])}
+        compare_attribution(c, label=name)
+
+
+def test_extreme_keys():
+    c = synth.tiny_case(5, n=500, streams=2, per_stream=60)
+    m = c["s"].shape[0]
+    c["key"] = np.array([0, 2**64 - 1, 2**63, 1, 2**64 - 2] * m, np.uint64)[:m]
+    compare_attribution(c, label="extreme keys")
+
+
+def test_key_capacity_error():
+    import paper_2512_08365_amd as mag
+    c = synth.tiny_case(6, n=300, streams=1, per_stream=40, keys=30)
+    nkeys = np.unique(c["key"]).shape[0]
+    d = to_gpu(c)
+    with pytest.raises(mag.MagnetonError) as ei:
+        mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], key_capacity=max(1, nkeys - 1))
+    assert ei.value.code == -3
+
+
+def test_device_detected_errors():
+    import paper_2512_08365_amd as mag
+    import torch
+    base = synth.tiny_case(8, n=5000, streams=2, per_stream=50)
+
+    def run(c, off=None):
+        d = to_gpu(c)
+        off = off or [int(x) for x in c["offsets"]]
+        mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], n_streams=len(off) - 1,
+                      stream_offsets=off)
+
+    bads = []
+    c = dict(base); c["t"] = base["t"].copy(); c["t"][3000] = c["t"][2999]; bads.append((c, -5))
+    c = dict(base); c["t"] = base["t"].copy(); c["t"][4999] = np.nan; bads.append((c, -5))
+    c = dict(base); c["P"] = base["P"].copy(); c["P"][1234] = -1.0; bads.append((c, -6))
+    c = dict(base); c["P"] = base["P"].copy(); c["P"][0] = np.inf; bads.append((c, -6))
+    c = dict(base); c["s"] = base["s"].copy(); c["s"][10] = c["e"][10] + 1.0; bads.append((c, -7))
+    a = int(np.argmax(np.diff(base["offsets"]) >= 2))
+    i = int(base["offsets"][a])
+    c = dict(base); c["e"] = base["e"].copy(); c["e"][i] = c["s"][i + 1] + 1e-3; bads.append((c, -7))
+    c = dict(base); c["s"] = base["s"].copy(); c["s"][0] = np.nan; bads.append((c, -7))
+    for i, (c, code) in enumerate(bads):
+        log(f"[case] invalid input {i} expects {code}")
+        with pytest.raises(mag.MagnetonError) as ei:
+            run(c)
+        assert ei.value.code == code, i
+    # host-detected: bad offsets
+    with pytest.raises(mag.MagnetonError) as ei:
+        run(base, off=[0, 5, 3, int(base["offsets"][-1])])
+    assert ei.value.code == -8
+    torch.cuda.synchronize()
+
+
+def test_deterministic_per_interval():
+    c = _long_trace(9, 60000, 4, 3000)
+    a, ka, _, _ = run_gpu(c)
+    b, kb, _, _ = run_gpu(c)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
+    assert np.array_equal(ka["keys"], kb["keys"])
+    assert np.array_equal(ka["count"], kb["count"])
+
+
+# ---------------------------------------------------------------------------
+# the workloads
+# ---------------------------------------------------------------------------
+
+def _diff_and_compare(ga_dev, gb_dev, ga, gb, k, label):
+    import paper_2512_08365_amd as mag
+    d = mag.diff(ga_dev, gb_dev, k)
+    o = oracle.diff(ga, gb, k)
+    log(f"[diff] {label}: k={k} joined={o['n_join']} margin={o['margin']:.3g}")
+    # the order is only well defined when adjacent ratios are separated by more
+    # than the ratios' own error (sums to 1e-9 relative move r by ~2e-9 (1 + |r|))
+    assert o["margin"] > 1e-8, f"{label}: workload has near-tied ratios"
+    key = d["key"].cpu().numpy().view(np.uint64)
+    assert np.array_equal(key, o["key"]), f"{label}: top-k keys/order"
+    r = d["ratio"].cpu().numpy()
+    assert np.all(np.abs(r - o["ratio"]) <= 3e-9 * (1 + np.abs(o["ratio"]))), label
+    assert np.array_equal(d["count_a"].cpu().numpy(), o["count_a"]), label
+    assert np.array_equal(d["count_b"].cpu().numpy(), o["count_b"]), label
+    assert_energy_close(d["energy_a"].cpu().numpy(), o["energy_a"], label)
+    assert_energy_close(d["energy_b"].cpu().numpy(), o["energy_b"], label)
+    assert (d["n_only_a"], d["n_only_b"], d["n_join"]) == (o["n_only_a"], o["n_only_b"], o["n_join"])
+
+
+@pytest.mark.parametrize("cfg,k", [(1, 10), (2, 10)])
+def test_workload_ab(cfg, k):
+    for seed in range(3):
+        A, B = synth.sides(cfg, seed)
+        ra = compare_attribution(A, label=f"cfg{cfg} A seed{seed}")
+        rb = compare_attribution(B, label=f"cfg{cfg} B seed{seed}")
+        _diff_and_compare(ra[5], rb[5], ra[1], rb[1], k, f"cfg{cfg} seed{seed}")
+
+
+def test_workload_multistream_100m():
+    A, B = synth.sides(3, 0)
+    ra = compare_attribution(A, label="cfg3 A")
+    rb = compare_attribution(B, label="cfg3 B")
+    _diff_and_compare(ra[5], rb[5], ra[1], rb[1], 100, "cfg3")
+
+
+def test_workload_batched_sweep():
+    sides = synth.sides(4, 0, which=range(4))
+    base = compare_attribution(sides[0], label="cfg4 A")
+    for b in range(1, len(sides)):
+        rb = compare_attribution(sides[b], label=f"cfg4 B{b}")
+        _diff_and_compare(base[5], rb[5], base[1], rb[1], 100, f"cfg4 B{b}")
