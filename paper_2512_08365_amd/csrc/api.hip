@@ -71,6 +71,7 @@ struct AttrWorkspace {
     uint32_t* slot2id;
     uint64_t* ukey;
     uint32_t* uslot;
+    uint32_t* urank;
     double* mean;
     uint32_t* pcnt;
     double* psum;
@@ -104,6 +105,7 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
         w.slot2id = c.take<uint32_t>((size_t)pl.H + 1);
         w.ukey = c.take<uint64_t>((size_t)pl.H + 1);
         w.uslot = c.take<uint32_t>((size_t)pl.H + 1);
+        w.urank = c.take<uint32_t>((size_t)pl.H + 1);
         w.mean = c.take<double>((size_t)std::max<int64_t>(pl.cap, 1));
         w.pcnt = c.take<uint32_t>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.psum = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
@@ -319,8 +321,10 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
     tp.status = w.status;
     tp.split = (flags & MAG_EQUAL_SPLIT) ? 1 : 0;
     tp.validate = (flags & MAG_SKIP_VALIDATE) ? 0 : 1;
+    tp.aligned16 = (aligned(timestamps, 16) && aligned(power, 16)) ? 1 : 0;
     timer.mark(1);
-    if ((e = mag::launch_tile(tp, grid, stream)) != hipSuccess) return hip_fail(e, "tile kernel");
+    e = mag::launch_tile(tp, grid, stream);
+    if (e != hipSuccess) return hip_fail(e, "tile kernel");
     timer.mark(2);
 
     mag::FixParams fp{};
@@ -360,6 +364,7 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         gp.slot2id = w.slot2id;
         gp.ukey = w.ukey;
         gp.uslot = w.uslot;
+        gp.urank = w.urank;
         gp.mean = w.mean;
         gp.pcnt = w.pcnt;
         gp.psum = w.psum;

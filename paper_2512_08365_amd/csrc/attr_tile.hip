@@ -1,21 +1,33 @@
 // attr_tile.hip -- per-interval energy attribution on gfx950.
 //
-// The power trace is cut into tiles of TILE sample segments.  A persistent
-// workgroup walks a contiguous run of tiles; for each tile it stages the
-// samples in LDS, builds positive partial sums of the segment energies
-// (per thread: 8 segments; per 8 threads: 64 segments), and consumes the
-// interval endpoints of every stream that fall in the tile, in time order.
-// The endpoints cut the tile into "gaps" with a constant set of active
-// intervals; each gap's energy (trapezoid pieces at its ends plus whole
-// segments in between) is divided by the number of active intervals (equal
-// split) and added to each of them.  Every energy is a sum of non-negative
-// terms, so no result is a difference of large running totals.
+// The power trace is cut into tiles of T = NTH * C sample segments
+// [t_j, t_{j+1}]; a persistent workgroup walks a contiguous run of tiles and
+// prefetches the next tile's samples (and endpoint window) into registers
+// while the current tile runs.
 //
-// Intervals whose endpoints lie in different tiles leave partial energies
-// (head: the piece of the interval active at a tile's start; tail: the piece
-// of the interval started in a tile and still active at its end), which
-// k_cross adds up in tile order.  Endpoints before t_0 or after t_{n-1} are
-// handled by k_outside.
+// Work inside a tile is split so that no lane ever loops over segments:
+//   samples   (lane k owns segments kC .. kC+C-1): segment energies
+//             S_j = (P_j + P_{j+1}) (t_{j+1} - t_j) / 2, input checks, and a
+//             segmented scan of S_j that restarts after every segment holding
+//             an interval endpoint ("run sums": the energy of the whole
+//             segments since the last endpoint);
+//   endpoints (one lane per endpoint of the round): its segment (guessed from
+//             the mean sample spacing, then corrected), its sample index, its
+//             position in the time-merged order of all streams;
+//   gaps      (one lane per gap between consecutive endpoints): the exact
+//             integral of the linear interpolant over the gap = trapezoid
+//             pieces at both ends + the run sum of the whole segments between,
+//             divided by the number of active intervals (equal split);
+//   intervals (one lane per interval starting in the round): the sum of its
+//             gaps.
+// Every energy is a sum of non-negative terms; no result is a difference of
+// running totals.  A tile whose endpoints exceed the LDS window is processed
+// in several rounds, each a time prefix of the remaining endpoints.
+//
+// Intervals whose endpoints lie in different tiles leave partial energies:
+// head[a][b], the piece in tile b of stream a's interval active at the tile's
+// start, and tail[a][b], the piece of the interval started in tile b and still
+// active at its end; k_cross adds them in tile order (attr_fix.hip).
 
 #include "mag_internal.hpp"
 
@@ -26,137 +38,98 @@ namespace {
 __device__ __forceinline__ double endpoint_x(const double* s, const double* e, int64_t off,
                                              int64_t q)
 {
-    // endpoint q of a stream: even q = start of interval q/2, odd q = its end
     const int64_t i = off + (q >> 1);
     return (q & 1) ? e[i] : s[i];
 }
 
-__device__ __forceinline__ bool finite_d(double x) { return fabs(x) < INFINITY; }
-
-// value of the linear interpolant at x in segment j (exact at the samples)
-__device__ __forceinline__ double power_at(const double* ts, const float* Ps, int j, double x)
+// linear interpolant on [ta, tb] at x, exactly the sample values at the ends
+__device__ __forceinline__ double lerp_power(double ta, double tb, double pa, double pb, double x)
 {
-    const double ta = ts[j], tb = ts[j + 1];
-    const double pa = (double)Ps[j], pb = (double)Ps[j + 1];
     if (x == ta) return pa;
     if (x == tb) return pb;
     return pa + (pb - pa) * ((x - ta) / (tb - ta));
 }
 
-__device__ __forceinline__ double piece(const double* ts, const float* Ps, int j, double a,
-                                        double b)
+// number of entries <= v (le) or < v (!le) in the sorted list xs[0, n)
+__device__ __forceinline__ int count_below(const double* xs, int n, double v, bool le)
 {
-    return 0.5 * (power_at(ts, Ps, j, a) + power_at(ts, Ps, j, b)) * (b - a);
-}
-
-__device__ __forceinline__ double seg_energy(const double* ts, const float* Ps, int j)
-{
-    return 0.5 * ((double)Ps[j] + (double)Ps[j + 1]) * (ts[j + 1] - ts[j]);
-}
-
-// sum of whole segment energies j in [a, b) from the per-8 and per-64 sums
-__device__ double full_sum(const double* ts, const float* Ps, const double* c1,
-                           const double* c2, int a, int b)
-{
-    double acc = 0.0;
-    int j = a;
-    while (j < b && (j & 7)) { acc += seg_energy(ts, Ps, j); ++j; }
-    while (j + 8 <= b && (j & 63)) { acc += c1[j >> 3]; j += 8; }
-    while (j + 64 <= b) { acc += c2[j >> 6]; j += 64; }
-    while (j + 8 <= b) { acc += c1[j >> 3]; j += 8; }
-    while (j < b) { acc += seg_energy(ts, Ps, j); ++j; }
-    return acc;
-}
-
-// energy of the interpolant between (xs in segment js) and (xe in segment je)
-__device__ double gap_energy(const double* ts, const float* Ps, const double* c1,
-                             const double* c2, double xs, int js, double xe, int je)
-{
-    if (js == je) return piece(ts, Ps, js, xs, xe);
-    double q = piece(ts, Ps, js, xs, ts[js + 1]);
-    q += full_sum(ts, Ps, c1, c2, js + 1, je);
-    q += piece(ts, Ps, je, ts[je], xe);
-    return q;
+    int lo = 0, hi = n;
+    while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        const bool go = le ? (xs[mid] <= v) : (xs[mid] < v);
+        if (go) lo = mid + 1; else hi = mid;
+    }
+    return lo;
 }
 
 template <int NTH>
-__device__ __forceinline__ double block_sum_ordered(double v, double* red)
+__device__ __forceinline__ double block_sum_fixed(double v, double* red)
 {
-    // deterministic: fixed butterfly inside each wave, then waves in order
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    if (lane == 0) red[wave] = v;
-    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    lds_barrier();
     double tot = 0.0;
+#pragma unroll
     for (int w = 0; w < NTH / 64; ++w) tot += red[w];
-    __syncthreads();
+    lds_barrier();
     return tot;
 }
 
 }  // namespace
 
-// ---------------------------------------------------------------------------
-// main tile kernel
-// ---------------------------------------------------------------------------
-template <int T, int NTH>
+template <int NTH, int C>
 __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 {
-    constexpr int C = T / NTH;
-    static_assert(C == 8, "full_sum assumes 8 segments per thread");
-    static_assert(NTH % 64 == 0 && (NTH / 8) * 64 == T, "per-64 sums");
+    constexpr int T = NTH * C;
     constexpr int E = ROUND_EVENTS;
-    static_assert(E <= 2 * NTH, "scan handles two events per thread");
+    constexpr int NW = NTH / 64;
+    constexpr int PER = E / NTH;  // window entries prefetched per lane
+    static_assert((E & (E - 1)) == 0 && E % NTH == 0 && E <= 2 * NTH, "window layout");
+    static_assert((C & (C - 1)) == 0, "C power of two");
 
-    __shared__ double sh_t[T + 1];
-    __shared__ float sh_P[T + 1];
-    __shared__ double sh_c1[NTH];
-    __shared__ double sh_c2[NTH / 8];
-    __shared__ double ev_x[E];
-    __shared__ int ev_pos[E];
+    // samples: column tid holds the C+1 samples of lane tid's segments
+    __shared__ double sh_t[C + 1][NTH];
+    __shared__ float sh_P[C + 1][NTH];
+    __shared__ double sh_rs[C][NTH];          // run sums per segment
+    __shared__ uint32_t sh_flag[T / 32];      // segment holds a breakpoint of the round
+    __shared__ double ev_x[E];                // endpoint window, stream-major
+    __shared__ int ev_pos[E];                 // merged position of a window slot
     __shared__ double mg_x[E];
-    __shared__ int mg_j[E];
-    __shared__ int mg_d[E];
+    __shared__ int mg_j[E];                   // segment (bits 0..30) | end flag (bit 31)
     __shared__ int mg_m[E + 1];
     __shared__ double gv[E + 1];
-    __shared__ int64_t st_q[MAX_STREAMS];
-    __shared__ int64_t st_len[MAX_STREAMS];
+    __shared__ int64_t st_q[MAX_STREAMS], st_q0[MAX_STREAMS], st_len[MAX_STREAMS];
     __shared__ int64_t st_off[MAX_STREAMS + 1];
-    __shared__ int st_k[MAX_STREAMS];
-    __shared__ int st_take[MAX_STREAMS];
-    __shared__ int st_started[MAX_STREAMS];
-    __shared__ int nx_started[MAX_STREAMS];
-    __shared__ double st_acc[MAX_STREAMS];
-    __shared__ double nx_acc[MAX_STREAMS];
-    __shared__ double sh_red[NTH / 64];
-    __shared__ int sh_wsum[NTH / 64];
-    __shared__ int sh_Er, sh_final, sh_m0;
-    __shared__ double sh_cut;
-    __shared__ double sh_rs_x;
-    __shared__ int sh_rs_j;
+    __shared__ int st_k[MAX_STREAMS], st_take[MAX_STREAMS], st_base[MAX_STREAMS + 1];
+    __shared__ int st_started[MAX_STREAMS], nx_started[MAX_STREAMS];
+    __shared__ double st_acc[MAX_STREAMS], nx_acc[MAX_STREAMS];
+    __shared__ double red[NW];
+    __shared__ int sh_wsum[NW];
+    __shared__ int sh_final, sh_m0, sh_rs_j;
+    __shared__ double sh_cut, sh_tend, sh_rs_x, sh_inv;
     __shared__ unsigned sh_err;
 
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int S = p.ss.S;
-    const int cap = E / S;
+    int lcap = 0;  // window slots per stream: the largest power of two with S * cap <= E
+    while ((S << (lcap + 1)) <= E) ++lcap;
+    const int cap = 1 << lcap;
     const int64_t NT = p.NT;
-
     const int64_t b0 = p.tile_begin + (int64_t)blockIdx.x * p.tiles_per_wg;
     const int64_t b1 = min(b0 + p.tiles_per_wg, p.tile_end);
-    if (b0 >= b1) return;  // uniform over the block
+    if (b0 >= b1) return;  // uniform
 
     if (tid <= S) st_off[tid] = p.ss.off[tid];
     if (tid == 0) sh_err = 0u;
-    __syncthreads();
+    for (int w = tid; w < T / 32; w += NTH) sh_flag[w] = 0u;
+    lds_barrier();
     if (tid < S) st_len[tid] = 2 * (st_off[tid + 1] - st_off[tid]);
-    __syncthreads();
-
-    // cursor of each stream at the first tile: endpoints <= its start time
-    // (64-ary search by one wave per stream: ~4 dependent loads)
+    lds_barrier();
     {
+        // cursor of each stream at the first tile: endpoints <= its start time
+        // (64-ary search, one wave per stream: about four dependent loads)
         const double tau0 = p.t[b0 * T - p.base];
-        for (int a = wave; a < S; a += NTH / 64) {
+        for (int a = wave; a < S; a += NW) {
             int64_t lo = 0, hi = st_len[a];
             while (hi - lo > 64) {
                 const int64_t step = (hi - lo + 63) / 64;
@@ -174,202 +147,316 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
             if (lane == 0) st_q[a] = lo + c;
         }
     }
-    if (tid < S) {
-        st_acc[tid] = 0.0;
-        st_started[tid] = 0;
-    }
-    __syncthreads();
+    lds_barrier();
 
+    // registers holding the next tile's samples of this lane (and window)
+    double nt[C + 1];
+    float nP[C + 1];
+    double ew[PER];
+    bool ew_ready = false;
     unsigned err = 0u;
+
+    auto load_samples = [&](int64_t b) {
+        const int64_t j0 = b * T;
+        const int L = (int)min((int64_t)T, p.nseg - j0);
+        const int cs = min(max(L - tid * C, 0), C);
+        const int64_t g = j0 + (int64_t)tid * C - p.base;
+        if (cs == C && p.aligned16) {
+            const double2* t2 = reinterpret_cast<const double2*>(p.t + g);
+            const float4* P4 = reinterpret_cast<const float4*>(p.P + g);
+#pragma unroll
+            for (int u = 0; u < C / 2; ++u) {
+                const double2 v = t2[u];
+                nt[2 * u] = v.x;
+                nt[2 * u + 1] = v.y;
+            }
+#pragma unroll
+            for (int u = 0; u < C / 4; ++u) {
+                const float4 v = P4[u];
+                nP[4 * u] = v.x;
+                nP[4 * u + 1] = v.y;
+                nP[4 * u + 2] = v.z;
+                nP[4 * u + 3] = v.w;
+            }
+            nt[C] = p.t[g + C];
+            nP[C] = p.P[g + C];
+        } else {
+#pragma unroll
+            for (int u = 0; u <= C; ++u) {
+                if (u <= cs && cs > 0) {
+                    nt[u] = p.t[g + u];
+                    nP[u] = p.P[g + u];
+                } else {
+                    nt[u] = 0.0;
+                    nP[u] = 0.0f;
+                }
+            }
+        }
+    };
+
+    load_samples(b0);
 
     for (int64_t b = b0; b < b1; ++b) {
         const int64_t j0 = b * T;
         const int L = (int)min((int64_t)T, p.nseg - j0);
+        const int cs = min(max(L - tid * C, 0), C);  // segments of this lane
 
-        // ---- stage the tile's samples
-        {
-            const double* tg = p.t + (j0 - p.base);
-            const float* Pg = p.P + (j0 - p.base);
-            for (int i = tid; i <= L; i += NTH) {
-                sh_t[i] = tg[i];
-                sh_P[i] = Pg[i];
+        // ---- samples: stage, segment energies, checks; then prefetch the next tile
+        double Sj[C];
+        double wsum = 0.0;
+#pragma unroll
+        for (int u = 0; u <= C; ++u) {
+            sh_t[u][tid] = nt[u];
+            sh_P[u][tid] = nP[u];
+        }
+#pragma unroll
+        for (int u = 0; u < C; ++u) {
+            const double ta = nt[u], tb = nt[u + 1];
+            const float pa = nP[u], pb = nP[u + 1];
+            Sj[u] = 0.0;
+            if (u < cs) {
+                if (p.validate) {
+                    if (!(tb > ta) || !(fabs(ta) < INFINITY) || !(fabs(tb) < INFINITY))
+                        err |= ERR_TIMESTAMPS;
+                    if (!(pa >= 0.0f && pa < INFINITY) || !(pb >= 0.0f && pb < INFINITY))
+                        err |= ERR_POWER;
+                }
+                Sj[u] = 0.5 * ((double)pa + (double)pb) * (tb - ta);
+                wsum += Sj[u];
             }
         }
+        if (cs > 0 && tid * C + cs == L) sh_tend = sh_t[cs][tid];
+        if (b + 1 < b1) load_samples(b + 1);  // in flight while this tile runs
+
         if (tid < S) {
             p.cnt[(int64_t)tid * (NT + 1) + b] = st_q[tid];
+            st_q0[tid] = st_q[tid];
             st_acc[tid] = 0.0;
             st_started[tid] = 0;
         }
-        __syncthreads();
-
-        // ---- segment energies: per-thread sums of 8, then sums of 64
-        {
-            double c1 = 0.0;
+        if (ew_ready) {
 #pragma unroll
-            for (int u = 0; u < C; ++u) {
-                const int j = tid * C + u;
-                if (j < L) {
-                    const double ta = sh_t[j], tb = sh_t[j + 1];
-                    const float pa = sh_P[j], pb = sh_P[j + 1];
-                    if (p.validate) {
-                        if (!(tb > ta) || !finite_d(ta) || !finite_d(tb)) err |= ERR_TIMESTAMPS;
-                        if (!(pa >= 0.0f && pa < INFINITY) || !(pb >= 0.0f && pb < INFINITY))
-                            err |= ERR_POWER;
-                    }
-                    c1 += 0.5 * ((double)pa + (double)pb) * (tb - ta);
+            for (int v = 0; v < PER; ++v) ev_x[tid + v * NTH] = ew[v];
+        }
+        const double W = block_sum_fixed<NTH>(wsum, red);  // barriers inside
+        const double tau_end = sh_tend;
+        const double t_begin = sh_t[0][0];
+        if (tid == 0) {
+            p.tileW[b] = W;
+            sh_rs_x = t_begin;
+            sh_rs_j = -1;  // the first gap starts at the tile's first sample
+            sh_inv = (double)L / (tau_end - t_begin);
+        }
+        lds_barrier();
+        const double inv_dt = sh_inv;
+
+        // sample time / power of tile index j in [0, L]
+        auto t_at = [&](int j) -> double {
+            const int u = j & (C - 1), k = j / C;
+            return (u == 0 && k > 0) ? sh_t[C][k - 1] : sh_t[u][k];
+        };
+        auto P_at = [&](int j) -> double {
+            const int u = j & (C - 1), k = j / C;
+            return (double)((u == 0 && k > 0) ? sh_P[C][k - 1] : sh_P[u][k]);
+        };
+        auto rs_at = [&](int j) -> double { return sh_rs[j & (C - 1)][j / C]; };
+
+        double idle = 0.0;
+        for (int round = 0;; ++round) {
+            // ---- endpoint window of this round
+            if (!(round == 0 && ew_ready)) {
+                for (int idx = tid; idx < (S << lcap); idx += NTH) {
+                    const int a = idx >> lcap, r = idx & (cap - 1);
+                    const int64_t q = st_q[a] + r;
+                    ev_x[idx] = (q < st_len[a]) ? endpoint_x(p.s, p.e, st_off[a], q) : INFINITY;
                 }
+                lds_barrier();
             }
-            sh_c1[tid] = c1;
-        }
-        if (tid == 0) {
-            sh_rs_x = sh_t[0];
-            sh_rs_j = 0;
-        }
-        __syncthreads();
-        if (tid < NTH / 8) {
-            double c2 = 0.0;
-#pragma unroll
-            for (int u = 0; u < 8; ++u) c2 += sh_c1[tid * 8 + u];
-            sh_c2[tid] = c2;
-        }
-        __syncthreads();
-        if (tid == 0) {
-            double w = 0.0;
-            for (int u = 0; u < NTH / 8; ++u) w += sh_c2[u];
-            p.tileW[b] = w;
-        }
-
-        const double tau_end = sh_t[L];
-        double idle_acc = 0.0;
-
-        // ---- endpoint rounds
-        for (;;) {
-            // window of up to `cap` endpoints per stream from its cursor
-            for (int idx = tid; idx < S * cap; idx += NTH) {
-                const int a = idx / cap, r = idx - a * cap;
-                const int64_t q = st_q[a] + r;
-                ev_x[idx] = (q < st_len[a]) ? endpoint_x(p.s, p.e, st_off[a], q) : INFINITY;
-            }
-            if (tid < S) st_k[tid] = cap;
-            __syncthreads();
-            // st_k[a]: length of the prefix of the window inside this tile
-            for (int idx = tid; idx < S * cap; idx += NTH) {
-                const int a = idx / cap, r = idx - a * cap;
-                if (!(ev_x[idx] <= tau_end)) atomicMin(&st_k[a], r);
-            }
-            __syncthreads();
+            ew_ready = false;
+            if (tid < S) st_k[tid] = count_below(ev_x + (tid << lcap), cap, tau_end, true);
+            lds_barrier();
             if (tid == 0) {
                 double cut = INFINITY;
-                int full = 0, m0 = 0;
-                for (int a = 0; a < S; ++a) {
+                int full = 0;
+                for (int a = 0; a < S; ++a)
                     if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
                         full = 1;
-                        cut = fmin(cut, ev_x[a * cap + cap - 1]);
+                        cut = fmin(cut, ev_x[(a << lcap) + cap - 1]);
                     }
-                    m0 += (int)(st_q[a] & 1);
-                }
                 sh_cut = cut;
                 sh_final = !full;
-                sh_m0 = m0;
             }
-            __syncthreads();
+            lds_barrier();
             const bool fin = sh_final != 0;
-            if (tid < S) st_take[tid] = st_k[tid];
-            __syncthreads();
-            if (!fin) {
-                // a window filled up: take only endpoints <= the smallest
-                // last-loaded time, so that the round holds a time-prefix
-                const double cut = sh_cut;
-                for (int idx = tid; idx < S * cap; idx += NTH) {
-                    const int a = idx / cap, r = idx - a * cap;
-                    if (r < st_k[a] && !(ev_x[idx] <= cut)) atomicMin(&st_take[a], r);
-                }
-                __syncthreads();
+            if (tid < S) {
+                // a full window limits the round to endpoints <= cut (a time prefix)
+                st_take[tid] = fin ? st_k[tid]
+                                   : count_below(ev_x + (tid << lcap), st_k[tid], sh_cut, true);
             }
+            lds_barrier();
             if (tid == 0) {
-                int tot = 0;
-                for (int a = 0; a < S; ++a) tot += st_take[a];
-                if (tot == 0 && !fin) {
-                    // only reachable with unsorted endpoints: force progress
-                    for (int a = 0; a < S; ++a)
-                        if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
-                            st_take[a] = 1;
-                            tot = 1;
-                            break;
-                        }
-                    sh_err |= ERR_INTERVAL;
+                int tot = 0, m0 = 0;
+                if (!fin) {
+                    for (int a = 0; a < S; ++a) tot += st_take[a];
+                    if (tot == 0) {  // only with unsorted endpoints: force progress
+                        for (int a = 0; a < S; ++a)
+                            if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
+                                st_take[a] = 1;
+                                break;
+                            }
+                        sh_err |= ERR_INTERVAL;
+                    }
                 }
-                sh_Er = tot;
+                tot = 0;
+                for (int a = 0; a < S; ++a) {
+                    st_base[a] = tot;
+                    tot += st_take[a];
+                    m0 += (int)(st_q[a] & 1);
+                }
+                st_base[S] = tot;
+                sh_m0 = m0;
+                // the round's start is a breakpoint too: runs restart after it
+                if (sh_rs_j >= 0) atomicOr(&sh_flag[sh_rs_j >> 5], 1u << (sh_rs_j & 31));
             }
-            __syncthreads();
-            const int Er = sh_Er;
+            lds_barrier();
+            const int Er = st_base[S];
 
-            // segment, sample index, validation and merged position of each endpoint
-            for (int idx = tid; idx < S * cap; idx += NTH) {
-                const int a = idx / cap, r = idx - a * cap;
-                if (r >= st_take[a]) continue;
-                const double x = ev_x[idx];
-                int lo = 0, hi = L + 1;
-                while (lo < hi) {
-                    const int mid = (lo + hi) >> 1;
-                    if (sh_t[mid] < x) lo = mid + 1; else hi = mid;
+            // prefetch the next tile's endpoint window (its cursor is known now)
+            if (fin && round == 0 && b + 1 < b1) {
+#pragma unroll
+                for (int v = 0; v < PER; ++v) {
+                    const int idx = tid + v * NTH;
+                    double x = INFINITY;
+                    if (idx < (S << lcap)) {
+                        const int a = idx >> lcap, r = idx & (cap - 1);
+                        const int64_t q = st_q[a] + st_take[a] + r;
+                        if (q < st_len[a]) x = endpoint_x(p.s, p.e, st_off[a], q);
+                    }
+                    ew[v] = x;
                 }
-                const int lb = min(max(lo, 1), L);
-                const int j = lb - 1;
+                ew_ready = true;
+            }
+
+            // ---- endpoints: segment, sample index, checks, merged position
+            for (int k = tid; k < Er; k += NTH) {
+                int a = 0;
+                while (a + 1 < S && st_base[a + 1] <= k) ++a;
+                const int r = k - st_base[a];
+                const int slot = (a << lcap) + r;
+                const double x = ev_x[slot];
                 const int64_t q = st_q[a] + r;
+                // segment j with t_j < x <= t_{j+1}: guess from the mean spacing, correct
+                int j = (int)fmin(fmax((x - t_begin) * inv_dt, 0.0), (double)(L - 1));
+                int steps = 0;
+                while (j > 0 && t_at(j) >= x && steps < 8) {
+                    --j;
+                    ++steps;
+                }
+                while (j < L - 1 && t_at(j + 1) < x && steps < 16) {
+                    ++j;
+                    ++steps;
+                }
+                if (t_at(j) >= x && j > 0 || (j < L - 1 && t_at(j + 1) < x)) {
+                    int lo = 0, hi = L;  // first sample index >= x
+                    while (lo < hi) {
+                        const int mid = (lo + hi) >> 1;
+                        if (t_at(mid) < x) lo = mid + 1; else hi = mid;
+                    }
+                    j = min(max(lo, 1), L) - 1;
+                }
                 const int64_t gid = st_off[a] + (q >> 1);
                 if (q & 1) {
-                    if (p.end_idx) p.end_idx[gid] = j0 + lb;
+                    if (p.end_idx) p.end_idx[gid] = j0 + j + 1;
                 } else {
-                    if (p.start_idx) p.start_idx[gid] = j0 + lb;
+                    if (p.start_idx) p.start_idx[gid] = j0 + j + 1;
                 }
                 if (p.validate) {
-                    bool bad = !finite_d(x);
+                    bool bad = !(fabs(x) < INFINITY);
                     if (q + 1 < st_len[a]) {
-                        const double xn = (r + 1 < cap) ? ev_x[idx + 1]
+                        const double xn = (r + 1 < cap) ? ev_x[slot + 1]
                                                         : endpoint_x(p.s, p.e, st_off[a], q + 1);
                         if (!(x <= xn)) bad = true;
                     }
                     if (bad) err |= ERR_INTERVAL;
                 }
                 int pos = r;
-                for (int a2 = 0; a2 < S; ++a2) {
-                    if (a2 == a) continue;
-                    const double* x2 = ev_x + a2 * cap;
-                    int l2 = 0, h2 = st_take[a2];
-                    if (a2 < a) {
-                        while (l2 < h2) {
-                            const int m = (l2 + h2) >> 1;
-                            if (x2[m] <= x) l2 = m + 1; else h2 = m;
-                        }
-                    } else {
-                        while (l2 < h2) {
-                            const int m = (l2 + h2) >> 1;
-                            if (x2[m] < x) l2 = m + 1; else h2 = m;
-                        }
-                    }
-                    pos += l2;
-                }
+                for (int a2 = 0; a2 < S; ++a2)
+                    if (a2 != a) pos += count_below(ev_x + (a2 << lcap), st_take[a2], x, a2 < a);
                 pos = min(pos, Er - 1);
-                ev_pos[idx] = pos;
+                ev_pos[slot] = pos;
                 mg_x[pos] = x;
-                mg_j[pos] = j;
-                mg_d[pos] = (q & 1) ? -1 : 1;
+                mg_j[pos] = j | ((q & 1) ? (int)0x80000000 : 0);
+                atomicOr(&sh_flag[j >> 5], 1u << (j & 31));
             }
-            __syncthreads();
+            lds_barrier();
 
-            // concurrency in each gap: m_g = m0 + sum of +-1 before endpoint g
+            // ---- run sums: segmented scan of whole-segment energies, restarting
+            // after every segment that holds a breakpoint (its energy is cut into
+            // pieces at the breakpoints instead)
+            {
+                double loc[C];
+                double run = 0.0;
+                bool reset = false;
+#pragma unroll
+                for (int u = 0; u < C; ++u) {
+                    const int j = tid * C + u;
+                    const bool prev_flag =
+                        j > 0 && ((sh_flag[(j - 1) >> 5] >> ((j - 1) & 31)) & 1u);
+                    const bool self_flag = (sh_flag[j >> 5] >> (j & 31)) & 1u;
+                    const double v = (self_flag || u >= cs) ? 0.0 : Sj[u];
+                    if (prev_flag) {
+                        run = v;
+                        reset = true;
+                    } else {
+                        run += v;
+                    }
+                    loc[u] = run;
+                }
+                // scan of the lanes' carries (reset flag, value)
+                int h = reset ? 1 : 0;
+                double x = run;
+                for (int off = 1; off < 64; off <<= 1) {
+                    const double xo = __shfl_up(x, off);
+                    const int ho = __shfl_up(h, off);
+                    if (lane >= off) {
+                        x = h ? x : xo + x;
+                        h |= ho;
+                    }
+                }
+                if (lane == 63) {
+                    red[wave] = x;
+                    sh_wsum[wave] = h;
+                }
+                lds_barrier();
+                double px = 0.0;
+#pragma unroll
+                for (int w = 0; w < NW; ++w)
+                    if (w < wave) px = sh_wsum[w] ? red[w] : px + red[w];
+                const double incl = h ? x : px + x;
+                double cin = __shfl_up(incl, 1);
+                if (lane == 0) cin = px;
+                bool seen = false;
+#pragma unroll
+                for (int u = 0; u < C; ++u) {
+                    const int j = tid * C + u;
+                    if (j > 0 && ((sh_flag[(j - 1) >> 5] >> ((j - 1) & 31)) & 1u)) seen = true;
+                    sh_rs[u][tid] = seen ? loc[u] : cin + loc[u];
+                }
+            }
+
+            // ---- concurrency in each gap: m_g = m0 + sum of +-1 before endpoint g
             {
                 const int g0 = 2 * tid, g1 = 2 * tid + 1;
-                const int v0 = (g0 < Er) ? mg_d[g0] : 0;
-                const int v1 = (g1 < Er) ? mg_d[g1] : 0;
+                const int v0 = (g0 < Er) ? ((mg_j[g0] < 0) ? -1 : 1) : 0;
+                const int v1 = (g1 < Er) ? ((mg_j[g1] < 0) ? -1 : 1) : 0;
                 int s = v0 + v1;
                 for (int off = 1; off < 64; off <<= 1) {
                     const int y = __shfl_up(s, off);
                     if (lane >= off) s += y;
                 }
+                lds_barrier();  // the carries' scratch above is free again
                 if (lane == 63) sh_wsum[wave] = s;
-                __syncthreads();
+                lds_barrier();
                 int wbase = 0;
                 for (int w = 0; w < wave; ++w) wbase += sh_wsum[w];
                 const int excl = wbase + s - (v0 + v1);
@@ -378,9 +465,9 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                 if (g1 < Er) mg_m[g1] = m0 + excl + v0;
                 if (tid == NTH - 1) mg_m[Er] = m0 + wbase + s;
             }
-            __syncthreads();
+            lds_barrier();
 
-            // energy of each gap, divided among its active intervals
+            // ---- gap energies, split among the active intervals
             const int G = Er + (fin ? 1 : 0);
             for (int g = tid; g < G; g += NTH) {
                 double xs, xe;
@@ -390,39 +477,57 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     js = sh_rs_j;
                 } else {
                     xs = mg_x[g - 1];
-                    js = min(max(mg_j[g - 1], 0), L - 1);
+                    js = min(mg_j[g - 1] & 0x7fffffff, L - 1);
                 }
                 if (g < Er) {
                     xe = mg_x[g];
-                    je = min(max(mg_j[g], 0), L - 1);
+                    je = min(mg_j[g] & 0x7fffffff, L - 1);
                 } else {
-                    xe = sh_t[L];
+                    xe = tau_end;
                     je = L - 1;
                 }
-                const double Q = gap_energy(sh_t, sh_P, sh_c1, sh_c2, xs, js, xe, je);
+                double Q;
+                if (js == je) {
+                    const double ta = t_at(js), tb = t_at(js + 1);
+                    const double pa = P_at(js), pb = P_at(js + 1);
+                    Q = 0.5 * (lerp_power(ta, tb, pa, pb, xs) + lerp_power(ta, tb, pa, pb, xe)) *
+                        (xe - xs);
+                } else {
+                    Q = 0.0;
+                    if (js >= 0) {
+                        const double ta = t_at(js), tb = t_at(js + 1);
+                        const double pa = P_at(js), pb = P_at(js + 1);
+                        Q += 0.5 * (lerp_power(ta, tb, pa, pb, xs) + pb) * (tb - xs);
+                    }
+                    if (je > js + 1) Q += rs_at(je - 1);
+                    const double ta = t_at(je), tb = t_at(je + 1);
+                    const double pa = P_at(je), pb = P_at(je + 1);
+                    Q += 0.5 * (pa + lerp_power(ta, tb, pa, pb, xe)) * (xe - ta);
+                }
                 const int m = mg_m[g];
                 double v = 0.0;
                 if (m > 0)
                     v = p.split ? Q / (double)m : Q;
                 else
-                    idle_acc += Q;
+                    idle += Q;
                 gv[g] = v;
             }
-            __syncthreads();
+            lds_barrier();
 
-            // interval energies: intervals that start in this round
-            for (int idx = tid; idx < S * cap; idx += NTH) {
-                const int a = idx / cap, r = idx - a * cap;
-                if (r >= st_take[a]) continue;
+            // ---- interval energies: intervals starting in this round
+            for (int k = tid; k < Er; k += NTH) {
+                int a = 0;
+                while (a + 1 < S && st_base[a + 1] <= k) ++a;
+                const int r = k - st_base[a];
                 const int64_t q = st_q[a] + r;
                 if (q & 1) continue;
-                const int ps = ev_pos[idx];
-                const int64_t gid = st_off[a] + (q >> 1);
+                const int slot = (a << lcap) + r;
+                const int ps = ev_pos[slot];
                 double acc = 0.0;
                 if (r + 1 < st_take[a]) {
-                    const int pe = min(ev_pos[idx + 1], G - 1);
+                    const int pe = min(ev_pos[slot + 1], G - 1);
                     for (int g = ps + 1; g <= pe; ++g) acc += gv[g];
-                    p.energy[gid] = acc;
+                    p.energy[st_off[a] + (q >> 1)] = acc;
                 } else {
                     for (int g = ps + 1; g < G; ++g) acc += gv[g];
                     nx_acc[a] = acc;
@@ -438,12 +543,11 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                 if (active) {
                     double acc = 0.0;
                     if (take > 0) {
-                        const int pe = min(ev_pos[a * cap], G - 1);
+                        const int pe = min(ev_pos[a << lcap], G - 1);
                         for (int g = 0; g <= pe; ++g) acc += gv[g];
                         const double Et = st_acc[a] + acc;
-                        const int64_t gid = st_off[a] + (st_q[a] >> 1);
                         if (st_started[a])
-                            p.energy[gid] = Et;
+                            p.energy[st_off[a] + (st_q[a] >> 1)] = Et;
                         else
                             p.head[(int64_t)a * NT + b] = Et;
                         if (!ends_open) {
@@ -460,7 +564,9 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     nx_started[a] = 0;
                 }
             }
-            __syncthreads();
+            // clear the breakpoint flags for the next round
+            for (int w = tid; w < T / 32; w += NTH) sh_flag[w] = 0u;
+            lds_barrier();
             if (tid < S) {
                 st_q[tid] += st_take[tid];
                 st_acc[tid] = nx_acc[tid];
@@ -468,24 +574,21 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
             }
             if (tid == 0 && Er > 0) {
                 sh_rs_x = mg_x[Er - 1];
-                sh_rs_j = min(max(mg_j[Er - 1], 0), L - 1);
+                sh_rs_j = min(mg_j[Er - 1] & 0x7fffffff, L - 1);
             }
-            __syncthreads();
+            lds_barrier();
             if (fin) break;
         }
 
-        // ---- intervals still active at the tile's end
-        if (tid < S) {
-            const int a = tid;
-            if (st_q[a] & 1) {
-                if (st_started[a])
-                    p.tail[(int64_t)a * NT + b] = st_acc[a];
-                else
-                    p.head[(int64_t)a * NT + b] = st_acc[a];
-            }
+        // ---- interval still open at the tile's end: its piece of this tile
+        if (tid < S && (st_q[tid] & 1)) {
+            if (st_started[tid])
+                p.tail[(int64_t)tid * NT + b] = st_acc[tid];
+            else
+                p.head[(int64_t)tid * NT + b] = st_acc[tid];
         }
-        const double idle = block_sum_ordered<NTH>(idle_acc, sh_red);
-        if (tid == 0) p.tileIdle[b] = idle;
+        const double I = block_sum_fixed<NTH>(idle, red);
+        if (tid == 0) p.tileIdle[b] = I;
     }
 
     if (tid < S) {
@@ -494,195 +597,14 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
         if (b1 == NT) p.cnt[(int64_t)tid * (NT + 1) + NT] = st_q[tid];
     }
     if (err) atomicOr(&sh_err, err);
-    __syncthreads();
+    lds_barrier();
     if (tid == 0 && sh_err) atomicOr(&p.status->err, sh_err);
-}
-
-// ---------------------------------------------------------------------------
-// intervals whose endpoints lie in different tiles
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_cross(const FixParams p)
-{
-    const int64_t NT = p.NT;
-    const int64_t total = (int64_t)p.ss.S * (NT + 1);
-    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (int64_t)gridDim.x * blockDim.x) {
-        const int a = (int)(idx / (NT + 1));
-        const int64_t b = idx - (int64_t)a * (NT + 1);
-        const int64_t* c = p.cnt + (int64_t)a * (NT + 1);
-        const int64_t c0 = c[b];
-        const int64_t len = 2 * (p.ss.off[a + 1] - p.ss.off[a]);
-        if (p.validate && b > p.tile_begin && b < NT && (b - p.tile_begin) % p.tiles_per_wg == 0 &&
-            p.cnt_fin[(int64_t)a * (NT + 1) + b] != c0) {
-            // the workgroups' endpoint ranges do not meet: some stream is unsorted
-            atomicOr(&p.status->err, ERR_INTERVAL);
-        }
-        if (!(c0 & 1) || c0 > len) continue;            // no interval active at tile start
-        if (b > 0 && c[b - 1] == c0) continue;         // not the first tile it is active at
-        const int64_t gid = p.ss.off[a] + (c0 >> 1);
-        double E = (b > 0) ? p.tail[(int64_t)a * NT + b - 1] : 0.0;
-        for (int64_t bb = b; bb < NT && c[bb] == c0; ++bb) E += p.head[(int64_t)a * NT + bb];
-        p.energy[gid] = E;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// endpoints before t_0 or after t_{n-1}
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_outside(const FixParams p)
-{
-    const int a = blockIdx.y;
-    const int64_t NT = p.NT;
-    const int64_t off = p.ss.off[a];
-    const int64_t len = 2 * (p.ss.off[a + 1] - off);
-    const int64_t* c = p.cnt + (int64_t)a * (NT + 1);
-    const int64_t c0 = min(max(c[0], (int64_t)0), len);
-    const int64_t cN = min(max(c[NT], c0), len);
-    const int64_t nbefore = c0, nafter = len - cN;
-    const double t0 = p.status->bounds[0], tn = p.status->bounds[1];
-    unsigned err = 0u;
-    unsigned long long clipped = 0;
-    for (int64_t qq = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; qq < nbefore + nafter;
-         qq += (int64_t)gridDim.x * blockDim.x) {
-        const int64_t q = (qq < nbefore) ? qq : cN + (qq - nbefore);
-        const int64_t gid = off + (q >> 1);
-        const double x = endpoint_x(p.s, p.e, off, q);
-        const int64_t sidx = (q < c0) ? 0 : p.n_total;
-        if (q & 1) {
-            if (p.end_idx) p.end_idx[gid] = sidx;
-        } else {
-            if (p.start_idx) p.start_idx[gid] = sidx;
-        }
-        if (p.validate) {
-            bool bad = !(fabs(x) < INFINITY);
-            if (q + 1 < len && !(x <= endpoint_x(p.s, p.e, off, q + 1))) bad = true;
-            if (bad) err |= ERR_INTERVAL;
-        }
-        if (!(q & 1)) {
-            if (q + 1 < c0 || q >= cN) p.energy[gid] = 0.0;  // wholly before or after
-            if (x < t0) ++clipped;
-        } else if (q >= cN && x > tn) {
-            if (!(p.s[gid] < t0)) ++clipped;
-        }
-    }
-    if (err) atomicOr(&p.status->err, err);
-    if (clipped) atomicAdd(&p.status->n_clipped, clipped);
-}
-
-// ---------------------------------------------------------------------------
-// small kernels
-// ---------------------------------------------------------------------------
-__global__ void k_init_status(Status* st, const double* t, int64_t n)
-{
-    if (threadIdx.x == 0) {
-        st->err = 0u;
-        st->n_inserted = 0u;
-        st->special = 0u;
-        st->overflow = 0u;
-        st->n_clipped = 0ull;
-        st->n_unique = 0u;
-        st->n_cand = 0u;
-        st->n_join = 0u;
-        st->trace_energy = 0.0;
-        st->idle_energy = 0.0;
-        st->attributed_energy = 0.0;
-        if (t) {
-            st->bounds[0] = t[0];
-            st->bounds[1] = t[n - 1];
-        }
-    }
-}
-
-// whole-trace and idle energy: fixed-order reduction of the per-tile sums
-__global__ __launch_bounds__(1024) void k_summary(const double* tileW, const double* tileIdle,
-                                                   int64_t NT, Status* st)
-{
-    __shared__ double red[2][16];
-    const int tid = threadIdx.x;
-    const int64_t per = (NT + 1023) / 1024;
-    const int64_t lo = (int64_t)tid * per, hi = min(lo + per, NT);
-    double w = 0.0, z = 0.0;
-    for (int64_t b = lo; b < hi; ++b) {
-        w += tileW[b];
-        z += tileIdle[b];
-    }
-    for (int off = 32; off > 0; off >>= 1) {
-        w += __shfl_xor(w, off);
-        z += __shfl_xor(z, off);
-    }
-    if ((tid & 63) == 0) {
-        red[0][tid >> 6] = w;
-        red[1][tid >> 6] = z;
-    }
-    __syncthreads();
-    if (tid == 0) {
-        double W = 0.0, I = 0.0;
-        for (int u = 0; u < 16; ++u) {
-            W += red[0][u];
-            I += red[1][u];
-        }
-        st->trace_energy = W;
-        st->idle_energy = I;
-    }
-}
-
-__global__ __launch_bounds__(1024) void k_energy_total(const double* energy, int64_t m, Status* st)
-{
-    __shared__ double red[16];
-    const int tid = threadIdx.x;
-    const int64_t per = (m + 1023) / 1024;
-    const int64_t lo = (int64_t)tid * per, hi = min(lo + per, m);
-    double v = 0.0;
-    for (int64_t i = lo; i < hi; ++i) v += energy[i];
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if ((tid & 63) == 0) red[tid >> 6] = v;
-    __syncthreads();
-    if (tid == 0) {
-        double s = 0.0;
-        for (int u = 0; u < 16; ++u) s += red[u];
-        st->attributed_energy = s;
-    }
-}
-
-// ---------------------------------------------------------------------------
-// launchers
-// ---------------------------------------------------------------------------
-hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream)
-{
-    hipLaunchKernelGGL(k_init_status, dim3(1), dim3(64), 0, stream, st, t, n);
-    return hipGetLastError();
 }
 
 hipError_t launch_tile(const TileParams& p, int grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((k_tile<TILE, TILE_THREADS>), dim3(grid), dim3(TILE_THREADS), 0, stream, p);
-    return hipGetLastError();
-}
-
-hipError_t launch_cross(const FixParams& p, hipStream_t stream)
-{
-    const int64_t total = (int64_t)p.ss.S * (p.NT + 1);
-    const int64_t blocks = min((total + 255) / 256, (int64_t)65536);
-    hipLaunchKernelGGL(k_cross, dim3((unsigned)blocks), dim3(256), 0, stream, p);
-    return hipGetLastError();
-}
-
-hipError_t launch_outside(const FixParams& p, hipStream_t stream)
-{
-    hipLaunchKernelGGL(k_outside, dim3(32, (unsigned)p.ss.S), dim3(256), 0, stream, p);
-    return hipGetLastError();
-}
-
-hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, Status* st,
-                          hipStream_t stream)
-{
-    hipLaunchKernelGGL(k_summary, dim3(1), dim3(1024), 0, stream, tileW, tileIdle, NT, st);
-    return hipGetLastError();
-}
-
-hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream)
-{
-    hipLaunchKernelGGL(k_energy_total, dim3(1), dim3(1024), 0, stream, energy, m, st);
+    hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD>), dim3(grid), dim3(TILE_THREADS), 0,
+                       stream, p);
     return hipGetLastError();
 }
 

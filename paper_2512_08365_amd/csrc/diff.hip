@@ -69,6 +69,7 @@ __global__ __launch_bounds__(256) void k_diff_join(const DiffParams p)
     __syncthreads();
     if (valid) {
         int64_t rank = 0;
+#pragma unroll 16
         for (int q = 0; q < 256; ++q)
             if (lv[q] && before(lr[q], lk[q], r, key)) ++rank;
         if (rank < p.k) {
@@ -101,7 +102,12 @@ __global__ __launch_bounds__(256) void k_diff_rank(const DiffParams p)
             tk[v] = p.cand_key[base + v];
         }
         __syncthreads();
-        for (uint32_t v = 0; v < cnt; ++v) rank += before(tr[v], tk[v], r, key) ? 1 : 0;
+        uint32_t v = 0;
+        for (; v + 16 <= cnt; v += 16) {
+#pragma unroll
+            for (int w = 0; w < 16; ++w) rank += before(tr[v + w], tk[v + w], r, key) ? 1 : 0;
+        }
+        for (; v < cnt; ++v) rank += before(tr[v], tk[v], r, key) ? 1 : 0;
     }
     if (c < nc && rank < p.k) {
         const int32_t ia = p.cand_ia[c], ib = p.cand_ib[c];

@@ -1,9 +1,10 @@
 // groupby.hip -- per-operator-key count, sum and M2 of the interval energies.
 //
-// 1. k_keymap: every interval's 64-bit key is inserted into an open-addressing
-//    hash table (linear probing, 64-bit compare-and-swap; the all-ones key is
-//    kept out of band so any uint64 is a legal key).  Repeated keys are found
-//    with a plain load, so hot keys cost no atomics.
+// 1. k_key_insert + k_keymap: the 64-bit keys go into an open-addressing hash
+//    table (linear probing, 64-bit compare-and-swap; the all-ones key is kept
+//    out of band so any uint64 is a legal key).  Insertion de-duplicates in
+//    LDS first; the lookup pass then finds almost every key with a plain,
+//    cached load (a separate launch, so no cached line predates an insert).
 // 2. k_compact + k_rank: the distinct keys are listed and ranked (rank = number
 //    of smaller keys), which gives dense ids in ascending key order.
 // 3. k_agg_sum / k_fin_sum: each workgroup aggregates one chunk of intervals
@@ -33,12 +34,67 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t k)
 
 }  // namespace
 
-__global__ __launch_bounds__(256) void k_table_fill(unsigned long long* table, uint32_t H)
+__global__ __launch_bounds__(256) void k_table_fill(unsigned long long* table, uint32_t* urank,
+                                                    uint32_t H)
 {
-    for (uint32_t h = blockIdx.x * blockDim.x + threadIdx.x; h < H; h += gridDim.x * blockDim.x)
-        table[h] = EMPTY_KEY;
+    for (uint32_t h = blockIdx.x * blockDim.x + threadIdx.x; h <= H; h += gridDim.x * blockDim.x) {
+        if (h < H) table[h] = EMPTY_KEY;
+        urank[h] = 0u;
+    }
 }
 
+// Insert the distinct keys of a prefix of the intervals.  Each workgroup first
+// de-duplicates its chunk in an LDS table, so a key costs at most one global
+// compare-and-swap per workgroup instead of one per interval.
+constexpr int INS_CHUNK = 4096;
+constexpr int INS_SLOTS = 8192;
+constexpr int INS_GROUPS = 256;
+
+__device__ __forceinline__ void global_insert(const GroupParams& p, unsigned long long k)
+{
+    const uint32_t mask = p.H - 1u;
+    uint32_t h = (uint32_t)fmix64(k) & mask;
+    for (uint32_t probe = 0; probe < p.H; ++probe) {
+        const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
+        if (old == EMPTY_KEY) {
+            atomicAdd(&p.status->n_inserted, 1u);
+            return;
+        }
+        if (old == k) return;
+        h = (h + 1u) & mask;
+    }
+    atomicOr(&p.status->overflow, 1u);
+}
+
+__global__ __launch_bounds__(256) void k_key_insert(const GroupParams p, int64_t n_insert)
+{
+    __shared__ unsigned long long lt[INS_SLOTS];
+    for (int v = threadIdx.x; v < INS_SLOTS; v += blockDim.x) lt[v] = EMPTY_KEY;
+    lds_barrier();
+    const int64_t lo = (int64_t)blockIdx.x * INS_CHUNK, hi = min(lo + INS_CHUNK, n_insert);
+    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
+        const unsigned long long k = p.keys[i];
+        if (k == EMPTY_KEY) {
+            atomicOr(&p.status->special, 1u);
+            continue;
+        }
+        uint32_t h = (uint32_t)fmix64(k) & (INS_SLOTS - 1);
+        bool first = true;  // also when the LDS table is full: insert globally
+        for (int probe = 0; probe < INS_SLOTS; ++probe) {
+            const unsigned long long old = atomicCAS(&lt[h], EMPTY_KEY, k);
+            if (old == EMPTY_KEY) break;
+            if (old == k) {
+                first = false;
+                break;
+            }
+            h = (h + 1u) & (INS_SLOTS - 1);
+        }
+        if (first) global_insert(p, k);
+    }
+}
+
+// slot of every interval's key (the table holds most keys already, so this is
+// normally a plain cached probe)
 __global__ __launch_bounds__(256) void k_keymap(const GroupParams p)
 {
     const uint32_t H = p.H;
@@ -49,13 +105,13 @@ __global__ __launch_bounds__(256) void k_keymap(const GroupParams p)
         uint32_t slot = H + 1u;  // invalid
         if (k == EMPTY_KEY) {
             slot = H;
-            if (__hip_atomic_load(&p.status->special, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == 0u)
-                atomicOr(&p.status->special, 1u);
+            if (p.status->special == 0u) atomicOr(&p.status->special, 1u);
         } else {
             uint32_t h = (uint32_t)fmix64(k) & mask;
             for (uint32_t probe = 0; probe < H; ++probe) {
-                unsigned long long cur =
-                    __hip_atomic_load(&p.table[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                // plain (cached) load: a slot only ever changes from empty to its
+                // final key, and the compare-and-swap below settles a stale read
+                unsigned long long cur = p.table[h];
                 if (cur == k) {
                     slot = h;
                     break;
@@ -101,25 +157,37 @@ __global__ __launch_bounds__(256) void k_compact(const GroupParams p)
     }
 }
 
-// dense id = number of distinct keys smaller than this one
+// dense id = number of distinct keys smaller than this one; block (x, y)
+// compares keys [256 x, 256 x + 256) against keys [1024 y, 1024 y + 1024)
 __global__ __launch_bounds__(256) void k_rank(const GroupParams p)
 {
     __shared__ uint64_t tile[1024];
     const uint32_t nu = p.status->n_unique;
-    const uint32_t u = blockIdx.x * blockDim.x + threadIdx.x;
-    if (blockIdx.x * blockDim.x >= nu) return;  // uniform over the block
-    const uint64_t mine = (u < nu) ? p.ukey[u] : 0ull;
+    const uint32_t base = blockIdx.y * 1024u;
+    if (blockIdx.x * 256u >= nu || base >= nu) return;  // uniform over the block
+    const uint32_t u = blockIdx.x * 256u + threadIdx.x;
+    const uint32_t cnt = min(1024u, nu - base);
+    for (uint32_t v = threadIdx.x; v < cnt; v += 256u) tile[v] = p.ukey[base + v];
+    lds_barrier();
+    if (u >= nu) return;
+    const uint64_t mine = p.ukey[u];
     uint32_t rank = 0;
-    for (uint32_t base = 0; base < nu; base += 1024) {
-        const uint32_t cnt = min(1024u, nu - base);
-        __syncthreads();
-        for (uint32_t v = threadIdx.x; v < cnt; v += blockDim.x) tile[v] = p.ukey[base + v];
-        __syncthreads();
-        for (uint32_t v = 0; v < cnt; ++v) rank += (tile[v] < mine) ? 1u : 0u;
+    uint32_t v = 0;
+    for (; v + 16 <= cnt; v += 16) {
+#pragma unroll
+        for (int w = 0; w < 16; ++w) rank += (tile[v + w] < mine) ? 1u : 0u;
     }
-    if (u < nu) {
+    for (; v < cnt; ++v) rank += (tile[v] < mine) ? 1u : 0u;
+    if (rank) atomicAdd(&p.urank[u], rank);
+}
+
+__global__ __launch_bounds__(256) void k_rank_write(const GroupParams p)
+{
+    const uint32_t nu = p.status->n_unique;
+    for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < nu; u += gridDim.x * blockDim.x) {
+        const uint32_t rank = p.urank[u];
         p.slot2id[p.uslot[u]] = rank;
-        if ((int64_t)rank < p.cap) p.keys_out[rank] = mine;
+        if ((int64_t)rank < p.cap) p.keys_out[rank] = p.ukey[u];
     }
 }
 
@@ -139,13 +207,25 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
     }
     __syncthreads();
     const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
-    for (int64_t i = lo + threadIdx.x; i < hi; i += AGG_THREADS) {
-        const uint32_t sl = p.slot[i];
-        if (sl > p.H) continue;
-        const int64_t id = (int64_t)p.slot2id[sl] - r0;
-        if (id < 0 || id >= nid) continue;
-        atomicAdd(&lcnt[id], 1u);
-        atomicAdd(&lsum[id], p.energy[i]);
+    constexpr int U = 4;  // independent loads in flight per thread
+    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)U * AGG_THREADS) {
+        uint32_t sl[U];
+        double en[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t i = i0 + (int64_t)k * AGG_THREADS;
+            sl[k] = (i < hi) ? p.slot[i] : 0xffffffffu;
+            en[k] = (i < hi) ? p.energy[i] : 0.0;
+        }
+        int64_t id[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) id[k] = (sl[k] <= p.H) ? (int64_t)p.slot2id[sl[k]] - r0 : -1;
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            if (id[k] < 0 || id[k] >= nid) continue;
+            atomicAdd(&lcnt[id[k]], 1u);
+            atomicAdd(&lsum[id[k]], en[k]);
+        }
     }
     __syncthreads();
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
@@ -154,17 +234,29 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
     }
 }
 
+// 4 threads per key each add a quarter of the chunk rows; quarters combined in order
 __global__ __launch_bounds__(256) void k_fin_sum(const GroupParams p)
 {
+    __shared__ uint64_t qc[4][64];
+    __shared__ double qs[4][64];
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
-    for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < nk;
-         id += (int64_t)gridDim.x * blockDim.x) {
-        uint64_t cnt = 0;
-        double sum = 0.0;
-        for (int c = 0; c < p.nchunks; ++c) {
+    const int kl = threadIdx.x & 63, qtr = threadIdx.x >> 6;
+    const int64_t id = (int64_t)blockIdx.x * 64 + kl;
+    if ((int64_t)blockIdx.x * 64 >= nk) return;  // uniform
+    uint64_t cnt = 0;
+    double sum = 0.0;
+    if (id < nk) {
+        for (int c = qtr; c < p.nchunks; c += 4) {
             cnt += p.pcnt[(int64_t)c * p.cap + id];
             sum += p.psum[(int64_t)c * p.cap + id];
         }
+    }
+    qc[qtr][kl] = cnt;
+    qs[qtr][kl] = sum;
+    __syncthreads();
+    if (qtr == 0 && id < nk) {
+        cnt = qc[0][kl] + qc[1][kl] + qc[2][kl] + qc[3][kl];
+        sum = ((qs[0][kl] + qs[1][kl]) + qs[2][kl]) + qs[3][kl];
         p.count_out[id] = (int64_t)cnt;
         p.sum_out[id] = sum;
         p.mean[id] = cnt ? sum / (double)cnt : 0.0;
@@ -186,13 +278,25 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
     }
     __syncthreads();
     const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
-    for (int64_t i = lo + threadIdx.x; i < hi; i += AGG_THREADS) {
-        const uint32_t sl = p.slot[i];
-        if (sl > p.H) continue;
-        const int64_t id = (int64_t)p.slot2id[sl] - r0;
-        if (id < 0 || id >= nid) continue;
-        const double d = p.energy[i] - lmean[id];
-        atomicAdd(&lm2[id], d * d);
+    constexpr int U = 4;
+    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)U * AGG_THREADS) {
+        uint32_t sl[U];
+        double en[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const int64_t i = i0 + (int64_t)k * AGG_THREADS;
+            sl[k] = (i < hi) ? p.slot[i] : 0xffffffffu;
+            en[k] = (i < hi) ? p.energy[i] : 0.0;
+        }
+        int64_t id[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) id[k] = (sl[k] <= p.H) ? (int64_t)p.slot2id[sl[k]] - r0 : -1;
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            if (id[k] < 0 || id[k] >= nid) continue;
+            const double d = en[k] - lmean[id[k]];
+            atomicAdd(&lm2[id[k]], d * d);
+        }
     }
     __syncthreads();
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) p.pm2[(int64_t)c * p.cap + r0 + v] = lm2[v];
@@ -200,13 +304,17 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
 
 __global__ __launch_bounds__(256) void k_fin_m2(const GroupParams p)
 {
+    __shared__ double qs[4][64];
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
-    for (int64_t id = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; id < nk;
-         id += (int64_t)gridDim.x * blockDim.x) {
-        double m2 = 0.0;
-        for (int c = 0; c < p.nchunks; ++c) m2 += p.pm2[(int64_t)c * p.cap + id];
-        p.m2_out[id] = m2;
-    }
+    const int kl = threadIdx.x & 63, qtr = threadIdx.x >> 6;
+    const int64_t id = (int64_t)blockIdx.x * 64 + kl;
+    if ((int64_t)blockIdx.x * 64 >= nk) return;  // uniform
+    double m2 = 0.0;
+    if (id < nk)
+        for (int c = qtr; c < p.nchunks; c += 4) m2 += p.pm2[(int64_t)c * p.cap + id];
+    qs[qtr][kl] = m2;
+    __syncthreads();
+    if (qtr == 0 && id < nk) p.m2_out[id] = ((qs[0][kl] + qs[1][kl]) + qs[2][kl]) + qs[3][kl];
 }
 
 // sum of the per-key sums (attributed energy), in key order
@@ -215,10 +323,8 @@ __global__ __launch_bounds__(1024) void k_key_total(const GroupParams p)
     __shared__ double red[16];
     const int tid = threadIdx.x;
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
-    const int64_t per = (nk + 1023) / 1024;
-    const int64_t lo = (int64_t)tid * per, hi = min(lo + per, nk);
     double v = 0.0;
-    for (int64_t i = lo; i < hi; ++i) v += p.sum_out[i];
+    for (int64_t i = tid; i < nk; i += 1024) v += p.sum_out[i];
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
     if ((tid & 63) == 0) red[tid >> 6] = v;
     __syncthreads();
@@ -231,19 +337,24 @@ __global__ __launch_bounds__(1024) void k_key_total(const GroupParams p)
 
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
 {
-    const unsigned fill_blocks = (unsigned)min((p.H + 255u) / 256u, 4096u);
-    hipLaunchKernelGGL(k_table_fill, dim3(fill_blocks), dim3(256), 0, stream, p.table, p.H);
+    const unsigned fill_blocks = (unsigned)min((p.H + 256u) / 256u, 4096u);
+    hipLaunchKernelGGL(k_table_fill, dim3(fill_blocks), dim3(256), 0, stream, p.table, p.urank, p.H);
+    const int64_t n_ins = min(p.m, (int64_t)INS_CHUNK * INS_GROUPS);
+    hipLaunchKernelGGL(k_key_insert, dim3((unsigned)((n_ins + INS_CHUNK - 1) / INS_CHUNK)),
+                       dim3(256), 0, stream, p, n_ins);
     const int64_t mb = min((p.m + 255) / 256, (int64_t)16384);
     hipLaunchKernelGGL(k_keymap, dim3((unsigned)max(mb, (int64_t)1)), dim3(256), 0, stream, p);
     const unsigned hb = (unsigned)min((int64_t)(p.H + 1 + 255) / 256, (int64_t)4096);
     hipLaunchKernelGGL(k_compact, dim3(hb), dim3(256), 0, stream, p);
-    const unsigned rb = (unsigned)(((int64_t)p.H + 1 + 255) / 256);
-    hipLaunchKernelGGL(k_rank, dim3(rb), dim3(256), 0, stream, p);
+    const unsigned rx = (unsigned)(((int64_t)p.H + 1 + 255) / 256);
+    const unsigned ry = (unsigned)(((int64_t)p.H + 1 + 1023) / 1024);
+    hipLaunchKernelGGL(k_rank, dim3(rx, ry), dim3(256), 0, stream, p);
+    hipLaunchKernelGGL(k_rank_write, dim3(hb), dim3(256), 0, stream, p);
     const unsigned ranges = (unsigned)((p.cap + AGG_IDS - 1) / AGG_IDS);
     if (ranges > 0) {
         hipLaunchKernelGGL(k_agg_sum, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);
-        const unsigned kb = (unsigned)max((int64_t)1, min((p.cap + 255) / 256, (int64_t)4096));
+        const unsigned kb = (unsigned)max((int64_t)1, (p.cap + 63) / 64);
         hipLaunchKernelGGL(k_fin_sum, dim3(kb), dim3(256), 0, stream, p);
         hipLaunchKernelGGL(k_agg_m2, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);

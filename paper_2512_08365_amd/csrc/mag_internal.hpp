@@ -19,7 +19,7 @@ constexpr int TILE_THREADS = 256;
 constexpr int SEG_PER_THREAD = TILE / TILE_THREADS;  // 8
 constexpr int ROUND_EVENTS = 512;
 constexpr int MAX_STREAMS = MAG_MAX_STREAMS;
-constexpr int TILE_WGS_PER_CU = 3;  // resident tile workgroups per CU (LDS-limited)
+constexpr int TILE_WGS_PER_CU = 2;  // resident tile workgroups per CU (LDS-limited)
 
 // group-by
 constexpr int AGG_THREADS = 256;
@@ -83,6 +83,7 @@ struct TileParams {
     Status* status;
     int split;
     int validate;
+    int aligned16;      // t and P are 16-byte aligned (vector loads)
 };
 
 struct FixParams {
@@ -117,6 +118,7 @@ struct GroupParams {
     uint32_t* slot2id;    // [H+1]
     uint64_t* ukey;       // [H+1]
     uint32_t* uslot;      // [H+1]
+    uint32_t* urank;      // [H+1] rank of each distinct key (zeroed, then counted)
     double* mean;         // [cap]
     uint32_t* pcnt;       // [nchunks][cap]
     double* psum;         // [nchunks][cap]
@@ -150,6 +152,16 @@ struct DiffParams {
     int64_t* out_cb;
     Status* status;
 };
+
+// Workgroup barrier for LDS traffic only: waits for this wave's LDS operations
+// and meets the other waves, without the global-memory fence that
+// __syncthreads() implies (which would also wait for every in-flight global
+// load and store, prefetches included).  Kernels use it wherever the waves
+// only communicate through LDS.
+__device__ __forceinline__ void lds_barrier()
+{
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // launchers (return hipError_t of the launch)
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
