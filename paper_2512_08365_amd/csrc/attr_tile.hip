@@ -77,7 +77,7 @@ __device__ __forceinline__ double block_sum_fixed(double v, double* red)
 
 }  // namespace
 
-template <int NTH, int C>
+template <int NTH, int C, int SMAX>
 __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 {
     constexpr int T = NTH * C;
@@ -100,13 +100,12 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
     __shared__ double gv[E + 1];
     __shared__ int64_t st_q[MAX_STREAMS], st_q0[MAX_STREAMS], st_len[MAX_STREAMS];
     __shared__ int64_t st_off[MAX_STREAMS + 1];
-    __shared__ int st_k[MAX_STREAMS], st_take[MAX_STREAMS], st_base[MAX_STREAMS + 1];
+    __shared__ int st_k[MAX_STREAMS], st_take[MAX_STREAMS];
     __shared__ int st_started[MAX_STREAMS], nx_started[MAX_STREAMS];
     __shared__ double st_acc[MAX_STREAMS], nx_acc[MAX_STREAMS];
     __shared__ double red[NW];
     __shared__ int sh_wsum[NW];
-    __shared__ int sh_final, sh_m0, sh_rs_j;
-    __shared__ double sh_cut, sh_tend, sh_rs_x, sh_inv;
+    __shared__ double sh_tend;
     __shared__ unsigned sh_err;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -120,6 +119,10 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
     if (b0 >= b1) return;  // uniform
 
     if (tid <= S) st_off[tid] = p.ss.off[tid];
+    if (tid < S) {
+        st_k[tid] = 0;
+        st_take[tid] = 0;
+    }
     if (tid == 0) sh_err = 0u;
     for (int w = tid; w < T / 32; w += NTH) sh_flag[w] = 0u;
     lds_barrier();
@@ -195,6 +198,7 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
     };
 
     load_samples(b0);
+    double w_acc = 0.0, idle = 0.0;  // this lane's share of the trace and idle energy
 
     for (int64_t b = b0; b < b1; ++b) {
         const int64_t j0 = b * T;
@@ -238,17 +242,13 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 #pragma unroll
             for (int v = 0; v < PER; ++v) ev_x[tid + v * NTH] = ew[v];
         }
-        const double W = block_sum_fixed<NTH>(wsum, red);  // barriers inside
+        w_acc += wsum;
+        lds_barrier();
         const double tau_end = sh_tend;
         const double t_begin = sh_t[0][0];
-        if (tid == 0) {
-            p.tileW[b] = W;
-            sh_rs_x = t_begin;
-            sh_rs_j = -1;  // the first gap starts at the tile's first sample
-            sh_inv = (double)L / (tau_end - t_begin);
-        }
-        lds_barrier();
-        const double inv_dt = sh_inv;
+        const double inv_dt = (double)L / (tau_end - t_begin);
+        double rs_x = t_begin;  // where the round's first gap starts
+        int rs_j = -1;          // its segment (-1: the tile's first sample)
 
         // sample time / power of tile index j in [0, L]
         auto t_at = [&](int j) -> double {
@@ -261,7 +261,6 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
         };
         auto rs_at = [&](int j) -> double { return sh_rs[j & (C - 1)][j / C]; };
 
-        double idle = 0.0;
         for (int round = 0;; ++round) {
             // ---- endpoint window of this round
             if (!(round == 0 && ew_ready)) {
@@ -273,30 +272,41 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                 lds_barrier();
             }
             ew_ready = false;
-            if (tid < S) st_k[tid] = count_below(ev_x + (tid << lcap), cap, tau_end, true);
-            lds_barrier();
-            if (tid == 0) {
-                double cut = INFINITY;
-                int full = 0;
-                for (int a = 0; a < S; ++a)
-                    if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
-                        full = 1;
-                        cut = fmin(cut, ev_x[(a << lcap) + cap - 1]);
-                    }
-                sh_cut = cut;
-                sh_final = !full;
+            // endpoints of each stream inside this tile: the window is sorted, so
+            // their count is the length of its prefix
+            for (int idx = tid; idx < (S << lcap); idx += NTH) {
+                const bool in = ev_x[idx] <= tau_end;
+                if (cap >= 64) {  // the wave lies inside one stream's window
+                    const int c = __popcll(__ballot(in));
+                    if (lane == 0 && c) atomicAdd(&st_k[idx >> lcap], c);
+                } else if (in) {
+                    atomicAdd(&st_k[idx >> lcap], 1);
+                }
             }
             lds_barrier();
-            const bool fin = sh_final != 0;
-            if (tid < S) {
+            // every lane derives the round's shape from the counts
+            double cut = INFINITY;
+            bool fin = true;
+            for (int a = 0; a < S; ++a)
+                if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
+                    fin = false;
+                    cut = fmin(cut, ev_x[(a << lcap) + cap - 1]);
+                }
+            if (!fin) {
                 // a full window limits the round to endpoints <= cut (a time prefix)
-                st_take[tid] = fin ? st_k[tid]
-                                   : count_below(ev_x + (tid << lcap), st_k[tid], sh_cut, true);
-            }
-            lds_barrier();
-            if (tid == 0) {
-                int tot = 0, m0 = 0;
-                if (!fin) {
+                for (int idx = tid; idx < (S << lcap); idx += NTH) {
+                    const int a = idx >> lcap, r = idx & (cap - 1);
+                    const bool in = r < st_k[a] && ev_x[idx] <= cut;
+                    if (cap >= 64) {
+                        const int c = __popcll(__ballot(in));
+                        if (lane == 0 && c) atomicAdd(&st_take[a], c);
+                    } else if (in) {
+                        atomicAdd(&st_take[a], 1);
+                    }
+                }
+                lds_barrier();
+                if (tid == 0) {
+                    int tot = 0;
                     for (int a = 0; a < S; ++a) tot += st_take[a];
                     if (tot == 0) {  // only with unsorted endpoints: force progress
                         for (int a = 0; a < S; ++a)
@@ -307,19 +317,16 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                         sh_err |= ERR_INTERVAL;
                     }
                 }
-                tot = 0;
-                for (int a = 0; a < S; ++a) {
-                    st_base[a] = tot;
-                    tot += st_take[a];
-                    m0 += (int)(st_q[a] & 1);
-                }
-                st_base[S] = tot;
-                sh_m0 = m0;
-                // the round's start is a breakpoint too: runs restart after it
-                if (sh_rs_j >= 0) atomicOr(&sh_flag[sh_rs_j >> 5], 1u << (sh_rs_j & 31));
+                lds_barrier();
             }
-            lds_barrier();
-            const int Er = st_base[S];
+            const int* take = fin ? st_k : st_take;
+            int Er = 0, m0 = 0;
+            for (int a = 0; a < S; ++a) {
+                Er += take[a];
+                m0 += (int)(st_q[a] & 1);
+            }
+            // the round's start is a breakpoint too: runs restart after it
+            if (tid == 0 && rs_j >= 0) atomicOr(&sh_flag[rs_j >> 5], 1u << (rs_j & 31));
 
             // prefetch the next tile's endpoint window (its cursor is known now)
             if (fin && round == 0 && b + 1 < b1) {
@@ -329,7 +336,7 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     double x = INFINITY;
                     if (idx < (S << lcap)) {
                         const int a = idx >> lcap, r = idx & (cap - 1);
-                        const int64_t q = st_q[a] + st_take[a] + r;
+                        const int64_t q = st_q[a] + take[a] + r;
                         if (q < st_len[a]) x = endpoint_x(p.s, p.e, st_off[a], q);
                     }
                     ew[v] = x;
@@ -339,9 +346,8 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 
             // ---- endpoints: segment, sample index, checks, merged position
             for (int k = tid; k < Er; k += NTH) {
-                int a = 0;
-                while (a + 1 < S && st_base[a + 1] <= k) ++a;
-                const int r = k - st_base[a];
+                int a = 0, r = k;
+                while (a + 1 < S && r >= take[a]) r -= take[a++];
                 const int slot = (a << lcap) + r;
                 const double x = ev_x[slot];
                 const int64_t q = st_q[a] + r;
@@ -356,7 +362,7 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     ++j;
                     ++steps;
                 }
-                if (t_at(j) >= x && j > 0 || (j < L - 1 && t_at(j + 1) < x)) {
+                if ((t_at(j) >= x && j > 0) || (j < L - 1 && t_at(j + 1) < x)) {
                     int lo = 0, hi = L;  // first sample index >= x
                     while (lo < hi) {
                         const int mid = (lo + hi) >> 1;
@@ -379,9 +385,33 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     }
                     if (bad) err |= ERR_INTERVAL;
                 }
+                // position in the time-merged order: endpoints of the other streams
+                // before x (ties: lower stream first).  Entries past a stream's take
+                // lie after x, so fixed-depth searches over the whole windows,
+                // interleaved across streams, give the counts.
                 int pos = r;
-                for (int a2 = 0; a2 < S; ++a2)
-                    if (a2 != a) pos += count_below(ev_x + (a2 << lcap), st_take[a2], x, a2 < a);
+                {
+                    int c[SMAX];
+#pragma unroll
+                    for (int a2 = 0; a2 < SMAX; ++a2) c[a2] = 0;
+                    for (int step = cap >> 1; step > 0; step >>= 1) {
+#pragma unroll
+                        for (int a2 = 0; a2 < SMAX; ++a2) {
+                            if (a2 < S && a2 != a) {
+                                const double y = ev_x[(a2 << lcap) + c[a2] + step - 1];
+                                if (a2 < a ? (y <= x) : (y < x)) c[a2] += step;
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int a2 = 0; a2 < SMAX; ++a2) {
+                        if (a2 < S && a2 != a) {
+                            const double y = ev_x[(a2 << lcap) + c[a2]];
+                            if (a2 < a ? (y <= x) : (y < x)) ++c[a2];
+                            pos += min(c[a2], take[a2]);
+                        }
+                    }
+                }
                 pos = min(pos, Er - 1);
                 ev_pos[slot] = pos;
                 mg_x[pos] = x;
@@ -460,7 +490,6 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                 int wbase = 0;
                 for (int w = 0; w < wave; ++w) wbase += sh_wsum[w];
                 const int excl = wbase + s - (v0 + v1);
-                const int m0 = sh_m0;
                 if (g0 < Er) mg_m[g0] = m0 + excl;
                 if (g1 < Er) mg_m[g1] = m0 + excl + v0;
                 if (tid == NTH - 1) mg_m[Er] = m0 + wbase + s;
@@ -473,8 +502,8 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                 double xs, xe;
                 int js, je;
                 if (g == 0) {
-                    xs = sh_rs_x;
-                    js = sh_rs_j;
+                    xs = rs_x;
+                    js = rs_j;
                 } else {
                     xs = mg_x[g - 1];
                     js = min(mg_j[g - 1] & 0x7fffffff, L - 1);
@@ -516,15 +545,14 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 
             // ---- interval energies: intervals starting in this round
             for (int k = tid; k < Er; k += NTH) {
-                int a = 0;
-                while (a + 1 < S && st_base[a + 1] <= k) ++a;
-                const int r = k - st_base[a];
+                int a = 0, r = k;
+                while (a + 1 < S && r >= take[a]) r -= take[a++];
                 const int64_t q = st_q[a] + r;
                 if (q & 1) continue;
                 const int slot = (a << lcap) + r;
                 const int ps = ev_pos[slot];
                 double acc = 0.0;
-                if (r + 1 < st_take[a]) {
+                if (r + 1 < take[a]) {
                     const int pe = min(ev_pos[slot + 1], G - 1);
                     for (int g = ps + 1; g <= pe; ++g) acc += gv[g];
                     p.energy[st_off[a] + (q >> 1)] = acc;
@@ -537,12 +565,12 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
             // the interval each stream carried into this round
             if (tid < S) {
                 const int a = tid;
-                const int take = st_take[a];
+                const int ta = take[a];
                 const bool active = (st_q[a] & 1) != 0;
-                const bool ends_open = ((st_q[a] + take) & 1) != 0;
+                const bool ends_open = ((st_q[a] + ta) & 1) != 0;
                 if (active) {
                     double acc = 0.0;
-                    if (take > 0) {
+                    if (ta > 0) {
                         const int pe = min(ev_pos[a << lcap], G - 1);
                         for (int g = 0; g <= pe; ++g) acc += gv[g];
                         const double Et = st_acc[a] + acc;
@@ -568,15 +596,19 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
             for (int w = tid; w < T / 32; w += NTH) sh_flag[w] = 0u;
             lds_barrier();
             if (tid < S) {
-                st_q[tid] += st_take[tid];
+                st_q[tid] += take[tid];
                 st_acc[tid] = nx_acc[tid];
                 st_started[tid] = nx_started[tid];
             }
-            if (tid == 0 && Er > 0) {
-                sh_rs_x = mg_x[Er - 1];
-                sh_rs_j = min(mg_j[Er - 1] & 0x7fffffff, L - 1);
-            }
             lds_barrier();
+            if (tid < S) {
+                st_k[tid] = 0;
+                st_take[tid] = 0;
+            }
+            if (Er > 0) {
+                rs_x = mg_x[Er - 1];
+                rs_j = min(mg_j[Er - 1] & 0x7fffffff, L - 1);
+            }
             if (fin) break;
         }
 
@@ -587,8 +619,14 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
             else
                 p.head[(int64_t)tid * NT + b] = st_acc[tid];
         }
-        const double I = block_sum_fixed<NTH>(idle, red);
-        if (tid == 0) p.tileIdle[b] = I;
+    }
+
+    // the workgroup's trace and idle energy, kept at its first tile (others 0)
+    const double Wt = block_sum_fixed<NTH>(w_acc, red);
+    const double It = block_sum_fixed<NTH>(idle, red);
+    for (int64_t b = b0 + tid; b < b1; b += NTH) {
+        p.tileW[b] = (b == b0) ? Wt : 0.0;
+        p.tileIdle[b] = (b == b0) ? It : 0.0;
     }
 
     if (tid < S) {
@@ -603,8 +641,15 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 
 hipError_t launch_tile(const TileParams& p, int grid, hipStream_t stream)
 {
-    hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD>), dim3(grid), dim3(TILE_THREADS), 0,
-                       stream, p);
+    if (p.ss.S == 1)
+        hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD, 1>), dim3(grid),
+                           dim3(TILE_THREADS), 0, stream, p);
+    else if (p.ss.S <= 4)
+        hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD, 4>), dim3(grid),
+                           dim3(TILE_THREADS), 0, stream, p);
+    else
+        hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD, MAX_STREAMS>), dim3(grid),
+                           dim3(TILE_THREADS), 0, stream, p);
     return hipGetLastError();
 }
 

@@ -5,7 +5,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-#include "../../include/magneton.h"
+#include "magneton.h"
 
 namespace mag {
 
