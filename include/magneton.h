@@ -197,6 +197,71 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
              const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
              size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Chunked streaming.  A long trace (for example an hour of samples at
+ * 100 kHz, Section 5.2's continuous power source) can be attributed while it
+ * arrives, chunk by chunk, with the intervals already resident on the device.
+ * The result is the one mag_attribute would give for the concatenated trace,
+ * bit for bit: the same tiles run the same kernels, whatever the chunking.
+ * Carried from chunk to chunk, inside the caller's workspace: the per-tile
+ * stream cursors and partial energies of intervals still open, the samples of
+ * the tile that straddles the chunk boundary, and the status block.
+ *
+ *   mag_stream_workspace_size(max_samples, n_intervals, key_capacity, opts,
+ *                             &bytes)
+ *       workspace for a trace of at most max_samples samples (host only).
+ *   mag_stream_begin(&h, max_samples, starts, ends, op_keys, n_intervals,
+ *                    opts, per_interval, key_capacity, workspace, bytes,
+ *                    stream)
+ *       intervals, keys, options and per-interval outputs as for
+ *       mag_attribute (they must stay valid and unchanged until
+ *       mag_stream_end); key_capacity > 0 reserves the per-key table
+ *       (op_keys required), 0 skips grouping.  Host checks only; *h is a
+ *       host object owned by the caller until mag_stream_end or
+ *       mag_stream_abort.
+ *   mag_stream_push(h, t_chunk, p_chunk, n_chunk)
+ *       the next n_chunk samples (device arrays, same layout and rules as
+ *       mag_attribute's timestamps/power; n_chunk may be 0).  Asynchronous on
+ *       the stream given at begin: the chunk must stay unchanged until the
+ *       work enqueued by this call has run (reusing it from later work on the
+ *       same stream is safe).  Errors: MAG_E_SIZE (more than max_samples in
+ *       total), MAG_E_NULL, MAG_E_ALIGN, MAG_E_STATE, MAG_E_HIP.
+ *       Device-detected input errors are reported by mag_stream_end.
+ *   mag_stream_end(h, keys_out, per_key, summary)
+ *       runs the last tile, the cross-tile fix-ups and the grouping, and
+ *       synchronizes; per_key (capacity equal to key_capacity) may be NULL.
+ *       Returns what mag_attribute would return for the whole trace, or
+ *       MAG_E_STATE (a failed push), MAG_E_SIZE (fewer than 2 samples).
+ *       Always releases h.
+ *   mag_stream_abort(h)
+ *       releases h without finishing (no device work).
+ *   mag_stream_state_export(h, host_buf, &bytes)
+ *       checkpoint: copies the carried state, and the per-interval outputs
+ *       written so far, to host memory (host_buf NULL: *bytes = size needed).
+ *       Synchronizes the stream.
+ *   mag_stream_state_import(h, host_buf, bytes)
+ *       resume: h must be freshly begun with the same sizes, options and
+ *       output set as the exported stream (other device addresses are fine);
+ *       the next push continues after the last exported sample.  MAG_E_STATE
+ *       for a mismatch, MAG_E_SIZE for a short buffer.
+ */
+typedef struct mag_stream mag_stream;
+
+int mag_stream_workspace_size(int64_t max_samples, int64_t n_intervals, int64_t key_capacity,
+                              const mag_attr_opts* opts, size_t* bytes);
+int mag_stream_begin(mag_stream** handle, int64_t max_samples, const double* starts,
+                     const double* ends, const uint64_t* op_keys, int64_t n_intervals,
+                     const mag_attr_opts* opts, mag_interval_out* per_interval,
+                     int64_t key_capacity, void* workspace, size_t workspace_bytes,
+                     hipStream_t stream);
+int mag_stream_push(mag_stream* handle, const double* t_chunk, const float* p_chunk,
+                    int64_t n_chunk);
+int mag_stream_end(mag_stream* handle, uint64_t* keys_out, mag_key_stats* per_key,
+                   mag_summary* summary);
+void mag_stream_abort(mag_stream* handle);
+int mag_stream_state_export(const mag_stream* handle, void* host_buf, size_t* bytes);
+int mag_stream_state_import(mag_stream* handle, const void* host_buf, size_t bytes);
+
 /* Static description of a status code. */
 const char* mag_strerror(int status);
 /* Detail of the last error on the calling thread ("" if none). */

@@ -14,8 +14,9 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "diff", "workspace_size", "diff_workspace_size",
-           "version", "EQUAL_SPLIT", "SKIP_VALIDATE"]
+__all__ = ["MagnetonError", "attribute", "diff", "Stream", "workspace_size",
+           "stream_workspace_size", "diff_workspace_size", "version", "EQUAL_SPLIT",
+           "SKIP_VALIDATE"]
 
 EQUAL_SPLIT = N.MAG_EQUAL_SPLIT
 SKIP_VALIDATE = N.MAG_SKIP_VALIDATE
@@ -179,3 +180,124 @@ def diff(a: dict, b: dict, k: int, workspace=None):
     return {"key": key[:r], "ratio": ratio[:r], "energy_a": ea[:r], "energy_b": eb[:r],
             "count_a": ca[:r], "count_b": cb[:r], "n_only_a": int(ro.n_only_a),
             "n_only_b": int(ro.n_only_b), "n_join": int(ro.n_join)}
+
+
+def stream_workspace_size(max_samples: int, n_intervals: int, key_capacity: int = 0,
+                          n_streams: int = 1, stream_offsets=None, flags: int = EQUAL_SPLIT) -> int:
+    o, keep = _opts(n_streams, stream_offsets, flags)
+    b = ctypes.c_size_t(0)
+    _check(_lib().mag_stream_workspace_size(max_samples, n_intervals, key_capacity,
+                                             ctypes.byref(o), ctypes.byref(b)))
+    return int(b.value)
+
+
+class Stream:
+    """Chunked attribution of a trace that arrives in pieces.
+
+    The intervals (and keys) are given up front; push() hands over the next
+    chunk of samples; end() returns what attribute() returns for the whole
+    trace.  Chunks are read asynchronously on the current stream: keep them
+    alive and unchanged until later work on that stream (this object keeps a
+    reference to each chunk until end()).
+    """
+
+    def __init__(self, max_samples: int, s, e, keys=None, *, n_streams: int = 1,
+                 stream_offsets=None, equal_split: bool = True, validate: bool = True,
+                 key_capacity: int | None = None, indices: bool = True):
+        lib = _lib()
+        m = int(s.shape[0])
+        dev = s.device
+        self._dev = dev
+        flags = (EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE)
+        self._o, self._keep = _opts(n_streams, stream_offsets, flags)
+        self._group = keys is not None
+        self._cap = (int(key_capacity) if key_capacity is not None else max(1, m)) if self._group else 0
+        ws = stream_workspace_size(max_samples, m, self._cap, n_streams, stream_offsets, flags)
+        self._ws = torch.empty(ws, dtype=torch.uint8, device=dev)
+        self.energy = torch.empty(m, dtype=torch.float64, device=dev)
+        self.start_idx = torch.empty(m, dtype=torch.int64, device=dev) if indices else None
+        self.end_idx = torch.empty(m, dtype=torch.int64, device=dev) if indices else None
+        self._pio = N.IntervalOut(self.energy.data_ptr(),
+                                  self.start_idx.data_ptr() if indices else None,
+                                  self.end_idx.data_ptr() if indices else None)
+        self._inputs = (s, e, keys)
+        self._chunks = []
+        h = ctypes.c_void_p(None)
+        _check(lib.mag_stream_begin(
+            ctypes.byref(h), int(max_samples), _dev_ptr(s, torch.float64, "s"),
+            _dev_ptr(e, torch.float64, "e"),
+            _dev_ptr(keys, torch.int64, "keys") if self._group else None, m, ctypes.byref(self._o),
+            ctypes.byref(self._pio), self._cap, self._ws.data_ptr(), self._ws.numel(),
+            _stream_handle(dev)))
+        self._h = h
+
+    def _handle(self):
+        if self._h is None or not self._h.value:
+            raise MagnetonError(N.MAG_E_STATE, "stream already ended")
+        return self._h
+
+    def push(self, t, P):
+        h = self._handle()
+        n = int(t.shape[0])
+        if int(P.shape[0]) != n:
+            raise MagnetonError(N.MAG_E_SIZE, "t and P differ in length")
+        self._chunks.append((t, P))
+        _check(_lib().mag_stream_push(h, _dev_ptr(t, torch.float64, "t"),
+                                      _dev_ptr(P, torch.float32, "P"), n))
+
+    def export_state(self) -> bytes:
+        h = self._handle()
+        lib = _lib()
+        b = ctypes.c_size_t(0)
+        _check(lib.mag_stream_state_export(h, None, ctypes.byref(b)))
+        buf = ctypes.create_string_buffer(int(b.value))
+        _check(lib.mag_stream_state_export(h, buf, ctypes.byref(b)))
+        return buf.raw[:int(b.value)]
+
+    def import_state(self, state: bytes):
+        h = self._handle()
+        buf = ctypes.create_string_buffer(state, len(state))
+        _check(_lib().mag_stream_state_import(h, buf, len(state)))
+
+    def abort(self):
+        if self._h is not None and self._h.value:
+            _lib().mag_stream_abort(self._h)
+        self._h = None
+        self._chunks = []
+
+    def end(self):
+        h = self._handle()
+        self._h = None
+        dev = self._dev
+        cap = self._cap
+        ks = None
+        kout = ksum = km2 = kcnt = None
+        if self._group:
+            kout = torch.empty(cap, dtype=torch.int64, device=dev)
+            ksum = torch.empty(cap, dtype=torch.float64, device=dev)
+            km2 = torch.empty(cap, dtype=torch.float64, device=dev)
+            kcnt = torch.empty(cap, dtype=torch.int64, device=dev)
+            ks = N.KeyStats(ksum.data_ptr(), km2.data_ptr(), kcnt.data_ptr(), cap, 0)
+        summ = N.Summary()
+        rc = _lib().mag_stream_end(h, kout.data_ptr() if self._group else None,
+                                   ctypes.byref(ks) if self._group else None, ctypes.byref(summ))
+        self._chunks = []
+        _check(rc)
+        per_interval = {"energy": self.energy}
+        if self.start_idx is not None:
+            per_interval["start_idx"] = self.start_idx
+            per_interval["end_idx"] = self.end_idx
+        per_key = None
+        if self._group:
+            nk = int(ks.n_keys)
+            per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+        summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
+                   "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
+                   "n_keys": int(summ.n_keys)}
+        return per_interval, per_key, summary
+
+    def __del__(self):
+        try:
+            self.abort()
+        except Exception:
+            pass

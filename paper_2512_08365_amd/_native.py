@@ -32,6 +32,8 @@ MAG_MAX_STREAMS = 32
 # every symbol include/magneton.h declares
 EXPORTED = (
     "mag_attribute_workspace_size", "mag_attribute", "mag_diff_workspace_size", "mag_diff",
+    "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
+    "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
     "mag_strerror", "mag_last_error", "mag_version",
 )
 
@@ -86,6 +88,21 @@ def load(path: str = LIB_PATH):
     lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,
                              ctypes.c_size_t, c_vp]
     lib.mag_diff.restype = ctypes.c_int
+    lib.mag_stream_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(AttrOpts), P(ctypes.c_size_t)]
+    lib.mag_stream_workspace_size.restype = ctypes.c_int
+    lib.mag_stream_begin.argtypes = [P(c_vp), c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),
+                                     P(IntervalOut), c_i64, c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_stream_begin.restype = ctypes.c_int
+    lib.mag_stream_push.argtypes = [c_vp, c_vp, c_vp, c_i64]
+    lib.mag_stream_push.restype = ctypes.c_int
+    lib.mag_stream_end.argtypes = [c_vp, c_vp, P(KeyStats), P(Summary)]
+    lib.mag_stream_end.restype = ctypes.c_int
+    lib.mag_stream_abort.argtypes = [c_vp]
+    lib.mag_stream_abort.restype = None
+    lib.mag_stream_state_export.argtypes = [c_vp, c_vp, P(ctypes.c_size_t)]
+    lib.mag_stream_state_export.restype = ctypes.c_int
+    lib.mag_stream_state_import.argtypes = [c_vp, c_vp, ctypes.c_size_t]
+    lib.mag_stream_state_import.restype = ctypes.c_int
     lib.mag_strerror.argtypes = [ctypes.c_int]
     lib.mag_strerror.restype = ctypes.c_char_p
     lib.mag_last_error.argtypes = []

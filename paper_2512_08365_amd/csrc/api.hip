@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <new>
 
 #include "mag_internal.hpp"
 
@@ -55,6 +56,7 @@ struct Plan {
     uint32_t H;
     int nchunks;
     int64_t chunk;
+    bool staging;
 };
 
 struct AttrWorkspace {
@@ -76,6 +78,8 @@ struct AttrWorkspace {
     uint32_t* pcnt;
     double* psum;
     double* pm2;
+    double* stage_t;
+    float* stage_P;
 };
 
 void plan_groupby(Plan& pl)
@@ -99,6 +103,10 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
     w.tileW = c.take<double>((size_t)pl.NT);
     w.tileIdle = c.take<double>((size_t)pl.NT);
     w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
+    if (pl.staging) {
+        w.stage_t = c.take<double>((size_t)mag::TILE + 1);
+        w.stage_P = c.take<float>((size_t)mag::TILE + 1);
+    }
     if (pl.H > 0) {
         w.table = c.take<unsigned long long>(pl.H);
         w.slot = c.take<uint32_t>((size_t)std::max<int64_t>(pl.m, 1));
@@ -216,145 +224,126 @@ const char* mag_strerror(int status)
 }
 
 int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
-                                 const mag_attr_opts* opts, size_t* bytes)
+                                 const mag_attr_opts* opts, size_t* bytes);
+
+}  // extern "C"
+
+namespace {
+
+int plan_attribution(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
+                     const mag_attr_opts* opts, bool streaming, uint32_t* flags,
+                     mag::StreamSet* ss)
 {
-    g_last_error[0] = 0;
-    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
     if (n_samples < 2) return fail(MAG_E_SIZE, "n_samples must be >= 2");
     if (n_intervals < 0 || key_capacity < 0) return fail(MAG_E_SIZE, "negative size");
     int S;
-    uint32_t flags;
-    int rc = check_opts(opts, n_intervals, &S, &flags, nullptr);
+    int rc = check_opts(opts, n_intervals, &S, flags, ss);
     if (rc) return rc;
-    Plan pl{};
+    pl = Plan{};
     pl.n = n_samples;
     pl.m = n_intervals;
     pl.S = S;
     pl.NT = (n_samples - 1 + mag::TILE - 1) / mag::TILE;
     pl.cap = key_capacity;
     pl.H = 0;
+    pl.staging = streaming;
     if (key_capacity > 0) plan_groupby(pl);
-    AttrWorkspace w{};
-    *bytes = carve(pl, nullptr, w);
     return MAG_OK;
 }
 
-int mag_attribute(const double* timestamps, const float* power, int64_t n_samples,
-                  const double* starts, const double* ends, const uint64_t* op_keys,
-                  int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
-                  uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary, void* workspace,
-                  size_t workspace_bytes, hipStream_t stream)
-{
-    g_last_error[0] = 0;
-    if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
-    if (n_samples < 2) return fail(MAG_E_SIZE, "n_samples must be >= 2");
-    if (n_intervals < 0) return fail(MAG_E_SIZE, "n_intervals must be >= 0");
-    if (n_intervals > 0 && (!starts || !ends)) return fail(MAG_E_NULL, "starts/ends is NULL");
-    if (per_key) {
-        if (per_key->capacity < 1) return fail(MAG_E_SIZE, "per_key->capacity must be >= 1");
-        if (!keys_out || !per_key->sum || !per_key->m2 || !per_key->count)
-            return fail(MAG_E_NULL, "per-key output array is NULL");
-        if (n_intervals > 0 && !op_keys) return fail(MAG_E_NULL, "op_keys is NULL");
-    }
-    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
-    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
-    if (!aligned(timestamps, 8) || !aligned(power, 4) || (starts && !aligned(starts, 8)) ||
-        (ends && !aligned(ends, 8)) || (op_keys && !aligned(op_keys, 8)))
-        return fail(MAG_E_ALIGN, "input array not aligned to its element size");
-
-    int S;
-    uint32_t flags;
-    mag::StreamSet ss;
-    int rc = check_opts(opts, n_intervals, &S, &flags, &ss);
-    if (rc) return rc;
-
-    const bool group = per_key != nullptr;
+// One attribution job: plan, carved workspace and launch parameters, shared
+// by the one-shot call and the chunked streaming calls.  pl.NT is the number
+// of tiles the workspace holds (the row stride of the per-tile arrays).
+struct Job {
     Plan pl{};
-    pl.n = n_samples;
-    pl.m = n_intervals;
-    pl.S = S;
-    pl.NT = (n_samples - 1 + mag::TILE - 1) / mag::TILE;
-    pl.cap = group ? per_key->capacity : 0;
-    pl.H = 0;
-    if (group) plan_groupby(pl);
     AttrWorkspace w{};
-    const size_t need = carve(pl, nullptr, w);
-    if (workspace_bytes < need) {
-        snprintf(g_last_error, sizeof(g_last_error), "workspace needs %zu bytes, got %zu", need,
-                 workspace_bytes);
-        return MAG_E_WORKSPACE;
+    mag::StreamSet ss{};
+    uint32_t flags = 0;
+    const double* s = nullptr;
+    const double* e = nullptr;
+    const uint64_t* keys = nullptr;
+    double* energy = nullptr;
+    int64_t* start_idx = nullptr;
+    int64_t* end_idx = nullptr;
+    hipStream_t stream = nullptr;
+
+    bool validate() const { return (flags & MAG_SKIP_VALIDATE) == 0; }
+
+    // Tiles [b_begin, b_end) of a trace with `nseg` segments and `NT` tiles
+    // (any larger value while the trace's end is unknown); sample g of the
+    // trace is t[g - base], P[g - base].
+    hipError_t run_tiles(const double* t, const float* P, int64_t base, int64_t b_begin,
+                         int64_t b_end, int64_t nseg, int64_t NT)
+    {
+        if (b_end <= b_begin) return hipSuccess;
+        mag::TileParams tp{};
+        tp.t = t;
+        tp.P = P;
+        tp.base = base;
+        tp.nseg = nseg;
+        tp.n_total = nseg + 1;
+        tp.tile_begin = b_begin;
+        tp.tile_end = b_end;
+        tp.NT = NT;
+        tp.ld = pl.NT;
+        tp.s = s;
+        tp.e = e;
+        tp.ss = ss;
+        tp.energy = energy;
+        tp.start_idx = start_idx;
+        tp.end_idx = end_idx;
+        tp.cnt = w.cnt;
+        tp.cnt_fin = w.cnt_fin;
+        tp.head = w.head;
+        tp.tail = w.tail;
+        tp.tileW = w.tileW;
+        tp.tileIdle = w.tileIdle;
+        tp.status = w.status;
+        tp.split = (flags & MAG_EQUAL_SPLIT) ? 1 : 0;
+        tp.validate = validate() ? 1 : 0;
+        const int64_t ntiles = b_end - b_begin;
+        const int64_t wgs = (int64_t)mag::device_cu_count() * mag::TILE_WGS_PER_CU;
+        tp.tiles_per_wg = std::max<int64_t>(1, (ntiles + wgs - 1) / wgs);
+        const int grid = (int)((ntiles + tp.tiles_per_wg - 1) / tp.tiles_per_wg);
+        // vector loads need 16-byte aligned rows: aligned arrays and a base at a
+        // multiple of 4 samples (every tile starts at a multiple of TILE)
+        tp.aligned16 = (aligned(t, 16) && aligned(P, 16) && (base % 4) == 0) ? 1 : 0;
+        return mag::launch_tile(tp, grid, stream);
     }
-    carve(pl, workspace, w);
 
-    double* energy = (per_interval && per_interval->energy) ? per_interval->energy : w.energy;
-    hipError_t e;
-    EventTimer timer((flags & MAG_TIME_KERNELS) != 0, stream);
-    timer.mark(0);
-    if ((e = mag::launch_init_status(w.status, timestamps, n_samples, stream)) != hipSuccess)
-        return hip_fail(e, "init");
+    // cross-tile intervals, endpoints outside the trace, trace/idle totals
+    hipError_t fixups(int64_t n_samples, int64_t NT)
+    {
+        mag::FixParams fp{};
+        fp.s = s;
+        fp.e = e;
+        fp.ss = ss;
+        fp.NT = NT;
+        fp.ld = pl.NT;
+        fp.n_total = n_samples;
+        fp.cnt = w.cnt;
+        fp.cnt_fin = w.cnt_fin;
+        fp.head = w.head;
+        fp.tail = w.tail;
+        fp.energy = energy;
+        fp.start_idx = start_idx;
+        fp.end_idx = end_idx;
+        fp.status = w.status;
+        fp.validate = validate() ? 1 : 0;
+        hipError_t e2;
+        if ((e2 = mag::launch_cross(fp, stream)) != hipSuccess) return e2;
+        if ((e2 = mag::launch_outside(fp, stream)) != hipSuccess) return e2;
+        return mag::launch_summary(w.tileW, w.tileIdle, NT, w.status, stream);
+    }
 
-    // --- attribution
-    mag::TileParams tp{};
-    tp.t = timestamps;
-    tp.P = power;
-    tp.base = 0;
-    tp.nseg = n_samples - 1;
-    tp.n_total = n_samples;
-    tp.NT = pl.NT;
-    tp.tile_begin = 0;
-    tp.tile_end = pl.NT;
-    const int64_t wgs = (int64_t)mag::device_cu_count() * mag::TILE_WGS_PER_CU;
-    tp.tiles_per_wg = std::max<int64_t>(1, (pl.NT + wgs - 1) / wgs);
-    const int grid = (int)((pl.NT + tp.tiles_per_wg - 1) / tp.tiles_per_wg);
-    tp.s = starts;
-    tp.e = ends;
-    tp.ss = ss;
-    tp.energy = energy;
-    tp.start_idx = per_interval ? per_interval->start_idx : nullptr;
-    tp.end_idx = per_interval ? per_interval->end_idx : nullptr;
-    tp.cnt = w.cnt;
-    tp.cnt_fin = w.cnt_fin;
-    tp.head = w.head;
-    tp.tail = w.tail;
-    tp.tileW = w.tileW;
-    tp.tileIdle = w.tileIdle;
-    tp.status = w.status;
-    tp.split = (flags & MAG_EQUAL_SPLIT) ? 1 : 0;
-    tp.validate = (flags & MAG_SKIP_VALIDATE) ? 0 : 1;
-    tp.aligned16 = (aligned(timestamps, 16) && aligned(power, 16)) ? 1 : 0;
-    timer.mark(1);
-    e = mag::launch_tile(tp, grid, stream);
-    if (e != hipSuccess) return hip_fail(e, "tile kernel");
-    timer.mark(2);
-
-    mag::FixParams fp{};
-    fp.s = starts;
-    fp.e = ends;
-    fp.ss = ss;
-    fp.NT = pl.NT;
-    fp.n_total = n_samples;
-    fp.cnt = w.cnt;
-    fp.cnt_fin = w.cnt_fin;
-    fp.tile_begin = tp.tile_begin;
-    fp.tiles_per_wg = tp.tiles_per_wg;
-    fp.head = w.head;
-    fp.tail = w.tail;
-    fp.energy = energy;
-    fp.start_idx = tp.start_idx;
-    fp.end_idx = tp.end_idx;
-    fp.status = w.status;
-    fp.validate = tp.validate;
-    if ((e = mag::launch_cross(fp, stream)) != hipSuccess) return hip_fail(e, "cross kernel");
-    if ((e = mag::launch_outside(fp, stream)) != hipSuccess) return hip_fail(e, "outside kernel");
-    if ((e = mag::launch_summary(w.tileW, w.tileIdle, pl.NT, w.status, stream)) != hipSuccess)
-        return hip_fail(e, "summary kernel");
-
-    // --- grouping
-    if (group && n_intervals > 0) {
+    hipError_t grouping(uint64_t* keys_out, mag_key_stats* per_key)
+    {
+        if (pl.m == 0) return hipSuccess;
+        if (!per_key) return mag::launch_energy_total(energy, pl.m, w.status, stream);
         mag::GroupParams gp{};
-        gp.keys = op_keys;
+        gp.keys = keys;
         gp.energy = energy;
-        gp.m = n_intervals;
+        gp.m = pl.m;
         gp.H = pl.H;
         gp.cap = pl.cap;
         gp.nchunks = pl.nchunks;
@@ -374,43 +363,476 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         gp.m2_out = per_key->m2;
         gp.count_out = per_key->count;
         gp.status = w.status;
-        if ((e = mag::launch_groupby(gp, stream)) != hipSuccess) return hip_fail(e, "group-by");
-    } else if (n_intervals > 0) {
-        if ((e = mag::launch_energy_total(energy, n_intervals, w.status, stream)) != hipSuccess)
-            return hip_fail(e, "energy total");
+        return mag::launch_groupby(gp, stream);
     }
 
-    timer.mark(3);
-    mag::Status st;
-    if ((e = hipMemcpyAsync(&st, w.status, sizeof(st), hipMemcpyDeviceToHost, stream)) != hipSuccess)
-        return hip_fail(e, "status copy");
-    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    // read the status block back and turn it into the call's result
+    int conclude(mag_key_stats* per_key, mag_summary* summary)
+    {
+        mag::Status st;
+        hipError_t e2;
+        if ((e2 = hipMemcpyAsync(&st, w.status, sizeof(st), hipMemcpyDeviceToHost, stream)) !=
+            hipSuccess)
+            return hip_fail(e2, "status copy");
+        if ((e2 = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e2, "synchronize");
+        const int64_t n_keys = (int64_t)st.n_unique;
+        if (per_key) per_key->n_keys = std::min<int64_t>(n_keys, per_key->capacity);
+        if (summary) {
+            summary->trace_energy = st.trace_energy;
+            summary->idle_energy = st.idle_energy;
+            summary->attributed_energy = st.attributed_energy;
+            summary->n_clipped = (int64_t)st.n_clipped;
+            summary->n_keys = n_keys;
+        }
+        if (st.err & mag::ERR_TIMESTAMPS)
+            return fail(MAG_E_TIMESTAMPS, "timestamps not finite or not strictly increasing");
+        if (st.err & mag::ERR_POWER) return fail(MAG_E_POWER, "power sample negative or not finite");
+        if (st.err & mag::ERR_INTERVAL)
+            return fail(MAG_E_INTERVAL,
+                        "interval bound not finite, start > end, or a stream unsorted/overlapping");
+        if (per_key && (st.overflow || n_keys > per_key->capacity)) {
+            per_key->n_keys = n_keys;
+            snprintf(g_last_error, sizeof(g_last_error),
+                     "%lld distinct keys%s exceed the key capacity %lld", (long long)n_keys,
+                     st.overflow ? " (at least)" : "", (long long)per_key->capacity);
+            return MAG_E_CAPACITY;
+        }
+        return MAG_OK;
+    }
+};
 
-    const int64_t n_keys = (int64_t)st.n_unique;
+int check_key_outputs(const uint64_t* keys_out, const mag_key_stats* per_key)
+{
+    if (per_key->capacity < 1) return fail(MAG_E_SIZE, "per_key->capacity must be >= 1");
+    if (!keys_out || !per_key->sum || !per_key->m2 || !per_key->count)
+        return fail(MAG_E_NULL, "per-key output array is NULL");
+    if (!aligned(keys_out, 8) || !aligned(per_key->sum, 8) || !aligned(per_key->m2, 8) ||
+        !aligned(per_key->count, 8))
+        return fail(MAG_E_ALIGN, "per-key output array not aligned to its element size");
+    return MAG_OK;
+}
+
+// checks, planning and carving shared by mag_attribute and mag_stream_begin
+int prepare(Job& job, int64_t n_samples, const double* starts, const double* ends,
+            const uint64_t* op_keys, int64_t n_intervals, const mag_attr_opts* opts,
+            mag_interval_out* per_interval, int64_t key_capacity, void* workspace,
+            size_t workspace_bytes, hipStream_t stream, bool streaming)
+{
+    int rc = plan_attribution(job.pl, n_samples, n_intervals, key_capacity, opts, streaming,
+                              &job.flags, &job.ss);
+    if (rc) return rc;
+    if (n_intervals > 0 && (!starts || !ends)) return fail(MAG_E_NULL, "starts/ends is NULL");
+    if (key_capacity > 0 && n_intervals > 0 && !op_keys) return fail(MAG_E_NULL, "op_keys is NULL");
+    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if ((starts && !aligned(starts, 8)) || (ends && !aligned(ends, 8)) ||
+        (op_keys && !aligned(op_keys, 8)))
+        return fail(MAG_E_ALIGN, "interval array not aligned to its element size");
+    if (per_interval && ((per_interval->energy && !aligned(per_interval->energy, 8)) ||
+                         (per_interval->start_idx && !aligned(per_interval->start_idx, 8)) ||
+                         (per_interval->end_idx && !aligned(per_interval->end_idx, 8))))
+        return fail(MAG_E_ALIGN, "per-interval output not aligned to its element size");
+    const size_t need = carve(job.pl, nullptr, job.w);
+    if (workspace_bytes < need) {
+        snprintf(g_last_error, sizeof(g_last_error), "workspace needs %zu bytes, got %zu", need,
+                 workspace_bytes);
+        return MAG_E_WORKSPACE;
+    }
+    carve(job.pl, workspace, job.w);
+    job.s = starts;
+    job.e = ends;
+    job.keys = op_keys;
+    job.energy = (per_interval && per_interval->energy) ? per_interval->energy : job.w.energy;
+    job.start_idx = per_interval ? per_interval->start_idx : nullptr;
+    job.end_idx = per_interval ? per_interval->end_idx : nullptr;
+    job.stream = stream;
+    return MAG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
+                                 const mag_attr_opts* opts, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    Plan pl;
+    uint32_t flags;
+    int rc = plan_attribution(pl, n_samples, n_intervals, key_capacity, opts, false, &flags,
+                              nullptr);
+    if (rc) return rc;
+    AttrWorkspace w{};
+    *bytes = carve(pl, nullptr, w);
+    return MAG_OK;
+}
+
+int mag_attribute(const double* timestamps, const float* power, int64_t n_samples,
+                  const double* starts, const double* ends, const uint64_t* op_keys,
+                  int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
+                  uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary, void* workspace,
+                  size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
+    if (!aligned(timestamps, 8) || !aligned(power, 4))
+        return fail(MAG_E_ALIGN, "input array not aligned to its element size");
+    int rc;
+    if (per_key && (rc = check_key_outputs(keys_out, per_key)) != MAG_OK) return rc;
+    Job job;
+    rc = prepare(job, n_samples, starts, ends, op_keys, n_intervals, opts, per_interval,
+                 per_key ? per_key->capacity : 0, workspace, workspace_bytes, stream, false);
+    if (rc) return rc;
+
+    hipError_t e;
+    const int64_t NT = job.pl.NT;
+    EventTimer timer((job.flags & MAG_TIME_KERNELS) != 0, stream);
+    timer.mark(0);
+    if ((e = mag::launch_init(job.w.status, job.w.cnt_fin, (int64_t)job.pl.S * (NT + 1),
+                              timestamps, n_samples, stream)) != hipSuccess)
+        return hip_fail(e, "init");
+    timer.mark(1);
+    if ((e = job.run_tiles(timestamps, power, 0, 0, NT, n_samples - 1, NT)) != hipSuccess)
+        return hip_fail(e, "tile kernel");
+    timer.mark(2);
+    if ((e = job.fixups(n_samples, NT)) != hipSuccess) return hip_fail(e, "fix-up kernels");
+    if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
+    timer.mark(3);
+    rc = job.conclude(per_key, summary);
     if (summary) {
         summary->tile_kernel_ms = timer.ms(1, 2);
         summary->device_ms = timer.ms(0, 3);
     }
-    if (per_key) per_key->n_keys = std::min<int64_t>(n_keys, per_key->capacity);
-    if (summary) {
-        summary->trace_energy = st.trace_energy;
-        summary->idle_energy = st.idle_energy;
-        summary->attributed_energy = st.attributed_energy;
-        summary->n_clipped = (int64_t)st.n_clipped;
-        summary->n_keys = n_keys;
+    return rc;
+}
+
+}  // extern "C"
+
+// ---------------------------------------------------------------------------
+// chunked streaming
+//
+// The trace arrives as consecutive chunks.  Tiles are the same as in the
+// one-shot call (tile b covers samples b*TILE .. b*TILE + TILE); a tile whose
+// samples all lie in one chunk runs in place, a tile spanning two or more
+// chunks is assembled in a staging buffer first.  A tile runs only once a
+// sample beyond it has arrived, so the trace's last tile (the only one that
+// may be short, and the one that records the final cursors) runs at the end.
+// Everything carried from chunk to chunk lives in the workspace: per-tile
+// cursors and partial energies, the staging buffer and the status block.
+// ---------------------------------------------------------------------------
+
+struct mag_stream {
+    Job job;
+    int64_t received = 0;  // samples pushed so far
+    int64_t b_next = 0;    // first tile not yet run
+    int64_t n_stage = 0;   // samples held in staging, from sample b_next * TILE on
+    int failed = 0;        // a launch failed: the handle only accepts end/abort
+};
+
+namespace {
+
+constexpr uint64_t STATE_MAGIC = 0x314554415453474dull;  // "MGSTATE1"
+
+struct StateHeader {
+    uint64_t magic;
+    int64_t max_samples, n_intervals, key_capacity;
+    int32_t n_streams;
+    uint32_t flags;
+    int64_t received, b_next, n_stage;
+    uint32_t has_energy, has_start, has_end, pad;
+    uint64_t bytes_total;
+};
+
+// device regions of the carried state, in checkpoint order
+struct Region {
+    void* ptr;
+    size_t bytes;
+};
+
+int state_regions(const mag_stream* h, Region* r)
+{
+    const Job& j = h->job;
+    const size_t S = (size_t)j.pl.S, ld = (size_t)j.pl.NT, m = (size_t)j.pl.m;
+    int k = 0;
+    r[k++] = {j.w.status, sizeof(mag::Status)};
+    r[k++] = {j.w.cnt, sizeof(int64_t) * S * (ld + 1)};
+    r[k++] = {j.w.cnt_fin, sizeof(int64_t) * S * (ld + 1)};
+    r[k++] = {j.w.head, sizeof(double) * S * ld};
+    r[k++] = {j.w.tail, sizeof(double) * S * ld};
+    r[k++] = {j.w.tileW, sizeof(double) * ld};
+    r[k++] = {j.w.tileIdle, sizeof(double) * ld};
+    r[k++] = {j.w.stage_t, sizeof(double) * (mag::TILE + 1)};
+    r[k++] = {j.w.stage_P, sizeof(float) * (mag::TILE + 1)};
+    r[k++] = {j.energy, sizeof(double) * m};
+    if (j.start_idx) r[k++] = {j.start_idx, sizeof(int64_t) * m};
+    if (j.end_idx) r[k++] = {j.end_idx, sizeof(int64_t) * m};
+    return k;
+}
+
+size_t state_bytes(const mag_stream* h)
+{
+    Region r[16];
+    const int k = state_regions(h, r);
+    size_t b = sizeof(StateHeader);
+    for (int i = 0; i < k; ++i) b += r[i].bytes;
+    return b;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mag_stream_workspace_size(int64_t max_samples, int64_t n_intervals, int64_t key_capacity,
+                              const mag_attr_opts* opts, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    Plan pl;
+    uint32_t flags;
+    int rc = plan_attribution(pl, max_samples, n_intervals, key_capacity, opts, true, &flags,
+                              nullptr);
+    if (rc) return rc;
+    AttrWorkspace w{};
+    *bytes = carve(pl, nullptr, w);
+    return MAG_OK;
+}
+
+int mag_stream_begin(mag_stream** handle, int64_t max_samples, const double* starts,
+                     const double* ends, const uint64_t* op_keys, int64_t n_intervals,
+                     const mag_attr_opts* opts, mag_interval_out* per_interval,
+                     int64_t key_capacity, void* workspace, size_t workspace_bytes,
+                     hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!handle) return fail(MAG_E_NULL, "handle is NULL");
+    *handle = nullptr;
+    mag_stream* h = new (std::nothrow) mag_stream();
+    if (!h) return fail(MAG_E_STATE, "out of host memory");
+    int rc = prepare(h->job, max_samples, starts, ends, op_keys, n_intervals, opts, per_interval,
+                     key_capacity, workspace, workspace_bytes, stream, true);
+    if (rc) {
+        delete h;
+        return rc;
     }
-    if (st.err & mag::ERR_TIMESTAMPS)
-        return fail(MAG_E_TIMESTAMPS, "timestamps not finite or not strictly increasing");
-    if (st.err & mag::ERR_POWER) return fail(MAG_E_POWER, "power sample negative or not finite");
-    if (st.err & mag::ERR_INTERVAL)
-        return fail(MAG_E_INTERVAL, "interval bound not finite, start > end, or a stream unsorted/overlapping");
-    if (group && (st.overflow || n_keys > per_key->capacity)) {
-        per_key->n_keys = n_keys;
-        snprintf(g_last_error, sizeof(g_last_error),
-                 "%lld distinct keys%s exceed the key capacity %lld", (long long)n_keys,
-                 st.overflow ? " (at least)" : "", (long long)per_key->capacity);
-        return MAG_E_CAPACITY;
+    const hipError_t e = mag::launch_init(h->job.w.status, h->job.w.cnt_fin,
+                                          (int64_t)h->job.pl.S * (h->job.pl.NT + 1), nullptr, 0,
+                                          stream);
+    if (e != hipSuccess) {
+        delete h;
+        return hip_fail(e, "init");
     }
+    *handle = h;
+    return MAG_OK;
+}
+
+int mag_stream_push(mag_stream* h, const double* t_chunk, const float* p_chunk, int64_t n_chunk)
+{
+    g_last_error[0] = 0;
+    if (!h) return fail(MAG_E_NULL, "handle is NULL");
+    if (h->failed) return fail(MAG_E_STATE, "a previous call on this stream failed");
+    if (n_chunk < 0) return fail(MAG_E_SIZE, "n_chunk must be >= 0");
+    if (n_chunk == 0) return MAG_OK;
+    if (!t_chunk || !p_chunk) return fail(MAG_E_NULL, "chunk pointer is NULL");
+    if (!aligned(t_chunk, 8) || !aligned(p_chunk, 4))
+        return fail(MAG_E_ALIGN, "chunk not aligned to its element size");
+    Job& job = h->job;
+    const int64_t T = mag::TILE;
+    const int64_t g0 = h->received, g1 = g0 + n_chunk;
+    if (g1 > job.pl.n) return fail(MAG_E_SIZE, "more samples pushed than max_samples");
+    const hipStream_t st = job.stream;
+    const int64_t unknown_end = job.pl.NT + 1;  // tile count while the end is unknown
+    const int64_t full = (int64_t)1 << 62;       // segment count while the end is unknown
+    hipError_t e = hipSuccess;
+    auto bad = [&](const char* where) {
+        h->failed = 1;
+        return hip_fail(e, where);
+    };
+    auto stage = [&](int64_t at, int64_t from, int64_t count) {
+        // chunk samples [from, from + count) into staging slots [at, at + count)
+        hipError_t r = hipMemcpyAsync(job.w.stage_t + at, t_chunk + (from - g0),
+                                      sizeof(double) * count, hipMemcpyDeviceToDevice, st);
+        if (r == hipSuccess)
+            r = hipMemcpyAsync(job.w.stage_P + at, p_chunk + (from - g0), sizeof(float) * count,
+                               hipMemcpyDeviceToDevice, st);
+        return r;
+    };
+    if (g0 == 0 &&
+        (e = hipMemcpyAsync(&job.w.status->bounds[0], t_chunk, sizeof(double),
+                            hipMemcpyDeviceToDevice, st)) != hipSuccess)
+        return bad("bounds copy");
+
+    int64_t pos = g0;  // first sample of this chunk not yet consumed
+    while (h->n_stage > 0) {
+        // complete the staged tile b_next
+        const int64_t take = std::min<int64_t>(T + 1 - h->n_stage, g1 - pos);
+        if (take > 0) {
+            if ((e = stage(h->n_stage, pos, take)) != hipSuccess) return bad("staging copy");
+            h->n_stage += take;
+            pos += take;
+        }
+        if (h->n_stage < T + 1 || pos >= g1) {
+            h->received = g1;  // wait for more samples
+            return MAG_OK;
+        }
+        const int64_t b = h->b_next;
+        if ((e = job.run_tiles(job.w.stage_t, job.w.stage_P, b * T, b, b + 1, full,
+                               unknown_end)) != hipSuccess)
+            return bad("tile kernel");
+        h->b_next = b + 1;
+        if (pos - 1 >= g0) {
+            // the next tile starts inside this chunk
+            h->n_stage = 0;
+            pos -= 1;
+        } else {
+            // its first sample is the staged tile's last one
+            if ((e = hipMemcpyAsync(job.w.stage_t, job.w.stage_t + T, sizeof(double),
+                                    hipMemcpyDeviceToDevice, st)) != hipSuccess ||
+                (e = hipMemcpyAsync(job.w.stage_P, job.w.stage_P + T, sizeof(float),
+                                    hipMemcpyDeviceToDevice, st)) != hipSuccess)
+                return bad("staging copy");
+            h->n_stage = 1;
+        }
+    }
+    // pos == b_next * TILE lies in this chunk: run in place every tile with a
+    // sample after it in this chunk (tile b needs b*T + T + 1 <= g1 - 1)
+    const int64_t b0 = h->b_next;
+    int64_t b1 = b0;
+    if (g1 - 2 - T >= 0) b1 = std::max<int64_t>(b0, (g1 - 2 - T) / T + 1);
+    if (b1 > b0) {
+        if ((e = job.run_tiles(t_chunk, p_chunk, g0, b0, b1, full, unknown_end)) != hipSuccess)
+            return bad("tile kernel");
+        h->b_next = b1;
+    }
+    const int64_t first = h->b_next * T;
+    if ((e = stage(0, first, g1 - first)) != hipSuccess) return bad("staging copy");
+    h->n_stage = g1 - first;
+    h->received = g1;
+    return MAG_OK;
+}
+
+int mag_stream_end(mag_stream* h, uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary)
+{
+    g_last_error[0] = 0;
+    if (!h) return fail(MAG_E_NULL, "handle is NULL");
+    Job& job = h->job;
+    int rc = MAG_OK;
+    hipError_t e;
+    const int64_t n = h->received;
+    const int64_t NT = (n - 1 + mag::TILE - 1) / mag::TILE;
+    if (h->failed) {
+        rc = fail(MAG_E_STATE, "a previous call on this stream failed");
+    } else if (n < 2) {
+        rc = fail(MAG_E_SIZE, "fewer than 2 samples pushed");
+    } else if (per_key && job.pl.cap == 0) {
+        rc = fail(MAG_E_STATE, "per-key outputs requested but key_capacity was 0 at begin");
+    } else if (per_key && per_key->capacity != job.pl.cap) {
+        rc = fail(MAG_E_SIZE, "per_key->capacity differs from the key_capacity given at begin");
+    } else if (per_key && (rc = check_key_outputs(keys_out, per_key)) != MAG_OK) {
+        // rc set
+    } else if ((e = hipMemcpyAsync(&job.w.status->bounds[1], job.w.stage_t + (h->n_stage - 1),
+                                   sizeof(double), hipMemcpyDeviceToDevice, job.stream)) !=
+               hipSuccess) {
+        rc = hip_fail(e, "bounds copy");
+    } else if ((e = job.run_tiles(job.w.stage_t, job.w.stage_P, h->b_next * mag::TILE, h->b_next,
+                                  NT, n - 1, NT)) != hipSuccess) {
+        rc = hip_fail(e, "tile kernel");
+    } else if ((e = job.fixups(n, NT)) != hipSuccess) {
+        rc = hip_fail(e, "fix-up kernels");
+    } else if ((e = job.grouping(keys_out, per_key)) != hipSuccess) {
+        rc = hip_fail(e, "group-by");
+    } else {
+        rc = job.conclude(per_key, summary);
+    }
+    delete h;
+    return rc;
+}
+
+void mag_stream_abort(mag_stream* h) { delete h; }
+
+int mag_stream_state_export(const mag_stream* h, void* host_buf, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!h || !bytes) return fail(MAG_E_NULL, "handle/bytes is NULL");
+    if (h->failed) return fail(MAG_E_STATE, "a previous call on this stream failed");
+    const size_t need = state_bytes(h);
+    if (!host_buf) {
+        *bytes = need;
+        return MAG_OK;
+    }
+    if (*bytes < need) {
+        *bytes = need;
+        return fail(MAG_E_SIZE, "state buffer too small");
+    }
+    const Job& j = h->job;
+    StateHeader hd{};
+    hd.magic = STATE_MAGIC;
+    hd.max_samples = j.pl.n;
+    hd.n_intervals = j.pl.m;
+    hd.key_capacity = j.pl.cap;
+    hd.n_streams = j.pl.S;
+    hd.flags = j.flags;
+    hd.received = h->received;
+    hd.b_next = h->b_next;
+    hd.n_stage = h->n_stage;
+    hd.has_energy = 1;
+    hd.has_start = j.start_idx ? 1 : 0;
+    hd.has_end = j.end_idx ? 1 : 0;
+    hd.bytes_total = need;
+    char* out = static_cast<char*>(host_buf);
+    memcpy(out, &hd, sizeof(hd));
+    size_t off = sizeof(hd);
+    Region r[16];
+    const int k = state_regions(h, r);
+    hipError_t e;
+    for (int i = 0; i < k; ++i) {
+        if (r[i].bytes &&
+            (e = hipMemcpyAsync(out + off, r[i].ptr, r[i].bytes, hipMemcpyDeviceToHost, j.stream)) !=
+                hipSuccess)
+            return hip_fail(e, "state copy");
+        off += r[i].bytes;
+    }
+    if ((e = hipStreamSynchronize(j.stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    *bytes = need;
+    return MAG_OK;
+}
+
+int mag_stream_state_import(mag_stream* h, const void* host_buf, size_t bytes)
+{
+    g_last_error[0] = 0;
+    if (!h || !host_buf) return fail(MAG_E_NULL, "handle/host_buf is NULL");
+    if (h->failed || h->received != 0)
+        return fail(MAG_E_STATE, "state can only be imported into a freshly begun stream");
+    StateHeader hd;
+    if (bytes < sizeof(hd)) return fail(MAG_E_SIZE, "state buffer too small");
+    memcpy(&hd, host_buf, sizeof(hd));
+    const Job& j = h->job;
+    if (hd.magic != STATE_MAGIC) return fail(MAG_E_STATE, "not a stream state");
+    if (hd.max_samples != j.pl.n || hd.n_intervals != j.pl.m || hd.key_capacity != j.pl.cap ||
+        hd.n_streams != j.pl.S || hd.flags != j.flags || hd.has_start != (j.start_idx ? 1u : 0u) ||
+        hd.has_end != (j.end_idx ? 1u : 0u))
+        return fail(MAG_E_STATE, "state was exported from a stream begun with other arguments");
+    const size_t need = state_bytes(h);
+    if (hd.bytes_total != need || bytes < need) return fail(MAG_E_SIZE, "state buffer size mismatch");
+    if (hd.received < 0 || hd.received > j.pl.n || hd.b_next < 0 || hd.n_stage < 0 ||
+        hd.n_stage > mag::TILE + 1)
+        return fail(MAG_E_STATE, "corrupt stream state");
+    const char* in = static_cast<const char*>(host_buf);
+    size_t off = sizeof(hd);
+    Region r[16];
+    const int k = state_regions(h, r);
+    hipError_t e;
+    for (int i = 0; i < k; ++i) {
+        if (r[i].bytes &&
+            (e = hipMemcpyAsync(r[i].ptr, in + off, r[i].bytes, hipMemcpyHostToDevice, j.stream)) !=
+                hipSuccess)
+            return hip_fail(e, "state copy");
+        off += r[i].bytes;
+    }
+    if ((e = hipStreamSynchronize(j.stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    h->received = hd.received;
+    h->b_next = hd.b_next;
+    h->n_stage = hd.n_stage;
     return MAG_OK;
 }
 

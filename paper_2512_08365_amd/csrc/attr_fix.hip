@@ -23,25 +23,26 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void k_cross(const FixParams p)
 {
-    const int64_t NT = p.NT;
+    const int64_t NT = p.NT, LD = p.ld;
     const int64_t total = (int64_t)p.ss.S * (NT + 1);
     for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
          idx += (int64_t)gridDim.x * blockDim.x) {
         const int a = (int)(idx / (NT + 1));
         const int64_t b = idx - (int64_t)a * (NT + 1);
-        const int64_t* c = p.cnt + (int64_t)a * (NT + 1);
+        const int64_t* c = p.cnt + (int64_t)a * (LD + 1);
         const int64_t c0 = c[b];
         const int64_t len = 2 * (p.ss.off[a + 1] - p.ss.off[a]);
-        if (p.validate && b > p.tile_begin && b < NT && (b - p.tile_begin) % p.tiles_per_wg == 0 &&
-            p.cnt_fin[(int64_t)a * (NT + 1) + b] != c0) {
-            // the workgroups' endpoint ranges do not meet: some stream is unsorted
+        const int64_t fin = p.cnt_fin[(int64_t)a * (LD + 1) + b];
+        if (p.validate && b > 0 && b < NT && fin != CNT_UNSET && fin != c0) {
+            // a workgroup stopped at tile b with a cursor other than the one the
+            // next workgroup searched for: some stream is unsorted
             atomicOr(&p.status->err, ERR_INTERVAL);
         }
         if (!(c0 & 1) || c0 > len) continue;            // no interval active at tile start
         if (b > 0 && c[b - 1] == c0) continue;         // not the first tile it is active at
         const int64_t gid = p.ss.off[a] + (c0 >> 1);
-        double E = (b > 0) ? p.tail[(int64_t)a * NT + b - 1] : 0.0;
-        for (int64_t bb = b; bb < NT && c[bb] == c0; ++bb) E += p.head[(int64_t)a * NT + bb];
+        double E = (b > 0) ? p.tail[(int64_t)a * LD + b - 1] : 0.0;
+        for (int64_t bb = b; bb < NT && c[bb] == c0; ++bb) E += p.head[(int64_t)a * LD + bb];
         p.energy[gid] = E;
     }
 }
@@ -55,7 +56,7 @@ __global__ __launch_bounds__(256) void k_outside(const FixParams p)
     const int64_t NT = p.NT;
     const int64_t off = p.ss.off[a];
     const int64_t len = 2 * (p.ss.off[a + 1] - off);
-    const int64_t* c = p.cnt + (int64_t)a * (NT + 1);
+    const int64_t* c = p.cnt + (int64_t)a * (p.ld + 1);
     const int64_t c0 = min(max(c[0], (int64_t)0), len);
     const int64_t cN = min(max(c[NT], c0), len);
     const int64_t nbefore = c0, nafter = len - cN;
@@ -92,9 +93,13 @@ __global__ __launch_bounds__(256) void k_outside(const FixParams p)
 // ---------------------------------------------------------------------------
 // small kernels
 // ---------------------------------------------------------------------------
-__global__ void k_init_status(Status* st, const double* t, int64_t n)
+__global__ __launch_bounds__(256) void k_init(Status* st, int64_t* cnt_fin, int64_t n_fin,
+                                              const double* t, int64_t n)
 {
-    if (threadIdx.x == 0) {
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_fin;
+         i += (int64_t)gridDim.x * blockDim.x)
+        cnt_fin[i] = CNT_UNSET;
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
         st->err = 0u;
         st->n_inserted = 0u;
         st->special = 0u;
@@ -163,10 +168,18 @@ __global__ __launch_bounds__(1024) void k_energy_total(const double* energy, int
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
+hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double* t, int64_t n,
+                       hipStream_t stream)
+{
+    const int64_t blocks = max((int64_t)1, min((n_fin + 255) / 256, (int64_t)1024));
+    hipLaunchKernelGGL(k_init, dim3((unsigned)blocks), dim3(256), 0, stream, st, cnt_fin, n_fin, t,
+                       n);
+    return hipGetLastError();
+}
+
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_init_status, dim3(1), dim3(64), 0, stream, st, t, n);
-    return hipGetLastError();
+    return launch_init(st, nullptr, 0, t, n, stream);
 }
 
 hipError_t launch_cross(const FixParams& p, hipStream_t stream)

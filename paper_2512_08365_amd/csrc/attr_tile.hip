@@ -113,7 +113,8 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
     int lcap = 0;  // window slots per stream: the largest power of two with S * cap <= E
     while ((S << (lcap + 1)) <= E) ++lcap;
     const int cap = 1 << lcap;
-    const int64_t NT = p.NT;
+    const int64_t NT = p.NT;  // the last tile's successor (larger while the end is unknown)
+    const int64_t LD = p.ld;
     const int64_t b0 = p.tile_begin + (int64_t)blockIdx.x * p.tiles_per_wg;
     const int64_t b1 = min(b0 + p.tiles_per_wg, p.tile_end);
     if (b0 >= b1) return;  // uniform
@@ -233,7 +234,7 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
         if (b + 1 < b1) load_samples(b + 1);  // in flight while this tile runs
 
         if (tid < S) {
-            p.cnt[(int64_t)tid * (NT + 1) + b] = st_q[tid];
+            p.cnt[(int64_t)tid * (LD + 1) + b] = st_q[tid];
             st_q0[tid] = st_q[tid];
             st_acc[tid] = 0.0;
             st_started[tid] = 0;
@@ -577,7 +578,7 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                         if (st_started[a])
                             p.energy[st_off[a] + (st_q[a] >> 1)] = Et;
                         else
-                            p.head[(int64_t)a * NT + b] = Et;
+                            p.head[(int64_t)a * LD + b] = Et;
                         if (!ends_open) {
                             nx_acc[a] = 0.0;
                             nx_started[a] = 0;
@@ -615,9 +616,9 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
         // ---- interval still open at the tile's end: its piece of this tile
         if (tid < S && (st_q[tid] & 1)) {
             if (st_started[tid])
-                p.tail[(int64_t)tid * NT + b] = st_acc[tid];
+                p.tail[(int64_t)tid * LD + b] = st_acc[tid];
             else
-                p.head[(int64_t)tid * NT + b] = st_acc[tid];
+                p.head[(int64_t)tid * LD + b] = st_acc[tid];
         }
     }
 
@@ -631,8 +632,8 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
 
     if (tid < S) {
         // where this workgroup stopped: the next workgroup must start there
-        p.cnt_fin[(int64_t)tid * (NT + 1) + b1] = st_q[tid];
-        if (b1 == NT) p.cnt[(int64_t)tid * (NT + 1) + NT] = st_q[tid];
+        p.cnt_fin[(int64_t)tid * (LD + 1) + b1] = st_q[tid];
+        if (b1 == NT) p.cnt[(int64_t)tid * (LD + 1) + NT] = st_q[tid];
     }
     if (err) atomicOr(&sh_err, err);
     lds_barrier();

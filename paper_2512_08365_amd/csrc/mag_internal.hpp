@@ -26,6 +26,9 @@ constexpr int AGG_THREADS = 256;
 constexpr int AGG_IDS = 4096;       // key ids per LDS table (count u32 + sum f64)
 constexpr int AGG_MAX_CHUNKS = 256; // interval chunks (partial tables)
 
+// cnt_fin entry that no workgroup wrote (no workgroup of any launch ended there)
+constexpr int64_t CNT_UNSET = -1;
+
 // device-side error bits
 enum : uint32_t {
     ERR_TIMESTAMPS = 1u,
@@ -67,17 +70,19 @@ struct TileParams {
     int64_t tile_begin; // global tile range of this launch
     int64_t tile_end;
     int64_t tiles_per_wg;
-    int64_t NT;         // tiles of the whole trace
+    int64_t NT;         // tiles of the whole trace (any larger value when not yet known)
+    int64_t ld;         // row stride of cnt/cnt_fin (ld + 1) and head/tail (ld), ld >= tiles
     const double* s;
     const double* e;
     StreamSet ss;
     double* energy;
     int64_t* start_idx;
     int64_t* end_idx;
-    int64_t* cnt;       // [S][NT+1] endpoints <= tile start time, per stream
-    int64_t* cnt_fin;   // [S][NT+1] cursor of a workgroup after its last tile (at that tile's end)
-    double* head;       // [S][NT] in-tile energy of the interval active at tile start
-    double* tail;       // [S][NT] in-tile energy of the interval started in the tile, active at its end
+    int64_t* cnt;       // [S][ld+1] endpoints <= tile start time, per stream
+    int64_t* cnt_fin;   // [S][ld+1] cursor of a workgroup after its last tile, at the index of
+                        // the tile after it (CNT_UNSET where no workgroup ended)
+    double* head;       // [S][ld] in-tile energy of the interval active at tile start
+    double* tail;       // [S][ld] in-tile energy of the interval started in the tile, active at its end
     double* tileW;      // [NT]
     double* tileIdle;   // [NT]
     Status* status;
@@ -91,9 +96,8 @@ struct FixParams {
     const double* e;
     StreamSet ss;
     int64_t NT;
+    int64_t ld;           // row strides as in TileParams
     int64_t n_total;
-    int64_t tile_begin;   // workgroup boundaries of the tile launch: tile_begin + w * tiles_per_wg
-    int64_t tiles_per_wg;
     const int64_t* cnt;
     const int64_t* cnt_fin;
     const double* head;
@@ -164,6 +168,9 @@ __device__ __forceinline__ void lds_barrier()
 }
 
 // launchers (return hipError_t of the launch)
+// status block reset (bounds from t[0], t[n-1] when t is given) and cnt_fin := CNT_UNSET
+hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double* t, int64_t n,
+                       hipStream_t stream);
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
 hipError_t launch_tile(const TileParams& p, int grid, hipStream_t stream);
 hipError_t launch_cross(const FixParams& p, hipStream_t stream);

@@ -168,3 +168,23 @@ def tiny_case(seed: int, n: int = 64, streams: int = 1, per_stream: int = 8,
     key = key_vocab[rng.integers(0, keys, size=s.shape[0])] if s.shape[0] else np.zeros(0, np.uint64)
     return {"t": t.astype(np.float64), "P": P, "s": s.astype(np.float64), "e": e.astype(np.float64),
             "key": key.astype(np.uint64), "offsets": np.array(off, dtype=np.int64)}
+
+
+def long_trace(seed, n, streams, per_stream, outside=True):
+    """A trace of ~1 us steps whose intervals range from sub-sample to many
+    thousands of samples, some starting before or ending after the trace."""
+    rng = np.random.default_rng(seed)
+    t = np.concatenate([[0.0], np.cumsum(rng.uniform(0.5, 1.5, n - 1))]) * 1e-6
+    P = rng.uniform(50, 800, n).astype(np.float32)
+    s_all, e_all, off = [], [], [0]
+    lo, hi = t[0], t[-1]
+    for a in range(streams):
+        pad = 0.05 * (hi - lo) if outside else 0.0
+        cuts = np.sort(rng.uniform(lo - pad, hi + pad, 2 * per_stream))
+        s_all.append(cuts[0::2])
+        e_all.append(cuts[1::2])
+        off.append(off[-1] + per_stream)
+    s = np.concatenate(s_all)
+    e = np.concatenate(e_all)
+    key = rng.integers(0, 40, s.shape[0]).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    return {"t": t, "P": P, "s": s, "e": e, "key": key, "offsets": np.array(off, np.int64)}

@@ -23,7 +23,9 @@ def _declared():
 def test_header_declares_the_entry_points():
     names = _declared()
     assert {"mag_attribute", "mag_diff", "mag_attribute_workspace_size",
-            "mag_diff_workspace_size", "mag_strerror", "mag_last_error"} <= names
+            "mag_diff_workspace_size", "mag_stream_workspace_size", "mag_stream_begin",
+            "mag_stream_push", "mag_stream_end", "mag_stream_abort", "mag_stream_state_export",
+            "mag_stream_state_import", "mag_strerror", "mag_last_error"} <= names
 
 
 def test_library_exports_every_declared_symbol():
@@ -72,6 +74,35 @@ def test_host_side_errors_without_gpu():
     assert lib.mag_diff_workspace_size(5, 5, -1, ctypes.byref(b)) == N.MAG_E_SIZE
     for code in range(-12, 1):
         assert lib.mag_strerror(code)
+
+
+def test_stream_host_side_errors_without_gpu():
+    from paper_2512_08365_amd import _native as N
+    lib = N.load()
+    b = ctypes.c_size_t(0)
+    assert lib.mag_stream_workspace_size(1, 0, 0, None, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_stream_workspace_size(10, 0, 0, None, None) == N.MAG_E_NULL
+    assert lib.mag_stream_workspace_size(10, 3, -1, None, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_stream_workspace_size(10_000, 3, 8, None, ctypes.byref(b)) == N.MAG_OK
+    one = b.value
+    assert lib.mag_attribute_workspace_size(10_000, 3, 8, None, ctypes.byref(b)) == N.MAG_OK
+    assert one > b.value  # the staging buffer of the tile spanning two chunks
+    h = ctypes.c_void_p(1234)
+    fake = ctypes.c_void_p(256)
+    assert lib.mag_stream_begin(None, 10, None, None, None, 0, None, None, 0, fake, 1 << 20,
+                                None) == N.MAG_E_NULL
+    assert lib.mag_stream_begin(ctypes.byref(h), 1, None, None, None, 0, None, None, 0, fake,
+                                1 << 20, None) == N.MAG_E_SIZE
+    assert h.value is None  # no handle on failure
+    assert lib.mag_stream_begin(ctypes.byref(h), 10, fake, fake, None, 3, None, None, 4, fake,
+                                1 << 20, None) == N.MAG_E_NULL  # keys needed for grouping
+    assert lib.mag_stream_begin(ctypes.byref(h), 10, fake, fake, None, 3, None, None, 0, fake,
+                                16, None) == N.MAG_E_WORKSPACE
+    assert lib.mag_stream_push(None, fake, fake, 10) == N.MAG_E_NULL
+    assert lib.mag_stream_end(None, None, None, None) == N.MAG_E_NULL
+    assert lib.mag_stream_state_export(None, None, ctypes.byref(b)) == N.MAG_E_NULL
+    assert lib.mag_stream_state_import(None, None, 0) == N.MAG_E_NULL
+    lib.mag_stream_abort(None)
 
 
 def test_product_has_no_cpu_fallback():

@@ -47,29 +47,10 @@ def test_dyadic_bit_exact():
         assert np.array_equal(gi["energy"], o["energy"]), seed
 
 
-def _long_trace(seed, n, streams, per_stream, span_frac=0.02, outside=True):
-    """intervals whose lengths range from sub-sample to many tiles"""
-    rng = np.random.default_rng(seed)
-    t = np.concatenate([[0.0], np.cumsum(rng.uniform(0.5, 1.5, n - 1))]) * 1e-6
-    P = rng.uniform(50, 800, n).astype(np.float32)
-    s_all, e_all, off = [], [], [0]
-    lo, hi = t[0], t[-1]
-    for a in range(streams):
-        pad = 0.05 * (hi - lo) if outside else 0.0
-        cuts = np.sort(rng.uniform(lo - pad, hi + pad, 2 * per_stream))
-        s_all.append(cuts[0::2])
-        e_all.append(cuts[1::2])
-        off.append(off[-1] + per_stream)
-    s = np.concatenate(s_all)
-    e = np.concatenate(e_all)
-    key = rng.integers(0, 40, s.shape[0]).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
-    return {"t": t, "P": P, "s": s, "e": e, "key": key, "offsets": np.array(off, np.int64)}
-
-
 @pytest.mark.parametrize("streams", [1, 4])
 def test_intervals_spanning_many_tiles(streams):
     for seed, (n, per) in enumerate([(20000, 3), (50001, 40), (100000, 400), (4097, 2000)]):
-        c = _long_trace(seed, n, streams, per)
+        c = synth.long_trace(seed, n, streams, per)
         compare_attribution(c, label=f"long s{streams} n{n} per{per}")
 
 
@@ -166,7 +147,7 @@ def test_device_detected_errors():
 
 
 def test_deterministic_per_interval():
-    c = _long_trace(9, 60000, 4, 3000)
+    c = synth.long_trace(9, 60000, 4, 3000)
     a, ka, _, _ = run_gpu(c)
     b, kb, _, _ = run_gpu(c)
     for k in a:

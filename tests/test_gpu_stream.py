@@ -1,0 +1,264 @@
+"""Chunked streaming (through the C ABI): any chunking of the trace gives the
+one-shot call's per-interval results bit for bit, and the oracle's within the
+parity bar; a checkpoint exported after some chunks and imported into a new
+stream resumes to the same result; misuse is rejected with its code."""
+import numpy as np
+import pytest
+
+import synth
+from gpu_util import assert_energy_close, log, run_oracle, to_gpu
+
+pytestmark = pytest.mark.gpu
+
+TILE = 2048  # samples per tile of the library (segments); boundaries are probed around it
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    import paper_2512_08365_amd as mag
+    mag.version()
+    yield
+
+
+def _one_shot(d, off, equal_split=True):
+    import paper_2512_08365_amd as mag
+    return mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], n_streams=len(off) - 1,
+                         stream_offsets=off, equal_split=equal_split)
+
+
+def _streamed(d, off, sizes, equal_split=True, max_samples=None, checkpoint_after=None):
+    import paper_2512_08365_amd as mag
+    n = int(d["t"].shape[0])
+    assert sum(sizes) == n
+    mx = max_samples or n
+    kw = dict(n_streams=len(off) - 1, stream_offsets=off, equal_split=equal_split)
+    st = mag.Stream(mx, d["s"], d["e"], d["key"], **kw)
+    pos = 0
+    for i, c in enumerate(sizes):
+        st.push(d["t"][pos:pos + c], d["P"][pos:pos + c])
+        pos += c
+        if checkpoint_after is not None and i == checkpoint_after:
+            state = st.export_state()
+            st.abort()
+            st = mag.Stream(mx, d["s"], d["e"], d["key"], **kw)
+            st.import_state(state)
+    return st.end()
+
+
+def _np(res):
+    pi, pk, summ = res
+    a = {k: v.cpu().numpy() for k, v in pi.items()}
+    k = {kk: v.cpu().numpy() for kk, v in pk.items()}
+    return a, k, summ
+
+
+def _assert_same(a, b, label):
+    ai, ak, asumm = _np(a)
+    bi, bk, bsumm = _np(b)
+    assert np.array_equal(ai["energy"], bi["energy"]), f"{label}: energies differ"
+    assert np.array_equal(ai["start_idx"], bi["start_idx"]), label
+    assert np.array_equal(ai["end_idx"], bi["end_idx"]), label
+    assert np.array_equal(ak["keys"], bk["keys"]), label
+    assert np.array_equal(ak["count"], bk["count"]), label
+    assert_energy_close(ak["sum"], bk["sum"], f"{label}: key sums")
+    W = abs(bsumm["trace_energy"])
+    for f in ("trace_energy", "idle_energy", "attributed_energy"):
+        assert abs(asumm[f] - bsumm[f]) <= 1e-12 * max(W, 1e-300), (label, f)
+    assert asumm["n_clipped"] == bsumm["n_clipped"], label
+    assert asumm["n_keys"] == bsumm["n_keys"], label
+
+
+def _chunkings(n, rng):
+    T = TILE
+    out = [[n]]
+    fixed = [1, 2, T - 1, T, T + 1, T + 2, 3 * T + 5, 1, T + 1]
+    sz, left = [], n
+    for c in fixed:
+        if left <= 0:
+            break
+        c = min(c, left)
+        sz.append(c)
+        left -= c
+    if left > 0:
+        sz.append(left)
+    out.append(sz)
+    # tile-aligned chunks: the staged tile completes exactly at a chunk's end
+    sz, left = [], n
+    first = True
+    while left > 0:
+        c = min(T + 1 if first else T, left)
+        first = False
+        sz.append(c)
+        left -= c
+    out.append(sz)
+    sz, left = [], n
+    while left > 0:
+        c = int(min(left, rng.integers(1, 3 * T)))
+        sz.append(c)
+        left -= c
+    out.append(sz)
+    return out
+
+
+@pytest.mark.parametrize("streams,split", [(1, True), (3, True), (4, False)])
+def test_any_chunking_equals_one_shot(streams, split):
+    import torch
+    rng = np.random.default_rng(11)
+    for seed, (n, per) in enumerate([(3 * TILE + 1, 40), (20000, 300), (4 * TILE + 1, 5),
+                                     (TILE + 1, 2000), (777, 30)]):
+        c = synth.long_trace(100 + seed, n, streams, per)
+        d = to_gpu(c)
+        off = [int(x) for x in c["offsets"]]
+        ref = _one_shot(d, off, split)
+        for sizes in _chunkings(n, rng):
+            log(f"[case] stream n={n} streams={streams} split={split} chunks={len(sizes)}")
+            got = _streamed(d, off, sizes, split)
+            _assert_same(got, ref, f"n={n} chunks={sizes[:6]}")
+        # a larger max_samples than pushed (the trace's length is unknown up front)
+        got = _streamed(d, off, _chunkings(n, rng)[1], split, max_samples=n + 5 * TILE + 3)
+        _assert_same(got, ref, f"n={n} max_samples larger")
+        torch.cuda.synchronize()
+
+
+def test_streamed_matches_oracle():
+    for seed in range(6):
+        c = synth.tiny_case(900 + seed, n=int(50 + seed * 1500), streams=1 + seed % 4,
+                            per_stream=40 + 10 * seed)
+        d = to_gpu(c)
+        off = [int(x) for x in c["offsets"]]
+        n = c["t"].shape[0]
+        sizes = []
+        left = n
+        k = 1
+        while left > 0:
+            sizes.append(min(left, k))
+            left -= sizes[-1]
+            k = k * 3 + 1
+        o, g = run_oracle(c)
+        gi, gk, summ = _np(_streamed(d, off, sizes))
+        assert np.array_equal(gi["start_idx"], o["start_idx"]), seed
+        assert np.array_equal(gi["end_idx"], o["end_idx"]), seed
+        assert_energy_close(gi["energy"], o["energy"], f"seed {seed}")
+        assert np.array_equal(gk["keys"].view(np.uint64), g["keys"]), seed
+        assert np.array_equal(gk["count"], g["count"]), seed
+        assert_energy_close(gk["sum"], g["sum"], f"seed {seed}: key sums")
+        assert abs(summ["trace_energy"] - o["trace_energy"]) <= 1e-12 * o["trace_energy"]
+        assert summ["n_clipped"] == o["n_clipped"]
+
+
+def test_checkpoint_resume_equals_uninterrupted():
+    c = synth.long_trace(5, 30000, 2, 500)
+    d = to_gpu(c)
+    off = [int(x) for x in c["offsets"]]
+    sizes = [5000, 1, 4095, 7000, 2049, 11855]
+    ref = _streamed(d, off, sizes)
+    for j in range(len(sizes) - 1):
+        log(f"[case] checkpoint after chunk {j}")
+        got = _streamed(d, off, sizes, checkpoint_after=j)
+        _assert_same(got, ref, f"resume after chunk {j}")
+
+
+def test_stream_errors():
+    import torch
+    import paper_2512_08365_amd as mag
+    from paper_2512_08365_amd import _native as N
+    c = synth.long_trace(6, 10000, 1, 50)
+    d = to_gpu(c)
+    # more samples than max_samples
+    st = mag.Stream(5000, d["s"], d["e"], d["key"])
+    st.push(d["t"][:4000], d["P"][:4000])
+    with pytest.raises(mag.MagnetonError) as ei:
+        st.push(d["t"][4000:6000], d["P"][4000:6000])
+    assert ei.value.code == N.MAG_E_SIZE
+    st.abort()
+    # fewer than two samples
+    st = mag.Stream(5000, d["s"], d["e"], d["key"])
+    st.push(d["t"][:1], d["P"][:1])
+    with pytest.raises(mag.MagnetonError) as ei:
+        st.end()
+    assert ei.value.code == N.MAG_E_SIZE
+    # timestamps that go back across a chunk boundary
+    t2 = d["t"].clone()
+    t2[3000] = t2[2999] - 1e-9
+    st = mag.Stream(10000, d["s"], d["e"], d["key"])
+    st.push(t2[:3000], d["P"][:3000])
+    st.push(t2[3000:], d["P"][3000:])
+    with pytest.raises(mag.MagnetonError) as ei:
+        st.end()
+    assert ei.value.code == N.MAG_E_TIMESTAMPS
+    # a negative power sample at a chunk's first position
+    P2 = d["P"].clone()
+    P2[TILE * 2] = -1.0
+    st = mag.Stream(10000, d["s"], d["e"], d["key"])
+    st.push(d["t"][:TILE * 2], P2[:TILE * 2])
+    st.push(d["t"][TILE * 2:], P2[TILE * 2:])
+    with pytest.raises(mag.MagnetonError) as ei:
+        st.end()
+    assert ei.value.code == N.MAG_E_POWER
+    # unsorted intervals are found at the end
+    s2 = d["s"].clone()
+    e2 = d["e"].clone()
+    s2[10], s2[11] = d["s"][11], d["s"][10]
+    e2[10], e2[11] = d["e"][11], d["e"][10]
+    st = mag.Stream(10000, s2, e2, d["key"])
+    st.push(d["t"][:5000], d["P"][:5000])
+    st.push(d["t"][5000:], d["P"][5000:])
+    with pytest.raises(mag.MagnetonError) as ei:
+        st.end()
+    assert ei.value.code == N.MAG_E_INTERVAL
+    # a checkpoint imported into a stream begun with other sizes
+    st = mag.Stream(10000, d["s"], d["e"], d["key"])
+    st.push(d["t"][:3000], d["P"][:3000])
+    state = st.export_state()
+    st.abort()
+    other = mag.Stream(12000, d["s"], d["e"], d["key"])
+    with pytest.raises(mag.MagnetonError) as ei:
+        other.import_state(state)
+    assert ei.value.code == N.MAG_E_STATE
+    other.abort()
+    # a truncated checkpoint
+    st = mag.Stream(10000, d["s"], d["e"], d["key"])
+    with pytest.raises(mag.MagnetonError) as ei:
+        st.import_state(state[:-8])
+    assert ei.value.code == N.MAG_E_SIZE
+    st.abort()
+    torch.cuda.synchronize()
+
+
+@pytest.mark.slow
+def test_long_run_workload_streamed_in_32M_chunks():
+    """One side of the hour-long trace (360,000,000 samples at 100 kHz,
+    50,000,000 sequential intervals): streamed in 32,000,000-sample chunks it
+    equals the one-shot call bit for bit, and sampled intervals equal the
+    oracle's (sequential intervals do not interact, so a subset of them can be
+    checked on its own)."""
+    import torch
+    import oracle
+    c = synth.trace(5, 0, 0)
+    n = c["t"].shape[0]
+    m = c["s"].shape[0]
+    log(f"[case] long-run trace n={n} m={m}")
+    d = to_gpu(c)
+    off = [int(x) for x in c["offsets"]]
+    ref = _one_shot(d, off)
+    sizes = [32_000_000] * (n // 32_000_000)
+    if n % 32_000_000:
+        sizes.append(n % 32_000_000)
+    got = _streamed(d, off, sizes)
+    _assert_same(got, ref, "long-run")
+    gi, gk, summ = _np(got)
+    del d, ref, got
+    torch.cuda.empty_cache()
+    rng = np.random.default_rng(0)
+    pick = np.sort(rng.choice(m, 20000, replace=False))
+    pick = np.concatenate([[0, 1, m - 2, m - 1], pick])
+    pick = np.unique(pick)
+    r = oracle.attribute(c["t"], c["P"], c["s"][pick], c["e"][pick], np.array([0, pick.size]),
+                         equal_split=True)
+    assert np.array_equal(gi["start_idx"][pick], r["start_idx"])
+    assert np.array_equal(gi["end_idx"][pick], r["end_idx"])
+    assert_energy_close(gi["energy"][pick], r["energy"], "long-run sampled energies")
+    assert abs(summ["trace_energy"] - r["trace_energy"]) <= 1e-12 * r["trace_energy"]
