@@ -44,18 +44,75 @@ def source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def counters_traffic(bytes_alg: float):
-    """HBM traffic of the tile kernel from the committed counter summary, if it
-    was taken on the current kernel source (else None)."""
-    path = os.path.join(ROOT, "profiles", "tile_kernel_counters.json")
+COUNTERS_JSON = os.path.join(ROOT, "profiles", "tile_kernel_counters.json")
+COPY_BYTES = 1 << 30  # calibration copy: 1 GiB read + 1 GiB written
+
+
+def counters_traffic():
+    """HBM bytes per launch of the tile kernel from the committed counter
+    summary, if it was taken on the current kernel source (else None)."""
     try:
-        with open(path) as f:
+        with open(COUNTERS_JSON) as f:
             d = json.load(f)
     except (OSError, ValueError):
         return None
     if d.get("source_hash") != source_hash():
         return None
     return d.get("traffic_bytes_per_launch")
+
+
+def copy_calibration():
+    """A plain streaming copy of COPY_BYTES (torch's elementwise kernel computing
+    dst = src * 1), run under the same counters as the tile kernel to scale
+    FETCH_SIZE / WRITE_SIZE."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    log(f"[calibration] copied {COPY_BYTES} bytes 3 times")
+
+
+def _counter_rows(path, kernel_substr, counter):
+    import csv
+    vals = []
+    with open(path) as f:
+        for row in csv.DictReader(f):
+            if kernel_substr in row["Kernel_Name"] and row["Counter_Name"] == counter:
+                vals.append(float(row["Counter_Value"]))
+    if not vals:
+        raise SystemExit(f"no {counter} rows for '{kernel_substr}' in {path}")
+    return vals
+
+
+def summarize_counters(tile_fetch, tile_write, copy_fetch, copy_write, copy_kernel, tile_bytes):
+    """FETCH_SIZE / WRITE_SIZE (KiB per dispatch) of the tile kernel, scaled by
+    what the same counters read for the calibration copy of known size."""
+    f_t = _counter_rows(tile_fetch, "k_tile", "FETCH_SIZE")
+    w_t = _counter_rows(tile_write, "k_tile", "WRITE_SIZE")
+    f_c = _counter_rows(copy_fetch, copy_kernel, "FETCH_SIZE")
+    w_c = _counter_rows(copy_write, copy_kernel, "WRITE_SIZE")
+    # the largest dispatches of the copy kernel are the 1 GiB copies
+    f_c = max(f_c)
+    w_c = max(w_c)
+    kf = COPY_BYTES / (f_c * 1024.0)
+    kw = COPY_BYTES / (w_c * 1024.0)
+    fetch = sum(f_t) / len(f_t) * 1024.0 * kf
+    write = sum(w_t) / len(w_t) * 1024.0 * kw
+    d = {"source_hash": source_hash(), "kernel": "k_tile",
+         "fetch_kib_per_dispatch_raw": sum(f_t) / len(f_t),
+         "write_kib_per_dispatch_raw": sum(w_t) / len(w_t),
+         "copy_fetch_kib_raw": f_c, "copy_write_kib_raw": w_c,
+         "fetch_scale": kf, "write_scale": kw,
+         "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+         "traffic_bytes_per_launch": fetch + write,
+         "algorithmic_bytes_per_launch": tile_bytes,
+         "traffic_over_algorithmic": (fetch + write) / tile_bytes}
+    with open(COUNTERS_JSON, "w") as f:
+        json.dump(d, f, indent=1)
+        f.write("\n")
+    print(json.dumps(d, indent=1))
 
 
 class Side:
@@ -129,7 +186,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the 1 GiB calibration copy (for the HBM counters)")
+    ap.add_argument("--summarize-counters", nargs=5,
+                    metavar=("TILE_FETCH_CSV", "TILE_WRITE_CSV", "COPY_FETCH_CSV",
+                             "COPY_WRITE_CSV", "COPY_KERNEL_SUBSTR"),
+                    help="write the tile kernel's scaled HBM traffic from rocprofv3 --pmc CSVs")
     args = ap.parse_args()
+    if args.summarize_counters:
+        import synth
+        sh = synth.shape(WORKLOAD)
+        summarize_counters(*args.summarize_counters, tile_bytes=12 * sh["n"] + 40 * sh["m"])
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "
               "(the multi-GPU sharding is design-only).", file=sys.stderr)
@@ -145,6 +213,9 @@ def main():
     if not torch.cuda.is_available():
         log("bench.py needs a GPU")
         sys.exit(1)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     lib = N.load()
     log(f"[bench] {mag.version()} on {torch.cuda.get_device_name(0)}")
     t0 = time.perf_counter()
@@ -225,7 +296,7 @@ def main():
         "hbm_frac_algorithmic": bytes_step / sec_per_step / 1e9 / HBM_PEAK_GBS,
         "roofline": {"kernel": "k_tile (interval energies)", "bound": "hbm",
                      "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": counters_traffic(tile_bytes),
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": counters_traffic(),
                      "algorithmic_bytes_per_launch": tile_bytes,
                      "avg_launch_ms": tile_avg_ms},
     }
