@@ -301,14 +301,10 @@ struct Job {
         tp.status = w.status;
         tp.split = (flags & MAG_EQUAL_SPLIT) ? 1 : 0;
         tp.validate = validate() ? 1 : 0;
-        const int64_t ntiles = b_end - b_begin;
-        const int64_t wgs = (int64_t)mag::device_cu_count() * mag::TILE_WGS_PER_CU;
-        tp.tiles_per_wg = std::max<int64_t>(1, (ntiles + wgs - 1) / wgs);
-        const int grid = (int)((ntiles + tp.tiles_per_wg - 1) / tp.tiles_per_wg);
         // vector loads need 16-byte aligned rows: aligned arrays and a base at a
         // multiple of 4 samples (every tile starts at a multiple of TILE)
         tp.aligned16 = (aligned(t, 16) && aligned(P, 16) && (base % 4) == 0) ? 1 : 0;
-        return mag::launch_tile(tp, grid, stream);
+        return mag::launch_tile(tp, stream);
     }
 
     // cross-tile intervals, endpoints outside the trace, trace/idle totals

@@ -1,28 +1,34 @@
 // attr_tile.hip -- per-interval energy attribution on gfx950.
 //
-// The power trace is cut into tiles of T = NTH * C sample segments
-// [t_j, t_{j+1}]; a persistent workgroup walks a contiguous run of tiles and
-// prefetches the next tile's samples (and endpoint window) into registers
-// while the current tile runs.
+// The power trace is cut into tiles of T = 64 * C sample segments
+// [t_j, t_{j+1}].  One wave (a 64-lane workgroup) owns one tile at a time and
+// walks a contiguous run of tiles, carrying one cursor per interval stream (the
+// number of that stream's interval endpoints at or before the tile's start).
+// Nothing inside a tile needs a workgroup barrier: lanes exchange data through
+// wave-private LDS and ballots, so many independent waves per CU hide each
+// other's memory and LDS latency.
 //
-// Work inside a tile is split so that no lane ever loops over segments:
+// Work inside a tile:
 //   samples   (lane k owns segments kC .. kC+C-1): segment energies
-//             S_j = (P_j + P_{j+1}) (t_{j+1} - t_j) / 2, input checks, and a
-//             segmented scan of S_j that restarts after every segment holding
-//             an interval endpoint ("run sums": the energy of the whole
-//             segments since the last endpoint);
-//   endpoints (one lane per endpoint of the round): its segment (guessed from
-//             the mean sample spacing, then corrected), its sample index, its
-//             position in the time-merged order of all streams;
+//             S_j = (P_j + P_{j+1}) (t_{j+1} - t_j) / 2 and the input checks;
+//   endpoints (up to two per lane per round): the endpoint's segment (guessed
+//             from the mean sample spacing, then corrected), its sample index,
+//             its position in the time-merged order of all streams and the
+//             number of intervals active just after it -- both follow from how
+//             many endpoints of each other stream precede it, since a stream
+//             is inside an interval exactly when its cursor is odd;
+//   run sums  a segmented scan of S_j that restarts after every segment
+//             holding an endpoint (the energy of the whole segments between
+//             two consecutive endpoints);
 //   gaps      (one lane per gap between consecutive endpoints): the exact
 //             integral of the linear interpolant over the gap = trapezoid
-//             pieces at both ends + the run sum of the whole segments between,
-//             divided by the number of active intervals (equal split);
+//             pieces at both ends + the run sum between, divided by the number
+//             of active intervals (equal split);
 //   intervals (one lane per interval starting in the round): the sum of its
 //             gaps.
 // Every energy is a sum of non-negative terms; no result is a difference of
-// running totals.  A tile whose endpoints exceed the LDS window is processed
-// in several rounds, each a time prefix of the remaining endpoints.
+// running totals.  A tile whose endpoints overflow the per-stream window is
+// processed in several rounds, each a time prefix of the remaining endpoints.
 //
 // Intervals whose endpoints lie in different tiles leave partial energies:
 // head[a][b], the piece in tile b of stream a's interval active at the tile's
@@ -34,6 +40,8 @@
 namespace mag {
 
 namespace {
+
+constexpr int WAVE = 64;
 
 __device__ __forceinline__ double endpoint_x(const double* s, const double* e, int64_t off,
                                              int64_t q)
@@ -50,95 +58,100 @@ __device__ __forceinline__ double lerp_power(double ta, double tb, double pa, do
     return pa + (pb - pa) * ((x - ta) / (tb - ta));
 }
 
-// number of entries <= v (le) or < v (!le) in the sorted list xs[0, n)
-__device__ __forceinline__ int count_below(const double* xs, int n, double v, bool le)
+// Lanes of one wave communicate through LDS without s_barrier: a wave's LDS
+// operations complete in program order, and these fences keep the compiler
+// from moving memory operations across the point.
+__device__ __forceinline__ void wave_sync()
 {
-    int lo = 0, hi = n;
-    while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        const bool go = le ? (xs[mid] <= v) : (xs[mid] < v);
-        if (go) lo = mid + 1; else hi = mid;
-    }
-    return lo;
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int NTH>
-__device__ __forceinline__ double block_sum_fixed(double v, double* red)
+// set bits of the 128-bit mask (hi:lo) at positions [b, e)
+__device__ __forceinline__ int popc_range(uint64_t lo, uint64_t hi, int b, int e)
+{
+    auto part = [](uint64_t m, int pb, int pe) -> int {
+        pb = max(pb, 0);
+        pe = min(pe, 64);
+        if (pe <= pb) return 0;
+        const uint64_t upto = (pe == 64) ? ~0ull : ((1ull << pe) - 1ull);
+        return __popcll(m & upto & ~((1ull << pb) - 1ull));
+    };
+    return part(lo, b, e) + part(hi, b - 64, e - 64);
+}
+
+__device__ __forceinline__ double wave_sum(double v)
 {
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
-    lds_barrier();
-    double tot = 0.0;
-#pragma unroll
-    for (int w = 0; w < NTH / 64; ++w) tot += red[w];
-    lds_barrier();
-    return tot;
+    return v;
 }
 
 }  // namespace
 
-template <int NTH, int C, int SMAX>
-__global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
+// LDS of one wave (a workgroup holds WPB independent waves)
+template <int C, int NV, int SMAX>
+struct WaveLds {
+    static constexpr int T = WAVE * C;
+    static constexpr int E = NV * WAVE;
+    double sh_t[C + 1][WAVE];    // column k holds the C+1 samples of lane k's segments
+    float sh_P[C + 1][WAVE];
+    uint32_t flag[T / 32];       // segment holds a breakpoint of the round
+    int wp[T / 32 + 1];          // set flags in the words before each word
+    double R[E + 2];             // run sums, by rank of the breakpoint segment they end at
+    double ev_x[E];              // endpoint window, stream-major
+    double mg_x[E];              // merged endpoints
+    uint32_t mg_jm[E];           // segment | active-after << 16 | end flag << 31
+    double gv[E + 1];            // per-gap energy share
+    uint8_t ev_pos[E];           // merged position of a window slot
+    int64_t st_q[SMAX], st_off[SMAX], st_len[SMAX];
+    int st_take[SMAX], st_started[SMAX], nx_started[SMAX];
+    double st_acc[SMAX], nx_acc[SMAX];
+    double st_lastx[SMAX];       // the stream's last consumed endpoint
+};
+
+template <int C, int NV, int SMAX, int WPB>
+__global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4))) void k_tile(
+    const TileParams p)
 {
-    constexpr int T = NTH * C;
-    constexpr int E = ROUND_EVENTS;
-    constexpr int NW = NTH / 64;
-    constexpr int PER = E / NTH;  // window entries prefetched per lane
-    static_assert((E & (E - 1)) == 0 && E % NTH == 0 && E <= 2 * NTH, "window layout");
-    static_assert((C & (C - 1)) == 0, "C power of two");
+    using Lds = WaveLds<C, NV, SMAX>;
+    constexpr int T = Lds::T;
+    constexpr int E = Lds::E;
+    constexpr int NWORD = T / 32;
+    static_assert((C & (C - 1)) == 0 && C >= 4 && NWORD <= WAVE && E <= 255, "tile layout");
 
-    // samples: column tid holds the C+1 samples of lane tid's segments
-    __shared__ double sh_t[C + 1][NTH];
-    __shared__ float sh_P[C + 1][NTH];
-    __shared__ double sh_rs[C][NTH];          // run sums per segment
-    __shared__ uint32_t sh_flag[T / 32];      // segment holds a breakpoint of the round
-    __shared__ double ev_x[E];                // endpoint window, stream-major
-    __shared__ int ev_pos[E];                 // merged position of a window slot
-    __shared__ double mg_x[E];
-    __shared__ int mg_j[E];                   // segment (bits 0..30) | end flag (bit 31)
-    __shared__ int mg_m[E + 1];
-    __shared__ double gv[E + 1];
-    __shared__ int64_t st_q[MAX_STREAMS], st_q0[MAX_STREAMS], st_len[MAX_STREAMS];
-    __shared__ int64_t st_off[MAX_STREAMS + 1];
-    __shared__ int st_k[MAX_STREAMS], st_take[MAX_STREAMS];
-    __shared__ int st_started[MAX_STREAMS], nx_started[MAX_STREAMS];
-    __shared__ double st_acc[MAX_STREAMS], nx_acc[MAX_STREAMS];
-    __shared__ double red[NW];
-    __shared__ int sh_wsum[NW];
-    __shared__ double sh_tend;
-    __shared__ unsigned sh_err;
-
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    __shared__ Lds lds_all[WPB];
+    const int lane = threadIdx.x & (WAVE - 1);
+    const int wave = threadIdx.x / WAVE;
+    Lds& sm = lds_all[wave];
     const int S = p.ss.S;
-    int lcap = 0;  // window slots per stream: the largest power of two with S * cap <= E
-    while ((S << (lcap + 1)) <= E) ++lcap;
-    const int cap = 1 << lcap;
+    int lc = 0;  // window slots per stream: the largest power of two with S * cap <= E
+    while ((S << (lc + 1)) <= E) ++lc;
+    const int cap = 1 << lc;
+    const int nslot = S << lc;
     const int64_t NT = p.NT;  // the last tile's successor (larger while the end is unknown)
     const int64_t LD = p.ld;
-    const int64_t b0 = p.tile_begin + (int64_t)blockIdx.x * p.tiles_per_wg;
+    const int64_t b0 = p.tile_begin + ((int64_t)blockIdx.x * WPB + wave) * p.tiles_per_wg;
     const int64_t b1 = min(b0 + p.tiles_per_wg, p.tile_end);
-    if (b0 >= b1) return;  // uniform
+    if (b0 >= b1) return;  // uniform per wave; waves never wait for each other
 
-    if (tid <= S) st_off[tid] = p.ss.off[tid];
-    if (tid < S) {
-        st_k[tid] = 0;
-        st_take[tid] = 0;
+    if (lane < S) {
+        sm.st_off[lane] = p.ss.off[lane];
+        sm.st_len[lane] = 2 * (p.ss.off[lane + 1] - p.ss.off[lane]);
     }
-    if (tid == 0) sh_err = 0u;
-    for (int w = tid; w < T / 32; w += NTH) sh_flag[w] = 0u;
-    lds_barrier();
-    if (tid < S) st_len[tid] = 2 * (st_off[tid + 1] - st_off[tid]);
-    lds_barrier();
+    if (lane < NWORD) sm.flag[lane] = 0u;
+    wave_sync();
     {
         // cursor of each stream at the first tile: endpoints <= its start time
-        // (64-ary search, one wave per stream: about four dependent loads)
+        // (64-ary search, about four dependent loads per stream)
         const double tau0 = p.t[b0 * T - p.base];
-        for (int a = wave; a < S; a += NW) {
-            int64_t lo = 0, hi = st_len[a];
-            while (hi - lo > 64) {
-                const int64_t step = (hi - lo + 63) / 64;
+        for (int a = 0; a < S; ++a) {
+            const int64_t off = sm.st_off[a];
+            int64_t lo = 0, hi = sm.st_len[a];
+            while (hi - lo > WAVE) {
+                const int64_t step = (hi - lo + WAVE - 1) / WAVE;
                 const int64_t pr = lo + (int64_t)(lane + 1) * step - 1;
-                const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, st_off[a], pr) <= tau0);
+                const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, off, pr) <= tau0);
                 const int c = __popcll(__ballot(ok));
                 const int64_t nlo = lo + (int64_t)c * step;
                 const int64_t nhi = min(hi, lo + (int64_t)(c + 1) * step - 1);
@@ -146,212 +159,192 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                 hi = max(nhi, lo);
             }
             const int64_t pr = lo + lane;
-            const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, st_off[a], pr) <= tau0);
+            const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, off, pr) <= tau0);
             const int c = __popcll(__ballot(ok));
-            if (lane == 0) st_q[a] = lo + c;
+            if (lane == 0) {
+                const int64_t q = lo + c;
+                sm.st_q[a] = q;
+                sm.st_lastx[a] = (q > 0) ? endpoint_x(p.s, p.e, off, q - 1) : -INFINITY;
+            }
         }
     }
-    lds_barrier();
+    wave_sync();
 
-    // registers holding the next tile's samples of this lane (and window)
-    double nt[C + 1];
-    float nP[C + 1];
-    double ew[PER];
-    bool ew_ready = false;
-    unsigned err = 0u;
-
-    auto load_samples = [&](int64_t b) {
-        const int64_t j0 = b * T;
-        const int L = (int)min((int64_t)T, p.nseg - j0);
-        const int cs = min(max(L - tid * C, 0), C);
-        const int64_t g = j0 + (int64_t)tid * C - p.base;
-        if (cs == C && p.aligned16) {
-            const double2* t2 = reinterpret_cast<const double2*>(p.t + g);
-            const float4* P4 = reinterpret_cast<const float4*>(p.P + g);
-#pragma unroll
-            for (int u = 0; u < C / 2; ++u) {
-                const double2 v = t2[u];
-                nt[2 * u] = v.x;
-                nt[2 * u + 1] = v.y;
-            }
-#pragma unroll
-            for (int u = 0; u < C / 4; ++u) {
-                const float4 v = P4[u];
-                nP[4 * u] = v.x;
-                nP[4 * u + 1] = v.y;
-                nP[4 * u + 2] = v.z;
-                nP[4 * u + 3] = v.w;
-            }
-            nt[C] = p.t[g + C];
-            nP[C] = p.P[g + C];
-        } else {
-#pragma unroll
-            for (int u = 0; u <= C; ++u) {
-                if (u <= cs && cs > 0) {
-                    nt[u] = p.t[g + u];
-                    nP[u] = p.P[g + u];
-                } else {
-                    nt[u] = 0.0;
-                    nP[u] = 0.0f;
-                }
-            }
-        }
+    // window slot of the stream cursors (advanced by each stream's take: the
+    // next tile's window)
+    auto window_x = [&](int slot, bool advance) -> double {
+        if (slot >= nslot) return INFINITY;
+        const int a = slot >> lc, r = slot & (cap - 1);
+        const int64_t q = sm.st_q[a] + (advance ? sm.st_take[a] : 0) + r;
+        return (q < sm.st_len[a]) ? endpoint_x(p.s, p.e, sm.st_off[a], q) : INFINITY;
+    };
+    // breakpoint segments before segment j (the run sum ending at j-1 is R[rank(j)])
+    auto rank_of = [&](int j) -> int {
+        const int w = j >> 5;
+        return sm.wp[w] + __popc(sm.flag[w] & ((1u << (j & 31)) - 1u));
     };
 
-    load_samples(b0);
+    double ew[NV];  // prefetched window of the next tile
+    bool ew_ready = false;
+    unsigned err = 0u;
     double w_acc = 0.0, idle = 0.0;  // this lane's share of the trace and idle energy
 
     for (int64_t b = b0; b < b1; ++b) {
         const int64_t j0 = b * T;
         const int L = (int)min((int64_t)T, p.nseg - j0);
-        const int cs = min(max(L - tid * C, 0), C);  // segments of this lane
+        const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
 
-        // ---- samples: stage, segment energies, checks; then prefetch the next tile
-        double Sj[C];
-        double wsum = 0.0;
+        // ---- samples: load, stage, segment energies, checks
+        {
+            double tv[C + 1];
+            float pv[C + 1];
+            const int64_t g = j0 + (int64_t)lane * C - p.base;
+            if (cs == C && p.aligned16) {
+                const double2* t2 = reinterpret_cast<const double2*>(p.t + g);
+                const float4* P4 = reinterpret_cast<const float4*>(p.P + g);
 #pragma unroll
-        for (int u = 0; u <= C; ++u) {
-            sh_t[u][tid] = nt[u];
-            sh_P[u][tid] = nP[u];
-        }
-#pragma unroll
-        for (int u = 0; u < C; ++u) {
-            const double ta = nt[u], tb = nt[u + 1];
-            const float pa = nP[u], pb = nP[u + 1];
-            Sj[u] = 0.0;
-            if (u < cs) {
-                if (p.validate) {
-                    if (!(tb > ta) || !(fabs(ta) < INFINITY) || !(fabs(tb) < INFINITY))
-                        err |= ERR_TIMESTAMPS;
-                    if (!(pa >= 0.0f && pa < INFINITY) || !(pb >= 0.0f && pb < INFINITY))
-                        err |= ERR_POWER;
+                for (int u = 0; u < C / 2; ++u) {
+                    const double2 v = t2[u];
+                    tv[2 * u] = v.x;
+                    tv[2 * u + 1] = v.y;
                 }
-                Sj[u] = 0.5 * ((double)pa + (double)pb) * (tb - ta);
-                wsum += Sj[u];
+#pragma unroll
+                for (int u = 0; u < C / 4; ++u) {
+                    const float4 v = P4[u];
+                    pv[4 * u] = v.x;
+                    pv[4 * u + 1] = v.y;
+                    pv[4 * u + 2] = v.z;
+                    pv[4 * u + 3] = v.w;
+                }
+                tv[C] = p.t[g + C];
+                pv[C] = p.P[g + C];
+            } else {
+#pragma unroll
+                for (int u = 0; u <= C; ++u) {
+                    if (u <= cs && cs > 0) {
+                        tv[u] = p.t[g + u];
+                        pv[u] = p.P[g + u];
+                    } else {
+                        tv[u] = 0.0;
+                        pv[u] = 0.0f;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u <= C; ++u) {
+                sm.sh_t[u][lane] = tv[u];
+                sm.sh_P[u][lane] = pv[u];
+            }
+#pragma unroll
+            for (int u = 0; u < C; ++u) {
+                const double ta = tv[u], tb = tv[u + 1];
+                const float pa = pv[u], pb = pv[u + 1];
+                if (u < cs) {
+                    if (p.validate) {
+                        if (!(tb > ta) || !(fabs(ta) < INFINITY) || !(fabs(tb) < INFINITY))
+                            err |= ERR_TIMESTAMPS;
+                        if (!(pa >= 0.0f && pa < INFINITY) || !(pb >= 0.0f && pb < INFINITY))
+                            err |= ERR_POWER;
+                    }
+                    w_acc += 0.5 * ((double)pa + (double)pb) * (tb - ta);
+                }
             }
         }
-        if (cs > 0 && tid * C + cs == L) sh_tend = sh_t[cs][tid];
-        if (b + 1 < b1) load_samples(b + 1);  // in flight while this tile runs
-
-        if (tid < S) {
-            p.cnt[(int64_t)tid * (LD + 1) + b] = st_q[tid];
-            st_q0[tid] = st_q[tid];
-            st_acc[tid] = 0.0;
-            st_started[tid] = 0;
+        if (lane < S) {
+            p.cnt[(int64_t)lane * (LD + 1) + b] = sm.st_q[lane];
+            sm.st_acc[lane] = 0.0;
+            sm.st_started[lane] = 0;
         }
-        if (ew_ready) {
-#pragma unroll
-            for (int v = 0; v < PER; ++v) ev_x[tid + v * NTH] = ew[v];
-        }
-        w_acc += wsum;
-        lds_barrier();
-        const double tau_end = sh_tend;
-        const double t_begin = sh_t[0][0];
-        const double inv_dt = (double)L / (tau_end - t_begin);
-        double rs_x = t_begin;  // where the round's first gap starts
-        int rs_j = -1;          // its segment (-1: the tile's first sample)
+        wave_sync();
 
         // sample time / power of tile index j in [0, L]
         auto t_at = [&](int j) -> double {
             const int u = j & (C - 1), k = j / C;
-            return (u == 0 && k > 0) ? sh_t[C][k - 1] : sh_t[u][k];
+            return (u == 0 && k > 0) ? sm.sh_t[C][k - 1] : sm.sh_t[u][k];
         };
         auto P_at = [&](int j) -> double {
             const int u = j & (C - 1), k = j / C;
-            return (double)((u == 0 && k > 0) ? sh_P[C][k - 1] : sh_P[u][k]);
+            return (double)((u == 0 && k > 0) ? sm.sh_P[C][k - 1] : sm.sh_P[u][k]);
         };
-        auto rs_at = [&](int j) -> double { return sh_rs[j & (C - 1)][j / C]; };
 
-        for (int round = 0;; ++round) {
-            // ---- endpoint window of this round
-            if (!(round == 0 && ew_ready)) {
-                for (int idx = tid; idx < (S << lcap); idx += NTH) {
-                    const int a = idx >> lcap, r = idx & (cap - 1);
-                    const int64_t q = st_q[a] + r;
-                    ev_x[idx] = (q < st_len[a]) ? endpoint_x(p.s, p.e, st_off[a], q) : INFINITY;
-                }
-                lds_barrier();
+        const double t_begin = sm.sh_t[0][0];
+        const double tau_end = t_at(L);
+        const double inv_dt = (double)L / (tau_end - t_begin);
+        double rs_x = t_begin;  // where the round's first gap starts
+        int rs_j = -1;          // its segment (-1: the tile's first sample)
+
+        for (;;) {
+            // ---- endpoint window of this round: slot = stream * cap + rank
+            double xv[NV];
+            uint64_t in[NV];
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                xv[v] = ew_ready ? ew[v] : window_x(lane + WAVE * v, false);
+                sm.ev_x[lane + WAVE * v] = xv[v];
+                in[v] = __ballot(xv[v] <= tau_end);
             }
             ew_ready = false;
-            // endpoints of each stream inside this tile: the window is sorted, so
-            // their count is the length of its prefix
-            for (int idx = tid; idx < (S << lcap); idx += NTH) {
-                const bool in = ev_x[idx] <= tau_end;
-                if (cap >= 64) {  // the wave lies inside one stream's window
-                    const int c = __popcll(__ballot(in));
-                    if (lane == 0 && c) atomicAdd(&st_k[idx >> lcap], c);
-                } else if (in) {
-                    atomicAdd(&st_k[idx >> lcap], 1);
-                }
-            }
-            lds_barrier();
-            // every lane derives the round's shape from the counts
+            wave_sync();
+            // each stream's endpoints in the tile are a prefix of its (sorted)
+            // window; a full window limits the round to endpoints <= cut
+            auto count_in = [&](const uint64_t* m, int a) -> int {
+                int c = 0;
+#pragma unroll
+                for (int v = 0; v < NV; ++v)
+                    c += popc_range(m[v], 0ull, (a << lc) - WAVE * v, ((a + 1) << lc) - WAVE * v);
+                return c;
+            };
             double cut = INFINITY;
             bool fin = true;
-            for (int a = 0; a < S; ++a)
-                if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
+            for (int a = 0; a < S; ++a) {
+                if (count_in(in, a) == cap && sm.st_q[a] + cap < sm.st_len[a]) {
                     fin = false;
-                    cut = fmin(cut, ev_x[(a << lcap) + cap - 1]);
+                    cut = fmin(cut, sm.ev_x[(a << lc) + cap - 1]);
                 }
-            if (!fin) {
-                // a full window limits the round to endpoints <= cut (a time prefix)
-                for (int idx = tid; idx < (S << lcap); idx += NTH) {
-                    const int a = idx >> lcap, r = idx & (cap - 1);
-                    const bool in = r < st_k[a] && ev_x[idx] <= cut;
-                    if (cap >= 64) {
-                        const int c = __popcll(__ballot(in));
-                        if (lane == 0 && c) atomicAdd(&st_take[a], c);
-                    } else if (in) {
-                        atomicAdd(&st_take[a], 1);
-                    }
-                }
-                lds_barrier();
-                if (tid == 0) {
-                    int tot = 0;
-                    for (int a = 0; a < S; ++a) tot += st_take[a];
-                    if (tot == 0) {  // only with unsorted endpoints: force progress
-                        for (int a = 0; a < S; ++a)
-                            if (st_k[a] == cap && st_q[a] + cap < st_len[a]) {
-                                st_take[a] = 1;
-                                break;
-                            }
-                        sh_err |= ERR_INTERVAL;
-                    }
-                }
-                lds_barrier();
             }
-            const int* take = fin ? st_k : st_take;
+            uint64_t tk[NV];
+#pragma unroll
+            for (int v = 0; v < NV; ++v) tk[v] = fin ? in[v] : (in[v] & __ballot(xv[v] <= cut));
             int Er = 0, m0 = 0;
             for (int a = 0; a < S; ++a) {
-                Er += take[a];
-                m0 += (int)(st_q[a] & 1);
+                const int ta = count_in(tk, a);
+                if (lane == 0) sm.st_take[a] = ta;
+                Er += ta;
+                m0 += (int)(sm.st_q[a] & 1);
+            }
+            if (!fin && Er == 0) {
+                // only with unsorted endpoints: force progress, report
+                for (int a = 0; a < S; ++a) {
+                    if (count_in(in, a) == cap && sm.st_q[a] + cap < sm.st_len[a]) {
+                        if (lane == 0) sm.st_take[a] = 1;
+                        Er = 1;
+                        break;
+                    }
+                }
+                err |= ERR_INTERVAL;
             }
             // the round's start is a breakpoint too: runs restart after it
-            if (tid == 0 && rs_j >= 0) atomicOr(&sh_flag[rs_j >> 5], 1u << (rs_j & 31));
+            if (lane == 0 && rs_j >= 0) atomicOr(&sm.flag[rs_j >> 5], 1u << (rs_j & 31));
+            wave_sync();
 
-            // prefetch the next tile's endpoint window (its cursor is known now)
-            if (fin && round == 0 && b + 1 < b1) {
+            // prefetch the next tile's window (its cursors are known now)
+            if (fin && b + 1 < b1) {
 #pragma unroll
-                for (int v = 0; v < PER; ++v) {
-                    const int idx = tid + v * NTH;
-                    double x = INFINITY;
-                    if (idx < (S << lcap)) {
-                        const int a = idx >> lcap, r = idx & (cap - 1);
-                        const int64_t q = st_q[a] + take[a] + r;
-                        if (q < st_len[a]) x = endpoint_x(p.s, p.e, st_off[a], q);
-                    }
-                    ew[v] = x;
-                }
+                for (int v = 0; v < NV; ++v) ew[v] = window_x(lane + WAVE * v, true);
                 ew_ready = true;
             }
 
-            // ---- endpoints: segment, sample index, checks, merged position
-            for (int k = tid; k < Er; k += NTH) {
-                int a = 0, r = k;
-                while (a + 1 < S && r >= take[a]) r -= take[a++];
-                const int slot = (a << lcap) + r;
-                const double x = ev_x[slot];
-                const int64_t q = st_q[a] + r;
+            // ---- endpoints, part 1: segment, sample index, checks, breakpoint flag
+            int jv[NV];
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                jv[v] = -1;
+                const int slot = lane + WAVE * v;
+                const double x = xv[v];
+                if (slot >= nslot) continue;
+                const int a = slot >> lc, r = slot & (cap - 1);
+                if (r >= sm.st_take[a]) continue;
+                const int64_t q = sm.st_q[a] + r;
                 // segment j with t_j < x <= t_{j+1}: guess from the mean spacing, correct
                 int j = (int)fmin(fmax((x - t_begin) * inv_dt, 0.0), (double)(L - 1));
                 int steps = 0;
@@ -371,70 +364,57 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     }
                     j = min(max(lo, 1), L) - 1;
                 }
-                const int64_t gid = st_off[a] + (q >> 1);
+                jv[v] = j;
+                const int64_t gid = sm.st_off[a] + (q >> 1);
                 if (q & 1) {
                     if (p.end_idx) p.end_idx[gid] = j0 + j + 1;
                 } else {
                     if (p.start_idx) p.start_idx[gid] = j0 + j + 1;
                 }
                 if (p.validate) {
-                    bool bad = !(fabs(x) < INFINITY);
-                    if (q + 1 < st_len[a]) {
-                        const double xn = (r + 1 < cap) ? ev_x[slot + 1]
-                                                        : endpoint_x(p.s, p.e, st_off[a], q + 1);
-                        if (!(x <= xn)) bad = true;
-                    }
-                    if (bad) err |= ERR_INTERVAL;
+                    // finite and not before the stream's previous endpoint
+                    const double xp = (r > 0) ? sm.ev_x[slot - 1] : sm.st_lastx[a];
+                    if (!(fabs(x) < INFINITY) || !(xp <= x)) err |= ERR_INTERVAL;
                 }
-                // position in the time-merged order: endpoints of the other streams
-                // before x (ties: lower stream first).  Entries past a stream's take
-                // lie after x, so fixed-depth searches over the whole windows,
-                // interleaved across streams, give the counts.
-                int pos = r;
-                {
-                    int c[SMAX];
-#pragma unroll
-                    for (int a2 = 0; a2 < SMAX; ++a2) c[a2] = 0;
-                    for (int step = cap >> 1; step > 0; step >>= 1) {
-#pragma unroll
-                        for (int a2 = 0; a2 < SMAX; ++a2) {
-                            if (a2 < S && a2 != a) {
-                                const double y = ev_x[(a2 << lcap) + c[a2] + step - 1];
-                                if (a2 < a ? (y <= x) : (y < x)) c[a2] += step;
-                            }
-                        }
-                    }
-#pragma unroll
-                    for (int a2 = 0; a2 < SMAX; ++a2) {
-                        if (a2 < S && a2 != a) {
-                            const double y = ev_x[(a2 << lcap) + c[a2]];
-                            if (a2 < a ? (y <= x) : (y < x)) ++c[a2];
-                            pos += min(c[a2], take[a2]);
-                        }
-                    }
-                }
-                pos = min(pos, Er - 1);
-                ev_pos[slot] = pos;
-                mg_x[pos] = x;
-                mg_j[pos] = j | ((q & 1) ? (int)0x80000000 : 0);
-                atomicOr(&sh_flag[j >> 5], 1u << (j & 31));
+                atomicOr(&sm.flag[j >> 5], 1u << (j & 31));
             }
-            lds_barrier();
+            wave_sync();
+            // set flags in the words before each word (ranks of breakpoint segments)
+            if (lane < NWORD) {
+                int c = __popc(sm.flag[lane]);
+                for (int off = 1; off < NWORD; off <<= 1) {
+                    const int y = __shfl_up(c, off);
+                    if (lane >= off) c += y;
+                }
+                sm.wp[lane + 1] = c;
+                if (lane == 0) sm.wp[0] = 0;
+            }
+            wave_sync();
 
-            // ---- run sums: segmented scan of whole-segment energies, restarting
-            // after every segment that holds a breakpoint (its energy is cut into
-            // pieces at the breakpoints instead)
+            // ---- run sums: segmented scan of whole-segment energies (recomputed
+            // from the staged samples, bit for bit as above), restarting after
+            // every breakpoint segment (whose energy is cut into pieces at its
+            // breakpoints instead).  The run ending just before breakpoint
+            // segment j (or before the tile's last segment) is stored at rank(j).
             {
+                const int j0l = lane * C;
+                const uint32_t myflags = (sm.flag[j0l >> 5] >> (j0l & 31)) & ((1u << C) - 1u);
+                const uint32_t nextflags =
+                    (j0l + C < T) ? ((sm.flag[(j0l + C) >> 5] >> ((j0l + C) & 31)) & 1u) : 0u;
+                const bool prev_lane_last =
+                    lane > 0 && ((sm.flag[(j0l - 1) >> 5] >> ((j0l - 1) & 31)) & 1u);
                 double loc[C];
                 double run = 0.0;
                 bool reset = false;
 #pragma unroll
                 for (int u = 0; u < C; ++u) {
-                    const int j = tid * C + u;
-                    const bool prev_flag =
-                        j > 0 && ((sh_flag[(j - 1) >> 5] >> ((j - 1) & 31)) & 1u);
-                    const bool self_flag = (sh_flag[j >> 5] >> (j & 31)) & 1u;
-                    const double v = (self_flag || u >= cs) ? 0.0 : Sj[u];
+                    const bool prev_flag = (u == 0) ? prev_lane_last : ((myflags >> (u - 1)) & 1u);
+                    const bool self_flag = (myflags >> u) & 1u;
+                    const double v =
+                        (self_flag || u >= cs)
+                            ? 0.0
+                            : 0.5 * ((double)sm.sh_P[u][lane] + (double)sm.sh_P[u + 1][lane]) *
+                                  (sm.sh_t[u + 1][lane] - sm.sh_t[u][lane]);
                     if (prev_flag) {
                         run = v;
                         reset = true;
@@ -443,75 +423,102 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                     }
                     loc[u] = run;
                 }
-                // scan of the lanes' carries (reset flag, value)
                 int h = reset ? 1 : 0;
-                double x = run;
-                for (int off = 1; off < 64; off <<= 1) {
-                    const double xo = __shfl_up(x, off);
+                double xs = run;
+                for (int off = 1; off < WAVE; off <<= 1) {
+                    const double xo = __shfl_up(xs, off);
                     const int ho = __shfl_up(h, off);
                     if (lane >= off) {
-                        x = h ? x : xo + x;
+                        xs = h ? xs : xo + xs;
                         h |= ho;
                     }
                 }
-                if (lane == 63) {
-                    red[wave] = x;
-                    sh_wsum[wave] = h;
-                }
-                lds_barrier();
-                double px = 0.0;
-#pragma unroll
-                for (int w = 0; w < NW; ++w)
-                    if (w < wave) px = sh_wsum[w] ? red[w] : px + red[w];
-                const double incl = h ? x : px + x;
-                double cin = __shfl_up(incl, 1);
-                if (lane == 0) cin = px;
+                double cin = __shfl_up(xs, 1);
+                if (lane == 0) cin = 0.0;
                 bool seen = false;
+                const uint32_t fl = myflags | (nextflags << C);
 #pragma unroll
                 for (int u = 0; u < C; ++u) {
-                    const int j = tid * C + u;
-                    if (j > 0 && ((sh_flag[(j - 1) >> 5] >> ((j - 1) & 31)) & 1u)) seen = true;
-                    sh_rs[u][tid] = seen ? loc[u] : cin + loc[u];
+                    const bool prev_flag = (u == 0) ? prev_lane_last : ((myflags >> (u - 1)) & 1u);
+                    if (prev_flag) seen = true;
+                    const int k = j0l + u;  // this run value ends at segment k
+                    const bool nxt = ((fl >> (u + 1)) & 1u) != 0;
+                    if (k + 1 < L && (nxt || (k + 1 == L - 1)))
+                        sm.R[rank_of(k + 1)] = seen ? loc[u] : cin + loc[u];
                 }
             }
 
-            // ---- concurrency in each gap: m_g = m0 + sum of +-1 before endpoint g
+            // ---- endpoints, part 2: merged position and the intervals active after
             {
-                const int g0 = 2 * tid, g1 = 2 * tid + 1;
-                const int v0 = (g0 < Er) ? ((mg_j[g0] < 0) ? -1 : 1) : 0;
-                const int v1 = (g1 < Er) ? ((mg_j[g1] < 0) ? -1 : 1) : 0;
-                int s = v0 + v1;
-                for (int off = 1; off < 64; off <<= 1) {
-                    const int y = __shfl_up(s, off);
-                    if (lane >= off) s += y;
+                int take[SMAX];
+                int qpar[SMAX];
+#pragma unroll
+                for (int a2 = 0; a2 < SMAX; ++a2) {
+                    take[a2] = (a2 < S) ? sm.st_take[a2] : 0;
+                    qpar[a2] = (a2 < S) ? (int)(sm.st_q[a2] & 1) : 0;
                 }
-                lds_barrier();  // the carries' scratch above is free again
-                if (lane == 63) sh_wsum[wave] = s;
-                lds_barrier();
-                int wbase = 0;
-                for (int w = 0; w < wave; ++w) wbase += sh_wsum[w];
-                const int excl = wbase + s - (v0 + v1);
-                if (g0 < Er) mg_m[g0] = m0 + excl;
-                if (g1 < Er) mg_m[g1] = m0 + excl + v0;
-                if (tid == NTH - 1) mg_m[Er] = m0 + wbase + s;
+#pragma unroll
+                for (int v = 0; v < NV; ++v) {
+                    if (jv[v] < 0) continue;
+                    const int slot = lane + WAVE * v;
+                    const double x = xv[v];
+                    const int a = slot >> lc, r = slot & (cap - 1);
+                    const int q0 = (int)(sm.st_q[a] & 1);
+                    // endpoints of each other stream before x in the merged order
+                    // (ties: lower stream first); entries past a stream's take lie
+                    // after x, so fixed-depth searches of the whole window suffice
+                    int pos = r;
+                    int m_after = (q0 + r + 1) & 1;
+                    int c[SMAX];
+#pragma unroll
+                    for (int a2 = 0; a2 < SMAX; ++a2) c[a2] = 0;
+                    for (int step = cap >> 1; step > 0; step >>= 1) {
+#pragma unroll
+                        for (int a2 = 0; a2 < SMAX; ++a2) {
+                            if (a2 < S && a2 != a) {
+                                const double y = sm.ev_x[(a2 << lc) + c[a2] + step - 1];
+                                if (a2 < a ? (y <= x) : (y < x)) c[a2] += step;
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int a2 = 0; a2 < SMAX; ++a2) {
+                        if (a2 < S && a2 != a) {
+                            const double y = sm.ev_x[(a2 << lc) + c[a2]];
+                            if (a2 < a ? (y <= x) : (y < x)) ++c[a2];
+                            const int ca = min(c[a2], take[a2]);
+                            pos += ca;
+                            m_after += (qpar[a2] + ca) & 1;
+                        }
+                    }
+                    pos = min(pos, Er - 1);
+                    const int64_t q = sm.st_q[a] + r;
+                    sm.ev_pos[slot] = (uint8_t)pos;
+                    sm.mg_x[pos] = x;
+                    sm.mg_jm[pos] = (uint32_t)jv[v] | ((uint32_t)m_after << 16) |
+                                    ((q & 1) ? 0x80000000u : 0u);
+                }
             }
-            lds_barrier();
+            wave_sync();
 
             // ---- gap energies, split among the active intervals
             const int G = Er + (fin ? 1 : 0);
-            for (int g = tid; g < G; g += NTH) {
+            for (int g = lane; g < G; g += WAVE) {
                 double xs, xe;
-                int js, je;
+                int js, je, m;
                 if (g == 0) {
                     xs = rs_x;
                     js = rs_j;
+                    m = m0;
                 } else {
-                    xs = mg_x[g - 1];
-                    js = min(mg_j[g - 1] & 0x7fffffff, L - 1);
+                    const uint32_t w = sm.mg_jm[g - 1];
+                    xs = sm.mg_x[g - 1];
+                    js = min((int)(w & 0xffffu), L - 1);
+                    m = (int)((w >> 16) & 0x7fffu);
                 }
                 if (g < Er) {
-                    xe = mg_x[g];
-                    je = min(mg_j[g] & 0x7fffffff, L - 1);
+                    xe = sm.mg_x[g];
+                    je = min((int)(sm.mg_jm[g] & 0xffffu), L - 1);
                 } else {
                     xe = tau_end;
                     je = L - 1;
@@ -529,129 +536,156 @@ __global__ __launch_bounds__(NTH) void k_tile(const TileParams p)
                         const double pa = P_at(js), pb = P_at(js + 1);
                         Q += 0.5 * (lerp_power(ta, tb, pa, pb, xs) + pb) * (tb - xs);
                     }
-                    if (je > js + 1) Q += rs_at(je - 1);
+                    if (je > js + 1) Q += sm.R[rank_of(je)];
                     const double ta = t_at(je), tb = t_at(je + 1);
                     const double pa = P_at(je), pb = P_at(je + 1);
                     Q += 0.5 * (pa + lerp_power(ta, tb, pa, pb, xe)) * (xe - ta);
                 }
-                const int m = mg_m[g];
                 double v = 0.0;
                 if (m > 0)
                     v = p.split ? Q / (double)m : Q;
                 else
                     idle += Q;
-                gv[g] = v;
+                sm.gv[g] = v;
             }
-            lds_barrier();
+            wave_sync();
 
             // ---- interval energies: intervals starting in this round
-            for (int k = tid; k < Er; k += NTH) {
-                int a = 0, r = k;
-                while (a + 1 < S && r >= take[a]) r -= take[a++];
-                const int64_t q = st_q[a] + r;
+#pragma unroll
+            for (int v = 0; v < NV; ++v) {
+                if (jv[v] < 0) continue;
+                const int slot = lane + WAVE * v;
+                const int a = slot >> lc, r = slot & (cap - 1);
+                const int64_t q = sm.st_q[a] + r;
                 if (q & 1) continue;
-                const int slot = (a << lcap) + r;
-                const int ps = ev_pos[slot];
+                const int ta = sm.st_take[a];
+                const int ps = sm.ev_pos[slot];
                 double acc = 0.0;
-                if (r + 1 < take[a]) {
-                    const int pe = min(ev_pos[slot + 1], G - 1);
-                    for (int g = ps + 1; g <= pe; ++g) acc += gv[g];
-                    p.energy[st_off[a] + (q >> 1)] = acc;
+                if (r + 1 < ta) {
+                    const int pe = min((int)sm.ev_pos[slot + 1], G - 1);
+                    for (int g = ps + 1; g <= pe; ++g) acc += sm.gv[g];
+                    p.energy[sm.st_off[a] + (q >> 1)] = acc;
                 } else {
-                    for (int g = ps + 1; g < G; ++g) acc += gv[g];
-                    nx_acc[a] = acc;
-                    nx_started[a] = 1;
+                    for (int g = ps + 1; g < G; ++g) acc += sm.gv[g];
+                    sm.nx_acc[a] = acc;
+                    sm.nx_started[a] = 1;
                 }
             }
             // the interval each stream carried into this round
-            if (tid < S) {
-                const int a = tid;
-                const int ta = take[a];
-                const bool active = (st_q[a] & 1) != 0;
-                const bool ends_open = ((st_q[a] + ta) & 1) != 0;
+            if (lane < S) {
+                const int a = lane;
+                const int ta = sm.st_take[a];
+                const bool active = (sm.st_q[a] & 1) != 0;
+                const bool ends_open = ((sm.st_q[a] + ta) & 1) != 0;
                 if (active) {
                     double acc = 0.0;
                     if (ta > 0) {
-                        const int pe = min(ev_pos[a << lcap], G - 1);
-                        for (int g = 0; g <= pe; ++g) acc += gv[g];
-                        const double Et = st_acc[a] + acc;
-                        if (st_started[a])
-                            p.energy[st_off[a] + (st_q[a] >> 1)] = Et;
+                        const int pe = min((int)sm.ev_pos[a << lc], G - 1);
+                        for (int g = 0; g <= pe; ++g) acc += sm.gv[g];
+                        const double Et = sm.st_acc[a] + acc;
+                        if (sm.st_started[a])
+                            p.energy[sm.st_off[a] + (sm.st_q[a] >> 1)] = Et;
                         else
                             p.head[(int64_t)a * LD + b] = Et;
                         if (!ends_open) {
-                            nx_acc[a] = 0.0;
-                            nx_started[a] = 0;
+                            sm.nx_acc[a] = 0.0;
+                            sm.nx_started[a] = 0;
                         }
                     } else {
-                        for (int g = 0; g < G; ++g) acc += gv[g];
-                        nx_acc[a] = st_acc[a] + acc;
-                        nx_started[a] = st_started[a];
+                        for (int g = 0; g < G; ++g) acc += sm.gv[g];
+                        sm.nx_acc[a] = sm.st_acc[a] + acc;
+                        sm.nx_started[a] = sm.st_started[a];
                     }
                 } else if (!ends_open) {
-                    nx_acc[a] = 0.0;
-                    nx_started[a] = 0;
+                    sm.nx_acc[a] = 0.0;
+                    sm.nx_started[a] = 0;
                 }
             }
-            // clear the breakpoint flags for the next round
-            for (int w = tid; w < T / 32; w += NTH) sh_flag[w] = 0u;
-            lds_barrier();
-            if (tid < S) {
-                st_q[tid] += take[tid];
-                st_acc[tid] = nx_acc[tid];
-                st_started[tid] = nx_started[tid];
-            }
-            lds_barrier();
-            if (tid < S) {
-                st_k[tid] = 0;
-                st_take[tid] = 0;
-            }
             if (Er > 0) {
-                rs_x = mg_x[Er - 1];
-                rs_j = min(mg_j[Er - 1] & 0x7fffffff, L - 1);
+                rs_x = sm.mg_x[Er - 1];
+                rs_j = min((int)(sm.mg_jm[Er - 1] & 0xffffu), L - 1);
             }
+            wave_sync();
+            // commit the round; clear the breakpoint flags
+            if (lane < S) {
+                const int ta = sm.st_take[lane];
+                if (ta > 0) sm.st_lastx[lane] = sm.ev_x[(lane << lc) + ta - 1];
+                sm.st_q[lane] += ta;
+                sm.st_acc[lane] = sm.nx_acc[lane];
+                sm.st_started[lane] = sm.nx_started[lane];
+            }
+            if (lane < NWORD) sm.flag[lane] = 0u;
+            wave_sync();
             if (fin) break;
         }
 
         // ---- interval still open at the tile's end: its piece of this tile
-        if (tid < S && (st_q[tid] & 1)) {
-            if (st_started[tid])
-                p.tail[(int64_t)tid * LD + b] = st_acc[tid];
+        if (lane < S && (sm.st_q[lane] & 1)) {
+            if (sm.st_started[lane])
+                p.tail[(int64_t)lane * LD + b] = sm.st_acc[lane];
             else
-                p.head[(int64_t)tid * LD + b] = st_acc[tid];
+                p.head[(int64_t)lane * LD + b] = sm.st_acc[lane];
         }
+        wave_sync();
     }
 
-    // the workgroup's trace and idle energy, kept at its first tile (others 0)
-    const double Wt = block_sum_fixed<NTH>(w_acc, red);
-    const double It = block_sum_fixed<NTH>(idle, red);
-    for (int64_t b = b0 + tid; b < b1; b += NTH) {
+    // the wave's trace and idle energy, kept at its first tile (others 0)
+    const double Wt = wave_sum(w_acc);
+    const double It = wave_sum(idle);
+    for (int64_t b = b0 + lane; b < b1; b += WAVE) {
         p.tileW[b] = (b == b0) ? Wt : 0.0;
         p.tileIdle[b] = (b == b0) ? It : 0.0;
     }
-
-    if (tid < S) {
-        // where this workgroup stopped: the next workgroup must start there
-        p.cnt_fin[(int64_t)tid * (LD + 1) + b1] = st_q[tid];
-        if (b1 == NT) p.cnt[(int64_t)tid * (LD + 1) + NT] = st_q[tid];
+    if (lane < S) {
+        // where this wave stopped: the next wave must start there
+        p.cnt_fin[(int64_t)lane * (LD + 1) + b1] = sm.st_q[lane];
+        if (b1 == NT) p.cnt[(int64_t)lane * (LD + 1) + NT] = sm.st_q[lane];
     }
-    if (err) atomicOr(&sh_err, err);
-    lds_barrier();
-    if (tid == 0 && sh_err) atomicOr(&p.status->err, sh_err);
+    if (__ballot(err != 0u)) {
+        unsigned e = err;
+        for (int off = 32; off > 0; off >>= 1) e |= __shfl_xor(e, off);
+        if (lane == 0) atomicOr(&p.status->err, e);
+    }
 }
 
-hipError_t launch_tile(const TileParams& p, int grid, hipStream_t stream)
+namespace {
+
+constexpr int TILE_WPB = 4;  // independent waves per workgroup
+constexpr int TILE_NV = ROUND_EVENTS / WAVE;
+
+template <int SMAX>
+hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream)
 {
-    if (p.ss.S == 1)
-        hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD, 1>), dim3(grid),
-                           dim3(TILE_THREADS), 0, stream, p);
-    else if (p.ss.S <= 4)
-        hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD, 4>), dim3(grid),
-                           dim3(TILE_THREADS), 0, stream, p);
-    else
-        hipLaunchKernelGGL((k_tile<TILE_THREADS, SEG_PER_THREAD, MAX_STREAMS>), dim3(grid),
-                           dim3(TILE_THREADS), 0, stream, p);
+    using K = decltype(&k_tile<SEG_PER_THREAD, TILE_NV, SMAX, TILE_WPB>);
+    const K kern = k_tile<SEG_PER_THREAD, TILE_NV, SMAX, TILE_WPB>;
+    // persistent waves: as many as can be resident at once, each over a
+    // contiguous run of tiles
+    static int per_cu = 0;
+    if (per_cu == 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, WAVE * TILE_WPB, 0) !=
+                hipSuccess ||
+            nb <= 0)
+            nb = 2;
+        per_cu = nb;
+    }
+    const int64_t waves = (int64_t)device_cu_count() * per_cu * TILE_WPB;
+    p.tiles_per_wg = (ntiles + waves - 1) / waves;
+    const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
+    const int grid = (int)((runs + TILE_WPB - 1) / TILE_WPB);
+    hipLaunchKernelGGL(kern, dim3(grid), dim3(WAVE * TILE_WPB), 0, stream, p);
     return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_tile(const TileParams& p, hipStream_t stream)
+{
+    const int64_t ntiles = p.tile_end - p.tile_begin;
+    if (ntiles <= 0) return hipSuccess;
+    if (p.ss.S == 1) return launch_tile_t<1>(p, ntiles, stream);
+    if (p.ss.S <= 4) return launch_tile_t<4>(p, ntiles, stream);
+    return launch_tile_t<MAX_STREAMS>(p, ntiles, stream);
 }
 
 }  // namespace mag

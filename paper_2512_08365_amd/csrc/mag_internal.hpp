@@ -11,15 +11,13 @@ namespace mag {
 
 // ---------------------------------------------------------------- tiling
 // A tile is TILE consecutive sample segments [t_j, t_{j+1}] (TILE + 1 samples,
-// the last one shared with the next tile).  TILE_THREADS threads each own
-// SEG_PER_THREAD consecutive segments.  Interval endpoints that fall inside a
-// tile are processed in rounds of at most ROUND_EVENTS endpoints.
-constexpr int TILE = 2048;
-constexpr int TILE_THREADS = 256;
-constexpr int SEG_PER_THREAD = TILE / TILE_THREADS;  // 8
-constexpr int ROUND_EVENTS = 512;
+// the last one shared with the next tile), processed by one 64-lane wave whose
+// lanes each own SEG_PER_THREAD consecutive segments.  Interval endpoints
+// inside a tile are processed in rounds of at most ROUND_EVENTS endpoints.
+constexpr int SEG_PER_THREAD = 8;
+constexpr int TILE = 64 * SEG_PER_THREAD;  // 512
+constexpr int ROUND_EVENTS = 64;
 constexpr int MAX_STREAMS = MAG_MAX_STREAMS;
-constexpr int TILE_WGS_PER_CU = 2;  // resident tile workgroups per CU (LDS-limited)
 
 // group-by
 constexpr int AGG_THREADS = 256;
@@ -69,7 +67,7 @@ struct TileParams {
     int64_t n_total;    // samples of the whole trace
     int64_t tile_begin; // global tile range of this launch
     int64_t tile_end;
-    int64_t tiles_per_wg;
+    int64_t tiles_per_wg; // set by launch_tile
     int64_t NT;         // tiles of the whole trace (any larger value when not yet known)
     int64_t ld;         // row stride of cnt/cnt_fin (ld + 1) and head/tail (ld), ld >= tiles
     const double* s;
@@ -172,7 +170,8 @@ __device__ __forceinline__ void lds_barrier()
 hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double* t, int64_t n,
                        hipStream_t stream);
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
-hipError_t launch_tile(const TileParams& p, int grid, hipStream_t stream);
+// tiles [p.tile_begin, p.tile_end) on persistent waves (sets the launch shape)
+hipError_t launch_tile(const TileParams& p, hipStream_t stream);
 hipError_t launch_cross(const FixParams& p, hipStream_t stream);
 hipError_t launch_outside(const FixParams& p, hipStream_t stream);
 hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, Status* st,

@@ -10,7 +10,7 @@ from gpu_util import assert_energy_close, log, run_oracle, to_gpu
 
 pytestmark = pytest.mark.gpu
 
-TILE = 2048  # samples per tile of the library (segments); boundaries are probed around it
+TILE = 512  # segments per tile of the library; chunk boundaries are probed around it
 
 
 @pytest.fixture(scope="module", autouse=True)
