@@ -67,6 +67,7 @@ struct AttrWorkspace {
     double* tail;
     double* tileW;
     double* tileIdle;
+    double* tsum;  // per-slice partial totals of tileW / tileIdle
     double* energy;
     unsigned long long* table;
     uint32_t* slot;
@@ -102,6 +103,7 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
     w.tail = c.take<double>((size_t)pl.S * pl.NT);
     w.tileW = c.take<double>((size_t)pl.NT);
     w.tileIdle = c.take<double>((size_t)pl.NT);
+    w.tsum = c.take<double>(2 * (size_t)((pl.NT + mag::SUM_SLICE - 1) / mag::SUM_SLICE) + 2);
     w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
     if (pl.staging) {
         w.stage_t = c.take<double>((size_t)mag::TILE + 1);
@@ -329,7 +331,7 @@ struct Job {
         hipError_t e2;
         if ((e2 = mag::launch_cross(fp, stream)) != hipSuccess) return e2;
         if ((e2 = mag::launch_outside(fp, stream)) != hipSuccess) return e2;
-        return mag::launch_summary(w.tileW, w.tileIdle, NT, w.status, stream);
+        return mag::launch_summary(w.tileW, w.tileIdle, NT, w.tsum, w.status, stream);
     }
 
     hipError_t grouping(uint64_t* keys_out, mag_key_stats* per_key)
@@ -839,11 +841,12 @@ int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_
     if (n_keys_a < 0 || n_keys_b < 0 || k < 0) return fail(MAG_E_SIZE, "negative size");
     Carver c;
     c.take<mag::Status>(1);
-    const size_t na = (size_t)std::max<int64_t>(n_keys_a, 1);
-    c.take<double>(na);
-    c.take<uint64_t>(na);
-    c.take<int32_t>(na);
-    c.take<int32_t>(na);
+    const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(n_keys_a, k), 1);
+    c.take<double>(nc);
+    c.take<uint64_t>(nc);
+    c.take<int32_t>(nc);
+    c.take<int32_t>(nc);
+    c.take<uint32_t>(nc);
     *bytes = c.off;
     return MAG_OK;
 }
@@ -873,13 +876,14 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
 
     Carver c;
     c.base = static_cast<char*>(workspace);
-    const size_t nas = (size_t)std::max<int64_t>(na, 1);
+    const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(na, k), 1);
     mag::DiffParams p{};
     p.status = c.take<mag::Status>(1);
-    p.cand_r = c.take<double>(nas);
-    p.cand_key = c.take<uint64_t>(nas);
-    p.cand_ia = c.take<int32_t>(nas);
-    p.cand_ib = c.take<int32_t>(nas);
+    p.cand_r = c.take<double>(nc);
+    p.cand_key = c.take<uint64_t>(nc);
+    p.cand_ia = c.take<int32_t>(nc);
+    p.cand_ib = c.take<int32_t>(nc);
+    p.cand_rank = c.take<uint32_t>(nc);
     p.ka = keysA;
     p.sa = statsA->sum;
     p.ca = statsA->count;

@@ -118,14 +118,16 @@ __global__ __launch_bounds__(256) void k_init(Status* st, int64_t* cnt_fin, int6
     }
 }
 
-// whole-trace and idle energy: fixed-order reduction of the per-tile sums
-__global__ __launch_bounds__(1024) void k_summary(const double* tileW, const double* tileIdle,
-                                                   int64_t NT, Status* st)
+// whole-trace and idle energy: fixed-order reduction of the per-tile sums,
+// first over slices of SUM_SLICE tiles (one workgroup each), then over slices
+__global__ __launch_bounds__(1024) void k_summary_part(const double* tileW, const double* tileIdle,
+                                                        int64_t NT, double* part)
 {
     __shared__ double red[2][16];
     const int tid = threadIdx.x;
+    const int64_t lo = (int64_t)blockIdx.x * SUM_SLICE, hi = min(lo + SUM_SLICE, NT);
     double w = 0.0, z = 0.0;
-    for (int64_t b = tid; b < NT; b += 1024) {
+    for (int64_t b = lo + tid; b < hi; b += 1024) {
         w += tileW[b];
         z += tileIdle[b];
     }
@@ -143,6 +145,19 @@ __global__ __launch_bounds__(1024) void k_summary(const double* tileW, const dou
         for (int u = 0; u < 16; ++u) {
             W += red[0][u];
             I += red[1][u];
+        }
+        part[2 * blockIdx.x] = W;
+        part[2 * blockIdx.x + 1] = I;
+    }
+}
+
+__global__ __launch_bounds__(64) void k_summary_final(const double* part, int64_t nparts, Status* st)
+{
+    if (threadIdx.x == 0) {
+        double W = 0.0, I = 0.0;
+        for (int64_t k = 0; k < nparts; ++k) {
+            W += part[2 * k];
+            I += part[2 * k + 1];
         }
         st->trace_energy = W;
         st->idle_energy = I;
@@ -196,10 +211,14 @@ hipError_t launch_outside(const FixParams& p, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, Status* st,
-                          hipStream_t stream)
+hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, double* part,
+                          Status* st, hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_summary, dim3(1), dim3(1024), 0, stream, tileW, tileIdle, NT, st);
+    const int64_t nparts = (NT + SUM_SLICE - 1) / SUM_SLICE;
+    if (nparts > 0)
+        hipLaunchKernelGGL(k_summary_part, dim3((unsigned)nparts), dim3(1024), 0, stream, tileW,
+                           tileIdle, NT, part);
+    hipLaunchKernelGGL(k_summary_final, dim3(1), dim3(64), 0, stream, part, nparts, st);
     return hipGetLastError();
 }
 

@@ -1,18 +1,25 @@
 // diff.hip -- join two per-key energy tables and rank the keys by
 // r = (E_B - E_A) / E_A, descending, ties by ascending key.
 //
-// Stage 1 (k_diff_join): each workgroup takes 256 consecutive rows of table A,
-// finds each key in table B by binary search (both tables are ascending), and
-// ranks its joined rows inside the workgroup; only rows whose local rank is
-// below k can be in the global top k, so only those become candidates.
+// Stage 1 (k_diff_join): each workgroup takes 256 consecutive rows of table A.
+// Both tables are ascending, so those rows can only match a contiguous range of
+// table B; one wave finds the range (64-ary search), the workgroup stages it in
+// LDS and every row finds its partner there.  Joined rows are ranked inside
+// the workgroup; only rows whose local rank is below k can be in the global
+// top k, so only those become candidates.
 // Stage 2 (k_diff_rank): every candidate's global rank is the number of
-// candidates ordered before it; ranks below k are written out.
+// candidates ordered before it, counted in 256-candidate slices by many small
+// workgroups; ranks below k are written out (k_diff_write).
 
 #include "mag_internal.hpp"
 
 namespace mag {
 
 namespace {
+
+constexpr int JOIN_ROWS = 256;
+constexpr int B_TILE = 2048;  // B keys staged per join workgroup
+constexpr int RANK_SLICE = 256;
 
 __device__ __forceinline__ double rel_diff(double ea, double eb)
 {
@@ -24,6 +31,29 @@ __device__ __forceinline__ double rel_diff(double ea, double eb)
 __device__ __forceinline__ bool before(double rq, uint64_t kq, double rp, uint64_t kp)
 {
     return rq > rp || (rq == rp && kq < kp);
+}
+
+// entries of the ascending array a[0, n) below v (or at most v), found by the
+// 64 lanes of one wave together: a 64-ary search, a few dependent loads
+__device__ int64_t wave_count_below(const uint64_t* a, int64_t n, uint64_t v, bool inclusive)
+{
+    const int lane = threadIdx.x & 63;
+    int64_t lo = 0, hi = n;
+    while (hi - lo > 64) {
+        const int64_t step = (hi - lo + 63) / 64;
+        const int64_t pr = lo + (int64_t)(lane + 1) * step - 1;
+        bool ok = false;
+        if (pr < hi) ok = inclusive ? (a[pr] <= v) : (a[pr] < v);
+        const int c = __popcll(__ballot(ok));
+        const int64_t nlo = lo + (int64_t)c * step;
+        const int64_t nhi = min(hi, lo + (int64_t)(c + 1) * step - 1);
+        lo = min(nlo, hi);
+        hi = max(nhi, lo);
+    }
+    const int64_t pr = lo + lane;
+    bool ok = false;
+    if (pr < hi) ok = inclusive ? (a[pr] <= v) : (a[pr] < v);
+    return lo + __popcll(__ballot(ok));
 }
 
 }  // namespace
@@ -39,85 +69,131 @@ __global__ __launch_bounds__(256) void k_diff_check(const DiffParams p)
     if (bad) atomicOr(&p.status->err, ERR_KEYS);
 }
 
-__global__ __launch_bounds__(256) void k_diff_join(const DiffParams p)
+__global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
 {
-    __shared__ double lr[256];
-    __shared__ uint64_t lk[256];
-    __shared__ int lv[256];
+    __shared__ uint64_t bk[B_TILE];
+    __shared__ double lr[JOIN_ROWS];
+    __shared__ uint64_t lk[JOIN_ROWS];
+    __shared__ int lv[JOIN_ROWS];
+    __shared__ int64_t sh_range[2];
     const int tid = threadIdx.x;
-    const int64_t row = (int64_t)blockIdx.x * 256 + tid;
+    const int64_t row0 = (int64_t)blockIdx.x * JOIN_ROWS;
+    const int64_t rows = min((int64_t)JOIN_ROWS, p.na - row0);
+    if (tid < 64) {
+        // B rows that can match: keys in [A[row0], A[row0 + rows - 1]]
+        const int64_t lo = wave_count_below(p.kb, p.nb, p.ka[row0], false);
+        const int64_t hi = wave_count_below(p.kb, p.nb, p.ka[row0 + rows - 1], true);
+        if (tid == 0) {
+            sh_range[0] = lo;
+            sh_range[1] = max(hi, lo);
+        }
+    }
+    __syncthreads();
+    const int64_t blo = sh_range[0], bn = sh_range[1] - sh_range[0];
+    const bool staged = bn <= B_TILE;
+    if (staged)
+        for (int64_t v = tid; v < bn; v += JOIN_ROWS) bk[v] = p.kb[blo + v];
+    __syncthreads();
+
     double r = 0.0;
     uint64_t key = 0;
     int valid = 0;
     int64_t ib = -1;
-    if (row < p.na) {
+    if (tid < rows) {
+        const int64_t row = row0 + tid;
         key = p.ka[row];
-        int64_t lo = 0, hi = p.nb;
+        int64_t lo = 0, hi = bn;
         while (lo < hi) {
             const int64_t mid = (lo + hi) >> 1;
-            if (p.kb[mid] < key) lo = mid + 1; else hi = mid;
+            const uint64_t y = staged ? bk[mid] : p.kb[blo + mid];
+            if (y < key) lo = mid + 1; else hi = mid;
         }
-        if (lo < p.nb && p.kb[lo] == key) {
+        if (lo < bn && (staged ? bk[lo] : p.kb[blo + lo]) == key) {
             valid = 1;
-            ib = lo;
-            r = rel_diff(p.sa[row], p.sb[lo]);
+            ib = blo + lo;
+            r = rel_diff(p.sa[row], p.sb[ib]);
         }
     }
     lr[tid] = r;
     lk[tid] = key;
     lv[tid] = valid;
     __syncthreads();
+    bool cand = false;
     if (valid) {
         int64_t rank = 0;
 #pragma unroll 16
-        for (int q = 0; q < 256; ++q)
+        for (int q = 0; q < JOIN_ROWS; ++q)
             if (lv[q] && before(lr[q], lk[q], r, key)) ++rank;
-        if (rank < p.k) {
-            const uint32_t c = atomicAdd(&p.status->n_cand, 1u);
-            p.cand_r[c] = r;
-            p.cand_key[c] = key;
-            p.cand_ia[c] = (int32_t)row;
-            p.cand_ib[c] = (int32_t)ib;
-        }
+        cand = rank < p.k;
     }
+    // one counter update per wave: candidates take consecutive slots
+    const int lane = tid & 63;
+    const uint64_t cb = __ballot(cand);
     const unsigned long long nvalid = __popcll(__ballot(valid != 0));
-    if ((tid & 63) == 0 && nvalid) atomicAdd(&p.status->n_join, (uint32_t)nvalid);
+    uint32_t base = 0u;
+    if (lane == 0) {
+        if (cb) base = atomicAdd(&p.status->n_cand, (uint32_t)__popcll(cb));
+        if (nvalid) atomicAdd(&p.status->n_join, (uint32_t)nvalid);
+    }
+    base = __shfl(base, 0);
+    if (cand) {
+        const uint32_t c = base + (uint32_t)__popcll(cb & ((1ull << lane) - 1ull));
+        p.cand_r[c] = r;
+        p.cand_key[c] = key;
+        p.cand_ia[c] = (int32_t)(row0 + tid);
+        p.cand_ib[c] = (int32_t)ib;
+        p.cand_rank[c] = 0u;
+    }
 }
 
-__global__ __launch_bounds__(256) void k_diff_rank(const DiffParams p)
+// candidates [64 bx, 64 bx + 64) counted against the slice [256 by, 256 by + 256)
+__global__ __launch_bounds__(64) void k_diff_rank(const DiffParams p)
 {
-    __shared__ double tr[1024];
-    __shared__ uint64_t tk[1024];
+    __shared__ double tr[RANK_SLICE];
+    __shared__ uint64_t tk[RANK_SLICE];
+    const uint32_t nc = p.status->n_cand;
+    const uint32_t c0 = blockIdx.x * 64u, s0 = blockIdx.y * (uint32_t)RANK_SLICE;
+    if (c0 >= nc || s0 >= nc) return;  // uniform
+    const uint32_t cnt = min((uint32_t)RANK_SLICE, nc - s0);
+    for (uint32_t v = threadIdx.x; v < cnt; v += 64) {
+        tr[v] = p.cand_r[s0 + v];
+        tk[v] = p.cand_key[s0 + v];
+    }
+    __syncthreads();
+    const uint32_t c = c0 + threadIdx.x;
+    if (c >= nc) return;
+    const double r = p.cand_r[c];
+    const uint64_t key = p.cand_key[c];
+    uint32_t rank = 0;
+    uint32_t v = 0;
+    for (; v + 8 <= cnt; v += 8) {
+#pragma unroll
+        for (int w = 0; w < 8; ++w) rank += before(tr[v + w], tk[v + w], r, key) ? 1u : 0u;
+    }
+    for (; v < cnt; ++v) rank += before(tr[v], tk[v], r, key) ? 1u : 0u;
+    if (rank) atomicAdd(&p.cand_rank[c], rank);
+}
+
+__global__ __launch_bounds__(256) void k_diff_write(const DiffParams p)
+{
     const uint32_t nc = p.status->n_cand;
     const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (blockIdx.x * blockDim.x >= nc) return;  // uniform
-    const double r = (c < nc) ? p.cand_r[c] : 0.0;
-    const uint64_t key = (c < nc) ? p.cand_key[c] : 0ull;
-    int64_t rank = 0;
-    for (uint32_t base = 0; base < nc; base += 1024) {
-        const uint32_t cnt = min(1024u, nc - base);
-        __syncthreads();
-        for (uint32_t v = threadIdx.x; v < cnt; v += blockDim.x) {
-            tr[v] = p.cand_r[base + v];
-            tk[v] = p.cand_key[base + v];
-        }
-        __syncthreads();
-        uint32_t v = 0;
-        for (; v + 16 <= cnt; v += 16) {
-#pragma unroll
-            for (int w = 0; w < 16; ++w) rank += before(tr[v + w], tk[v + w], r, key) ? 1 : 0;
-        }
-        for (; v < cnt; ++v) rank += before(tr[v], tk[v], r, key) ? 1 : 0;
-    }
-    if (c < nc && rank < p.k) {
-        const int32_t ia = p.cand_ia[c], ib = p.cand_ib[c];
-        p.out_key[rank] = key;
-        p.out_ratio[rank] = r;
-        p.out_ea[rank] = p.sa[ia];
-        p.out_eb[rank] = p.sb[ib];
-        p.out_ca[rank] = p.ca[ia];
-        p.out_cb[rank] = p.cb[ib];
-    }
+    if (c >= nc) return;
+    const uint32_t rank = p.cand_rank[c];
+    if ((int64_t)rank >= p.k) return;
+    const int32_t ia = p.cand_ia[c], ib = p.cand_ib[c];
+    p.out_key[rank] = p.cand_key[c];
+    p.out_ratio[rank] = p.cand_r[c];
+    p.out_ea[rank] = p.sa[ia];
+    p.out_eb[rank] = p.sb[ib];
+    p.out_ca[rank] = p.ca[ia];
+    p.out_cb[rank] = p.cb[ib];
+}
+
+int64_t diff_max_candidates(int64_t na, int64_t k)
+{
+    const int64_t groups = (na + JOIN_ROWS - 1) / JOIN_ROWS;
+    return min(na, groups * min(k, (int64_t)JOIN_ROWS));
 }
 
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream)
@@ -126,9 +202,15 @@ hipError_t launch_diff(const DiffParams& p, hipStream_t stream)
     const unsigned cb = (unsigned)max((int64_t)1, min((mx + 255) / 256, (int64_t)1024));
     hipLaunchKernelGGL(k_diff_check, dim3(cb), dim3(256), 0, stream, p);
     if (p.na > 0 && p.nb > 0) {
-        const unsigned jb = (unsigned)((p.na + 255) / 256);
-        hipLaunchKernelGGL(k_diff_join, dim3(jb), dim3(256), 0, stream, p);
-        if (p.k > 0) hipLaunchKernelGGL(k_diff_rank, dim3(jb), dim3(256), 0, stream, p);
+        const unsigned jb = (unsigned)((p.na + JOIN_ROWS - 1) / JOIN_ROWS);
+        hipLaunchKernelGGL(k_diff_join, dim3(jb), dim3(JOIN_ROWS), 0, stream, p);
+        const int64_t mc = diff_max_candidates(p.na, p.k);
+        if (p.k > 0 && mc > 0) {
+            const dim3 rg((unsigned)((mc + 63) / 64), (unsigned)((mc + RANK_SLICE - 1) / RANK_SLICE));
+            hipLaunchKernelGGL(k_diff_rank, rg, dim3(64), 0, stream, p);
+            hipLaunchKernelGGL(k_diff_write, dim3((unsigned)((mc + 255) / 256)), dim3(256), 0,
+                               stream, p);
+        }
     }
     return hipGetLastError();
 }

@@ -48,19 +48,26 @@ __global__ __launch_bounds__(256) void k_table_fill(unsigned long long* table, u
 // compare-and-swap per workgroup instead of one per interval.
 constexpr int INS_CHUNK = 4096;
 constexpr int INS_SLOTS = 8192;
-constexpr int INS_GROUPS = 256;
+constexpr int INS_GROUPS = 64;  // the lookup pass inserts keys first seen later
 
 __device__ __forceinline__ void global_insert(const GroupParams& p, unsigned long long k)
 {
     const uint32_t mask = p.H - 1u;
     uint32_t h = (uint32_t)fmix64(k) & mask;
     for (uint32_t probe = 0; probe < p.H; ++probe) {
-        const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
-        if (old == EMPTY_KEY) {
-            atomicAdd(&p.status->n_inserted, 1u);
-            return;
+        // a plain load first: before this launch every slot was empty, and a slot
+        // only changes from empty to its final key, so a non-empty value read here
+        // is final; an empty one may be stale and is settled by the swap
+        const unsigned long long cur = p.table[h];
+        if (cur == k) return;
+        if (cur == EMPTY_KEY) {
+            const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
+            if (old == EMPTY_KEY) {
+                atomicAdd(&p.status->n_inserted, 1u);
+                return;
+            }
+            if (old == k) return;
         }
-        if (old == k) return;
         h = (h + 1u) & mask;
     }
     atomicOr(&p.status->overflow, 1u);
@@ -139,18 +146,25 @@ __global__ __launch_bounds__(256) void k_keymap(const GroupParams p)
 // list the occupied slots (order irrelevant: ranks come from key comparisons)
 __global__ __launch_bounds__(256) void k_compact(const GroupParams p)
 {
-    for (uint32_t h = blockIdx.x * blockDim.x + threadIdx.x; h <= p.H; h += gridDim.x * blockDim.x) {
-        unsigned long long k;
-        bool occ;
+    const int lane = threadIdx.x & 63;
+    // whole waves iterate together (the ballot below needs every lane)
+    const uint32_t span = ((p.H + 1u + 63u) / 64u) * 64u;
+    for (uint32_t h = blockIdx.x * blockDim.x + threadIdx.x; h < span; h += gridDim.x * blockDim.x) {
+        unsigned long long k = EMPTY_KEY;
+        bool occ = false;
         if (h < p.H) {
             k = p.table[h];
             occ = (k != EMPTY_KEY);
-        } else {
-            k = EMPTY_KEY;
+        } else if (h == p.H) {
             occ = p.status->special != 0u;
         }
+        // one counter update per wave: occupied slots take consecutive rows
+        const uint64_t ob = __ballot(occ);
+        uint32_t base = 0u;
+        if (lane == 0 && ob) base = atomicAdd(&p.status->n_unique, (uint32_t)__popcll(ob));
+        base = __shfl(base, 0);
         if (occ) {
-            const uint32_t u = atomicAdd(&p.status->n_unique, 1u);
+            const uint32_t u = base + (uint32_t)__popcll(ob & ((1ull << lane) - 1ull));
             p.ukey[u] = k;
             p.uslot[u] = h;
         }
@@ -234,29 +248,37 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
     }
 }
 
-// 4 threads per key each add a quarter of the chunk rows; quarters combined in order
-__global__ __launch_bounds__(256) void k_fin_sum(const GroupParams p)
+// per key, the chunk rows are added in FIN_GROUPS interleaved groups (each in
+// chunk order), and the groups are combined in order: a fixed summation order
+constexpr int FIN_KEYS = 64;
+constexpr int FIN_GROUPS = 16;
+
+__global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupParams p)
 {
-    __shared__ uint64_t qc[4][64];
-    __shared__ double qs[4][64];
+    __shared__ uint64_t qc[FIN_GROUPS][FIN_KEYS];
+    __shared__ double qs[FIN_GROUPS][FIN_KEYS];
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
-    const int kl = threadIdx.x & 63, qtr = threadIdx.x >> 6;
-    const int64_t id = (int64_t)blockIdx.x * 64 + kl;
-    if ((int64_t)blockIdx.x * 64 >= nk) return;  // uniform
+    const int kl = threadIdx.x % FIN_KEYS, grp = threadIdx.x / FIN_KEYS;
+    const int64_t id = (int64_t)blockIdx.x * FIN_KEYS + kl;
+    if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     uint64_t cnt = 0;
     double sum = 0.0;
     if (id < nk) {
-        for (int c = qtr; c < p.nchunks; c += 4) {
+        for (int c = grp; c < p.nchunks; c += FIN_GROUPS) {
             cnt += p.pcnt[(int64_t)c * p.cap + id];
             sum += p.psum[(int64_t)c * p.cap + id];
         }
     }
-    qc[qtr][kl] = cnt;
-    qs[qtr][kl] = sum;
+    qc[grp][kl] = cnt;
+    qs[grp][kl] = sum;
     __syncthreads();
-    if (qtr == 0 && id < nk) {
-        cnt = qc[0][kl] + qc[1][kl] + qc[2][kl] + qc[3][kl];
-        sum = ((qs[0][kl] + qs[1][kl]) + qs[2][kl]) + qs[3][kl];
+    if (grp == 0 && id < nk) {
+        cnt = 0;
+        sum = 0.0;
+        for (int g = 0; g < FIN_GROUPS; ++g) {
+            cnt += qc[g][kl];
+            sum += qs[g][kl];
+        }
         p.count_out[id] = (int64_t)cnt;
         p.sum_out[id] = sum;
         p.mean[id] = cnt ? sum / (double)cnt : 0.0;
@@ -302,19 +324,23 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) p.pm2[(int64_t)c * p.cap + r0 + v] = lm2[v];
 }
 
-__global__ __launch_bounds__(256) void k_fin_m2(const GroupParams p)
+__global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupParams p)
 {
-    __shared__ double qs[4][64];
+    __shared__ double qs[FIN_GROUPS][FIN_KEYS];
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
-    const int kl = threadIdx.x & 63, qtr = threadIdx.x >> 6;
-    const int64_t id = (int64_t)blockIdx.x * 64 + kl;
-    if ((int64_t)blockIdx.x * 64 >= nk) return;  // uniform
+    const int kl = threadIdx.x % FIN_KEYS, grp = threadIdx.x / FIN_KEYS;
+    const int64_t id = (int64_t)blockIdx.x * FIN_KEYS + kl;
+    if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     double m2 = 0.0;
     if (id < nk)
-        for (int c = qtr; c < p.nchunks; c += 4) m2 += p.pm2[(int64_t)c * p.cap + id];
-    qs[qtr][kl] = m2;
+        for (int c = grp; c < p.nchunks; c += FIN_GROUPS) m2 += p.pm2[(int64_t)c * p.cap + id];
+    qs[grp][kl] = m2;
     __syncthreads();
-    if (qtr == 0 && id < nk) p.m2_out[id] = ((qs[0][kl] + qs[1][kl]) + qs[2][kl]) + qs[3][kl];
+    if (grp == 0 && id < nk) {
+        m2 = 0.0;
+        for (int g = 0; g < FIN_GROUPS; ++g) m2 += qs[g][kl];
+        p.m2_out[id] = m2;
+    }
 }
 
 // sum of the per-key sums (attributed energy), in key order
@@ -354,11 +380,11 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
     if (ranges > 0) {
         hipLaunchKernelGGL(k_agg_sum, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);
-        const unsigned kb = (unsigned)max((int64_t)1, (p.cap + 63) / 64);
-        hipLaunchKernelGGL(k_fin_sum, dim3(kb), dim3(256), 0, stream, p);
+        const unsigned kb = (unsigned)max((int64_t)1, (p.cap + FIN_KEYS - 1) / FIN_KEYS);
+        hipLaunchKernelGGL(k_fin_sum, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
         hipLaunchKernelGGL(k_agg_m2, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);
-        hipLaunchKernelGGL(k_fin_m2, dim3(kb), dim3(256), 0, stream, p);
+        hipLaunchKernelGGL(k_fin_m2, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
         hipLaunchKernelGGL(k_key_total, dim3(1), dim3(1024), 0, stream, p);
     }
     return hipGetLastError();

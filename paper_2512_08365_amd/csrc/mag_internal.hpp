@@ -18,10 +18,11 @@ constexpr int SEG_PER_THREAD = 8;
 constexpr int TILE = 64 * SEG_PER_THREAD;  // 512
 constexpr int ROUND_EVENTS = 64;
 constexpr int MAX_STREAMS = MAG_MAX_STREAMS;
+constexpr int SUM_SLICE = 8192;  // tiles per workgroup of the per-tile total reduction
 
 // group-by
-constexpr int AGG_THREADS = 256;
-constexpr int AGG_IDS = 4096;       // key ids per LDS table (count u32 + sum f64)
+constexpr int AGG_THREADS = 1024;
+constexpr int AGG_IDS = 8192;       // key ids per LDS table (count u32 + sum f64)
 constexpr int AGG_MAX_CHUNKS = 256; // interval chunks (partial tables)
 
 // cnt_fin entry that no workgroup wrote (no workgroup of any launch ended there)
@@ -146,6 +147,7 @@ struct DiffParams {
     uint64_t* cand_key;
     int32_t* cand_ia;
     int32_t* cand_ib;
+    uint32_t* cand_rank;  // global rank of each candidate (counted by k_diff_rank)
     uint64_t* out_key;
     double* out_ratio;
     double* out_ea;
@@ -174,11 +176,14 @@ hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_
 hipError_t launch_tile(const TileParams& p, hipStream_t stream);
 hipError_t launch_cross(const FixParams& p, hipStream_t stream);
 hipError_t launch_outside(const FixParams& p, hipStream_t stream);
-hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, Status* st,
-                          hipStream_t stream);
+// whole-trace and idle energy from the per-tile totals (part: 2 * ceil(NT / SUM_SLICE) doubles)
+hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, double* part,
+                          Status* st, hipStream_t stream);
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
 hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream);
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream);
+// upper bound of the diff's stage-1 candidates for n_keys_a rows and top k
+int64_t diff_max_candidates(int64_t na, int64_t k);
 
 int device_cu_count();
 
