@@ -90,33 +90,36 @@ __device__ __forceinline__ double wave_sum(double v)
 }  // namespace
 
 // LDS of one wave (a workgroup holds WPB independent waves)
-template <int C, int NV, int SMAX>
+template <int C, int SMAX>
 struct WaveLds {
     static constexpr int T = WAVE * C;
-    static constexpr int E = NV * WAVE;
+    static constexpr int E = WAVE;      // endpoints per round: one per lane
+    static constexpr int W = 2 * WAVE;  // window entries: two per lane
     double sh_t[C + 1][WAVE];    // column k holds the C+1 samples of lane k's segments
     float sh_P[C + 1][WAVE];
     uint32_t flag[T / 32];       // segment holds a breakpoint of the round
     int wp[T / 32 + 1];          // set flags in the words before each word
     double R[E + 2];             // run sums, by rank of the breakpoint segment they end at
-    double ev_x[E];              // endpoint window, stream-major
+    double ev_x[W];              // endpoint window, stream-major
     double mg_x[E];              // merged endpoints
     uint32_t mg_jm[E];           // segment | active-after << 16 | end flag << 31
     double gv[E + 1];            // per-gap energy share
-    uint8_t ev_pos[E];           // merged position of a window slot
+    uint8_t ev_pos[E];           // merged position of a round slot
     int64_t st_q[SMAX], st_off[SMAX], st_len[SMAX];
-    int st_take[SMAX], st_started[SMAX], nx_started[SMAX];
+    int st_take[SMAX], st_first[SMAX];  // endpoints taken this round; first round slot
+    int st_started[SMAX], nx_started[SMAX];
     double st_acc[SMAX], nx_acc[SMAX];
     double st_lastx[SMAX];       // the stream's last consumed endpoint
 };
 
-template <int C, int NV, int SMAX, int WPB>
+template <int C, int SMAX, int WPB>
 __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4))) void k_tile(
     const TileParams p)
 {
-    using Lds = WaveLds<C, NV, SMAX>;
+    using Lds = WaveLds<C, SMAX>;
     constexpr int T = Lds::T;
     constexpr int E = Lds::E;
+    constexpr int W = Lds::W;
     constexpr int NWORD = T / 32;
     static_assert((C & (C - 1)) == 0 && C >= 4 && NWORD <= WAVE && E <= 255, "tile layout");
 
@@ -125,10 +128,11 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     const int wave = threadIdx.x / WAVE;
     Lds& sm = lds_all[wave];
     const int S = p.ss.S;
-    int lc = 0;  // window slots per stream: the largest power of two with S * cap <= E
-    while ((S << (lc + 1)) <= E) ++lc;
+    int lc = 0;  // window entries per stream: the largest power of two with S * cap <= W
+    while ((S << (lc + 1)) <= W) ++lc;
     const int cap = 1 << lc;
     const int nslot = S << lc;
+    const int budget = cap >> 1;  // per-stream share of the round slots when they run short
     const int64_t NT = p.NT;  // the last tile's successor (larger while the end is unknown)
     const int64_t LD = p.ld;
     const int64_t b0 = p.tile_begin + ((int64_t)blockIdx.x * WPB + wave) * p.tiles_per_wg;
@@ -184,7 +188,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
         return sm.wp[w] + __popc(sm.flag[w] & ((1u << (j & 31)) - 1u));
     };
 
-    double ew[NV];  // prefetched window of the next tile
+    double ew[2];  // prefetched window of the next tile
     bool ew_ready = false;
     unsigned err = 0u;
     double w_acc = 0.0, idle = 0.0;  // this lane's share of the trace and idle energy
@@ -274,49 +278,63 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
         int rs_j = -1;          // its segment (-1: the tile's first sample)
 
         for (;;) {
-            // ---- endpoint window of this round: slot = stream * cap + rank
-            double xv[NV];
-            uint64_t in[NV];
+            // ---- endpoint window of this round: entry = stream * cap + rank
+            double xw[2];
+            uint64_t in[2];
 #pragma unroll
-            for (int v = 0; v < NV; ++v) {
-                xv[v] = ew_ready ? ew[v] : window_x(lane + WAVE * v, false);
-                sm.ev_x[lane + WAVE * v] = xv[v];
-                in[v] = __ballot(xv[v] <= tau_end);
+            for (int v = 0; v < 2; ++v) {
+                xw[v] = ew_ready ? ew[v] : window_x(lane + WAVE * v, false);
+                sm.ev_x[lane + WAVE * v] = xw[v];
+                in[v] = __ballot(xw[v] <= tau_end);
             }
             ew_ready = false;
             wave_sync();
             // each stream's endpoints in the tile are a prefix of its (sorted)
-            // window; a full window limits the round to endpoints <= cut
+            // window.  If they all fit the round's slots they are all taken;
+            // otherwise every stream keeps at most `budget` and the round ends at
+            // the earliest time a stream runs out of its share (a time prefix)
             auto count_in = [&](const uint64_t* m, int a) -> int {
-                int c = 0;
-#pragma unroll
-                for (int v = 0; v < NV; ++v)
-                    c += popc_range(m[v], 0ull, (a << lc) - WAVE * v, ((a + 1) << lc) - WAVE * v);
-                return c;
+                return popc_range(m[0], m[1], a << lc, (a + 1) << lc);
             };
+            int tot = 0;
+            bool over = false;
+            for (int a = 0; a < S; ++a) {
+                const int ka = count_in(in, a);
+                tot += ka;
+                if (ka == cap && sm.st_q[a] + cap < sm.st_len[a]) over = true;
+            }
             double cut = INFINITY;
             bool fin = true;
-            for (int a = 0; a < S; ++a) {
-                if (count_in(in, a) == cap && sm.st_q[a] + cap < sm.st_len[a]) {
-                    fin = false;
-                    cut = fmin(cut, sm.ev_x[(a << lc) + cap - 1]);
+            if (over || tot > E) {
+                for (int a = 0; a < S; ++a) {
+                    if (count_in(in, a) > budget) {
+                        fin = false;
+                        cut = fmin(cut, sm.ev_x[(a << lc) + budget - 1]);
+                    }
                 }
             }
-            uint64_t tk[NV];
+            uint64_t tk[2];
 #pragma unroll
-            for (int v = 0; v < NV; ++v) tk[v] = fin ? in[v] : (in[v] & __ballot(xv[v] <= cut));
+            for (int v = 0; v < 2; ++v) tk[v] = fin ? in[v] : (in[v] & __ballot(xw[v] <= cut));
             int Er = 0, m0 = 0;
             for (int a = 0; a < S; ++a) {
-                const int ta = count_in(tk, a);
-                if (lane == 0) sm.st_take[a] = ta;
+                int ta = count_in(tk, a);
+                if (!fin) ta = min(ta, budget);  // endpoints equal to the cut may wait
+                if (lane == 0) {
+                    sm.st_take[a] = ta;
+                    sm.st_first[a] = Er;
+                }
                 Er += ta;
                 m0 += (int)(sm.st_q[a] & 1);
             }
             if (!fin && Er == 0) {
                 // only with unsorted endpoints: force progress, report
                 for (int a = 0; a < S; ++a) {
-                    if (count_in(in, a) == cap && sm.st_q[a] + cap < sm.st_len[a]) {
-                        if (lane == 0) sm.st_take[a] = 1;
+                    if (count_in(in, a) > budget) {
+                        if (lane == 0) {
+                            sm.st_take[a] = 1;
+                            for (int a2 = 0; a2 < S; ++a2) sm.st_first[a2] = (a2 > a) ? 1 : 0;
+                        }
                         Er = 1;
                         break;
                     }
@@ -330,20 +348,25 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
             // prefetch the next tile's window (its cursors are known now)
             if (fin && b + 1 < b1) {
 #pragma unroll
-                for (int v = 0; v < NV; ++v) ew[v] = window_x(lane + WAVE * v, true);
+                for (int v = 0; v < 2; ++v) ew[v] = window_x(lane + WAVE * v, true);
                 ew_ready = true;
             }
 
+            // round slot of this lane: stream a (the last with first[a] <= lane), rank r
+            int my_a = -1, my_r = 0;
+            if (lane < Er) {
+                my_a = 0;
+                for (int a = 1; a < S; ++a)
+                    if (sm.st_first[a] <= lane) my_a = a;
+                my_r = lane - sm.st_first[my_a];
+            }
+            const double my_x = (my_a >= 0) ? sm.ev_x[(my_a << lc) + my_r] : 0.0;
+
             // ---- endpoints, part 1: segment, sample index, checks, breakpoint flag
-            int jv[NV];
-#pragma unroll
-            for (int v = 0; v < NV; ++v) {
-                jv[v] = -1;
-                const int slot = lane + WAVE * v;
-                const double x = xv[v];
-                if (slot >= nslot) continue;
-                const int a = slot >> lc, r = slot & (cap - 1);
-                if (r >= sm.st_take[a]) continue;
+            int my_j = -1;
+            if (my_a >= 0) {
+                const int a = my_a, r = my_r;
+                const double x = my_x;
                 const int64_t q = sm.st_q[a] + r;
                 // segment j with t_j < x <= t_{j+1}: guess from the mean spacing, correct
                 int j = (int)fmin(fmax((x - t_begin) * inv_dt, 0.0), (double)(L - 1));
@@ -364,7 +387,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     }
                     j = min(max(lo, 1), L) - 1;
                 }
-                jv[v] = j;
+                my_j = j;
                 const int64_t gid = sm.st_off[a] + (q >> 1);
                 if (q & 1) {
                     if (p.end_idx) p.end_idx[gid] = j0 + j + 1;
@@ -373,7 +396,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                 }
                 if (p.validate) {
                     // finite and not before the stream's previous endpoint
-                    const double xp = (r > 0) ? sm.ev_x[slot - 1] : sm.st_lastx[a];
+                    const double xp = (r > 0) ? sm.ev_x[(a << lc) + r - 1] : sm.st_lastx[a];
                     if (!(fabs(x) < INFINITY) || !(xp <= x)) err |= ERR_INTERVAL;
                 }
                 atomicOr(&sm.flag[j >> 5], 1u << (j & 31));
@@ -457,12 +480,9 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     take[a2] = (a2 < S) ? sm.st_take[a2] : 0;
                     qpar[a2] = (a2 < S) ? (int)(sm.st_q[a2] & 1) : 0;
                 }
-#pragma unroll
-                for (int v = 0; v < NV; ++v) {
-                    if (jv[v] < 0) continue;
-                    const int slot = lane + WAVE * v;
-                    const double x = xv[v];
-                    const int a = slot >> lc, r = slot & (cap - 1);
+                if (my_j >= 0) {
+                    const double x = my_x;
+                    const int a = my_a, r = my_r;
                     const int q0 = (int)(sm.st_q[a] & 1);
                     // endpoints of each other stream before x in the merged order
                     // (ties: lower stream first); entries past a stream's take lie
@@ -493,9 +513,9 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     }
                     pos = min(pos, Er - 1);
                     const int64_t q = sm.st_q[a] + r;
-                    sm.ev_pos[slot] = (uint8_t)pos;
+                    sm.ev_pos[lane] = (uint8_t)pos;
                     sm.mg_x[pos] = x;
-                    sm.mg_jm[pos] = (uint32_t)jv[v] | ((uint32_t)m_after << 16) |
+                    sm.mg_jm[pos] = (uint32_t)my_j | ((uint32_t)m_after << 16) |
                                     ((q & 1) ? 0x80000000u : 0u);
                 }
             }
@@ -551,18 +571,14 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
             wave_sync();
 
             // ---- interval energies: intervals starting in this round
-#pragma unroll
-            for (int v = 0; v < NV; ++v) {
-                if (jv[v] < 0) continue;
-                const int slot = lane + WAVE * v;
-                const int a = slot >> lc, r = slot & (cap - 1);
+            if (my_j >= 0 && !((sm.st_q[my_a] + my_r) & 1)) {
+                const int a = my_a, r = my_r;
                 const int64_t q = sm.st_q[a] + r;
-                if (q & 1) continue;
                 const int ta = sm.st_take[a];
-                const int ps = sm.ev_pos[slot];
+                const int ps = sm.ev_pos[lane];
                 double acc = 0.0;
                 if (r + 1 < ta) {
-                    const int pe = min((int)sm.ev_pos[slot + 1], G - 1);
+                    const int pe = min((int)sm.ev_pos[lane + 1], G - 1);
                     for (int g = ps + 1; g <= pe; ++g) acc += sm.gv[g];
                     p.energy[sm.st_off[a] + (q >> 1)] = acc;
                 } else {
@@ -580,7 +596,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                 if (active) {
                     double acc = 0.0;
                     if (ta > 0) {
-                        const int pe = min((int)sm.ev_pos[a << lc], G - 1);
+                        const int pe = min((int)sm.ev_pos[sm.st_first[a]], G - 1);
                         for (int g = 0; g <= pe; ++g) acc += sm.gv[g];
                         const double Et = sm.st_acc[a] + acc;
                         if (sm.st_started[a])
@@ -651,13 +667,12 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
 namespace {
 
 constexpr int TILE_WPB = 4;  // independent waves per workgroup
-constexpr int TILE_NV = ROUND_EVENTS / WAVE;
 
 template <int SMAX>
 hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream)
 {
-    using K = decltype(&k_tile<SEG_PER_THREAD, TILE_NV, SMAX, TILE_WPB>);
-    const K kern = k_tile<SEG_PER_THREAD, TILE_NV, SMAX, TILE_WPB>;
+    using K = decltype(&k_tile<SEG_PER_THREAD, SMAX, TILE_WPB>);
+    const K kern = k_tile<SEG_PER_THREAD, SMAX, TILE_WPB>;
     // persistent waves: as many as can be resident at once, each over a
     // contiguous run of tiles
     static int per_cu = 0;
