@@ -81,6 +81,48 @@ __device__ __forceinline__ int popc_range(uint64_t lo, uint64_t hi, int b, int e
     return part(lo, b, e) + part(hi, b - 64, e - 64);
 }
 
+// DPP lane moves (bound_ctrl: lanes without a source read 0)
+constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114,
+              DPP_ROW_SHR8 = 0x118, DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143,
+              DPP_WAVE_SHR1 = 0x138;
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ int dpp_i32(int v)
+{
+    return __builtin_amdgcn_update_dpp(0, v, CTRL, ROWS, 0xf, true);
+}
+
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)dpp_i32<CTRL, ROWS>((int)(uint32_t)b);
+    const uint32_t hi = (uint32_t)dpp_i32<CTRL, ROWS>((int)(uint32_t)(b >> 32));
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// one step of a segmented inclusive scan: (h, x) after (hy, y) is
+// (hy | h, h ? x : y + x); lanes without a source combine with (0, 0)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ void seg_step(int& h, double& x)
+{
+    const int hy = dpp_i32<CTRL, ROWS>(h);
+    const double y = dpp_f64<CTRL, ROWS>(x);
+    x = h ? x : y + x;
+    h |= hy;
+}
+
+// inclusive segmented scan over the 64 lanes: within rows of 16, then across rows
+__device__ __forceinline__ void seg_scan_wave(int& h, double& x)
+{
+    seg_step<DPP_ROW_SHR1, 0xf>(h, x);
+    seg_step<DPP_ROW_SHR2, 0xf>(h, x);
+    seg_step<DPP_ROW_SHR4, 0xf>(h, x);
+    seg_step<DPP_ROW_SHR8, 0xf>(h, x);
+    seg_step<DPP_ROW_BCAST15, 0xa>(h, x);
+    seg_step<DPP_ROW_BCAST31, 0xc>(h, x);
+}
+
 __device__ __forceinline__ double wave_sum(double v)
 {
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
@@ -446,20 +488,15 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     }
                     loc[u] = run;
                 }
+                // the lanes' carries (reset flag, value): inclusive segmented
+                // scan across the wave, then shifted by one lane
                 int h = reset ? 1 : 0;
                 double xs = run;
-                for (int off = 1; off < WAVE; off <<= 1) {
-                    const double xo = __shfl_up(xs, off);
-                    const int ho = __shfl_up(h, off);
-                    if (lane >= off) {
-                        xs = h ? xs : xo + xs;
-                        h |= ho;
-                    }
-                }
-                double cin = __shfl_up(xs, 1);
-                if (lane == 0) cin = 0.0;
+                seg_scan_wave(h, xs);
+                const double cin = dpp_f64<DPP_WAVE_SHR1, 0xf>(xs);
                 bool seen = false;
                 const uint32_t fl = myflags | (nextflags << C);
+                const int rbase = rank_of(j0l);  // breakpoint segments before this lane's
 #pragma unroll
                 for (int u = 0; u < C; ++u) {
                     const bool prev_flag = (u == 0) ? prev_lane_last : ((myflags >> (u - 1)) & 1u);
@@ -467,7 +504,8 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     const int k = j0l + u;  // this run value ends at segment k
                     const bool nxt = ((fl >> (u + 1)) & 1u) != 0;
                     if (k + 1 < L && (nxt || (k + 1 == L - 1)))
-                        sm.R[rank_of(k + 1)] = seen ? loc[u] : cin + loc[u];
+                        sm.R[rbase + __popc(myflags & ((2u << u) - 1u))] =
+                            seen ? loc[u] : cin + loc[u];
                 }
             }
 
