@@ -237,6 +237,7 @@ int plan_attribution(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t k
                      mag::StreamSet* ss)
 {
     if (n_samples < 2) return fail(MAG_E_SIZE, "n_samples must be >= 2");
+    if (n_samples > MAG_MAX_SAMPLES) return fail(MAG_E_SIZE, "n_samples exceeds MAG_MAX_SAMPLES");
     if (n_intervals < 0 || key_capacity < 0) return fail(MAG_E_SIZE, "negative size");
     int S;
     int rc = check_opts(opts, n_intervals, &S, flags, ss);

@@ -175,10 +175,11 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     const int cap = 1 << lc;
     const int nslot = S << lc;
     const int budget = cap >> 1;  // per-stream share of the round slots when they run short
-    const int64_t NT = p.NT;  // the last tile's successor (larger while the end is unknown)
-    const int64_t LD = p.ld;
-    const int64_t b0 = p.tile_begin + ((int64_t)blockIdx.x * WPB + wave) * p.tiles_per_wg;
-    const int64_t b1 = min(b0 + p.tiles_per_wg, p.tile_end);
+    // tile indices fit 32 bits (the host caps the trace length)
+    const int NT = (int)p.NT;  // the last tile's successor (larger while the end is unknown)
+    const int LD = (int)p.ld;
+    const int b0 = (int)p.tile_begin + ((int)blockIdx.x * WPB + wave) * (int)p.tiles_per_wg;
+    const int b1 = min(b0 + (int)p.tiles_per_wg, (int)p.tile_end);
     if (b0 >= b1) return;  // uniform per wave; waves never wait for each other
 
     if (lane < S) {
@@ -190,7 +191,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     {
         // cursor of each stream at the first tile: endpoints <= its start time
         // (64-ary search, about four dependent loads per stream)
-        const double tau0 = p.t[b0 * T - p.base];
+        const double tau0 = p.t[(int64_t)b0 * T - p.base];
         for (int a = 0; a < S; ++a) {
             const int64_t off = sm.st_off[a];
             int64_t lo = 0, hi = sm.st_len[a];
@@ -235,8 +236,8 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     unsigned err = 0u;
     double w_acc = 0.0, idle = 0.0;  // this lane's share of the trace and idle energy
 
-    for (int64_t b = b0; b < b1; ++b) {
-        const int64_t j0 = b * T;
+    for (int b = b0; b < b1; ++b) {
+        const int64_t j0 = (int64_t)b * T;
         const int L = (int)min((int64_t)T, p.nseg - j0);
         const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
 
@@ -686,7 +687,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     // the wave's trace and idle energy, kept at its first tile (others 0)
     const double Wt = wave_sum(w_acc);
     const double It = wave_sum(idle);
-    for (int64_t b = b0 + lane; b < b1; b += WAVE) {
+    for (int b = b0 + lane; b < b1; b += WAVE) {
         p.tileW[b] = (b == b0) ? Wt : 0.0;
         p.tileIdle[b] = (b == b0) ? It : 0.0;
     }

@@ -43,6 +43,7 @@ def test_host_side_errors_without_gpu():
     assert lib.mag_attribute_workspace_size(1, 0, 0, None, ctypes.byref(b)) == N.MAG_E_SIZE
     assert lib.mag_attribute_workspace_size(10, -1, 0, None, ctypes.byref(b)) == N.MAG_E_SIZE
     assert lib.mag_attribute_workspace_size(10, 5, 0, None, None) == N.MAG_E_NULL
+    assert lib.mag_attribute_workspace_size((1 << 40) + 1, 0, 0, None, ctypes.byref(b)) == N.MAG_E_SIZE
     o = N.AttrOpts(2, N.MAG_EQUAL_SPLIT, None)
     assert lib.mag_attribute_workspace_size(10, 5, 0, ctypes.byref(o), ctypes.byref(b)) == N.MAG_E_STREAMS
     offs = (ctypes.c_int64 * 3)(0, 4, 3)
