@@ -101,7 +101,6 @@ __global__ __launch_bounds__(256) void k_init(Status* st, int64_t* cnt_fin, int6
         cnt_fin[i] = CNT_UNSET;
     if (blockIdx.x == 0 && threadIdx.x == 0) {
         st->err = 0u;
-        st->n_inserted = 0u;
         st->special = 0u;
         st->overflow = 0u;
         st->n_clipped = 0ull;

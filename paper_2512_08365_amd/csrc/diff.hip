@@ -27,10 +27,11 @@ __device__ __forceinline__ double rel_diff(double ea, double eb)
     return (eb - ea) / ea;
 }
 
-// total order of the ranking: larger r first, then smaller key
+// total order of the ranking: larger r first, then smaller key (evaluated
+// without short-circuit branches, so loops over it stay straight-line code)
 __device__ __forceinline__ bool before(double rq, uint64_t kq, double rp, uint64_t kp)
 {
-    return rq > rp || (rq == rp && kq < kp);
+    return (rq > rp) | ((rq == rp) & (kq < kp));
 }
 
 // entries of the ascending array a[0, n) below v (or at most v), found by the
@@ -122,8 +123,7 @@ __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
     if (valid) {
         int64_t rank = 0;
 #pragma unroll 16
-        for (int q = 0; q < JOIN_ROWS; ++q)
-            if (lv[q] && before(lr[q], lk[q], r, key)) ++rank;
+        for (int q = 0; q < JOIN_ROWS; ++q) rank += (lv[q] != 0) & before(lr[q], lk[q], r, key);
         cand = rank < p.k;
     }
     // one counter update per wave: candidates take consecutive slots

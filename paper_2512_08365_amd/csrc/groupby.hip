@@ -44,40 +44,40 @@ __global__ __launch_bounds__(256) void k_table_fill(unsigned long long* table, u
 }
 
 // Insert the distinct keys of a prefix of the intervals.  Each workgroup first
-// de-duplicates its chunk in an LDS table, so a key costs at most one global
-// compare-and-swap per workgroup instead of one per interval.
-constexpr int INS_CHUNK = 4096;
-constexpr int INS_SLOTS = 8192;
-constexpr int INS_GROUPS = 64;  // the lookup pass inserts keys first seen later
+// de-duplicates its chunk in an LDS table; then every thread takes a few LDS
+// slots and inserts their keys into the global table, so a key costs one global
+// probe per workgroup and the probe chains of a workgroup run in parallel.
+constexpr int INS_THREADS = 1024;
+constexpr int INS_CHUNK = 8192;
+constexpr int INS_SLOTS = 16384;
+constexpr int INS_GROUPS = 32;  // the lookup pass inserts keys first seen later
 
 __device__ __forceinline__ void global_insert(const GroupParams& p, unsigned long long k)
 {
     const uint32_t mask = p.H - 1u;
     uint32_t h = (uint32_t)fmix64(k) & mask;
     for (uint32_t probe = 0; probe < p.H; ++probe) {
-        // a plain load first: before this launch every slot was empty, and a slot
-        // only changes from empty to its final key, so a non-empty value read here
-        // is final; an empty one may be stale and is settled by the swap
-        const unsigned long long cur = p.table[h];
+        // a device-coherent load first (the level-2 caches of the XCDs are not
+        // coherent with each other, so a plain load could keep returning a stale
+        // empty slot and force a swap per probe); a slot only ever changes from
+        // empty to its final key, so a non-empty value read here is final
+        const unsigned long long cur =
+            __hip_atomic_load(&p.table[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (cur == k) return;
         if (cur == EMPTY_KEY) {
             const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
-            if (old == EMPTY_KEY) {
-                atomicAdd(&p.status->n_inserted, 1u);
-                return;
-            }
-            if (old == k) return;
+            if (old == EMPTY_KEY || old == k) return;
         }
         h = (h + 1u) & mask;
     }
     atomicOr(&p.status->overflow, 1u);
 }
 
-__global__ __launch_bounds__(256) void k_key_insert(const GroupParams p, int64_t n_insert)
+__global__ __launch_bounds__(INS_THREADS) void k_key_insert(const GroupParams p, int64_t n_insert)
 {
     __shared__ unsigned long long lt[INS_SLOTS];
     for (int v = threadIdx.x; v < INS_SLOTS; v += blockDim.x) lt[v] = EMPTY_KEY;
-    lds_barrier();
+    __syncthreads();
     const int64_t lo = (int64_t)blockIdx.x * INS_CHUNK, hi = min(lo + INS_CHUNK, n_insert);
     for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
         const unsigned long long k = p.keys[i];
@@ -86,17 +86,16 @@ __global__ __launch_bounds__(256) void k_key_insert(const GroupParams p, int64_t
             continue;
         }
         uint32_t h = (uint32_t)fmix64(k) & (INS_SLOTS - 1);
-        bool first = true;  // also when the LDS table is full: insert globally
         for (int probe = 0; probe < INS_SLOTS; ++probe) {
             const unsigned long long old = atomicCAS(&lt[h], EMPTY_KEY, k);
-            if (old == EMPTY_KEY) break;
-            if (old == k) {
-                first = false;
-                break;
-            }
+            if (old == EMPTY_KEY || old == k) break;
             h = (h + 1u) & (INS_SLOTS - 1);
         }
-        if (first) global_insert(p, k);
+    }
+    __syncthreads();
+    for (int v = threadIdx.x; v < INS_SLOTS; v += blockDim.x) {
+        const unsigned long long k = lt[v];
+        if (k != EMPTY_KEY) global_insert(p, k);
     }
 }
 
@@ -125,12 +124,7 @@ __global__ __launch_bounds__(256) void k_keymap(const GroupParams p)
                 }
                 if (cur == EMPTY_KEY) {
                     const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
-                    if (old == EMPTY_KEY) {
-                        atomicAdd(&p.status->n_inserted, 1u);
-                        slot = h;
-                        break;
-                    }
-                    if (old == k) {
+                    if (old == EMPTY_KEY || old == k) {
                         slot = h;
                         break;
                     }
@@ -172,15 +166,17 @@ __global__ __launch_bounds__(256) void k_compact(const GroupParams p)
 }
 
 // dense id = number of distinct keys smaller than this one; block (x, y)
-// compares keys [256 x, 256 x + 256) against keys [1024 y, 1024 y + 1024)
+// compares keys [256 x, 256 x + 256) against keys [RANK_TILE y, RANK_TILE (y + 1))
+constexpr uint32_t RANK_TILE = 256u;
+
 __global__ __launch_bounds__(256) void k_rank(const GroupParams p)
 {
-    __shared__ uint64_t tile[1024];
+    __shared__ uint64_t tile[RANK_TILE];
     const uint32_t nu = p.status->n_unique;
-    const uint32_t base = blockIdx.y * 1024u;
+    const uint32_t base = blockIdx.y * RANK_TILE;
     if (blockIdx.x * 256u >= nu || base >= nu) return;  // uniform over the block
     const uint32_t u = blockIdx.x * 256u + threadIdx.x;
-    const uint32_t cnt = min(1024u, nu - base);
+    const uint32_t cnt = min(RANK_TILE, nu - base);
     for (uint32_t v = threadIdx.x; v < cnt; v += 256u) tile[v] = p.ukey[base + v];
     lds_barrier();
     if (u >= nu) return;
@@ -367,13 +363,16 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
     hipLaunchKernelGGL(k_table_fill, dim3(fill_blocks), dim3(256), 0, stream, p.table, p.urank, p.H);
     const int64_t n_ins = min(p.m, (int64_t)INS_CHUNK * INS_GROUPS);
     hipLaunchKernelGGL(k_key_insert, dim3((unsigned)((n_ins + INS_CHUNK - 1) / INS_CHUNK)),
-                       dim3(256), 0, stream, p, n_ins);
+                       dim3(INS_THREADS), 0, stream, p, n_ins);
     const int64_t mb = min((p.m + 255) / 256, (int64_t)16384);
     hipLaunchKernelGGL(k_keymap, dim3((unsigned)max(mb, (int64_t)1)), dim3(256), 0, stream, p);
     const unsigned hb = (unsigned)min((int64_t)(p.H + 1 + 255) / 256, (int64_t)4096);
     hipLaunchKernelGGL(k_compact, dim3(hb), dim3(256), 0, stream, p);
-    const unsigned rx = (unsigned)(((int64_t)p.H + 1 + 255) / 256);
-    const unsigned ry = (unsigned)(((int64_t)p.H + 1 + 1023) / 1024);
+    // the distinct keys are at most min(H + 1, cap + 1) when they fit (more only
+    // on overflow, which is reported and ranked partially)
+    const int64_t nmax = min((int64_t)p.H + 1, p.cap + 1);
+    const unsigned rx = (unsigned)((nmax + 255) / 256);
+    const unsigned ry = (unsigned)((nmax + RANK_TILE - 1) / RANK_TILE);
     hipLaunchKernelGGL(k_rank, dim3(rx, ry), dim3(256), 0, stream, p);
     hipLaunchKernelGGL(k_rank_write, dim3(hb), dim3(256), 0, stream, p);
     const unsigned ranges = (unsigned)((p.cap + AGG_IDS - 1) / AGG_IDS);

@@ -39,7 +39,7 @@ enum : uint32_t {
 // small device status block at the head of every workspace
 struct Status {
     uint32_t err;
-    uint32_t n_inserted;  // distinct keys inserted into the hash table
+    uint32_t pad1;
     uint32_t special;     // the all-ones key was seen (stored out of band)
     uint32_t overflow;    // a key found no free slot
     unsigned long long n_clipped;
