@@ -531,24 +531,23 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     int c[SMAX];
 #pragma unroll
                     for (int a2 = 0; a2 < SMAX; ++a2) c[a2] = 0;
+                    // (straight-line: every lane runs every step of every search)
                     for (int step = cap >> 1; step > 0; step >>= 1) {
 #pragma unroll
                         for (int a2 = 0; a2 < SMAX; ++a2) {
-                            if (a2 < S && a2 != a) {
-                                const double y = sm.ev_x[(a2 << lc) + c[a2] + step - 1];
-                                if (a2 < a ? (y <= x) : (y < x)) c[a2] += step;
-                            }
+                            const double y = sm.ev_x[(min(a2, S - 1) << lc) + c[a2] + step - 1];
+                            const bool pr = (y < x) | ((a2 < a) & (y == x));
+                            c[a2] += pr ? step : 0;
                         }
                     }
 #pragma unroll
                     for (int a2 = 0; a2 < SMAX; ++a2) {
-                        if (a2 < S && a2 != a) {
-                            const double y = sm.ev_x[(a2 << lc) + c[a2]];
-                            if (a2 < a ? (y <= x) : (y < x)) ++c[a2];
-                            const int ca = min(c[a2], take[a2]);
-                            pos += ca;
-                            m_after += (qpar[a2] + ca) & 1;
-                        }
+                        const double y = sm.ev_x[(min(a2, S - 1) << lc) + c[a2]];
+                        const bool pr = (y < x) | ((a2 < a) & (y == x));
+                        const int ca = min(c[a2] + (pr ? 1 : 0), take[a2]);
+                        const bool other = (a2 < S) & (a2 != a);
+                        pos += other ? ca : 0;
+                        m_after += other ? ((qpar[a2] + ca) & 1) : 0;
                     }
                     pos = min(pos, Er - 1);
                     const int64_t q = sm.st_q[a] + r;
@@ -582,29 +581,23 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     xe = tau_end;
                     je = L - 1;
                 }
-                double Q;
-                if (js == je) {
-                    const double ta = t_at(js), tb = t_at(js + 1);
-                    const double pa = P_at(js), pb = P_at(js + 1);
-                    Q = 0.5 * (lerp_power(ta, tb, pa, pb, xs) + lerp_power(ta, tb, pa, pb, xe)) *
-                        (xe - xs);
-                } else {
-                    Q = 0.0;
-                    if (js >= 0) {
-                        const double ta = t_at(js), tb = t_at(js + 1);
-                        const double pa = P_at(js), pb = P_at(js + 1);
-                        Q += 0.5 * (lerp_power(ta, tb, pa, pb, xs) + pb) * (tb - xs);
-                    }
-                    if (je > js + 1) Q += sm.R[rank_of(je)];
-                    const double ta = t_at(je), tb = t_at(je + 1);
-                    const double pa = P_at(je), pb = P_at(je + 1);
-                    Q += 0.5 * (pa + lerp_power(ta, tb, pa, pb, xe)) * (xe - ta);
-                }
-                double v = 0.0;
-                if (m > 0)
-                    v = p.split ? Q / (double)m : Q;
-                else
-                    idle += Q;
+                // trapezoids of the interpolant: within one segment, or the piece to
+                // the end of the first segment + whole segments + the piece from the
+                // start of the last (straight-line code: both forms are evaluated)
+                const int js0 = max(js, 0);
+                const double ta_s = t_at(js0), tb_s = t_at(js0 + 1);
+                const double pa_s = P_at(js0), pb_s = P_at(js0 + 1);
+                const double ta_e = t_at(je), tb_e = t_at(je + 1);
+                const double pa_e = P_at(je), pb_e = P_at(je + 1);
+                const double px_s = lerp_power(ta_s, tb_s, pa_s, pb_s, xs);
+                const double px_e = lerp_power(ta_e, tb_e, pa_e, pb_e, xe);
+                const double q_in = 0.5 * (px_s + px_e) * (xe - xs);
+                const double q_first = (js >= 0) ? 0.5 * (px_s + pb_s) * (tb_s - xs) : 0.0;
+                const double q_mid = (je > js + 1) ? sm.R[rank_of(je)] : 0.0;
+                const double q_last = 0.5 * (pa_e + px_e) * (xe - ta_e);
+                const double Q = (js == je) ? q_in : (q_first + q_mid) + q_last;
+                const double v = (m > 0) ? (p.split ? Q / (double)m : Q) : 0.0;
+                idle += (m > 0) ? 0.0 : Q;
                 sm.gv[g] = v;
             }
             wave_sync();
