@@ -68,19 +68,6 @@ __device__ __forceinline__ void wave_sync()
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// set bits of the 128-bit mask (hi:lo) at positions [b, e)
-__device__ __forceinline__ int popc_range(uint64_t lo, uint64_t hi, int b, int e)
-{
-    auto part = [](uint64_t m, int pb, int pe) -> int {
-        pb = max(pb, 0);
-        pe = min(pe, 64);
-        if (pe <= pb) return 0;
-        const uint64_t upto = (pe == 64) ? ~0ull : ((1ull << pe) - 1ull);
-        return __popcll(m & upto & ~((1ull << pb) - 1ull));
-    };
-    return part(lo, b, e) + part(hi, b - 64, e - 64);
-}
-
 // DPP lane moves (bound_ctrl: lanes without a source read 0)
 constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114,
               DPP_ROW_SHR8 = 0x118, DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143,
@@ -336,8 +323,13 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
             // window.  If they all fit the round's slots they are all taken;
             // otherwise every stream keeps at most `budget` and the round ends at
             // the earliest time a stream runs out of its share (a time prefix)
+            // stream a's entries are bits [a cap, (a + 1) cap) of the 128-bit mask
             auto count_in = [&](const uint64_t* m, int a) -> int {
-                return popc_range(m[0], m[1], a << lc, (a + 1) << lc);
+                if (cap > WAVE) return __popcll(m[0]) + __popcll(m[1]);  // one stream
+                if (cap == WAVE) return __popcll(m[a]);                     // two streams
+                const int b0 = a << lc;
+                const uint64_t w = (b0 >= WAVE) ? m[1] : m[0];
+                return __popcll((w >> (b0 & (WAVE - 1))) & ((1ull << cap) - 1ull));
             };
             int tot = 0;
             bool over = false;
