@@ -224,6 +224,11 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     double w_acc = 0.0, idle = 0.0;  // this lane's share of the trace and idle energy
 
     for (int b = b0; b < b1; ++b) {
+        // the lane index, opaque to the compiler within this tile: keeps per-lane
+        // 64-bit addresses from being hoisted out of the tile loop (where they
+        // would occupy registers for the whole kernel and spill)
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
         const int64_t j0 = (int64_t)b * T;
         const int L = (int)min((int64_t)T, p.nseg - j0);
         const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
@@ -232,7 +237,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
         {
             double tv[C + 1];
             float pv[C + 1];
-            const int64_t g = j0 + (int64_t)lane * C - p.base;
+            const int64_t g = j0 + (int64_t)ln * C - p.base;
             if (cs == C && p.aligned16) {
                 const double2* t2 = reinterpret_cast<const double2*>(p.t + g);
                 const float4* P4 = reinterpret_cast<const float4*>(p.P + g);
@@ -285,7 +290,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
             }
         }
         if (lane < S) {
-            p.cnt[(int64_t)lane * (LD + 1) + b] = sm.st_q[lane];
+            p.cnt[(int64_t)ln * (LD + 1) + b] = sm.st_q[lane];
             sm.st_acc[lane] = 0.0;
             sm.st_started[lane] = 0;
         }
@@ -626,7 +631,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                         if (sm.st_started[a])
                             p.energy[sm.st_off[a] + (sm.st_q[a] >> 1)] = Et;
                         else
-                            p.head[(int64_t)a * LD + b] = Et;
+                            p.head[(int64_t)(a + ln - lane) * LD + b] = Et;
                         if (!ends_open) {
                             sm.nx_acc[a] = 0.0;
                             sm.nx_started[a] = 0;
@@ -662,9 +667,9 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
         // ---- interval still open at the tile's end: its piece of this tile
         if (lane < S && (sm.st_q[lane] & 1)) {
             if (sm.st_started[lane])
-                p.tail[(int64_t)lane * LD + b] = sm.st_acc[lane];
+                p.tail[(int64_t)ln * LD + b] = sm.st_acc[lane];
             else
-                p.head[(int64_t)lane * LD + b] = sm.st_acc[lane];
+                p.head[(int64_t)ln * LD + b] = sm.st_acc[lane];
         }
         wave_sync();
     }
