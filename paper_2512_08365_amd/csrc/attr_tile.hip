@@ -50,6 +50,19 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
     return (q & 1) ? e[i] : s[i];
 }
 
+// The kernel's arguments, read again from the kernel-argument segment where
+// they are used (scalar loads that hit the constant cache).  Loaded once at
+// entry, as the compiler does for a plain parameter, they would occupy scalar
+// registers for the whole kernel and spill.  The pointer is made opaque at
+// every call so that no load is shared between (or hoisted out of) phases.
+typedef const __attribute__((address_space(4))) TileParams* KArgs;
+__device__ __forceinline__ KArgs kargs()
+{
+    KArgs k = (KArgs)__builtin_amdgcn_kernarg_segment_ptr();
+    asm volatile("" : "+s"(k));
+    return k;
+}
+
 // linear interpolant on [ta, tb] at x, exactly the sample values at the ends
 __device__ __forceinline__ double lerp_power(double ta, double tb, double pa, double pb, double x)
 {
@@ -163,8 +176,6 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     const int nslot = S << lc;
     const int budget = cap >> 1;  // per-stream share of the round slots when they run short
     // tile indices fit 32 bits (the host caps the trace length)
-    const int NT = (int)p.NT;  // the last tile's successor (larger while the end is unknown)
-    const int LD = (int)p.ld;
     const int b0 = (int)p.tile_begin + ((int)blockIdx.x * WPB + wave) * (int)p.tiles_per_wg;
     const int b1 = min(b0 + (int)p.tiles_per_wg, (int)p.tile_end);
     if (b0 >= b1) return;  // uniform per wave; waves never wait for each other
@@ -210,7 +221,8 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
         if (slot >= nslot) return INFINITY;
         const int a = slot >> lc, r = slot & (cap - 1);
         const int64_t q = sm.st_q[a] + (advance ? sm.st_take[a] : 0) + r;
-        return (q < sm.st_len[a]) ? endpoint_x(p.s, p.e, sm.st_off[a], q) : INFINITY;
+        const KArgs k = kargs();
+        return (q < sm.st_len[a]) ? endpoint_x(k->s, k->e, sm.st_off[a], q) : INFINITY;
     };
     // breakpoint segments before segment j (the run sum ending at j-1 is R[rank(j)])
     auto rank_of = [&](int j) -> int {
@@ -230,17 +242,20 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
         int ln = lane;
         asm volatile("" : "+v"(ln));
         const int64_t j0 = (int64_t)b * T;
-        const int L = (int)min((int64_t)T, p.nseg - j0);
+        const int L = (int)min((int64_t)T, kargs()->nseg - j0);
         const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
 
         // ---- samples: load, stage, segment energies, checks
         {
             double tv[C + 1];
             float pv[C + 1];
-            const int64_t g = j0 + (int64_t)ln * C - p.base;
-            if (cs == C && p.aligned16) {
-                const double2* t2 = reinterpret_cast<const double2*>(p.t + g);
-                const float4* P4 = reinterpret_cast<const float4*>(p.P + g);
+            const KArgs k = kargs();
+            const double* tp = k->t;
+            const float* Pp = k->P;
+            const int64_t g = j0 + (int64_t)ln * C - k->base;
+            if (cs == C && k->aligned16) {
+                const double2* t2 = reinterpret_cast<const double2*>(tp + g);
+                const float4* P4 = reinterpret_cast<const float4*>(Pp + g);
 #pragma unroll
                 for (int u = 0; u < C / 2; ++u) {
                     const double2 v = t2[u];
@@ -255,42 +270,54 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                     pv[4 * u + 2] = v.z;
                     pv[4 * u + 3] = v.w;
                 }
-                tv[C] = p.t[g + C];
-                pv[C] = p.P[g + C];
+                tv[C] = tp[g + C];
+                pv[C] = Pp[g + C];
             } else {
+                // a lane with fewer segments repeats its last sample time with
+                // zero power: the missing segments have zero width and energy
 #pragma unroll
                 for (int u = 0; u <= C; ++u) {
                     if (u <= cs && cs > 0) {
-                        tv[u] = p.t[g + u];
-                        pv[u] = p.P[g + u];
+                        tv[u] = tp[g + u];
+                        pv[u] = Pp[g + u];
                     } else {
-                        tv[u] = 0.0;
+                        tv[u] = (u > 0) ? tv[u - 1] : 0.0;
                         pv[u] = 0.0f;
                     }
                 }
+            }
+            if (k->validate) {
+                // every segment of the lane rises (the repeated last time of a
+                // short lane does not), and a strictly increasing run whose ends
+                // are finite is finite throughout (a NaN fails every comparison)
+                int rising = 0;
+#pragma unroll
+                for (int u = 0; u < C; ++u) rising += (tv[u + 1] > tv[u]) ? 1 : 0;
+                const bool t_ok =
+                    (rising == cs) & (fabs(tv[0]) < INFINITY) & (fabs(tv[C]) < INFINITY);
+                bool p_ok = true;
+#pragma unroll
+                for (int u = 0; u <= C; ++u) p_ok &= (pv[u] >= 0.0f) & (pv[u] < INFINITY);
+                err |= (t_ok ? 0u : ERR_TIMESTAMPS) | (p_ok ? 0u : ERR_POWER);
             }
 #pragma unroll
             for (int u = 0; u <= C; ++u) {
                 sm.sh_t[u][lane] = tv[u];
                 sm.sh_P[u][lane] = pv[u];
             }
+            // segment energies (P_u + P_{u+1}) (t_{u+1} - t_u), halved once at the end
+            double wl = 0.0;
 #pragma unroll
-            for (int u = 0; u < C; ++u) {
-                const double ta = tv[u], tb = tv[u + 1];
-                const float pa = pv[u], pb = pv[u + 1];
-                if (u < cs) {
-                    if (p.validate) {
-                        if (!(tb > ta) || !(fabs(ta) < INFINITY) || !(fabs(tb) < INFINITY))
-                            err |= ERR_TIMESTAMPS;
-                        if (!(pa >= 0.0f && pa < INFINITY) || !(pb >= 0.0f && pb < INFINITY))
-                            err |= ERR_POWER;
-                    }
-                    w_acc += 0.5 * ((double)pa + (double)pb) * (tb - ta);
-                }
-            }
+            for (int u = 0; u < C; ++u)
+                wl += ((double)pv[u] + (double)pv[u + 1]) * (tv[u + 1] - tv[u]);
+            w_acc += 0.5 * wl;
+            // computed here, while the samples are in registers (not sunk to the
+            // end of the tile, which would keep them live through the rounds)
+            asm volatile("" : "+v"(w_acc));
         }
         if (lane < S) {
-            p.cnt[(int64_t)ln * (LD + 1) + b] = sm.st_q[lane];
+            const KArgs k = kargs();
+            k->cnt[(int64_t)ln * (k->ld + 1) + b] = sm.st_q[lane];
             sm.st_acc[lane] = 0.0;
             sm.st_started[lane] = 0;
         }
@@ -429,12 +456,10 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                 }
                 my_j = j;
                 const int64_t gid = sm.st_off[a] + (q >> 1);
-                if (q & 1) {
-                    if (p.end_idx) p.end_idx[gid] = j0 + j + 1;
-                } else {
-                    if (p.start_idx) p.start_idx[gid] = j0 + j + 1;
-                }
-                if (p.validate) {
+                const KArgs k = kargs();
+                int64_t* idx = (q & 1) ? k->end_idx : k->start_idx;
+                if (idx) idx[gid] = j0 + j + 1;
+                if (k->validate) {
                     // finite and not before the stream's previous endpoint
                     const double xp = (r > 0) ? sm.ev_x[(a << lc) + r - 1] : sm.st_lastx[a];
                     if (!(fabs(x) < INFINITY) || !(xp <= x)) err |= ERR_INTERVAL;
@@ -593,7 +618,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                 const double q_mid = (je > js + 1) ? sm.R[rank_of(je)] : 0.0;
                 const double q_last = 0.5 * (pa_e + px_e) * (xe - ta_e);
                 const double Q = (js == je) ? q_in : (q_first + q_mid) + q_last;
-                const double v = (m > 0) ? (p.split ? Q / (double)m : Q) : 0.0;
+                const double v = (m > 0) ? (kargs()->split ? Q / (double)m : Q) : 0.0;
                 idle += (m > 0) ? 0.0 : Q;
                 sm.gv[g] = v;
             }
@@ -609,7 +634,7 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                 if (r + 1 < ta) {
                     const int pe = min((int)sm.ev_pos[lane + 1], G - 1);
                     for (int g = ps + 1; g <= pe; ++g) acc += sm.gv[g];
-                    p.energy[sm.st_off[a] + (q >> 1)] = acc;
+                    kargs()->energy[sm.st_off[a] + (q >> 1)] = acc;
                 } else {
                     for (int g = ps + 1; g < G; ++g) acc += sm.gv[g];
                     sm.nx_acc[a] = acc;
@@ -628,10 +653,11 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                         const int pe = min((int)sm.ev_pos[sm.st_first[a]], G - 1);
                         for (int g = 0; g <= pe; ++g) acc += sm.gv[g];
                         const double Et = sm.st_acc[a] + acc;
+                        const KArgs k = kargs();
                         if (sm.st_started[a])
-                            p.energy[sm.st_off[a] + (sm.st_q[a] >> 1)] = Et;
+                            k->energy[sm.st_off[a] + (sm.st_q[a] >> 1)] = Et;
                         else
-                            p.head[(int64_t)(a + ln - lane) * LD + b] = Et;
+                            k->head[(int64_t)(a + ln - lane) * k->ld + b] = Et;
                         if (!ends_open) {
                             sm.nx_acc[a] = 0.0;
                             sm.nx_started[a] = 0;
@@ -666,10 +692,9 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
 
         // ---- interval still open at the tile's end: its piece of this tile
         if (lane < S && (sm.st_q[lane] & 1)) {
-            if (sm.st_started[lane])
-                p.tail[(int64_t)ln * LD + b] = sm.st_acc[lane];
-            else
-                p.head[(int64_t)ln * LD + b] = sm.st_acc[lane];
+            const KArgs k = kargs();
+            double* dst = sm.st_started[lane] ? k->tail : k->head;
+            dst[(int64_t)ln * k->ld + b] = sm.st_acc[lane];
         }
         wave_sync();
     }
@@ -677,19 +702,21 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
     // the wave's trace and idle energy, kept at its first tile (others 0)
     const double Wt = wave_sum(w_acc);
     const double It = wave_sum(idle);
+    const KArgs k = kargs();
     for (int b = b0 + lane; b < b1; b += WAVE) {
-        p.tileW[b] = (b == b0) ? Wt : 0.0;
-        p.tileIdle[b] = (b == b0) ? It : 0.0;
+        k->tileW[b] = (b == b0) ? Wt : 0.0;
+        k->tileIdle[b] = (b == b0) ? It : 0.0;
     }
     if (lane < S) {
         // where this wave stopped: the next wave must start there
-        p.cnt_fin[(int64_t)lane * (LD + 1) + b1] = sm.st_q[lane];
-        if (b1 == NT) p.cnt[(int64_t)lane * (LD + 1) + NT] = sm.st_q[lane];
+        const int LD = (int)k->ld;
+        k->cnt_fin[(int64_t)lane * (LD + 1) + b1] = sm.st_q[lane];
+        if (b1 == (int)k->NT) k->cnt[(int64_t)lane * (LD + 1) + b1] = sm.st_q[lane];
     }
     if (__ballot(err != 0u)) {
         unsigned e = err;
         for (int off = 32; off > 0; off >>= 1) e |= __shfl_xor(e, off);
-        if (lane == 0) atomicOr(&p.status->err, e);
+        if (lane == 0) atomicOr(&k->status->err, e);
     }
 }
 
