@@ -4,31 +4,42 @@
 // [t_j, t_{j+1}].  One wave (a 64-lane workgroup) owns one tile at a time and
 // walks a contiguous run of tiles, carrying one cursor per interval stream (the
 // number of that stream's interval endpoints at or before the tile's start).
-// Nothing inside a tile needs a workgroup barrier: lanes exchange data through
-// wave-private LDS and ballots, so many independent waves per CU hide each
-// other's memory and LDS latency.
+// Nothing needs a workgroup barrier: lanes exchange data through wave-private
+// LDS, ballots and DPP, so many independent waves per CU hide each other's
+// memory and LDS latency.
 //
 // Work inside a tile:
-//   samples   (lane k owns segments kC .. kC+C-1): segment energies
-//             S_j = (P_j + P_{j+1}) (t_{j+1} - t_j) / 2 and the input checks;
-//   endpoints (up to two per lane per round): the endpoint's segment (guessed
-//             from the mean sample spacing, then corrected), its sample index,
-//             its position in the time-merged order of all streams and the
-//             number of intervals active just after it -- both follow from how
-//             many endpoints of each other stream precede it, since a stream
-//             is inside an interval exactly when its cursor is odd;
-//   run sums  a segmented scan of S_j that restarts after every segment
-//             holding an endpoint (the energy of the whole segments between
-//             two consecutive endpoints);
-//   gaps      (one lane per gap between consecutive endpoints): the exact
-//             integral of the linear interpolant over the gap = trapezoid
-//             pieces at both ends + the run sum between, divided by the number
+//   samples   lane k owns segments kC .. kC+C-1: segment energies
+//             S_j = (P_j + P_{j+1}) (t_{j+1} - t_j) / 2, the input checks, and
+//             the tile-local prefix F_i = S_0 + ... + S_{i-1} (a per-lane
+//             running sum plus a DPP scan of the lane totals), staged in LDS
+//             with the samples;
+//   endpoints one lane per endpoint of the round: its segment j (guessed from
+//             the mean spacing, checked, binary search as the fallback), which
+//             is also its sample index; the interpolated power P^(x); the
+//             pieces of segment j left and right of x; its position in the
+//             time order of all streams (the number of endpoints of every
+//             stream that precede it, by searches of the streams' sorted
+//             windows) and the number of intervals active after it (a stream
+//             is inside an interval exactly when its cursor is odd);
+//   gaps      the lane of each endpoint integrates the gap from the endpoint
+//             before it in time order: within one segment the trapezoid of the
+//             two interpolated values; otherwise the right piece of the earlier
+//             endpoint + the whole segments between (a difference of two
+//             tile-local prefixes) + its own left piece; divided by the number
 //             of active intervals (equal split);
-//   intervals (one lane per interval starting in the round): the sum of its
-//             gaps.
-// Every energy is a sum of non-negative terms; no result is a difference of
-// running totals.  A tile whose endpoints overflow the per-stream window is
-// processed in several rounds, each a time prefix of the remaining endpoints.
+//   intervals the lane of each interval's start sums the gap values up to the
+//             interval's end.
+// Every energy is a sum of non-negative terms.  The one difference taken, of
+// two tile-local prefixes for the whole segments inside a gap, carries an
+// absolute error of at most about 31 u F (u the unit roundoff, F the prefix,
+// at most the tile's energy); when the difference is smaller than F / 2^14
+// the whole segments are summed directly instead, so the relative error of a
+// gap stays below 6e-11.
+//
+// A round takes at most 63 endpoints: every stream's endpoints in the tile
+// when they fit, otherwise a time prefix of them; one lane is left for the
+// gap from the round's last endpoint to the tile's end.
 //
 // Intervals whose endpoints lie in different tiles leave partial energies:
 // head[a][b], the piece in tile b of stream a's interval active at the tile's
@@ -42,19 +53,25 @@ namespace mag {
 namespace {
 
 constexpr int WAVE = 64;
+constexpr int C = SEG_PER_THREAD;
+constexpr int T = TILE;
+constexpr int NCOL = WAVE + 1;  // sample columns: the tile's last sample is row 0, column 64
+constexpr int WIN = 2 * WAVE;   // window entries, two per lane
+constexpr int SLOTS = WAVE - 1; // endpoints per round
+static_assert(T == WAVE * C && C == 8, "tile layout");
 
 __device__ __forceinline__ double endpoint_x(const double* s, const double* e, int64_t off,
                                              int64_t q)
 {
+    // endpoint q of a stream: even q = start of interval q/2, odd q = its end
     const int64_t i = off + (q >> 1);
     return (q & 1) ? e[i] : s[i];
 }
 
-// The kernel's arguments, read again from the kernel-argument segment where
-// they are used (scalar loads that hit the constant cache).  Loaded once at
-// entry, as the compiler does for a plain parameter, they would occupy scalar
-// registers for the whole kernel and spill.  The pointer is made opaque at
-// every call so that no load is shared between (or hoisted out of) phases.
+// the kernel's arguments, read from the kernel-argument segment where used
+// (scalar loads through the constant cache) so that pointers do not occupy
+// scalar registers for the whole kernel; opaque at every use so that no load
+// is hoisted out of a phase
 typedef const __attribute__((address_space(4))) TileParams* KArgs;
 __device__ __forceinline__ KArgs kargs()
 {
@@ -63,17 +80,9 @@ __device__ __forceinline__ KArgs kargs()
     return k;
 }
 
-// linear interpolant on [ta, tb] at x, exactly the sample values at the ends
-__device__ __forceinline__ double lerp_power(double ta, double tb, double pa, double pb, double x)
-{
-    if (x == ta) return pa;
-    if (x == tb) return pb;
-    return pa + (pb - pa) * ((x - ta) / (tb - ta));
-}
-
-// Lanes of one wave communicate through LDS without s_barrier: a wave's LDS
-// operations complete in program order, and these fences keep the compiler
-// from moving memory operations across the point.
+// lanes of one wave communicate through LDS without s_barrier: a wave's LDS
+// operations complete in program order; the fences keep the compiler from
+// moving memory operations across this point
 __device__ __forceinline__ void wave_sync()
 {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -84,7 +93,7 @@ __device__ __forceinline__ void wave_sync()
 // DPP lane moves (bound_ctrl: lanes without a source read 0)
 constexpr int DPP_ROW_SHR1 = 0x111, DPP_ROW_SHR2 = 0x112, DPP_ROW_SHR4 = 0x114,
               DPP_ROW_SHR8 = 0x118, DPP_ROW_BCAST15 = 0x142, DPP_ROW_BCAST31 = 0x143,
-              DPP_WAVE_SHR1 = 0x138;
+              DPP_WAVE_SHR1 = 0x138, DPP_WAVE_SHL1 = 0x130;
 
 template <int CTRL, int ROWS>
 __device__ __forceinline__ int dpp_i32(int v)
@@ -101,26 +110,22 @@ __device__ __forceinline__ double dpp_f64(double v)
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// one step of a segmented inclusive scan: (h, x) after (hy, y) is
-// (hy | h, h ? x : y + x); lanes without a source combine with (0, 0)
 template <int CTRL, int ROWS>
-__device__ __forceinline__ void seg_step(int& h, double& x)
+__device__ __forceinline__ float dpp_f32(float v)
 {
-    const int hy = dpp_i32<CTRL, ROWS>(h);
-    const double y = dpp_f64<CTRL, ROWS>(x);
-    x = h ? x : y + x;
-    h |= hy;
+    return __int_as_float(dpp_i32<CTRL, ROWS>(__float_as_int(v)));
 }
 
-// inclusive segmented scan over the 64 lanes: within rows of 16, then across rows
-__device__ __forceinline__ void seg_scan_wave(int& h, double& x)
+// inclusive scan of a non-negative double over the 64 lanes
+__device__ __forceinline__ double scan_wave(double x)
 {
-    seg_step<DPP_ROW_SHR1, 0xf>(h, x);
-    seg_step<DPP_ROW_SHR2, 0xf>(h, x);
-    seg_step<DPP_ROW_SHR4, 0xf>(h, x);
-    seg_step<DPP_ROW_SHR8, 0xf>(h, x);
-    seg_step<DPP_ROW_BCAST15, 0xa>(h, x);
-    seg_step<DPP_ROW_BCAST31, 0xc>(h, x);
+    x += dpp_f64<DPP_ROW_SHR1, 0xf>(x);
+    x += dpp_f64<DPP_ROW_SHR2, 0xf>(x);
+    x += dpp_f64<DPP_ROW_SHR4, 0xf>(x);
+    x += dpp_f64<DPP_ROW_SHR8, 0xf>(x);
+    x += dpp_f64<DPP_ROW_BCAST15, 0xa>(x);
+    x += dpp_f64<DPP_ROW_BCAST31, 0xc>(x);
+    return x;
 }
 
 __device__ __forceinline__ double wave_sum(double v)
@@ -129,70 +134,127 @@ __device__ __forceinline__ double wave_sum(double v)
     return v;
 }
 
+__device__ __forceinline__ double read_lane_f64(double v, int l)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, l);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), l);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// the smallest double above a finite x (so that y <= x  <=>  y < next_up(x))
+__device__ __forceinline__ double next_up(double x)
+{
+    const long long b = __double_as_longlong(x);
+    if (x == 0.0) return __longlong_as_double(1ll);
+    return __longlong_as_double(x > 0.0 ? b + 1 : b - 1);
+}
+
+// segment energy, one expression for every place that computes it
+__device__ __forceinline__ double seg_energy(double ta, double tb, float pa, float pb)
+{
+    return (((double)pa + (double)pb) * (tb - ta)) * 0.5;
+}
+
 }  // namespace
 
-// LDS of one wave (a workgroup holds WPB independent waves)
-template <int C, int SMAX>
-struct WaveLds {
-    static constexpr int T = WAVE * C;
-    static constexpr int E = WAVE;      // endpoints per round: one per lane
-    static constexpr int W = 2 * WAVE;  // window entries: two per lane
-    double sh_t[C + 1][WAVE];    // column k holds the C+1 samples of lane k's segments
-    float sh_P[C + 1][WAVE];
-    uint32_t flag[T / 32];       // segment holds a breakpoint of the round
-    int wp[T / 32 + 1];          // set flags in the words before each word
-    double R[E + 2];             // run sums, by rank of the breakpoint segment they end at
-    double ev_x[W];              // endpoint window, stream-major
-    double mg_x[E];              // merged endpoints
-    uint32_t mg_jm[E];           // segment | active-after << 16 | end flag << 31
-    double gv[E + 1];            // per-gap energy share
-    uint8_t ev_pos[E];           // merged position of a round slot
-    int64_t st_q[SMAX], st_off[SMAX], st_len[SMAX];
-    int st_take[SMAX], st_first[SMAX];  // endpoints taken this round; first round slot
-    int st_started[SMAX], nx_started[SMAX];
-    double st_acc[SMAX], nx_acc[SMAX];
-    double st_lastx[SMAX];       // the stream's last consumed endpoint
+// LDS of one wave
+template <int SP>
+struct TileLds {
+    double2 tF[C][NCOL];  // {t_i, F_i} of local sample i at [i % C][i / C]
+    float P[C][NCOL];
+    // endpoint window: stream a's entry r at a * WS + r; once the round's merged
+    // positions are known, wx[g] holds the value of gap g (ending at entry g):
+    // its energy per active interval
+    double wx[WIN];
+    // inv[p]: the lane holding the round's p-th endpoint in time order; before
+    // the merge (more than 8 streams), inv[l] marks the round slot l of a
+    // stream's first endpoint: (stream + 1) << 8 | l
+    int inv[WAVE];
 };
 
-template <int C, int SMAX, int WPB>
-__global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4))) void k_tile(
-    const TileParams p)
+namespace {
+
+__device__ __forceinline__ int bperm(int v, int src)
 {
-    using Lds = WaveLds<C, SMAX>;
-    constexpr int T = Lds::T;
-    constexpr int E = Lds::E;
-    constexpr int W = Lds::W;
-    constexpr int NWORD = T / 32;
-    static_assert((C & (C - 1)) == 0 && C >= 4 && NWORD <= WAVE && E <= 255, "tile layout");
+    return __builtin_amdgcn_ds_bpermute(src << 2, v);
+}
+__device__ __forceinline__ int64_t bperm64(int64_t v, int src)
+{
+    const uint32_t lo = (uint32_t)bperm((int)(uint32_t)v, src);
+    const uint32_t hi = (uint32_t)bperm((int)(uint32_t)((uint64_t)v >> 32), src);
+    return (int64_t)(((uint64_t)hi << 32) | lo);
+}
+__device__ __forceinline__ double bpermf(double v, int src)
+{
+    return __longlong_as_double(bperm64(__double_as_longlong(v), src));
+}
 
-    __shared__ Lds lds_all[WPB];
-    const int lane = threadIdx.x & (WAVE - 1);
-    const int wave = threadIdx.x / WAVE;
-    Lds& sm = lds_all[wave];
+// inclusive scans of non-negative ints over the 64 lanes
+__device__ __forceinline__ int scan_add_i32(int x)
+{
+    x += dpp_i32<DPP_ROW_SHR1, 0xf>(x);
+    x += dpp_i32<DPP_ROW_SHR2, 0xf>(x);
+    x += dpp_i32<DPP_ROW_SHR4, 0xf>(x);
+    x += dpp_i32<DPP_ROW_SHR8, 0xf>(x);
+    x += dpp_i32<DPP_ROW_BCAST15, 0xa>(x);
+    x += dpp_i32<DPP_ROW_BCAST31, 0xc>(x);
+    return x;
+}
+__device__ __forceinline__ int scan_max_i32(int x)
+{
+    x = max(x, dpp_i32<DPP_ROW_SHR1, 0xf>(x));
+    x = max(x, dpp_i32<DPP_ROW_SHR2, 0xf>(x));
+    x = max(x, dpp_i32<DPP_ROW_SHR4, 0xf>(x));
+    x = max(x, dpp_i32<DPP_ROW_SHR8, 0xf>(x));
+    x = max(x, dpp_i32<DPP_ROW_BCAST15, 0xa>(x));
+    x = max(x, dpp_i32<DPP_ROW_BCAST31, 0xc>(x));
+    return x;
+}
+__device__ __forceinline__ double wave_min(double v)
+{
+    for (int off = 32; off > 0; off >>= 1) v = fmin(v, __shfl_xor(v, off));
+    return v;
+}
+
+constexpr int log2_exact(int v) { return v <= 1 ? 0 : 1 + log2_exact(v >> 1); }
+
+}  // namespace
+
+// SP: the number of streams rounded up to a power of two (streams S .. SP-1
+// are treated as empty).  Lane a < SP holds stream a's state in registers.
+template <int SP>
+__global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
+{
+    constexpr int LSP = log2_exact(SP);
+    static_assert((1 << LSP) == SP && SP <= 32, "streams");
+    constexpr int LW = 7 - LSP;  // window entries per stream: WS = 2^LW
+    constexpr int WS = 1 << LW;
+    constexpr int B = (SLOTS >> LSP) > 0 ? (SLOTS >> LSP) : 1;  // per-stream share of a cut round
+    __shared__ TileLds<SP> sm;
+    const int lane = threadIdx.x;
     const int S = p.ss.S;
-    int lc = 0;  // window entries per stream: the largest power of two with S * cap <= W
-    while ((S << (lc + 1)) <= W) ++lc;
-    const int cap = 1 << lc;
-    const int nslot = S << lc;
-    const int budget = cap >> 1;  // per-stream share of the round slots when they run short
     // tile indices fit 32 bits (the host caps the trace length)
-    const int b0 = (int)p.tile_begin + ((int)blockIdx.x * WPB + wave) * (int)p.tiles_per_wg;
+    const int b0 = (int)p.tile_begin + (int)blockIdx.x * (int)p.tiles_per_wg;
     const int b1 = min(b0 + (int)p.tiles_per_wg, (int)p.tile_end);
-    if (b0 >= b1) return;  // uniform per wave; waves never wait for each other
+    if (b0 >= b1) return;
 
-    if (lane < S) {
-        sm.st_off[lane] = p.ss.off[lane];
-        sm.st_len[lane] = 2 * (p.ss.off[lane + 1] - p.ss.off[lane]);
-    }
-    if (lane < NWORD) sm.flag[lane] = 0u;
-    wave_sync();
+    // ---- stream lanes: offsets, lengths, cursors
+    const bool slane = lane < S;
+    const int64_t soff = slane ? p.ss.off[lane] : 0;
+    const int64_t slen = slane ? 2 * (p.ss.off[lane + 1] - p.ss.off[lane]) : 0;
+    int64_t sq = 0;            // endpoints of the stream consumed so far
+    double slastx = -INFINITY; // the stream's last consumed endpoint
+    double sacc = 0.0;         // this tile's energy of the stream's open interval so far
+    int sstarted = 0;          // the open interval started in this tile
     {
-        // cursor of each stream at the first tile: endpoints <= its start time
-        // (64-ary search, about four dependent loads per stream)
+        // cursor at the first tile: endpoints <= its start time (64-ary search,
+        // about four dependent loads per stream)
         const double tau0 = p.t[(int64_t)b0 * T - p.base];
         for (int a = 0; a < S; ++a) {
-            const int64_t off = sm.st_off[a];
-            int64_t lo = 0, hi = sm.st_len[a];
+            const int64_t off = p.ss.off[a];
+            const int64_t len = 2 * (p.ss.off[a + 1] - off);
+            int64_t lo = 0, hi = len;
             while (hi - lo > WAVE) {
                 const int64_t step = (hi - lo + WAVE - 1) / WAVE;
                 const int64_t pr = lo + (int64_t)(lane + 1) * step - 1;
@@ -206,87 +268,112 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
             const int64_t pr = lo + lane;
             const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, off, pr) <= tau0);
             const int c = __popcll(__ballot(ok));
-            if (lane == 0) {
-                const int64_t q = lo + c;
-                sm.st_q[a] = q;
-                sm.st_lastx[a] = (q > 0) ? endpoint_x(p.s, p.e, off, q - 1) : -INFINITY;
+            const int64_t q = lo + c;
+            if (lane == a) {
+                sq = q;
+                slastx = (q > 0) ? endpoint_x(p.s, p.e, off, q - 1) : -INFINITY;
             }
         }
     }
-    wave_sync();
 
-    // window slot of the stream cursors (advanced by each stream's take: the
-    // next tile's window)
-    auto window_x = [&](int slot, bool advance) -> double {
-        if (slot >= nslot) return INFINITY;
-        const int a = slot >> lc, r = slot & (cap - 1);
-        const int64_t q = sm.st_q[a] + (advance ? sm.st_take[a] : 0) + r;
+    // the lane's two window entries: stream, rank, and that stream's extent
+    const int wa0 = lane >> LW, wa1 = (lane + WAVE) >> LW;
+    const int wr0 = lane & (WS - 1), wr1 = (lane + WAVE) & (WS - 1);
+    const int64_t woff0 = bperm64(soff, wa0), wlen0 = bperm64(slen, wa0);
+    const int64_t woff1 = bperm64(soff, wa1), wlen1 = bperm64(slen, wa1);
+    // window entry of rank r from cursor cur (+inf past the stream's end); `more`:
+    // the last entry of the stream's window, with endpoints after it.  An entry
+    // past the end loads the first sample of this wave's first tile instead (an
+    // address every launch reads), so the load needs no branch.
+    auto wload = [&](int64_t cur, int r, int64_t off, int64_t len, bool& more) -> double {
+        const int64_t q = cur + r;
+        more = (r == WS - 1) && (q + 1 < len);
+        const bool ok = q < len;
         const KArgs k = kargs();
-        return (q < sm.st_len[a]) ? endpoint_x(k->s, k->e, sm.st_off[a], q) : INFINITY;
+        const double* ptr = ok ? (((q & 1) ? k->e : k->s) + off + (q >> 1))
+                               : k->t + ((int64_t)b0 * T - k->base);
+        const double v = *ptr;
+        return ok ? v : INFINITY;
     };
-    // breakpoint segments before segment j (the run sum ending at j-1 is R[rank(j)])
-    auto rank_of = [&](int j) -> int {
-        const int w = j >> 5;
-        return sm.wp[w] + __popc(sm.flag[w] & ((1u << (j & 31)) - 1u));
-    };
+    bool em0, em1;  // `more` flags of the prefetched window
+    double ew0 = wload(bperm64(sq, wa0), wr0, woff0, wlen0, em0);
+    double ew1 = wload(bperm64(sq, wa1), wr1, woff1, wlen1, em1);
 
-    double ew[2];  // prefetched window of the next tile
-    bool ew_ready = false;
-    unsigned err = 0u;
-    double w_acc = 0.0, idle = 0.0;  // this lane's share of the trace and idle energy
-
-    for (int b = b0; b < b1; ++b) {
-        // the lane index, opaque to the compiler within this tile: keeps per-lane
-        // 64-bit addresses from being hoisted out of the tile loop (where they
-        // would occupy registers for the whole kernel and spill)
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
+    // ---- samples of a tile into registers (lane k: local samples kC .. kC+C)
+    double tv[C + 1];
+    float pv[C + 1];
+    auto load_samples = [&](int b) {
+        const KArgs k = kargs();
         const int64_t j0 = (int64_t)b * T;
-        const int L = (int)min((int64_t)T, kargs()->nseg - j0);
-        const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
-
-        // ---- samples: load, stage, segment energies, checks
-        {
-            double tv[C + 1];
-            float pv[C + 1];
-            const KArgs k = kargs();
-            const double* tp = k->t;
-            const float* Pp = k->P;
-            const int64_t g = j0 + (int64_t)ln * C - k->base;
-            if (cs == C && k->aligned16) {
-                const double2* t2 = reinterpret_cast<const double2*>(tp + g);
-                const float4* P4 = reinterpret_cast<const float4*>(Pp + g);
+        const int L = (int)min((int64_t)T, k->nseg - j0);
+        const int64_t g = j0 + (int64_t)lane * C - k->base;
+        const double* tp = k->t;
+        const float* Pp = k->P;
+        if (L == T && k->aligned16) {
+            const double2* t2 = reinterpret_cast<const double2*>(tp + g);
+            const float4* P4 = reinterpret_cast<const float4*>(Pp + g);
 #pragma unroll
-                for (int u = 0; u < C / 2; ++u) {
-                    const double2 v = t2[u];
-                    tv[2 * u] = v.x;
-                    tv[2 * u + 1] = v.y;
-                }
+            for (int u = 0; u < C / 2; ++u) {
+                const double2 v = t2[u];
+                tv[2 * u] = v.x;
+                tv[2 * u + 1] = v.y;
+            }
 #pragma unroll
-                for (int u = 0; u < C / 4; ++u) {
-                    const float4 v = P4[u];
-                    pv[4 * u] = v.x;
-                    pv[4 * u + 1] = v.y;
-                    pv[4 * u + 2] = v.z;
-                    pv[4 * u + 3] = v.w;
-                }
+            for (int u = 0; u < C / 4; ++u) {
+                const float4 v = P4[u];
+                pv[4 * u] = v.x;
+                pv[4 * u + 1] = v.y;
+                pv[4 * u + 2] = v.z;
+                pv[4 * u + 3] = v.w;
+            }
+            // sample C of the lane is the next lane's first (lane 63: the tile's last)
+            if (lane == WAVE - 1) {
                 tv[C] = tp[g + C];
                 pv[C] = Pp[g + C];
             } else {
-                // a lane with fewer segments repeats its last sample time with
-                // zero power: the missing segments have zero width and energy
+                tv[C] = 0.0;
+                pv[C] = 0.0f;
+            }
+        } else {
+            // a lane past the tile's last sample repeats the last one it has
+            // with zero power: missing segments have zero width and energy
+            const int have = min(max(L - lane * C, -1), C);  // last local sample of the lane
 #pragma unroll
-                for (int u = 0; u <= C; ++u) {
-                    if (u <= cs && cs > 0) {
-                        tv[u] = tp[g + u];
-                        pv[u] = Pp[g + u];
-                    } else {
-                        tv[u] = (u > 0) ? tv[u - 1] : 0.0;
-                        pv[u] = 0.0f;
-                    }
+            for (int u = 0; u <= C; ++u) {
+                if (u <= have) {
+                    tv[u] = tp[g + u];
+                    pv[u] = Pp[g + u];
+                } else {
+                    tv[u] = (u > 0) ? tv[u - 1] : 0.0;
+                    pv[u] = 0.0f;
                 }
             }
-            if (k->validate) {
+        }
+    };
+
+    load_samples(b0);
+    unsigned err = 0u;
+    double idle = 0.0;    // this lane's share of the idle energy
+    double w_wave = 0.0;  // the wave's trace energy (uniform)
+
+    for (int b = b0; b < b1; ++b) {
+        const KArgs kk = kargs();
+        const int64_t j0 = (int64_t)b * T;
+        const int L = (int)min((int64_t)T, kk->nseg - j0);
+        const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
+
+        // ---- samples: checks, segment energies, tile-local prefix, staging
+        {
+            if (L == T && kk->aligned16) {
+                // sample C from the next lane (lane 63 loaded its own)
+                const double tn = dpp_f64<DPP_WAVE_SHL1, 0xf>(tv[0]);
+                const float pn = dpp_f32<DPP_WAVE_SHL1, 0xf>(pv[0]);
+                if (lane != WAVE - 1) {
+                    tv[C] = tn;
+                    pv[C] = pn;
+                }
+            }
+            if (kk->validate) {
                 // every segment of the lane rises (the repeated last time of a
                 // short lane does not), and a strictly increasing run whose ends
                 // are finite is finite throughout (a NaN fails every comparison)
@@ -300,418 +387,331 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
                 for (int u = 0; u <= C; ++u) p_ok &= (pv[u] >= 0.0f) & (pv[u] < INFINITY);
                 err |= (t_ok ? 0u : ERR_TIMESTAMPS) | (p_ok ? 0u : ERR_POWER);
             }
-#pragma unroll
-            for (int u = 0; u <= C; ++u) {
-                sm.sh_t[u][lane] = tv[u];
-                sm.sh_P[u][lane] = pv[u];
-            }
-            // segment energies (P_u + P_{u+1}) (t_{u+1} - t_u), halved once at the end
-            double wl = 0.0;
+            double f[C + 1];
+            f[0] = 0.0;
 #pragma unroll
             for (int u = 0; u < C; ++u)
-                wl += ((double)pv[u] + (double)pv[u + 1]) * (tv[u + 1] - tv[u]);
-            w_acc += 0.5 * wl;
-            // computed here, while the samples are in registers (not sunk to the
-            // end of the tile, which would keep them live through the rounds)
-            asm volatile("" : "+v"(w_acc));
+                f[u + 1] = f[u] + seg_energy(tv[u], tv[u + 1], pv[u], pv[u + 1]);
+            const double incl = scan_wave(f[C]);
+            // F at the lane's first sample: the exclusive scan (lane 0 reads 0)
+            const double base = dpp_f64<DPP_WAVE_SHR1, 0xf>(incl);
+#pragma unroll
+            for (int u = 0; u < C; ++u) {
+                sm.tF[u][lane] = make_double2(tv[u], base + f[u]);
+                sm.P[u][lane] = pv[u];
+            }
+            const double Wt = read_lane_f64(incl, WAVE - 1);
+            if (lane == WAVE - 1) {
+                sm.tF[0][WAVE] = make_double2(tv[C], Wt);
+                sm.P[0][WAVE] = pv[C];
+            }
+            w_wave += Wt;
         }
-        if (lane < S) {
+        // samples of the next tile (in flight during this tile's rounds)
+        if (b + 1 < b1) load_samples(b + 1);
+        if (slane) {
             const KArgs k = kargs();
-            k->cnt[(int64_t)ln * (k->ld + 1) + b] = sm.st_q[lane];
-            sm.st_acc[lane] = 0.0;
-            sm.st_started[lane] = 0;
+            k->cnt[(int64_t)lane * (k->ld + 1) + b] = sq;
         }
+        sacc = 0.0;
+        sstarted = 0;
         wave_sync();
-
-        // sample time / power of tile index j in [0, L]
-        auto t_at = [&](int j) -> double {
-            const int u = j & (C - 1), k = j / C;
-            return (u == 0 && k > 0) ? sm.sh_t[C][k - 1] : sm.sh_t[u][k];
-        };
-        auto P_at = [&](int j) -> double {
-            const int u = j & (C - 1), k = j / C;
-            return (double)((u == 0 && k > 0) ? sm.sh_P[C][k - 1] : sm.sh_P[u][k]);
-        };
-
-        const double t_begin = sm.sh_t[0][0];
+        auto tF_at = [&](int i) -> double2 { return sm.tF[i & (C - 1)][i >> 3]; };
+        auto t_at = [&](int i) -> double { return sm.tF[i & (C - 1)][i >> 3].x; };
+        auto P_at = [&](int i) -> double { return (double)sm.P[i & (C - 1)][i >> 3]; };
+        const double t_begin = t_at(0);
         const double tau_end = t_at(L);
         const double inv_dt = (double)L / (tau_end - t_begin);
-        double rs_x = t_begin;  // where the round's first gap starts
-        int rs_j = -1;          // its segment (-1: the tile's first sample)
+        // the point the round starts from (uniform): the tile's first sample,
+        // later the previous round's last endpoint -- x, the piece from x to the
+        // end of its segment, F at that end, (segment + 1) | active after << 16
+        double rs_x = t_begin, rs_right = 0.0, rs_Fn = 0.0;
+        int rs_jm = __popcll(__ballot((sq & 1) != 0)) << 16;
 
         for (;;) {
-            // ---- endpoint window of this round: entry = stream * cap + rank
-            double xw[2];
-            uint64_t in[2];
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-                xw[v] = ew_ready ? ew[v] : window_x(lane + WAVE * v, false);
-                sm.ev_x[lane + WAVE * v] = xw[v];
-                in[v] = __ballot(xw[v] <= tau_end);
-            }
-            ew_ready = false;
-            wave_sync();
-            // each stream's endpoints in the tile are a prefix of its (sorted)
-            // window.  If they all fit the round's slots they are all taken;
-            // otherwise every stream keeps at most `budget` and the round ends at
-            // the earliest time a stream runs out of its share (a time prefix)
-            // stream a's entries are bits [a cap, (a + 1) cap) of the 128-bit mask
-            auto count_in = [&](const uint64_t* m, int a) -> int {
-                if (cap > WAVE) return __popcll(m[0]) + __popcll(m[1]);  // one stream
-                if (cap == WAVE) return __popcll(m[a]);                     // two streams
-                const int b0 = a << lc;
-                const uint64_t w = (b0 >= WAVE) ? m[1] : m[0];
-                return __popcll((w >> (b0 & (WAVE - 1))) & ((1ull << cap) - 1ull));
+            // ---- the round's endpoints: a prefix of every stream's window
+            const double xw0 = ew0, xw1 = ew1;
+            sm.wx[lane] = xw0;
+            sm.wx[lane + WAVE] = xw1;
+            if (SP > 8) sm.inv[lane] = 0;  // no slot marked
+            const uint64_t in0 = __ballot(xw0 <= tau_end), in1 = __ballot(xw1 <= tau_end);
+            const uint64_t mo0 = __ballot(em0), mo1 = __ballot(em1);
+            const int tot = __popcll(in0) + __popcll(in1);
+            // stream lane a: its entries are bits [a WS, (a + 1) WS) of a 128-bit mask
+            auto sbits = [&](uint64_t m0w, uint64_t m1w) -> int {
+                if (WS == 2 * WAVE) return __popcll(m0w) + __popcll(m1w);
+                const uint64_t w = (lane * WS >= WAVE) ? m1w : m0w;
+                if (WS == WAVE) return __popcll(w);
+                return __popcll((w >> ((lane * WS) & (WAVE - 1))) & ((1ull << (WS & 63)) - 1ull));
             };
-            int tot = 0;
-            bool over = false;
-            for (int a = 0; a < S; ++a) {
-                const int ka = count_in(in, a);
-                tot += ka;
-                if (ka == cap && sm.st_q[a] + cap < sm.st_len[a]) over = true;
-            }
-            double cut = INFINITY;
-            bool fin = true;
-            if (over || tot > E) {
-                for (int a = 0; a < S; ++a) {
-                    if (count_in(in, a) > budget) {
-                        fin = false;
-                        cut = fmin(cut, sm.ev_x[(a << lc) + budget - 1]);
-                    }
-                }
-            }
-            uint64_t tk[2];
-#pragma unroll
-            for (int v = 0; v < 2; ++v) tk[v] = fin ? in[v] : (in[v] & __ballot(xw[v] <= cut));
-            int Er = 0, m0 = 0;
-            for (int a = 0; a < S; ++a) {
-                int ta = count_in(tk, a);
-                if (!fin) ta = min(ta, budget);  // endpoints equal to the cut may wait
-                if (lane == 0) {
-                    sm.st_take[a] = ta;
-                    sm.st_first[a] = Er;
-                }
-                Er += ta;
-                m0 += (int)(sm.st_q[a] & 1);
-            }
-            if (!fin && Er == 0) {
-                // only with unsorted endpoints: force progress, report
-                for (int a = 0; a < S; ++a) {
-                    if (count_in(in, a) > budget) {
-                        if (lane == 0) {
-                            sm.st_take[a] = 1;
-                            for (int a2 = 0; a2 < S; ++a2) sm.st_first[a2] = (a2 > a) ? 1 : 0;
-                        }
-                        Er = 1;
-                        break;
-                    }
-                }
-                err |= ERR_INTERVAL;
-            }
-            // the round's start is a breakpoint too: runs restart after it
-            if (lane == 0 && rs_j >= 0) atomicOr(&sm.flag[rs_j >> 5], 1u << (rs_j & 31));
+            const int ka = (lane < SP) ? sbits(in0, in1) : 0;
+            const bool smore = (lane < SP) && (sbits(mo0, mo1) != 0);
+            const bool over = __ballot(ka == WS && smore) != 0ull;
+            const bool fin = !over && tot <= SLOTS;
             wave_sync();
-
-            // prefetch the next tile's window (its cursors are known now)
-            if (fin && b + 1 < b1) {
+            int ta = ka;
+            if (!fin) {
+                // time prefix: each stream keeps at most B endpoints; the round
+                // ends at the earliest time a stream runs out of its share
+                const double cv = sm.wx[(min(lane, SP - 1) << LW) + B - 1];
+                const double cut = wave_min((lane < SP && ka > B) ? cv : INFINITY);
+                const uint64_t tk0 = in0 & __ballot(xw0 <= cut);
+                const uint64_t tk1 = in1 & __ballot(xw1 <= cut);
+                ta = (lane < SP) ? min(sbits(tk0, tk1), B) : 0;  // endpoints equal to the cut may wait
+                if (__ballot(ta > 0) == 0ull) {
+                    // only with unsorted or non-finite endpoints: force progress
+                    ta = min(ka, B);
+                    err |= ERR_INTERVAL;
+                }
+            }
+            const int incl = scan_add_i32(ta);
+            const int fa = incl - ta;
+            const int Er = __builtin_amdgcn_readlane(incl, WAVE - 1);
+            const int G = Er + (fin ? 1 : 0);  // gaps of the round
+            int top = 1;  // smallest power of two >= every stream's take
 #pragma unroll
-                for (int v = 0; v < 2; ++v) ew[v] = window_x(lane + WAVE * v, true);
-                ew_ready = true;
+            for (int v = 1; v < WS; v <<= 1)
+                if (__ballot(ta > v) != 0ull) top = v << 1;
+            if (SP > 8 && lane < SP && ta > 0) sm.inv[fa] = ((lane + 1) << 8) | fa;
+            wave_sync();
+            // the next round's window (this tile's next round, or the next
+            // tile's first): both start at the cursors after this round
+            const int64_t sqn = sq + ta;
+            if (!fin || b + 1 < b1) {
+                ew0 = wload(bperm64(sqn, wa0), wr0, woff0, wlen0, em0);
+                ew1 = wload(bperm64(sqn, wa1), wr1, woff1, wlen1, em1);
             }
 
-            // round slot of this lane: stream a (the last with first[a] <= lane), rank r
-            int my_a = -1, my_r = 0;
-            if (lane < Er) {
-                my_a = 0;
-                for (int a = 1; a < S; ++a)
-                    if (sm.st_first[a] <= lane) my_a = a;
-                my_r = lane - sm.st_first[my_a];
+            // ---- round slot of this lane: stream my_a, rank my_r (lane Er: the tile's end)
+            const bool real = lane < Er;
+            const bool pend = fin && lane == Er;
+            const bool has_gap = real || pend;
+            int my_a = 0, my_r = 0;
+            if (SP <= 8) {
+                // the stream of slot l is the last one whose first slot is <= l
+                int a_l = 0, f_l = 0;
+#pragma unroll
+                for (int a = 1; a < SP; ++a) {
+                    const int f = __builtin_amdgcn_readlane(fa, a);
+                    const bool in = f <= lane;
+                    a_l += in ? 1 : 0;
+                    f_l = in ? f : f_l;
+                }
+                if (real) {
+                    my_a = a_l;
+                    my_r = lane - f_l;
+                }
+            } else {
+                // each stream marked its first slot; a max-scan spreads the marks
+                const int mkv = scan_max_i32(sm.inv[lane]);
+                if (real) {
+                    my_a = (mkv >> 8) - 1;
+                    my_r = lane - (mkv & 255);
+                }
             }
-            const double my_x = (my_a >= 0) ? sm.ev_x[(my_a << lc) + my_r] : 0.0;
+            const int64_t q = bperm64(sq, my_a) + my_r;
+            const int64_t off_a = bperm64(soff, my_a);
+            const int ta_a = bperm(ta, my_a);
+            const double acc_a = bpermf(sacc, my_a);
+            const int st_a = bperm(sstarted, my_a);
+            const double lx_a = bpermf(slastx, my_a);
+            const uint64_t qpar = __ballot(lane < SP && (sq & 1));
+            const double x = real ? sm.wx[(my_a << LW) + my_r] : tau_end;
+            const double xp = (my_r > 0) ? sm.wx[(my_a << LW) + max(my_r - 1, 0)] : lx_a;
 
-            // ---- endpoints, part 1: segment, sample index, checks, breakpoint flag
-            int my_j = -1;
-            if (my_a >= 0) {
-                const int a = my_a, r = my_r;
-                const double x = my_x;
-                const int64_t q = sm.st_q[a] + r;
-                // segment j with t_j < x <= t_{j+1}: guess from the mean spacing, correct
-                int j = (int)fmin(fmax((x - t_begin) * inv_dt, 0.0), (double)(L - 1));
-                int steps = 0;
-                while (j > 0 && t_at(j) >= x && steps < 8) {
-                    --j;
-                    ++steps;
-                }
-                while (j < L - 1 && t_at(j + 1) < x && steps < 16) {
-                    ++j;
-                    ++steps;
-                }
-                if ((t_at(j) >= x && j > 0) || (j < L - 1 && t_at(j + 1) < x)) {
-                    int lo = 0, hi = L;  // first sample index >= x
+            // ---- segment j: t_j < x <= t_{j+1}; sample index j0 + j + 1
+            int j;
+            {
+                const int jg = (int)fmin(fmax((x - t_begin) * inv_dt, 0.0), (double)(L - 1));
+                const int c0 = max(0, min(jg - 1, L - 3));
+                const double u0 = t_at(c0), u1 = t_at(min(c0 + 1, L)), u2 = t_at(min(c0 + 2, L)),
+                             u3 = t_at(min(c0 + 3, L));
+                j = (u0 < x && x <= u1) ? c0
+                  : (c0 + 1 < L && u1 < x && x <= u2) ? c0 + 1
+                  : (c0 + 2 < L && u2 < x && x <= u3) ? c0 + 2 : -1;
+                if (!real) j = L;
+            }
+            if (__ballot(j < 0) != 0ull) {
+                if (j < 0) {
+                    // first sample index >= x (x > t_0 of the tile for sorted input)
+                    int lo = 0, hi = L;
                     while (lo < hi) {
                         const int mid = (lo + hi) >> 1;
                         if (t_at(mid) < x) lo = mid + 1; else hi = mid;
                     }
                     j = min(max(lo, 1), L) - 1;
                 }
-                my_j = j;
-                const int64_t gid = sm.st_off[a] + (q >> 1);
+            }
+            const double2 A0 = tF_at(j), A1 = tF_at(min(j + 1, L));
+            const double pj = P_at(j), pj1 = P_at(min(j + 1, L));
+            // interpolated power and the pieces of segment j left and right of x
+            const double rh = 1.0 / (A1.x - A0.x);
+            auto lerp = [&](double y) -> double {
+                return (y == A1.x) ? pj1 : pj + (pj1 - pj) * ((y - A0.x) * rh);
+            };
+            const double ph = real ? lerp(x) : pj;
+            const double left = real ? ((pj + ph) * (x - A0.x)) * 0.5 : 0.0;
+            const double right = real ? ((ph + pj1) * (A1.x - x)) * 0.5 : 0.0;
+            const double Fj = A0.y;  // prefix at the start of segment j (the tile's end: F_L)
+
+            const int64_t gid = off_a + (q >> 1);
+            if (real) {
                 const KArgs k = kargs();
                 int64_t* idx = (q & 1) ? k->end_idx : k->start_idx;
                 if (idx) idx[gid] = j0 + j + 1;
-                if (k->validate) {
-                    // finite and not before the stream's previous endpoint
-                    const double xp = (r > 0) ? sm.ev_x[(a << lc) + r - 1] : sm.st_lastx[a];
-                    if (!(fabs(x) < INFINITY) || !(xp <= x)) err |= ERR_INTERVAL;
-                }
-                atomicOr(&sm.flag[j >> 5], 1u << (j & 31));
             }
-            wave_sync();
-            // set flags in the words before each word (ranks of breakpoint segments)
-            if (lane < NWORD) {
-                int c = __popc(sm.flag[lane]);
-                for (int off = 1; off < NWORD; off <<= 1) {
-                    const int y = __shfl_up(c, off);
-                    if (lane >= off) c += y;
+            // finite and not before the stream's previous endpoint
+            if (real && kk->validate && (!(fabs(x) < INFINITY) || !(xp <= x))) err |= ERR_INTERVAL;
+
+            // ---- merged position and the number of intervals active after x
+            int pos = lane;
+            int m_after = (int)((q + 1) & 1);
+            if constexpr (SP > 1) {
+                // endpoints of every other stream before x (ties: the lower stream
+                // first): binary searches of the sorted windows, run side by side
+                const double xu = next_up(x);
+                constexpr int NO = SP > 1 ? SP - 1 : 1;  // other streams
+                int c[NO], wb[NO], tb[NO];
+                double thr[NO];
+#pragma unroll
+                for (int d = 0; d < SP - 1; ++d) {
+                    const int bs = (my_a + d + 1) & (SP - 1);
+                    tb[d] = bperm(ta, bs);
+                    thr[d] = (bs < my_a) ? xu : x;
+                    wb[d] = bs << LW;
+                    c[d] = 0;
                 }
-                sm.wp[lane + 1] = c;
-                if (lane == 0) sm.wp[0] = 0;
+#pragma unroll
+                for (int step = WS / 2; step > 0; step >>= 1) {
+                    if (step < top) {
+#pragma unroll
+                        for (int d = 0; d < SP - 1; ++d)
+                            c[d] += (sm.wx[wb[d] + c[d] + step - 1] < thr[d]) ? step : 0;
+                    }
+                }
+                int ps = my_r;
+#pragma unroll
+                for (int d = 0; d < SP - 1; ++d) {
+                    const int bs = (my_a + d + 1) & (SP - 1);
+                    const int cc = min(c[d] + ((sm.wx[wb[d] + c[d]] < thr[d]) ? 1 : 0), tb[d]);
+                    ps += cc;
+                    m_after += (int)(((qpar >> bs) + (uint64_t)cc) & 1ull);
+                }
+                if (real) pos = ps;
             }
+            const int jm = (j + 1) | (m_after << 16);
+            if (has_gap) sm.inv[pos] = lane;
             wave_sync();
 
-            // ---- run sums: segmented scan of whole-segment energies (recomputed
-            // from the staged samples, bit for bit as above), restarting after
-            // every breakpoint segment (whose energy is cut into pieces at its
-            // breakpoints instead).  The run ending just before breakpoint
-            // segment j (or before the tile's last segment) is stored at rank(j).
+            // ---- gap ending at this lane's entry (from the entry before it)
+            double v;
             {
-                const int j0l = lane * C;
-                const uint32_t myflags = (sm.flag[j0l >> 5] >> (j0l & 31)) & ((1u << C) - 1u);
-                const uint32_t nextflags =
-                    (j0l + C < T) ? ((sm.flag[(j0l + C) >> 5] >> ((j0l + C) & 31)) & 1u) : 0u;
-                const bool prev_lane_last =
-                    lane > 0 && ((sm.flag[(j0l - 1) >> 5] >> ((j0l - 1) & 31)) & 1u);
-                double loc[C];
-                double run = 0.0;
-                bool reset = false;
-#pragma unroll
-                for (int u = 0; u < C; ++u) {
-                    const bool prev_flag = (u == 0) ? prev_lane_last : ((myflags >> (u - 1)) & 1u);
-                    const bool self_flag = (myflags >> u) & 1u;
-                    const double v =
-                        (self_flag || u >= cs)
-                            ? 0.0
-                            : 0.5 * ((double)sm.sh_P[u][lane] + (double)sm.sh_P[u + 1][lane]) *
-                                  (sm.sh_t[u + 1][lane] - sm.sh_t[u][lane]);
-                    if (prev_flag) {
-                        run = v;
-                        reset = true;
-                    } else {
-                        run += v;
+                // the entry before: another lane's (read across lanes), or the
+                // round's starting point
+                const int pl = sm.inv[max(pos - 1, 0)];
+                const double px = bpermf(x, pl), pr = bpermf(right, pl), pF = bpermf(A1.y, pl);
+                const int pjm = bperm(jm, pl);
+                const bool head_gap = (pos == 0);
+                const double xpv = head_gap ? rs_x : px;
+                const double pright = head_gap ? rs_right : pr;
+                const double pFn = head_gap ? rs_Fn : pF;
+                const int pe = head_gap ? rs_jm : pjm;
+                const int pjx = (pe & 0xffff) - 1;  // segment of the entry before
+                const bool same = (pjx == j);
+                // both in segment j: the trapezoid of the two interpolated values
+                const double q_in = ((lerp(xpv) + ph) * (x - xpv)) * 0.5;
+                double whole = fmax(Fj - pFn, 0.0);
+                const bool ill = has_gap && !same && (j >= pjx + 2) && (whole < Fj * 0x1p-14);
+                if (__ballot(ill) != 0ull) {
+                    if (ill) {
+                        // the whole segments summed directly
+                        double sum = 0.0;
+                        for (int i = pjx + 1; i < j; ++i)
+                            sum += seg_energy(t_at(i), t_at(i + 1), sm.P[i & 7][i >> 3],
+                                              sm.P[(i + 1) & 7][(i + 1) >> 3]);
+                        whole = sum;
                     }
-                    loc[u] = run;
                 }
-                // the lanes' carries (reset flag, value): inclusive segmented
-                // scan across the wave, then shifted by one lane
-                int h = reset ? 1 : 0;
-                double xs = run;
-                seg_scan_wave(h, xs);
-                const double cin = dpp_f64<DPP_WAVE_SHR1, 0xf>(xs);
-                bool seen = false;
-                const uint32_t fl = myflags | (nextflags << C);
-                const int rbase = rank_of(j0l);  // breakpoint segments before this lane's
-#pragma unroll
-                for (int u = 0; u < C; ++u) {
-                    const bool prev_flag = (u == 0) ? prev_lane_last : ((myflags >> (u - 1)) & 1u);
-                    if (prev_flag) seen = true;
-                    const int k = j0l + u;  // this run value ends at segment k
-                    const bool nxt = ((fl >> (u + 1)) & 1u) != 0;
-                    if (k + 1 < L && (nxt || (k + 1 == L - 1)))
-                        sm.R[rbase + __popc(myflags & ((2u << u) - 1u))] =
-                            seen ? loc[u] : cin + loc[u];
-                }
+                const double Q = same ? q_in : (pright + whole) + left;
+                const int mp = pe >> 16;
+                v = (has_gap && mp > 0) ? (kk->split ? Q / (double)mp : Q) : 0.0;
+                idle += (has_gap && mp == 0) ? Q : 0.0;
+                if (has_gap) sm.wx[pos] = v;
             }
+            wave_sync();
 
-            // ---- endpoints, part 2: merged position and the intervals active after
+            // ---- interval energies: intervals starting in the round sum their
+            // gaps; the interval a stream carried into the round ends at its first
+            const int pos_next = dpp_i32<DPP_WAVE_SHL1, 0xf>(pos);
+            const bool start = real && !(q & 1);
+            const bool closes = start && (my_r + 1 < ta_a);
+            const bool carried = real && (q & 1) && my_r == 0;
+            const int lo = start ? pos + 1 : 0;
+            const int hi = start ? (closes ? pos_next : G - 1) : (carried ? pos : -1);
+            double acc = 0.0;
+            for (int i = 0; __ballot(lo + i <= hi) != 0ull; i += 2) {
+                const double y0 = sm.wx[min(lo + i, WAVE - 1)];
+                const double y1 = sm.wx[min(lo + i + 1, WAVE - 1)];
+                acc += (lo + i <= hi) ? y0 : 0.0;
+                acc += (lo + i + 1 <= hi) ? y1 : 0.0;
+            }
+            if (closes || carried) {
+                const KArgs k = kargs();
+                double* dst = (carried && !st_a) ? (k->head + (int64_t)my_a * k->ld + b)
+                                                 : (k->energy + gid);
+                *dst = carried ? acc_a + acc : acc;
+            }
+            // energy per active interval over the whole round (streams that stay
+            // inside one interval through it)
+            double vall = 0.0;
+            if (__ballot(lane < SP && ta == 0 && (sq & 1)) != 0ull) vall = wave_sum(v);
+            // the round's last entry is where the next round starts
+            if (!fin) {
+                const int ll = __builtin_amdgcn_readfirstlane(sm.inv[Er - 1]);
+                rs_x = read_lane_f64(x, ll);
+                rs_right = read_lane_f64(right, ll);
+                rs_Fn = read_lane_f64(A1.y, ll);
+                rs_jm = __builtin_amdgcn_readlane(jm, ll);
+            }
+            // ---- commit the round (stream lanes)
             {
-                int take[SMAX];
-                int qpar[SMAX];
-#pragma unroll
-                for (int a2 = 0; a2 < SMAX; ++a2) {
-                    take[a2] = (a2 < S) ? sm.st_take[a2] : 0;
-                    qpar[a2] = (a2 < S) ? (int)(sm.st_q[a2] & 1) : 0;
+                const int last = max(fa + ta - 1, 0);  // round slot of the stream's last endpoint
+                const double acc_l = bpermf(acc, last);
+                const double x_l = bpermf(x, last);
+                const bool open = (sqn & 1) != 0;
+                if (ta > 0) {
+                    sacc = open ? acc_l : 0.0;
+                    sstarted = open ? 1 : 0;
+                    slastx = x_l;
+                } else if (sq & 1) {
+                    sacc += vall;
                 }
-                if (my_j >= 0) {
-                    const double x = my_x;
-                    const int a = my_a, r = my_r;
-                    const int q0 = (int)(sm.st_q[a] & 1);
-                    // endpoints of each other stream before x in the merged order
-                    // (ties: lower stream first); entries past a stream's take lie
-                    // after x, so fixed-depth searches of the whole window suffice
-                    int pos = r;
-                    int m_after = (q0 + r + 1) & 1;
-                    int c[SMAX];
-#pragma unroll
-                    for (int a2 = 0; a2 < SMAX; ++a2) c[a2] = 0;
-                    // (straight-line: every lane runs every step of every search)
-                    for (int step = cap >> 1; step > 0; step >>= 1) {
-#pragma unroll
-                        for (int a2 = 0; a2 < SMAX; ++a2) {
-                            const double y = sm.ev_x[(min(a2, S - 1) << lc) + c[a2] + step - 1];
-                            const bool pr = (y < x) | ((a2 < a) & (y == x));
-                            c[a2] += pr ? step : 0;
-                        }
-                    }
-#pragma unroll
-                    for (int a2 = 0; a2 < SMAX; ++a2) {
-                        const double y = sm.ev_x[(min(a2, S - 1) << lc) + c[a2]];
-                        const bool pr = (y < x) | ((a2 < a) & (y == x));
-                        const int ca = min(c[a2] + (pr ? 1 : 0), take[a2]);
-                        const bool other = (a2 < S) & (a2 != a);
-                        pos += other ? ca : 0;
-                        m_after += other ? ((qpar[a2] + ca) & 1) : 0;
-                    }
-                    pos = min(pos, Er - 1);
-                    const int64_t q = sm.st_q[a] + r;
-                    sm.ev_pos[lane] = (uint8_t)pos;
-                    sm.mg_x[pos] = x;
-                    sm.mg_jm[pos] = (uint32_t)my_j | ((uint32_t)m_after << 16) |
-                                    ((q & 1) ? 0x80000000u : 0u);
-                }
+                sq = sqn;
             }
-            wave_sync();
-
-            // ---- gap energies, split among the active intervals
-            const int G = Er + (fin ? 1 : 0);
-            for (int g = lane; g < G; g += WAVE) {
-                double xs, xe;
-                int js, je, m;
-                if (g == 0) {
-                    xs = rs_x;
-                    js = rs_j;
-                    m = m0;
-                } else {
-                    const uint32_t w = sm.mg_jm[g - 1];
-                    xs = sm.mg_x[g - 1];
-                    js = min((int)(w & 0xffffu), L - 1);
-                    m = (int)((w >> 16) & 0x7fffu);
-                }
-                if (g < Er) {
-                    xe = sm.mg_x[g];
-                    je = min((int)(sm.mg_jm[g] & 0xffffu), L - 1);
-                } else {
-                    xe = tau_end;
-                    je = L - 1;
-                }
-                // trapezoids of the interpolant: within one segment, or the piece to
-                // the end of the first segment + whole segments + the piece from the
-                // start of the last (straight-line code: both forms are evaluated)
-                const int js0 = max(js, 0);
-                const double ta_s = t_at(js0), tb_s = t_at(js0 + 1);
-                const double pa_s = P_at(js0), pb_s = P_at(js0 + 1);
-                const double ta_e = t_at(je), tb_e = t_at(je + 1);
-                const double pa_e = P_at(je), pb_e = P_at(je + 1);
-                const double px_s = lerp_power(ta_s, tb_s, pa_s, pb_s, xs);
-                const double px_e = lerp_power(ta_e, tb_e, pa_e, pb_e, xe);
-                const double q_in = 0.5 * (px_s + px_e) * (xe - xs);
-                const double q_first = (js >= 0) ? 0.5 * (px_s + pb_s) * (tb_s - xs) : 0.0;
-                const double q_mid = (je > js + 1) ? sm.R[rank_of(je)] : 0.0;
-                const double q_last = 0.5 * (pa_e + px_e) * (xe - ta_e);
-                const double Q = (js == je) ? q_in : (q_first + q_mid) + q_last;
-                const double v = (m > 0) ? (kargs()->split ? Q / (double)m : Q) : 0.0;
-                idle += (m > 0) ? 0.0 : Q;
-                sm.gv[g] = v;
-            }
-            wave_sync();
-
-            // ---- interval energies: intervals starting in this round
-            if (my_j >= 0 && !((sm.st_q[my_a] + my_r) & 1)) {
-                const int a = my_a, r = my_r;
-                const int64_t q = sm.st_q[a] + r;
-                const int ta = sm.st_take[a];
-                const int ps = sm.ev_pos[lane];
-                double acc = 0.0;
-                if (r + 1 < ta) {
-                    const int pe = min((int)sm.ev_pos[lane + 1], G - 1);
-                    for (int g = ps + 1; g <= pe; ++g) acc += sm.gv[g];
-                    kargs()->energy[sm.st_off[a] + (q >> 1)] = acc;
-                } else {
-                    for (int g = ps + 1; g < G; ++g) acc += sm.gv[g];
-                    sm.nx_acc[a] = acc;
-                    sm.nx_started[a] = 1;
-                }
-            }
-            // the interval each stream carried into this round
-            if (lane < S) {
-                const int a = lane;
-                const int ta = sm.st_take[a];
-                const bool active = (sm.st_q[a] & 1) != 0;
-                const bool ends_open = ((sm.st_q[a] + ta) & 1) != 0;
-                if (active) {
-                    double acc = 0.0;
-                    if (ta > 0) {
-                        const int pe = min((int)sm.ev_pos[sm.st_first[a]], G - 1);
-                        for (int g = 0; g <= pe; ++g) acc += sm.gv[g];
-                        const double Et = sm.st_acc[a] + acc;
-                        const KArgs k = kargs();
-                        if (sm.st_started[a])
-                            k->energy[sm.st_off[a] + (sm.st_q[a] >> 1)] = Et;
-                        else
-                            k->head[(int64_t)(a + ln - lane) * k->ld + b] = Et;
-                        if (!ends_open) {
-                            sm.nx_acc[a] = 0.0;
-                            sm.nx_started[a] = 0;
-                        }
-                    } else {
-                        for (int g = 0; g < G; ++g) acc += sm.gv[g];
-                        sm.nx_acc[a] = sm.st_acc[a] + acc;
-                        sm.nx_started[a] = sm.st_started[a];
-                    }
-                } else if (!ends_open) {
-                    sm.nx_acc[a] = 0.0;
-                    sm.nx_started[a] = 0;
-                }
-            }
-            if (Er > 0) {
-                rs_x = sm.mg_x[Er - 1];
-                rs_j = min((int)(sm.mg_jm[Er - 1] & 0xffffu), L - 1);
-            }
-            wave_sync();
-            // commit the round; clear the breakpoint flags
-            if (lane < S) {
-                const int ta = sm.st_take[lane];
-                if (ta > 0) sm.st_lastx[lane] = sm.ev_x[(lane << lc) + ta - 1];
-                sm.st_q[lane] += ta;
-                sm.st_acc[lane] = sm.nx_acc[lane];
-                sm.st_started[lane] = sm.nx_started[lane];
-            }
-            if (lane < NWORD) sm.flag[lane] = 0u;
             wave_sync();
             if (fin) break;
         }
 
         // ---- interval still open at the tile's end: its piece of this tile
-        if (lane < S && (sm.st_q[lane] & 1)) {
+        if (slane && (sq & 1)) {
             const KArgs k = kargs();
-            double* dst = sm.st_started[lane] ? k->tail : k->head;
-            dst[(int64_t)ln * k->ld + b] = sm.st_acc[lane];
+            double* dst = sstarted ? k->tail : k->head;
+            dst[(int64_t)lane * k->ld + b] = sacc;
         }
-        wave_sync();
     }
 
     // the wave's trace and idle energy, kept at its first tile (others 0)
-    const double Wt = wave_sum(w_acc);
     const double It = wave_sum(idle);
     const KArgs k = kargs();
     for (int b = b0 + lane; b < b1; b += WAVE) {
-        k->tileW[b] = (b == b0) ? Wt : 0.0;
+        k->tileW[b] = (b == b0) ? w_wave : 0.0;
         k->tileIdle[b] = (b == b0) ? It : 0.0;
     }
-    if (lane < S) {
+    if (slane) {
         // where this wave stopped: the next wave must start there
         const int LD = (int)k->ld;
-        k->cnt_fin[(int64_t)lane * (LD + 1) + b1] = sm.st_q[lane];
-        if (b1 == (int)k->NT) k->cnt[(int64_t)lane * (LD + 1) + b1] = sm.st_q[lane];
+        k->cnt_fin[(int64_t)lane * (LD + 1) + b1] = sq;
+        if (b1 == (int)k->NT) k->cnt[(int64_t)lane * (LD + 1) + b1] = sq;
     }
     if (__ballot(err != 0u)) {
         unsigned e = err;
@@ -722,29 +722,34 @@ __global__ __launch_bounds__(WAVE * WPB) __attribute__((amdgpu_waves_per_eu(4)))
 
 namespace {
 
-constexpr int TILE_WPB = 4;  // independent waves per workgroup
-
-template <int SMAX>
+template <int SP>
 hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream)
 {
-    using K = decltype(&k_tile<SEG_PER_THREAD, SMAX, TILE_WPB>);
-    const K kern = k_tile<SEG_PER_THREAD, SMAX, TILE_WPB>;
+    using K = decltype(&k_tile<SP>);
+    const K kern = k_tile<SP>;
     // persistent waves: as many as can be resident at once, each over a
     // contiguous run of tiles
     static int per_cu = 0;
     if (per_cu == 0) {
         int nb = 0;
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, WAVE * TILE_WPB, 0) !=
-                hipSuccess ||
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, WAVE, 0) != hipSuccess ||
             nb <= 0)
-            nb = 2;
+            nb = 8;
+        // LDS is granted in 2 KiB blocks: never count on more waves than fit that way
+        int dev = 0, lds = 0;
+        if (hipGetDevice(&dev) == hipSuccess &&
+            hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) ==
+                hipSuccess &&
+            lds > 0) {
+            const int per_wave = (int)((sizeof(TileLds<SP>) + 2047) / 2048) * 2048;
+            nb = max(1, min(nb, lds / per_wave));
+        }
         per_cu = nb;
     }
-    const int64_t waves = (int64_t)device_cu_count() * per_cu * TILE_WPB;
+    const int64_t waves = (int64_t)device_cu_count() * per_cu;
     p.tiles_per_wg = (ntiles + waves - 1) / waves;
     const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
-    const int grid = (int)((runs + TILE_WPB - 1) / TILE_WPB);
-    hipLaunchKernelGGL(kern, dim3(grid), dim3(WAVE * TILE_WPB), 0, stream, p);
+    hipLaunchKernelGGL(kern, dim3((unsigned)runs), dim3(WAVE), 0, stream, p);
     return hipGetLastError();
 }
 
@@ -754,9 +759,13 @@ hipError_t launch_tile(const TileParams& p, hipStream_t stream)
 {
     const int64_t ntiles = p.tile_end - p.tile_begin;
     if (ntiles <= 0) return hipSuccess;
-    if (p.ss.S == 1) return launch_tile_t<1>(p, ntiles, stream);
-    if (p.ss.S <= 4) return launch_tile_t<4>(p, ntiles, stream);
-    return launch_tile_t<MAX_STREAMS>(p, ntiles, stream);
+    const int S = p.ss.S;
+    if (S == 1) return launch_tile_t<1>(p, ntiles, stream);
+    if (S == 2) return launch_tile_t<2>(p, ntiles, stream);
+    if (S <= 4) return launch_tile_t<4>(p, ntiles, stream);
+    if (S <= 8) return launch_tile_t<8>(p, ntiles, stream);
+    if (S <= 16) return launch_tile_t<16>(p, ntiles, stream);
+    return launch_tile_t<32>(p, ntiles, stream);
 }
 
 }  // namespace mag
