@@ -65,9 +65,6 @@ struct AttrWorkspace {
     int64_t* cnt_fin;
     double* head;
     double* tail;
-    double* tileW;
-    double* tileIdle;
-    double* tsum;  // per-slice partial totals of tileW / tileIdle
     double* energy;
     unsigned long long* table;
     uint32_t* slot;
@@ -101,9 +98,6 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
     w.cnt_fin = c.take<int64_t>((size_t)pl.S * (pl.NT + 1));
     w.head = c.take<double>((size_t)pl.S * pl.NT);
     w.tail = c.take<double>((size_t)pl.S * pl.NT);
-    w.tileW = c.take<double>((size_t)pl.NT);
-    w.tileIdle = c.take<double>((size_t)pl.NT);
-    w.tsum = c.take<double>(2 * (size_t)((pl.NT + mag::SUM_SLICE - 1) / mag::SUM_SLICE) + 2);
     w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
     if (pl.staging) {
         w.stage_t = c.take<double>((size_t)mag::TILE + 1);
@@ -299,8 +293,6 @@ struct Job {
         tp.cnt_fin = w.cnt_fin;
         tp.head = w.head;
         tp.tail = w.tail;
-        tp.tileW = w.tileW;
-        tp.tileIdle = w.tileIdle;
         tp.status = w.status;
         tp.split = (flags & MAG_EQUAL_SPLIT) ? 1 : 0;
         tp.validate = validate() ? 1 : 0;
@@ -310,8 +302,9 @@ struct Job {
         return mag::launch_tile(tp, stream);
     }
 
-    // cross-tile intervals, endpoints outside the trace, trace/idle totals
-    hipError_t fixups(int64_t n_samples, int64_t NT)
+    // cross-tile intervals, endpoints outside the trace; the group-by state is
+    // cleared in the same launch when a grouping follows
+    hipError_t fixups(int64_t n_samples, int64_t NT, bool grouping)
     {
         mag::FixParams fp{};
         fp.s = s;
@@ -329,10 +322,12 @@ struct Job {
         fp.end_idx = end_idx;
         fp.status = w.status;
         fp.validate = validate() ? 1 : 0;
-        hipError_t e2;
-        if ((e2 = mag::launch_cross(fp, stream)) != hipSuccess) return e2;
-        if ((e2 = mag::launch_outside(fp, stream)) != hipSuccess) return e2;
-        return mag::launch_summary(w.tileW, w.tileIdle, NT, w.tsum, w.status, stream);
+        if (grouping && pl.m > 0 && pl.H > 0) {
+            fp.table = w.table;
+            fp.H = pl.H;
+            fp.urank = w.urank;
+        }
+        return mag::launch_fix(fp, stream);
     }
 
     hipError_t grouping(uint64_t* keys_out, mag_key_stats* per_key)
@@ -495,7 +490,8 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
     if ((e = job.run_tiles(timestamps, power, 0, 0, NT, n_samples - 1, NT)) != hipSuccess)
         return hip_fail(e, "tile kernel");
     timer.mark(2);
-    if ((e = job.fixups(n_samples, NT)) != hipSuccess) return hip_fail(e, "fix-up kernels");
+    if ((e = job.fixups(n_samples, NT, per_key != nullptr)) != hipSuccess)
+        return hip_fail(e, "fix-up kernels");
     if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
     timer.mark(3);
     rc = job.conclude(per_key, summary);
@@ -559,8 +555,6 @@ int state_regions(const mag_stream* h, Region* r)
     r[k++] = {j.w.cnt_fin, sizeof(int64_t) * S * (ld + 1)};
     r[k++] = {j.w.head, sizeof(double) * S * ld};
     r[k++] = {j.w.tail, sizeof(double) * S * ld};
-    r[k++] = {j.w.tileW, sizeof(double) * ld};
-    r[k++] = {j.w.tileIdle, sizeof(double) * ld};
     r[k++] = {j.w.stage_t, sizeof(double) * (mag::TILE + 1)};
     r[k++] = {j.w.stage_P, sizeof(float) * (mag::TILE + 1)};
     r[k++] = {j.energy, sizeof(double) * m};
@@ -736,7 +730,7 @@ int mag_stream_end(mag_stream* h, uint64_t* keys_out, mag_key_stats* per_key, ma
     } else if ((e = job.run_tiles(job.w.stage_t, job.w.stage_P, h->b_next * mag::TILE, h->b_next,
                                   NT, n - 1, NT)) != hipSuccess) {
         rc = hip_fail(e, "tile kernel");
-    } else if ((e = job.fixups(n, NT)) != hipSuccess) {
+    } else if ((e = job.fixups(n, NT, per_key != nullptr)) != hipSuccess) {
         rc = hip_fail(e, "fix-up kernels");
     } else if ((e = job.grouping(keys_out, per_key)) != hipSuccess) {
         rc = hip_fail(e, "group-by");

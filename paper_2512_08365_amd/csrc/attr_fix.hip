@@ -1,6 +1,8 @@
 // attr_fix.hip -- the small kernels around the tile kernel: intervals whose
 // endpoints lie in different tiles, endpoints outside [t_0, t_{n-1}], the
-// status block, and the fixed-order reductions of the per-tile totals.
+// status block, and the clearing of the group-by state.
+
+#include <algorithm>
 
 #include "mag_internal.hpp"
 
@@ -19,40 +21,38 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
 }  // namespace
 
 // ---------------------------------------------------------------------------
-// intervals whose endpoints lie in different tiles
+// one launch after the tiles: three kinds of workgroups
+//   [0, nb_cross)               intervals whose endpoints lie in different tiles
+//   [nb_cross, + 32 S)          endpoints before t_0 or after t_{n-1}
+//   [.., + nb_clear)            the group-by state, cleared for the grouping
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_cross(const FixParams p)
+namespace {
+
+__device__ void fix_cross(const FixParams& p, int64_t idx)
 {
     const int64_t NT = p.NT, LD = p.ld;
-    const int64_t total = (int64_t)p.ss.S * (NT + 1);
-    for (int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; idx < total;
-         idx += (int64_t)gridDim.x * blockDim.x) {
-        const int a = (int)(idx / (NT + 1));
-        const int64_t b = idx - (int64_t)a * (NT + 1);
-        const int64_t* c = p.cnt + (int64_t)a * (LD + 1);
-        const int64_t c0 = c[b];
-        const int64_t len = 2 * (p.ss.off[a + 1] - p.ss.off[a]);
-        const int64_t fin = p.cnt_fin[(int64_t)a * (LD + 1) + b];
-        if (p.validate && b > 0 && b < NT && fin != CNT_UNSET && fin != c0) {
-            // a workgroup stopped at tile b with a cursor other than the one the
-            // next workgroup searched for: some stream is unsorted
-            atomicOr(&p.status->err, ERR_INTERVAL);
-        }
-        if (!(c0 & 1) || c0 > len) continue;            // no interval active at tile start
-        if (b > 0 && c[b - 1] == c0) continue;         // not the first tile it is active at
-        const int64_t gid = p.ss.off[a] + (c0 >> 1);
-        double E = (b > 0) ? p.tail[(int64_t)a * LD + b - 1] : 0.0;
-        for (int64_t bb = b; bb < NT && c[bb] == c0; ++bb) E += p.head[(int64_t)a * LD + bb];
-        p.energy[gid] = E;
+    const int a = (int)(idx / (NT + 1));
+    const int64_t b = idx - (int64_t)a * (NT + 1);
+    const int64_t* c = p.cnt + (int64_t)a * (LD + 1);
+    const int64_t c0 = c[b];
+    const int64_t len = 2 * (p.ss.off[a + 1] - p.ss.off[a]);
+    const int64_t fin = p.cnt_fin[(int64_t)a * (LD + 1) + b];
+    if (p.validate && b > 0 && b < NT && fin != CNT_UNSET && fin != c0) {
+        // a wave stopped at tile b with a cursor other than the one the next
+        // wave searched for: some stream is unsorted
+        atomicOr(&p.status->err, ERR_INTERVAL);
     }
+    if (!(c0 & 1) || c0 > len) return;         // no interval active at tile start
+    if (b > 0 && c[b - 1] == c0) return;       // not the first tile it is active at
+    const int64_t gid = p.ss.off[a] + (c0 >> 1);
+    double E = (b > 0) ? p.tail[(int64_t)a * LD + b - 1] : 0.0;
+    for (int64_t bb = b; bb < NT && c[bb] == c0; ++bb) E += p.head[(int64_t)a * LD + bb];
+    p.energy[gid] = E;
 }
 
-// ---------------------------------------------------------------------------
-// endpoints before t_0 or after t_{n-1}
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_outside(const FixParams p)
+// endpoints of stream a before t_0 / after t_{n-1}: thread r of nthreads
+__device__ void fix_outside(const FixParams& p, int a, int64_t r, int64_t nthreads)
 {
-    const int a = blockIdx.y;
     const int64_t NT = p.NT;
     const int64_t off = p.ss.off[a];
     const int64_t len = 2 * (p.ss.off[a + 1] - off);
@@ -63,8 +63,7 @@ __global__ __launch_bounds__(256) void k_outside(const FixParams p)
     const double t0 = p.status->bounds[0], tn = p.status->bounds[1];
     unsigned err = 0u;
     unsigned long long clipped = 0;
-    for (int64_t qq = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; qq < nbefore + nafter;
-         qq += (int64_t)gridDim.x * blockDim.x) {
+    for (int64_t qq = r; qq < nbefore + nafter; qq += nthreads) {
         const int64_t q = (qq < nbefore) ? qq : cN + (qq - nbefore);
         const int64_t gid = off + (q >> 1);
         const double x = endpoint_x(p.s, p.e, off, q);
@@ -88,6 +87,35 @@ __global__ __launch_bounds__(256) void k_outside(const FixParams p)
     }
     if (err) atomicOr(&p.status->err, err);
     if (clipped) atomicAdd(&p.status->n_clipped, clipped);
+}
+
+constexpr int FIX_THREADS = 256;
+constexpr int OUT_BLOCKS = 32;  // workgroups per stream for the outside endpoints
+
+}  // namespace
+
+__global__ __launch_bounds__(FIX_THREADS) void k_fix(const FixParams p, int64_t nb_cross,
+                                                    int64_t nb_clear)
+{
+    const int64_t blk = blockIdx.x;
+    if (blk < nb_cross) {
+        const int64_t idx = blk * FIX_THREADS + threadIdx.x;
+        if (idx < (int64_t)p.ss.S * (p.NT + 1)) fix_cross(p, idx);
+        return;
+    }
+    const int64_t bo = blk - nb_cross;
+    if (bo < (int64_t)OUT_BLOCKS * p.ss.S) {
+        const int a = (int)(bo / OUT_BLOCKS);
+        fix_outside(p, a, (bo % OUT_BLOCKS) * FIX_THREADS + threadIdx.x,
+                    (int64_t)OUT_BLOCKS * FIX_THREADS);
+        return;
+    }
+    const int64_t bc = bo - (int64_t)OUT_BLOCKS * p.ss.S;
+    for (int64_t h = bc * FIX_THREADS + threadIdx.x; h <= (int64_t)p.H;
+         h += nb_clear * FIX_THREADS) {
+        if (h < (int64_t)p.H) p.table[h] = ~0ull;
+        p.urank[h] = 0u;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -114,52 +142,6 @@ __global__ __launch_bounds__(256) void k_init(Status* st, int64_t* cnt_fin, int6
             st->bounds[0] = t[0];
             st->bounds[1] = t[n - 1];
         }
-    }
-}
-
-// whole-trace and idle energy: fixed-order reduction of the per-tile sums,
-// first over slices of SUM_SLICE tiles (one workgroup each), then over slices
-__global__ __launch_bounds__(1024) void k_summary_part(const double* tileW, const double* tileIdle,
-                                                        int64_t NT, double* part)
-{
-    __shared__ double red[2][16];
-    const int tid = threadIdx.x;
-    const int64_t lo = (int64_t)blockIdx.x * SUM_SLICE, hi = min(lo + SUM_SLICE, NT);
-    double w = 0.0, z = 0.0;
-    for (int64_t b = lo + tid; b < hi; b += 1024) {
-        w += tileW[b];
-        z += tileIdle[b];
-    }
-    for (int off = 32; off > 0; off >>= 1) {
-        w += __shfl_xor(w, off);
-        z += __shfl_xor(z, off);
-    }
-    if ((tid & 63) == 0) {
-        red[0][tid >> 6] = w;
-        red[1][tid >> 6] = z;
-    }
-    lds_barrier();
-    if (tid == 0) {
-        double W = 0.0, I = 0.0;
-        for (int u = 0; u < 16; ++u) {
-            W += red[0][u];
-            I += red[1][u];
-        }
-        part[2 * blockIdx.x] = W;
-        part[2 * blockIdx.x + 1] = I;
-    }
-}
-
-__global__ __launch_bounds__(64) void k_summary_final(const double* part, int64_t nparts, Status* st)
-{
-    if (threadIdx.x == 0) {
-        double W = 0.0, I = 0.0;
-        for (int64_t k = 0; k < nparts; ++k) {
-            W += part[2 * k];
-            I += part[2 * k + 1];
-        }
-        st->trace_energy = W;
-        st->idle_energy = I;
     }
 }
 
@@ -196,28 +178,15 @@ hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_
     return launch_init(st, nullptr, 0, t, n, stream);
 }
 
-hipError_t launch_cross(const FixParams& p, hipStream_t stream)
+hipError_t launch_fix(const FixParams& p, hipStream_t stream)
 {
     const int64_t total = (int64_t)p.ss.S * (p.NT + 1);
-    const int64_t blocks = min((total + 255) / 256, (int64_t)65536);
-    hipLaunchKernelGGL(k_cross, dim3((unsigned)blocks), dim3(256), 0, stream, p);
-    return hipGetLastError();
-}
-
-hipError_t launch_outside(const FixParams& p, hipStream_t stream)
-{
-    hipLaunchKernelGGL(k_outside, dim3(32, (unsigned)p.ss.S), dim3(256), 0, stream, p);
-    return hipGetLastError();
-}
-
-hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, double* part,
-                          Status* st, hipStream_t stream)
-{
-    const int64_t nparts = (NT + SUM_SLICE - 1) / SUM_SLICE;
-    if (nparts > 0)
-        hipLaunchKernelGGL(k_summary_part, dim3((unsigned)nparts), dim3(1024), 0, stream, tileW,
-                           tileIdle, NT, part);
-    hipLaunchKernelGGL(k_summary_final, dim3(1), dim3(64), 0, stream, part, nparts, st);
+    const int64_t nb_cross = (total + FIX_THREADS - 1) / FIX_THREADS;
+    const int64_t nb_clear =
+        p.table ? std::min<int64_t>(((int64_t)p.H + FIX_THREADS) / FIX_THREADS, 2048) : 0;
+    const int64_t blocks = nb_cross + (int64_t)OUT_BLOCKS * p.ss.S + nb_clear;
+    hipLaunchKernelGGL(k_fix, dim3((unsigned)blocks), dim3(FIX_THREADS), 0, stream, p, nb_cross,
+                       nb_clear);
     return hipGetLastError();
 }
 

@@ -700,12 +700,12 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         }
     }
 
-    // the wave's trace and idle energy, kept at its first tile (others 0)
+    // the wave's trace and idle energy
     const double It = wave_sum(idle);
     const KArgs k = kargs();
-    for (int b = b0 + lane; b < b1; b += WAVE) {
-        k->tileW[b] = (b == b0) ? w_wave : 0.0;
-        k->tileIdle[b] = (b == b0) ? It : 0.0;
+    if (lane == 0) {
+        atomicAdd(&k->status->trace_energy, w_wave);
+        atomicAdd(&k->status->idle_energy, It);
     }
     if (slane) {
         // where this wave stopped: the next wave must start there

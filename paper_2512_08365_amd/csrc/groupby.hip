@@ -1,17 +1,24 @@
 // groupby.hip -- per-operator-key count, sum and M2 of the interval energies.
 //
+// The key table and the rank counters are cleared by k_fix, the launch before.
+//
 // 1. k_key_insert + k_keymap: the 64-bit keys go into an open-addressing hash
 //    table (linear probing, 64-bit compare-and-swap; the all-ones key is kept
-//    out of band so any uint64 is a legal key).  Insertion de-duplicates in
-//    LDS first; the lookup pass then finds almost every key with a plain,
-//    cached load (a separate launch, so no cached line predates an insert).
-// 2. k_compact + k_rank: the distinct keys are listed and ranked (rank = number
-//    of smaller keys), which gives dense ids in ascending key order.
+//    out of band so any uint64 is a legal key).  Insertion (of the keys of a
+//    prefix of the intervals) de-duplicates in LDS first; the lookup pass then
+//    finds almost every key with a plain, cached load (a separate launch, so
+//    no cached line predates an insert) and inserts the rest.
+// 2. k_compact: the distinct keys are listed; a key's place in the list is its
+//    dense id.  k_rank: rank of each key = number of smaller keys (its row in
+//    the output, ascending by key).
 // 3. k_agg_sum / k_fin_sum: each workgroup aggregates one chunk of intervals
 //    into an LDS table indexed by dense id (count, sum); the partial tables are
-//    reduced per key in chunk order.
+//    reduced per key in chunk order, and the key, count and sum written to the
+//    key's row.  Per-workgroup atomics add the rows into the attributed energy.
 // 4. k_agg_m2 / k_fin_m2: second pass over the chunk for sum (E - mean)^2
 //    (the two-pass definition of M2).
+// Plain stores carry every partial result: device-scope atomics, which are
+// slow on this part, are used only for counters and one add per workgroup.
 
 #include "mag_internal.hpp"
 
@@ -34,23 +41,14 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t k)
 
 }  // namespace
 
-__global__ __launch_bounds__(256) void k_table_fill(unsigned long long* table, uint32_t* urank,
-                                                    uint32_t H)
-{
-    for (uint32_t h = blockIdx.x * blockDim.x + threadIdx.x; h <= H; h += gridDim.x * blockDim.x) {
-        if (h < H) table[h] = EMPTY_KEY;
-        urank[h] = 0u;
-    }
-}
-
 // Insert the distinct keys of a prefix of the intervals.  Each workgroup first
 // de-duplicates its chunk in an LDS table; then every thread takes a few LDS
 // slots and inserts their keys into the global table, so a key costs one global
 // probe per workgroup and the probe chains of a workgroup run in parallel.
-constexpr int INS_THREADS = 1024;
-constexpr int INS_CHUNK = 8192;
-constexpr int INS_SLOTS = 16384;
-constexpr int INS_GROUPS = 32;  // the lookup pass inserts keys first seen later
+constexpr int INS_THREADS = 512;
+constexpr int INS_CHUNK = 4096;
+constexpr int INS_SLOTS = 8192;
+constexpr int INS_GROUPS = 64;  // the lookup pass inserts keys first seen later
 
 __device__ __forceinline__ void global_insert(const GroupParams& p, unsigned long long k)
 {
@@ -161,43 +159,41 @@ __global__ __launch_bounds__(256) void k_compact(const GroupParams p)
             const uint32_t u = base + (uint32_t)__popcll(ob & ((1ull << lane) - 1ull));
             p.ukey[u] = k;
             p.uslot[u] = h;
+            p.slot2id[h] = u;
         }
     }
 }
 
-// dense id = number of distinct keys smaller than this one; block (x, y)
-// compares keys [256 x, 256 x + 256) against keys [RANK_TILE y, RANK_TILE (y + 1))
+// rank = number of distinct keys smaller than this one: the pairs (x, y) of key
+// tiles are spread over the workgroups; pair (x, y) compares keys
+// [256 x, 256 x + 256) against keys [256 y, 256 y + 256)
 constexpr uint32_t RANK_TILE = 256u;
 
-__global__ __launch_bounds__(256) void k_rank(const GroupParams p)
+__global__ __launch_bounds__(RANK_TILE) void k_rank(const GroupParams p)
 {
     __shared__ uint64_t tile[RANK_TILE];
     const uint32_t nu = p.status->n_unique;
-    const uint32_t base = blockIdx.y * RANK_TILE;
-    if (blockIdx.x * 256u >= nu || base >= nu) return;  // uniform over the block
-    const uint32_t u = blockIdx.x * 256u + threadIdx.x;
-    const uint32_t cnt = min(RANK_TILE, nu - base);
-    for (uint32_t v = threadIdx.x; v < cnt; v += 256u) tile[v] = p.ukey[base + v];
-    lds_barrier();
-    if (u >= nu) return;
-    const uint64_t mine = p.ukey[u];
-    uint32_t rank = 0;
-    uint32_t v = 0;
-    for (; v + 16 <= cnt; v += 16) {
+    const uint32_t nt = (nu + RANK_TILE - 1) / RANK_TILE;
+    const uint64_t pairs = (uint64_t)nt * nt;
+    for (uint64_t pr = blockIdx.x; pr < pairs; pr += gridDim.x) {
+        const uint32_t bx = (uint32_t)(pr % nt), by = (uint32_t)(pr / nt);
+        const uint32_t base = by * RANK_TILE;
+        const uint32_t cnt = min(RANK_TILE, nu - base);
+        __syncthreads();  // the previous pair's reads of the tile are done
+        for (uint32_t v = threadIdx.x; v < cnt; v += RANK_TILE) tile[v] = p.ukey[base + v];
+        __syncthreads();
+        const uint32_t u = bx * RANK_TILE + threadIdx.x;
+        if (u < nu) {
+            const uint64_t mine = p.ukey[u];
+            uint32_t rank = 0;
+            uint32_t v = 0;
+            for (; v + 16 <= cnt; v += 16) {
 #pragma unroll
-        for (int w = 0; w < 16; ++w) rank += (tile[v + w] < mine) ? 1u : 0u;
-    }
-    for (; v < cnt; ++v) rank += (tile[v] < mine) ? 1u : 0u;
-    if (rank) atomicAdd(&p.urank[u], rank);
-}
-
-__global__ __launch_bounds__(256) void k_rank_write(const GroupParams p)
-{
-    const uint32_t nu = p.status->n_unique;
-    for (uint32_t u = blockIdx.x * blockDim.x + threadIdx.x; u < nu; u += gridDim.x * blockDim.x) {
-        const uint32_t rank = p.urank[u];
-        p.slot2id[p.uslot[u]] = rank;
-        if ((int64_t)rank < p.cap) p.keys_out[rank] = p.ukey[u];
+                for (int w = 0; w < 16; ++w) rank += (tile[v + w] < mine) ? 1u : 0u;
+            }
+            for (; v < cnt; ++v) rank += (tile[v] < mine) ? 1u : 0u;
+            if (rank) atomicAdd(&p.urank[u], rank);
+        }
     }
 }
 
@@ -268,6 +264,7 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
     qc[grp][kl] = cnt;
     qs[grp][kl] = sum;
     __syncthreads();
+    double tot = 0.0;
     if (grp == 0 && id < nk) {
         cnt = 0;
         sum = 0.0;
@@ -275,9 +272,19 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
             cnt += qc[g][kl];
             sum += qs[g][kl];
         }
-        p.count_out[id] = (int64_t)cnt;
-        p.sum_out[id] = sum;
+        const uint32_t r = p.urank[id];
+        if ((int64_t)r < p.cap) {
+            p.keys_out[r] = p.ukey[id];
+            p.count_out[r] = (int64_t)cnt;
+            p.sum_out[r] = sum;
+        }
         p.mean[id] = cnt ? sum / (double)cnt : 0.0;
+        tot = sum;
+    }
+    if (grp == 0) {
+        // this workgroup's rows, once into the attributed energy
+        for (int off = 32; off > 0; off >>= 1) tot += __shfl_xor(tot, off);
+        if (kl == 0 && tot != 0.0) atomicAdd(&p.status->attributed_energy, tot);
     }
 }
 
@@ -335,32 +342,14 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupPar
     if (grp == 0 && id < nk) {
         m2 = 0.0;
         for (int g = 0; g < FIN_GROUPS; ++g) m2 += qs[g][kl];
-        p.m2_out[id] = m2;
-    }
-}
-
-// sum of the per-key sums (attributed energy), in key order
-__global__ __launch_bounds__(1024) void k_key_total(const GroupParams p)
-{
-    __shared__ double red[16];
-    const int tid = threadIdx.x;
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
-    double v = 0.0;
-    for (int64_t i = tid; i < nk; i += 1024) v += p.sum_out[i];
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if ((tid & 63) == 0) red[tid >> 6] = v;
-    __syncthreads();
-    if (tid == 0) {
-        double s = 0.0;
-        for (int u = 0; u < 16; ++u) s += red[u];
-        p.status->attributed_energy = s;
+        const uint32_t r = p.urank[id];
+        if ((int64_t)r < p.cap) p.m2_out[r] = m2;
     }
 }
 
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
 {
-    const unsigned fill_blocks = (unsigned)min((p.H + 256u) / 256u, 4096u);
-    hipLaunchKernelGGL(k_table_fill, dim3(fill_blocks), dim3(256), 0, stream, p.table, p.urank, p.H);
+    if (p.m <= 0) return hipSuccess;
     const int64_t n_ins = min(p.m, (int64_t)INS_CHUNK * INS_GROUPS);
     hipLaunchKernelGGL(k_key_insert, dim3((unsigned)((n_ins + INS_CHUNK - 1) / INS_CHUNK)),
                        dim3(INS_THREADS), 0, stream, p, n_ins);
@@ -368,13 +357,12 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
     hipLaunchKernelGGL(k_keymap, dim3((unsigned)max(mb, (int64_t)1)), dim3(256), 0, stream, p);
     const unsigned hb = (unsigned)min((int64_t)(p.H + 1 + 255) / 256, (int64_t)4096);
     hipLaunchKernelGGL(k_compact, dim3(hb), dim3(256), 0, stream, p);
-    // the distinct keys are at most min(H + 1, cap + 1) when they fit (more only
-    // on overflow, which is reported and ranked partially)
+    // the distinct keys that can get a row are at most min(H + 1, cap + 1)
+    // (more only on overflow, which is reported and ranked partially)
     const int64_t nmax = min((int64_t)p.H + 1, p.cap + 1);
-    const unsigned rx = (unsigned)((nmax + 255) / 256);
-    const unsigned ry = (unsigned)((nmax + RANK_TILE - 1) / RANK_TILE);
-    hipLaunchKernelGGL(k_rank, dim3(rx, ry), dim3(256), 0, stream, p);
-    hipLaunchKernelGGL(k_rank_write, dim3(hb), dim3(256), 0, stream, p);
+    const int64_t ntile = (nmax + RANK_TILE - 1) / RANK_TILE;
+    hipLaunchKernelGGL(k_rank, dim3((unsigned)min(ntile * ntile, (int64_t)4096)), dim3(RANK_TILE),
+                       0, stream, p);
     const unsigned ranges = (unsigned)((p.cap + AGG_IDS - 1) / AGG_IDS);
     if (ranges > 0) {
         hipLaunchKernelGGL(k_agg_sum, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
@@ -384,7 +372,6 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
         hipLaunchKernelGGL(k_agg_m2, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);
         hipLaunchKernelGGL(k_fin_m2, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
-        hipLaunchKernelGGL(k_key_total, dim3(1), dim3(1024), 0, stream, p);
     }
     return hipGetLastError();
 }

@@ -18,7 +18,6 @@ constexpr int SEG_PER_THREAD = 8;
 constexpr int TILE = 64 * SEG_PER_THREAD;  // 512
 constexpr int ROUND_EVENTS = 64;
 constexpr int MAX_STREAMS = MAG_MAX_STREAMS;
-constexpr int SUM_SLICE = 8192;  // tiles per workgroup of the per-tile total reduction
 
 // group-by
 constexpr int AGG_THREADS = 1024;
@@ -82,9 +81,7 @@ struct TileParams {
                         // the tile after it (CNT_UNSET where no workgroup ended)
     double* head;       // [S][ld] in-tile energy of the interval active at tile start
     double* tail;       // [S][ld] in-tile energy of the interval started in the tile, active at its end
-    double* tileW;      // [NT]
-    double* tileIdle;   // [NT]
-    Status* status;
+    Status* status;     // trace and idle energy are added here
     int split;
     int validate;
     int aligned16;      // t and P are 16-byte aligned (vector loads)
@@ -106,6 +103,10 @@ struct FixParams {
     int64_t* end_idx;
     Status* status;
     int validate;
+    // group-by state cleared for the grouping that follows (table NULL: none)
+    unsigned long long* table;     // [H] key table: all ones = empty
+    uint32_t H;
+    uint32_t* urank;               // [H+1] rank counters
 };
 
 struct GroupParams {
@@ -118,8 +119,8 @@ struct GroupParams {
     int64_t chunk;        // intervals per chunk
     unsigned long long* table;  // [H]
     uint32_t* slot;       // [m]
-    uint32_t* slot2id;    // [H+1]
-    uint64_t* ukey;       // [H+1]
+    uint32_t* slot2id;    // [H+1] dense id of an occupied slot (its place in the list)
+    uint64_t* ukey;       // [H+1] distinct keys, by dense id
     uint32_t* uslot;      // [H+1]
     uint32_t* urank;      // [H+1] rank of each distinct key (zeroed, then counted)
     double* mean;         // [cap]
@@ -174,11 +175,8 @@ hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
 // tiles [p.tile_begin, p.tile_end) on persistent waves (sets the launch shape)
 hipError_t launch_tile(const TileParams& p, hipStream_t stream);
-hipError_t launch_cross(const FixParams& p, hipStream_t stream);
-hipError_t launch_outside(const FixParams& p, hipStream_t stream);
-// whole-trace and idle energy from the per-tile totals (part: 2 * ceil(NT / SUM_SLICE) doubles)
-hipError_t launch_summary(const double* tileW, const double* tileIdle, int64_t NT, double* part,
-                          Status* st, hipStream_t stream);
+// intervals spanning tiles, endpoints outside the trace, clearing of the group-by state
+hipError_t launch_fix(const FixParams& p, hipStream_t stream);
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
 hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream);
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream);
