@@ -78,6 +78,37 @@ def test_dense_endpoints_force_rounds():
     compare_attribution(c, label="one segment")
 
 
+def test_tiny_energies_behind_a_large_tile_prefix():
+    # 1 MW for the first samples of every tile, then 1 mW: an interval over
+    # whole low-power segments holds ~1e-11 of the tile's prefix energy, far
+    # below what a difference of two tile-local prefixes resolves to 1e-9, so
+    # the whole segments must be summed directly.  Several streams overlap
+    # (equal split), some intervals span tiles, some sit inside one segment.
+    rng = np.random.default_rng(11)
+    n = 4 * 512 + 37
+    t = np.arange(n, dtype=np.float64) * 1e-3
+    P = np.where((np.arange(n) % 512) < 300, 1.0e6, 1.0e-3).astype(np.float32)
+    P[::97] = 0.0
+    for streams in (1, 3):
+        s_all, e_all, off = [], [], [0]
+        for a in range(streams):
+            cuts = np.sort(rng.uniform(0.0, t[-1], 2 * 40))
+            s_all.append(cuts[0::2])
+            e_all.append(cuts[1::2])
+            off.append(off[-1] + 40)
+        # intervals wholly inside the low-power stretch of tile 1, over whole segments
+        lo = (512 + 310) * 1e-3
+        extra_s = lo + np.arange(5) * 0.02 + 0.0003
+        extra_e = extra_s + np.array([0.0021, 0.005, 0.0107, 0.0004, 0.0015])
+        s_all.append(extra_s)
+        e_all.append(extra_e)
+        off.append(off[-1] + 5)
+        c = {"t": t, "P": P, "s": np.concatenate(s_all), "e": np.concatenate(e_all),
+             "key": rng.integers(0, 7, off[-1]).astype(np.uint64), "offsets": np.array(off)}
+        for split in (True, False):
+            compare_attribution(c, equal_split=split, label=f"tiny energies s{streams + 1}")
+
+
 def test_degenerate_cases():
     t = np.array([0.0, 1.0])
     P = np.array([3.0, 5.0], np.float32)
