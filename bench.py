@@ -6,6 +6,7 @@ One step = the whole path over one A/B pair of the multi-stream workload
 operator intervals, 5,000 Zipf(1.2) keys): attribute side A, attribute side B
 (equal split of concurrent power, per-interval energies and sample indices,
 per-key count/sum/M2), then join and rank the top-100 excess-energy keys.
+Both sides are enqueued back to back (MAG_ASYNC) and finished before the diff.
 Inputs are synthetic, seeded and resident in HBM before timing.
 
 Prints ONE JSON line.  `value` is operator intervals attributed per second
@@ -138,7 +139,8 @@ class Side:
         self.kcnt = torch.empty(k_cap, dtype=torch.int64, device=dev)
         self.k_cap = k_cap
         self.offs = (ctypes.c_int64 * len(self.off))(*self.off)
-        self.opts = N.AttrOpts(len(self.off) - 1, N.MAG_EQUAL_SPLIT | N.MAG_TIME_KERNELS,
+        self.opts = N.AttrOpts(len(self.off) - 1,
+                               N.MAG_EQUAL_SPLIT | N.MAG_TIME_KERNELS | N.MAG_ASYNC,
                                ctypes.cast(self.offs, ctypes.c_void_p))
         b = ctypes.c_size_t(0)
         rc = lib.mag_attribute_workspace_size(self.n, self.m, k_cap, ctypes.byref(self.opts),
@@ -150,6 +152,7 @@ class Side:
         self.summ = N.Summary()
 
     def attribute(self, lib, stream):
+        """Enqueue this side's attribution (MAG_ASYNC: returns at once)."""
         rc = lib.mag_attribute(self.t.data_ptr(), self.P.data_ptr(), self.n, self.s.data_ptr(),
                                self.e.data_ptr(), self.key.data_ptr(), self.m,
                                ctypes.byref(self.opts), ctypes.byref(self.pio), self.kout.data_ptr(),
@@ -157,6 +160,13 @@ class Side:
                                self.ws.numel(), stream)
         if rc != 0:
             raise RuntimeError(f"mag_attribute failed {rc}: {lib.mag_last_error().decode()}")
+
+    def finish(self, lib, stream):
+        """Wait for the attribution; its key count, errors and tile-kernel time."""
+        rc = lib.mag_attribute_finish(self.ws.data_ptr(), ctypes.byref(self.ks),
+                                      ctypes.byref(self.summ), stream)
+        if rc != 0:
+            raise RuntimeError(f"mag_attribute_finish failed {rc}: {lib.mag_last_error().decode()}")
         return self.summ.tile_kernel_ms
 
 
@@ -244,8 +254,11 @@ def main():
     tile_ms = []
 
     def step(record):
-        ta = sa.attribute(lib, stream)
-        tb = sb.attribute(lib, stream)
+        # both sides enqueued back to back, then finished (one wait for both)
+        sa.attribute(lib, stream)
+        sb.attribute(lib, stream)
+        ta = sa.finish(lib, stream)
+        tb = sb.finish(lib, stream)
         rc = lib.mag_diff(sa.kout.data_ptr(), ctypes.byref(sa.ks), sb.kout.data_ptr(),
                           ctypes.byref(sb.ks), TOP_K, ctypes.byref(ro), d_ws.data_ptr(),
                           d_ws.numel(), stream)

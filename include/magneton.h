@@ -62,6 +62,9 @@ extern "C" {
 #define MAG_SKIP_VALIDATE 0x2u
 /* Time the call on `stream` with HIP events and report it in mag_summary. */
 #define MAG_TIME_KERNELS 0x4u
+/* mag_attribute returns once its work is enqueued; mag_attribute_finish
+   delivers n_keys, the summary and device-detected errors. */
+#define MAG_ASYNC 0x8u
 
 /* Most concurrent streams one call accepts. */
 #define MAG_MAX_STREAMS 32
@@ -71,7 +74,7 @@ extern "C" {
 typedef struct mag_attr_opts {
     int32_t n_streams;              /* >= 1; intervals are concatenated by stream   */
     uint32_t flags;                 /* MAG_EQUAL_SPLIT | MAG_SKIP_VALIDATE |          */
-                                    /* MAG_TIME_KERNELS                               */
+                                    /* MAG_TIME_KERNELS | MAG_ASYNC                   */
     const int64_t* stream_offsets;  /* HOST int64[n_streams + 1]: stream a owns       */
                                     /* intervals [offs[a], offs[a+1]); offs[0] = 0,   */
                                     /* offs[n_streams] = n_intervals; NULL allowed    */
@@ -104,7 +107,8 @@ typedef struct mag_summary {
     int64_t n_keys;           /* distinct keys (also when over capacity)            */
     double tile_kernel_ms;    /* MAG_TIME_KERNELS: duration of the interval-energy  */
                               /* kernel (HIP events on `stream`), else 0            */
-    double device_ms;         /* MAG_TIME_KERNELS: all device work of the call      */
+    double device_ms;         /* MAG_TIME_KERNELS: device time from the start of    */
+                              /* that kernel to the end of the call's work          */
 } mag_summary;
 
 /* Ranked join of two key tables (device arrays of `capacity` rows). */
@@ -144,8 +148,11 @@ int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t
  *   E_i    = integral over [starts[i], ends[i]] of P^(x) / m(x)  (MAG_EQUAL_SPLIT)
  *          = integral over [starts[i], ends[i]] of P^(x)          (otherwise).
  * Per key: count, sum of E_i and M2 = sum of (E_i - mean)^2; rows ascending by
- * unsigned key.  Every energy is computed as a sum of non-negative pieces (no
- * difference of running totals), in fp64.
+ * unsigned key.  Every energy is computed in fp64 as a sum of non-negative
+ * pieces; no energy is a difference of whole-trace running totals (the whole
+ * sample segments between two endpoints are a difference of two prefixes
+ * local to a 512-segment tile only where that difference keeps 6e-11
+ * relative accuracy, and a direct sum otherwise).
  *
  * Arguments (device arrays unless noted):
  *   timestamps[n_samples] fp64, strictly increasing, finite (seconds)
@@ -164,7 +171,8 @@ int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t
  *   workspace             device, >= mag_attribute_workspace_size(...,
  *                          per_key ? per_key->capacity : 0, opts) bytes,
  *                          256-byte aligned; its contents are scratch
- * Synchronizes `stream`.  Errors: MAG_E_NULL, MAG_E_SIZE, MAG_E_STREAMS,
+ * Synchronizes `stream` (with MAG_ASYNC: returns once the work is enqueued,
+ * see mag_attribute_finish).  Errors: MAG_E_NULL, MAG_E_SIZE, MAG_E_STREAMS,
  * MAG_E_WORKSPACE, MAG_E_ALIGN (host-detected, before any device work);
  * MAG_E_TIMESTAMPS, MAG_E_POWER, MAG_E_INTERVAL (device-detected, unless
  * MAG_SKIP_VALIDATE); MAG_E_CAPACITY (n_keys and summary->n_keys still report
@@ -175,6 +183,27 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
                   int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
                   uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary, void* workspace,
                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * mag_attribute_finish -- complete a mag_attribute call made with MAG_ASYNC.
+ * The paper's comparison is between two systems running the same workload
+ * (Section 3.2); attributing both traces back to back, and waiting once, keeps
+ * the device busy while the host enqueues the second.
+ *   workspace  the call's workspace (its status block sits at its head); it
+ *              must not be reused before this call
+ *   per_key    host struct of the call (same capacity), or NULL if the call
+ *              had none: n_keys is written
+ *   summary    host struct, may be NULL: filled as by a synchronous call
+ *              (tile_kernel_ms and device_ms when the call had MAG_TIME_KERNELS
+ *              and is finished on the thread that made it)
+ * Synchronizes `stream` (the call's stream) and returns what the synchronous
+ * call would have returned for its device work: MAG_OK, MAG_E_TIMESTAMPS,
+ * MAG_E_POWER, MAG_E_INTERVAL, MAG_E_CAPACITY or MAG_E_HIP; MAG_E_NULL or
+ * MAG_E_WORKSPACE for a NULL or misaligned workspace.  A workspace that no
+ * asynchronous call used gives unspecified results.
+ */
+int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summary* summary,
+                         hipStream_t stream);
 
 /*
  * mag_diff_workspace_size -- device workspace bytes for mag_diff.  Host only.

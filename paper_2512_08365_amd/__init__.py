@@ -20,6 +20,7 @@ __all__ = ["MagnetonError", "attribute", "diff", "Stream", "workspace_size",
 
 EQUAL_SPLIT = N.MAG_EQUAL_SPLIT
 SKIP_VALIDATE = N.MAG_SKIP_VALIDATE
+ASYNC = N.MAG_ASYNC
 
 
 class MagnetonError(RuntimeError):
@@ -85,20 +86,41 @@ def _stream_handle(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
+class Pending:
+    """An attribution enqueued with asynchronous=True; finish() waits for it and
+    returns what attribute() returns (raising its errors)."""
+
+    def __init__(self, workspace, ks, summ, build, keep):
+        self._workspace, self._ks, self._summ, self._build, self._keep = (
+            workspace, ks, summ, build, keep)
+        self._result = None
+
+    def finish(self):
+        if self._result is None:
+            rc = _lib().mag_attribute_finish(
+                self._workspace.data_ptr(), ctypes.byref(self._ks) if self._ks else None,
+                ctypes.byref(self._summ), _stream_handle(self._workspace.device))
+            _check(rc)
+            self._result = self._build()
+        return self._result
+
+
 def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
               equal_split: bool = True, validate: bool = True, key_capacity: int | None = None,
-              indices: bool = True, workspace=None, out=None):
+              indices: bool = True, workspace=None, out=None, asynchronous: bool = False):
     """Attribute the energy of a power trace to intervals and group it by key.
 
     t: float64 [n] timestamps (s), P: float32 [n] power (W), s/e: float64 [m]
     interval bounds, keys: int64 [m] (bits read as uint64) or None.
-    Returns (per_interval, per_key, summary): dicts of tensors / numbers.
+    Returns (per_interval, per_key, summary): dicts of tensors / numbers; with
+    asynchronous=True a Pending whose finish() returns them once the work ran.
     """
     lib = _lib()
     n = int(t.shape[0])
     m = int(s.shape[0])
     dev = t.device
-    flags = (EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE)
+    flags = ((EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE) |
+             (ASYNC if asynchronous else 0))
     o, keep = _opts(n_streams, stream_offsets, flags)
     group = keys is not None
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
@@ -136,18 +158,25 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
         ctypes.byref(ks) if group else None, ctypes.byref(summ), workspace.data_ptr(),
         workspace.numel(), _stream_handle(dev))
     _check(rc)
-    per_interval = {"energy": energy}
-    if indices:
-        per_interval["start_idx"] = si
-        per_interval["end_idx"] = ei
-    per_key = None
-    if group:
-        nk = int(ks.n_keys)
-        per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
-    summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
-               "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
-               "n_keys": int(summ.n_keys)}
-    return per_interval, per_key, summary
+
+    def build():
+        per_interval = {"energy": energy}
+        if indices:
+            per_interval["start_idx"] = si
+            per_interval["end_idx"] = ei
+        per_key = None
+        if group:
+            nk = int(ks.n_keys)
+            per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+        summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
+                   "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
+                   "n_keys": int(summ.n_keys)}
+        return per_interval, per_key, summary
+
+    if asynchronous:
+        # the inputs and the options stay referenced until finish()
+        return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys))
+    return build()
 
 
 def diff(a: dict, b: dict, k: int, workspace=None):

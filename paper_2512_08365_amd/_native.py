@@ -27,11 +27,13 @@ MAG_E_KEYS = -12
 MAG_EQUAL_SPLIT = 0x1
 MAG_SKIP_VALIDATE = 0x2
 MAG_TIME_KERNELS = 0x4
+MAG_ASYNC = 0x8
 MAG_MAX_STREAMS = 32
 
 # every symbol include/magneton.h declares
 EXPORTED = (
-    "mag_attribute_workspace_size", "mag_attribute", "mag_diff_workspace_size", "mag_diff",
+    "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_finish",
+    "mag_diff_workspace_size", "mag_diff",
     "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
     "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
     "mag_strerror", "mag_last_error", "mag_version",
@@ -83,6 +85,8 @@ def load(path: str = LIB_PATH):
                                   P(IntervalOut), c_vp, P(KeyStats), P(Summary), c_vp,
                                   ctypes.c_size_t, c_vp]
     lib.mag_attribute.restype = ctypes.c_int
+    lib.mag_attribute_finish.argtypes = [c_vp, P(KeyStats), P(Summary), c_vp]
+    lib.mag_attribute_finish.restype = ctypes.c_int
     lib.mag_diff_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
     lib.mag_diff_workspace_size.restype = ctypes.c_int
     lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,

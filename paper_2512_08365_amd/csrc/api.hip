@@ -149,30 +149,66 @@ int check_opts(const mag_attr_opts* opts, int64_t m, int* S, uint32_t* flags, ma
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-// optional HIP-event timing of a call's device work on its stream
-struct EventTimer {
-    bool on = false;
-    hipStream_t stream;
+// optional HIP-event timing of a call's device work on its stream.  The events
+// belong to (thread, device, workspace) and are created once: a call made with
+// MAG_ASYNC reads them back in mag_attribute_finish, on the same thread.
+struct TimerSlot {
+    int dev = -1;
+    const void* ws = nullptr;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
-    EventTimer(bool enable, hipStream_t s) : on(enable), stream(s)
+    bool pending = false;  // recorded by an asynchronous call, not read yet
+    bool status_pending = false;   // an asynchronous call copied its status here
+    mag::Status* host_status = nullptr;  // pinned host copy of the status block
+};
+constexpr int TIMER_SLOTS = 16;
+thread_local TimerSlot g_timers[TIMER_SLOTS];
+thread_local int g_timer_next = 0;
+
+TimerSlot* timer_slot(const void* ws, bool create)
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+    for (auto& t : g_timers)
+        if (t.dev == dev && t.ws == ws) return &t;
+    if (!create) return nullptr;
+    TimerSlot& t = g_timers[g_timer_next];
+    g_timer_next = (g_timer_next + 1) % TIMER_SLOTS;
+    for (auto& x : t.ev)
+        if (x) (void)hipEventDestroy(x);
+    mag::Status* keep = t.host_status;  // the pinned buffer is reused
+    t = TimerSlot{};
+    t.host_status = keep;
+    for (auto& x : t.ev)
+        if (hipEventCreate(&x) != hipSuccess) return nullptr;
+    if (!t.host_status) {
+        void* h = nullptr;
+        if (hipHostMalloc(&h, sizeof(mag::Status), hipHostMallocDefault) != hipSuccess)
+            return nullptr;
+        t.host_status = static_cast<mag::Status*>(h);
+    }
+    t.dev = dev;
+    t.ws = ws;
+    return &t;
+}
+
+struct EventTimer {
+    bool on;
+    hipStream_t stream;
+    TimerSlot* slot = nullptr;
+    EventTimer(bool enable, hipStream_t s, const void* ws) : on(enable), stream(s)
     {
         if (!on) return;
-        for (auto& x : ev)
-            if (hipEventCreate(&x) != hipSuccess) on = false;
-    }
-    ~EventTimer()
-    {
-        for (auto& x : ev)
-            if (x) (void)hipEventDestroy(x);
+        slot = timer_slot(ws, true);
+        on = slot != nullptr;
     }
     void mark(int i)
     {
-        if (on) (void)hipEventRecord(ev[i], stream);
+        if (on) (void)hipEventRecord(slot->ev[i], stream);
     }
     double ms(int a, int b) const
     {
         float v = 0.0f;
-        if (!on || hipEventElapsedTime(&v, ev[a], ev[b]) != hipSuccess) return 0.0;
+        if (!on || hipEventElapsedTime(&v, slot->ev[a], slot->ev[b]) != hipSuccess) return 0.0;
         return (double)v;
     }
 };
@@ -183,11 +219,14 @@ namespace mag {
 
 int device_cu_count()
 {
+    static int cached[16] = {};  // per device, queried once
     int dev = 0, cus = 0;
     if (hipGetDevice(&dev) != hipSuccess) return 256;
+    if (dev >= 0 && dev < 16 && cached[dev] > 0) return cached[dev];
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
         cus <= 0)
         return 256;
+    if (dev >= 0 && dev < 16) cached[dev] = cus;
     return cus;
 }
 
@@ -251,6 +290,59 @@ int plan_attribution(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t k
 // One attribution job: plan, carved workspace and launch parameters, shared
 // by the one-shot call and the chunked streaming calls.  pl.NT is the number
 // of tiles the workspace holds (the row stride of the per-tile arrays).
+// read a call's status block back (synchronizing its stream) and turn it into
+// the call's result
+int interpret_status(const mag::Status& st, mag_key_stats* per_key, mag_summary* summary)
+{
+    const int64_t n_keys = (int64_t)st.n_unique;
+    if (per_key) per_key->n_keys = std::min<int64_t>(n_keys, per_key->capacity);
+    if (summary) {
+        summary->trace_energy = st.trace_energy;
+        summary->idle_energy = st.idle_energy;
+        summary->attributed_energy = st.attributed_energy;
+        summary->n_clipped = (int64_t)st.n_clipped;
+        summary->n_keys = n_keys;
+    }
+    if (st.err & mag::ERR_TIMESTAMPS)
+        return fail(MAG_E_TIMESTAMPS, "timestamps not finite or not strictly increasing");
+    if (st.err & mag::ERR_POWER) return fail(MAG_E_POWER, "power sample negative or not finite");
+    if (st.err & mag::ERR_INTERVAL)
+        return fail(MAG_E_INTERVAL,
+                    "interval bound not finite, start > end, or a stream unsorted/overlapping");
+    if (per_key && (st.overflow || n_keys > per_key->capacity)) {
+        per_key->n_keys = n_keys;
+        snprintf(g_last_error, sizeof(g_last_error),
+                 "%lld distinct keys%s exceed the key capacity %lld", (long long)n_keys,
+                 st.overflow ? " (at least)" : "", (long long)per_key->capacity);
+        return MAG_E_CAPACITY;
+    }
+    return MAG_OK;
+}
+
+// copy a device status block to the host (through the workspace's pinned
+// buffer) and synchronize `stream`
+int read_status(const mag::Status* status, hipStream_t stream, mag::Status* out)
+{
+    TimerSlot* t = timer_slot(status, true);
+    mag::Status* dst = (t && t->host_status) ? t->host_status : out;
+    hipError_t e2;
+    if ((e2 = hipMemcpyAsync(dst, status, sizeof(mag::Status), hipMemcpyDeviceToHost, stream)) !=
+        hipSuccess)
+        return hip_fail(e2, "status copy");
+    if ((e2 = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e2, "synchronize");
+    if (dst != out) *out = *dst;
+    return MAG_OK;
+}
+
+int finish_status(const mag::Status* status, mag_key_stats* per_key, mag_summary* summary,
+                  hipStream_t stream)
+{
+    mag::Status st;
+    const int rc = read_status(status, stream, &st);
+    if (rc != MAG_OK) return rc;
+    return interpret_status(st, per_key, summary);
+}
+
 struct Job {
     Plan pl{};
     AttrWorkspace w{};
@@ -270,7 +362,8 @@ struct Job {
     // (any larger value while the trace's end is unknown); sample g of the
     // trace is t[g - base], P[g - base].
     hipError_t run_tiles(const double* t, const float* P, int64_t base, int64_t b_begin,
-                         int64_t b_end, int64_t nseg, int64_t NT)
+                         int64_t b_end, int64_t nseg, int64_t NT, hipEvent_t ev_start = nullptr,
+                         hipEvent_t ev_stop = nullptr)
     {
         if (b_end <= b_begin) return hipSuccess;
         mag::TileParams tp{};
@@ -299,7 +392,7 @@ struct Job {
         // vector loads need 16-byte aligned rows: aligned arrays and a base at a
         // multiple of 4 samples (every tile starts at a multiple of TILE)
         tp.aligned16 = (aligned(t, 16) && aligned(P, 16) && (base % 4) == 0) ? 1 : 0;
-        return mag::launch_tile(tp, stream);
+        return mag::launch_tile(tp, stream, ev_start, ev_stop);
     }
 
     // cross-tile intervals, endpoints outside the trace; the group-by state is
@@ -363,35 +456,7 @@ struct Job {
     // read the status block back and turn it into the call's result
     int conclude(mag_key_stats* per_key, mag_summary* summary)
     {
-        mag::Status st;
-        hipError_t e2;
-        if ((e2 = hipMemcpyAsync(&st, w.status, sizeof(st), hipMemcpyDeviceToHost, stream)) !=
-            hipSuccess)
-            return hip_fail(e2, "status copy");
-        if ((e2 = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e2, "synchronize");
-        const int64_t n_keys = (int64_t)st.n_unique;
-        if (per_key) per_key->n_keys = std::min<int64_t>(n_keys, per_key->capacity);
-        if (summary) {
-            summary->trace_energy = st.trace_energy;
-            summary->idle_energy = st.idle_energy;
-            summary->attributed_energy = st.attributed_energy;
-            summary->n_clipped = (int64_t)st.n_clipped;
-            summary->n_keys = n_keys;
-        }
-        if (st.err & mag::ERR_TIMESTAMPS)
-            return fail(MAG_E_TIMESTAMPS, "timestamps not finite or not strictly increasing");
-        if (st.err & mag::ERR_POWER) return fail(MAG_E_POWER, "power sample negative or not finite");
-        if (st.err & mag::ERR_INTERVAL)
-            return fail(MAG_E_INTERVAL,
-                        "interval bound not finite, start > end, or a stream unsorted/overlapping");
-        if (per_key && (st.overflow || n_keys > per_key->capacity)) {
-            per_key->n_keys = n_keys;
-            snprintf(g_last_error, sizeof(g_last_error),
-                     "%lld distinct keys%s exceed the key capacity %lld", (long long)n_keys,
-                     st.overflow ? " (at least)" : "", (long long)per_key->capacity);
-            return MAG_E_CAPACITY;
-        }
-        return MAG_OK;
+        return finish_status(w.status, per_key, summary, stream);
     }
 };
 
@@ -481,23 +546,72 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
 
     hipError_t e;
     const int64_t NT = job.pl.NT;
-    EventTimer timer((job.flags & MAG_TIME_KERNELS) != 0, stream);
-    timer.mark(0);
+    // timing (MAG_TIME_KERNELS): events 1 and 2 travel with the tile kernel's
+    // dispatch, event 3 follows the call's last kernel
+    EventTimer timer((job.flags & MAG_TIME_KERNELS) != 0, stream, workspace);
     if ((e = mag::launch_init(job.w.status, job.w.cnt_fin, (int64_t)job.pl.S * (NT + 1),
                               timestamps, n_samples, stream)) != hipSuccess)
         return hip_fail(e, "init");
-    timer.mark(1);
-    if ((e = job.run_tiles(timestamps, power, 0, 0, NT, n_samples - 1, NT)) != hipSuccess)
+    if ((e = job.run_tiles(timestamps, power, 0, 0, NT, n_samples - 1, NT,
+                           timer.on ? timer.slot->ev[1] : nullptr,
+                           timer.on ? timer.slot->ev[2] : nullptr)) != hipSuccess)
         return hip_fail(e, "tile kernel");
-    timer.mark(2);
     if ((e = job.fixups(n_samples, NT, per_key != nullptr)) != hipSuccess)
         return hip_fail(e, "fix-up kernels");
     if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
     timer.mark(3);
+    if (job.flags & MAG_ASYNC) {
+        // results, errors and timings come from mag_attribute_finish; the status
+        // block is copied to pinned host memory now, so that finishing needs
+        // no further device work
+        if (timer.on) timer.slot->pending = true;
+        TimerSlot* t = timer_slot(workspace, true);
+        if (t && t->host_status) {
+            if ((e = hipMemcpyAsync(t->host_status, job.w.status, sizeof(mag::Status),
+                                    hipMemcpyDeviceToHost, stream)) != hipSuccess)
+                return hip_fail(e, "status copy");
+            t->status_pending = true;
+        }
+        return MAG_OK;
+    }
     rc = job.conclude(per_key, summary);
     if (summary) {
         summary->tile_kernel_ms = timer.ms(1, 2);
-        summary->device_ms = timer.ms(0, 3);
+        summary->device_ms = timer.ms(1, 3);
+    }
+    return rc;
+}
+
+int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summary* summary,
+                         hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    // the status block is the first piece of every attribution workspace
+    TimerSlot* t = timer_slot(workspace, false);
+    int rc;
+    if (t && t->status_pending && t->host_status) {
+        // the call already copied its status to pinned memory on `stream`
+        t->status_pending = false;
+        hipError_t e2;
+        if ((e2 = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e2, "synchronize");
+        rc = interpret_status(*t->host_status, per_key, summary);
+    } else {
+        rc = finish_status(static_cast<const mag::Status*>(workspace), per_key, summary, stream);
+        t = timer_slot(workspace, false);
+    }
+    if (summary) {
+        summary->tile_kernel_ms = 0.0;
+        summary->device_ms = 0.0;
+    }
+    if (t && t->pending) {
+        t->pending = false;
+        float v = 0.0f;
+        if (summary && hipEventElapsedTime(&v, t->ev[1], t->ev[2]) == hipSuccess)
+            summary->tile_kernel_ms = (double)v;
+        if (summary && hipEventElapsedTime(&v, t->ev[1], t->ev[3]) == hipSuccess)
+            summary->device_ms = (double)v;
     }
     return rc;
 }
@@ -899,9 +1013,8 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
         return hip_fail(e, "init");
     if ((e = mag::launch_diff(p, stream)) != hipSuccess) return hip_fail(e, "diff kernels");
     mag::Status st;
-    if ((e = hipMemcpyAsync(&st, p.status, sizeof(st), hipMemcpyDeviceToHost, stream)) != hipSuccess)
-        return hip_fail(e, "status copy");
-    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    const int rc = read_status(p.status, stream, &st);
+    if (rc != MAG_OK) return rc;
     if (st.err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
     out->n_join = st.n_join;
     out->n_out = std::min<int64_t>(k, st.n_join);

@@ -46,6 +46,8 @@
 // start, and tail[a][b], the piece of the interval started in tile b and still
 // active at its end; k_cross adds them in tile order (attr_fix.hip).
 
+#include <hip/hip_ext.h>
+
 #include "mag_internal.hpp"
 
 namespace mag {
@@ -723,7 +725,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
 namespace {
 
 template <int SP>
-hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream)
+hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream, hipEvent_t ev_start,
+                         hipEvent_t ev_stop)
 {
     using K = decltype(&k_tile<SP>);
     const K kern = k_tile<SP>;
@@ -749,23 +752,29 @@ hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream)
     const int64_t waves = (int64_t)device_cu_count() * per_cu;
     p.tiles_per_wg = (ntiles + waves - 1) / waves;
     const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
-    hipLaunchKernelGGL(kern, dim3((unsigned)runs), dim3(WAVE), 0, stream, p);
+    if (ev_start || ev_stop)
+        // timing events travel with the dispatch: no marker packets around it
+        hipExtLaunchKernelGGL(kern, dim3((unsigned)runs), dim3(WAVE), 0, stream, ev_start, ev_stop,
+                              0, p);
+    else
+        hipLaunchKernelGGL(kern, dim3((unsigned)runs), dim3(WAVE), 0, stream, p);
     return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_tile(const TileParams& p, hipStream_t stream)
+hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_start,
+                       hipEvent_t ev_stop)
 {
     const int64_t ntiles = p.tile_end - p.tile_begin;
     if (ntiles <= 0) return hipSuccess;
     const int S = p.ss.S;
-    if (S == 1) return launch_tile_t<1>(p, ntiles, stream);
-    if (S == 2) return launch_tile_t<2>(p, ntiles, stream);
-    if (S <= 4) return launch_tile_t<4>(p, ntiles, stream);
-    if (S <= 8) return launch_tile_t<8>(p, ntiles, stream);
-    if (S <= 16) return launch_tile_t<16>(p, ntiles, stream);
-    return launch_tile_t<32>(p, ntiles, stream);
+    if (S == 1) return launch_tile_t<1>(p, ntiles, stream, ev_start, ev_stop);
+    if (S == 2) return launch_tile_t<2>(p, ntiles, stream, ev_start, ev_stop);
+    if (S <= 4) return launch_tile_t<4>(p, ntiles, stream, ev_start, ev_stop);
+    if (S <= 8) return launch_tile_t<8>(p, ntiles, stream, ev_start, ev_stop);
+    if (S <= 16) return launch_tile_t<16>(p, ntiles, stream, ev_start, ev_stop);
+    return launch_tile_t<32>(p, ntiles, stream, ev_start, ev_stop);
 }
 
 }  // namespace mag

@@ -59,7 +59,8 @@ __device__ int64_t wave_count_below(const uint64_t* a, int64_t n, uint64_t v, bo
 
 }  // namespace
 
-__global__ __launch_bounds__(256) void k_diff_check(const DiffParams p)
+// both key tables strictly ascending (the grid strides over the rows)
+__device__ __forceinline__ void check_ascending(const DiffParams& p)
 {
     unsigned bad = 0u;
     for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i + 1 < max(p.na, p.nb);
@@ -70,6 +71,8 @@ __global__ __launch_bounds__(256) void k_diff_check(const DiffParams p)
     if (bad) atomicOr(&p.status->err, ERR_KEYS);
 }
 
+__global__ __launch_bounds__(256) void k_diff_check(const DiffParams p) { check_ascending(p); }
+
 __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
 {
     __shared__ uint64_t bk[B_TILE];
@@ -78,6 +81,7 @@ __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
     __shared__ int lv[JOIN_ROWS];
     __shared__ int64_t sh_range[2];
     const int tid = threadIdx.x;
+    check_ascending(p);  // (in the same launch: a failed check voids the result anyway)
     const int64_t row0 = (int64_t)blockIdx.x * JOIN_ROWS;
     const int64_t rows = min((int64_t)JOIN_ROWS, p.na - row0);
     if (tid < 64) {
@@ -198,9 +202,11 @@ int64_t diff_max_candidates(int64_t na, int64_t k)
 
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream)
 {
-    const int64_t mx = max(p.na, p.nb);
-    const unsigned cb = (unsigned)max((int64_t)1, min((mx + 255) / 256, (int64_t)1024));
-    hipLaunchKernelGGL(k_diff_check, dim3(cb), dim3(256), 0, stream, p);
+    if (p.na == 0 || p.nb == 0) {
+        const int64_t mx = max(p.na, p.nb);
+        const unsigned cb = (unsigned)max((int64_t)1, min((mx + 255) / 256, (int64_t)1024));
+        hipLaunchKernelGGL(k_diff_check, dim3(cb), dim3(256), 0, stream, p);
+    }
     if (p.na > 0 && p.nb > 0) {
         const unsigned jb = (unsigned)((p.na + JOIN_ROWS - 1) / JOIN_ROWS);
         hipLaunchKernelGGL(k_diff_join, dim3(jb), dim3(JOIN_ROWS), 0, stream, p);

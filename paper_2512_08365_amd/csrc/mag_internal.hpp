@@ -173,8 +173,10 @@ __device__ __forceinline__ void lds_barrier()
 hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double* t, int64_t n,
                        hipStream_t stream);
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
-// tiles [p.tile_begin, p.tile_end) on persistent waves (sets the launch shape)
-hipError_t launch_tile(const TileParams& p, hipStream_t stream);
+// tiles [p.tile_begin, p.tile_end) on persistent waves (sets the launch shape);
+// ev_start / ev_stop (may be NULL) are recorded by the launch itself
+hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_start = nullptr,
+                       hipEvent_t ev_stop = nullptr);
 // intervals spanning tiles, endpoints outside the trace, clearing of the group-by state
 hipError_t launch_fix(const FixParams& p, hipStream_t stream);
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);

@@ -177,6 +177,42 @@ def test_device_detected_errors():
     torch.cuda.synchronize()
 
 
+def test_asynchronous_pair_equals_synchronous():
+    # both sides enqueued back to back, finished afterwards: the same results
+    import paper_2512_08365_amd as mag
+    A, B = synth.sides(1, 1)
+    ref = []
+    for c in (A, B):
+        gi, gk, summ, _ = run_gpu(c)
+        ref.append((gi, gk, summ))
+    pend = []
+    for c in (A, B):
+        d = to_gpu(c)
+        off = [int(x) for x in c["offsets"]]
+        pend.append(mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], n_streams=len(off) - 1,
+                                  stream_offsets=off, asynchronous=True))
+    for (gi, gk, summ), p in zip(ref, pend):
+        pi, pk, ps = p.finish()
+        for k in gi:
+            assert np.array_equal(pi[k].cpu().numpy(), gi[k]), k
+        assert np.array_equal(pk["keys"].cpu().numpy().view(np.uint64), gk["keys"])
+        assert np.array_equal(pk["count"].cpu().numpy(), gk["count"])
+        assert_energy_close(pk["sum"].cpu().numpy(), gk["sum"], "async key sums")
+        assert ps["n_keys"] == summ["n_keys"] and ps["n_clipped"] == summ["n_clipped"]
+        assert abs(ps["trace_energy"] - summ["trace_energy"]) <= 1e-12 * summ["trace_energy"]
+    # a device-detected error is reported by finish()
+    c = synth.tiny_case(8, n=5000, streams=2, per_stream=50)
+    c["P"] = c["P"].copy()
+    c["P"][77] = -1.0
+    d = to_gpu(c)
+    off = [int(x) for x in c["offsets"]]
+    p = mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], n_streams=len(off) - 1,
+                      stream_offsets=off, asynchronous=True)
+    with pytest.raises(mag.MagnetonError) as ei:
+        p.finish()
+    assert ei.value.code == -6
+
+
 def test_deterministic_per_interval():
     c = synth.long_trace(9, 60000, 4, 3000)
     a, ka, _, _ = run_gpu(c)
