@@ -75,6 +75,22 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
 // scalar registers for the whole kernel; opaque at every use so that no load
 // is hoisted out of a phase
 typedef const __attribute__((address_space(4))) TileParams* KArgs;
+// the value of a window entry past the end of its stream
+__device__ const double kPastEnd = INFINITY;
+
+// a global-memory pointer argument held in scalar registers, opaque to the
+// compiler: a per-lane choice between two such pointers stays a register
+// select instead of becoming a per-lane load of the chosen argument
+template <class T>
+using gptr = __attribute__((address_space(1))) T*;
+
+template <class T>
+__device__ __forceinline__ gptr<T> sreg(T* v)
+{
+    asm volatile("" : "+s"(v));
+    return (gptr<T>)v;
+}
+
 __device__ __forceinline__ KArgs kargs()
 {
     KArgs k = (KArgs)__builtin_amdgcn_kernarg_segment_ptr();
@@ -290,70 +306,46 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     auto wload = [&](int64_t cur, int r, int64_t off, int64_t len, bool& more) -> double {
         const int64_t q = cur + r;
         more = (r == WS - 1) && (q + 1 < len);
-        const bool ok = q < len;
         const KArgs k = kargs();
-        const double* ptr = ok ? (((q & 1) ? k->e : k->s) + off + (q >> 1))
-                               : k->t + ((int64_t)b0 * T - k->base);
-        const double v = *ptr;
-        return ok ? v : INFINITY;
+        // an entry past the stream's end reads +inf from device memory, so the
+        // value needs no select after its load and is first waited for where
+        // it is used
+        const gptr<const double> ptr = (q < len)
+                                           ? ((q & 1) ? sreg(k->e) : sreg(k->s)) + off + (q >> 1)
+                                           : (gptr<const double>)&kPastEnd;
+        return *ptr;
     };
     bool em0, em1;  // `more` flags of the prefetched window
     double ew0 = wload(bperm64(sq, wa0), wr0, woff0, wlen0, em0);
     double ew1 = wload(bperm64(sq, wa1), wr1, woff1, wlen1, em1);
 
-    // ---- samples of a tile into registers (lane k: local samples kC .. kC+C)
-    double tv[C + 1];
-    float pv[C + 1];
-    auto load_samples = [&](int b) {
+    // ---- samples of a tile into registers (lane k: local samples kC .. kC+C).
+    // A whole tile of a 16-byte aligned trace is fetched one tile ahead and
+    // kept in the vectors the loads produce until it is processed (unpacking
+    // them earlier would wait for the loads right after their issue); a short
+    // tile or an unaligned trace is read when its tile starts.
+    double2 pt[C / 2];
+    float4 pp[C / 4];
+    double ptl;  // local sample kC + C: the next lane's first (lane 63: the tile's last)
+    float ppl;
+    auto vector_tile = [&](int b) {
         const KArgs k = kargs();
-        const int64_t j0 = (int64_t)b * T;
-        const int L = (int)min((int64_t)T, k->nseg - j0);
-        const int64_t g = j0 + (int64_t)lane * C - k->base;
-        const double* tp = k->t;
-        const float* Pp = k->P;
-        if (L == T && k->aligned16) {
-            const double2* t2 = reinterpret_cast<const double2*>(tp + g);
-            const float4* P4 = reinterpret_cast<const float4*>(Pp + g);
+        return k->aligned16 && (int64_t)b * T + T <= k->nseg;
+    };
+    auto prefetch = [&](int b) {
+        const KArgs k = kargs();
+        const int64_t g = (int64_t)b * T + (int64_t)lane * C - k->base;
+        const double2* t2 = reinterpret_cast<const double2*>(k->t + g);
+        const float4* P4 = reinterpret_cast<const float4*>(k->P + g);
 #pragma unroll
-            for (int u = 0; u < C / 2; ++u) {
-                const double2 v = t2[u];
-                tv[2 * u] = v.x;
-                tv[2 * u + 1] = v.y;
-            }
+        for (int u = 0; u < C / 2; ++u) pt[u] = t2[u];
 #pragma unroll
-            for (int u = 0; u < C / 4; ++u) {
-                const float4 v = P4[u];
-                pv[4 * u] = v.x;
-                pv[4 * u + 1] = v.y;
-                pv[4 * u + 2] = v.z;
-                pv[4 * u + 3] = v.w;
-            }
-            // sample C of the lane is the next lane's first (lane 63: the tile's last)
-            if (lane == WAVE - 1) {
-                tv[C] = tp[g + C];
-                pv[C] = Pp[g + C];
-            } else {
-                tv[C] = 0.0;
-                pv[C] = 0.0f;
-            }
-        } else {
-            // a lane past the tile's last sample repeats the last one it has
-            // with zero power: missing segments have zero width and energy
-            const int have = min(max(L - lane * C, -1), C);  // last local sample of the lane
-#pragma unroll
-            for (int u = 0; u <= C; ++u) {
-                if (u <= have) {
-                    tv[u] = tp[g + u];
-                    pv[u] = Pp[g + u];
-                } else {
-                    tv[u] = (u > 0) ? tv[u - 1] : 0.0;
-                    pv[u] = 0.0f;
-                }
-            }
-        }
+        for (int u = 0; u < C / 4; ++u) pp[u] = P4[u];
+        ptl = k->t[g + C];
+        ppl = k->P[g + C];
     };
 
-    load_samples(b0);
+    if (vector_tile(b0)) prefetch(b0);
     unsigned err = 0u;
     double idle = 0.0;    // this lane's share of the idle energy
     double w_wave = 0.0;  // the wave's trace energy (uniform)
@@ -366,13 +358,34 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
 
         // ---- samples: checks, segment energies, tile-local prefix, staging
         {
-            if (L == T && kk->aligned16) {
-                // sample C from the next lane (lane 63 loaded its own)
-                const double tn = dpp_f64<DPP_WAVE_SHL1, 0xf>(tv[0]);
-                const float pn = dpp_f32<DPP_WAVE_SHL1, 0xf>(pv[0]);
-                if (lane != WAVE - 1) {
-                    tv[C] = tn;
-                    pv[C] = pn;
+            double tv[C + 1];
+            float pv[C + 1];
+            if (vector_tile(b)) {
+#pragma unroll
+                for (int u = 0; u < C / 2; ++u) {
+                    tv[2 * u] = pt[u].x;
+                    tv[2 * u + 1] = pt[u].y;
+                }
+#pragma unroll
+                for (int u = 0; u < C / 4; ++u) {
+                    pv[4 * u] = pp[u].x;
+                    pv[4 * u + 1] = pp[u].y;
+                    pv[4 * u + 2] = pp[u].z;
+                    pv[4 * u + 3] = pp[u].w;
+                }
+                tv[C] = ptl;
+                pv[C] = ppl;
+            } else {
+                // a lane past the tile's last sample repeats the last one it
+                // has with zero power: missing segments have zero width and energy
+                const int64_t g = j0 + (int64_t)lane * C - kk->base;
+                const int have = min(max(L - lane * C, -1), C);  // last local sample of the lane
+                double tl = 0.0;
+#pragma unroll
+                for (int u = 0; u <= C; ++u) {
+                    tv[u] = (u <= have) ? kk->t[g + u] : tl;
+                    pv[u] = (u <= have) ? kk->P[g + u] : 0.0f;
+                    tl = tv[u];
                 }
             }
             if (kk->validate) {
@@ -410,7 +423,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             w_wave += Wt;
         }
         // samples of the next tile (in flight during this tile's rounds)
-        if (b + 1 < b1) load_samples(b + 1);
+        if (b + 1 < b1 && vector_tile(b + 1)) prefetch(b + 1);
         if (slane) {
             const KArgs k = kargs();
             k->cnt[(int64_t)lane * (k->ld + 1) + b] = sq;
@@ -559,7 +572,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const int64_t gid = off_a + (q >> 1);
             if (real) {
                 const KArgs k = kargs();
-                int64_t* idx = (q & 1) ? k->end_idx : k->start_idx;
+                const gptr<int64_t> idx = (q & 1) ? sreg(k->end_idx) : sreg(k->start_idx);
                 if (idx) idx[gid] = j0 + j + 1;
             }
             // finite and not before the stream's previous endpoint
@@ -659,8 +672,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             }
             if (closes || carried) {
                 const KArgs k = kargs();
-                double* dst = (carried && !st_a) ? (k->head + (int64_t)my_a * k->ld + b)
-                                                 : (k->energy + gid);
+                const gptr<double> dst = (carried && !st_a) ? (sreg(k->head) + (int64_t)my_a * k->ld + b)
+                                                 : (sreg(k->energy) + gid);
                 *dst = carried ? acc_a + acc : acc;
             }
             // energy per active interval over the whole round (streams that stay
@@ -697,7 +710,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         // ---- interval still open at the tile's end: its piece of this tile
         if (slane && (sq & 1)) {
             const KArgs k = kargs();
-            double* dst = sstarted ? k->tail : k->head;
+            const gptr<double> dst = sstarted ? sreg(k->tail) : sreg(k->head);
             dst[(int64_t)lane * k->ld + b] = sacc;
         }
     }
