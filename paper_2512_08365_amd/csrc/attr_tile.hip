@@ -422,8 +422,6 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             }
             w_wave += Wt;
         }
-        // samples of the next tile (in flight during this tile's rounds)
-        if (b + 1 < b1 && vector_tile(b + 1)) prefetch(b + 1);
         if (slane) {
             const KArgs k = kargs();
             k->cnt[(int64_t)lane * (k->ld + 1) + b] = sq;
@@ -443,6 +441,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         double rs_x = t_begin, rs_right = 0.0, rs_Fn = 0.0;
         int rs_jm = __popcll(__ballot((sq & 1) != 0)) << 16;
 
+        bool first_round = true;
         for (;;) {
             // ---- the round's endpoints: a prefix of every stream's window
             const double xw0 = ew0, xw1 = ew1;
@@ -450,6 +449,11 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             sm.wx[lane + WAVE] = xw1;
             if (SP > 8) sm.inv[lane] = 0;  // no slot marked
             const uint64_t in0 = __ballot(xw0 <= tau_end), in1 = __ballot(xw1 <= tau_end);
+            // samples of the next tile, in flight during this tile's rounds;
+            // issued after the window is read, so that the wait for the window
+            // loads does not wait for them (loads complete in issue order)
+            if (first_round && b + 1 < b1 && vector_tile(b + 1)) prefetch(b + 1);
+            first_round = false;
             const uint64_t mo0 = __ballot(em0), mo1 = __ballot(em1);
             const int tot = __popcll(in0) + __popcll(in1);
             // stream lane a: its entries are bits [a WS, (a + 1) WS) of a 128-bit mask
@@ -492,10 +496,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             // the next round's window (this tile's next round, or the next
             // tile's first): both start at the cursors after this round
             const int64_t sqn = sq + ta;
-            if (!fin || b + 1 < b1) {
-                ew0 = wload(bperm64(sqn, wa0), wr0, woff0, wlen0, em0);
-                ew1 = wload(bperm64(sqn, wa1), wr1, woff1, wlen1, em1);
-            }
+            ew0 = wload(bperm64(sqn, wa0), wr0, woff0, wlen0, em0);
+            ew1 = wload(bperm64(sqn, wa1), wr1, woff1, wlen1, em1);
 
             // ---- round slot of this lane: stream my_a, rank my_r (lane Er: the tile's end)
             const bool real = lane < Er;
