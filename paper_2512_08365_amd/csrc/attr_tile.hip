@@ -75,6 +75,20 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
 // scalar registers for the whole kernel; opaque at every use so that no load
 // is hoisted out of a phase
 typedef const __attribute__((address_space(4))) TileParams* KArgs;
+// 1/d for d >= 0 (zero gives +inf) within about an ulp: the hardware
+// estimate refined by two Newton steps, far cheaper than a correctly rounded
+// division; the quotients it serves (an interpolation weight, an equal share)
+// need no more
+__device__ __forceinline__ double recip(double d)
+{
+    double r = __builtin_amdgcn_rcp(d);
+    double e = fma(-d, r, 1.0);
+    r = fma(r, e, r);
+    e = fma(-d, r, 1.0);
+    r = fma(r, e, r);
+    return (d > 0.0) ? r : INFINITY;
+}
+
 // the value of a window entry past the end of its stream
 __device__ const double kPastEnd = INFINITY;
 
@@ -434,7 +448,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         auto P_at = [&](int i) -> double { return (double)sm.P[i & (C - 1)][i >> 3]; };
         const double t_begin = t_at(0);
         const double tau_end = t_at(L);
-        const double inv_dt = (double)L / (tau_end - t_begin);
+        const double inv_dt = (double)L * recip(tau_end - t_begin);
         // the point the round starts from (uniform): the tile's first sample,
         // later the previous round's last endpoint -- x, the piece from x to the
         // end of its segment, F at that end, (segment + 1) | active after << 16
@@ -562,7 +576,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const double2 A0 = tF_at(j), A1 = tF_at(min(j + 1, L));
             const double pj = P_at(j), pj1 = P_at(min(j + 1, L));
             // interpolated power and the pieces of segment j left and right of x
-            const double rh = 1.0 / (A1.x - A0.x);
+            const double rh = recip(A1.x - A0.x);
             auto lerp = [&](double y) -> double {
                 return (y == A1.x) ? pj1 : pj + (pj1 - pj) * ((y - A0.x) * rh);
             };
@@ -651,7 +665,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
                 }
                 const double Q = same ? q_in : (pright + whole) + left;
                 const int mp = pe >> 16;
-                v = (has_gap && mp > 0) ? (kk->split ? Q / (double)mp : Q) : 0.0;
+                v = (has_gap && mp > 0) ? (kk->split ? Q * recip((double)mp) : Q) : 0.0;
                 idle += (has_gap && mp == 0) ? Q : 0.0;
                 if (has_gap) sm.wx[pos] = v;
             }
