@@ -39,7 +39,8 @@ extern "C" {
 /* ---------------------------------------------------------------- status */
 #define MAG_OK 0
 #define MAG_E_NULL (-1)       /* a required pointer is NULL                          */
-#define MAG_E_SIZE (-2)       /* n_samples < 2 or > MAG_MAX_SAMPLES, a negative count */
+#define MAG_E_SIZE (-2)       /* n_samples < 2 or > MAG_MAX_SAMPLES, a negative count, */
+                              /* a key capacity above MAG_MAX_KEYS                     */
 #define MAG_E_CAPACITY (-3)   /* more distinct keys than the key table capacity       */
 #define MAG_E_WORKSPACE (-4)  /* workspace too small (or misaligned: 256 B required)  */
 #define MAG_E_TIMESTAMPS (-5) /* timestamps not finite or not strictly increasing     */
@@ -70,6 +71,8 @@ extern "C" {
 #define MAG_MAX_STREAMS 32
 /* Longest trace one call (or one stream) accepts, in samples. */
 #define MAG_MAX_SAMPLES (1LL << 40)
+/* Largest key-table capacity (rows of per-key statistics) one call accepts. */
+#define MAG_MAX_KEYS (1LL << 28)
 
 typedef struct mag_attr_opts {
     int32_t n_streams;              /* >= 1; intervals are concatenated by stream   */

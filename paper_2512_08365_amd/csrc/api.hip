@@ -65,12 +65,11 @@ struct AttrWorkspace {
     int64_t* cnt_fin;
     double* head;
     double* tail;
+    double2* part;
     double* energy;
     unsigned long long* table;
     uint32_t* slot;
-    uint32_t* slot2id;
     uint64_t* ukey;
-    uint32_t* uslot;
     uint32_t* urank;
     double* mean;
     uint32_t* pcnt;
@@ -98,17 +97,16 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
     w.cnt_fin = c.take<int64_t>((size_t)pl.S * (pl.NT + 1));
     w.head = c.take<double>((size_t)pl.S * pl.NT);
     w.tail = c.take<double>((size_t)pl.S * pl.NT);
+    w.part = c.take<double2>((size_t)pl.NT);
     w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
     if (pl.staging) {
         w.stage_t = c.take<double>((size_t)mag::TILE + 1);
         w.stage_P = c.take<float>((size_t)mag::TILE + 1);
     }
     if (pl.H > 0) {
-        w.table = c.take<unsigned long long>(pl.H);
+        w.table = c.take<unsigned long long>(2 * ((size_t)pl.H + 1));
         w.slot = c.take<uint32_t>((size_t)std::max<int64_t>(pl.m, 1));
-        w.slot2id = c.take<uint32_t>((size_t)pl.H + 1);
         w.ukey = c.take<uint64_t>((size_t)pl.H + 1);
-        w.uslot = c.take<uint32_t>((size_t)pl.H + 1);
         w.urank = c.take<uint32_t>((size_t)pl.H + 1);
         w.mean = c.take<double>((size_t)std::max<int64_t>(pl.cap, 1));
         w.pcnt = c.take<uint32_t>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
@@ -272,6 +270,7 @@ int plan_attribution(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t k
     if (n_samples < 2) return fail(MAG_E_SIZE, "n_samples must be >= 2");
     if (n_samples > MAG_MAX_SAMPLES) return fail(MAG_E_SIZE, "n_samples exceeds MAG_MAX_SAMPLES");
     if (n_intervals < 0 || key_capacity < 0) return fail(MAG_E_SIZE, "negative size");
+    if (key_capacity > MAG_MAX_KEYS) return fail(MAG_E_SIZE, "key_capacity exceeds MAG_MAX_KEYS");
     int S;
     int rc = check_opts(opts, n_intervals, &S, flags, ss);
     if (rc) return rc;
@@ -387,6 +386,7 @@ struct Job {
         tp.head = w.head;
         tp.tail = w.tail;
         tp.status = w.status;
+        tp.part = w.part;
         tp.split = (flags & MAG_EQUAL_SPLIT) ? 1 : 0;
         tp.validate = validate() ? 1 : 0;
         // vector loads need 16-byte aligned rows: aligned arrays and a base at a
@@ -414,6 +414,7 @@ struct Job {
         fp.start_idx = start_idx;
         fp.end_idx = end_idx;
         fp.status = w.status;
+        fp.part = w.part;
         fp.validate = validate() ? 1 : 0;
         if (grouping && pl.m > 0 && pl.H > 0) {
             fp.table = w.table;
@@ -437,9 +438,7 @@ struct Job {
         gp.chunk = pl.chunk;
         gp.table = w.table;
         gp.slot = w.slot;
-        gp.slot2id = w.slot2id;
         gp.ukey = w.ukey;
-        gp.uslot = w.uslot;
         gp.urank = w.urank;
         gp.mean = w.mean;
         gp.pcnt = w.pcnt;
@@ -669,6 +668,7 @@ int state_regions(const mag_stream* h, Region* r)
     r[k++] = {j.w.cnt_fin, sizeof(int64_t) * S * (ld + 1)};
     r[k++] = {j.w.head, sizeof(double) * S * ld};
     r[k++] = {j.w.tail, sizeof(double) * S * ld};
+    r[k++] = {j.w.part, sizeof(double2) * ld};
     r[k++] = {j.w.stage_t, sizeof(double) * (mag::TILE + 1)};
     r[k++] = {j.w.stage_P, sizeof(float) * (mag::TILE + 1)};
     r[k++] = {j.energy, sizeof(double) * m};

@@ -24,6 +24,7 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
 // one launch after the tiles: three kinds of workgroups
 //   [0, nb_cross)               intervals whose endpoints lie in different tiles
 //   [nb_cross, + 32 S)          endpoints before t_0 or after t_{n-1}
+//   [.., + FOLD_BLOCKS)         the trace and idle energies of the tile waves
 //   [.., + nb_clear)            the group-by state, cleared for the grouping
 // ---------------------------------------------------------------------------
 namespace {
@@ -91,6 +92,42 @@ __device__ void fix_outside(const FixParams& p, int a, int64_t r, int64_t nthrea
 
 constexpr int FIX_THREADS = 256;
 constexpr int OUT_BLOCKS = 32;  // workgroups per stream for the outside endpoints
+constexpr int FOLD_BLOCKS = 256; // workgroups adding up the per-run trace and idle energies
+
+// the {trace, idle} energies the tile waves left at the first tile of their
+// runs; a run starts at tile 0 and at every tile where a wave stopped (its
+// cnt_fin entry is set)
+__device__ void fold_parts(const FixParams& p, int blk)
+{
+    __shared__ double2 red[FIX_THREADS / 64];
+    const int64_t NT = p.NT;
+    const int64_t per = (NT + FOLD_BLOCKS - 1) / FOLD_BLOCKS;
+    const int64_t lo = (int64_t)blk * per, hi = min(lo + per, NT);
+    double w = 0.0, idle = 0.0;
+    for (int64_t b = lo + threadIdx.x; b < hi; b += FIX_THREADS) {
+        // both loads issued together; other tiles' entries are never written
+        const int64_t f = p.cnt_fin[b];
+        const double2 v = p.part[b];
+        const bool start = (b == 0) || (f != CNT_UNSET);
+        w += start ? v.x : 0.0;
+        idle += start ? v.y : 0.0;
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        w += __shfl_xor(w, off);
+        idle += __shfl_xor(idle, off);
+    }
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = make_double2(w, idle);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double2 t = red[0];
+        for (int u = 1; u < FIX_THREADS / 64; ++u) {
+            t.x += red[u].x;
+            t.y += red[u].y;
+        }
+        if (t.x != 0.0) atomicAdd(&p.status->trace_energy, t.x);
+        if (t.y != 0.0) atomicAdd(&p.status->idle_energy, t.y);
+    }
+}
 
 }  // namespace
 
@@ -110,10 +147,15 @@ __global__ __launch_bounds__(FIX_THREADS) void k_fix(const FixParams p, int64_t 
                     (int64_t)OUT_BLOCKS * FIX_THREADS);
         return;
     }
-    const int64_t bc = bo - (int64_t)OUT_BLOCKS * p.ss.S;
+    const int64_t bf = bo - (int64_t)OUT_BLOCKS * p.ss.S;
+    if (bf < FOLD_BLOCKS) {
+        fold_parts(p, (int)bf);
+        return;
+    }
+    const int64_t bc = bf - FOLD_BLOCKS;
     for (int64_t h = bc * FIX_THREADS + threadIdx.x; h <= (int64_t)p.H;
          h += nb_clear * FIX_THREADS) {
-        if (h < (int64_t)p.H) p.table[h] = ~0ull;
+        reinterpret_cast<ulonglong2*>(p.table)[h] = make_ulonglong2(~0ull, ~0ull);  // empty, no id
         p.urank[h] = 0u;
     }
 }
@@ -184,7 +226,7 @@ hipError_t launch_fix(const FixParams& p, hipStream_t stream)
     const int64_t nb_cross = (total + FIX_THREADS - 1) / FIX_THREADS;
     const int64_t nb_clear =
         p.table ? std::min<int64_t>(((int64_t)p.H + FIX_THREADS) / FIX_THREADS, 2048) : 0;
-    const int64_t blocks = nb_cross + (int64_t)OUT_BLOCKS * p.ss.S + nb_clear;
+    const int64_t blocks = nb_cross + (int64_t)OUT_BLOCKS * p.ss.S + FOLD_BLOCKS + nb_clear;
     hipLaunchKernelGGL(k_fix, dim3((unsigned)blocks), dim3(FIX_THREADS), 0, stream, p, nb_cross,
                        nb_clear);
     return hipGetLastError();

@@ -731,13 +731,11 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         }
     }
 
-    // the wave's trace and idle energy
+    // the wave's trace and idle energy, at its first tile (k_fix adds them up:
+    // thousands of waves adding into one address would queue at the end)
     const double It = wave_sum(idle);
     const KArgs k = kargs();
-    if (lane == 0) {
-        atomicAdd(&k->status->trace_energy, w_wave);
-        atomicAdd(&k->status->idle_energy, It);
-    }
+    if (lane == 0) k->part[b0] = make_double2(w_wave, It);
     if (slane) {
         // where this wave stopped: the next wave must start there
         const int LD = (int)k->ld;

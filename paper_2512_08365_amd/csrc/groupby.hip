@@ -1,24 +1,31 @@
 // groupby.hip -- per-operator-key count, sum and M2 of the interval energies.
 //
-// The key table and the rank counters are cleared by k_fix, the launch before.
+// The key table (keys and ids) and the rank counters are cleared by k_fix,
+// the launch before.
 //
-// 1. k_key_insert + k_keymap: the 64-bit keys go into an open-addressing hash
-//    table (linear probing, 64-bit compare-and-swap; the all-ones key is kept
-//    out of band so any uint64 is a legal key).  Insertion (of the keys of a
-//    prefix of the intervals) de-duplicates in LDS first; the lookup pass then
-//    finds almost every key with a plain, cached load (a separate launch, so
-//    no cached line predates an insert) and inserts the rest.
-// 2. k_compact: the distinct keys are listed; a key's place in the list is its
-//    dense id.  k_rank: rank of each key = number of smaller keys (its row in
-//    the output, ascending by key).
-// 3. k_agg_sum / k_fin_sum: each workgroup aggregates one chunk of intervals
-//    into an LDS table indexed by dense id (count, sum); the partial tables are
+// 1. k_key_insert: the distinct keys of a prefix of the intervals go into an
+//    open-addressing hash table (linear probing, 64-bit compare-and-swap; the
+//    all-ones key is kept out of band in slot H so any uint64 is a legal key).
+//    A slot is 16 bytes, {key, id}, so a lookup reads both from one line.
+//    Each workgroup de-duplicates its part of the prefix in LDS first.
+// 2. k_compact: every occupied slot without an id takes the next dense id (its
+//    place in the distinct-key list).
+// 3. k_keymap: the id of every interval's key, found with plain cached loads
+//    (the table and the ids come from earlier launches).  A key first seen
+//    after the prefix is inserted and recorded as MISS | slot; k_compact, run
+//    again, gives it an id, which the aggregation passes look up.
+// 4. k_rank: rank of each key = number of smaller keys (its row in the output,
+//    ascending by key).
+// 5. k_agg_sum / k_fin_sum: each workgroup aggregates one chunk of intervals
+//    into an LDS table indexed by id (count, sum); the partial tables are
 //    reduced per key in chunk order, and the key, count and sum written to the
 //    key's row.  Per-workgroup atomics add the rows into the attributed energy.
-// 4. k_agg_m2 / k_fin_m2: second pass over the chunk for sum (E - mean)^2
+// 6. k_agg_m2 / k_fin_m2: second pass over the chunk for sum (E - mean)^2
 //    (the two-pass definition of M2).
 // Plain stores carry every partial result: device-scope atomics, which are
-// slow on this part, are used only for counters and one add per workgroup.
+// slow on this part, are used only for counters, inserts and one add per
+// workgroup.  Every thread requests all the loads of a batch before it uses
+// any of them, so a pass costs about one memory latency per batch.
 
 #include "mag_internal.hpp"
 
@@ -27,6 +34,8 @@ namespace mag {
 namespace {
 
 constexpr unsigned long long EMPTY_KEY = ~0ull;
+constexpr uint32_t NO_ID = 0xffffffffu;  // no id (also: table full)
+constexpr uint32_t MISS = 0x80000000u;   // MISS | slot: id assigned after the lookup pass
 
 // 64-bit finalizer of MurmurHash3 (Appleby): spreads keys over the table
 __device__ __forceinline__ uint64_t fmix64(uint64_t k)
@@ -39,48 +48,58 @@ __device__ __forceinline__ uint64_t fmix64(uint64_t k)
     return k;
 }
 
+// slot h of the table: {key, id}
+__device__ __forceinline__ unsigned long long* slot_key(const GroupParams& p, uint32_t h)
+{
+    return p.table + 2 * (size_t)h;
+}
+__device__ __forceinline__ ulonglong2 slot_load(const GroupParams& p, uint32_t h)
+{
+    return reinterpret_cast<const ulonglong2*>(p.table)[h];
+}
+
+// the id of an interval's key from what the lookup pass recorded (NO_ID: none)
+__device__ __forceinline__ uint32_t resolve_id(const GroupParams& p, uint32_t r)
+{
+    if (r == NO_ID || !(r & MISS)) return r;
+    const uint32_t h = r & ~MISS;
+    return (h <= p.H) ? (uint32_t)p.table[2 * (size_t)h + 1] : NO_ID;
+}
+
 }  // namespace
 
 // Insert the distinct keys of a prefix of the intervals.  Each workgroup first
 // de-duplicates its chunk in an LDS table; then every thread takes a few LDS
-// slots and inserts their keys into the global table, so a key costs one global
-// probe per workgroup and the probe chains of a workgroup run in parallel.
+// slots and inserts their keys into the global table, all of them side by side
+// (one probe round of every key per memory round trip).
 constexpr int INS_THREADS = 512;
 constexpr int INS_CHUNK = 4096;
 constexpr int INS_SLOTS = 8192;
 constexpr int INS_GROUPS = 64;  // the lookup pass inserts keys first seen later
-
-__device__ __forceinline__ void global_insert(const GroupParams& p, unsigned long long k)
-{
-    const uint32_t mask = p.H - 1u;
-    uint32_t h = (uint32_t)fmix64(k) & mask;
-    for (uint32_t probe = 0; probe < p.H; ++probe) {
-        // a device-coherent load first (the level-2 caches of the XCDs are not
-        // coherent with each other, so a plain load could keep returning a stale
-        // empty slot and force a swap per probe); a slot only ever changes from
-        // empty to its final key, so a non-empty value read here is final
-        const unsigned long long cur =
-            __hip_atomic_load(&p.table[h], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (cur == k) return;
-        if (cur == EMPTY_KEY) {
-            const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
-            if (old == EMPTY_KEY || old == k) return;
-        }
-        h = (h + 1u) & mask;
-    }
-    atomicOr(&p.status->overflow, 1u);
-}
+constexpr int INS_PER = INS_CHUNK / INS_THREADS;
+constexpr int INS_SPT = INS_SLOTS / INS_THREADS;
 
 __global__ __launch_bounds__(INS_THREADS) void k_key_insert(const GroupParams p, int64_t n_insert)
 {
     __shared__ unsigned long long lt[INS_SLOTS];
-    for (int v = threadIdx.x; v < INS_SLOTS; v += blockDim.x) lt[v] = EMPTY_KEY;
+    const int tid = threadIdx.x;
+    const int64_t lo = (int64_t)blockIdx.x * INS_CHUNK;
+    unsigned long long kv[INS_PER];
+#pragma unroll
+    for (int u = 0; u < INS_PER; ++u) {
+        const int64_t i = lo + tid + (int64_t)u * INS_THREADS;
+        kv[u] = (i < n_insert) ? p.keys[i] : EMPTY_KEY;
+    }
+    for (int v = tid; v < INS_SLOTS; v += INS_THREADS) lt[v] = EMPTY_KEY;
     __syncthreads();
-    const int64_t lo = (int64_t)blockIdx.x * INS_CHUNK, hi = min(lo + INS_CHUNK, n_insert);
-    for (int64_t i = lo + threadIdx.x; i < hi; i += blockDim.x) {
-        const unsigned long long k = p.keys[i];
+    bool special = false;
+#pragma unroll
+    for (int u = 0; u < INS_PER; ++u) {
+        const int64_t i = lo + tid + (int64_t)u * INS_THREADS;
+        const unsigned long long k = kv[u];
+        if (i >= n_insert) continue;
         if (k == EMPTY_KEY) {
-            atomicOr(&p.status->special, 1u);
+            special = true;
             continue;
         }
         uint32_t h = (uint32_t)fmix64(k) & (INS_SLOTS - 1);
@@ -90,78 +109,174 @@ __global__ __launch_bounds__(INS_THREADS) void k_key_insert(const GroupParams p,
             h = (h + 1u) & (INS_SLOTS - 1);
         }
     }
+    if (special) atomicOr(&p.status->special, 1u);
     __syncthreads();
-    for (int v = threadIdx.x; v < INS_SLOTS; v += blockDim.x) {
-        const unsigned long long k = lt[v];
-        if (k != EMPTY_KEY) global_insert(p, k);
+
+    const uint32_t mask = p.H - 1u;
+    unsigned long long key[INS_SPT];
+    uint32_t h[INS_SPT];
+    uint32_t pending = 0u;
+#pragma unroll
+    for (int u = 0; u < INS_SPT; ++u) {
+        key[u] = lt[tid + u * INS_THREADS];
+        h[u] = (uint32_t)fmix64(key[u]) & mask;
+        if (key[u] != EMPTY_KEY) pending |= 1u << u;
+    }
+    for (uint32_t probe = 0; pending != 0u && probe < p.H; ++probe) {
+        // device-coherent loads (the level-2 caches of the XCDs are not
+        // coherent with each other, so a plain load could keep returning a
+        // stale empty slot and force a swap per probe); a slot only ever
+        // changes from empty to its final key, so a non-empty value is final
+        unsigned long long cur[INS_SPT];
+#pragma unroll
+        for (int u = 0; u < INS_SPT; ++u)
+            cur[u] = ((pending >> u) & 1u)
+                         ? __hip_atomic_load(slot_key(p, h[u]), __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT)
+                         : 0ull;
+        unsigned long long old[INS_SPT];
+#pragma unroll
+        for (int u = 0; u < INS_SPT; ++u)
+            old[u] = (((pending >> u) & 1u) && cur[u] == EMPTY_KEY)
+                         ? atomicCAS(slot_key(p, h[u]), EMPTY_KEY, key[u])
+                         : cur[u];
+#pragma unroll
+        for (int u = 0; u < INS_SPT; ++u) {
+            if (!((pending >> u) & 1u)) continue;
+            if (old[u] == key[u] || (cur[u] == EMPTY_KEY && old[u] == EMPTY_KEY))
+                pending &= ~(1u << u);
+            else
+                h[u] = (h[u] + 1u) & mask;
+        }
+    }
+    if (pending) atomicOr(&p.status->overflow, 1u);
+}
+
+// ids for the occupied slots that have none yet (slot H: the all-ones key);
+// each workgroup counts its new ids, takes a range of them with one atomic,
+// and hands them out in slot order within the workgroup
+constexpr int CMP_THREADS = 1024;
+constexpr int CMP_PER = 8;  // slots per thread
+
+__global__ __launch_bounds__(CMP_THREADS) void k_compact(const GroupParams p)
+{
+    __shared__ uint32_t wtot[CMP_THREADS / 64];
+    __shared__ uint32_t wbase[CMP_THREADS / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int64_t b0 = (int64_t)blockIdx.x * CMP_THREADS * CMP_PER;
+    const bool special = p.status->special != 0u;
+    unsigned long long key[CMP_PER];
+    uint32_t cur[CMP_PER];
+#pragma unroll
+    for (int u = 0; u < CMP_PER; ++u) {
+        const int64_t h = b0 + (int64_t)u * CMP_THREADS + tid;
+        const ulonglong2 e = (h <= (int64_t)p.H) ? slot_load(p, (uint32_t)h)
+                                                 : make_ulonglong2(EMPTY_KEY, 0ull);
+        key[u] = e.x;
+        cur[u] = (uint32_t)e.y;
+    }
+    uint32_t mine = 0u;  // bit u: slot u of this thread takes a new id
+#pragma unroll
+    for (int u = 0; u < CMP_PER; ++u) {
+        const int64_t h = b0 + (int64_t)u * CMP_THREADS + tid;
+        const bool occ = (h < (int64_t)p.H) ? (key[u] != EMPTY_KEY)
+                                            : (h == (int64_t)p.H && special);
+        if (occ && cur[u] == NO_ID) mine |= 1u << u;
+    }
+    // exclusive prefix of the counts over the workgroup
+    const uint32_t c = (uint32_t)__popc(mine);
+    uint32_t incl = c;
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint32_t v = __shfl_up(incl, off);
+        if (lane >= off) incl += v;
+    }
+    if (lane == 63) wtot[wave] = incl;
+    __syncthreads();
+    if (tid == 0) {
+        uint32_t t = 0u;
+        for (int w = 0; w < CMP_THREADS / 64; ++w) {
+            wbase[w] = t;
+            t += wtot[w];
+        }
+        const uint32_t base = t ? atomicAdd(&p.status->n_unique, t) : 0u;
+        for (int w = 0; w < CMP_THREADS / 64; ++w) wbase[w] += base;
+    }
+    __syncthreads();
+    uint32_t id = wbase[wave] + incl - c;
+#pragma unroll
+    for (int u = 0; u < CMP_PER; ++u) {
+        if (!((mine >> u) & 1u)) continue;
+        const int64_t h = b0 + (int64_t)u * CMP_THREADS + tid;
+        p.ukey[id] = (h < (int64_t)p.H) ? key[u] : EMPTY_KEY;
+        p.table[2 * h + 1] = id;
+        ++id;
     }
 }
 
-// slot of every interval's key (the table holds most keys already, so this is
-// normally a plain cached probe)
-__global__ __launch_bounds__(256) void k_keymap(const GroupParams p)
+// the id of every interval's key (plain cached probes: the table and the ids
+// were written by earlier launches); keys missing from the table are inserted
+// and recorded as MISS | slot.  A thread looks up KM_BATCH intervals, spaced
+// a grid apart, with all their first probes in flight together.
+constexpr int KM_THREADS = 256;
+constexpr int KM_BATCH = 8;
+
+__device__ __noinline__ uint32_t keymap_probe(const GroupParams& p, unsigned long long k,
+                                              uint32_t h, bool& over)
+{
+    // the first probe missed: walk the chain, inserting the key if absent
+    const uint32_t mask = p.H - 1u;
+    for (uint32_t probe = 0; probe < p.H; ++probe) {
+        const ulonglong2 e = slot_load(p, h);
+        if (e.x == k) return ((uint32_t)e.y != NO_ID) ? (uint32_t)e.y : (MISS | h);
+        if (e.x == EMPTY_KEY) {
+            // a stale empty read is settled by the swap
+            const unsigned long long old = atomicCAS(slot_key(p, h), EMPTY_KEY, k);
+            if (old == EMPTY_KEY || old == k) return MISS | h;
+        }
+        h = (h + 1u) & mask;
+    }
+    over = true;
+    return NO_ID;
+}
+
+__global__ __launch_bounds__(KM_THREADS) void k_keymap(const GroupParams p)
 {
     const uint32_t H = p.H;
     const uint32_t mask = H - 1u;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < p.m;
-         i += (int64_t)gridDim.x * blockDim.x) {
-        const unsigned long long k = p.keys[i];
-        uint32_t slot = H + 1u;  // invalid
-        if (k == EMPTY_KEY) {
-            slot = H;
-            if (p.status->special == 0u) atomicOr(&p.status->special, 1u);
-        } else {
-            uint32_t h = (uint32_t)fmix64(k) & mask;
-            for (uint32_t probe = 0; probe < H; ++probe) {
-                // plain (cached) load: a slot only ever changes from empty to its
-                // final key, and the compare-and-swap below settles a stale read
-                unsigned long long cur = p.table[h];
-                if (cur == k) {
-                    slot = h;
-                    break;
-                }
-                if (cur == EMPTY_KEY) {
-                    const unsigned long long old = atomicCAS(&p.table[h], EMPTY_KEY, k);
-                    if (old == EMPTY_KEY || old == k) {
-                        slot = h;
-                        break;
-                    }
-                }
-                h = (h + 1u) & mask;
+    const int64_t T = (int64_t)gridDim.x * KM_THREADS;
+    bool special = false, over = false;
+    for (int64_t i0 = (int64_t)blockIdx.x * KM_THREADS + threadIdx.x; i0 < p.m;
+         i0 += T * KM_BATCH) {
+        unsigned long long k[KM_BATCH];
+#pragma unroll
+        for (int u = 0; u < KM_BATCH; ++u) {
+            const int64_t i = min(i0 + u * T, p.m - 1);  // in bounds; extra lanes repeat the last
+            k[u] = p.keys[i];
+        }
+        uint32_t h[KM_BATCH];
+#pragma unroll
+        for (int u = 0; u < KM_BATCH; ++u) h[u] = (uint32_t)fmix64(k[u]) & mask;
+        // every first probe is issued before the first one is used
+        asm volatile("" ::: "memory");
+        ulonglong2 e[KM_BATCH];
+#pragma unroll
+        for (int u = 0; u < KM_BATCH; ++u) e[u] = slot_load(p, h[u]);
+        asm volatile("" ::: "memory");
+#pragma unroll
+        for (int u = 0; u < KM_BATCH; ++u) {
+            uint32_t id = (uint32_t)e[u].y;
+            if (k[u] == EMPTY_KEY) {
+                special = true;
+                id = MISS | H;
+            } else if (e[u].x != k[u] || id == NO_ID) {
+                id = keymap_probe(p, k[u], h[u], over);
             }
-            if (slot > H) atomicOr(&p.status->overflow, 1u);
-        }
-        p.slot[i] = slot;
-    }
-}
-
-// list the occupied slots (order irrelevant: ranks come from key comparisons)
-__global__ __launch_bounds__(256) void k_compact(const GroupParams p)
-{
-    const int lane = threadIdx.x & 63;
-    // whole waves iterate together (the ballot below needs every lane)
-    const uint32_t span = ((p.H + 1u + 63u) / 64u) * 64u;
-    for (uint32_t h = blockIdx.x * blockDim.x + threadIdx.x; h < span; h += gridDim.x * blockDim.x) {
-        unsigned long long k = EMPTY_KEY;
-        bool occ = false;
-        if (h < p.H) {
-            k = p.table[h];
-            occ = (k != EMPTY_KEY);
-        } else if (h == p.H) {
-            occ = p.status->special != 0u;
-        }
-        // one counter update per wave: occupied slots take consecutive rows
-        const uint64_t ob = __ballot(occ);
-        uint32_t base = 0u;
-        if (lane == 0 && ob) base = atomicAdd(&p.status->n_unique, (uint32_t)__popcll(ob));
-        base = __shfl(base, 0);
-        if (occ) {
-            const uint32_t u = base + (uint32_t)__popcll(ob & ((1ull << lane) - 1ull));
-            p.ukey[u] = k;
-            p.uslot[u] = h;
-            p.slot2id[h] = u;
+            const int64_t i = i0 + u * T;
+            if (i < p.m) p.slot[i] = id;
         }
     }
+    if (special && p.status->special == 0u) atomicOr(&p.status->special, 1u);
+    if (over) atomicOr(&p.status->overflow, 1u);
 }
 
 // rank = number of distinct keys smaller than this one: the pairs (x, y) of key
@@ -197,6 +312,9 @@ __global__ __launch_bounds__(RANK_TILE) void k_rank(const GroupParams p)
     }
 }
 
+// intervals per thread whose loads are requested together
+constexpr int AGG_BATCH = 16;
+
 // chunk of intervals -> LDS table over ids [r0, r0 + AGG_IDS) -> partial table row
 __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
 {
@@ -213,24 +331,22 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
     }
     __syncthreads();
     const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
-    constexpr int U = 4;  // independent loads in flight per thread
-    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)U * AGG_THREADS) {
-        uint32_t sl[U];
-        double en[U];
+    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)AGG_BATCH * AGG_THREADS) {
+        uint32_t sl[AGG_BATCH];
+        double en[AGG_BATCH];
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
+        for (int k = 0; k < AGG_BATCH; ++k) {
             const int64_t i = i0 + (int64_t)k * AGG_THREADS;
-            sl[k] = (i < hi) ? p.slot[i] : 0xffffffffu;
+            sl[k] = (i < hi) ? p.slot[i] : NO_ID;
             en[k] = (i < hi) ? p.energy[i] : 0.0;
         }
-        int64_t id[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) id[k] = (sl[k] <= p.H) ? (int64_t)p.slot2id[sl[k]] - r0 : -1;
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            if (id[k] < 0 || id[k] >= nid) continue;
-            atomicAdd(&lcnt[id[k]], 1u);
-            atomicAdd(&lsum[id[k]], en[k]);
+        for (int k = 0; k < AGG_BATCH; ++k) {
+            const uint32_t id = resolve_id(p, sl[k]);
+            const int64_t d = (id == NO_ID) ? -1 : (int64_t)id - r0;
+            if (d < 0 || d >= nid) continue;
+            atomicAdd(&lcnt[d], 1u);
+            atomicAdd(&lsum[d], en[k]);
         }
     }
     __syncthreads();
@@ -256,6 +372,7 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
     uint64_t cnt = 0;
     double sum = 0.0;
     if (id < nk) {
+#pragma unroll 16
         for (int c = grp; c < p.nchunks; c += FIN_GROUPS) {
             cnt += p.pcnt[(int64_t)c * p.cap + id];
             sum += p.psum[(int64_t)c * p.cap + id];
@@ -303,24 +420,22 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
     }
     __syncthreads();
     const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
-    constexpr int U = 4;
-    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)U * AGG_THREADS) {
-        uint32_t sl[U];
-        double en[U];
+    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)AGG_BATCH * AGG_THREADS) {
+        uint32_t sl[AGG_BATCH];
+        double en[AGG_BATCH];
 #pragma unroll
-        for (int k = 0; k < U; ++k) {
+        for (int k = 0; k < AGG_BATCH; ++k) {
             const int64_t i = i0 + (int64_t)k * AGG_THREADS;
-            sl[k] = (i < hi) ? p.slot[i] : 0xffffffffu;
+            sl[k] = (i < hi) ? p.slot[i] : NO_ID;
             en[k] = (i < hi) ? p.energy[i] : 0.0;
         }
-        int64_t id[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) id[k] = (sl[k] <= p.H) ? (int64_t)p.slot2id[sl[k]] - r0 : -1;
-#pragma unroll
-        for (int k = 0; k < U; ++k) {
-            if (id[k] < 0 || id[k] >= nid) continue;
-            const double d = en[k] - lmean[id[k]];
-            atomicAdd(&lm2[id[k]], d * d);
+        for (int k = 0; k < AGG_BATCH; ++k) {
+            const uint32_t id = resolve_id(p, sl[k]);
+            const int64_t d = (id == NO_ID) ? -1 : (int64_t)id - r0;
+            if (d < 0 || d >= nid) continue;
+            const double x = en[k] - lmean[d];
+            atomicAdd(&lm2[d], x * x);
         }
     }
     __syncthreads();
@@ -336,6 +451,7 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupPar
     if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     double m2 = 0.0;
     if (id < nk)
+#pragma unroll 16
         for (int c = grp; c < p.nchunks; c += FIN_GROUPS) m2 += p.pm2[(int64_t)c * p.cap + id];
     qs[grp][kl] = m2;
     __syncthreads();
@@ -353,10 +469,15 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
     const int64_t n_ins = min(p.m, (int64_t)INS_CHUNK * INS_GROUPS);
     hipLaunchKernelGGL(k_key_insert, dim3((unsigned)((n_ins + INS_CHUNK - 1) / INS_CHUNK)),
                        dim3(INS_THREADS), 0, stream, p, n_ins);
-    const int64_t mb = min((p.m + 255) / 256, (int64_t)16384);
-    hipLaunchKernelGGL(k_keymap, dim3((unsigned)max(mb, (int64_t)1)), dim3(256), 0, stream, p);
-    const unsigned hb = (unsigned)min((int64_t)(p.H + 1 + 255) / 256, (int64_t)4096);
-    hipLaunchKernelGGL(k_compact, dim3(hb), dim3(256), 0, stream, p);
+    const unsigned hb =
+        (unsigned)(((int64_t)p.H + 1 + CMP_THREADS * CMP_PER - 1) / (CMP_THREADS * CMP_PER));
+    hipLaunchKernelGGL(k_compact, dim3(hb), dim3(CMP_THREADS), 0, stream, p);
+    const int64_t mb =
+        min((p.m + KM_THREADS * KM_BATCH - 1) / (KM_THREADS * KM_BATCH), (int64_t)8192);
+    hipLaunchKernelGGL(k_keymap, dim3((unsigned)max(mb, (int64_t)1)), dim3(KM_THREADS), 0, stream,
+                       p);
+    // ids for the keys the lookup pass inserted
+    hipLaunchKernelGGL(k_compact, dim3(hb), dim3(CMP_THREADS), 0, stream, p);
     // the distinct keys that can get a row are at most min(H + 1, cap + 1)
     // (more only on overflow, which is reported and ranked partially)
     const int64_t nmax = min((int64_t)p.H + 1, p.cap + 1);

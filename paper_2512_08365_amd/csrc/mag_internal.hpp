@@ -81,7 +81,8 @@ struct TileParams {
                         // the tile after it (CNT_UNSET where no workgroup ended)
     double* head;       // [S][ld] in-tile energy of the interval active at tile start
     double* tail;       // [S][ld] in-tile energy of the interval started in the tile, active at its end
-    Status* status;     // trace and idle energy are added here
+    Status* status;
+    double2* part;      // [ld] {trace, idle} energy of the wave whose run of tiles starts at b
     int split;
     int validate;
     int aligned16;      // t and P are 16-byte aligned (vector loads)
@@ -102,9 +103,10 @@ struct FixParams {
     int64_t* start_idx;
     int64_t* end_idx;
     Status* status;
+    const double2* part;  // per-run {trace, idle} energies (TileParams::part), added up here
     int validate;
     // group-by state cleared for the grouping that follows (table NULL: none)
-    unsigned long long* table;     // [H] key table: all ones = empty
+    unsigned long long* table;     // [2 (H+1)] {key, id} slots: all ones = empty / no id
     uint32_t H;
     uint32_t* urank;               // [H+1] rank counters
 };
@@ -117,11 +119,9 @@ struct GroupParams {
     int64_t cap;          // key rows available
     int nchunks;
     int64_t chunk;        // intervals per chunk
-    unsigned long long* table;  // [H]
-    uint32_t* slot;       // [m]
-    uint32_t* slot2id;    // [H+1] dense id of an occupied slot (its place in the list)
+    unsigned long long* table;  // [2 (H+1)] slot h = {key, id}; slot H: the all-ones key
+    uint32_t* slot;       // [m] id of each interval's key, or MISS | slot (k_keymap)
     uint64_t* ukey;       // [H+1] distinct keys, by dense id
-    uint32_t* uslot;      // [H+1]
     uint32_t* urank;      // [H+1] rank of each distinct key (zeroed, then counted)
     double* mean;         // [cap]
     uint32_t* pcnt;       // [nchunks][cap]
