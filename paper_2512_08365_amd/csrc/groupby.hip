@@ -218,7 +218,7 @@ __global__ __launch_bounds__(CMP_THREADS) void k_compact(const GroupParams p)
 // and recorded as MISS | slot.  A thread looks up KM_BATCH intervals, spaced
 // a grid apart, with all their first probes in flight together.
 constexpr int KM_THREADS = 256;
-constexpr int KM_BATCH = 8;
+constexpr int KM_BATCH = 4;
 
 __device__ __noinline__ uint32_t keymap_probe(const GroupParams& p, unsigned long long k,
                                               uint32_t h, bool& over)

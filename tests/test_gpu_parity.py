@@ -134,6 +134,22 @@ def test_extreme_keys():
     compare_attribution(c, label="extreme keys")
 
 
+@pytest.mark.parametrize("vocab", [1000, 9000])
+def test_keys_first_seen_after_the_insertion_prefix(vocab):
+    # more intervals than the key-insertion prefix; some keys, the all-ones key
+    # among them, occur only in the tail; a vocabulary that fits the LDS
+    # dictionary of the lookup pass and one that does not
+    c = synth.long_trace(11, 400000, 2, 160000, outside=False)
+    m = c["s"].shape[0]
+    rng = np.random.default_rng(vocab)
+    key = rng.integers(0, vocab, m).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
+    tail = np.arange(m) >= m - 20000
+    key[tail] = (rng.integers(0, 300, int(tail.sum())) + 10**6).astype(np.uint64)
+    key[m - 5] = np.uint64(2**64 - 1)
+    c["key"] = key
+    compare_attribution(c, label=f"late keys vocab{vocab}")
+
+
 def test_key_capacity_error():
     import paper_2512_08365_amd as mag
     c = synth.tiny_case(6, n=300, streams=1, per_stream=40, keys=30)
