@@ -93,8 +93,9 @@ __device__ __forceinline__ double recip(double d)
 __device__ const double kPastEnd = INFINITY;
 
 // a global-memory pointer argument held in scalar registers, opaque to the
-// compiler: a per-lane choice between two such pointers stays a register
-// select instead of becoming a per-lane load of the chosen argument
+// compiler: a per-lane choice between two such pointers (both taken first,
+// outside the choice) stays a register select instead of becoming a per-lane
+// load of the chosen argument or a branch
 template <class T>
 using gptr = __attribute__((address_space(1))) T*;
 
@@ -324,9 +325,9 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         // an entry past the stream's end reads +inf from device memory, so the
         // value needs no select after its load and is first waited for where
         // it is used
-        const gptr<const double> ptr = (q < len)
-                                           ? ((q & 1) ? sreg(k->e) : sreg(k->s)) + off + (q >> 1)
-                                           : (gptr<const double>)&kPastEnd;
+        const gptr<const double> pe = sreg(k->e), ps = sreg(k->s);
+        const gptr<const double> ptr = (q < len) ? ((q & 1) ? pe : ps) + off + (q >> 1)
+                                                 : (gptr<const double>)&kPastEnd;
         return *ptr;
     };
     bool em0, em1;  // `more` flags of the prefetched window
@@ -588,7 +589,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const int64_t gid = off_a + (q >> 1);
             if (real) {
                 const KArgs k = kargs();
-                const gptr<int64_t> idx = (q & 1) ? sreg(k->end_idx) : sreg(k->start_idx);
+                const gptr<int64_t> ie = sreg(k->end_idx), is = sreg(k->start_idx);
+                const gptr<int64_t> idx = (q & 1) ? ie : is;
                 if (idx) idx[gid] = j0 + j + 1;
             }
             // finite and not before the stream's previous endpoint
@@ -688,8 +690,9 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             }
             if (closes || carried) {
                 const KArgs k = kargs();
-                const gptr<double> dst = (carried && !st_a) ? (sreg(k->head) + (int64_t)my_a * k->ld + b)
-                                                 : (sreg(k->energy) + gid);
+                const gptr<double> ph = sreg(k->head), pen = sreg(k->energy);
+                const gptr<double> dst =
+                    (carried && !st_a) ? (ph + (int64_t)my_a * k->ld + b) : (pen + gid);
                 *dst = carried ? acc_a + acc : acc;
             }
             // energy per active interval over the whole round (streams that stay
@@ -726,7 +729,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         // ---- interval still open at the tile's end: its piece of this tile
         if (slane && (sq & 1)) {
             const KArgs k = kargs();
-            const gptr<double> dst = sstarted ? sreg(k->tail) : sreg(k->head);
+            const gptr<double> pt_ = sreg(k->tail), ph = sreg(k->head);
+            const gptr<double> dst = sstarted ? pt_ : ph;
             dst[(int64_t)lane * k->ld + b] = sacc;
         }
     }
