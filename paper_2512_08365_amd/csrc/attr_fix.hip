@@ -35,16 +35,18 @@ __device__ void fix_cross(const FixParams& p, int64_t idx)
     const int a = (int)(idx / (NT + 1));
     const int64_t b = idx - (int64_t)a * (NT + 1);
     const int64_t* c = p.cnt + (int64_t)a * (LD + 1);
+    // the three loads requested together
     const int64_t c0 = c[b];
-    const int64_t len = 2 * (p.ss.off[a + 1] - p.ss.off[a]);
+    const int64_t cprev = (b > 0) ? c[b - 1] : -1;
     const int64_t fin = p.cnt_fin[(int64_t)a * (LD + 1) + b];
+    const int64_t len = 2 * (p.ss.off[a + 1] - p.ss.off[a]);
     if (p.validate && b > 0 && b < NT && fin != CNT_UNSET && fin != c0) {
         // a wave stopped at tile b with a cursor other than the one the next
         // wave searched for: some stream is unsorted
         atomicOr(&p.status->err, ERR_INTERVAL);
     }
     if (!(c0 & 1) || c0 > len) return;         // no interval active at tile start
-    if (b > 0 && c[b - 1] == c0) return;       // not the first tile it is active at
+    if (cprev == c0) return;                   // not the first tile it is active at
     const int64_t gid = p.ss.off[a] + (c0 >> 1);
     double E = (b > 0) ? p.tail[(int64_t)a * LD + b - 1] : 0.0;
     for (int64_t bb = b; bb < NT && c[bb] == c0; ++bb) E += p.head[(int64_t)a * LD + bb];

@@ -73,9 +73,9 @@ __device__ __forceinline__ uint32_t resolve_id(const GroupParams& p, uint32_t r)
 // slots and inserts their keys into the global table, all of them side by side
 // (one probe round of every key per memory round trip).
 constexpr int INS_THREADS = 512;
-constexpr int INS_CHUNK = 4096;
-constexpr int INS_SLOTS = 8192;
-constexpr int INS_GROUPS = 64;  // the lookup pass inserts keys first seen later
+constexpr int INS_CHUNK = 2048;
+constexpr int INS_SLOTS = 4096;
+constexpr int INS_GROUPS = 128;  // the lookup pass inserts keys first seen later
 constexpr int INS_PER = INS_CHUNK / INS_THREADS;
 constexpr int INS_SPT = INS_SLOTS / INS_THREADS;
 
@@ -365,19 +365,27 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
 {
     __shared__ uint64_t qc[FIN_GROUPS][FIN_KEYS];
     __shared__ double qs[FIN_GROUPS][FIN_KEYS];
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
     const int kl = threadIdx.x % FIN_KEYS, grp = threadIdx.x / FIN_KEYS;
     const int64_t id = (int64_t)blockIdx.x * FIN_KEYS + kl;
-    if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
+    // every load is requested before the key count is read (rows up to the
+    // capacity exist; those past the count are ignored)
     uint64_t cnt = 0;
     double sum = 0.0;
-    if (id < nk) {
+    if (id < p.cap) {
 #pragma unroll 16
         for (int c = grp; c < p.nchunks; c += FIN_GROUPS) {
             cnt += p.pcnt[(int64_t)c * p.cap + id];
             sum += p.psum[(int64_t)c * p.cap + id];
         }
     }
+    uint32_t r = 0xffffffffu;
+    uint64_t key = 0;
+    if (grp == 0 && id < p.cap) {
+        r = p.urank[id];
+        key = p.ukey[id];
+    }
+    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     qc[grp][kl] = cnt;
     qs[grp][kl] = sum;
     __syncthreads();
@@ -389,9 +397,8 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
             cnt += qc[g][kl];
             sum += qs[g][kl];
         }
-        const uint32_t r = p.urank[id];
         if ((int64_t)r < p.cap) {
-            p.keys_out[r] = p.ukey[id];
+            p.keys_out[r] = key;
             p.count_out[r] = (int64_t)cnt;
             p.sum_out[r] = sum;
         }
@@ -445,20 +452,21 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
 __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupParams p)
 {
     __shared__ double qs[FIN_GROUPS][FIN_KEYS];
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
     const int kl = threadIdx.x % FIN_KEYS, grp = threadIdx.x / FIN_KEYS;
     const int64_t id = (int64_t)blockIdx.x * FIN_KEYS + kl;
-    if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
+    // loads requested before the key count is read, as in k_fin_sum
     double m2 = 0.0;
-    if (id < nk)
+    if (id < p.cap)
 #pragma unroll 16
         for (int c = grp; c < p.nchunks; c += FIN_GROUPS) m2 += p.pm2[(int64_t)c * p.cap + id];
+    const uint32_t r = (grp == 0 && id < p.cap) ? p.urank[id] : 0xffffffffu;
+    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     qs[grp][kl] = m2;
     __syncthreads();
     if (grp == 0 && id < nk) {
         m2 = 0.0;
         for (int g = 0; g < FIN_GROUPS; ++g) m2 += qs[g][kl];
-        const uint32_t r = p.urank[id];
         if ((int64_t)r < p.cap) p.m2_out[r] = m2;
     }
 }
