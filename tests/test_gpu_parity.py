@@ -150,6 +150,25 @@ def test_keys_first_seen_after_the_insertion_prefix(vocab):
     compare_attribution(c, label=f"late keys vocab{vocab}")
 
 
+def test_rows_not_16_byte_aligned():
+    # timestamps and power one element into their allocations: 8- and 4-byte
+    # aligned, so the tile kernel reads them without vector loads
+    import torch
+    c = synth.long_trace(21, 70001, 3, 900)
+    d = to_gpu(c)
+    for name, dt in (("t", torch.float64), ("P", torch.float32)):
+        buf = torch.empty(d[name].numel() + 1, dtype=dt, device=d[name].device)
+        buf[1:].copy_(d[name])
+        d[name] = buf[1:]
+        assert d[name].data_ptr() % 16 != 0
+    o, g = run_oracle(c)
+    gi, gk, _, _ = run_gpu(c, dev=d)
+    assert np.array_equal(gi["start_idx"], o["start_idx"])
+    assert np.array_equal(gi["end_idx"], o["end_idx"])
+    assert_energy_close(gi["energy"], o["energy"], "unaligned rows")
+    assert np.array_equal(gk["count"], g["count"])
+
+
 def test_key_capacity_error():
     import paper_2512_08365_amd as mag
     c = synth.tiny_case(6, n=300, streams=1, per_stream=40, keys=30)
