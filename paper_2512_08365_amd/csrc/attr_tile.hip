@@ -71,9 +71,8 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
 }
 
 // the kernel's arguments, read from the kernel-argument segment where used
-// (scalar loads through the constant cache) so that pointers do not occupy
-// scalar registers for the whole kernel; opaque at every use so that no load
-// is hoisted out of a phase
+// (scalar loads through the constant cache; the compiler keeps or reloads
+// them as scalar-register pressure allows)
 typedef const __attribute__((address_space(4))) TileParams* KArgs;
 // 1/d for d >= 0 (zero gives +inf) within about an ulp: the hardware
 // estimate refined by two Newton steps, far cheaper than a correctly rounded
@@ -108,9 +107,7 @@ __device__ __forceinline__ gptr<T> sreg(T* v)
 
 __device__ __forceinline__ KArgs kargs()
 {
-    KArgs k = (KArgs)__builtin_amdgcn_kernarg_segment_ptr();
-    asm volatile("" : "+s"(k));
-    return k;
+    return (KArgs)__builtin_amdgcn_kernarg_segment_ptr();
 }
 
 // lanes of one wave communicate through LDS without s_barrier: a wave's LDS
@@ -361,6 +358,28 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     };
 
     if (vector_tile(b0)) prefetch(b0);
+    // Outputs are written one round late, right after the next round's window
+    // has arrived: loads complete in issue order, so a store issued between a
+    // load and its use would make the use wait for the store as well.  Null:
+    // nothing pending.
+    gptr<int64_t> pend_idx = nullptr;  // the lane's endpoint index
+    int64_t pend_idx_v = 0;
+    gptr<double> pend_en = nullptr;    // an interval's energy, or a piece of it
+    double pend_en_v = 0.0;
+    gptr<int64_t> pend_cnt = nullptr;  // a stream's cursor at a tile's start
+    int64_t pend_cnt_v = 0;
+    gptr<double> pend_piece = nullptr; // a stream's open-interval piece of a tile
+    double pend_piece_v = 0.0;
+    auto flush = [&]() {
+        if (pend_idx) *pend_idx = pend_idx_v;
+        if (pend_en) *pend_en = pend_en_v;
+        if (pend_cnt) *pend_cnt = pend_cnt_v;
+        if (pend_piece) *pend_piece = pend_piece_v;
+        pend_idx = nullptr;
+        pend_en = nullptr;
+        pend_cnt = nullptr;
+        pend_piece = nullptr;
+    };
     unsigned err = 0u;
     double idle = 0.0;    // this lane's share of the idle energy
     double w_wave = 0.0;  // the wave's trace energy (uniform)
@@ -439,7 +458,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         }
         if (slane) {
             const KArgs k = kargs();
-            k->cnt[(int64_t)lane * (k->ld + 1) + b] = sq;
+            pend_cnt = sreg(k->cnt) + ((int64_t)lane * (k->ld + 1) + b);
+            pend_cnt_v = sq;
         }
         sacc = 0.0;
         sstarted = 0;
@@ -462,6 +482,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const double xw0 = ew0, xw1 = ew1;
             sm.wx[lane] = xw0;
             sm.wx[lane + WAVE] = xw1;
+            flush();  // the previous round's outputs, now that the window is here
             if (SP > 8) sm.inv[lane] = 0;  // no slot marked
             const uint64_t in0 = __ballot(xw0 <= tau_end), in1 = __ballot(xw1 <= tau_end);
             // samples of the next tile, in flight during this tile's rounds;
@@ -591,7 +612,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
                 const KArgs k = kargs();
                 const gptr<int64_t> ie = sreg(k->end_idx), is = sreg(k->start_idx);
                 const gptr<int64_t> idx = (q & 1) ? ie : is;
-                if (idx) idx[gid] = j0 + j + 1;
+                pend_idx = idx ? idx + gid : nullptr;
+                pend_idx_v = j0 + j + 1;
             }
             // finite and not before the stream's previous endpoint
             if (real && kk->validate && (!(fabs(x) < INFINITY) || !(xp <= x))) err |= ERR_INTERVAL;
@@ -691,9 +713,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             if (closes || carried) {
                 const KArgs k = kargs();
                 const gptr<double> ph = sreg(k->head), pen = sreg(k->energy);
-                const gptr<double> dst =
-                    (carried && !st_a) ? (ph + (int64_t)my_a * k->ld + b) : (pen + gid);
-                *dst = carried ? acc_a + acc : acc;
+                pend_en = (carried && !st_a) ? (ph + (int64_t)my_a * k->ld + b) : (pen + gid);
+                pend_en_v = carried ? acc_a + acc : acc;
             }
             // energy per active interval over the whole round (streams that stay
             // inside one interval through it)
@@ -730,10 +751,11 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         if (slane && (sq & 1)) {
             const KArgs k = kargs();
             const gptr<double> pt_ = sreg(k->tail), ph = sreg(k->head);
-            const gptr<double> dst = sstarted ? pt_ : ph;
-            dst[(int64_t)lane * k->ld + b] = sacc;
+            pend_piece = (sstarted ? pt_ : ph) + ((int64_t)lane * k->ld + b);
+            pend_piece_v = sacc;
         }
     }
+    flush();
 
     // the wave's trace and idle energy, at its first tile (k_fix adds them up:
     // thousands of waves adding into one address would queue at the end)
