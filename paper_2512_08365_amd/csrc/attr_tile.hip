@@ -703,12 +703,26 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const bool carried = real && (q & 1) && my_r == 0;
             const int lo = start ? pos + 1 : 0;
             const int hi = start ? (closes ? pos_next : G - 1) : (carried ? pos : -1);
-            double acc = 0.0;
-            for (int i = 0; __ballot(lo + i <= hi) != 0ull; i += 2) {
-                const double y0 = sm.wx[min(lo + i, WAVE - 1)];
-                const double y1 = sm.wx[min(lo + i + 1, WAVE - 1)];
-                acc += (lo + i <= hi) ? y0 : 0.0;
-                acc += (lo + i + 1 <= hi) ? y1 : 0.0;
+            // gaps [lo, hi] summed as a difference of the round's prefix over
+            // positions (lane l holds the gap ending at position l).  The
+            // difference carries about 12 ulp of the prefix in rounding error;
+            // where it is below 2^-16 of the prefix (that error could reach
+            // 1e-10 of it) the gaps are added directly instead
+            const double gl = (lane < G) ? sm.wx[lane] : 0.0;
+            const double gpre = scan_wave(gl);
+            const double g_hi = bpermf(gpre, max(hi, 0));
+            const double g_lo = bpermf(gpre, max(lo - 1, 0));
+            double acc = (hi < lo) ? 0.0 : g_hi - ((lo > 0) ? g_lo : 0.0);
+            const bool direct = (hi >= lo) && !(acc >= g_hi * 0x1p-16);
+            if (__ballot(direct) != 0ull) {
+                double d = 0.0;
+                for (int i = 0; __ballot(direct && lo + i <= hi) != 0ull; i += 2) {
+                    const double y0 = sm.wx[min(lo + i, WAVE - 1)];
+                    const double y1 = sm.wx[min(lo + i + 1, WAVE - 1)];
+                    d += (lo + i <= hi) ? y0 : 0.0;
+                    d += (lo + i + 1 <= hi) ? y1 : 0.0;
+                }
+                if (direct) acc = d;
             }
             if (closes || carried) {
                 const KArgs k = kargs();
@@ -718,8 +732,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             }
             // energy per active interval over the whole round (streams that stay
             // inside one interval through it)
-            double vall = 0.0;
-            if (__ballot(lane < SP && ta == 0 && (sq & 1)) != 0ull) vall = wave_sum(v);
+            const double vall = read_lane_f64(gpre, WAVE - 1);
             // the round's last entry is where the next round starts
             if (!fin) {
                 const int ll = __builtin_amdgcn_readfirstlane(sm.inv[Er - 1]);
