@@ -199,14 +199,20 @@ struct EventTimer {
         slot = timer_slot(ws, true);
         on = slot != nullptr;
     }
+    // timing is best effort: a failed event call reads as zero time, and its
+    // error is cleared so that it is not reported by a later launch check
     void mark(int i)
     {
-        if (on) (void)hipEventRecord(slot->ev[i], stream);
+        if (on && hipEventRecord(slot->ev[i], stream) != hipSuccess) (void)hipGetLastError();
     }
     double ms(int a, int b) const
     {
         float v = 0.0f;
-        if (!on || hipEventElapsedTime(&v, slot->ev[a], slot->ev[b]) != hipSuccess) return 0.0;
+        if (!on) return 0.0;
+        if (hipEventElapsedTime(&v, slot->ev[a], slot->ev[b]) != hipSuccess) {
+            (void)hipGetLastError();
+            return 0.0;
+        }
         return (double)v;
     }
 };
@@ -607,10 +613,17 @@ int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summ
     if (t && t->pending) {
         t->pending = false;
         float v = 0.0f;
-        if (summary && hipEventElapsedTime(&v, t->ev[1], t->ev[2]) == hipSuccess)
-            summary->tile_kernel_ms = (double)v;
-        if (summary && hipEventElapsedTime(&v, t->ev[1], t->ev[3]) == hipSuccess)
-            summary->device_ms = (double)v;
+        // best effort, as in EventTimer: a failure reads as zero and is cleared
+        if (summary) {
+            if (hipEventElapsedTime(&v, t->ev[1], t->ev[2]) == hipSuccess)
+                summary->tile_kernel_ms = (double)v;
+            else
+                (void)hipGetLastError();
+            if (hipEventElapsedTime(&v, t->ev[1], t->ev[3]) == hipSuccess)
+                summary->device_ms = (double)v;
+            else
+                (void)hipGetLastError();
+        }
     }
     return rc;
 }
