@@ -9,7 +9,11 @@ Pins of the oracle (see tests/test_oracle_pins.py): closed forms for constant,
 linear and quadratic power, exact dyadic cases, the equal-split examples,
 tiling/additivity/split invariants, brute force on tiny inputs, textbook
 lower_bound, M2 closed form and the sign convention of the relative difference
-printed in the paper's Table "tab:energy-profiling".
+printed in the paper's Table "tab:energy-profiling".  The counter (software
+replay) attribution is pinned in tests/test_oracle_counter_pins.py: exact
+dyadic closed forms, the delay and replay scenarios worked out by hand,
+numpy.interp, exact rational arithmetic and the invariants of a cumulative
+quantity.
 """
 from __future__ import annotations
 
@@ -52,6 +56,8 @@ def _load():
         lib.orc_lower_bound.restype = i64
         lib.orc_attribute.argtypes = [p, p, i64, p, p, i64, p, ctypes.c_int32, ctypes.c_int32,
                                       p, p, p, p]
+        lib.orc_counter_attribute.argtypes = [p, p, i64, ctypes.c_double, p, p, p, i64, p, p, p,
+                                              p]
         lib.orc_groupby.argtypes = [p, p, i64, p, p, p, p, p, p]
         lib.orc_diff.argtypes = [p, p, p, i64, p, p, p, i64, i64, p, p, p, p, p, p, p, p]
         lib.orc_ratio.argtypes = [ctypes.c_double, ctypes.c_double]
@@ -92,6 +98,32 @@ def attribute(t, P, s, e, offsets=None, equal_split: bool = True) -> dict:
     summ = np.zeros(4, dtype=np.float64)
     rc = _load().orc_attribute(_p(t), _p(P), t.shape[0], _p(s), _p(e), m, _p(off), n_streams,
                                1 if equal_split else 0, _p(energy), _p(si), _p(ei), _p(summ))
+    if rc != 0:
+        raise OracleError(rc)
+    return {"energy": energy, "start_idx": si, "end_idx": ei, "trace_energy": float(summ[0]),
+            "idle_energy": float(summ[1]), "attributed_energy": float(summ[2]),
+            "n_clipped": int(summ[3])}
+
+
+def counter_attribute(t, C, s, e, delay: float = 0.0, reps=None) -> dict:
+    """Per-window operator energy (J per replay) from a cumulative energy counter.
+
+    Readings C[j] taken at t[j] hold the energy used up to t[j] - delay; the
+    counter is interpolated linearly between readings and held outside them;
+    window i ran its operator reps[i] times (1 when reps is None).
+    """
+    t = _c(t, np.float64)
+    C = _c(C, np.float64)
+    s = _c(s, np.float64)
+    e = _c(e, np.float64)
+    m = s.shape[0]
+    r = None if reps is None else _c(reps, np.int32)
+    energy = np.zeros(m, dtype=np.float64)
+    si = np.zeros(m, dtype=np.int64)
+    ei = np.zeros(m, dtype=np.int64)
+    summ = np.zeros(4, dtype=np.float64)
+    rc = _load().orc_counter_attribute(_p(t), _p(C), t.shape[0], float(delay), _p(s), _p(e), _p(r),
+                                       m, _p(energy), _p(si), _p(ei), _p(summ))
     if rc != 0:
         raise OracleError(rc)
     return {"energy": energy, "start_idx": si, "end_idx": ei, "trace_energy": float(summ[0]),
