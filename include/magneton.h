@@ -53,6 +53,7 @@ extern "C" {
 #define MAG_E_ALIGN (-11)     /* a device array is not aligned to its element size    */
 #define MAG_E_KEYS (-12)      /* a key table passed to mag_diff is not strictly       */
                               /* ascending                                            */
+#define MAG_E_COUNTER (-13)   /* an energy-counter reading is not finite or decreases */
 
 /* ----------------------------------------------------------------- flags */
 /* Split the power at each instant equally among the intervals active at that
@@ -188,7 +189,8 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
                   size_t workspace_bytes, hipStream_t stream);
 
 /*
- * mag_attribute_finish -- complete a mag_attribute call made with MAG_ASYNC.
+ * mag_attribute_finish -- complete a mag_attribute (or mag_attribute_counter)
+ * call made with MAG_ASYNC.
  * The paper's comparison is between two systems running the same workload
  * (Section 3.2); attributing both traces back to back, and waiting once, keeps
  * the device busy while the host enqueues the second.
@@ -207,6 +209,68 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
  */
 int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summary* summary,
                          hipStream_t stream);
+
+/*
+ * mag_counter_workspace_size -- bytes of device workspace mag_attribute_counter
+ * needs for the given sizes and key-table capacity (0 when no per-key output is
+ * asked for).  Host only.  Returns MAG_OK, MAG_E_SIZE or MAG_E_NULL.
+ */
+int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
+                               size_t* bytes);
+
+/*
+ * mag_attribute_counter -- per-operator energy from a cumulative energy
+ * counter, the software mode of Section 5.2: vendor energy interfaces refresh
+ * at 10-50 Hz and lag the device, so each operator is replayed back to back
+ * until its window is long enough, and its energy is the counter's increase
+ * over the window divided by the number of replays.  This library's reading:
+ *   u_j    = timestamps[j] - delay (fp64): a reading taken at t_j holds the
+ *            energy used up to t_j - delay;
+ *   C^(x)  = linear interpolant of (u_j, counter[j]); C^(x) = counter[0] for
+ *            x <= u_0 and counter[n-1] for x >= u_{n-1};
+ *   E_i    = (C^(ends[i]) - C^(starts[i])) / replays[i].
+ * The increase is computed as the part of the start's segment after the
+ * start, plus the difference of the two readings that bound the whole
+ * segments in between, plus the part of the end's segment before the end; it
+ * is never a difference of two interpolated values.
+ * Per key: count, sum of E_i and M2, as mag_attribute.
+ *
+ * Arguments (device arrays unless noted):
+ *   timestamps[n_samples] fp64 reading times (s); timestamps - delay strictly
+ *                          increasing and finite
+ *   counter[n_samples]    fp64 cumulative energy (J), finite, non-decreasing
+ *   delay                 host fp64, seconds (finite; may be 0 or negative)
+ *   starts/ends[n_intervals] fp64 replay windows, one sequence:
+ *                          starts[i] <= ends[i] <= starts[i+1]
+ *   replays[n_intervals]  int32 >= 1, or NULL for one run per window
+ *   op_keys[n_intervals]  uint64 operator key; may be NULL when per_key is NULL
+ *   flags                 MAG_SKIP_VALIDATE | MAG_TIME_KERNELS | MAG_ASYNC
+ *                          (other bits are ignored)
+ *   per_interval          energy = E_i (J per run), start_idx / end_idx =
+ *                          lower_bound of starts[i] / ends[i] among u; may be
+ *                          NULL
+ *   keys_out, per_key     as mag_attribute
+ *   summary               host, may be NULL: trace_energy = counter[n-1] -
+ *                          counter[0]; idle_energy = counter increase outside
+ *                          every window; attributed_energy = sum of E_i;
+ *                          n_clipped = windows with start < u_0 or end >
+ *                          u_{n-1}; tile_kernel_ms = duration of the window
+ *                          kernel
+ *   workspace             device, >= mag_counter_workspace_size(...) bytes,
+ *                          256-byte aligned
+ * Synchronizes `stream` (with MAG_ASYNC: returns once the work is enqueued;
+ * mag_attribute_finish completes it).  Errors: MAG_E_NULL, MAG_E_SIZE,
+ * MAG_E_WORKSPACE, MAG_E_ALIGN, MAG_E_TIMESTAMPS (also for a non-finite delay)
+ * (host-detected); MAG_E_TIMESTAMPS, MAG_E_COUNTER, MAG_E_INTERVAL (also for
+ * replays < 1) (device-detected unless MAG_SKIP_VALIDATE); MAG_E_CAPACITY;
+ * MAG_E_HIP.
+ */
+int mag_attribute_counter(const double* timestamps, const double* counter, int64_t n_samples,
+                          double delay, const double* starts, const double* ends,
+                          const int32_t* replays, const uint64_t* op_keys, int64_t n_intervals,
+                          uint32_t flags, mag_interval_out* per_interval, uint64_t* keys_out,
+                          mag_key_stats* per_key, mag_summary* summary, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream);
 
 /*
  * mag_diff_workspace_size -- device workspace bytes for mag_diff.  Host only.

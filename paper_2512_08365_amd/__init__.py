@@ -14,8 +14,8 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "diff", "Stream", "workspace_size",
-           "stream_workspace_size", "diff_workspace_size", "version", "EQUAL_SPLIT",
+__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "Stream", "workspace_size",
+           "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
 
 EQUAL_SPLIT = N.MAG_EQUAL_SPLIT
@@ -177,6 +177,80 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
         # the inputs and the options stay referenced until finish()
         return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys))
     return build()
+
+
+def counter_workspace_size(n_samples: int, n_intervals: int, key_capacity: int = 0) -> int:
+    b = ctypes.c_size_t(0)
+    _check(_lib().mag_counter_workspace_size(n_samples, n_intervals, key_capacity, ctypes.byref(b)))
+    return int(b.value)
+
+
+def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None,
+                      validate: bool = True, key_capacity: int | None = None,
+                      indices: bool = True, workspace=None, out=None, time_kernels: bool = False):
+    """Per-operator energy from a cumulative energy counter (software replay mode).
+
+    t: float64 [n] reading times (s), C: float64 [n] cumulative energy (J),
+    delay: seconds by which the counter lags (a reading at t holds the energy
+    used up to t - delay), s/e: float64 [m] replay windows (one sequence),
+    replays: int32 [m] runs per window or None, keys: int64 [m] or None.
+    Returns (per_interval, per_key, summary) as attribute() does; the energies
+    are per run (the window's counter increase over its replay count).
+    """
+    lib = _lib()
+    n = int(t.shape[0])
+    m = int(s.shape[0])
+    dev = t.device
+    flags = (0 if validate else SKIP_VALIDATE) | (N.MAG_TIME_KERNELS if time_kernels else 0)
+    group = keys is not None
+    cap = int(key_capacity) if key_capacity is not None else max(1, m)
+    ws_bytes = counter_workspace_size(n, m, cap if group else 0)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    out = out or {}
+    energy = out.get("energy")
+    if energy is None:
+        energy = torch.empty(m, dtype=torch.float64, device=dev)
+    si = ei = None
+    if indices:
+        si = out.get("start_idx")
+        ei = out.get("end_idx")
+        if si is None:
+            si = torch.empty(m, dtype=torch.int64, device=dev)
+        if ei is None:
+            ei = torch.empty(m, dtype=torch.int64, device=dev)
+    pio = N.IntervalOut(_dev_ptr(energy, torch.float64, "energy"),
+                        _dev_ptr(si, torch.int64, "start_idx"), _dev_ptr(ei, torch.int64, "end_idx"))
+    ks = None
+    kout = ksum = km2 = kcnt = None
+    if group:
+        kout = torch.empty(cap, dtype=torch.int64, device=dev)
+        ksum = torch.empty(cap, dtype=torch.float64, device=dev)
+        km2 = torch.empty(cap, dtype=torch.float64, device=dev)
+        kcnt = torch.empty(cap, dtype=torch.int64, device=dev)
+        ks = N.KeyStats(ksum.data_ptr(), km2.data_ptr(), kcnt.data_ptr(), cap, 0)
+    summ = N.Summary()
+    rc = lib.mag_attribute_counter(
+        _dev_ptr(t, torch.float64, "t"), _dev_ptr(C, torch.float64, "C"), n, float(delay),
+        _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
+        _dev_ptr(replays, torch.int32, "replays"),
+        _dev_ptr(keys, torch.int64, "keys") if group else None, m, flags, ctypes.byref(pio),
+        kout.data_ptr() if group else None, ctypes.byref(ks) if group else None,
+        ctypes.byref(summ), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
+    _check(rc)
+    per_interval = {"energy": energy}
+    if indices:
+        per_interval["start_idx"] = si
+        per_interval["end_idx"] = ei
+    per_key = None
+    if group:
+        nk = int(ks.n_keys)
+        per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+    summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
+               "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
+               "n_keys": int(summ.n_keys), "kernel_ms": summ.tile_kernel_ms,
+               "device_ms": summ.device_ms}
+    return per_interval, per_key, summary
 
 
 def diff(a: dict, b: dict, k: int, workspace=None):

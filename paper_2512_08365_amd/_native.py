@@ -23,6 +23,7 @@ MAG_E_STATE = -9
 MAG_E_HIP = -10
 MAG_E_ALIGN = -11
 MAG_E_KEYS = -12
+MAG_E_COUNTER = -13
 
 MAG_EQUAL_SPLIT = 0x1
 MAG_SKIP_VALIDATE = 0x2
@@ -33,6 +34,7 @@ MAG_MAX_STREAMS = 32
 # every symbol include/magneton.h declares
 EXPORTED = (
     "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_finish",
+    "mag_counter_workspace_size", "mag_attribute_counter",
     "mag_diff_workspace_size", "mag_diff",
     "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
     "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
@@ -87,6 +89,12 @@ def load(path: str = LIB_PATH):
     lib.mag_attribute.restype = ctypes.c_int
     lib.mag_attribute_finish.argtypes = [c_vp, P(KeyStats), P(Summary), c_vp]
     lib.mag_attribute_finish.restype = ctypes.c_int
+    lib.mag_counter_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
+    lib.mag_counter_workspace_size.restype = ctypes.c_int
+    lib.mag_attribute_counter.argtypes = [c_vp, c_vp, c_i64, ctypes.c_double, c_vp, c_vp, c_vp,
+                                          c_vp, c_i64, ctypes.c_uint32, P(IntervalOut), c_vp,
+                                          P(KeyStats), P(Summary), c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_attribute_counter.restype = ctypes.c_int
     lib.mag_diff_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
     lib.mag_diff_workspace_size.restype = ctypes.c_int
     lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,

@@ -88,6 +88,8 @@ void plan_groupby(Plan& pl)
     pl.chunk = (pl.m + nc - 1) / nc;
 }
 
+void carve_groupby(Carver& c, const Plan& pl, AttrWorkspace& w);
+
 size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
 {
     Carver c;
@@ -103,6 +105,24 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
         w.stage_t = c.take<double>((size_t)mag::TILE + 1);
         w.stage_P = c.take<float>((size_t)mag::TILE + 1);
     }
+    carve_groupby(c, pl, w);
+    return c.off;
+}
+
+// the counter mode: status, per-chunk figures, energies, group-by state
+size_t carve_counter(const Plan& pl, void* ws, AttrWorkspace& w)
+{
+    Carver c;
+    c.base = static_cast<char*>(ws);
+    w.status = c.take<mag::Status>(1);
+    w.part = c.take<double2>((size_t)pl.NT);
+    w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
+    carve_groupby(c, pl, w);
+    return c.off;
+}
+
+void carve_groupby(Carver& c, const Plan& pl, AttrWorkspace& w)
+{
     if (pl.H > 0) {
         w.table = c.take<unsigned long long>(2 * ((size_t)pl.H + 1));
         w.slot = c.take<uint32_t>((size_t)std::max<int64_t>(pl.m, 1));
@@ -113,7 +133,6 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
         w.psum = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.pm2 = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
     }
-    return c.off;
 }
 
 int check_opts(const mag_attr_opts* opts, int64_t m, int* S, uint32_t* flags, mag::StreamSet* ss)
@@ -258,6 +277,7 @@ const char* mag_strerror(int status)
     case MAG_E_HIP: return "HIP runtime error";
     case MAG_E_ALIGN: return "device array misaligned";
     case MAG_E_KEYS: return "key table not strictly ascending";
+    case MAG_E_COUNTER: return "energy-counter reading not finite or decreasing";
     default: return "unknown status";
     }
 }
@@ -310,6 +330,8 @@ int interpret_status(const mag::Status& st, mag_key_stats* per_key, mag_summary*
     }
     if (st.err & mag::ERR_TIMESTAMPS)
         return fail(MAG_E_TIMESTAMPS, "timestamps not finite or not strictly increasing");
+    if (st.err & mag::ERR_COUNTER)
+        return fail(MAG_E_COUNTER, "energy-counter reading not finite or decreasing");
     if (st.err & mag::ERR_POWER) return fail(MAG_E_POWER, "power sample negative or not finite");
     if (st.err & mag::ERR_INTERVAL)
         return fail(MAG_E_INTERVAL,
@@ -515,6 +537,29 @@ int prepare(Job& job, int64_t n_samples, const double* starts, const double* end
 
 }  // namespace
 
+namespace {
+
+int plan_counter(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t key_capacity)
+{
+    if (n_samples < 2) return fail(MAG_E_SIZE, "n_samples must be >= 2");
+    if (n_samples > MAG_MAX_SAMPLES) return fail(MAG_E_SIZE, "n_samples exceeds MAG_MAX_SAMPLES");
+    if (n_intervals < 0 || key_capacity < 0) return fail(MAG_E_SIZE, "negative size");
+    if (key_capacity > MAG_MAX_KEYS) return fail(MAG_E_SIZE, "key_capacity exceeds MAG_MAX_KEYS");
+    pl = Plan{};
+    pl.n = n_samples;
+    pl.m = n_intervals;
+    pl.S = 1;
+    // NT: chunks of windows, one wave each (at least one, which checks the readings)
+    pl.NT = std::max<int64_t>(1, (n_intervals + mag::CNT_CHUNK - 1) / mag::CNT_CHUNK);
+    pl.cap = key_capacity;
+    pl.H = 0;
+    pl.staging = false;
+    if (key_capacity > 0) plan_groupby(pl);
+    return MAG_OK;
+}
+
+}  // namespace
+
 extern "C" {
 
 int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
@@ -569,6 +614,114 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         // results, errors and timings come from mag_attribute_finish; the status
         // block is copied to pinned host memory now, so that finishing needs
         // no further device work
+        if (timer.on) timer.slot->pending = true;
+        TimerSlot* t = timer_slot(workspace, true);
+        if (t && t->host_status) {
+            if ((e = hipMemcpyAsync(t->host_status, job.w.status, sizeof(mag::Status),
+                                    hipMemcpyDeviceToHost, stream)) != hipSuccess)
+                return hip_fail(e, "status copy");
+            t->status_pending = true;
+        }
+        return MAG_OK;
+    }
+    rc = job.conclude(per_key, summary);
+    if (summary) {
+        summary->tile_kernel_ms = timer.ms(1, 2);
+        summary->device_ms = timer.ms(1, 3);
+    }
+    return rc;
+}
+
+int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
+                               size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    Plan pl;
+    int rc = plan_counter(pl, n_samples, n_intervals, key_capacity);
+    if (rc) return rc;
+    AttrWorkspace w{};
+    *bytes = carve_counter(pl, nullptr, w);
+    return MAG_OK;
+}
+
+int mag_attribute_counter(const double* timestamps, const double* counter, int64_t n_samples,
+                          double delay, const double* starts, const double* ends,
+                          const int32_t* replays, const uint64_t* op_keys, int64_t n_intervals,
+                          uint32_t flags, mag_interval_out* per_interval, uint64_t* keys_out,
+                          mag_key_stats* per_key, mag_summary* summary, void* workspace,
+                          size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!timestamps || !counter) return fail(MAG_E_NULL, "timestamps/counter is NULL");
+    if (!aligned(timestamps, 8) || !aligned(counter, 8))
+        return fail(MAG_E_ALIGN, "input array not aligned to its element size");
+    if (!(delay - delay == 0.0)) return fail(MAG_E_TIMESTAMPS, "delay is not finite");
+    int rc;
+    if (per_key && (rc = check_key_outputs(keys_out, per_key)) != MAG_OK) return rc;
+    Job job;
+    const int64_t cap = per_key ? per_key->capacity : 0;
+    if ((rc = plan_counter(job.pl, n_samples, n_intervals, cap)) != MAG_OK) return rc;
+    if (n_intervals > 0 && (!starts || !ends)) return fail(MAG_E_NULL, "starts/ends is NULL");
+    if (cap > 0 && n_intervals > 0 && !op_keys) return fail(MAG_E_NULL, "op_keys is NULL");
+    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if ((starts && !aligned(starts, 8)) || (ends && !aligned(ends, 8)) ||
+        (op_keys && !aligned(op_keys, 8)) || (replays && !aligned(replays, 4)))
+        return fail(MAG_E_ALIGN, "window array not aligned to its element size");
+    if (per_interval && ((per_interval->energy && !aligned(per_interval->energy, 8)) ||
+                         (per_interval->start_idx && !aligned(per_interval->start_idx, 8)) ||
+                         (per_interval->end_idx && !aligned(per_interval->end_idx, 8))))
+        return fail(MAG_E_ALIGN, "per-interval output not aligned to its element size");
+    const size_t need = carve_counter(job.pl, nullptr, job.w);
+    if (workspace_bytes < need) {
+        snprintf(g_last_error, sizeof(g_last_error), "workspace needs %zu bytes, got %zu", need,
+                 workspace_bytes);
+        return MAG_E_WORKSPACE;
+    }
+    carve_counter(job.pl, workspace, job.w);
+    job.flags = flags;
+    job.s = starts;
+    job.e = ends;
+    job.keys = op_keys;
+    job.energy = (per_interval && per_interval->energy) ? per_interval->energy : job.w.energy;
+    job.start_idx = per_interval ? per_interval->start_idx : nullptr;
+    job.end_idx = per_interval ? per_interval->end_idx : nullptr;
+    job.stream = stream;
+
+    mag::CounterParams cp{};
+    cp.t = timestamps;
+    cp.C = counter;
+    cp.n = n_samples;
+    cp.delay = delay;
+    cp.s = starts;
+    cp.e = ends;
+    cp.reps = replays;
+    cp.m = n_intervals;
+    cp.nchunks = job.pl.NT;
+    cp.energy = job.energy;
+    cp.start_idx = job.start_idx;
+    cp.end_idx = job.end_idx;
+    cp.part = job.w.part;
+    cp.status = job.w.status;
+    cp.validate = job.validate() ? 1 : 0;
+    if (per_key && n_intervals > 0 && job.pl.H > 0) {
+        cp.table = job.w.table;
+        cp.H = job.pl.H;
+        cp.urank = job.w.urank;
+    }
+
+    hipError_t e;
+    EventTimer timer((flags & MAG_TIME_KERNELS) != 0, stream, workspace);
+    if ((e = mag::launch_init_status(job.w.status, nullptr, 0, stream)) != hipSuccess)
+        return hip_fail(e, "init");
+    if ((e = mag::launch_counter(cp, stream, timer.on ? timer.slot->ev[1] : nullptr,
+                                 timer.on ? timer.slot->ev[2] : nullptr)) != hipSuccess)
+        return hip_fail(e, "counter kernel");
+    if ((e = mag::launch_counter_fold(cp, stream)) != hipSuccess) return hip_fail(e, "fold kernel");
+    if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
+    timer.mark(3);
+    if (flags & MAG_ASYNC) {
         if (timer.on) timer.slot->pending = true;
         TimerSlot* t = timer_slot(workspace, true);
         if (t && t->host_status) {

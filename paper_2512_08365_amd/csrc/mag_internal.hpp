@@ -33,6 +33,7 @@ enum : uint32_t {
     ERR_POWER = 2u,
     ERR_INTERVAL = 4u,
     ERR_KEYS = 8u,
+    ERR_COUNTER = 16u,
 };
 
 // small device status block at the head of every workspace
@@ -134,6 +135,33 @@ struct GroupParams {
     Status* status;
 };
 
+// per-operator energy from a delayed cumulative energy counter
+constexpr int CNT_CHUNK = 64;   // windows per wave (one per lane)
+constexpr int CNT_BLOCK = 256;  // readings streamed through LDS at a time (4 per lane)
+constexpr int CNT_WAVES = 4;    // waves (independent chunks) per workgroup
+
+struct CounterParams {
+    const double* t;      // [n] reading times
+    const double* C;      // [n] cumulative energy
+    int64_t n;
+    double delay;         // u_j = t_j - delay
+    const double* s;      // [m] window starts
+    const double* e;      // [m] window ends
+    const int32_t* reps;  // [m] replays per window, NULL: 1
+    int64_t m;
+    int64_t nchunks;      // ceil(m / CNT_CHUNK), at least 1
+    double* energy;       // [m]
+    int64_t* start_idx;   // [m] or NULL
+    int64_t* end_idx;     // [m] or NULL
+    double2* part;        // [nchunks] {sum of window increases, windows clipped}
+    Status* status;
+    int validate;
+    // group-by state cleared by the fold kernel (table NULL: none)
+    unsigned long long* table;
+    uint32_t H;
+    uint32_t* urank;
+};
+
 struct DiffParams {
     const uint64_t* ka;
     const double* sa;
@@ -180,6 +208,11 @@ hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_st
 // intervals spanning tiles, endpoints outside the trace, clearing of the group-by state
 hipError_t launch_fix(const FixParams& p, hipStream_t stream);
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
+// window energies of the counter mode (ev_start / ev_stop may be NULL), then the
+// fold of the per-chunk figures into the status block and the group-by clearing
+hipError_t launch_counter(const CounterParams& p, hipStream_t stream, hipEvent_t ev_start = nullptr,
+                          hipEvent_t ev_stop = nullptr);
+hipError_t launch_counter_fold(const CounterParams& p, hipStream_t stream);
 hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream);
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream);
 // upper bound of the diff's stage-1 candidates for n_keys_a rows and top k

@@ -2,8 +2,9 @@
 
 The heavy workloads are drawn by ``synth.c`` (compiled into ``_synth.so`` next
 to this file by :func:`build`); the small randomized edge-case traces are drawn
-here with numpy.  Nothing in this module computes energies: it only produces
-timestamps, power samples, interval bounds and operator keys.
+here with numpy.  Nothing in this module attributes energy: it only produces
+timestamps, power samples, readings of a cumulative energy counter (drawn as
+running sums of random increments), interval bounds and operator keys.
 """
 from __future__ import annotations
 
@@ -188,3 +189,79 @@ def long_trace(seed, n, streams, per_stream, outside=True):
     e = np.concatenate(e_all)
     key = rng.integers(0, 40, s.shape[0]).astype(np.uint64) * np.uint64(0x9E3779B97F4A7C15)
     return {"t": t, "P": P, "s": s, "e": e, "key": key, "offsets": np.array(off, np.int64)}
+
+
+def counter_case(seed: int, n: int = 64, m: int = 8, period: float = 0.02, jitter: float = 0.2,
+                 delay: float | None = None, snap: float = 0.3, zero_len: float = 0.1,
+                 outside: bool = True, replays: bool = True, keys: int = 5,
+                 irregular: bool = False) -> dict:
+    """Readings of a cumulative energy counter and a sequence of replay windows.
+
+    Readings come every ``period`` seconds (uniform jitter of ``jitter``
+    periods; with ``irregular`` the spacing varies over three decades) and the
+    counter never decreases (flat stretches included).  Windows satisfy
+    s_0 <= e_0 <= s_1 <= ...; some bounds sit exactly on shifted reading times
+    t_j - delay, some windows have zero length, some reach past the readings.
+    """
+    rng = np.random.default_rng(seed)
+    if irregular:
+        gaps = period * 10.0 ** rng.uniform(-1.5, 1.5, n - 1)
+    else:
+        gaps = period * (1.0 + rng.uniform(-jitter, jitter, n - 1))
+    t = rng.uniform(-1.0, 1.0) + np.concatenate([[0.0], np.cumsum(gaps)])
+    watts = rng.uniform(50.0, 700.0, n - 1)
+    watts[rng.random(n - 1) < 0.05] = 0.0
+    C = rng.uniform(0.0, 1e4) + np.concatenate([[0.0], np.cumsum(watts * gaps)])
+    if delay is None:
+        delay = float(rng.choice([0.0, rng.uniform(0.0, 0.3), -rng.uniform(0.0, 0.05)]))
+    u = t - delay
+    lo, hi = u[0], u[-1]
+    pad = 0.1 * (hi - lo) if outside else 0.0
+    cuts = np.sort(rng.uniform(lo - pad, hi + pad, 2 * m))
+    if snap > 0 and m:
+        pick = rng.random(2 * m) < snap
+        idx = np.clip(np.searchsorted(u, cuts), 0, n - 1)
+        cuts = np.sort(np.where(pick, u[idx], cuts))
+    s = cuts[0::2].copy()
+    e = cuts[1::2].copy()
+    if zero_len > 0 and m:
+        e = np.where(rng.random(m) < zero_len, s, e)
+    reps = rng.integers(1, 2000, m).astype(np.int32) if replays else None
+    vocab = rng.integers(0, 2**63, size=keys, dtype=np.int64).astype(np.uint64) * np.uint64(2) + \
+        rng.integers(0, 2, size=keys).astype(np.uint64)
+    key = vocab[rng.integers(0, keys, size=m)] if m else np.zeros(0, np.uint64)
+    return {"t": t, "C": C, "delay": float(delay), "s": s, "e": e, "reps": reps,
+            "key": key.astype(np.uint64)}
+
+
+def replay_session(seed: int, n_ops: int = 98_304, n_keys: int = 416, rate_hz: float = 50.0,
+                   delay: float = 0.1, reps: int = 1000, median_s: float = 20e-6,
+                   sigma: float = 1.0) -> dict:
+    """A replay profiling session of the energy counter.
+
+    Each of ``n_ops`` operator instances (lognormal duration, keys uniform over
+    ``n_keys``) is replayed ``reps`` times back to back; consecutive windows
+    are separated by a 10-50 ms pause for setup and settling.  The counter is
+    read at ``rate_hz`` (5 % jitter) and lags by ``delay`` seconds; its
+    increments follow a power random walk between 100 and 700 W.
+    """
+    rng = np.random.default_rng(seed)
+    dur = np.exp(np.log(median_s) + sigma * rng.standard_normal(n_ops)) * reps
+    pause = rng.uniform(0.010, 0.050, n_ops)
+    s = np.cumsum(pause + np.concatenate([[0.0], dur[:-1]]))
+    e = s + dur
+    span = float(e[-1]) + 1.0
+    n = int(span * rate_hz) + 2
+    t = (np.arange(n) + rng.uniform(-0.05, 0.05, n)) / rate_hz - 0.5 + delay
+    t[0] = -0.5 + delay - 1.0 / rate_hz
+    watts = np.clip(400.0 + np.cumsum(rng.normal(0.0, 5.0, n - 1)), 100.0, 700.0)
+    C = 5e5 + np.concatenate([[0.0], np.cumsum(watts * np.diff(t))])
+    vocab = np.array([synth_key(k) for k in range(n_keys)], dtype=np.uint64)
+    key = vocab[rng.integers(0, n_keys, n_ops)]
+    return {"t": t, "C": C, "delay": float(delay), "s": s, "e": e,
+            "reps": np.full(n_ops, reps, np.int32), "key": key}
+
+
+def synth_key(k: int) -> int:
+    """A 64-bit operator key for vocabulary index k (splitmix64 finaliser)."""
+    return int(_load().synth_mix64(ctypes.c_uint64(0x4D41474E45544F4E ^ k)))

@@ -73,8 +73,43 @@ def test_host_side_errors_without_gpu():
     assert lib.mag_diff(None, ctypes.byref(sa), None, ctypes.byref(sa), -1, ctypes.byref(ro),
                         None, 0, None) == N.MAG_E_SIZE
     assert lib.mag_diff_workspace_size(5, 5, -1, ctypes.byref(b)) == N.MAG_E_SIZE
-    for code in range(-12, 1):
-        assert lib.mag_strerror(code)
+    for code in range(-13, 1):
+        assert b"unknown" not in lib.mag_strerror(code)
+
+
+def test_counter_host_side_errors_without_gpu():
+    from paper_2512_08365_amd import _native as N
+    lib = N.load()
+    b = ctypes.c_size_t(0)
+    assert lib.mag_counter_workspace_size(1, 0, 0, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_counter_workspace_size(10, -1, 0, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_counter_workspace_size(10, 5, -1, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_counter_workspace_size(10, 5, 0, None) == N.MAG_E_NULL
+    assert lib.mag_counter_workspace_size(10, 500, 0, ctypes.byref(b)) == N.MAG_OK
+    plain = b.value
+    assert lib.mag_counter_workspace_size(10, 500, 64, ctypes.byref(b)) == N.MAG_OK
+    assert b.value > plain  # the group-by state
+    fake = ctypes.c_void_p(256)
+    big = 1 << 30
+
+    def call(t=fake, C=fake, n=10, delay=0.0, s=fake, e=fake, reps=None, keys=None, m=3,
+             ws=fake, ws_bytes=big):
+        return lib.mag_attribute_counter(t, C, n, delay, s, e, reps, keys, m, 0, None, None,
+                                         None, None, ws, ws_bytes, None)
+
+    assert call(t=None) == N.MAG_E_NULL
+    assert call(C=None) == N.MAG_E_NULL
+    assert call(delay=float("inf")) == N.MAG_E_TIMESTAMPS
+    assert call(delay=float("nan")) == N.MAG_E_TIMESTAMPS
+    assert call(n=1) == N.MAG_E_SIZE
+    assert call(m=-1) == N.MAG_E_SIZE
+    assert call(s=None) == N.MAG_E_NULL
+    assert call(ws=None) == N.MAG_E_NULL
+    assert call(ws=ctypes.c_void_p(264)) == N.MAG_E_WORKSPACE
+    assert call(t=ctypes.c_void_p(260)) == N.MAG_E_ALIGN
+    assert call(reps=ctypes.c_void_p(258)) == N.MAG_E_ALIGN
+    assert call(ws_bytes=16) == N.MAG_E_WORKSPACE
+    assert b"workspace" in lib.mag_last_error()
 
 
 def test_stream_host_side_errors_without_gpu():
