@@ -83,6 +83,12 @@ typedef struct mag_attr_opts {
                                     /* intervals [offs[a], offs[a+1]); offs[0] = 0,   */
                                     /* offs[n_streams] = n_intervals; NULL allowed    */
                                     /* only when n_streams == 1                       */
+    hipEvent_t intervals_ready;     /* mag_attribute only, may be NULL: recorded on   */
+                                    /* `stream` once the per-interval outputs are     */
+                                    /* complete, before the per-key grouping, so that */
+                                    /* work on another stream (the other system's     */
+                                    /* attribution, Section 3.2) can start while the  */
+                                    /* grouping runs; the caller owns the event       */
 } mag_attr_opts;
 
 /* Per-interval outputs (device arrays of n_intervals entries; any may be NULL). */

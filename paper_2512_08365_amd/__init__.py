@@ -44,10 +44,20 @@ def version() -> str:
     return _lib().mag_version().decode()
 
 
-def _opts(n_streams: int, stream_offsets, flags: int):
+def _event_handle(ev):
+    """Raw HIP event of a torch.cuda.Event (created by a first record if needed)."""
+    if ev is None:
+        return None
+    if not ev.cuda_event:
+        ev.record()
+    return ctypes.c_void_p(ev.cuda_event)
+
+
+def _opts(n_streams: int, stream_offsets, flags: int, intervals_ready=None):
     o = N.AttrOpts()
     o.n_streams = int(n_streams)
     o.flags = int(flags)
+    o.intervals_ready = _event_handle(intervals_ready)
     keep = None
     if stream_offsets is not None:
         keep = (ctypes.c_int64 * len(stream_offsets))(*[int(x) for x in stream_offsets])
@@ -107,11 +117,14 @@ class Pending:
 
 def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
               equal_split: bool = True, validate: bool = True, key_capacity: int | None = None,
-              indices: bool = True, workspace=None, out=None, asynchronous: bool = False):
+              indices: bool = True, workspace=None, out=None, asynchronous: bool = False,
+              intervals_ready=None):
     """Attribute the energy of a power trace to intervals and group it by key.
 
     t: float64 [n] timestamps (s), P: float32 [n] power (W), s/e: float64 [m]
     interval bounds, keys: int64 [m] (bits read as uint64) or None.
+    intervals_ready: a torch.cuda.Event recorded on the current stream once the
+    per-interval outputs are complete (before the grouping), or None.
     Returns (per_interval, per_key, summary): dicts of tensors / numbers; with
     asynchronous=True a Pending whose finish() returns them once the work ran.
     """
@@ -121,7 +134,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     dev = t.device
     flags = ((EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE) |
              (ASYNC if asynchronous else 0))
-    o, keep = _opts(n_streams, stream_offsets, flags)
+    o, keep = _opts(n_streams, stream_offsets, flags, intervals_ready)
     group = keys is not None
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
     ws_bytes = workspace_size(n, m, cap if group else 0, n_streams, stream_offsets, flags)

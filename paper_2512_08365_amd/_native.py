@@ -44,7 +44,7 @@ EXPORTED = (
 
 class AttrOpts(ctypes.Structure):
     _fields_ = [("n_streams", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("stream_offsets", c_vp)]
+                ("stream_offsets", c_vp), ("intervals_ready", c_vp)]
 
 
 class IntervalOut(ctypes.Structure):

@@ -608,6 +608,9 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         return hip_fail(e, "tile kernel");
     if ((e = job.fixups(n_samples, NT, per_key != nullptr)) != hipSuccess)
         return hip_fail(e, "fix-up kernels");
+    if (opts && opts->intervals_ready &&
+        (e = hipEventRecord(opts->intervals_ready, stream)) != hipSuccess)
+        return hip_fail(e, "intervals_ready event");
     if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
     timer.mark(3);
     if (job.flags & MAG_ASYNC) {
