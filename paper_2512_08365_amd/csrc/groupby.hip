@@ -22,6 +22,12 @@
 //    key's row.  Per-workgroup atomics add the rows into the attributed energy.
 // 6. k_agg_m2 / k_fin_m2: second pass over the chunk for sum (E - mean)^2
 //    (the two-pass definition of M2).
+// When a chunk fits one batch of loads per thread (up to AGG_THREADS *
+// AGG_BATCH intervals), steps 5 and 6 are one pass instead: k_agg_one keeps
+// the chunk's ids and energies in registers, takes count and sum, then the
+// chunk's own M2 about the chunk mean; k_fin_one merges the chunk rows per key
+// by Chan, Golub and LeVeque's pairwise update, M2 = sum_c M2_c +
+// sum_c n_c (mean_c - mean)^2 (every term non-negative).
 // Plain stores carry every partial result: device-scope atomics, which are
 // slow on this part, are used only for counters, inserts and one add per
 // workgroup.  Every thread requests all the loads of a batch before it uses
@@ -471,6 +477,142 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupPar
     }
 }
 
+// count, sum and M2 about the chunk's own mean, per id of one chunk held in
+// registers (the chunk is at most AGG_THREADS * AGG_BATCH intervals)
+__global__ __launch_bounds__(AGG_THREADS) void k_agg_one(const GroupParams p)
+{
+    __shared__ uint32_t lcnt[AGG_IDS];
+    __shared__ double lsum[AGG_IDS];
+    const int c = blockIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.y * AGG_IDS;
+    const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
+    uint32_t sl[AGG_BATCH];
+    double en[AGG_BATCH];
+    // the loads are requested before the key count is read
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k) {
+        const int64_t i = lo + threadIdx.x + (int64_t)k * AGG_THREADS;
+        sl[k] = (i < hi) ? p.slot[i] : NO_ID;
+        en[k] = (i < hi) ? p.energy[i] : 0.0;
+    }
+    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if (r0 >= nk) return;  // uniform
+    const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
+        lcnt[v] = 0u;
+        lsum[v] = 0.0;
+    }
+    int d[AGG_BATCH];
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k) {
+        const uint32_t id = resolve_id(p, sl[k]);
+        const int64_t x = (id == NO_ID) ? -1 : (int64_t)id - r0;
+        d[k] = (x < 0 || x >= nid) ? -1 : (int)x;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k) {
+        if (d[k] < 0) continue;
+        atomicAdd(&lcnt[d[k]], 1u);
+        atomicAdd(&lsum[d[k]], en[k]);
+    }
+    __syncthreads();
+    // each interval's deviation from its key's chunk mean
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k)
+        if (d[k] >= 0) en[k] -= lsum[d[k]] / (double)lcnt[d[k]];
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
+        p.pcnt[(int64_t)c * p.cap + r0 + v] = lcnt[v];
+        p.psum[(int64_t)c * p.cap + r0 + v] = lsum[v];
+    }
+    __syncthreads();
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) lsum[v] = 0.0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k)
+        if (d[k] >= 0) atomicAdd(&lsum[d[k]], en[k] * en[k]);
+    __syncthreads();
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) p.pm2[(int64_t)c * p.cap + r0 + v] = lsum[v];
+}
+
+// per key: count and sum over the chunk rows (as k_fin_sum), then
+// M2 = sum_c (M2_c + n_c (mean_c - mean)^2) over the same rows; 32 keys per
+// workgroup, each key's rows split over 32 interleaved groups
+constexpr int FO_KEYS = 32;
+constexpr int FO_GROUPS = 32;
+__global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupParams p)
+{
+    __shared__ uint64_t qc[FO_GROUPS][FO_KEYS];
+    __shared__ double qs[FO_GROUPS][FO_KEYS];
+    __shared__ double qmean[FO_KEYS];
+    const int kl = threadIdx.x % FO_KEYS, grp = threadIdx.x / FO_KEYS;
+    const int64_t id = (int64_t)blockIdx.x * FO_KEYS + kl;
+    uint64_t cnt = 0;
+    double sum = 0.0;
+    if (id < p.cap) {
+#pragma unroll 8
+        for (int c = grp; c < p.nchunks; c += FO_GROUPS) {
+            cnt += p.pcnt[(int64_t)c * p.cap + id];
+            sum += p.psum[(int64_t)c * p.cap + id];
+        }
+    }
+    uint32_t r = 0xffffffffu;
+    uint64_t key = 0;
+    if (grp == 0 && id < p.cap) {
+        r = p.urank[id];
+        key = p.ukey[id];
+    }
+    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if ((int64_t)blockIdx.x * FO_KEYS >= nk) return;  // uniform
+    qc[grp][kl] = cnt;
+    qs[grp][kl] = sum;
+    __syncthreads();
+    double tot = 0.0;
+    if (grp == 0) {
+        cnt = 0;
+        sum = 0.0;
+        for (int g = 0; g < FO_GROUPS; ++g) {
+            cnt += qc[g][kl];
+            sum += qs[g][kl];
+        }
+        qmean[kl] = cnt ? sum / (double)cnt : 0.0;
+        if (id < nk) {
+            if ((int64_t)r < p.cap) {
+                p.keys_out[r] = key;
+                p.count_out[r] = (int64_t)cnt;
+                p.sum_out[r] = sum;
+            }
+            tot = sum;
+        }
+        // this workgroup's rows, once into the attributed energy
+        for (int off = FO_KEYS / 2; off > 0; off >>= 1) tot += __shfl_xor(tot, off);
+        if (kl == 0 && tot != 0.0) atomicAdd(&p.status->attributed_energy, tot);
+    }
+    __syncthreads();
+    double m2 = 0.0;
+    if (id < nk) {
+        // branch-free, so that the loads of many chunk rows are in flight together
+        const double mean = qmean[kl];
+#pragma unroll 8
+        for (int c = grp; c < p.nchunks; c += FO_GROUPS) {
+            const uint32_t nc = p.pcnt[(int64_t)c * p.cap + id];
+            const double sc = p.psum[(int64_t)c * p.cap + id];
+            const double mc = p.pm2[(int64_t)c * p.cap + id];
+            const double dn = (double)nc;
+            const double dm = (nc ? sc / dn : mean) - mean;
+            m2 += mc + dn * dm * dm;
+        }
+    }
+    __syncthreads();
+    qs[grp][kl] = m2;
+    __syncthreads();
+    if (grp == 0 && id < nk) {
+        m2 = 0.0;
+        for (int g = 0; g < FO_GROUPS; ++g) m2 += qs[g][kl];
+        if ((int64_t)r < p.cap) p.m2_out[r] = m2;
+    }
+}
+
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
 {
     if (p.m <= 0) return hipSuccess;
@@ -493,10 +635,15 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
     hipLaunchKernelGGL(k_rank, dim3((unsigned)min(ntile * ntile, (int64_t)4096)), dim3(RANK_TILE),
                        0, stream, p);
     const unsigned ranges = (unsigned)((p.cap + AGG_IDS - 1) / AGG_IDS);
-    if (ranges > 0) {
+    const unsigned kb = (unsigned)max((int64_t)1, (p.cap + FIN_KEYS - 1) / FIN_KEYS);
+    if (ranges > 0 && p.chunk <= (int64_t)AGG_THREADS * AGG_BATCH) {
+        hipLaunchKernelGGL(k_agg_one, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
+                           stream, p);
+        const unsigned kb1 = (unsigned)max((int64_t)1, (p.cap + FO_KEYS - 1) / FO_KEYS);
+        hipLaunchKernelGGL(k_fin_one, dim3(kb1), dim3(FO_KEYS * FO_GROUPS), 0, stream, p);
+    } else if (ranges > 0) {
         hipLaunchKernelGGL(k_agg_sum, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);
-        const unsigned kb = (unsigned)max((int64_t)1, (p.cap + FIN_KEYS - 1) / FIN_KEYS);
         hipLaunchKernelGGL(k_fin_sum, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
         hipLaunchKernelGGL(k_agg_m2, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);

@@ -252,6 +252,15 @@ def test_long_run_workload_streamed_in_32M_chunks():
     gi, gk, summ = _np(got)
     del d, ref, got
     torch.cuda.empty_cache()
+    # grouping of 50M intervals (chunks larger than one batch of loads per
+    # thread: the two-pass per-key path) against the oracle's grouping of the
+    # same energies
+    g = oracle.groupby(c["key"], gi["energy"])
+    assert np.array_equal(gk["keys"].view(np.uint64), g["keys"])
+    assert np.array_equal(gk["count"], g["count"])
+    assert_energy_close(gk["sum"], g["sum"], "long-run key sums")
+    second = g["m2"] + g["sum"] ** 2 / np.maximum(g["count"], 1)
+    assert np.all(np.abs(gk["m2"] - g["m2"]) <= 1e-9 * second)
     rng = np.random.default_rng(0)
     pick = np.sort(rng.choice(m, 20000, replace=False))
     pick = np.concatenate([[0, 1, m - 2, m - 1], pick])
