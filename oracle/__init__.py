@@ -13,7 +13,10 @@ printed in the paper's Table "tab:energy-profiling".  The counter (software
 replay) attribution is pinned in tests/test_oracle_counter_pins.py: exact
 dyadic closed forms, the delay and replay scenarios worked out by hand,
 numpy.interp, exact rational arithmetic and the invariants of a cumulative
-quantity.
+quantity.  Per-key latency and the detection rule (flag threshold, waste vs
+trade-off) are pinned in tests/test_oracle_detect_pins.py: exactly rounded
+sums (math.fsum) by brute force, dyadic closed forms, hand-worked threshold
+and tolerance boundaries and a brute-force ranking.
 """
 from __future__ import annotations
 
@@ -59,6 +62,7 @@ def _load():
         lib.orc_counter_attribute.argtypes = [p, p, i64, ctypes.c_double, p, p, p, i64, p, p, p,
                                               p]
         lib.orc_groupby.argtypes = [p, p, i64, p, p, p, p, p, p]
+        lib.orc_key_latency.argtypes = [p, p, p, p, i64, p, p, p]
         lib.orc_diff.argtypes = [p, p, p, i64, p, p, p, i64, i64, p, p, p, p, p, p, p, p]
         lib.orc_ratio.argtypes = [ctypes.c_double, ctypes.c_double]
         lib.orc_ratio.restype = ctypes.c_double
@@ -149,6 +153,56 @@ def groupby(keys, energy) -> dict:
     r = int(nk[0])
     return {"keys": ok[:r].copy(), "count": oc[:r].copy(), "sum": osum[:r].copy(),
             "m2": om2[:r].copy(), "m2_welford": omw[:r].copy()}
+
+
+def key_latency(keys, starts, ends, reps=None) -> dict:
+    """Per distinct key in ascending order: the sum of its interval durations
+    (end - start, divided by the replay count when reps is given)."""
+    keys = _c(keys, np.uint64)
+    s = _c(starts, np.float64)
+    e = _c(ends, np.float64)
+    r = None if reps is None else _c(reps, np.int32)
+    m = keys.shape[0]
+    ok = np.zeros(max(m, 1), np.uint64)
+    ol = np.zeros(max(m, 1), np.float64)
+    nk = np.zeros(1, np.int64)
+    rc = _load().orc_key_latency(_p(keys), _p(s), _p(e), _p(r), m, _p(ok), _p(ol), _p(nk))
+    if rc != 0:
+        raise OracleError(rc)
+    n = int(nk[0])
+    return {"keys": ok[:n].copy(), "latency": ol[:n].copy()}
+
+
+WASTE = 1
+TRADEOFF = 2
+
+
+def detect(a: dict, b: dict, threshold: float = 0.10, tolerance: float = 0.01) -> dict:
+    """Section 6.1's detection rule over two per-key tables (keys ascending,
+    with sum, count and latency).
+
+    A key present on both sides is flagged when B's energy exceeds A's by at
+    least `threshold` of A's, r = (E_B - E_A)/E_A >= threshold (10 %, or 5 %).
+    A flagged key is waste when the efficient side A is not slower than B by
+    more than `tolerance` of B's latency, (L_A - L_B) <= tolerance * L_B
+    (1 %); otherwise B trades the extra energy for speed.  Rows come in the
+    ranking's order (r descending, key ascending).
+    """
+    full = diff(a, b, len(a["keys"]))  # every joined key, ranked
+    flag = full["ratio"] >= threshold
+    nf = int(np.count_nonzero(flag))
+    assert np.all(flag[:nf]), "flagged keys form a prefix of the ranking"
+    ka = _c(a["keys"], np.uint64)
+    kb = _c(b["keys"], np.uint64)
+    keys = full["key"][:nf]
+    la = _c(a["latency"], np.float64)[np.searchsorted(ka, keys)]
+    lb = _c(b["latency"], np.float64)[np.searchsorted(kb, keys)]
+    verdict = np.where((la - lb) <= tolerance * lb, WASTE, TRADEOFF).astype(np.int32)
+    return {"key": keys, "ratio": full["ratio"][:nf], "energy_a": full["energy_a"][:nf],
+            "energy_b": full["energy_b"][:nf], "latency_a": la, "latency_b": lb,
+            "verdict": verdict, "n_flagged": nf,
+            "n_waste": int(np.count_nonzero(verdict == WASTE)),
+            "n_tradeoff": int(np.count_nonzero(verdict == TRADEOFF))}
 
 
 def diff(a: dict, b: dict, k: int) -> dict:

@@ -400,6 +400,54 @@ int orc_groupby(const uint64_t* keys, const double* energy, int64_t m, uint64_t*
     return ORC_OK;
 }
 
+/*
+ * orc_key_latency: per distinct key, in ascending unsigned key order, the
+ * operator's latency: the compensated sum of its interval durations
+ * ends[i] - starts[i] (unclipped bounds), each divided by reps[i] when reps
+ * is given (a replay window's duration per run).  Section 6.1 weighs an
+ * operator's energy difference against its performance difference; this is
+ * the performance side.  Output arrays hold m rows; *n_keys receives the
+ * number written.
+ */
+int orc_key_latency(const uint64_t* keys, const double* starts, const double* ends,
+                    const int32_t* reps, int64_t m, uint64_t* out_keys, double* out_latency,
+                    int64_t* n_keys)
+{
+    orc_kv* kv;
+    int64_t i, r = 0;
+    if (m < 0)
+        return ORC_E_SIZE;
+    if (!n_keys || (m > 0 && (!keys || !starts || !ends || !out_keys || !out_latency)))
+        return ORC_E_NULL;
+    kv = (orc_kv*)malloc(sizeof(orc_kv) * (size_t)(m + 1));
+    if (!kv)
+        return ORC_E_NOMEM;
+    for (i = 0; i < m; ++i) {
+        kv[i].key = keys[i];
+        kv[i].idx = i;
+    }
+    qsort(kv, (size_t)m, sizeof(orc_kv), cmp_kv);
+    i = 0;
+    while (i < m) {
+        int64_t lo = i, hi = i, u;
+        orc_ksum sum = {0, 0};
+        while (hi < m && kv[hi].key == kv[lo].key)
+            ++hi;
+        for (u = lo; u < hi; ++u) {
+            int64_t x = kv[u].idx;
+            double d = ends[x] - starts[x];
+            ks_add(&sum, reps ? d / (double)reps[x] : d);
+        }
+        out_keys[r] = kv[lo].key;
+        out_latency[r] = ks_get(&sum);
+        ++r;
+        i = hi;
+    }
+    *n_keys = r;
+    free(kv);
+    return ORC_OK;
+}
+
 /* ------------------------------------------------------------------ */
 /* diff: join and rank                                                  */
 /* ------------------------------------------------------------------ */
