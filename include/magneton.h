@@ -67,6 +67,14 @@ extern "C" {
 /* mag_attribute returns once its work is enqueued; mag_attribute_finish
    delivers n_keys, the summary and device-detected errors. */
 #define MAG_ASYNC 0x8u
+/* Also sum each key's interval durations (end - start; per replay run in the
+   counter mode) into per_key->duration, which must then be non-NULL: the
+   latency side of Section 6.1's comparison. */
+#define MAG_KEY_LATENCY 0x10u
+
+/* Verdicts of mag_detect (Section 6.1). */
+#define MAG_WASTE 1    /* the efficient side is at most `tolerance` slower     */
+#define MAG_TRADEOFF 2 /* the extra energy buys more speed than that           */
 
 /* Most concurrent streams one call accepts. */
 #define MAG_MAX_STREAMS 32
@@ -78,7 +86,7 @@ extern "C" {
 typedef struct mag_attr_opts {
     int32_t n_streams;              /* >= 1; intervals are concatenated by stream   */
     uint32_t flags;                 /* MAG_EQUAL_SPLIT | MAG_SKIP_VALIDATE |          */
-                                    /* MAG_TIME_KERNELS | MAG_ASYNC                   */
+                                    /* MAG_TIME_KERNELS | MAG_ASYNC | MAG_KEY_LATENCY */
     const int64_t* stream_offsets;  /* HOST int64[n_streams + 1]: stream a owns       */
                                     /* intervals [offs[a], offs[a+1]); offs[0] = 0,   */
                                     /* offs[n_streams] = n_intervals; NULL allowed    */
@@ -106,6 +114,8 @@ typedef struct mag_key_stats {
     int64_t capacity; /* rows available in each array (host value)                 */
     int64_t n_keys;   /* rows filled (host value): output of mag_attribute, input  */
                       /* of mag_diff                                               */
+    double* duration; /* with MAG_KEY_LATENCY: sum of the key's interval durations */
+                      /* (s); read by mag_detect; may be NULL otherwise           */
 } mag_key_stats;
 
 /* Whole-trace figures (host struct). */
@@ -136,6 +146,24 @@ typedef struct mag_rank_out {
     int64_t n_join;   /* keys present in both (host output)                          */
 } mag_rank_out;
 
+/* Options of mag_detect (Section 6.1's values: 0.10, or 0.05; and 0.01). */
+typedef struct mag_detect_opts {
+    double threshold; /* flag a joined key when (E_B - E_A) / E_A >= threshold    */
+    double tolerance; /* waste when (L_A - L_B) <= tolerance * L_B, else trade-off */
+} mag_detect_opts;
+
+/* Flagged keys of mag_detect (device arrays of `rank.capacity` rows). */
+typedef struct mag_detect_out {
+    mag_rank_out rank;  /* the flagged keys in ranking order (rank.n_out rows)   */
+    double* latency_a;  /* L_A: statsA->duration of the row's key                */
+    double* latency_b;  /* L_B                                                   */
+    int32_t* verdict;   /* MAG_WASTE or MAG_TRADEOFF                             */
+    int64_t n_flagged;  /* host output: joined keys with r >= threshold (all of  */
+                        /* them, also beyond the rows written)                   */
+    int64_t n_waste;    /* host output: flagged keys judged waste                */
+    int64_t n_tradeoff; /* host output: flagged keys judged a trade-off          */
+} mag_detect_out;
+
 /*
  * mag_attribute_workspace_size -- bytes of device workspace mag_attribute needs
  * for the given sizes, key-table capacity (0 when no per-key output is asked
@@ -158,7 +186,8 @@ int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t
  *   E_i    = integral over [starts[i], ends[i]] of P^(x) / m(x)  (MAG_EQUAL_SPLIT)
  *          = integral over [starts[i], ends[i]] of P^(x)          (otherwise).
  * Per key: count, sum of E_i and M2 = sum of (E_i - mean)^2; rows ascending by
- * unsigned key.  Every energy is computed in fp64 as a sum of non-negative
+ * unsigned key; with MAG_KEY_LATENCY also the sum of (ends[i] - starts[i]),
+ * the operator's latency (Section 6.1).  Every energy is computed in fp64 as a sum of non-negative
  * pieces; no energy is a difference of whole-trace running totals (the whole
  * sample segments between two endpoints are a difference of two prefixes
  * local to a 512-segment tile only where that difference keeps 6e-11
@@ -218,11 +247,12 @@ int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summ
 
 /*
  * mag_counter_workspace_size -- bytes of device workspace mag_attribute_counter
- * needs for the given sizes and key-table capacity (0 when no per-key output is
- * asked for).  Host only.  Returns MAG_OK, MAG_E_SIZE or MAG_E_NULL.
+ * needs for the given sizes, key-table capacity (0 when no per-key output is
+ * asked for) and flags (MAG_KEY_LATENCY needs more).  Host only.  Returns
+ * MAG_OK, MAG_E_SIZE or MAG_E_NULL.
  */
 int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
-                               size_t* bytes);
+                               uint32_t flags, size_t* bytes);
 
 /*
  * mag_attribute_counter -- per-operator energy from a cumulative energy
@@ -250,8 +280,9 @@ int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t k
  *                          starts[i] <= ends[i] <= starts[i+1]
  *   replays[n_intervals]  int32 >= 1, or NULL for one run per window
  *   op_keys[n_intervals]  uint64 operator key; may be NULL when per_key is NULL
- *   flags                 MAG_SKIP_VALIDATE | MAG_TIME_KERNELS | MAG_ASYNC
- *                          (other bits are ignored)
+ *   flags                 MAG_SKIP_VALIDATE | MAG_TIME_KERNELS | MAG_ASYNC |
+ *                          MAG_KEY_LATENCY (per-key sum of (ends - starts) /
+ *                          replays); other bits are ignored
  *   per_interval          energy = E_i (J per run), start_idx / end_idx =
  *                          lower_bound of starts[i] / ends[i] among u; may be
  *                          NULL
@@ -300,6 +331,38 @@ int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_
 int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
              const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
              size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * mag_detect_workspace_size -- device workspace bytes for mag_detect with
+ * `rows` output rows.  Host only.
+ */
+int mag_detect_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t rows, size_t* bytes);
+
+/*
+ * mag_detect -- Section 6.1's detection of energy inefficiencies over two
+ * per-key tables: a key present on both sides is flagged when B's energy
+ * exceeds A's by at least the threshold, r = (E_B - E_A) / E_A >= threshold
+ * (the paper uses 10 % and finds 5 % free of false positives); a flagged key
+ * is software energy waste when the efficient side A is not slower than B by
+ * more than the tolerance, (L_A - L_B) <= tolerance * L_B with L the per-key
+ * latency (the paper allows 1 %), and a performance-energy trade-off
+ * otherwise.  (The paper's second condition, outputs within 1 %, concerns the
+ * operators' results, which this library does not see.)  Swap A and B to
+ * examine the other direction.
+ *   keysA/statsA, keysB/statsB as for mag_diff, and both duration arrays
+ *   (mag_attribute with MAG_KEY_LATENCY) must be given.
+ *   out->rank.capacity rows are available; the first
+ *   min(capacity, n_flagged) flagged keys, in the ranking's order (r
+ *   descending, key ascending), are written with their energies, counts,
+ *   latencies and verdicts; out->rank.n_out receives that number, and
+ *   n_flagged / n_waste / n_tradeoff count every flagged key.
+ *   opts: NULL for threshold 0.10 and tolerance 0.01.
+ * Synchronizes `stream`.  Errors: as mag_diff, plus MAG_E_NULL for a missing
+ * duration array and MAG_E_SIZE for a threshold or tolerance that is NaN.
+ */
+int mag_detect(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+               const mag_key_stats* statsB, const mag_detect_opts* opts, mag_detect_out* out,
+               void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
  * Chunked streaming.  A long trace (for example an hour of samples at

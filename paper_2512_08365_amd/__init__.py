@@ -14,13 +14,16 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "Stream", "workspace_size",
+__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "detect", "Stream", "workspace_size",
            "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
 
 EQUAL_SPLIT = N.MAG_EQUAL_SPLIT
 SKIP_VALIDATE = N.MAG_SKIP_VALIDATE
 ASYNC = N.MAG_ASYNC
+KEY_LATENCY = N.MAG_KEY_LATENCY
+WASTE = N.MAG_WASTE
+TRADEOFF = N.MAG_TRADEOFF
 
 
 class MagnetonError(RuntimeError):
@@ -92,6 +95,24 @@ def diff_workspace_size(n_keys_a: int, n_keys_b: int, k: int) -> int:
     return int(b.value)
 
 
+def _key_outputs(cap: int, dev, latency: bool):
+    """Device arrays of a per-key table and the KeyStats struct naming them."""
+    t = {"keys": torch.empty(cap, dtype=torch.int64, device=dev),
+         "sum": torch.empty(cap, dtype=torch.float64, device=dev),
+         "m2": torch.empty(cap, dtype=torch.float64, device=dev),
+         "count": torch.empty(cap, dtype=torch.int64, device=dev)}
+    if latency:
+        t["duration"] = torch.empty(cap, dtype=torch.float64, device=dev)
+    ks = N.KeyStats(t["sum"].data_ptr(), t["m2"].data_ptr(), t["count"].data_ptr(), cap, 0,
+                    t["duration"].data_ptr() if latency else None)
+    return t, ks
+
+
+def _key_rows(t: dict, ks) -> dict:
+    nk = int(ks.n_keys)
+    return {k: v[:nk] for k, v in t.items()}
+
+
 def _stream_handle(device):
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
@@ -118,13 +139,14 @@ class Pending:
 def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
               equal_split: bool = True, validate: bool = True, key_capacity: int | None = None,
               indices: bool = True, workspace=None, out=None, asynchronous: bool = False,
-              intervals_ready=None):
+              intervals_ready=None, latency: bool = False):
     """Attribute the energy of a power trace to intervals and group it by key.
 
     t: float64 [n] timestamps (s), P: float32 [n] power (W), s/e: float64 [m]
     interval bounds, keys: int64 [m] (bits read as uint64) or None.
     intervals_ready: a torch.cuda.Event recorded on the current stream once the
     per-interval outputs are complete (before the grouping), or None.
+    latency: also sum each key's interval durations (per_key["duration"]).
     Returns (per_interval, per_key, summary): dicts of tensors / numbers; with
     asynchronous=True a Pending whose finish() returns them once the work ran.
     """
@@ -133,7 +155,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     m = int(s.shape[0])
     dev = t.device
     flags = ((EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE) |
-             (ASYNC if asynchronous else 0))
+             (ASYNC if asynchronous else 0) | (KEY_LATENCY if latency and keys is not None else 0))
     o, keep = _opts(n_streams, stream_offsets, flags, intervals_ready)
     group = keys is not None
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
@@ -154,20 +176,15 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
             ei = torch.empty(m, dtype=torch.int64, device=dev)
     pio = N.IntervalOut(_dev_ptr(energy, torch.float64, "energy"),
                         _dev_ptr(si, torch.int64, "start_idx"), _dev_ptr(ei, torch.int64, "end_idx"))
-    ks = None
-    kout = ksum = km2 = kcnt = None
+    ks = tab = None
     if group:
-        kout = torch.empty(cap, dtype=torch.int64, device=dev)
-        ksum = torch.empty(cap, dtype=torch.float64, device=dev)
-        km2 = torch.empty(cap, dtype=torch.float64, device=dev)
-        kcnt = torch.empty(cap, dtype=torch.int64, device=dev)
-        ks = N.KeyStats(ksum.data_ptr(), km2.data_ptr(), kcnt.data_ptr(), cap, 0)
+        tab, ks = _key_outputs(cap, dev, latency)
     summ = N.Summary()
     rc = lib.mag_attribute(
         _dev_ptr(t, torch.float64, "t"), _dev_ptr(P, torch.float32, "P"), n,
         _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
         _dev_ptr(keys, torch.int64, "keys") if group else None, m, ctypes.byref(o),
-        ctypes.byref(pio), kout.data_ptr() if group else None,
+        ctypes.byref(pio), tab["keys"].data_ptr() if group else None,
         ctypes.byref(ks) if group else None, ctypes.byref(summ), workspace.data_ptr(),
         workspace.numel(), _stream_handle(dev))
     _check(rc)
@@ -177,10 +194,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
         if indices:
             per_interval["start_idx"] = si
             per_interval["end_idx"] = ei
-        per_key = None
-        if group:
-            nk = int(ks.n_keys)
-            per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+        per_key = _key_rows(tab, ks) if group else None
         summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
                    "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
                    "n_keys": int(summ.n_keys)}
@@ -192,15 +206,18 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     return build()
 
 
-def counter_workspace_size(n_samples: int, n_intervals: int, key_capacity: int = 0) -> int:
+def counter_workspace_size(n_samples: int, n_intervals: int, key_capacity: int = 0,
+                           flags: int = 0) -> int:
     b = ctypes.c_size_t(0)
-    _check(_lib().mag_counter_workspace_size(n_samples, n_intervals, key_capacity, ctypes.byref(b)))
+    _check(_lib().mag_counter_workspace_size(n_samples, n_intervals, key_capacity, flags,
+                                             ctypes.byref(b)))
     return int(b.value)
 
 
 def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None,
                       validate: bool = True, key_capacity: int | None = None,
-                      indices: bool = True, workspace=None, out=None, time_kernels: bool = False):
+                      indices: bool = True, workspace=None, out=None, time_kernels: bool = False,
+                      latency: bool = False):
     """Per-operator energy from a cumulative energy counter (software replay mode).
 
     t: float64 [n] reading times (s), C: float64 [n] cumulative energy (J),
@@ -214,10 +231,11 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
     n = int(t.shape[0])
     m = int(s.shape[0])
     dev = t.device
-    flags = (0 if validate else SKIP_VALIDATE) | (N.MAG_TIME_KERNELS if time_kernels else 0)
     group = keys is not None
+    flags = ((0 if validate else SKIP_VALIDATE) | (N.MAG_TIME_KERNELS if time_kernels else 0) |
+             (KEY_LATENCY if latency and group else 0))
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
-    ws_bytes = counter_workspace_size(n, m, cap if group else 0)
+    ws_bytes = counter_workspace_size(n, m, cap if group else 0, flags)
     if workspace is None or workspace.numel() < ws_bytes:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     out = out or {}
@@ -234,31 +252,23 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
             ei = torch.empty(m, dtype=torch.int64, device=dev)
     pio = N.IntervalOut(_dev_ptr(energy, torch.float64, "energy"),
                         _dev_ptr(si, torch.int64, "start_idx"), _dev_ptr(ei, torch.int64, "end_idx"))
-    ks = None
-    kout = ksum = km2 = kcnt = None
+    ks = tab = None
     if group:
-        kout = torch.empty(cap, dtype=torch.int64, device=dev)
-        ksum = torch.empty(cap, dtype=torch.float64, device=dev)
-        km2 = torch.empty(cap, dtype=torch.float64, device=dev)
-        kcnt = torch.empty(cap, dtype=torch.int64, device=dev)
-        ks = N.KeyStats(ksum.data_ptr(), km2.data_ptr(), kcnt.data_ptr(), cap, 0)
+        tab, ks = _key_outputs(cap, dev, latency)
     summ = N.Summary()
     rc = lib.mag_attribute_counter(
         _dev_ptr(t, torch.float64, "t"), _dev_ptr(C, torch.float64, "C"), n, float(delay),
         _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
         _dev_ptr(replays, torch.int32, "replays"),
         _dev_ptr(keys, torch.int64, "keys") if group else None, m, flags, ctypes.byref(pio),
-        kout.data_ptr() if group else None, ctypes.byref(ks) if group else None,
+        tab["keys"].data_ptr() if group else None, ctypes.byref(ks) if group else None,
         ctypes.byref(summ), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
     _check(rc)
     per_interval = {"energy": energy}
     if indices:
         per_interval["start_idx"] = si
         per_interval["end_idx"] = ei
-    per_key = None
-    if group:
-        nk = int(ks.n_keys)
-        per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+    per_key = _key_rows(tab, ks) if group else None
     summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
                "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
                "n_keys": int(summ.n_keys), "kernel_ms": summ.tile_kernel_ms,
@@ -298,6 +308,52 @@ def diff(a: dict, b: dict, k: int, workspace=None):
             "n_only_b": int(ro.n_only_b), "n_join": int(ro.n_join)}
 
 
+def detect(a: dict, b: dict, threshold: float = 0.10, tolerance: float = 0.01,
+           rows: int | None = None, workspace=None):
+    """Section 6.1's detection over two per-key tables from attribute(...,
+    latency=True): keys with (E_B - E_A)/E_A >= threshold, in ranking order,
+    with their latencies and a verdict (WASTE when A is at most `tolerance`
+    slower than B, else TRADEOFF).  rows: how many flagged keys to return
+    (default: all keys of A)."""
+    lib = _lib()
+    dev = a["keys"].device
+    na, nb = int(a["keys"].shape[0]), int(b["keys"].shape[0])
+    cap = max(1, int(rows) if rows is not None else na)
+    b_ws = ctypes.c_size_t(0)
+    _check(lib.mag_detect_workspace_size(na, nb, cap, ctypes.byref(b_ws)))
+    if workspace is None or workspace.numel() < int(b_ws.value):
+        workspace = torch.empty(int(b_ws.value), dtype=torch.uint8, device=dev)
+    o = {k: torch.empty(cap, dtype=dt, device=dev) for k, dt in
+         (("key", torch.int64), ("ratio", torch.float64), ("energy_a", torch.float64),
+          ("energy_b", torch.float64), ("count_a", torch.int64), ("count_b", torch.int64),
+          ("latency_a", torch.float64), ("latency_b", torch.float64), ("verdict", torch.int32))}
+
+    def stats(t, n, name):
+        return N.KeyStats(_dev_ptr(t["sum"], torch.float64, f"{name}.sum"),
+                          t["m2"].data_ptr() if "m2" in t else None,
+                          _dev_ptr(t["count"], torch.int64, f"{name}.count"), n, n,
+                          _dev_ptr(t.get("duration"), torch.float64, f"{name}.duration"))
+
+    sa, sb = stats(a, na, "a"), stats(b, nb, "b")
+    out = N.DetectOut()
+    out.rank = N.RankOut(o["key"].data_ptr(), o["ratio"].data_ptr(), o["energy_a"].data_ptr(),
+                         o["energy_b"].data_ptr(), o["count_a"].data_ptr(),
+                         o["count_b"].data_ptr(), cap, 0, 0, 0, 0)
+    out.latency_a = o["latency_a"].data_ptr()
+    out.latency_b = o["latency_b"].data_ptr()
+    out.verdict = o["verdict"].data_ptr()
+    opts = N.DetectOpts(float(threshold), float(tolerance))
+    _check(lib.mag_detect(_dev_ptr(a["keys"], torch.int64, "a.keys"), ctypes.byref(sa),
+                          _dev_ptr(b["keys"], torch.int64, "b.keys"), ctypes.byref(sb),
+                          ctypes.byref(opts), ctypes.byref(out), workspace.data_ptr(),
+                          workspace.numel(), _stream_handle(dev)))
+    r = int(out.rank.n_out)
+    res = {k: v[:r] for k, v in o.items()}
+    res.update(n_flagged=int(out.n_flagged), n_waste=int(out.n_waste),
+               n_tradeoff=int(out.n_tradeoff), n_join=int(out.rank.n_join))
+    return res
+
+
 def stream_workspace_size(max_samples: int, n_intervals: int, key_capacity: int = 0,
                           n_streams: int = 1, stream_offsets=None, flags: int = EQUAL_SPLIT) -> int:
     o, keep = _opts(n_streams, stream_offsets, flags)
@@ -319,12 +375,14 @@ class Stream:
 
     def __init__(self, max_samples: int, s, e, keys=None, *, n_streams: int = 1,
                  stream_offsets=None, equal_split: bool = True, validate: bool = True,
-                 key_capacity: int | None = None, indices: bool = True):
+                 key_capacity: int | None = None, indices: bool = True, latency: bool = False):
         lib = _lib()
         m = int(s.shape[0])
         dev = s.device
         self._dev = dev
-        flags = (EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE)
+        self._lat = latency and keys is not None
+        flags = ((EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE) |
+                 (KEY_LATENCY if self._lat else 0))
         self._o, self._keep = _opts(n_streams, stream_offsets, flags)
         self._group = keys is not None
         self._cap = (int(key_capacity) if key_capacity is not None else max(1, m)) if self._group else 0
@@ -386,16 +444,11 @@ class Stream:
         self._h = None
         dev = self._dev
         cap = self._cap
-        ks = None
-        kout = ksum = km2 = kcnt = None
+        ks = tab = None
         if self._group:
-            kout = torch.empty(cap, dtype=torch.int64, device=dev)
-            ksum = torch.empty(cap, dtype=torch.float64, device=dev)
-            km2 = torch.empty(cap, dtype=torch.float64, device=dev)
-            kcnt = torch.empty(cap, dtype=torch.int64, device=dev)
-            ks = N.KeyStats(ksum.data_ptr(), km2.data_ptr(), kcnt.data_ptr(), cap, 0)
+            tab, ks = _key_outputs(cap, dev, self._lat)
         summ = N.Summary()
-        rc = _lib().mag_stream_end(h, kout.data_ptr() if self._group else None,
+        rc = _lib().mag_stream_end(h, tab["keys"].data_ptr() if self._group else None,
                                    ctypes.byref(ks) if self._group else None, ctypes.byref(summ))
         self._chunks = []
         _check(rc)
@@ -403,10 +456,7 @@ class Stream:
         if self.start_idx is not None:
             per_interval["start_idx"] = self.start_idx
             per_interval["end_idx"] = self.end_idx
-        per_key = None
-        if self._group:
-            nk = int(ks.n_keys)
-            per_key = {"keys": kout[:nk], "sum": ksum[:nk], "m2": km2[:nk], "count": kcnt[:nk]}
+        per_key = _key_rows(tab, ks) if self._group else None
         summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
                    "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
                    "n_keys": int(summ.n_keys)}

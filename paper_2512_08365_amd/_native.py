@@ -29,13 +29,16 @@ MAG_EQUAL_SPLIT = 0x1
 MAG_SKIP_VALIDATE = 0x2
 MAG_TIME_KERNELS = 0x4
 MAG_ASYNC = 0x8
+MAG_KEY_LATENCY = 0x10
+MAG_WASTE = 1
+MAG_TRADEOFF = 2
 MAG_MAX_STREAMS = 32
 
 # every symbol include/magneton.h declares
 EXPORTED = (
     "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_finish",
     "mag_counter_workspace_size", "mag_attribute_counter",
-    "mag_diff_workspace_size", "mag_diff",
+    "mag_diff_workspace_size", "mag_diff", "mag_detect_workspace_size", "mag_detect",
     "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
     "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
     "mag_strerror", "mag_last_error", "mag_version",
@@ -53,7 +56,7 @@ class IntervalOut(ctypes.Structure):
 
 class KeyStats(ctypes.Structure):
     _fields_ = [("sum", c_vp), ("m2", c_vp), ("count", c_vp), ("capacity", c_i64),
-                ("n_keys", c_i64)]
+                ("n_keys", c_i64), ("duration", c_vp)]
 
 
 class Summary(ctypes.Structure):
@@ -66,6 +69,15 @@ class RankOut(ctypes.Structure):
     _fields_ = [("key", c_vp), ("ratio", c_vp), ("energy_a", c_vp), ("energy_b", c_vp),
                 ("count_a", c_vp), ("count_b", c_vp), ("capacity", c_i64), ("n_out", c_i64),
                 ("n_only_a", c_i64), ("n_only_b", c_i64), ("n_join", c_i64)]
+
+
+class DetectOpts(ctypes.Structure):
+    _fields_ = [("threshold", ctypes.c_double), ("tolerance", ctypes.c_double)]
+
+
+class DetectOut(ctypes.Structure):
+    _fields_ = [("rank", RankOut), ("latency_a", c_vp), ("latency_b", c_vp), ("verdict", c_vp),
+                ("n_flagged", c_i64), ("n_waste", c_i64), ("n_tradeoff", c_i64)]
 
 
 _lib = None
@@ -89,7 +101,8 @@ def load(path: str = LIB_PATH):
     lib.mag_attribute.restype = ctypes.c_int
     lib.mag_attribute_finish.argtypes = [c_vp, P(KeyStats), P(Summary), c_vp]
     lib.mag_attribute_finish.restype = ctypes.c_int
-    lib.mag_counter_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
+    lib.mag_counter_workspace_size.argtypes = [c_i64, c_i64, c_i64, ctypes.c_uint32,
+                                               P(ctypes.c_size_t)]
     lib.mag_counter_workspace_size.restype = ctypes.c_int
     lib.mag_attribute_counter.argtypes = [c_vp, c_vp, c_i64, ctypes.c_double, c_vp, c_vp, c_vp,
                                           c_vp, c_i64, ctypes.c_uint32, P(IntervalOut), c_vp,
@@ -100,6 +113,11 @@ def load(path: str = LIB_PATH):
     lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,
                              ctypes.c_size_t, c_vp]
     lib.mag_diff.restype = ctypes.c_int
+    lib.mag_detect_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
+    lib.mag_detect_workspace_size.restype = ctypes.c_int
+    lib.mag_detect.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), P(DetectOpts), P(DetectOut),
+                               c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_detect.restype = ctypes.c_int
     lib.mag_stream_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(AttrOpts), P(ctypes.c_size_t)]
     lib.mag_stream_workspace_size.restype = ctypes.c_int
     lib.mag_stream_begin.argtypes = [P(c_vp), c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),

@@ -57,6 +57,7 @@ struct Plan {
     int nchunks;
     int64_t chunk;
     bool staging;
+    bool lat;  // per-key latency sums (MAG_KEY_LATENCY)
 };
 
 struct AttrWorkspace {
@@ -75,6 +76,7 @@ struct AttrWorkspace {
     uint32_t* pcnt;
     double* psum;
     double* pm2;
+    double* pdur;
     double* stage_t;
     float* stage_P;
 };
@@ -132,6 +134,7 @@ void carve_groupby(Carver& c, const Plan& pl, AttrWorkspace& w)
         w.pcnt = c.take<uint32_t>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.psum = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.pm2 = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
+        if (pl.lat) w.pdur = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
     }
 }
 
@@ -308,6 +311,7 @@ int plan_attribution(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t k
     pl.cap = key_capacity;
     pl.H = 0;
     pl.staging = streaming;
+    pl.lat = key_capacity > 0 && (*flags & MAG_KEY_LATENCY) != 0;
     if (key_capacity > 0) plan_groupby(pl);
     return MAG_OK;
 }
@@ -378,6 +382,7 @@ struct Job {
     const double* s = nullptr;
     const double* e = nullptr;
     const uint64_t* keys = nullptr;
+    const int32_t* reps = nullptr;  // counter mode: replays per window
     double* energy = nullptr;
     int64_t* start_idx = nullptr;
     int64_t* end_idx = nullptr;
@@ -477,6 +482,13 @@ struct Job {
         gp.m2_out = per_key->m2;
         gp.count_out = per_key->count;
         gp.status = w.status;
+        if (pl.lat) {
+            gp.s = s;
+            gp.e = e;
+            gp.reps = reps;
+            gp.dur_out = per_key->duration;
+            gp.pdur = w.pdur;
+        }
         return mag::launch_groupby(gp, stream);
     }
 
@@ -487,13 +499,15 @@ struct Job {
     }
 };
 
-int check_key_outputs(const uint64_t* keys_out, const mag_key_stats* per_key)
+int check_key_outputs(const uint64_t* keys_out, const mag_key_stats* per_key, uint32_t flags)
 {
     if (per_key->capacity < 1) return fail(MAG_E_SIZE, "per_key->capacity must be >= 1");
     if (!keys_out || !per_key->sum || !per_key->m2 || !per_key->count)
         return fail(MAG_E_NULL, "per-key output array is NULL");
+    if ((flags & MAG_KEY_LATENCY) && !per_key->duration)
+        return fail(MAG_E_NULL, "per_key->duration is NULL with MAG_KEY_LATENCY");
     if (!aligned(keys_out, 8) || !aligned(per_key->sum, 8) || !aligned(per_key->m2, 8) ||
-        !aligned(per_key->count, 8))
+        !aligned(per_key->count, 8) || !aligned(per_key->duration, 8))
         return fail(MAG_E_ALIGN, "per-key output array not aligned to its element size");
     return MAG_OK;
 }
@@ -539,7 +553,8 @@ int prepare(Job& job, int64_t n_samples, const double* starts, const double* end
 
 namespace {
 
-int plan_counter(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t key_capacity)
+int plan_counter(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
+                 uint32_t flags)
 {
     if (n_samples < 2) return fail(MAG_E_SIZE, "n_samples must be >= 2");
     if (n_samples > MAG_MAX_SAMPLES) return fail(MAG_E_SIZE, "n_samples exceeds MAG_MAX_SAMPLES");
@@ -554,6 +569,7 @@ int plan_counter(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t key_c
     pl.cap = key_capacity;
     pl.H = 0;
     pl.staging = false;
+    pl.lat = key_capacity > 0 && (flags & MAG_KEY_LATENCY) != 0;
     if (key_capacity > 0) plan_groupby(pl);
     return MAG_OK;
 }
@@ -588,7 +604,8 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
     if (!aligned(timestamps, 8) || !aligned(power, 4))
         return fail(MAG_E_ALIGN, "input array not aligned to its element size");
     int rc;
-    if (per_key && (rc = check_key_outputs(keys_out, per_key)) != MAG_OK) return rc;
+    if (per_key && (rc = check_key_outputs(keys_out, per_key, opts ? opts->flags : 0u)) != MAG_OK)
+        return rc;
     Job job;
     rc = prepare(job, n_samples, starts, ends, op_keys, n_intervals, opts, per_interval,
                  per_key ? per_key->capacity : 0, workspace, workspace_bytes, stream, false);
@@ -636,12 +653,12 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
 }
 
 int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
-                               size_t* bytes)
+                               uint32_t flags, size_t* bytes)
 {
     g_last_error[0] = 0;
     if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
     Plan pl;
-    int rc = plan_counter(pl, n_samples, n_intervals, key_capacity);
+    int rc = plan_counter(pl, n_samples, n_intervals, key_capacity, flags);
     if (rc) return rc;
     AttrWorkspace w{};
     *bytes = carve_counter(pl, nullptr, w);
@@ -661,10 +678,10 @@ int mag_attribute_counter(const double* timestamps, const double* counter, int64
         return fail(MAG_E_ALIGN, "input array not aligned to its element size");
     if (!(delay - delay == 0.0)) return fail(MAG_E_TIMESTAMPS, "delay is not finite");
     int rc;
-    if (per_key && (rc = check_key_outputs(keys_out, per_key)) != MAG_OK) return rc;
+    if (per_key && (rc = check_key_outputs(keys_out, per_key, flags)) != MAG_OK) return rc;
     Job job;
     const int64_t cap = per_key ? per_key->capacity : 0;
-    if ((rc = plan_counter(job.pl, n_samples, n_intervals, cap)) != MAG_OK) return rc;
+    if ((rc = plan_counter(job.pl, n_samples, n_intervals, cap, flags)) != MAG_OK) return rc;
     if (n_intervals > 0 && (!starts || !ends)) return fail(MAG_E_NULL, "starts/ends is NULL");
     if (cap > 0 && n_intervals > 0 && !op_keys) return fail(MAG_E_NULL, "op_keys is NULL");
     if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
@@ -687,6 +704,7 @@ int mag_attribute_counter(const double* timestamps, const double* counter, int64
     job.s = starts;
     job.e = ends;
     job.keys = op_keys;
+    job.reps = replays;
     job.energy = (per_interval && per_interval->energy) ? per_interval->energy : job.w.energy;
     job.start_idx = per_interval ? per_interval->start_idx : nullptr;
     job.end_idx = per_interval ? per_interval->end_idx : nullptr;
@@ -1004,7 +1022,7 @@ int mag_stream_end(mag_stream* h, uint64_t* keys_out, mag_key_stats* per_key, ma
         rc = fail(MAG_E_STATE, "per-key outputs requested but key_capacity was 0 at begin");
     } else if (per_key && per_key->capacity != job.pl.cap) {
         rc = fail(MAG_E_SIZE, "per_key->capacity differs from the key_capacity given at begin");
-    } else if (per_key && (rc = check_key_outputs(keys_out, per_key)) != MAG_OK) {
+    } else if (per_key && (rc = check_key_outputs(keys_out, per_key, job.flags)) != MAG_OK) {
         // rc set
     } else if ((e = hipMemcpyAsync(&job.w.status->bounds[1], job.w.stage_t + (h->n_stage - 1),
                                    sizeof(double), hipMemcpyDeviceToDevice, job.stream)) !=
@@ -1129,22 +1147,30 @@ int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_
     return MAG_OK;
 }
 
-int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
-             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
-             size_t workspace_bytes, hipStream_t stream)
+}  // extern "C"
+
+namespace {
+
+// the join and ranking shared by mag_diff and mag_detect; p's detection fields
+// are set by the caller; the status block is returned in *st
+int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p,
+             void* workspace, size_t workspace_bytes, hipStream_t stream, mag::Status* st)
 {
-    g_last_error[0] = 0;
     if (!statsA || !statsB || !out) return fail(MAG_E_NULL, "statsA/statsB/out is NULL");
     if (k < 0 || statsA->n_keys < 0 || statsB->n_keys < 0) return fail(MAG_E_SIZE, "negative size");
     const int64_t na = statsA->n_keys, nb = statsB->n_keys;
     if ((na > 0 && (!keysA || !statsA->sum || !statsA->count)) ||
         (nb > 0 && (!keysB || !statsB->sum || !statsB->count)))
         return fail(MAG_E_NULL, "key table array is NULL");
+    if (p.detect && ((na > 0 && !statsA->duration) || (nb > 0 && !statsB->duration)))
+        return fail(MAG_E_NULL, "per-key duration array is NULL");
     if (na > INT32_MAX || nb > INT32_MAX) return fail(MAG_E_SIZE, "key table too large");
     const int64_t need_rows = std::min(k, na);
     if (out->capacity < need_rows) return fail(MAG_E_CAPACITY, "out->capacity < min(k, n_keys_a)");
     if (need_rows > 0 && (!out->key || !out->ratio || !out->energy_a || !out->energy_b ||
-                          !out->count_a || !out->count_b))
+                          !out->count_a || !out->count_b ||
+                          (p.detect && (!p.out_la || !p.out_lb || !p.out_verdict))))
         return fail(MAG_E_NULL, "output array is NULL");
     if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
     if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
@@ -1155,7 +1181,6 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     Carver c;
     c.base = static_cast<char*>(workspace);
     const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(na, k), 1);
-    mag::DiffParams p{};
     p.status = c.take<mag::Status>(1);
     p.cand_r = c.take<double>(nc);
     p.cand_key = c.take<uint64_t>(nc);
@@ -1177,18 +1202,68 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     p.out_eb = out->energy_b;
     p.out_ca = out->count_a;
     p.out_cb = out->count_b;
+    if (p.detect) {
+        p.la = statsA->duration;
+        p.lb = statsB->duration;
+    }
     hipError_t e;
     if ((e = mag::launch_init_status(p.status, nullptr, 0, stream)) != hipSuccess)
         return hip_fail(e, "init");
     if ((e = mag::launch_diff(p, stream)) != hipSuccess) return hip_fail(e, "diff kernels");
-    mag::Status st;
-    const int rc = read_status(p.status, stream, &st);
+    const int rc = read_status(p.status, stream, st);
     if (rc != MAG_OK) return rc;
-    if (st.err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
-    out->n_join = st.n_join;
-    out->n_out = std::min<int64_t>(k, st.n_join);
-    out->n_only_a = na - st.n_join;
-    out->n_only_b = nb - st.n_join;
+    if (st->err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
+    out->n_join = st->n_join;
+    out->n_out = std::min<int64_t>(k, st->n_join);
+    out->n_only_a = na - st->n_join;
+    out->n_only_b = nb - st->n_join;
+    return MAG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
+             size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    mag::DiffParams p{};
+    mag::Status st;
+    return run_diff(keysA, statsA, keysB, statsB, k, out, p, workspace, workspace_bytes, stream,
+                    &st);
+}
+
+int mag_detect_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t rows, size_t* bytes)
+{
+    return mag_diff_workspace_size(n_keys_a, n_keys_b, rows, bytes);
+}
+
+int mag_detect(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+               const mag_key_stats* statsB, const mag_detect_opts* opts, mag_detect_out* out,
+               void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!out) return fail(MAG_E_NULL, "out is NULL");
+    mag::DiffParams p{};
+    p.detect = 1;
+    p.threshold = opts ? opts->threshold : 0.10;
+    p.tolerance = opts ? opts->tolerance : 0.01;
+    if (p.threshold != p.threshold || p.tolerance != p.tolerance)
+        return fail(MAG_E_SIZE, "threshold or tolerance is NaN");
+    p.out_la = out->latency_a;
+    p.out_lb = out->latency_b;
+    p.out_verdict = out->verdict;
+    mag::Status st;
+    // the flagged keys are a prefix of the ranking: rank as many rows as fit
+    const int rc = run_diff(keysA, statsA, keysB, statsB, out->rank.capacity, &out->rank, p,
+                            workspace, workspace_bytes, stream, &st);
+    if (rc != MAG_OK) return rc;
+    out->n_flagged = st.n_flag;
+    out->n_waste = st.n_waste;
+    out->n_tradeoff = (int64_t)st.n_flag - (int64_t)st.n_waste;
+    out->rank.n_out = std::min<int64_t>(out->rank.n_out, out->n_flagged);
     return MAG_OK;
 }
 

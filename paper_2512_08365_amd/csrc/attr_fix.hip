@@ -179,6 +179,8 @@ __global__ __launch_bounds__(256) void k_init(Status* st, int64_t* cnt_fin, int6
         st->n_unique = 0u;
         st->n_cand = 0u;
         st->n_join = 0u;
+        st->n_flag = 0u;
+        st->n_waste = 0u;
         st->trace_energy = 0.0;
         st->idle_energy = 0.0;
         st->attributed_energy = 0.0;

@@ -10,6 +10,10 @@
 // Stage 2 (k_diff_rank): every candidate's global rank is the number of
 // candidates ordered before it, counted in 256-candidate slices by many small
 // workgroups; ranks below k are written out (k_diff_write).
+// Detection (Section 6.1) runs the same stages with k = the rows wanted: the
+// flagged keys (r >= threshold) are a prefix of the ranking, so the first
+// rows are the flagged ones; stage 1 also counts every flagged key and the
+// waste among them, and stage 2 writes each row's latencies and verdict.
 
 #include "mag_internal.hpp"
 
@@ -25,6 +29,13 @@ __device__ __forceinline__ double rel_diff(double ea, double eb)
 {
     if (ea == 0.0) return eb > 0.0 ? INFINITY : 0.0;
     return (eb - ea) / ea;
+}
+
+// a flagged key is waste when the efficient side A is at most `tolerance`
+// slower than B
+__device__ __forceinline__ bool is_waste(double la, double lb, double tolerance)
+{
+    return (la - lb) <= tolerance * lb;
 }
 
 // total order of the ranking: larger r first, then smaller key (evaluated
@@ -134,10 +145,19 @@ __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
     const int lane = tid & 63;
     const uint64_t cb = __ballot(cand);
     const unsigned long long nvalid = __popcll(__ballot(valid != 0));
+    bool flag = false, waste = false;
+    if (p.detect && valid) {
+        flag = r >= p.threshold;
+        waste = flag && is_waste(p.la[row0 + tid], p.lb[ib], p.tolerance);
+    }
+    const unsigned long long nflag = __popcll(__ballot(flag));
+    const unsigned long long nwaste = __popcll(__ballot(waste));
     uint32_t base = 0u;
     if (lane == 0) {
         if (cb) base = atomicAdd(&p.status->n_cand, (uint32_t)__popcll(cb));
         if (nvalid) atomicAdd(&p.status->n_join, (uint32_t)nvalid);
+        if (nflag) atomicAdd(&p.status->n_flag, (uint32_t)nflag);
+        if (nwaste) atomicAdd(&p.status->n_waste, (uint32_t)nwaste);
     }
     base = __shfl(base, 0);
     if (cand) {
@@ -192,6 +212,12 @@ __global__ __launch_bounds__(256) void k_diff_write(const DiffParams p)
     p.out_eb[rank] = p.sb[ib];
     p.out_ca[rank] = p.ca[ia];
     p.out_cb[rank] = p.cb[ib];
+    if (p.detect) {
+        const double la = p.la[ia], lb = p.lb[ib];
+        p.out_la[rank] = la;
+        p.out_lb[rank] = lb;
+        p.out_verdict[rank] = is_waste(la, lb, p.tolerance) ? MAG_WASTE : MAG_TRADEOFF;
+    }
 }
 
 int64_t diff_max_candidates(int64_t na, int64_t k)

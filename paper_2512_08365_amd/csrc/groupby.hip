@@ -72,6 +72,13 @@ __device__ __forceinline__ uint32_t resolve_id(const GroupParams& p, uint32_t r)
     return (h <= p.H) ? (uint32_t)p.table[2 * (size_t)h + 1] : NO_ID;
 }
 
+// an interval's duration, per replay run when replay counts are given
+__device__ __forceinline__ double interval_duration(const GroupParams& p, int64_t i)
+{
+    const double d = p.e[i] - p.s[i];
+    return p.reps ? d / (double)p.reps[i] : d;
+}
+
 }  // namespace
 
 // Insert the distinct keys of a prefix of the intervals.  Each workgroup first
@@ -458,22 +465,34 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
 __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupParams p)
 {
     __shared__ double qs[FIN_GROUPS][FIN_KEYS];
+    __shared__ double qd[FIN_GROUPS][FIN_KEYS];
     const int kl = threadIdx.x % FIN_KEYS, grp = threadIdx.x / FIN_KEYS;
     const int64_t id = (int64_t)blockIdx.x * FIN_KEYS + kl;
     // loads requested before the key count is read, as in k_fin_sum
-    double m2 = 0.0;
+    double m2 = 0.0, du = 0.0;
     if (id < p.cap)
 #pragma unroll 16
         for (int c = grp; c < p.nchunks; c += FIN_GROUPS) m2 += p.pm2[(int64_t)c * p.cap + id];
+    if (p.dur_out && id < p.cap)
+#pragma unroll 16
+        for (int c = grp; c < p.nchunks; c += FIN_GROUPS) du += p.pdur[(int64_t)c * p.cap + id];
     const uint32_t r = (grp == 0 && id < p.cap) ? p.urank[id] : 0xffffffffu;
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
     if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     qs[grp][kl] = m2;
+    qd[grp][kl] = du;
     __syncthreads();
     if (grp == 0 && id < nk) {
         m2 = 0.0;
-        for (int g = 0; g < FIN_GROUPS; ++g) m2 += qs[g][kl];
-        if ((int64_t)r < p.cap) p.m2_out[r] = m2;
+        du = 0.0;
+        for (int g = 0; g < FIN_GROUPS; ++g) {
+            m2 += qs[g][kl];
+            du += qd[g][kl];
+        }
+        if ((int64_t)r < p.cap) {
+            p.m2_out[r] = m2;
+            if (p.dur_out) p.dur_out[r] = du;
+        }
     }
 }
 
@@ -533,6 +552,52 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_one(const GroupParams p)
         if (d[k] >= 0) atomicAdd(&lsum[d[k]], en[k] * en[k]);
     __syncthreads();
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) p.pm2[(int64_t)c * p.cap + r0 + v] = lsum[v];
+    if (!p.dur_out) return;  // uniform
+    // per-key latency: the same table once more, over the interval durations
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k)
+        en[k] = (d[k] >= 0) ? interval_duration(p, lo + threadIdx.x + (int64_t)k * AGG_THREADS) : 0.0;
+    __syncthreads();
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) lsum[v] = 0.0;
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < AGG_BATCH; ++k)
+        if (d[k] >= 0) atomicAdd(&lsum[d[k]], en[k]);
+    __syncthreads();
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) p.pdur[(int64_t)c * p.cap + r0 + v] = lsum[v];
+}
+
+// per-key latency when a chunk spans several batches: one more pass
+__global__ __launch_bounds__(AGG_THREADS) void k_agg_dur(const GroupParams p)
+{
+    __shared__ double ldur[AGG_IDS];
+    const int c = blockIdx.x;
+    const int64_t r0 = (int64_t)blockIdx.y * AGG_IDS;
+    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if (r0 >= nk) return;
+    const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) ldur[v] = 0.0;
+    __syncthreads();
+    const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
+    for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)AGG_BATCH * AGG_THREADS) {
+        uint32_t sl[AGG_BATCH];
+        double du[AGG_BATCH];
+#pragma unroll
+        for (int k = 0; k < AGG_BATCH; ++k) {
+            const int64_t i = i0 + (int64_t)k * AGG_THREADS;
+            sl[k] = (i < hi) ? p.slot[i] : NO_ID;
+            du[k] = (i < hi) ? interval_duration(p, i) : 0.0;
+        }
+#pragma unroll
+        for (int k = 0; k < AGG_BATCH; ++k) {
+            const uint32_t id = resolve_id(p, sl[k]);
+            const int64_t d = (id == NO_ID) ? -1 : (int64_t)id - r0;
+            if (d < 0 || d >= nid) continue;
+            atomicAdd(&ldur[d], du[k]);
+        }
+    }
+    __syncthreads();
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) p.pdur[(int64_t)c * p.cap + r0 + v] = ldur[v];
 }
 
 // per key: count and sum over the chunk rows (as k_fin_sum), then
@@ -545,16 +610,21 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
     __shared__ uint64_t qc[FO_GROUPS][FO_KEYS];
     __shared__ double qs[FO_GROUPS][FO_KEYS];
     __shared__ double qmean[FO_KEYS];
+    __shared__ double qdu[FO_GROUPS][FO_KEYS];
     const int kl = threadIdx.x % FO_KEYS, grp = threadIdx.x / FO_KEYS;
     const int64_t id = (int64_t)blockIdx.x * FO_KEYS + kl;
     uint64_t cnt = 0;
-    double sum = 0.0;
+    double sum = 0.0, du = 0.0;
     if (id < p.cap) {
 #pragma unroll 8
         for (int c = grp; c < p.nchunks; c += FO_GROUPS) {
             cnt += p.pcnt[(int64_t)c * p.cap + id];
             sum += p.psum[(int64_t)c * p.cap + id];
         }
+    }
+    if (p.dur_out && id < p.cap) {
+#pragma unroll 8
+        for (int c = grp; c < p.nchunks; c += FO_GROUPS) du += p.pdur[(int64_t)c * p.cap + id];
     }
     uint32_t r = 0xffffffffu;
     uint64_t key = 0;
@@ -566,14 +636,17 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
     if ((int64_t)blockIdx.x * FO_KEYS >= nk) return;  // uniform
     qc[grp][kl] = cnt;
     qs[grp][kl] = sum;
+    qdu[grp][kl] = du;
     __syncthreads();
     double tot = 0.0;
     if (grp == 0) {
         cnt = 0;
         sum = 0.0;
+        du = 0.0;
         for (int g = 0; g < FO_GROUPS; ++g) {
             cnt += qc[g][kl];
             sum += qs[g][kl];
+            du += qdu[g][kl];
         }
         qmean[kl] = cnt ? sum / (double)cnt : 0.0;
         if (id < nk) {
@@ -581,6 +654,7 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
                 p.keys_out[r] = key;
                 p.count_out[r] = (int64_t)cnt;
                 p.sum_out[r] = sum;
+                if (p.dur_out) p.dur_out[r] = du;
             }
             tot = sum;
         }
@@ -647,6 +721,9 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
         hipLaunchKernelGGL(k_fin_sum, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
         hipLaunchKernelGGL(k_agg_m2, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
                            stream, p);
+        if (p.dur_out)
+            hipLaunchKernelGGL(k_agg_dur, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS),
+                               0, stream, p);
         hipLaunchKernelGGL(k_fin_m2, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
     }
     return hipGetLastError();

@@ -39,14 +39,14 @@ enum : uint32_t {
 // small device status block at the head of every workspace
 struct Status {
     uint32_t err;
-    uint32_t pad1;
+    uint32_t n_flag;      // detect: joined keys at or above the threshold
     uint32_t special;     // the all-ones key was seen (stored out of band)
     uint32_t overflow;    // a key found no free slot
     unsigned long long n_clipped;
     uint32_t n_unique;    // rows of the compacted distinct-key list
     uint32_t n_cand;      // diff: surviving candidates
     uint32_t n_join;      // diff: keys present on both sides
-    uint32_t pad0;
+    uint32_t n_waste;     // detect: flagged keys judged waste
     double trace_energy;
     double idle_energy;
     double attributed_energy;
@@ -133,6 +133,12 @@ struct GroupParams {
     double* m2_out;
     int64_t* count_out;
     Status* status;
+    // per-key latency (dur_out NULL: none): sum of (e - s) / reps (reps NULL: 1)
+    const double* s;
+    const double* e;
+    const int32_t* reps;
+    double* dur_out;      // [cap]
+    double* pdur;         // [nchunks][cap]
 };
 
 // per-operator energy from a delayed cumulative energy counter
@@ -184,6 +190,16 @@ struct DiffParams {
     int64_t* out_ca;
     int64_t* out_cb;
     Status* status;
+    // detection (detect != 0): flag r >= threshold; waste when
+    // (la - lb) <= tolerance * lb
+    int detect;
+    double threshold;
+    double tolerance;
+    const double* la;     // [na] per-key latency of A
+    const double* lb;     // [nb]
+    double* out_la;
+    double* out_lb;
+    int32_t* out_verdict;
 };
 
 // Workgroup barrier for LDS traffic only: waits for this wave's LDS operations

@@ -81,14 +81,17 @@ def test_counter_host_side_errors_without_gpu():
     from paper_2512_08365_amd import _native as N
     lib = N.load()
     b = ctypes.c_size_t(0)
-    assert lib.mag_counter_workspace_size(1, 0, 0, ctypes.byref(b)) == N.MAG_E_SIZE
-    assert lib.mag_counter_workspace_size(10, -1, 0, ctypes.byref(b)) == N.MAG_E_SIZE
-    assert lib.mag_counter_workspace_size(10, 5, -1, ctypes.byref(b)) == N.MAG_E_SIZE
-    assert lib.mag_counter_workspace_size(10, 5, 0, None) == N.MAG_E_NULL
-    assert lib.mag_counter_workspace_size(10, 500, 0, ctypes.byref(b)) == N.MAG_OK
+    assert lib.mag_counter_workspace_size(1, 0, 0, 0, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_counter_workspace_size(10, -1, 0, 0, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_counter_workspace_size(10, 5, -1, 0, ctypes.byref(b)) == N.MAG_E_SIZE
+    assert lib.mag_counter_workspace_size(10, 5, 0, 0, None) == N.MAG_E_NULL
+    assert lib.mag_counter_workspace_size(10, 500, 0, 0, ctypes.byref(b)) == N.MAG_OK
     plain = b.value
-    assert lib.mag_counter_workspace_size(10, 500, 64, ctypes.byref(b)) == N.MAG_OK
-    assert b.value > plain  # the group-by state
+    assert lib.mag_counter_workspace_size(10, 500, 64, 0, ctypes.byref(b)) == N.MAG_OK
+    grouped = b.value
+    assert grouped > plain  # the group-by state
+    assert lib.mag_counter_workspace_size(10, 500, 64, N.MAG_KEY_LATENCY, ctypes.byref(b)) == 0
+    assert b.value > grouped  # the per-chunk latency rows
     fake = ctypes.c_void_p(256)
     big = 1 << 30
 
@@ -110,6 +113,43 @@ def test_counter_host_side_errors_without_gpu():
     assert call(reps=ctypes.c_void_p(258)) == N.MAG_E_ALIGN
     assert call(ws_bytes=16) == N.MAG_E_WORKSPACE
     assert b"workspace" in lib.mag_last_error()
+
+
+def test_latency_and_detect_host_side_errors_without_gpu():
+    from paper_2512_08365_amd import _native as N
+    lib = N.load()
+    b = ctypes.c_size_t(0)
+    assert lib.mag_attribute_workspace_size(10_000, 3, 8, None, ctypes.byref(b)) == N.MAG_OK
+    plain = b.value
+    o = N.AttrOpts(1, N.MAG_EQUAL_SPLIT | N.MAG_KEY_LATENCY, None)
+    assert lib.mag_attribute_workspace_size(10_000, 3, 8, ctypes.byref(o), ctypes.byref(b)) == 0
+    assert b.value > plain
+    fake = ctypes.c_void_p(256)
+    # MAG_KEY_LATENCY needs the per-key duration array
+    ks = N.KeyStats(fake, fake, fake, 8, 0, None)
+    assert lib.mag_attribute(fake, fake, 10, fake, fake, fake, 3, ctypes.byref(o), None, fake,
+                             ctypes.byref(ks), None, fake, 1 << 30, None) == N.MAG_E_NULL
+    assert b"duration" in lib.mag_last_error()
+    ks.duration = ctypes.c_void_p(260)
+    assert lib.mag_attribute(fake, fake, 10, fake, fake, fake, 3, ctypes.byref(o), None, fake,
+                             ctypes.byref(ks), None, fake, 1 << 30, None) == N.MAG_E_ALIGN
+    # detect: durations required on both sides, thresholds must be numbers
+    sa = N.KeyStats(fake, None, fake, 5, 5, None)
+    sb = N.KeyStats(fake, None, fake, 5, 5, fake)
+    out = N.DetectOut()
+    out.rank = N.RankOut(fake, fake, fake, fake, fake, fake, 5, 0, 0, 0, 0)
+    out.latency_a = out.latency_b = out.verdict = fake
+    assert lib.mag_detect(fake, ctypes.byref(sa), fake, ctypes.byref(sb), None, ctypes.byref(out),
+                          fake, 1 << 20, None) == N.MAG_E_NULL
+    sa.duration = fake
+    nan = N.DetectOpts(float("nan"), 0.01)
+    assert lib.mag_detect(fake, ctypes.byref(sa), fake, ctypes.byref(sb), ctypes.byref(nan),
+                          ctypes.byref(out), fake, 1 << 20, None) == N.MAG_E_SIZE
+    out.verdict = None
+    assert lib.mag_detect(fake, ctypes.byref(sa), fake, ctypes.byref(sb), None, ctypes.byref(out),
+                          fake, 1 << 20, None) == N.MAG_E_NULL
+    assert lib.mag_detect(None, None, None, None, None, None, None, 0, None) == N.MAG_E_NULL
+    assert lib.mag_detect_workspace_size(5, 5, -1, ctypes.byref(b)) == N.MAG_E_SIZE
 
 
 def test_stream_host_side_errors_without_gpu():
