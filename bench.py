@@ -195,6 +195,56 @@ def cpu_baseline(A, B):
             "samples_per_s": (A["t"].shape[0] + B["t"].shape[0]) / dt}
 
 
+def counter_session(args, torch, mag):
+    """Counter (software replay) attribution of a replay profiling session:
+    98,304 operator windows x 1,000 replays read by a 50 Hz counter with a
+    0.1 s lag, with per-key energy and latency; one JSON line."""
+    import numpy as np
+    import synth
+    c = synth.replay_session(args.seed)
+    d = {k: torch.from_numpy(np.ascontiguousarray(c[k])).cuda() for k in ("t", "C", "s", "e")}
+    key = torch.from_numpy(c["key"].view(np.int64)).cuda()
+    reps = torch.from_numpy(c["reps"]).cuda()
+    n, m = int(c["t"].shape[0]), int(c["s"].shape[0])
+    cap = 1024
+    ws = torch.empty(mag.counter_workspace_size(n, m, cap, mag.KEY_LATENCY), dtype=torch.uint8,
+                     device="cuda")
+    out = {"energy": torch.empty(m, dtype=torch.float64, device="cuda"),
+           "start_idx": torch.empty(m, dtype=torch.int64, device="cuda"),
+           "end_idx": torch.empty(m, dtype=torch.int64, device="cuda")}
+
+    def call(timed):
+        return mag.attribute_counter(d["t"], d["C"], d["s"], d["e"], key, delay=c["delay"],
+                                     replays=reps, key_capacity=cap, workspace=ws, out=out,
+                                     latency=True, time_kernels=timed)
+
+    for _ in range(args.warmup):
+        call(False)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        call(False)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    kms = [call(True)[2]["kernel_ms"] for _ in range(args.steps)]
+    kernel_ms = sum(kms) / len(kms)
+    res = {"mode": "counter replay session", "n_readings": n, "n_windows": m, "keys": 416,
+           "ms_per_call": sec * 1e3, "windows_per_s": m / sec, "readings_per_s": n / sec,
+           "window_kernel_ms": kernel_ms,
+           "window_kernel_gbps": (16 * n + 44 * m) / (kernel_ms * 1e-3) / 1e9}
+    if not args.no_cpu_baseline:
+        import oracle
+        t0 = time.perf_counter()
+        r = oracle.counter_attribute(c["t"], c["C"], c["s"], c["e"], c["delay"], c["reps"])
+        oracle.groupby(c["key"], r["energy"])
+        oracle.key_latency(c["key"], c["s"], c["e"], c["reps"])
+        dt = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": m / dt, "unit": "windows/s", "cores": 1, "kind": "oracle",
+                               "sample": "the whole session, attribution + grouping + latency",
+                               "seconds": round(dt, 3)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +252,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--counter-session", action="store_true",
+                    help="measure the counter (software replay) attribution instead")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run the 1 GiB calibration copy (for the HBM counters)")
     ap.add_argument("--summarize-counters", nargs=5,
@@ -231,6 +283,9 @@ def main():
         sys.exit(1)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.counter_session:
+        counter_session(args, torch, mag)
         return
     lib = N.load()
     log(f"[bench] {mag.version()} on {torch.cuda.get_device_name(0)}")
