@@ -116,6 +116,11 @@ typedef struct mag_key_stats {
                       /* of mag_diff                                               */
     double* duration; /* with MAG_KEY_LATENCY: sum of the key's interval durations */
                       /* (s); read by mag_detect; may be NULL otherwise           */
+    int64_t* n_keys_device; /* device int64, may be NULL: the attribution writes   */
+                      /* the number of rows filled there, in stream order; mag_diff */
+                      /* and mag_detect read the count there when n_keys < 0, so  */
+                      /* that the comparison can be enqueued before the           */
+                      /* attributions have finished (capacity then bounds it)     */
 } mag_key_stats;
 
 /* Whole-trace figures (host struct). */

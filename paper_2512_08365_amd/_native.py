@@ -56,7 +56,7 @@ class IntervalOut(ctypes.Structure):
 
 class KeyStats(ctypes.Structure):
     _fields_ = [("sum", c_vp), ("m2", c_vp), ("count", c_vp), ("capacity", c_i64),
-                ("n_keys", c_i64), ("duration", c_vp)]
+                ("n_keys", c_i64), ("duration", c_vp), ("n_keys_device", c_vp)]
 
 
 class Summary(ctypes.Structure):

@@ -459,7 +459,10 @@ struct Job {
 
     hipError_t grouping(uint64_t* keys_out, mag_key_stats* per_key)
     {
-        if (pl.m == 0) return hipSuccess;
+        if (pl.m == 0)
+            return (per_key && per_key->n_keys_device)
+                       ? mag::launch_set_i64(per_key->n_keys_device, 0, stream)
+                       : hipSuccess;
         if (!per_key) return mag::launch_energy_total(energy, pl.m, w.status, stream);
         mag::GroupParams gp{};
         gp.keys = keys;
@@ -482,6 +485,7 @@ struct Job {
         gp.m2_out = per_key->m2;
         gp.count_out = per_key->count;
         gp.status = w.status;
+        gp.n_keys_out = per_key->n_keys_device;
         if (pl.lat) {
             gp.s = s;
             gp.e = e;
@@ -507,7 +511,8 @@ int check_key_outputs(const uint64_t* keys_out, const mag_key_stats* per_key, ui
     if ((flags & MAG_KEY_LATENCY) && !per_key->duration)
         return fail(MAG_E_NULL, "per_key->duration is NULL with MAG_KEY_LATENCY");
     if (!aligned(keys_out, 8) || !aligned(per_key->sum, 8) || !aligned(per_key->m2, 8) ||
-        !aligned(per_key->count, 8) || !aligned(per_key->duration, 8))
+        !aligned(per_key->count, 8) || !aligned(per_key->duration, 8) ||
+        !aligned(per_key->n_keys_device, 8))
         return fail(MAG_E_ALIGN, "per-key output array not aligned to its element size");
     return MAG_OK;
 }
@@ -1158,8 +1163,13 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
              void* workspace, size_t workspace_bytes, hipStream_t stream, mag::Status* st)
 {
     if (!statsA || !statsB || !out) return fail(MAG_E_NULL, "statsA/statsB/out is NULL");
-    if (k < 0 || statsA->n_keys < 0 || statsB->n_keys < 0) return fail(MAG_E_SIZE, "negative size");
-    const int64_t na = statsA->n_keys, nb = statsB->n_keys;
+    // a negative n_keys: the count is read on the device, bounded by the capacity
+    const bool devA = statsA->n_keys < 0, devB = statsB->n_keys < 0;
+    if (k < 0 || (devA && (!statsA->n_keys_device || statsA->capacity < 0)) ||
+        (devB && (!statsB->n_keys_device || statsB->capacity < 0)))
+        return fail(MAG_E_SIZE, "negative size (or n_keys < 0 without n_keys_device)");
+    const int64_t na = devA ? statsA->capacity : statsA->n_keys;
+    const int64_t nb = devB ? statsB->capacity : statsB->n_keys;
     if ((na > 0 && (!keysA || !statsA->sum || !statsA->count)) ||
         (nb > 0 && (!keysB || !statsB->sum || !statsB->count)))
         return fail(MAG_E_NULL, "key table array is NULL");
@@ -1195,6 +1205,8 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     p.sb = statsB->sum;
     p.cb = statsB->count;
     p.nb = nb;
+    p.na_dev = devA ? statsA->n_keys_device : nullptr;
+    p.nb_dev = devB ? statsB->n_keys_device : nullptr;
     p.k = k;
     p.out_key = out->key;
     p.out_ratio = out->ratio;
@@ -1213,10 +1225,12 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     const int rc = read_status(p.status, stream, st);
     if (rc != MAG_OK) return rc;
     if (st->err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
+    const int64_t ra = (devA || devB) ? (int64_t)st->diff_na : na;
+    const int64_t rb = (devA || devB) ? (int64_t)st->diff_nb : nb;
     out->n_join = st->n_join;
     out->n_out = std::min<int64_t>(k, st->n_join);
-    out->n_only_a = na - st->n_join;
-    out->n_only_b = nb - st->n_join;
+    out->n_only_a = ra - st->n_join;
+    out->n_only_b = rb - st->n_join;
     return MAG_OK;
 }
 

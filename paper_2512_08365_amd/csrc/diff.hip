@@ -70,19 +70,33 @@ __device__ int64_t wave_count_below(const uint64_t* a, int64_t n, uint64_t v, bo
 
 }  // namespace
 
+// the key-table sizes: host values, or counts the attributions left on the
+// device (never above the host bound)
+__device__ __forceinline__ int64_t rows_a(const DiffParams& p)
+{
+    return p.na_dev ? min(max(*p.na_dev, (int64_t)0), p.na) : p.na;
+}
+__device__ __forceinline__ int64_t rows_b(const DiffParams& p)
+{
+    return p.nb_dev ? min(max(*p.nb_dev, (int64_t)0), p.nb) : p.nb;
+}
+
 // both key tables strictly ascending (the grid strides over the rows)
-__device__ __forceinline__ void check_ascending(const DiffParams& p)
+__device__ __forceinline__ void check_ascending(const DiffParams& p, int64_t na, int64_t nb)
 {
     unsigned bad = 0u;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i + 1 < max(p.na, p.nb);
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i + 1 < max(na, nb);
          i += (int64_t)gridDim.x * blockDim.x) {
-        if (i + 1 < p.na && !(p.ka[i] < p.ka[i + 1])) bad = 1u;
-        if (i + 1 < p.nb && !(p.kb[i] < p.kb[i + 1])) bad = 1u;
+        if (i + 1 < na && !(p.ka[i] < p.ka[i + 1])) bad = 1u;
+        if (i + 1 < nb && !(p.kb[i] < p.kb[i + 1])) bad = 1u;
     }
     if (bad) atomicOr(&p.status->err, ERR_KEYS);
 }
 
-__global__ __launch_bounds__(256) void k_diff_check(const DiffParams p) { check_ascending(p); }
+__global__ __launch_bounds__(256) void k_diff_check(const DiffParams p)
+{
+    check_ascending(p, rows_a(p), rows_b(p));
+}
 
 __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
 {
@@ -92,13 +106,19 @@ __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
     __shared__ int lv[JOIN_ROWS];
     __shared__ int64_t sh_range[2];
     const int tid = threadIdx.x;
-    check_ascending(p);  // (in the same launch: a failed check voids the result anyway)
+    const int64_t na = rows_a(p), nb = rows_b(p);
+    if (blockIdx.x == 0 && tid == 0) {
+        p.status->diff_na = (uint32_t)na;
+        p.status->diff_nb = (uint32_t)nb;
+    }
+    check_ascending(p, na, nb);  // (in the same launch: a failed check voids the result anyway)
     const int64_t row0 = (int64_t)blockIdx.x * JOIN_ROWS;
-    const int64_t rows = min((int64_t)JOIN_ROWS, p.na - row0);
+    const int64_t rows = min((int64_t)JOIN_ROWS, na - row0);
+    if (rows <= 0) return;  // uniform: rows past a count read on the device
     if (tid < 64) {
         // B rows that can match: keys in [A[row0], A[row0 + rows - 1]]
-        const int64_t lo = wave_count_below(p.kb, p.nb, p.ka[row0], false);
-        const int64_t hi = wave_count_below(p.kb, p.nb, p.ka[row0 + rows - 1], true);
+        const int64_t lo = wave_count_below(p.kb, nb, p.ka[row0], false);
+        const int64_t hi = wave_count_below(p.kb, nb, p.ka[row0 + rows - 1], true);
         if (tid == 0) {
             sh_range[0] = lo;
             sh_range[1] = max(hi, lo);
@@ -228,12 +248,13 @@ int64_t diff_max_candidates(int64_t na, int64_t k)
 
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream)
 {
-    if (p.na == 0 || p.nb == 0) {
+    const bool on_device = p.na_dev || p.nb_dev;  // sizes known on the device only
+    if (!on_device && (p.na == 0 || p.nb == 0)) {
         const int64_t mx = max(p.na, p.nb);
         const unsigned cb = (unsigned)max((int64_t)1, min((mx + 255) / 256, (int64_t)1024));
         hipLaunchKernelGGL(k_diff_check, dim3(cb), dim3(256), 0, stream, p);
     }
-    if (p.na > 0 && p.nb > 0) {
+    if (on_device ? p.na > 0 : (p.na > 0 && p.nb > 0)) {
         const unsigned jb = (unsigned)((p.na + JOIN_ROWS - 1) / JOIN_ROWS);
         hipLaunchKernelGGL(k_diff_join, dim3(jb), dim3(JOIN_ROWS), 0, stream, p);
         const int64_t mc = diff_max_candidates(p.na, p.k);

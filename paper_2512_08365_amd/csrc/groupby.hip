@@ -398,6 +398,7 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
         key = p.ukey[id];
     }
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if (p.n_keys_out && blockIdx.x == 0 && threadIdx.x == 0) *p.n_keys_out = nk;
     if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     qc[grp][kl] = cnt;
     qs[grp][kl] = sum;
@@ -633,6 +634,7 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
         key = p.ukey[id];
     }
     const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    if (p.n_keys_out && blockIdx.x == 0 && threadIdx.x == 0) *p.n_keys_out = nk;
     if ((int64_t)blockIdx.x * FO_KEYS >= nk) return;  // uniform
     qc[grp][kl] = cnt;
     qs[grp][kl] = sum;
@@ -687,9 +689,17 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
     }
 }
 
+__global__ void k_set_i64(int64_t* dst, int64_t v) { *dst = v; }
+
+hipError_t launch_set_i64(int64_t* dst, int64_t v, hipStream_t stream)
+{
+    hipLaunchKernelGGL(k_set_i64, dim3(1), dim3(1), 0, stream, dst, v);
+    return hipGetLastError();
+}
+
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
 {
-    if (p.m <= 0) return hipSuccess;
+    if (p.m <= 0) return p.n_keys_out ? launch_set_i64(p.n_keys_out, 0, stream) : hipSuccess;
     const int64_t n_ins = min(p.m, (int64_t)INS_CHUNK * INS_GROUPS);
     hipLaunchKernelGGL(k_key_insert, dim3((unsigned)((n_ins + INS_CHUNK - 1) / INS_CHUNK)),
                        dim3(INS_THREADS), 0, stream, p, n_ins);

@@ -51,6 +51,8 @@ struct Status {
     double idle_energy;
     double attributed_energy;
     double bounds[2];     // t_0 and t_{n-1}
+    uint32_t diff_na;     // diff: key-table rows read on the device
+    uint32_t diff_nb;
 };
 static_assert(sizeof(Status) <= 256, "status block");
 
@@ -139,6 +141,7 @@ struct GroupParams {
     const int32_t* reps;
     double* dur_out;      // [cap]
     double* pdur;         // [nchunks][cap]
+    int64_t* n_keys_out;  // device copy of the number of rows filled, or NULL
 };
 
 // per-operator energy from a delayed cumulative energy counter
@@ -192,6 +195,10 @@ struct DiffParams {
     Status* status;
     // detection (detect != 0): flag r >= threshold; waste when
     // (la - lb) <= tolerance * lb
+    // key-table rows on the device (NULL: na / nb are the counts; otherwise
+    // na / nb are upper bounds and the counts are read here)
+    const int64_t* na_dev;
+    const int64_t* nb_dev;
     int detect;
     double threshold;
     double tolerance;
@@ -224,6 +231,8 @@ hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_st
 // intervals spanning tiles, endpoints outside the trace, clearing of the group-by state
 hipError_t launch_fix(const FixParams& p, hipStream_t stream);
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
+// *dst = v, in stream order (a kernel, so the write can sit in a captured graph)
+hipError_t launch_set_i64(int64_t* dst, int64_t v, hipStream_t stream);
 // window energies of the counter mode (ev_start / ev_stop may be NULL), then the
 // fold of the per-chunk figures into the status block and the group-by clearing
 hipError_t launch_counter(const CounterParams& p, hipStream_t stream, hipEvent_t ev_start = nullptr,

@@ -52,3 +52,114 @@ def test_overlapped_sides_match_serial_and_event_orders_the_outputs():
                                        rtol=1e-12)
             assert got[2]["n_clipped"] == want[2]["n_clipped"]
         assert torch.equal(seen, serial[0][0]["energy"])
+
+
+def test_diff_enqueued_before_the_attributions_finish():
+    """Key counts left on the device (n_keys_device, n_keys = -1 for the diff):
+    A on one stream, B on another from A's intervals_ready event, the diff and
+    the detection enqueued right after without a host wait, against the same
+    calls made one after the other with host counts."""
+    import ctypes
+    import torch
+    import paper_2512_08365_amd as mag
+    from paper_2512_08365_amd import _native as N
+    lib = N.load()
+    A, B = synth.sides(1, 0)
+    cap, k = 64, 10
+
+    class Side:
+        def __init__(self, c, ready=None):
+            self.d = to_gpu(c)
+            self.m = int(c["s"].shape[0])
+            self.n = int(c["t"].shape[0])
+            self.tab = {"keys": torch.empty(cap, dtype=torch.int64, device="cuda"),
+                        "sum": torch.empty(cap, dtype=torch.float64, device="cuda"),
+                        "m2": torch.empty(cap, dtype=torch.float64, device="cuda"),
+                        "count": torch.empty(cap, dtype=torch.int64, device="cuda"),
+                        "duration": torch.empty(cap, dtype=torch.float64, device="cuda")}
+            self.nk = torch.full((1,), -7, dtype=torch.int64, device="cuda")
+            t = self.tab
+            self.ks = N.KeyStats(t["sum"].data_ptr(), t["m2"].data_ptr(), t["count"].data_ptr(),
+                                 cap, 0, t["duration"].data_ptr(), self.nk.data_ptr())
+            # the diff's view: count on the device
+            self.kd = N.KeyStats(t["sum"].data_ptr(), t["m2"].data_ptr(), t["count"].data_ptr(),
+                                 cap, -1, t["duration"].data_ptr(), self.nk.data_ptr())
+            self.opts = N.AttrOpts(1, N.MAG_EQUAL_SPLIT | N.MAG_ASYNC | N.MAG_KEY_LATENCY, None,
+                                   ready)
+            b = ctypes.c_size_t(0)
+            assert lib.mag_attribute_workspace_size(self.n, self.m, cap, ctypes.byref(self.opts),
+                                                    ctypes.byref(b)) == 0
+            self.ws = torch.empty(int(b.value), dtype=torch.uint8, device="cuda")
+            self.summ = N.Summary()
+
+        def attribute(self, stream):
+            d = self.d
+            assert lib.mag_attribute(d["t"].data_ptr(), d["P"].data_ptr(), self.n,
+                                     d["s"].data_ptr(), d["e"].data_ptr(), d["key"].data_ptr(),
+                                     self.m, ctypes.byref(self.opts), None,
+                                     self.tab["keys"].data_ptr(), ctypes.byref(self.ks),
+                                     ctypes.byref(self.summ), self.ws.data_ptr(),
+                                     self.ws.numel(), stream) == 0
+
+        def finish(self, stream):
+            assert lib.mag_attribute_finish(self.ws.data_ptr(), ctypes.byref(self.ks),
+                                            ctypes.byref(self.summ), stream) == 0
+
+    s1 = torch.cuda.current_stream()
+    s2 = torch.cuda.Stream()
+    ready = torch.cuda.Event()
+    ready.record(s1)
+    sa = Side(A, ctypes.c_void_p(ready.cuda_event))
+    sb = Side(B)
+    h1, h2 = ctypes.c_void_p(s1.cuda_stream), ctypes.c_void_p(s2.cuda_stream)
+
+    def outputs(rows):
+        o = {n: torch.empty(rows, dtype=dt, device="cuda") for n, dt in
+             (("key", torch.int64), ("ratio", torch.float64), ("ea", torch.float64),
+              ("eb", torch.float64), ("ca", torch.int64), ("cb", torch.int64),
+              ("la", torch.float64), ("lb", torch.float64), ("v", torch.int32))}
+        ro = N.RankOut(o["key"].data_ptr(), o["ratio"].data_ptr(), o["ea"].data_ptr(),
+                       o["eb"].data_ptr(), o["ca"].data_ptr(), o["cb"].data_ptr(), rows, 0, 0,
+                       0, 0)
+        return o, ro
+
+    b = ctypes.c_size_t(0)
+    lib.mag_diff_workspace_size(cap, cap, cap, ctypes.byref(b))
+    dws = torch.empty(int(b.value), dtype=torch.uint8, device="cuda")
+    for rep in range(3):
+        log(f"[device counts] repetition {rep}")
+        sa.nk.fill_(-7)
+        sb.nk.fill_(-7)
+        sa.attribute(h1)
+        s2.wait_event(ready)
+        sb.attribute(h2)
+        s1.wait_stream(s2)
+        o1, ro1 = outputs(k)
+        assert lib.mag_diff(sa.tab["keys"].data_ptr(), ctypes.byref(sa.kd),
+                            sb.tab["keys"].data_ptr(), ctypes.byref(sb.kd), k, ctypes.byref(ro1),
+                            dws.data_ptr(), dws.numel(), h1) == 0, lib.mag_last_error()
+        o2, ro2 = outputs(cap)
+        det = N.DetectOut()
+        det.rank = ro2
+        det.latency_a, det.latency_b, det.verdict = (o2["la"].data_ptr(), o2["lb"].data_ptr(),
+                                                     o2["v"].data_ptr())
+        opt = N.DetectOpts(0.05, 0.01)
+        assert lib.mag_detect(sa.tab["keys"].data_ptr(), ctypes.byref(sa.kd),
+                              sb.tab["keys"].data_ptr(), ctypes.byref(sb.kd), ctypes.byref(opt),
+                              ctypes.byref(det), dws.data_ptr(), dws.numel(), h1) == 0
+        sa.finish(h1)
+        sb.finish(h2)
+        assert int(sa.nk.item()) == sa.ks.n_keys and int(sb.nk.item()) == sb.ks.n_keys
+        # the same comparison with host counts
+        ta = {n: v[:sa.ks.n_keys] for n, v in sa.tab.items()}
+        tb = {n: v[:sb.ks.n_keys] for n, v in sb.tab.items()}
+        ref = mag.diff(ta, tb, k)
+        r = int(ro1.n_out)
+        assert r == len(ref["key"]) and ro1.n_join == ref["n_join"]
+        assert ro1.n_only_a == ref["n_only_a"] and ro1.n_only_b == ref["n_only_b"]
+        assert torch.equal(o1["key"][:r], ref["key"]) and torch.equal(o1["ratio"][:r], ref["ratio"])
+        dref = mag.detect(ta, tb, 0.05, 0.01)
+        assert det.n_flagged == dref["n_flagged"] and det.n_waste == dref["n_waste"]
+        nf = int(det.rank.n_out)
+        assert torch.equal(o2["key"][:nf], dref["key"])
+        assert torch.equal(o2["v"][:nf], dref["verdict"])
