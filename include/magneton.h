@@ -337,6 +337,64 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
              const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
              size_t workspace_bytes, hipStream_t stream);
 
+/* ------------------------------------------------ tensor matching (4.2) */
+#define MAG_SVD_MAX_RANK 5
+#define MAG_SVD_MAX_K 512 /* largest min(M, N) of an unfolding this library handles */
+
+/* A dense tensor: fp32, row-major (the last mode fastest), on the device. */
+typedef struct mag_tensor {
+    const float* data;
+    int32_t rank;  /* 1 .. MAG_SVD_MAX_RANK */
+    int32_t reserved;
+    int64_t dims[MAG_SVD_MAX_RANK]; /* each >= 1; the product below 2^31 */
+} mag_tensor;
+
+/*
+ * mag_invariant_count -- size of a tensor's multi-mode SVD invariant list
+ * (Section 4.2): the unfoldings T_(G) over the non-empty proper mode subsets G
+ * that contain mode 0 (T_(G^c) is the transpose of T_(G) and has the same
+ * singular values), 2^(rank-1) - 1 of them, and the total number of singular
+ * values, the sum of min(M_G, N_G).  Host only.  MAG_E_NULL, MAG_E_SIZE
+ * (a rank or size out of range, or an unfolding with min(M, N) above
+ * MAG_SVD_MAX_K).
+ */
+int mag_invariant_count(const mag_tensor* tensor, int32_t* n_unfoldings, int64_t* n_values);
+
+/*
+ * mag_invariants_workspace_size / mag_invariants -- the invariant lists of
+ * n_tensors tensors (host array of descriptors).  spectra (device fp64)
+ * receives the lists one after the other in tensor order; inside a list the
+ * unfoldings come in increasing order of the bit mask of G (bit i = mode i),
+ * each as its min(M, N) singular values in descending order.  The unfolding
+ * has the modes of G as rows and the others as columns, both in increasing
+ * mode order.  Singular values are the square roots of the eigenvalues of the
+ * fp64 Gram matrix of the unfolding's shorter side (fp32 data widened
+ * exactly; MFMA products), reduced to tridiagonal form and bisected; an
+ * eigenvalue is within about 1e-13 of the largest (relative), so a singular
+ * value far below the largest carries an absolute error near 3e-7 of it.
+ * Synchronizes `stream`.  Errors: MAG_E_NULL, MAG_E_SIZE, MAG_E_ALIGN,
+ * MAG_E_WORKSPACE, MAG_E_HIP.
+ */
+int mag_invariants_workspace_size(const mag_tensor* tensors, int32_t n_tensors, size_t* bytes);
+int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * mag_match_workspace_size / mag_match -- which tensors of set A are
+ * equivalent to which tensors of set B (Section 4.2: equivalent when their
+ * invariant sets match under a tolerance).  spectra_a / spectra_b are
+ * mag_invariants outputs for the same descriptors.  Tensors a and b match when
+ * their lists can be paired one to one so that paired spectra have the same
+ * length and differ by at most eps x (the larger of the two leading singular
+ * values) at every position.  match[i * nb + j] (device uint8) = 1 or 0.
+ * Synchronizes `stream`.  Errors: MAG_E_NULL, MAG_E_SIZE (also eps negative or
+ * NaN), MAG_E_WORKSPACE, MAG_E_HIP.
+ */
+int mag_match_workspace_size(int32_t na, int32_t nb, size_t* bytes);
+int mag_match(const mag_tensor* ta, int32_t na, const double* spectra_a, const mag_tensor* tb,
+              int32_t nb, const double* spectra_b, double eps, uint8_t* match, void* workspace,
+              size_t workspace_bytes, hipStream_t stream);
+
 /*
  * mag_detect_workspace_size -- device workspace bytes for mag_detect with
  * `rows` output rows.  Host only.

@@ -14,7 +14,8 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "detect", "Stream", "workspace_size",
+__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "detect", "invariants",
+           "match", "Stream", "workspace_size",
            "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
 
@@ -352,6 +353,76 @@ def detect(a: dict, b: dict, threshold: float = 0.10, tolerance: float = 0.01,
     res.update(n_flagged=int(out.n_flagged), n_waste=int(out.n_waste),
                n_tradeoff=int(out.n_tradeoff), n_join=int(out.rank.n_join))
     return res
+
+
+def _tensor_descs(tensors):
+    arr = (N.Tensor * max(1, len(tensors)))()
+    for i, x in enumerate(tensors):
+        if x.dim() < 1 or x.dim() > N.MAG_SVD_MAX_RANK:
+            raise MagnetonError(N.MAG_E_SIZE, f"tensor {i}: rank {x.dim()} out of range")
+        arr[i].data = _dev_ptr(x, torch.float32, f"tensor {i}")
+        arr[i].rank = x.dim()
+        for d, n in enumerate(x.shape):
+            arr[i].dims[d] = int(n)
+    return arr
+
+
+def invariant_layout(tensor) -> list:
+    """Lengths of a tensor's spectra, in the order invariants() writes them."""
+    r = tensor.dim()
+    out = []
+    for g in range(1, (1 << r) - 1, 2):
+        M = N_ = 1
+        for i, n in enumerate(tensor.shape):
+            if g >> i & 1:
+                M *= int(n)
+            else:
+                N_ *= int(n)
+        out.append(min(M, N_))
+    return out
+
+
+def invariants(tensors, workspace=None):
+    """Multi-mode SVD invariants (Section 4.2) of fp32 GPU tensors (rank 1-5):
+    one fp64 tensor holding each tensor's spectra back to back (unfoldings in
+    increasing bit-mask order of G, mode 0 always in G, values descending),
+    and per tensor the list of spectrum lengths."""
+    lib = _lib()
+    tensors = list(tensors)
+    descs = _tensor_descs(tensors)
+    n = len(tensors)
+    dev = tensors[0].device if n else torch.device("cuda")
+    total = 0
+    for i in range(n):
+        u, v = ctypes.c_int32(0), ctypes.c_int64(0)
+        _check(lib.mag_invariant_count(ctypes.byref(descs[i]), ctypes.byref(u), ctypes.byref(v)))
+        total += int(v.value)
+    b = ctypes.c_size_t(0)
+    _check(lib.mag_invariants_workspace_size(descs, n, ctypes.byref(b)))
+    if workspace is None or workspace.numel() < int(b.value):
+        workspace = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
+    spectra = torch.empty(max(total, 1), dtype=torch.float64, device=dev)
+    _check(lib.mag_invariants(descs, n, spectra.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                              _stream_handle(dev)))
+    return spectra[:total], [invariant_layout(x) for x in tensors]
+
+
+def match(tensors_a, spectra_a, tensors_b, spectra_b, eps: float = 1e-5):
+    """Which tensors of A are equivalent to which of B: a uint8 [len(A), len(B)]
+    GPU tensor, 1 where the invariant lists pair up within eps x the leading
+    singular value."""
+    lib = _lib()
+    ta, tb = list(tensors_a), list(tensors_b)
+    da, db = _tensor_descs(ta), _tensor_descs(tb)
+    dev = spectra_a.device
+    out = torch.zeros((len(ta), len(tb)), dtype=torch.uint8, device=dev)
+    b = ctypes.c_size_t(0)
+    _check(lib.mag_match_workspace_size(len(ta), len(tb), ctypes.byref(b)))
+    ws = torch.empty(max(int(b.value), 1), dtype=torch.uint8, device=dev)
+    _check(lib.mag_match(da, len(ta), _dev_ptr(spectra_a, torch.float64, "spectra_a"), db, len(tb),
+                         _dev_ptr(spectra_b, torch.float64, "spectra_b"), float(eps),
+                         out.data_ptr(), ws.data_ptr(), ws.numel(), _stream_handle(dev)))
+    return out
 
 
 def stream_workspace_size(max_samples: int, n_intervals: int, key_capacity: int = 0,

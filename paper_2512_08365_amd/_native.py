@@ -39,6 +39,8 @@ EXPORTED = (
     "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_finish",
     "mag_counter_workspace_size", "mag_attribute_counter",
     "mag_diff_workspace_size", "mag_diff", "mag_detect_workspace_size", "mag_detect",
+    "mag_invariant_count", "mag_invariants_workspace_size", "mag_invariants",
+    "mag_match_workspace_size", "mag_match",
     "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
     "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
     "mag_strerror", "mag_last_error", "mag_version",
@@ -69,6 +71,15 @@ class RankOut(ctypes.Structure):
     _fields_ = [("key", c_vp), ("ratio", c_vp), ("energy_a", c_vp), ("energy_b", c_vp),
                 ("count_a", c_vp), ("count_b", c_vp), ("capacity", c_i64), ("n_out", c_i64),
                 ("n_only_a", c_i64), ("n_only_b", c_i64), ("n_join", c_i64)]
+
+
+MAG_SVD_MAX_RANK = 5
+MAG_SVD_MAX_K = 512
+
+
+class Tensor(ctypes.Structure):
+    _fields_ = [("data", c_vp), ("rank", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("dims", c_i64 * MAG_SVD_MAX_RANK)]
 
 
 class DetectOpts(ctypes.Structure):
@@ -118,6 +129,18 @@ def load(path: str = LIB_PATH):
     lib.mag_detect.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), P(DetectOpts), P(DetectOut),
                                c_vp, ctypes.c_size_t, c_vp]
     lib.mag_detect.restype = ctypes.c_int
+    i32 = ctypes.c_int32
+    lib.mag_invariant_count.argtypes = [P(Tensor), P(i32), P(c_i64)]
+    lib.mag_invariant_count.restype = ctypes.c_int
+    lib.mag_invariants_workspace_size.argtypes = [P(Tensor), i32, P(ctypes.c_size_t)]
+    lib.mag_invariants_workspace_size.restype = ctypes.c_int
+    lib.mag_invariants.argtypes = [P(Tensor), i32, c_vp, c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_invariants.restype = ctypes.c_int
+    lib.mag_match_workspace_size.argtypes = [i32, i32, P(ctypes.c_size_t)]
+    lib.mag_match_workspace_size.restype = ctypes.c_int
+    lib.mag_match.argtypes = [P(Tensor), i32, c_vp, P(Tensor), i32, c_vp, ctypes.c_double, c_vp,
+                              c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_match.restype = ctypes.c_int
     lib.mag_stream_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(AttrOpts), P(ctypes.c_size_t)]
     lib.mag_stream_workspace_size.restype = ctypes.c_int
     lib.mag_stream_begin.argtypes = [P(c_vp), c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),

@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <new>
+#include <vector>
 
 #include "mag_internal.hpp"
 
@@ -1278,6 +1279,240 @@ int mag_detect(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_
     out->n_waste = st.n_waste;
     out->n_tradeoff = (int64_t)st.n_flag - (int64_t)st.n_waste;
     out->rank.n_out = std::min<int64_t>(out->rank.n_out, out->n_flagged);
+    return MAG_OK;
+}
+
+}  // extern "C"
+
+// ------------------------------------------------------ tensor matching (4.2)
+
+namespace {
+
+int check_tensor(const mag_tensor* t)
+{
+    if (!t) return fail(MAG_E_NULL, "tensor descriptor is NULL");
+    if (t->rank < 1 || t->rank > MAG_SVD_MAX_RANK) return fail(MAG_E_SIZE, "tensor rank out of range");
+    int64_t total = 1;
+    for (int i = 0; i < t->rank; ++i) {
+        if (t->dims[i] < 1) return fail(MAG_E_SIZE, "tensor dimension < 1");
+        total *= t->dims[i];
+        if (total >= ((int64_t)1 << 31)) return fail(MAG_E_SIZE, "tensor has 2^31 elements or more");
+    }
+    return MAG_OK;
+}
+
+// the unfolding of mask g as a Gram task (K side = the shorter side)
+void unfolding_task(const mag_tensor* t, int g, mag::SvdTask& task)
+{
+    const int r = t->rank;
+    int64_t str[MAG_SVD_MAX_RANK];
+    str[r - 1] = 1;
+    for (int i = r - 2; i >= 0; --i) str[i] = str[i + 1] * t->dims[i + 1];
+    int64_t M = 1, N = 1;
+    for (int i = 0; i < r; ++i) ((g >> i) & 1 ? M : N) *= t->dims[i];
+    const bool rows_k = M <= N;
+    task = mag::SvdTask{};
+    task.data = t->data;
+    task.K = rows_k ? M : N;
+    task.L = rows_k ? N : M;
+    for (int i = 0; i < r; ++i) {
+        const bool in_g = (g >> i) & 1;
+        if (in_g == rows_k) {
+            task.kdim[task.nk] = t->dims[i];
+            task.kstr[task.nk++] = str[i];
+        } else {
+            task.ldim[task.nl] = t->dims[i];
+            task.lstr[task.nl++] = str[i];
+        }
+    }
+    task.nt = (int32_t)((task.K + 15) / 16);
+    task.nchunk = (int32_t)((task.L + mag::GRAM_CHUNK - 1) / mag::GRAM_CHUNK);
+}
+
+int count_invariants(const mag_tensor* t, int32_t* n_unf, int64_t* n_values)
+{
+    int rc = check_tensor(t);
+    if (rc) return rc;
+    int32_t u = 0;
+    int64_t v = 0;
+    for (int g = 1; g < (1 << t->rank) - 1; g += 2) {  // masks containing mode 0
+        mag::SvdTask task;
+        unfolding_task(t, g, task);
+        if (task.K > MAG_SVD_MAX_K) {
+            snprintf(g_last_error, sizeof(g_last_error),
+                     "an unfolding has min(M, N) = %lld > %d", (long long)task.K, MAG_SVD_MAX_K);
+            return MAG_E_SIZE;
+        }
+        ++u;
+        v += task.K;
+    }
+    *n_unf = u;
+    *n_values = v;
+    return MAG_OK;
+}
+
+struct InvPlan {
+    std::vector<mag::SvdTask> tasks;
+    int64_t gram_len = 0, n_items = 0;
+};
+
+int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
+{
+    if (n < 0) return fail(MAG_E_SIZE, "n_tensors < 0");
+    if (n > 0 && !ts) return fail(MAG_E_NULL, "tensors is NULL");
+    pl = InvPlan{};
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t u;
+        int64_t v;
+        int rc = count_invariants(&ts[i], &u, &v);
+        if (rc) return rc;
+        for (int g = 1; g < (1 << ts[i].rank) - 1; g += 2) {
+            mag::SvdTask task;
+            unfolding_task(&ts[i], g, task);
+            task.item0 = pl.n_items;
+            pl.n_items += (int64_t)task.nt * (task.nt + 1) / 2 * task.nchunk;
+            pl.gram_len += task.K * task.K;
+            pl.tasks.push_back(task);
+        }
+    }
+    return MAG_OK;
+}
+
+size_t carve_invariants(const InvPlan& pl, void* ws, mag::SvdTask** tasks, double** gram)
+{
+    Carver c;
+    c.base = static_cast<char*>(ws);
+    *tasks = c.take<mag::SvdTask>(std::max<size_t>(pl.tasks.size(), 1));
+    *gram = c.take<double>((size_t)std::max<int64_t>(pl.gram_len, 1));
+    return c.off;
+}
+
+// spectra descriptors of a tensor set: offsets in the order mag_invariants writes
+int spec_descs(const mag_tensor* ts, int32_t n, std::vector<mag::SpecDesc>& out)
+{
+    out.assign((size_t)std::max(n, 0), mag::SpecDesc{});
+    int64_t off = 0;
+    for (int32_t i = 0; i < n; ++i) {
+        int32_t u;
+        int64_t v;
+        int rc = count_invariants(&ts[i], &u, &v);
+        if (rc) return rc;
+        mag::SpecDesc& d = out[i];
+        for (int g = 1; g < (1 << ts[i].rank) - 1; g += 2) {
+            mag::SvdTask task;
+            unfolding_task(&ts[i], g, task);
+            d.off[d.n] = off;
+            d.len[d.n++] = task.K;
+            off += task.K;
+        }
+    }
+    return MAG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mag_invariant_count(const mag_tensor* tensor, int32_t* n_unfoldings, int64_t* n_values)
+{
+    g_last_error[0] = 0;
+    if (!n_unfoldings || !n_values) return fail(MAG_E_NULL, "output pointer is NULL");
+    return count_invariants(tensor, n_unfoldings, n_values);
+}
+
+int mag_invariants_workspace_size(const mag_tensor* tensors, int32_t n_tensors, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    InvPlan pl;
+    int rc = plan_invariants(tensors, n_tensors, pl);
+    if (rc) return rc;
+    mag::SvdTask* t;
+    double* g;
+    *bytes = carve_invariants(pl, nullptr, &t, &g);
+    return MAG_OK;
+}
+
+int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    InvPlan pl;
+    int rc = plan_invariants(tensors, n_tensors, pl);
+    if (rc) return rc;
+    if (pl.tasks.empty()) return MAG_OK;
+    for (int32_t i = 0; i < n_tensors; ++i) {
+        if (!tensors[i].data) return fail(MAG_E_NULL, "tensor data is NULL");
+        if (!aligned(tensors[i].data, 4)) return fail(MAG_E_ALIGN, "tensor data not 4-byte aligned");
+    }
+    if (!spectra) return fail(MAG_E_NULL, "spectra is NULL");
+    if (!aligned(spectra, 8)) return fail(MAG_E_ALIGN, "spectra not 8-byte aligned");
+    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    mag::SvdTask* dtasks;
+    double* gram;
+    const size_t need = carve_invariants(pl, nullptr, &dtasks, &gram);
+    if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
+    carve_invariants(pl, workspace, &dtasks, &gram);
+    int64_t go = 0, so = 0;
+    for (auto& t : pl.tasks) {
+        t.gram = gram + go;
+        t.out = spectra + so;
+        go += t.K * t.K;
+        so += t.K;
+    }
+    hipError_t e;
+    if ((e = hipMemcpyAsync(dtasks, pl.tasks.data(), sizeof(mag::SvdTask) * pl.tasks.size(),
+                            hipMemcpyHostToDevice, stream)) != hipSuccess)
+        return hip_fail(e, "task copy");
+    if ((e = mag::launch_svd(dtasks, (int)pl.tasks.size(), pl.n_items, gram, pl.gram_len, stream)) !=
+        hipSuccess)
+        return hip_fail(e, "invariant kernels");
+    // (the task table on the host stays alive until the copy is done)
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    return MAG_OK;
+}
+
+int mag_match_workspace_size(int32_t na, int32_t nb, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    if (na < 0 || nb < 0) return fail(MAG_E_SIZE, "negative count");
+    Carver c;
+    c.take<mag::SpecDesc>((size_t)std::max(na + nb, 1));
+    *bytes = c.off;
+    return MAG_OK;
+}
+
+int mag_match(const mag_tensor* ta, int32_t na, const double* spectra_a, const mag_tensor* tb,
+              int32_t nb, const double* spectra_b, double eps, uint8_t* match, void* workspace,
+              size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (na < 0 || nb < 0) return fail(MAG_E_SIZE, "negative count");
+    if (!(eps >= 0.0)) return fail(MAG_E_SIZE, "eps must be >= 0");
+    if ((int64_t)na * nb == 0) return MAG_OK;
+    if (!ta || !tb || !spectra_a || !spectra_b || !match || !workspace)
+        return fail(MAG_E_NULL, "NULL argument");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if ((int64_t)na * nb > 0x7fffffffLL) return fail(MAG_E_SIZE, "too many pairs");
+    std::vector<mag::SpecDesc> da, db;
+    int rc = spec_descs(ta, na, da);
+    if (rc == MAG_OK) rc = spec_descs(tb, nb, db);
+    if (rc) return rc;
+    size_t need = 0;
+    mag_match_workspace_size(na, nb, &need);
+    if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
+    auto* dd = static_cast<mag::SpecDesc*>(workspace);
+    da.insert(da.end(), db.begin(), db.end());
+    hipError_t e;
+    if ((e = hipMemcpyAsync(dd, da.data(), sizeof(mag::SpecDesc) * da.size(), hipMemcpyHostToDevice,
+                            stream)) != hipSuccess)
+        return hip_fail(e, "descriptor copy");
+    if ((e = mag::launch_svd_match(dd, na, spectra_a, dd + na, nb, spectra_b, eps, match,
+                                   stream)) != hipSuccess)
+        return hip_fail(e, "match kernel");
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
     return MAG_OK;
 }
 

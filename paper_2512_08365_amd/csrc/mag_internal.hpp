@@ -230,6 +230,41 @@ hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_st
                        hipEvent_t ev_stop = nullptr);
 // intervals spanning tiles, endpoints outside the trace, clearing of the group-by state
 hipError_t launch_fix(const FixParams& p, hipStream_t stream);
+// multi-mode SVD invariants (Section 4.2): one task per (tensor, unfolding)
+constexpr int SVD_MAX_RANK = 5;
+constexpr int SVD_MAX_K = 512;        // largest Gram side (min(M, N) of an unfolding)
+constexpr int SVD_MAX_UNF = 15;       // unfoldings of a rank-5 tensor, complements folded
+constexpr int64_t GRAM_CHUNK = 2048;  // unfolding columns per Gram work item
+
+struct SvdTask {
+    const float* data;
+    int64_t K, L;  // the Gram matrix X X^T is K x K, X the unfolding's shorter-side view
+    int32_t nk, nl;  // modes on the K side and on the L side
+    int64_t kdim[SVD_MAX_RANK], kstr[SVD_MAX_RANK];  // sizes and element strides, last fastest
+    int64_t ldim[SVD_MAX_RANK], lstr[SVD_MAX_RANK];
+    double* gram;    // [K][K]
+    double* out;     // [K] singular values, descending
+    int64_t item0;   // first Gram work item of this task
+    int32_t nt;      // 16-row tiles: ceil(K / 16)
+    int32_t nchunk;  // column chunks: ceil(L / GRAM_CHUNK)
+};
+
+// a tensor's invariant list inside a spectra array
+struct SpecDesc {
+    int32_t n;  // unfoldings
+    int32_t pad;
+    int64_t off[SVD_MAX_UNF];
+    int64_t len[SVD_MAX_UNF];
+};
+
+// Gram matrices (zeroed, then accumulated), then the spectra
+hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double* gram,
+                      int64_t gram_len, hipStream_t stream);
+// match[i * nb + j] = 1 when tensor i of A and tensor j of B have matching invariants
+hipError_t launch_svd_match(const SpecDesc* da, int na, const double* sa, const SpecDesc* db,
+                            int nb, const double* sb, double eps, uint8_t* match,
+                            hipStream_t stream);
+
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
 // *dst = v, in stream order (a kernel, so the write can sit in a captured graph)
 hipError_t launch_set_i64(int64_t* dst, int64_t v, hipStream_t stream);

@@ -198,3 +198,33 @@ def test_product_does_not_import_the_oracle():
         if os.path.isfile(path) and path.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
             text = open(path).read()
             assert "oracle" not in text.lower().replace("oracle-free", ""), path
+
+
+def test_invariants_host_side_errors_without_gpu():
+    from paper_2512_08365_amd import _native as N
+    lib = N.load()
+    u, v = ctypes.c_int32(0), ctypes.c_int64(0)
+    t = N.Tensor(ctypes.c_void_p(256), 3, 0, (ctypes.c_int64 * 5)(4, 6, 5, 0, 0))
+    assert lib.mag_invariant_count(ctypes.byref(t), ctypes.byref(u), ctypes.byref(v)) == 0
+    # masks {0}, {0,1}, {0,2}: min(4, 30) + min(24, 5) + min(20, 6)
+    assert u.value == 3 and v.value == 4 + 5 + 6
+    t.rank = 6
+    assert lib.mag_invariant_count(ctypes.byref(t), ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_SIZE
+    t.rank, t.dims[1] = 3, 0
+    assert lib.mag_invariant_count(ctypes.byref(t), ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_SIZE
+    big = N.Tensor(ctypes.c_void_p(256), 2, 0, (ctypes.c_int64 * 5)(600, 700, 0, 0, 0))
+    assert lib.mag_invariant_count(ctypes.byref(big), ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_SIZE
+    assert b"512" in lib.mag_last_error()
+    assert lib.mag_invariant_count(None, ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_NULL
+    b = ctypes.c_size_t(0)
+    ok = N.Tensor(ctypes.c_void_p(256), 2, 0, (ctypes.c_int64 * 5)(30, 40, 0, 0, 0))
+    assert lib.mag_invariants_workspace_size(ctypes.byref(ok), 1, ctypes.byref(b)) == 0
+    assert b.value >= 30 * 30 * 8
+    assert lib.mag_invariants(ctypes.byref(ok), 1, None, ctypes.c_void_p(256), b.value,
+                              None) == N.MAG_E_NULL
+    assert lib.mag_invariants(ctypes.byref(ok), 1, ctypes.c_void_p(256), ctypes.c_void_p(256),
+                              16, None) == N.MAG_E_WORKSPACE
+    assert lib.mag_match(None, 1, None, None, 1, None, float("nan"), None, None, 0,
+                         None) == N.MAG_E_SIZE
+    assert lib.mag_match(None, 1, None, None, 1, None, 1e-5, None, None, 0, None) == N.MAG_E_NULL
+    assert lib.mag_match_workspace_size(-1, 2, ctypes.byref(b)) == N.MAG_E_SIZE

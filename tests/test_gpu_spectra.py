@@ -1,0 +1,131 @@
+"""Multi-mode SVD invariants and tensor matching (Section 4.2) on the GPU,
+through the C ABI, against the oracle.
+
+Spectra: every eigenvalue sigma^2 within 1e-9 of the unfolding's largest
+(the fp64 Gram sums at most a few million fp32 products, each exact, and the
+tridiagonal reduction and bisection are backward stable, so the error is far
+below that).  Matching: the GPU's decisions equal the oracle's on the same
+spectra, and planted permutations match while perturbed tensors do not.
+"""
+import itertools
+
+import numpy as np
+import pytest
+
+from gpu_util import log
+from oracle import spectra as S
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    import paper_2512_08365_amd as mag
+    mag.version()
+    yield
+
+
+def _gpu_lists(arrays):
+    import torch
+    import paper_2512_08365_amd as mag
+    ts = [torch.from_numpy(np.ascontiguousarray(a, np.float32)).cuda() for a in arrays]
+    spec, lay = mag.invariants(ts)
+    flat = spec.cpu().numpy()
+    out, o = [], 0
+    for lens in lay:
+        lst = []
+        for n in lens:
+            lst.append(flat[o:o + n])
+            o += n
+        out.append(lst)
+    assert o == flat.size
+    return ts, spec, out
+
+
+def _assert_spectra(got, want, label):
+    assert len(got) == len(want), label
+    for g, w in zip(got, want):
+        assert g.shape == w.shape, label
+        top = max(float(w[0]), 1e-300) ** 2
+        err = np.abs(g.astype(np.float64) ** 2 - w ** 2).max()
+        assert err <= 1e-9 * top, (label, err / top)
+        assert np.all(np.diff(g) <= 0), label  # descending
+
+
+SHAPES = [(5,), (1, 1), (3, 7), (16, 16), (17, 33), (2, 3, 4), (4, 1, 9), (8, 64, 128),
+          (3, 5, 2, 7), (2, 3, 2, 3, 2), (1, 4, 1, 5, 1), (100, 600), (511, 40), (512, 512),
+          (2, 256, 4096), (20, 25, 700)]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_spectra_match_the_oracle(shape):
+    rng = np.random.default_rng(sum(shape))
+    T = rng.standard_normal(shape).astype(np.float32)
+    if len(shape) >= 2:
+        T[..., 0] *= 50.0  # a spread of singular values
+    log(f"[spectra] shape {shape}")
+    _, _, (got,) = _gpu_lists([T])
+    _assert_spectra(got, S.invariants(T), f"{shape}")
+
+
+def test_closed_forms_on_the_gpu():
+    rng = np.random.default_rng(4)
+    vs = [rng.standard_normal(n).astype(np.float32) for n in (6, 9, 5)]
+    R1 = np.einsum("i,j,k->ijk", *vs)
+    H = np.array([[1, 1, 1, 1], [1, -1, 1, -1], [1, 1, -1, -1], [1, -1, -1, 1]], np.float32) / 2
+    _, _, (r1, h) = _gpu_lists([R1, H.reshape(2, 2, 2, 2)])
+    norm = float(np.prod([np.linalg.norm(v.astype(np.float64)) for v in vs]))
+    for s in r1:
+        assert abs(s[0] - norm) <= 1e-6 * norm and np.all(s[1:] <= 1e-6 * norm)
+    assert np.allclose(h[S.canonical_masks(4).index(0b0011)], 1.0, atol=1e-7)
+
+
+def test_matching_planted_permutations():
+    rng = np.random.default_rng(11)
+    A = [rng.standard_normal(s).astype(np.float32) for s in
+         [(4, 6, 5), (3, 3, 8), (2, 5, 2, 3), (30, 20), (6, 8, 10)]]
+    B = []
+    truth = np.zeros((len(A), 0), bool)
+    cols = []
+    for i, a in enumerate(A):
+        perm = tuple(rng.permutation(a.ndim))
+        B.append(np.ascontiguousarray(np.transpose(a, perm)))  # a layout change: matches
+        cols.append(i)
+        bad = a.copy()
+        bad.flat[7] += 1e-2 * np.abs(a).max()  # a different tensor: does not
+        B.append(bad)
+        cols.append(-1)
+    B.append(A[0].reshape(6, 4, 5).copy())  # regrouped modes: not a layout change
+    cols.append(-1)
+    import paper_2512_08365_amd as mag
+    ta, sa, la = _gpu_lists(A)
+    tb, sb, lb = _gpu_lists(B)
+    got = mag.match(ta, sa, tb, sb, 1e-5).cpu().numpy()
+    want = np.array([[S.match(x, y, 1e-5) for y in lb] for x in la], np.uint8)
+    assert np.array_equal(got, want)  # the same decisions on the same spectra
+    planted = np.array([[c == i for c in cols] for i in range(len(A))], np.uint8)
+    assert np.array_equal(got, planted), (got, planted)
+
+
+@pytest.mark.parametrize("shape", [(3, 4, 5, 2)])
+def test_every_permutation_matches_on_the_gpu(shape):
+    import paper_2512_08365_amd as mag
+    rng = np.random.default_rng(5)
+    T = rng.standard_normal(shape).astype(np.float32)
+    perms = [np.ascontiguousarray(np.transpose(T, p)) for p in itertools.permutations(range(4))]
+    ta, sa, _ = _gpu_lists([T])
+    tb, sb, _ = _gpu_lists(perms)
+    assert mag.match(ta, sa, tb, sb, 1e-5).cpu().numpy().all()
+
+
+def test_unsupported_shapes_are_rejected():
+    import torch
+    import paper_2512_08365_amd as mag
+    with pytest.raises(mag.MagnetonError) as e:
+        mag.invariants([torch.zeros((600, 700), device="cuda")])  # min(M, N) = 600 > 512
+    assert e.value.code == -2
+    with pytest.raises(mag.MagnetonError):
+        mag.invariants([torch.zeros((2,) * 6, device="cuda")])  # rank 6
