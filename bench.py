@@ -245,6 +245,58 @@ def counter_session(args, torch, mag):
     print(json.dumps(res), flush=True)
 
 
+def invariants_bench(args, torch, mag):
+    """Multi-mode SVD invariants of a batch shaped like per-layer attention
+    K/V tensors (64 x fp32 [32 heads, 128 tokens, 128 head dims]) and the
+    all-pairs matching of the batch against a permuted copy; one JSON line."""
+    import numpy as np
+    rng = np.random.default_rng(args.seed)
+    shape, count = (32, 128, 128), 64
+    host = [rng.standard_normal(shape).astype(np.float32) for _ in range(count)]
+    A = [torch.from_numpy(h).cuda() for h in host]
+    B = [x.permute(1, 0, 2).contiguous() for x in A]  # the other system's layout (NHD)
+    lay = mag.invariant_layout(A[0])
+    # algorithmic work of the Gram products: K (K + 1) L flops per unfolding
+    flops = 0
+    for g in range(1, 7, 2):
+        M = int(np.prod([shape[i] for i in range(3) if g >> i & 1]))
+        N = int(np.prod(shape)) // M
+        K, L = min(M, N), max(M, N)
+        flops += K * (K + 1) * L
+    flops *= count
+    ws = torch.empty(1, dtype=torch.uint8, device="cuda")
+    for _ in range(max(args.warmup, 1)):
+        sa, _ = mag.invariants(A)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        sa, _ = mag.invariants(A)
+    torch.cuda.synchronize()
+    sec = (time.perf_counter() - t0) / args.steps
+    sb, _ = mag.invariants(B)
+    t1 = time.perf_counter()
+    m = mag.match(A, sa, B, sb, 1e-5)
+    torch.cuda.synchronize()
+    msec = time.perf_counter() - t1
+    matched = int(m.sum().item())
+    res = {"mode": "tensor invariants", "tensors": count, "shape": list(shape),
+           "spectrum_lengths": lay, "ms_per_batch": sec * 1e3, "tensors_per_s": count / sec,
+           "gram_tflops_algorithmic_over_call": flops / sec / 1e12,
+           "match_ms_64x64": msec * 1e3, "matched_pairs": matched}
+    if not args.no_cpu_baseline:
+        from threadpoolctl import threadpool_limits
+        from oracle import spectra as S
+        with threadpool_limits(1):
+            t0 = time.perf_counter()
+            for h in host[:8]:
+                S.invariants(h)
+            dt = (time.perf_counter() - t0) / 8
+        res["cpu_baseline"] = {"value": 1.0 / dt, "unit": "tensors/s", "cores": 1,
+                               "kind": "oracle", "sample": "8 of the 64 tensors, numpy SVD",
+                               "seconds_per_tensor": round(dt, 4)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -252,6 +304,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--invariants", action="store_true",
+                    help="measure the tensor invariants (Section 4.2) instead")
     ap.add_argument("--counter-session", action="store_true",
                     help="measure the counter (software replay) attribution instead")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -286,6 +340,9 @@ def main():
         return
     if args.counter_session:
         counter_session(args, torch, mag)
+        return
+    if args.invariants:
+        invariants_bench(args, torch, mag)
         return
     lib = N.load()
     log(f"[bench] {mag.version()} on {torch.cuda.get_device_name(0)}")

@@ -83,13 +83,23 @@ __global__ __launch_bounds__(GW * GRAM_WAVES) void k_gram(const SvdTask* tasks, 
     const int64_t oa = va ? mode_offset((uint32_t)ra, t.nk, t.kdim, t.kstr) : 0;
     const int64_t ob = vb ? mode_offset((uint32_t)rb, t.nk, t.kdim, t.kstr) : 0;
     const int64_t b0 = chunk * GRAM_CHUNK, b1 = min(b0 + GRAM_CHUNK, t.L);
+    // the chunk's column offsets, computed once by the wave's lanes together
+    __shared__ int32_t loff_s[GRAM_WAVES][GRAM_CHUNK];
+    int32_t* loff = loff_s[threadIdx.x / GW];
+    for (int64_t q = lane; q < b1 - b0; q += GW)
+        loff[q] = (int32_t)mode_offset((uint32_t)(b0 + q), t.nl, t.ldim, t.lstr);
+    // the lanes read each other's entries: a wave's LDS operations complete in
+    // order; the fences keep the compiler from moving the reads above the writes
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     d4 acc = {0.0, 0.0, 0.0, 0.0};
     // A operand: lane holds X[ti*16 + lane%16][b + lane/16]; B operand: lane
     // holds X[tj*16 + lane%16][b + lane/16]; the product is the Gram tile
     for (int64_t b = b0; b < b1; b += 4) {
         const int64_t bb = b + kq;
         const bool vl = bb < b1;
-        const int64_t ol = vl ? mode_offset((uint32_t)bb, t.nl, t.ldim, t.lstr) : 0;
+        const int64_t ol = vl ? (int64_t)loff[bb - b0] : 0;
         const double xa = (va && vl) ? (double)t.data[oa + ol] : 0.0;
         const double xb = (vb && vl) ? (double)t.data[ob + ol] : 0.0;
         acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, xb, acc, 0, 0, 0);
@@ -131,14 +141,13 @@ __device__ int sturm_count(const double* d, const double* e2, int n, double x, d
     return c;
 }
 
-__global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
+constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in LDS
+
+// Householder reduction of the symmetric n x n matrix A (row stride n) to
+// tridiagonal form: d[k] the diagonal, e2[k] the squared off-diagonal
+__device__ void tridiagonalize(double* A, int n, double* v, double* w, double* d, double* e2,
+                               double* red)
 {
-    __shared__ double v[SVD_MAX_K], w[SVD_MAX_K];
-    __shared__ double d[SVD_MAX_K], e2[SVD_MAX_K];
-    __shared__ double red[EIG_THREADS / 64];
-    const SvdTask& t = tasks[blockIdx.x];
-    const int n = (int)t.K;
-    double* A = t.gram;
     const int tid = threadIdx.x;
     // Householder reduction: step k annihilates column k below the subdiagonal
     for (int k = 0; k + 2 < n; ++k) {
@@ -202,6 +211,24 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
         d[n - 1] = A[(size_t)(n - 1) * n + (n - 1)];
     }
     __syncthreads();
+}
+
+__global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
+{
+    __shared__ double v[SVD_MAX_K], w[SVD_MAX_K];
+    __shared__ double d[SVD_MAX_K], e2[SVD_MAX_K];
+    __shared__ double red[EIG_THREADS / 64];
+    __shared__ double As[EIG_LDS_K * EIG_LDS_K];
+    const SvdTask& t = tasks[blockIdx.x];
+    const int n = (int)t.K;
+    const int tid = threadIdx.x;
+    if (n <= EIG_LDS_K) {
+        for (int q = tid; q < n * n; q += EIG_THREADS) As[q] = t.gram[q];
+        __syncthreads();
+        tridiagonalize(As, n, v, w, d, e2, red);
+    } else {
+        tridiagonalize(t.gram, n, v, w, d, e2, red);
+    }
     // Gershgorin interval and the smallest pivot allowed in a Sturm count
     double glo = INFINITY, ghi = -INFINITY, emax = 0.0;
     for (int i = 0; i < n; ++i) {
