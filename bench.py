@@ -297,6 +297,31 @@ def invariants_bench(args, torch, mag):
     print(json.dumps(res), flush=True)
 
 
+def subgraphs_bench(args):
+    """Section 4.2's subgraph matching (host code) on two planted graphs of
+    20,000 blocks (about 100,000 operators each); the oracle on 300 blocks."""
+    import paper_2512_08365_amd as mag
+    import synth
+    from oracle import graph_match as G
+    c = synth.graph_pair(args.seed, blocks=20000, width=4, decoys=2000, crossing=200)
+    nodes = c["n1"] + c["n2"]
+    t0 = time.perf_counter()
+    pairs = mag.match_subgraphs(c["n1"], c["edges1"], c["n2"], c["edges2"], c["eq"])
+    dt = time.perf_counter() - t0
+    res = {"mode": "subgraph matching (host)", "nodes": nodes,
+           "edges": len(c["edges1"]) + len(c["edges2"]), "pairs": len(pairs),
+           "seconds": dt, "nodes_per_s": nodes / dt}
+    if not args.no_cpu_baseline:
+        s = synth.graph_pair(args.seed, blocks=300, width=4, decoys=30, crossing=3)
+        t0 = time.perf_counter()
+        G.match(s["n1"], s["edges1"], s["n2"], s["edges2"], s["eq"])
+        ot = time.perf_counter() - t0
+        res["cpu_baseline"] = {"value": (s["n1"] + s["n2"]) / ot, "unit": "nodes/s", "cores": 1,
+                               "kind": "oracle", "sample": "the same generator at 300 blocks",
+                               "seconds": round(ot, 3)}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -304,6 +329,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--subgraphs", action="store_true",
+                    help="measure the host-side subgraph matching (Section 4.2) instead")
     ap.add_argument("--invariants", action="store_true",
                     help="measure the tensor invariants (Section 4.2) instead")
     ap.add_argument("--counter-session", action="store_true",
@@ -319,6 +346,9 @@ def main():
         import synth
         sh = synth.shape(WORKLOAD)
         summarize_counters(*args.summarize_counters, tile_bytes=12 * sh["n"] + 40 * sh["m"])
+        return
+    if args.subgraphs:
+        subgraphs_bench(args)
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported by this build "

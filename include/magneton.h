@@ -54,6 +54,8 @@ extern "C" {
 #define MAG_E_KEYS (-12)      /* a key table passed to mag_diff is not strictly       */
                               /* ascending                                            */
 #define MAG_E_COUNTER (-13)   /* an energy-counter reading is not finite or decreases */
+#define MAG_E_GRAPH (-14)     /* a graph is not a DAG from node 0 to node n-1 through  */
+                              /* every node                                           */
 
 /* ----------------------------------------------------------------- flags */
 /* Split the power at each instant equally among the intervals active at that
@@ -394,6 +396,37 @@ int mag_match_workspace_size(int32_t na, int32_t nb, size_t* bytes);
 int mag_match(const mag_tensor* ta, int32_t na, const double* spectra_a, const mag_tensor* tb,
               int32_t nb, const double* spectra_b, double eps, uint8_t* match, void* workspace,
               size_t workspace_bytes, hipStream_t stream);
+
+/* ------------------------------------------- subgraph matching (4.2) */
+/* A computational graph on the host: operators 0..n_nodes-1, edge e (a tensor)
+   from src[e] to dst[e]; node 0 is the input, node n_nodes-1 the output. */
+typedef struct mag_graph {
+    int32_t n_nodes;
+    int32_t n_edges;
+    const int32_t* src;
+    const int32_t* dst;
+} mag_graph;
+
+/*
+ * mag_match_subgraphs -- Section 4.2's topology-aware matching of two
+ * computational graphs (host only; no device work).  eq[2 p], eq[2 p + 1]:
+ * node of g1 and node of g2 whose output tensors are equivalent (as found by
+ * mag_match).  Readings of the printed algorithm: the dominator path of a
+ * graph is the chain of its output's dominators, input first; the cut points
+ * are the eq pairs on both dominator paths plus the inputs and the outputs,
+ * reduced to the longest chain rising in both paths (ties: the chain whose
+ * sequence of path positions is lexicographically smallest); the region
+ * between consecutive cuts c and c' is every node c dominates minus those c'
+ * strictly dominates; region pairs are matched again recursively with eq
+ * restricted to them, and a pair without an interior cut is a finest match.
+ * out[4 q .. 4 q + 3] = entry and exit node of the q-th finest pair in g1,
+ * then in g2, in path order; *n_out = the number of pairs.
+ * Errors: MAG_E_NULL, MAG_E_SIZE (fewer than 2 nodes, a node index out of
+ * range), MAG_E_GRAPH (a cycle, or a node off every input-to-output path),
+ * MAG_E_CAPACITY (*n_out still reports the count).
+ */
+int mag_match_subgraphs(const mag_graph* g1, const mag_graph* g2, const int32_t* eq,
+                        int32_t n_eq, int32_t* out, int32_t capacity, int32_t* n_out);
 
 /*
  * mag_detect_workspace_size -- device workspace bytes for mag_detect with

@@ -15,7 +15,7 @@ import torch
 from . import _native as N
 
 __all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "detect", "invariants",
-           "match", "Stream", "workspace_size",
+           "match", "match_subgraphs", "Stream", "workspace_size",
            "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
 
@@ -423,6 +423,30 @@ def match(tensors_a, spectra_a, tensors_b, spectra_b, eps: float = 1e-5):
                          _dev_ptr(spectra_b, torch.float64, "spectra_b"), float(eps),
                          out.data_ptr(), ws.data_ptr(), ws.numel(), _stream_handle(dev)))
     return out
+
+
+def match_subgraphs(n1: int, edges1, n2: int, edges2, eq):
+    """Section 4.2's topology-aware matching of two computational graphs (host
+    code): edges as (src, dst) node pairs, node 0 the input and node n-1 the
+    output of each graph; eq: (node of graph 1, node of graph 2) pairs with
+    equivalent outputs.  Returns the finest matched pairs as ((entry1, exit1),
+    (entry2, exit2)), in path order."""
+    import numpy as np
+    lib = _lib()
+    e1 = np.ascontiguousarray(np.asarray(edges1, np.int32).reshape(-1, 2))
+    e2 = np.ascontiguousarray(np.asarray(edges2, np.int32).reshape(-1, 2))
+    q = np.ascontiguousarray(np.asarray(eq, np.int32).reshape(-1, 2))
+    s1, d1 = np.ascontiguousarray(e1[:, 0]), np.ascontiguousarray(e1[:, 1])
+    s2, d2 = np.ascontiguousarray(e2[:, 0]), np.ascontiguousarray(e2[:, 1])
+    g1 = N.GraphDesc(int(n1), len(e1), s1.ctypes.data, d1.ctypes.data)
+    g2 = N.GraphDesc(int(n2), len(e2), s2.ctypes.data, d2.ctypes.data)
+    cap = max(n1, n2)
+    out = np.zeros(4 * cap, np.int32)
+    n_out = ctypes.c_int32(0)
+    _check(lib.mag_match_subgraphs(ctypes.byref(g1), ctypes.byref(g2), q.ctypes.data, len(q),
+                                   out.ctypes.data, cap, ctypes.byref(n_out)))
+    r = out[:4 * n_out.value].reshape(-1, 4)
+    return [((int(a), int(b)), (int(c), int(d))) for a, b, c, d in r]
 
 
 def stream_workspace_size(max_samples: int, n_intervals: int, key_capacity: int = 0,

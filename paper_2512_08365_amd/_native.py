@@ -24,6 +24,7 @@ MAG_E_HIP = -10
 MAG_E_ALIGN = -11
 MAG_E_KEYS = -12
 MAG_E_COUNTER = -13
+MAG_E_GRAPH = -14
 
 MAG_EQUAL_SPLIT = 0x1
 MAG_SKIP_VALIDATE = 0x2
@@ -40,7 +41,7 @@ EXPORTED = (
     "mag_counter_workspace_size", "mag_attribute_counter",
     "mag_diff_workspace_size", "mag_diff", "mag_detect_workspace_size", "mag_detect",
     "mag_invariant_count", "mag_invariants_workspace_size", "mag_invariants",
-    "mag_match_workspace_size", "mag_match",
+    "mag_match_workspace_size", "mag_match", "mag_match_subgraphs",
     "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
     "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
     "mag_strerror", "mag_last_error", "mag_version",
@@ -80,6 +81,11 @@ MAG_SVD_MAX_K = 512
 class Tensor(ctypes.Structure):
     _fields_ = [("data", c_vp), ("rank", ctypes.c_int32), ("reserved", ctypes.c_int32),
                 ("dims", c_i64 * MAG_SVD_MAX_RANK)]
+
+
+class GraphDesc(ctypes.Structure):
+    _fields_ = [("n_nodes", ctypes.c_int32), ("n_edges", ctypes.c_int32), ("src", c_vp),
+                ("dst", c_vp)]
 
 
 class DetectOpts(ctypes.Structure):
@@ -141,6 +147,8 @@ def load(path: str = LIB_PATH):
     lib.mag_match.argtypes = [P(Tensor), i32, c_vp, P(Tensor), i32, c_vp, ctypes.c_double, c_vp,
                               c_vp, ctypes.c_size_t, c_vp]
     lib.mag_match.restype = ctypes.c_int
+    lib.mag_match_subgraphs.argtypes = [P(GraphDesc), P(GraphDesc), c_vp, i32, c_vp, i32, P(i32)]
+    lib.mag_match_subgraphs.restype = ctypes.c_int
     lib.mag_stream_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(AttrOpts), P(ctypes.c_size_t)]
     lib.mag_stream_workspace_size.restype = ctypes.c_int
     lib.mag_stream_begin.argtypes = [P(c_vp), c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),

@@ -1517,3 +1517,50 @@ int mag_match(const mag_tensor* ta, int32_t na, const double* spectra_a, const m
 }
 
 }  // extern "C"
+
+// ------------------------------------------------------ subgraph matching
+
+namespace {
+
+int check_graph(const mag_graph* g)
+{
+    if (!g) return fail(MAG_E_NULL, "graph is NULL");
+    if (g->n_nodes < 2) return fail(MAG_E_SIZE, "a graph needs at least 2 nodes");
+    if (g->n_edges < 0) return fail(MAG_E_SIZE, "n_edges < 0");
+    if (g->n_edges > 0 && (!g->src || !g->dst)) return fail(MAG_E_NULL, "edge arrays are NULL");
+    for (int32_t e = 0; e < g->n_edges; ++e)
+        if (g->src[e] < 0 || g->src[e] >= g->n_nodes || g->dst[e] < 0 || g->dst[e] >= g->n_nodes)
+            return fail(MAG_E_SIZE, "edge endpoint out of range");
+    return MAG_OK;
+}
+
+}  // namespace
+
+extern "C" int mag_match_subgraphs(const mag_graph* g1, const mag_graph* g2, const int32_t* eq,
+                                   int32_t n_eq, int32_t* out, int32_t capacity, int32_t* n_out)
+{
+    g_last_error[0] = 0;
+    int rc;
+    if ((rc = check_graph(g1)) != MAG_OK || (rc = check_graph(g2)) != MAG_OK) return rc;
+    if (!n_out) return fail(MAG_E_NULL, "n_out is NULL");
+    if (n_eq < 0 || capacity < 0) return fail(MAG_E_SIZE, "negative count");
+    if (n_eq > 0 && !eq) return fail(MAG_E_NULL, "eq is NULL");
+    for (int32_t p = 0; p < n_eq; ++p)
+        if (eq[2 * p] < 0 || eq[2 * p] >= g1->n_nodes || eq[2 * p + 1] < 0 ||
+            eq[2 * p + 1] >= g2->n_nodes)
+            return fail(MAG_E_SIZE, "eq node out of range");
+    std::vector<int32_t> pairs;
+    try {
+        rc = mag::match_subgraphs(*g1, *g2, eq, n_eq, pairs);
+    } catch (const std::bad_alloc&) {
+        return fail(MAG_E_SIZE, "out of host memory");
+    }
+    if (rc == MAG_E_GRAPH)
+        return fail(MAG_E_GRAPH, "a graph has a cycle or a node off every input-to-output path");
+    const int32_t np = (int32_t)(pairs.size() / 4);
+    *n_out = np;
+    if (np > capacity) return fail(MAG_E_CAPACITY, "more matched pairs than capacity");
+    if (np > 0 && !out) return fail(MAG_E_NULL, "out is NULL");
+    std::copy(pairs.begin(), pairs.end(), out);
+    return MAG_OK;
+}

@@ -5,6 +5,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <vector>
+
 #include "magneton.h"
 
 namespace mag {
@@ -264,6 +266,11 @@ hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double
 hipError_t launch_svd_match(const SpecDesc* da, int na, const double* sa, const SpecDesc* db,
                             int nb, const double* sb, double eps, uint8_t* match,
                             hipStream_t stream);
+
+// Section 4.2's subgraph matching (host): finest pairs as (entry1, exit1,
+// entry2, exit2) quadruples appended to out; MAG_OK or MAG_E_GRAPH
+int match_subgraphs(const mag_graph& a, const mag_graph& b, const int32_t* eq, int32_t n_eq,
+                    std::vector<int32_t>& out);
 
 hipError_t launch_groupby(const GroupParams& p, hipStream_t stream);
 // *dst = v, in stream order (a kernel, so the write can sit in a captured graph)

@@ -265,3 +265,52 @@ def replay_session(seed: int, n_ops: int = 98_304, n_keys: int = 416, rate_hz: f
 def synth_key(k: int) -> int:
     """A 64-bit operator key for vocabulary index k (splitmix64 finaliser)."""
     return int(_load().synth_mix64(ctypes.c_uint64(0x4D41474E45544F4E ^ k)))
+
+
+def graph_pair(seed: int, blocks: int = 8, width: int = 4, decoys: int = 5,
+               crossing: int = 0) -> dict:
+    """Two computational graphs made of the same sequence of blocks, each block
+    built differently in the two graphs (random fan-out width and depth
+    between the block's input and output operators), with the block outputs
+    declared equivalent, plus decoy pairs between interior operators and
+    optionally crossing pairs between block outputs of different positions.
+    Node 0 is each graph's input and node n-1 its output."""
+    rng = np.random.default_rng(seed)
+
+    def make():
+        edges, bounds = [], [0]
+        nxt = 1
+        interior = []
+        for _ in range(blocks):
+            a = bounds[-1]
+            w = int(rng.integers(1, width + 1))
+            tails = []
+            for _ in range(w):
+                depth = int(rng.integers(1, 4))
+                prev = a
+                for _ in range(depth):
+                    edges.append((prev, nxt))
+                    interior.append(nxt)
+                    prev = nxt
+                    nxt += 1
+                tails.append(prev)
+            b = nxt
+            nxt += 1
+            for t in tails:
+                edges.append((t, b))
+            if rng.random() < 0.3:
+                edges.append((a, b))  # a residual edge
+            bounds.append(b)
+        return nxt, edges, bounds, interior
+
+    n1, e1, b1, i1 = make()
+    n2, e2, b2, i2 = make()
+    eq = [(x, y) for x, y in zip(b1, b2)]
+    for _ in range(decoys):
+        eq.append((int(rng.choice(i1)), int(rng.choice(i2))))
+    for _ in range(crossing):
+        i, j = rng.integers(1, blocks, 2)
+        eq.append((b1[int(i)], b2[int(j)]))
+    order = rng.permutation(len(eq))
+    return {"n1": n1, "edges1": e1, "n2": n2, "edges2": e2,
+            "eq": [eq[k] for k in order], "bounds1": b1, "bounds2": b2}
