@@ -1325,7 +1325,7 @@ void unfolding_task(const mag_tensor* t, int g, mag::SvdTask& task)
             task.lstr[task.nl++] = str[i];
         }
     }
-    task.nt = (int32_t)((task.K + 15) / 16);
+    task.nt = (int32_t)((task.K + 63) / 64);  // 64-row Gram blocks
     task.nchunk = (int32_t)((task.L + mag::GRAM_CHUNK - 1) / mag::GRAM_CHUNK);
 }
 

@@ -247,7 +247,7 @@ struct SvdTask {
     double* gram;    // [K][K]
     double* out;     // [K] singular values, descending
     int64_t item0;   // first Gram work item of this task
-    int32_t nt;      // 16-row tiles: ceil(K / 16)
+    int32_t nt;      // 64-row blocks: ceil(K / 64)
     int32_t nchunk;  // column chunks: ceil(L / GRAM_CHUNK)
 };
 

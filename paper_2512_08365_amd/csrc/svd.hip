@@ -7,11 +7,12 @@
 // eigenvalues of the Gram matrix X X^T, X the unfolding or its transpose,
 // whichever has fewer rows (K = min(M, N) <= SVD_MAX_K, L = max(M, N)).
 //
-// k_gram: one wave per (task, 16 x 16 tile pair of the upper triangle, chunk
-//   of GRAM_CHUNK columns); the tile is a sum of fp64 16x16x4 MFMA products
-//   over the chunk (fp32 data widened exactly), added into the Gram matrix
-//   (and its mirror) with fp64 atomics.  The elements of X are gathered
-//   through the unfolding's mixed-radix offsets.
+// k_gram: one workgroup per (task, 64 x 64 block of the upper triangle,
+//   chunk of GRAM_CHUNK columns); the block's rows are staged in LDS a step
+//   of columns at a time and its 16 tiles are sums of fp64 16x16x4 MFMA
+//   products (fp32 data widened exactly), added into the Gram matrix (and its
+//   mirror) with fp64 atomics.  The elements of X are gathered through the
+//   unfolding's mixed-radix offsets.
 // k_svd_eig: one workgroup per task: Householder reduction of the Gram
 //   matrix (in place, in global memory) to tridiagonal form, then every
 //   eigenvalue by bisection on Sturm counts, sigma = sqrt(max(lambda, 0)),
@@ -28,7 +29,6 @@ namespace mag {
 namespace {
 
 constexpr int GW = 64;
-constexpr int GRAM_WAVES = 4;
 constexpr int EIG_THREADS = 256;
 
 typedef double d4 __attribute__((ext_vector_type(4)));
@@ -55,12 +55,23 @@ __global__ void k_svd_clear(double* g, int64_t n)
         g[i] = 0.0;
 }
 
-__global__ __launch_bounds__(GW * GRAM_WAVES) void k_gram(const SvdTask* tasks, int n_tasks,
-                                                          int64_t n_items)
+// One workgroup of 16 waves per (task, 64 x 64 block of the upper triangle,
+// chunk of GRAM_CHUNK columns).  Each 64-column step stages the block's 64
+// rows of each operand in LDS as fp64 (one global load per element, rows
+// fastest across threads, so a unit-stride row mode gives coalesced loads);
+// wave w then multiplies tile (w / 4, w % 4) from LDS with 16 MFMA steps.
+constexpr int GB = 64;              // block side
+constexpr int GSTEP = 64;           // columns staged per step
+constexpr int GTHREADS = 1024;      // 16 waves: one per 16 x 16 tile of the block
+
+__global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_tasks,
+                                                   int64_t n_items)
 {
-    const int lane = threadIdx.x % GW;
-    const int64_t item = (int64_t)blockIdx.x * GRAM_WAVES + threadIdx.x / GW;
-    if (item >= n_items) return;  // the whole wave
+    __shared__ double xa[GSTEP][GB + 1], xb[GSTEP][GB + 1];  // [column][row], padded
+    __shared__ int32_t loff[GRAM_CHUNK];
+    __shared__ int64_t roff[2][GB];
+    const int64_t item = blockIdx.x;
+    if (item >= n_items) return;  // uniform
     int lo = 0, hi = n_tasks - 1;  // the last task whose first item is <= item
     while (lo < hi) {
         const int mid = (lo + hi + 1) >> 1;
@@ -70,47 +81,54 @@ __global__ __launch_bounds__(GW * GRAM_WAVES) void k_gram(const SvdTask* tasks, 
     const int64_t local = item - t.item0;
     const int64_t chunk = local % t.nchunk;
     int64_t pr = local / t.nchunk;
-    int ti = 0, rowlen = t.nt;
+    int bi = 0, rowlen = t.nt;  // nt counts 64-row blocks here
     while (pr >= rowlen && rowlen > 0) {
         pr -= rowlen;
-        ++ti;
+        ++bi;
         --rowlen;
     }
-    const int tj = ti + (int)pr;
-    const int r = lane & 15, kq = lane >> 4;
-    const int64_t ra = (int64_t)ti * 16 + r, rb = (int64_t)tj * 16 + r;
-    const bool va = ra < t.K, vb = rb < t.K;
-    const int64_t oa = va ? mode_offset((uint32_t)ra, t.nk, t.kdim, t.kstr) : 0;
-    const int64_t ob = vb ? mode_offset((uint32_t)rb, t.nk, t.kdim, t.kstr) : 0;
+    const int bj = bi + (int)pr;
+    const int tid = threadIdx.x, lane = tid % GW, wv = tid / GW;
     const int64_t b0 = chunk * GRAM_CHUNK, b1 = min(b0 + GRAM_CHUNK, t.L);
-    // the chunk's column offsets, computed once by the wave's lanes together
-    __shared__ int32_t loff_s[GRAM_WAVES][GRAM_CHUNK];
-    int32_t* loff = loff_s[threadIdx.x / GW];
-    for (int64_t q = lane; q < b1 - b0; q += GW)
+    for (int64_t q = tid; q < b1 - b0; q += GTHREADS)
         loff[q] = (int32_t)mode_offset((uint32_t)(b0 + q), t.nl, t.ldim, t.lstr);
-    // the lanes read each other's entries: a wave's LDS operations complete in
-    // order; the fences keep the compiler from moving the reads above the writes
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    if (tid < 2 * GB) {
+        const int side = tid / GB, r = tid % GB;
+        const int64_t row = (int64_t)(side ? bj : bi) * GB + r;
+        roff[side][r] = (row < t.K) ? mode_offset((uint32_t)row, t.nk, t.kdim, t.kstr) : -1;
+    }
+    __syncthreads();
+    const int ti = wv / 4, tj = wv % 4;  // this wave's tile inside the block
+    const int r = lane & 15, kq = lane >> 4;
     d4 acc = {0.0, 0.0, 0.0, 0.0};
-    // A operand: lane holds X[ti*16 + lane%16][b + lane/16]; B operand: lane
-    // holds X[tj*16 + lane%16][b + lane/16]; the product is the Gram tile
-    for (int64_t b = b0; b < b1; b += 4) {
-        const int64_t bb = b + kq;
-        const bool vl = bb < b1;
-        const int64_t ol = vl ? (int64_t)loff[bb - b0] : 0;
-        const double xa = (va && vl) ? (double)t.data[oa + ol] : 0.0;
-        const double xb = (vb && vl) ? (double)t.data[ob + ol] : 0.0;
-        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(xa, xb, acc, 0, 0, 0);
+    for (int64_t s0 = b0; s0 < b1; s0 += GSTEP) {
+        const int cols = (int)min((int64_t)GSTEP, b1 - s0);
+        // stage: element (row, column) of each operand; rows fastest
+        for (int q = tid; q < 2 * GB * GSTEP; q += GTHREADS) {
+            const int side = q / (GB * GSTEP), rem = q % (GB * GSTEP);
+            const int c = rem / GB, rr = rem % GB;
+            const int64_t ro = roff[side][rr];
+            double x = 0.0;
+            if (c < cols && ro >= 0) x = (double)t.data[ro + loff[s0 - b0 + c]];
+            (side ? xb : xa)[c][rr] = x;
+        }
+        __syncthreads();
+#pragma unroll 4
+        for (int c = 0; c < GSTEP; c += 4) {
+            const double a = xa[c + kq][ti * 16 + r];
+            const double b = xb[c + kq][tj * 16 + r];
+            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+        }
+        __syncthreads();  // before the next step overwrites the staged rows
     }
     // register j of a lane holds row 4 j + lane/16, column lane%16 of the tile
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-        const int64_t row = (int64_t)ti * 16 + 4 * j + kq, col = (int64_t)tj * 16 + r;
-        if (row < t.K && col < t.K) {
+        const int64_t row = (int64_t)bi * GB + ti * 16 + 4 * j + kq;
+        const int64_t col = (int64_t)bj * GB + tj * 16 + r;
+        if (row < t.K && col < t.K && (bi != bj || row <= col)) {
             atomicAdd(&t.gram[row * t.K + col], acc[j]);
-            if (ti != tj) atomicAdd(&t.gram[col * t.K + row], acc[j]);
+            if (row != col) atomicAdd(&t.gram[col * t.K + row], acc[j]);
         }
     }
 }
@@ -126,7 +144,19 @@ __device__ double block_sum(double v, double* red)
     return s;
 }
 
+// 1/q within about an ulp: the hardware estimate refined by two Newton steps
+// (the Sturm recurrence is a chain of these; a correctly rounded division
+// would lengthen every link)
+__device__ __forceinline__ double recip_nr(double q)
+{
+    double r = __builtin_amdgcn_rcp(q);
+    r = fma(r, fma(-q, r, 1.0), r);
+    r = fma(r, fma(-q, r, 1.0), r);
+    return r;
+}
+
 // eigenvalues of the symmetric tridiagonal (d, e) below x: Sturm count
+// (|q| >= pivmin > 0 keeps every reciprocal finite)
 __device__ int sturm_count(const double* d, const double* e2, int n, double x, double pivmin)
 {
     int c = 0;
@@ -134,7 +164,7 @@ __device__ int sturm_count(const double* d, const double* e2, int n, double x, d
     if (fabs(q) < pivmin) q = -pivmin;
     c += q < 0.0;
     for (int i = 1; i < n; ++i) {
-        q = d[i] - x - e2[i - 1] / q;
+        q = d[i] - x - e2[i - 1] * recip_nr(q);
         if (fabs(q) < pivmin) q = -pivmin;
         c += q < 0.0;
     }
@@ -145,7 +175,10 @@ constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in 
 
 // Householder reduction of the symmetric n x n matrix A (row stride n) to
 // tridiagonal form: d[k] the diagonal, e2[k] the squared off-diagonal
-__device__ void tridiagonalize(double* A, int n, double* v, double* w, double* d, double* e2,
+typedef __attribute__((address_space(3))) double lds_f64;
+
+template <class Ptr>
+__device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* d, double* e2,
                                double* red)
 {
     const int tid = threadIdx.x;
@@ -176,7 +209,7 @@ __device__ void tridiagonalize(double* A, int n, double* v, double* w, double* d
         // p = beta A_sub v (columns by threads: row j of A is read across threads)
         double pv = 0.0;
         for (int i = tid; i < m; i += EIG_THREADS) {
-            const double* col = A + (size_t)(k + 1) * n + (k + 1 + i);
+            const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
             double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
             int j = 0;
             for (; j + 4 <= m; j += 4) {  // four independent loads in flight
@@ -195,7 +228,7 @@ __device__ void tridiagonalize(double* A, int n, double* v, double* w, double* d
         // A_sub -= v w^T + w v^T (each thread walks its columns down the rows;
         // the rows of one column are independent, so the loop is unrolled)
         for (int i = tid; i < m; i += EIG_THREADS) {
-            double* col = A + (size_t)(k + 1) * n + (k + 1 + i);
+            const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
             const double vi = v[i], wi = w[i];
 #pragma unroll 8
             for (int j = 0; j < m; ++j) col[(size_t)j * n] -= v[j] * wi + w[j] * vi;
@@ -225,7 +258,7 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
     if (n <= EIG_LDS_K) {
         for (int q = tid; q < n * n; q += EIG_THREADS) As[q] = t.gram[q];
         __syncthreads();
-        tridiagonalize(As, n, v, w, d, e2, red);
+        tridiagonalize((lds_f64*)As, n, v, w, d, e2, red);  // ds_ instructions
     } else {
         tridiagonalize(t.gram, n, v, w, d, e2, red);
     }
@@ -334,8 +367,8 @@ hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double
     hipLaunchKernelGGL(k_svd_clear, dim3((unsigned)max(cb, (int64_t)1)), dim3(256), 0, stream,
                        gram, gram_len);
     if (n_items > 0)
-        hipLaunchKernelGGL(k_gram, dim3((unsigned)((n_items + GRAM_WAVES - 1) / GRAM_WAVES)),
-                           dim3(GW * GRAM_WAVES), 0, stream, tasks, n_tasks, n_items);
+        hipLaunchKernelGGL(k_gram, dim3((unsigned)n_items), dim3(GTHREADS), 0, stream, tasks,
+                           n_tasks, n_items);
     hipLaunchKernelGGL(k_svd_eig, dim3((unsigned)n_tasks), dim3(EIG_THREADS), 0, stream, tasks);
     return hipGetLastError();
 }
