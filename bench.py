@@ -302,7 +302,6 @@ def subgraphs_bench(args):
     20,000 blocks (about 100,000 operators each); the oracle on 300 blocks."""
     import paper_2512_08365_amd as mag
     import synth
-    from oracle import graph_match as G
     c = synth.graph_pair(args.seed, blocks=20000, width=4, decoys=2000, crossing=200)
     nodes = c["n1"] + c["n2"]
     t0 = time.perf_counter()
@@ -312,6 +311,7 @@ def subgraphs_bench(args):
            "edges": len(c["edges1"]) + len(c["edges2"]), "pairs": len(pairs),
            "seconds": dt, "nodes_per_s": nodes / dt}
     if not args.no_cpu_baseline:
+        from oracle import graph_match as G
         s = synth.graph_pair(args.seed, blocks=300, width=4, decoys=30, crossing=3)
         t0 = time.perf_counter()
         G.match(s["n1"], s["edges1"], s["n2"], s["edges2"], s["eq"])
