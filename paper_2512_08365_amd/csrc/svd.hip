@@ -14,9 +14,10 @@
 //   mirror) with fp64 atomics.  The elements of X are gathered through the
 //   unfolding's mixed-radix offsets.
 // k_svd_eig: one workgroup per task: Householder reduction of the Gram
-//   matrix (in place, in global memory) to tridiagonal form, then every
-//   eigenvalue by bisection on Sturm counts, sigma = sqrt(max(lambda, 0)),
-//   written in descending order.
+//   matrix (in LDS up to side 128, else in place in global memory) to
+//   tridiagonal form, then every eigenvalue by multisection on Sturm counts
+//   (the count of eigenvalues below x), sigma = sqrt(max(lambda, 0)), written
+//   in descending order.
 // k_svd_match: one workgroup per tensor pair: which spectra of the two lists
 //   are close, then a one-to-one pairing by augmenting paths.
 
@@ -155,22 +156,6 @@ __device__ __forceinline__ double recip_nr(double q)
     return r;
 }
 
-// eigenvalues of the symmetric tridiagonal (d, e) below x: Sturm count
-// (|q| >= pivmin > 0 keeps every reciprocal finite)
-__device__ int sturm_count(const double* d, const double* e2, int n, double x, double pivmin)
-{
-    int c = 0;
-    double q = d[0] - x;
-    if (fabs(q) < pivmin) q = -pivmin;
-    c += q < 0.0;
-    for (int i = 1; i < n; ++i) {
-        q = d[i] - x - e2[i - 1] * recip_nr(q);
-        if (fabs(q) < pivmin) q = -pivmin;
-        c += q < 0.0;
-    }
-    return c;
-}
-
 constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in LDS
 
 // Householder reduction of the symmetric n x n matrix A (row stride n) to
@@ -178,8 +163,8 @@ constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in 
 typedef __attribute__((address_space(3))) double lds_f64;
 
 template <class Ptr>
-__device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* d, double* e2,
-                               double* red)
+__device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double (*w2)[EIG_THREADS / 2],
+                               double* d, double* e2, double* red)
 {
     const int tid = threadIdx.x;
     // Householder reduction: step k annihilates column k below the subdiagonal
@@ -206,32 +191,50 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* d, do
         __syncthreads();
         if (tid == 0) v[0] = v0;
         __syncthreads();
-        // p = beta A_sub v (columns by threads: row j of A is read across threads)
+        // p = beta A_sub v (columns by threads: row j of A is read across
+        // threads); with at most half as many columns as threads, two threads
+        // share a column, each taking half of the rows
+        const bool split = m <= EIG_THREADS / 2;
+        const int ci = split ? tid % (EIG_THREADS / 2) : tid;
+        const int hf = split ? tid / (EIG_THREADS / 2) : 0;
+        const int jlo = split ? hf * (m / 2) : 0, jhi = split ? (hf ? m : m / 2) : m;
         double pv = 0.0;
-        for (int i = tid; i < m; i += EIG_THREADS) {
+        for (int i = ci; i < m; i += (split ? m + 1 : EIG_THREADS)) {
             const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
             double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
-            int j = 0;
-            for (; j + 4 <= m; j += 4) {  // four independent loads in flight
+            int j = jlo;
+            for (; j + 4 <= jhi; j += 4) {  // four independent loads in flight
                 s0 += col[(size_t)j * n] * v[j];
                 s1 += col[(size_t)(j + 1) * n] * v[j + 1];
                 s2 += col[(size_t)(j + 2) * n] * v[j + 2];
                 s3 += col[(size_t)(j + 3) * n] * v[j + 3];
             }
-            for (; j < m; ++j) s0 += col[(size_t)j * n] * v[j];
-            w[i] = beta * ((s0 + s1) + (s2 + s3));
-            pv += w[i] * v[i];
+            for (; j < jhi; ++j) s0 += col[(size_t)j * n] * v[j];
+            const double part = beta * ((s0 + s1) + (s2 + s3));
+            if (split) {
+                w2[hf][i] = part;
+            } else {
+                w[i] = part;
+                pv += part * v[i];
+            }
+        }
+        if (split) {
+            __syncthreads();
+            if (hf == 0 && ci < m) {
+                w[ci] = w2[0][ci] + w2[1][ci];
+                pv = w[ci] * v[ci];
+            }
         }
         const double K2 = 0.5 * beta * block_sum(pv, red);
         for (int i = tid; i < m; i += EIG_THREADS) w[i] -= K2 * v[i];
         __syncthreads();
         // A_sub -= v w^T + w v^T (each thread walks its columns down the rows;
         // the rows of one column are independent, so the loop is unrolled)
-        for (int i = tid; i < m; i += EIG_THREADS) {
+        for (int i = ci; i < m; i += (split ? m + 1 : EIG_THREADS)) {
             const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
             const double vi = v[i], wi = w[i];
 #pragma unroll 8
-            for (int j = 0; j < m; ++j) col[(size_t)j * n] -= v[j] * wi + w[j] * vi;
+            for (int j = jlo; j < jhi; ++j) col[(size_t)j * n] -= v[j] * wi + w[j] * vi;
         }
         __syncthreads();
     }
@@ -252,15 +255,16 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
     __shared__ double d[SVD_MAX_K], e2[SVD_MAX_K];
     __shared__ double red[EIG_THREADS / 64];
     __shared__ double As[EIG_LDS_K * EIG_LDS_K];
+    __shared__ double w2[2][EIG_THREADS / 2];
     const SvdTask& t = tasks[blockIdx.x];
     const int n = (int)t.K;
     const int tid = threadIdx.x;
     if (n <= EIG_LDS_K) {
         for (int q = tid; q < n * n; q += EIG_THREADS) As[q] = t.gram[q];
         __syncthreads();
-        tridiagonalize((lds_f64*)As, n, v, w, d, e2, red);  // ds_ instructions
+        tridiagonalize((lds_f64*)As, n, v, w, w2, d, e2, red);  // ds_ instructions
     } else {
-        tridiagonalize(t.gram, n, v, w, d, e2, red);
+        tridiagonalize(t.gram, n, v, w, w2, d, e2, red);
     }
     // Gershgorin interval and the smallest pivot allowed in a Sturm count
     double glo = INFINITY, ghi = -INFINITY, emax = 0.0;
@@ -275,14 +279,39 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
     glo -= 2.0 * DBL_EPSILON * span + pivmin;
     ghi += 2.0 * DBL_EPSILON * span + pivmin;
     for (int k = tid; k < n; k += EIG_THREADS) {
-        // the k-th smallest eigenvalue: count(lo) <= k < count(hi)
+        // the k-th smallest eigenvalue: count(lo) <= k < count(hi); each
+        // round counts at four interior points (four independent Sturm
+        // chains side by side) and keeps the fifth of the interval holding it
         double lo = glo, hi = ghi;
-        for (int it = 0; it < 128; ++it) {
-            const double mid = 0.5 * (lo + hi);
-            if (!(hi - lo > 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin) || mid == lo ||
-                mid == hi)
-                break;
-            if (sturm_count(d, e2, n, mid, pivmin) <= k) lo = mid; else hi = mid;
+        for (int it = 0; it < 64; ++it) {
+            if (!(hi - lo > 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin)) break;
+            const double h = (hi - lo) * 0.2;
+            double x[4], q[4];
+            int c[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                x[u] = lo + h * (double)(u + 1);
+                q[u] = d[0] - x[u];
+                if (fabs(q[u]) < pivmin) q[u] = -pivmin;
+                c[u] = q[u] < 0.0;
+            }
+            for (int i = 1; i < n; ++i) {
+#pragma unroll
+                for (int u = 0; u < 4; ++u) {
+                    q[u] = d[i] - x[u] - e2[i - 1] * recip_nr(q[u]);
+                    if (fabs(q[u]) < pivmin) q[u] = -pivmin;
+                    c[u] += q[u] < 0.0;
+                }
+            }
+            double nlo = lo, nhi = hi;
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                if (c[u] <= k) nlo = fmax(nlo, x[u]);
+                else nhi = fmin(nhi, x[u]);
+            }
+            if (nlo == lo && nhi == hi) break;  // no representable progress
+            lo = nlo;
+            hi = nhi;
         }
         const double lam = 0.5 * (lo + hi);
         t.out[n - 1 - k] = sqrt(fmax(lam, 0.0));
