@@ -218,7 +218,7 @@ def counter_workspace_size(n_samples: int, n_intervals: int, key_capacity: int =
 def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None,
                       validate: bool = True, key_capacity: int | None = None,
                       indices: bool = True, workspace=None, out=None, time_kernels: bool = False,
-                      latency: bool = False):
+                      latency: bool = False, asynchronous: bool = False):
     """Per-operator energy from a cumulative energy counter (software replay mode).
 
     t: float64 [n] reading times (s), C: float64 [n] cumulative energy (J),
@@ -226,7 +226,8 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
     used up to t - delay), s/e: float64 [m] replay windows (one sequence),
     replays: int32 [m] runs per window or None, keys: int64 [m] or None.
     Returns (per_interval, per_key, summary) as attribute() does; the energies
-    are per run (the window's counter increase over its replay count).
+    are per run (the window's counter increase over its replay count).  With
+    asynchronous=True a Pending whose finish() returns them once the work ran.
     """
     lib = _lib()
     n = int(t.shape[0])
@@ -234,7 +235,7 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
     dev = t.device
     group = keys is not None
     flags = ((0 if validate else SKIP_VALIDATE) | (N.MAG_TIME_KERNELS if time_kernels else 0) |
-             (KEY_LATENCY if latency and group else 0))
+             (KEY_LATENCY if latency and group else 0) | (ASYNC if asynchronous else 0))
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
     ws_bytes = counter_workspace_size(n, m, cap if group else 0, flags)
     if workspace is None or workspace.numel() < ws_bytes:
@@ -265,16 +266,22 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
         tab["keys"].data_ptr() if group else None, ctypes.byref(ks) if group else None,
         ctypes.byref(summ), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
     _check(rc)
-    per_interval = {"energy": energy}
-    if indices:
-        per_interval["start_idx"] = si
-        per_interval["end_idx"] = ei
-    per_key = _key_rows(tab, ks) if group else None
-    summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
-               "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
-               "n_keys": int(summ.n_keys), "kernel_ms": summ.tile_kernel_ms,
-               "device_ms": summ.device_ms}
-    return per_interval, per_key, summary
+
+    def build():
+        per_interval = {"energy": energy}
+        if indices:
+            per_interval["start_idx"] = si
+            per_interval["end_idx"] = ei
+        per_key = _key_rows(tab, ks) if group else None
+        summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
+                   "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
+                   "n_keys": int(summ.n_keys), "kernel_ms": summ.tile_kernel_ms,
+                   "device_ms": summ.device_ms}
+        return per_interval, per_key, summary
+
+    if asynchronous:
+        return Pending(workspace, ks, summ, build, (t, C, s, e, keys, replays))
+    return build()
 
 
 def diff(a: dict, b: dict, k: int, workspace=None):

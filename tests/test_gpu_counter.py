@@ -165,3 +165,22 @@ def test_device_detected_errors(case, code):
         mag.attribute_counter(d["t"], d["C"], d["s"], d["e"], delay=delay,
                               replays=torch.from_numpy(reps).cuda())
     assert got.value.code == code, case
+
+
+def test_asynchronous_and_timed_calls_equal_the_synchronous_one():
+    import paper_2512_08365_amd as mag
+    c = synth.counter_case(51, n=20000, m=3000)
+    d = _dev(c)
+    args = (d["t"], d["C"], d["s"], d["e"], d["key"])
+    kw = dict(delay=c["delay"], replays=d["reps"], latency=True)
+    ref = mag.attribute_counter(*args, **kw)
+    pend = mag.attribute_counter(*args, asynchronous=True, time_kernels=True, **kw)
+    got = pend.finish()
+    for k in ("energy", "start_idx", "end_idx"):
+        assert np.array_equal(got[0][k].cpu().numpy(), ref[0][k].cpu().numpy()), k
+    for k in ("keys", "count"):
+        assert np.array_equal(got[1][k].cpu().numpy(), ref[1][k].cpu().numpy()), k
+    assert_energy_close(got[1]["duration"].cpu().numpy(), ref[1]["duration"].cpu().numpy(),
+                        "latency")
+    assert got[2]["n_clipped"] == ref[2]["n_clipped"]
+    assert got[2]["kernel_ms"] > 0.0 and got[2]["device_ms"] >= got[2]["kernel_ms"]
