@@ -1,25 +1,33 @@
 #!/usr/bin/env python3
 """Throughput of operator energy attribution + A/B diff on one MI355X.
 
-One step = the whole path over one A/B pair of the multi-stream workload
-(100,000,000 power samples at 1 MHz, 4 concurrent streams x 1,000,000
-operator intervals, 5,000 Zipf(1.2) keys): attribute side A, attribute side B
-(equal split of concurrent power, per-interval energies and sample indices,
-per-key count/sum/M2), then join and rank the top-100 excess-energy keys.
-Side A runs on the current stream; side B on a second stream (default
-priority) that waits for A's per-interval outputs (the `intervals_ready`
-event), so B's tile kernel runs while A's per-key grouping does, and A's tile
-kernel has the device to itself.  Both are enqueued (MAG_ASYNC) and finished
-before the diff.  Side A's tile kernel is timed with HIP events carried on its
-dispatch in every timed step; side B runs untimed (the events add about 20 us
-per call).
-Inputs are synthetic, seeded and resident in HBM before timing.
+Default (the headline): one step = the whole path over one A/B pair of the
+multi-stream workload (100,000,000 power samples at 1 MHz, 4 concurrent
+streams x 1,000,000 operator intervals, 5,000 Zipf(1.2) keys): attribute side
+A, attribute side B (equal split of concurrent power, per-interval energies
+and sample indices, per-key count/sum/M2), then join and rank the top-100
+excess-energy keys.  Side A runs on the current stream; side B on a second
+stream (default priority) that waits for A's per-interval outputs (the
+`intervals_ready` event), so B's tile kernel runs while A's per-key grouping
+does, and A's tile kernel has the device to itself.  Both attributions are
+enqueued asynchronously and leave their key counts on the device; the diff is
+enqueued behind both and its synchronization is the step's only host wait.
+Side A's tile kernel is timed with HIP events carried on its dispatch in every
+timed step; side B runs untimed.  Inputs are synthetic, seeded and resident in
+HBM before timing.
+
+--workload 1/2/3/4/5 times the other workloads the same way (2 and 4 fit in
+or near the 256 MB Infinity Cache and are timed with a 512 MB flush before
+each step); workload 5 streams both sides in 32,000,000-sample chunks,
+kernel-only (chunks already in HBM) or --end-to-end (from pinned host memory,
+PCIe-bound).
 
 Prints ONE JSON line.  `value` is operator intervals attributed per second
-(both sides); samples/s and the pipeline's algorithmic HBM GB/s ride along.
-`roofline` covers the dominant kernel (the interval-energy tile kernel),
-timed with HIP events on the call's stream; `cpu_baseline` is the CPU oracle
-timed on this host's cores over both sides of the same workload.
+(all sides); samples/s and the step's algorithmic HBM GB/s ride along
+(`pipeline_roofline`, at 12 B per sample and 48 B per interval).  `roofline`
+covers the dominant kernel (the interval-energy tile kernel), timed with HIP
+events on the call's stream; `cpu_baseline` is the CPU oracle timed on one
+pinned host core over sides of the same workload.
 """
 from __future__ import annotations
 
@@ -154,7 +162,13 @@ class Side:
         assert rc == 0
         self.ws = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
         self.pio = N.IntervalOut(self.energy.data_ptr(), self.si.data_ptr(), self.ei.data_ptr())
-        self.ks = N.KeyStats(self.ksum.data_ptr(), self.km2.data_ptr(), self.kcnt.data_ptr(), k_cap, 0)
+        # the key-row count is also left on the device, so that the diff can
+        # be enqueued behind the attribution without a host wait
+        self.nkd = torch.zeros(1, dtype=torch.int64, device=dev)
+        self.ks = N.KeyStats(self.ksum.data_ptr(), self.km2.data_ptr(), self.kcnt.data_ptr(), k_cap,
+                             0, None, self.nkd.data_ptr())
+        self.ks_dev = N.KeyStats(self.ksum.data_ptr(), self.km2.data_ptr(), self.kcnt.data_ptr(),
+                                 k_cap, -1, None, self.nkd.data_ptr())
         self.summ = N.Summary()
 
     def attribute(self, lib, stream):
@@ -176,23 +190,65 @@ class Side:
         return self.summ.tile_kernel_ms
 
 
-def cpu_baseline(A, B):
-    """The oracle, as it stands, on both sides of the workload (one core)."""
+def host_description() -> dict:
+    """This host's core count and CPU model (recorded with the oracle baseline)."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        allowed = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        allowed = None
+    return {"nproc": os.cpu_count(), "cpus_allowed": allowed, "cpu_model": model}
+
+
+class pinned_thread:
+    """Pin the calling thread (not the process: the GPU runtime's own threads
+    keep their affinity) to one allowed CPU while the oracle is timed."""
+
+    def __enter__(self):
+        self.old = None
+        self.cpu = None
+        try:
+            self.old = os.sched_getaffinity(0)
+            self.cpu = min(self.old)
+            os.sched_setaffinity(0, {self.cpu})
+        except (AttributeError, OSError):
+            self.old = None
+        return self
+
+    def __exit__(self, *exc):
+        if self.old is not None:
+            os.sched_setaffinity(0, self.old)
+        return False
+
+
+def cpu_baseline(sides, pairs, label):
+    """The oracle, as it stands, on the given sides of the workload, pinned to
+    one core: attribution and grouping of every side, then the diffs."""
     import oracle
-    t0 = time.perf_counter()
-    tabs = []
-    for c in (A, B):
-        r = oracle.attribute(c["t"], c["P"], c["s"], c["e"], c["offsets"])
-        tabs.append(oracle.groupby(c["key"], r["energy"]))
-    oracle.diff(tabs[0], tabs[1], TOP_K)
-    dt = time.perf_counter() - t0
-    m = A["s"].shape[0] + B["s"].shape[0]
-    return {"value": m / dt, "unit": "intervals/s", "cores": 1, "kind": "oracle",
-            "sample": ("both sides of the benchmark workload (2 x 100,000,000 samples, "
-                       f"2 x 4,000,000 intervals), attribution + grouping + top-{TOP_K} diff, "
-                       f"{dt:.1f} s on one host core"),
-            "seconds": round(dt, 2),
-            "samples_per_s": (A["t"].shape[0] + B["t"].shape[0]) / dt}
+    with pinned_thread() as pin:
+        t0 = time.perf_counter()
+        tabs = []
+        for c in sides:
+            r = oracle.attribute(c["t"], c["P"], c["s"], c["e"], c["offsets"])
+            tabs.append(oracle.groupby(c["key"], r["energy"]))
+        for a, b in pairs:
+            oracle.diff(tabs[a], tabs[b], TOP_K)
+        dt = time.perf_counter() - t0
+    m = sum(c["s"].shape[0] for c in sides)
+    n = sum(c["t"].shape[0] for c in sides)
+    res = {"value": m / dt, "unit": "intervals/s", "cores": 1, "kind": "oracle",
+           "sample": f"{label}: attribution + grouping + top-{TOP_K} diff, {dt:.1f} s",
+           "seconds": round(dt, 2), "samples_per_s": n / dt, "pinned_cpu": pin.cpu}
+    res.update(host_description())
+    return res
 
 
 def counter_session(args, torch, mag):
@@ -329,6 +385,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", type=int, default=WORKLOAD, choices=[1, 2, 3, 4, 5],
+                    help="workload to time (default 3, the multi-stream 100M-sample trace)")
+    ap.add_argument("--end-to-end", action="store_true",
+                    help="workload 5 only: push the chunks from pinned host memory")
     ap.add_argument("--subgraphs", action="store_true",
                     help="measure the host-side subgraph matching (Section 4.2) instead")
     ap.add_argument("--invariants", action="store_true",
@@ -345,7 +405,7 @@ def main():
     if args.summarize_counters:
         import synth
         sh = synth.shape(WORKLOAD)
-        summarize_counters(*args.summarize_counters, tile_bytes=12 * sh["n"] + 40 * sh["m"])
+        summarize_counters(*args.summarize_counters, tile_bytes=12 * sh["n"] + 48 * sh["m"])
         return
     if args.subgraphs:
         subgraphs_bench(args)
@@ -376,73 +436,39 @@ def main():
         return
     lib = N.load()
     log(f"[bench] {mag.version()} on {torch.cuda.get_device_name(0)}")
-    t0 = time.perf_counter()
-    A, B = synth.sides(WORKLOAD, args.seed)
-    log(f"[bench] generated workload in {time.perf_counter() - t0:.1f} s")
-    sh = synth.shape(WORKLOAD)
-    k_cap = 8192
-    s1 = torch.cuda.current_stream()
-    s2 = torch.cuda.Stream()  # default priority
-    a_ready = torch.cuda.Event()
-    a_ready.record(s1)  # creates the HIP event
-    sa = Side(A, lib, N, torch, k_cap, ready_event=ctypes.c_void_p(a_ready.cuda_event))
-    sb = Side(B, lib, N, torch, k_cap, timed=False)
-    torch.cuda.synchronize()
-    stream = ctypes.c_void_p(s1.cuda_stream)
-    stream_b = ctypes.c_void_p(s2.cuda_stream)
+    if args.workload in (1, 2, 3):
+        ab_bench(args, torch, mag, lib, N, synth)
+    elif args.workload == 4:
+        sweep_bench(args, torch, mag, lib, N, synth)
+    else:
+        long_bench(args, torch, mag, synth)
 
-    # diff buffers
-    dev = "cuda"
-    dcap = TOP_K
-    d_out = {k: torch.empty(dcap, dtype=dt, device=dev) for k, dt in
-             (("key", torch.int64), ("ratio", torch.float64), ("ea", torch.float64),
-              ("eb", torch.float64), ("ca", torch.int64), ("cb", torch.int64))}
-    b = ctypes.c_size_t(0)
-    lib.mag_diff_workspace_size(k_cap, k_cap, TOP_K, ctypes.byref(b))
-    d_ws = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
-    ro = N.RankOut(d_out["key"].data_ptr(), d_out["ratio"].data_ptr(), d_out["ea"].data_ptr(),
-                   d_out["eb"].data_ptr(), d_out["ca"].data_ptr(), d_out["cb"].data_ptr(), dcap,
-                   0, 0, 0, 0)
 
-    tile_ms = []
+WORKLOADS = {
+    1: ("tiny A/B pair: 10,000 samples at 1 ms (jittered), 2,000 sequential intervals, "
+        "50 Zipf(1.1) keys; A+B attribution + top-10 diff"),
+    2: ("decode-shaped trace: 2,000,000 samples at 100 kHz, 32 layers x 12 ops x 256 steps = "
+        "98,304 sequential intervals, 416 keys; A+B attribution + top-10 diff"),
+    3: ("multi-stream trace: 100,000,000 fp32 power samples at 1 MHz, 4 concurrent streams x "
+        "1,000,000 intervals (equal split), 5,000 Zipf(1.2) keys; A+B attribution + top-100 diff"),
+    4: ("batched sweep: baseline + 8 candidate traces, each 20,000,000 samples at 200 kHz and "
+        "1,000,000 sequential intervals, 2,000 keys; 9 attributions + one batched top-100 diff "
+        "of the 8 candidates"),
+    5: ("long-run trace: 360,000,000 samples at 100 kHz, 50,000,000 sequential intervals, "
+        "20,000 Zipf(1.05) keys, both sides streamed in 32,000,000-sample chunks; "
+        "A+B attribution + top-100 diff"),
+}
+TOPK = {1: 10, 2: 10, 3: 100, 4: 100, 5: 100}
+MALL_FLUSH_BYTES = 512 << 20  # larger than the 256 MB Infinity Cache
 
-    def step(record):
-        # side B starts once A's per-interval outputs are complete; one wait for both
-        sa.attribute(lib, stream)
-        s2.wait_event(a_ready)
-        sb.attribute(lib, stream_b)
-        ta = sa.finish(lib, stream)
-        sb.finish(lib, stream_b)
-        rc = lib.mag_diff(sa.kout.data_ptr(), ctypes.byref(sa.ks), sb.kout.data_ptr(),
-                          ctypes.byref(sb.ks), TOP_K, ctypes.byref(ro), d_ws.data_ptr(),
-                          d_ws.numel(), stream)
-        if rc != 0:
-            raise RuntimeError(f"mag_diff failed {rc}: {lib.mag_last_error().decode()}")
-        if record:
-            tile_ms.append(ta)
 
-    for _ in range(args.warmup):
-        step(False)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(True)
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    sec_per_step = dt / args.steps
-    log(f"[bench] {args.steps} steps in {dt:.3f} s -> {sec_per_step * 1e3:.3f} ms/step; "
-        f"keys A={sa.ks.n_keys} B={sb.ks.n_keys} joined={ro.n_join}")
-
+def result_line(args, cfg, sh, sides, sec_per_step, extra):
     n, m = sh["n"], sh["m"]
-    intervals = 2 * m
-    samples = 2 * n
-    bytes_step = 2 * (12 * n + 48 * m)  # algorithmic bytes of the step (see design notes)
-    tile_bytes = 12 * n + 40 * m        # per launch of the tile kernel
-    tile_avg_ms = sum(tile_ms) / len(tile_ms)
-    achieved = tile_bytes / (tile_avg_ms * 1e-3) / 1e9
-    result = {
+    bytes_step = sides * (12 * n + 48 * m)  # algorithmic bytes of a step (12 B/sample + 48 B/interval)
+    gbs = bytes_step / sec_per_step / 1e9
+    r = {
         "metric": METRIC,
-        "value": intervals / sec_per_step,
+        "value": sides * m / sec_per_step,
         "unit": "intervals/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -453,24 +479,283 @@ def main():
         "vs_baseline": None,
         "dtype": "f64",
         "data": "synthetic",
-        "config": {"workload": ("multi-stream trace: 100,000,000 fp32 power samples at 1 MHz, "
-                                "4 concurrent streams x 1,000,000 intervals (equal split), "
-                                "5,000 Zipf(1.2) keys; A+B attribution + top-100 diff"),
-                   "n_samples_per_side": n, "n_intervals_per_side": m, "streams": 4,
-                   "keys": sh["K"], "top_k": TOP_K, "sides": 2, "seed": args.seed},
-        "samples_per_s": samples / sec_per_step,
-        "hbm_gbps_algorithmic": bytes_step / sec_per_step / 1e9,
-        "hbm_frac_algorithmic": bytes_step / sec_per_step / 1e9 / HBM_PEAK_GBS,
-        "roofline": {"kernel": "k_tile (interval energies)", "bound": "hbm",
-                     "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": counters_traffic(),
-                     "algorithmic_bytes_per_launch": tile_bytes,
-                     "avg_launch_ms": tile_avg_ms},
+        "config": {"workload": WORKLOADS[cfg], "n_samples_per_side": n, "n_intervals_per_side": m,
+                   "streams": sh["streams"], "keys": sh["K"], "top_k": TOPK[cfg], "sides": sides,
+                   "seed": args.seed},
+        "samples_per_s": sides * n / sec_per_step,
+        "hbm_gbps_algorithmic": gbs,
+        "hbm_frac_algorithmic": gbs / HBM_PEAK_GBS,
+        # the whole step (attributions + grouping + diff) against the HBM roofline,
+        # at 12 B per sample and 48 B per interval
+        "pipeline_roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS,
+                              "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                              "algorithmic_bytes_per_step": bytes_step},
     }
+    r.update(extra)
+    return r
+
+
+def tile_roofline(tile_ms, n, m):
+    """The dominant kernel (interval energies) against the HBM roofline, timed
+    with HIP events carried on its dispatch."""
+    avg = sum(tile_ms) / len(tile_ms)
+    b48 = 12 * n + 48 * m  # per-unit figures of the method: samples and intervals
+    b40 = 12 * n + 40 * m  # what the kernel itself moves (it does not read the keys)
+    return {"kernel": "k_tile (interval energies)", "bound": "hbm",
+            "achieved": b48 / (avg * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": b48 / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "traffic": counters_traffic(),
+            "traffic_source": ("rocprofv3 FETCH_SIZE + WRITE_SIZE of this kernel source, scaled "
+                               "by a 1 GiB copy (profiles/tile_kernel_counters.json); null when "
+                               "the source changed since"),
+            "algorithmic_bytes_per_launch": b48, "avg_launch_ms": avg,
+            "achieved_at_40B_per_interval": b40 / (avg * 1e-3) / 1e9,
+            "frac_at_40B_per_interval": b40 / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS}
+
+
+def ab_bench(args, torch, mag, lib, N, synth):
+    """One step = attribute A, attribute B, top-k diff; one host wait per step."""
+    cfg = args.workload
+    t0 = time.perf_counter()
+    A, B = synth.sides(cfg, args.seed)
+    log(f"[bench] generated workload {cfg} in {time.perf_counter() - t0:.1f} s")
+    sh = synth.shape(cfg)
+    k_cap = 8192
+    top = TOPK[cfg]
+    s1 = torch.cuda.current_stream()
+    s2 = torch.cuda.Stream()  # default priority
+    a_ready = torch.cuda.Event()
+    a_ready.record(s1)  # creates the HIP event
+    b_done = torch.cuda.Event()
+    sa = Side(A, lib, N, torch, k_cap, ready_event=ctypes.c_void_p(a_ready.cuda_event))
+    sb = Side(B, lib, N, torch, k_cap, timed=False)
+    torch.cuda.synchronize()
+    stream = ctypes.c_void_p(s1.cuda_stream)
+    stream_b = ctypes.c_void_p(s2.cuda_stream)
+    d_out = {k: torch.empty(top, dtype=dt, device="cuda") for k, dt in
+             (("key", torch.int64), ("ratio", torch.float64), ("ea", torch.float64),
+              ("eb", torch.float64), ("ca", torch.int64), ("cb", torch.int64))}
+    b = ctypes.c_size_t(0)
+    lib.mag_diff_workspace_size(k_cap, k_cap, top, ctypes.byref(b))
+    d_ws = torch.empty(int(b.value), dtype=torch.uint8, device="cuda")
+    ro = N.RankOut(d_out["key"].data_ptr(), d_out["ratio"].data_ptr(), d_out["ea"].data_ptr(),
+                   d_out["eb"].data_ptr(), d_out["ca"].data_ptr(), d_out["cb"].data_ptr(), top,
+                   0, 0, 0, 0)
+    tile_ms = []
+
+    def step(record):
+        # B starts once A's per-interval outputs are complete; the diff reads
+        # both key counts on the device, behind both attributions; the diff's
+        # synchronization is the step's one host wait
+        sa.attribute(lib, stream)
+        s2.wait_event(a_ready)
+        sb.attribute(lib, stream_b)
+        b_done.record(s2)
+        s1.wait_event(b_done)
+        rc = lib.mag_diff(sa.kout.data_ptr(), ctypes.byref(sa.ks_dev), sb.kout.data_ptr(),
+                          ctypes.byref(sb.ks_dev), top, ctypes.byref(ro), d_ws.data_ptr(),
+                          d_ws.numel(), stream)
+        if rc != 0:
+            raise RuntimeError(f"mag_diff failed {rc}: {lib.mag_last_error().decode()}")
+        ta = sa.finish(lib, stream)
+        sb.finish(lib, stream_b)
+        if record:
+            tile_ms.append(ta)
+
+    flush = None
+    if cfg == 2:
+        flush_buf = torch.empty(MALL_FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+        flush = lambda: flush_buf.fill_(1.0)  # noqa: E731
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    if flush is None:
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            step(True)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        timing = "wall clock over the timed steps"
+    else:
+        # the cache is flushed before every step, outside the timed region
+        evs = []
+        for _ in range(args.steps):
+            flush()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(s1)
+            step(True)
+            e1.record(s1)
+            evs.append((e0, e1))
+        torch.cuda.synchronize()
+        dt = sum(a.elapsed_time(b_) for a, b_ in evs) * 1e-3
+        timing = "HIP events around each step; a 512 MB write flushes the Infinity Cache before it"
+    sec_per_step = dt / args.steps
+    log(f"[bench] {args.steps} steps in {dt:.4f} s -> {sec_per_step * 1e3:.4f} ms/step; "
+        f"keys A={sa.ks.n_keys} B={sb.ks.n_keys} joined={ro.n_join}")
+    extra = {"timing": timing, "roofline": tile_roofline(tile_ms, sh["n"], sh["m"])}
+    res = result_line(args, cfg, sh, 2, sec_per_step, extra)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on both sides ...")
-        result["cpu_baseline"] = cpu_baseline(A, B)
-    print(json.dumps(result), flush=True)
+        res["cpu_baseline"] = cpu_baseline([A, B], [(0, 1)], "both sides of the same workload")
+    print(json.dumps(res), flush=True)
+
+
+def sweep_bench(args, torch, mag, lib, N, synth):
+    """One step = 9 attributions (baseline + 8 candidates, alternating two
+    streams, each tile kernel behind the previous side's per-interval outputs)
+    and one batched top-100 diff of the 8 candidates against the baseline."""
+    cfg = 4
+    t0 = time.perf_counter()
+    sides_h = synth.sides(cfg, args.seed)
+    log(f"[bench] generated workload {cfg} in {time.perf_counter() - t0:.1f} s")
+    sh = synth.shape(cfg)
+    k_cap = 4096
+    top = TOPK[cfg]
+    s = [torch.cuda.current_stream(), torch.cuda.Stream()]
+    ready = [torch.cuda.Event() for _ in sides_h]
+    for ev in ready:
+        ev.record(s[0])
+    last = torch.cuda.Event()
+    sides = [Side(c, lib, N, torch, k_cap, timed=(i == 0),
+                  ready_event=ctypes.c_void_p(ready[i].cuda_event))
+             for i, c in enumerate(sides_h)]
+    torch.cuda.synchronize()
+    handles = [ctypes.c_void_p(x.cuda_stream) for x in s]
+    nb = len(sides) - 1
+    b = ctypes.c_size_t(0)
+    lib.mag_diff_batch_workspace_size(k_cap, nb, top, ctypes.byref(b))
+    d_ws = torch.empty(int(b.value), dtype=torch.uint8, device="cuda")
+    outs = (N.RankOut * nb)()
+    keep = []
+    for c in range(nb):
+        t = [torch.empty(top, dtype=dt, device="cuda") for dt in
+             (torch.int64, torch.float64, torch.float64, torch.float64, torch.int64, torch.int64)]
+        keep.append(t)
+        outs[c] = N.RankOut(*[x.data_ptr() for x in t], top, 0, 0, 0, 0)
+    keys_b = (ctypes.c_void_p * nb)(*[x.kout.data_ptr() for x in sides[1:]])
+    stats_b = (N.KeyStats * nb)(*[x.ks_dev for x in sides[1:]])
+    tile_ms = []
+
+    def step(record):
+        for i, side in enumerate(sides):
+            st = s[i % 2]
+            if i > 0:
+                st.wait_event(ready[i - 1])
+            side.attribute(lib, handles[i % 2])
+        # the diff waits for every side's grouping: the sides on the second
+        # stream are all behind this event
+        last.record(s[1])
+        s[0].wait_event(last)
+        rc = lib.mag_diff_batch(sides[0].kout.data_ptr(), ctypes.byref(sides[0].ks_dev), nb,
+                                keys_b, stats_b, top, outs, d_ws.data_ptr(), d_ws.numel(),
+                                handles[0])
+        if rc != 0:
+            raise RuntimeError(f"mag_diff_batch failed {rc}: {lib.mag_last_error().decode()}")
+        for i, side in enumerate(sides):
+            t = side.finish(lib, handles[i % 2])
+            if i == 0 and record:
+                tile_ms.append(t)
+
+    flush_buf = torch.empty(MALL_FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
+    for _ in range(args.warmup):
+        step(False)
+    torch.cuda.synchronize()
+    evs = []
+    for _ in range(args.steps):
+        flush_buf.fill_(1.0)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(s[0])
+        step(True)
+        e1.record(s[0])
+        evs.append((e0, e1))
+    torch.cuda.synchronize()
+    dt = sum(a.elapsed_time(b_) for a, b_ in evs) * 1e-3
+    sec_per_step = dt / args.steps
+    log(f"[bench] {args.steps} steps in {dt:.4f} s -> {sec_per_step * 1e3:.4f} ms/step; "
+        f"joined={[int(o.n_join) for o in outs]}")
+    extra = {"timing": ("HIP events around each step; a 512 MB write flushes the Infinity Cache "
+                        "before it"),
+             "roofline": tile_roofline(tile_ms, sh["n"], sh["m"])}
+    res = result_line(args, cfg, sh, len(sides), sec_per_step, extra)
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on the baseline and one candidate ...")
+        res["cpu_baseline"] = cpu_baseline(sides_h[:2], [(0, 1)],
+                                           "the baseline and candidate B1 (2 of the 9 traces)")
+    print(json.dumps(res), flush=True)
+
+
+def long_bench(args, torch, mag, synth):
+    """Both sides of the long-run workload streamed in 32,000,000-sample
+    chunks, then the top-100 diff.  Kernel-only: chunks already in HBM
+    (mag_stream_push); end to end (--end-to-end): chunks in pinned host memory,
+    copied over PCIe on a copy stream, double-buffered (mag_stream_push_host)."""
+    import numpy as np
+    cfg = 5
+    t0 = time.perf_counter()
+    sides_h = synth.sides(cfg, args.seed)
+    log(f"[bench] generated workload {cfg} in {time.perf_counter() - t0:.1f} s")
+    sh = synth.shape(cfg)
+    n = sh["n"]
+    chunk = 32_000_000
+    sizes = [chunk] * (n // chunk) + ([n % chunk] if n % chunk else [])
+    s_ = [torch.cuda.current_stream(), torch.cuda.Stream()]
+    dev = []
+    for c in sides_h:
+        d = {"s": torch.from_numpy(c["s"]).cuda(), "e": torch.from_numpy(c["e"]).cuda(),
+             "key": torch.from_numpy(np.ascontiguousarray(c["key"]).view(np.int64)).cuda()}
+        if args.end_to_end:
+            d["t"] = torch.from_numpy(c["t"]).pin_memory()
+            d["P"] = torch.from_numpy(c["P"]).pin_memory()
+        else:
+            d["t"] = torch.from_numpy(c["t"]).cuda()
+            d["P"] = torch.from_numpy(c["P"]).cuda()
+        dev.append(d)
+    torch.cuda.synchronize()
+
+    def step():
+        streams = []
+        for i, d in enumerate(dev):
+            with torch.cuda.stream(s_[i]):
+                st = mag.Stream(n, d["s"], d["e"], d["key"], key_capacity=32768,
+                                host_chunk=chunk if args.end_to_end else 0)
+                pos = 0
+                for k in sizes:
+                    if args.end_to_end:
+                        st.push_host(d["t"][pos:pos + k], d["P"][pos:pos + k])
+                    else:
+                        st.push(d["t"][pos:pos + k], d["P"][pos:pos + k])
+                    pos += k
+                streams.append(st)
+        tabs = []
+        for i, st in enumerate(streams):
+            with torch.cuda.stream(s_[i]):
+                tabs.append(st.end()[1])
+        return mag.diff(tabs[0], tabs[1], TOPK[cfg])
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        d = step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    sec_per_step = dt / args.steps
+    log(f"[bench] {args.steps} steps in {dt:.3f} s -> {sec_per_step * 1e3:.2f} ms/step; "
+        f"joined={d['n_join']}")
+    if args.end_to_end:
+        timing = ("end to end: wall clock from pinned host chunks (PCIe H2D included, "
+                  "bound by the link, not by HBM)")
+        extra = {"timing": timing,
+                 "h2d_gbps": 2 * 12 * n / sec_per_step / 1e9}
+    else:
+        extra = {"timing": "kernel-only: chunks resident in HBM, wall clock over the timed steps"}
+    res = result_line(args, cfg, sh, 2, sec_per_step, extra)
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle on side A ...")
+        res["cpu_baseline"] = cpu_baseline(sides_h[:1], [], "side A (one of the two traces), "
+                                           "unchunked")
+    print(json.dumps(res), flush=True)
 
 
 if __name__ == "__main__":

@@ -67,7 +67,11 @@ extern "C" {
 /* Time the call on `stream` with HIP events and report it in mag_summary. */
 #define MAG_TIME_KERNELS 0x4u
 /* mag_attribute returns once its work is enqueued; mag_attribute_finish
-   delivers n_keys, the summary and device-detected errors. */
+   delivers n_keys, the summary and device-detected errors.  A workspace holds
+   at most one unfinished asynchronous call: any attribution on it before
+   mag_attribute_finish returns MAG_E_STATE.  One thread may have up to 4096
+   unfinished asynchronous calls (on as many workspaces); beyond that the
+   status is read back by mag_attribute_finish from the device instead. */
 #define MAG_ASYNC 0x8u
 /* Also sum each key's interval durations (end - start; per replay run in the
    counter mode) into per_key->duration, which must then be non-NULL: the
@@ -243,11 +247,13 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
  *   summary    host struct, may be NULL: filled as by a synchronous call
  *              (tile_kernel_ms and device_ms when the call had MAG_TIME_KERNELS
  *              and is finished on the thread that made it)
- * Synchronizes `stream` (the call's stream) and returns what the synchronous
- * call would have returned for its device work: MAG_OK, MAG_E_TIMESTAMPS,
- * MAG_E_POWER, MAG_E_INTERVAL, MAG_E_CAPACITY or MAG_E_HIP; MAG_E_NULL or
- * MAG_E_WORKSPACE for a NULL or misaligned workspace.  A workspace that no
- * asynchronous call used gives unspecified results.
+ * Synchronizes the stream the call was enqueued on when it was made on this
+ * thread (its status copy is in flight there), otherwise `stream`, which must
+ * then be the call's stream; returns what the synchronous call would have
+ * returned for its device work: MAG_OK, MAG_E_TIMESTAMPS, MAG_E_POWER,
+ * MAG_E_INTERVAL, MAG_E_CAPACITY or MAG_E_HIP; MAG_E_NULL or MAG_E_WORKSPACE
+ * for a NULL or misaligned workspace.  A workspace that no asynchronous call
+ * used gives unspecified results.
  */
 int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summary* summary,
                          hipStream_t stream);
@@ -338,6 +344,30 @@ int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_
 int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
              const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
              size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * mag_diff_batch -- one baseline table A ranked against several candidate
+ * tables B_0 .. B_{n-1} (Section 6.1 evaluates each case by comparing a
+ * system against its more efficient counterparts, Table
+ * "tab:known-issues-diagnosis"): for every candidate c exactly what
+ * mag_diff(keysA, statsA, keysB[c], &statsB[c], k, &out[c]) computes, in a
+ * fixed number of launches per 8 candidates (the candidates' parameters
+ * travel as kernel arguments, one candidate per grid z index).
+ *   n_candidates  0 .. MAG_DIFF_BATCH_MAX (0: nothing is done)
+ *   keysB         HOST array of n_candidates device pointers
+ *   statsB, out   HOST arrays of n_candidates structs (as in mag_diff)
+ *   workspace     device, >= mag_diff_batch_workspace_size(n_keys_a,
+ *                 n_candidates, k) bytes (n_keys_a: statsA's n_keys, or its
+ *                 capacity when counted on the device)
+ * Synchronizes `stream` once.  Errors as mag_diff (the first failing
+ * candidate's), and MAG_E_SIZE for n_candidates out of range.
+ */
+#define MAG_DIFF_BATCH_MAX 1024
+int mag_diff_batch_workspace_size(int64_t n_keys_a, int32_t n_candidates, int64_t k,
+                                  size_t* bytes);
+int mag_diff_batch(const uint64_t* keysA, const mag_key_stats* statsA, int32_t n_candidates,
+                   const uint64_t* const* keysB, const mag_key_stats* statsB, int64_t k,
+                   mag_rank_out* out, void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /* ------------------------------------------------ tensor matching (4.2) */
 #define MAG_SVD_MAX_RANK 5
@@ -524,6 +554,40 @@ int mag_stream_end(mag_stream* handle, uint64_t* keys_out, mag_key_stats* per_ke
 void mag_stream_abort(mag_stream* handle);
 int mag_stream_state_export(const mag_stream* handle, void* host_buf, size_t* bytes);
 int mag_stream_state_import(mag_stream* handle, const void* host_buf, size_t bytes);
+
+/*
+ * Chunks pushed from HOST memory (the long-run case of a trace that arrives
+ * over time, Section 5.2's continuous microsecond-resolution power source,
+ * reaching the GPU over PCIe).  The chunk is copied into one of two device
+ * halves of a caller-owned staging buffer on a caller-owned copy stream while
+ * the previous chunk's tiles run on the compute stream, so copy and compute
+ * overlap (pinned host memory is needed for the copies to be asynchronous;
+ * pageable memory works, with copies that block the calling thread).
+ *   mag_stream_host_staging_size(max_chunk, &bytes)
+ *       device bytes of a staging buffer for chunks of up to max_chunk
+ *       samples (two halves of 12 B per sample).  MAG_E_SIZE for
+ *       max_chunk < 1 or > MAG_MAX_SAMPLES.
+ *   mag_stream_set_host_staging(h, max_chunk, staging, staging_bytes, copy_stream)
+ *       once per handle, before the first mag_stream_push_host: staging is
+ *       device memory (256-byte aligned, >= the size above) that must stay
+ *       allocated until mag_stream_end / mag_stream_abort; copy_stream must
+ *       differ from the stream given at begin.  Creates two pairs of HIP
+ *       events, released with the handle.  MAG_E_STATE if staging is already
+ *       set, MAG_E_WORKSPACE, MAG_E_NULL, MAG_E_HIP.
+ *   mag_stream_push_host(h, t_host, p_host, n_chunk)
+ *       the next n_chunk <= max_chunk samples from host memory, same rules as
+ *       mag_stream_push otherwise.  The host chunk must stay unchanged until
+ *       the second later mag_stream_push_host call returns, or until
+ *       mag_stream_end / mag_stream_abort (the call waits on the host for the
+ *       copy of the chunk pushed two calls earlier, whose half it reuses).
+ *       Chunks from device memory (mag_stream_push) and from host memory may
+ *       be mixed.  Errors as mag_stream_push, and MAG_E_STATE without staging.
+ */
+int mag_stream_host_staging_size(int64_t max_chunk, size_t* bytes);
+int mag_stream_set_host_staging(mag_stream* handle, int64_t max_chunk, void* staging,
+                                size_t staging_bytes, hipStream_t copy_stream);
+int mag_stream_push_host(mag_stream* handle, const double* t_host, const float* p_host,
+                         int64_t n_chunk);
 
 /* Static description of a status code. */
 const char* mag_strerror(int status);

@@ -14,7 +14,7 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "detect", "invariants",
+__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "diff_batch", "detect", "invariants",
            "match", "match_subgraphs", "Stream", "workspace_size",
            "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
@@ -120,18 +120,21 @@ def _stream_handle(device):
 
 class Pending:
     """An attribution enqueued with asynchronous=True; finish() waits for it and
-    returns what attribute() returns (raising its errors)."""
+    returns what attribute() returns (raising its errors).  The stream current
+    when the call was made is the one waited for, whatever stream is current
+    when finish() runs."""
 
-    def __init__(self, workspace, ks, summ, build, keep):
+    def __init__(self, workspace, ks, summ, build, keep, stream):
         self._workspace, self._ks, self._summ, self._build, self._keep = (
             workspace, ks, summ, build, keep)
+        self._stream = stream
         self._result = None
 
     def finish(self):
         if self._result is None:
             rc = _lib().mag_attribute_finish(
                 self._workspace.data_ptr(), ctypes.byref(self._ks) if self._ks else None,
-                ctypes.byref(self._summ), _stream_handle(self._workspace.device))
+                ctypes.byref(self._summ), self._stream)
             _check(rc)
             self._result = self._build()
         return self._result
@@ -181,13 +184,14 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     if group:
         tab, ks = _key_outputs(cap, dev, latency)
     summ = N.Summary()
+    sh = _stream_handle(dev)
     rc = lib.mag_attribute(
         _dev_ptr(t, torch.float64, "t"), _dev_ptr(P, torch.float32, "P"), n,
         _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
         _dev_ptr(keys, torch.int64, "keys") if group else None, m, ctypes.byref(o),
         ctypes.byref(pio), tab["keys"].data_ptr() if group else None,
         ctypes.byref(ks) if group else None, ctypes.byref(summ), workspace.data_ptr(),
-        workspace.numel(), _stream_handle(dev))
+        workspace.numel(), sh)
     _check(rc)
 
     def build():
@@ -203,7 +207,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
 
     if asynchronous:
         # the inputs and the options stay referenced until finish()
-        return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys))
+        return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys), sh)
     return build()
 
 
@@ -258,13 +262,14 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
     if group:
         tab, ks = _key_outputs(cap, dev, latency)
     summ = N.Summary()
+    sh = _stream_handle(dev)
     rc = lib.mag_attribute_counter(
         _dev_ptr(t, torch.float64, "t"), _dev_ptr(C, torch.float64, "C"), n, float(delay),
         _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
         _dev_ptr(replays, torch.int32, "replays"),
         _dev_ptr(keys, torch.int64, "keys") if group else None, m, flags, ctypes.byref(pio),
         tab["keys"].data_ptr() if group else None, ctypes.byref(ks) if group else None,
-        ctypes.byref(summ), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
+        ctypes.byref(summ), workspace.data_ptr(), workspace.numel(), sh)
     _check(rc)
 
     def build():
@@ -280,7 +285,7 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
         return per_interval, per_key, summary
 
     if asynchronous:
-        return Pending(workspace, ks, summ, build, (t, C, s, e, keys, replays))
+        return Pending(workspace, ks, summ, build, (t, C, s, e, keys, replays), sh)
     return build()
 
 
@@ -314,6 +319,53 @@ def diff(a: dict, b: dict, k: int, workspace=None):
     return {"key": key[:r], "ratio": ratio[:r], "energy_a": ea[:r], "energy_b": eb[:r],
             "count_a": ca[:r], "count_b": cb[:r], "n_only_a": int(ro.n_only_a),
             "n_only_b": int(ro.n_only_b), "n_join": int(ro.n_join)}
+
+
+def diff_batch(a: dict, bs: list, k: int, workspace=None) -> list:
+    """diff(a, b, k) for every per-key table b in bs, in one library call
+    (mag_diff_batch: a fixed number of launches per 8 candidates, one
+    synchronization)."""
+    lib = _lib()
+    dev = a["keys"].device
+    n = len(bs)
+    na = int(a["keys"].shape[0])
+    b_ws = ctypes.c_size_t(0)
+    _check(lib.mag_diff_batch_workspace_size(na, n, int(k), ctypes.byref(b_ws)))
+    if workspace is None or workspace.numel() < int(b_ws.value):
+        workspace = torch.empty(max(1, int(b_ws.value)), dtype=torch.uint8, device=dev)
+    cap = max(1, min(int(k), na))
+    sa = N.KeyStats(_dev_ptr(a["sum"], torch.float64, "a.sum"), None,
+                    _dev_ptr(a["count"], torch.int64, "a.count"), na, na)
+    keys_b = (ctypes.c_void_p * max(n, 1))()
+    stats_b = (N.KeyStats * max(n, 1))()
+    outs = (N.RankOut * max(n, 1))()
+    tens = []
+    for c, b in enumerate(bs):
+        nb = int(b["keys"].shape[0])
+        keys_b[c] = _dev_ptr(b["keys"], torch.int64, "b.keys")
+        stats_b[c] = N.KeyStats(_dev_ptr(b["sum"], torch.float64, "b.sum"), None,
+                                _dev_ptr(b["count"], torch.int64, "b.count"), nb, nb)
+        t = {"key": torch.empty(cap, dtype=torch.int64, device=dev),
+             "ratio": torch.empty(cap, dtype=torch.float64, device=dev),
+             "energy_a": torch.empty(cap, dtype=torch.float64, device=dev),
+             "energy_b": torch.empty(cap, dtype=torch.float64, device=dev),
+             "count_a": torch.empty(cap, dtype=torch.int64, device=dev),
+             "count_b": torch.empty(cap, dtype=torch.int64, device=dev)}
+        outs[c] = N.RankOut(t["key"].data_ptr(), t["ratio"].data_ptr(), t["energy_a"].data_ptr(),
+                            t["energy_b"].data_ptr(), t["count_a"].data_ptr(),
+                            t["count_b"].data_ptr(), cap, 0, 0, 0, 0)
+        tens.append(t)
+    _check(lib.mag_diff_batch(_dev_ptr(a["keys"], torch.int64, "a.keys"), ctypes.byref(sa), n,
+                              keys_b, stats_b, int(k), outs, workspace.data_ptr(),
+                              workspace.numel(), _stream_handle(dev)))
+    res = []
+    for c, t in enumerate(tens):
+        r = int(outs[c].n_out)
+        d = {kk: v[:r] for kk, v in t.items()}
+        d.update(n_only_a=int(outs[c].n_only_a), n_only_b=int(outs[c].n_only_b),
+                 n_join=int(outs[c].n_join))
+        res.append(d)
+    return res
 
 
 def detect(a: dict, b: dict, threshold: float = 0.10, tolerance: float = 0.01,
@@ -477,7 +529,8 @@ class Stream:
 
     def __init__(self, max_samples: int, s, e, keys=None, *, n_streams: int = 1,
                  stream_offsets=None, equal_split: bool = True, validate: bool = True,
-                 key_capacity: int | None = None, indices: bool = True, latency: bool = False):
+                 key_capacity: int | None = None, indices: bool = True, latency: bool = False,
+                 host_chunk: int = 0):
         lib = _lib()
         m = int(s.shape[0])
         dev = s.device
@@ -506,6 +559,20 @@ class Stream:
             ctypes.byref(self._pio), self._cap, self._ws.data_ptr(), self._ws.numel(),
             _stream_handle(dev)))
         self._h = h
+        self._staging = self._copy_stream = None
+        if host_chunk:
+            # two device halves filled from host memory on a copy stream of
+            # the default priority, while the compute stream runs the tiles
+            b = ctypes.c_size_t(0)
+            _check(lib.mag_stream_host_staging_size(int(host_chunk), ctypes.byref(b)))
+            self._staging = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
+            self._copy_stream = torch.cuda.Stream(dev)
+            rc = lib.mag_stream_set_host_staging(
+                h, int(host_chunk), self._staging.data_ptr(), self._staging.numel(),
+                ctypes.c_void_p(self._copy_stream.cuda_stream))
+            if rc != N.MAG_OK:
+                self.abort()
+                _check(rc)
 
     def _handle(self):
         if self._h is None or not self._h.value:
@@ -520,6 +587,21 @@ class Stream:
         self._chunks.append((t, P))
         _check(_lib().mag_stream_push(h, _dev_ptr(t, torch.float64, "t"),
                                       _dev_ptr(P, torch.float32, "P"), n))
+
+    def push_host(self, t, P):
+        """The next chunk from host memory (CPU tensors, pinned for asynchronous
+        copies): float64 t and float32 P, at most host_chunk samples."""
+        h = self._handle()
+        n = int(t.shape[0])
+        if int(P.shape[0]) != n:
+            raise MagnetonError(N.MAG_E_SIZE, "t and P differ in length")
+        for x, dt, name in ((t, torch.float64, "t"), (P, torch.float32, "P")):
+            if not isinstance(x, torch.Tensor) or x.is_cuda:
+                raise MagnetonError(N.MAG_E_NULL, f"{name} must be a CPU tensor")
+            if x.dtype != dt or not x.is_contiguous():
+                raise MagnetonError(N.MAG_E_SIZE, f"{name} must be contiguous {dt}")
+        self._chunks.append((t, P))
+        _check(_lib().mag_stream_push_host(h, t.data_ptr(), P.data_ptr(), n))
 
     def export_state(self) -> bytes:
         h = self._handle()
@@ -539,6 +621,9 @@ class Stream:
         if self._h is not None and self._h.value:
             _lib().mag_stream_abort(self._h)
         self._h = None
+        if getattr(self, "_copy_stream", None) is not None:
+            # copies may still be landing in the staging buffer
+            self._copy_stream.synchronize()
         self._chunks = []
 
     def end(self):

@@ -39,11 +39,13 @@ MAG_MAX_STREAMS = 32
 EXPORTED = (
     "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_finish",
     "mag_counter_workspace_size", "mag_attribute_counter",
-    "mag_diff_workspace_size", "mag_diff", "mag_detect_workspace_size", "mag_detect",
+    "mag_diff_workspace_size", "mag_diff", "mag_diff_batch_workspace_size", "mag_diff_batch",
+    "mag_detect_workspace_size", "mag_detect",
     "mag_invariant_count", "mag_invariants_workspace_size", "mag_invariants",
     "mag_match_workspace_size", "mag_match", "mag_match_subgraphs",
     "mag_stream_workspace_size", "mag_stream_begin", "mag_stream_push", "mag_stream_end",
     "mag_stream_abort", "mag_stream_state_export", "mag_stream_state_import",
+    "mag_stream_host_staging_size", "mag_stream_set_host_staging", "mag_stream_push_host",
     "mag_strerror", "mag_last_error", "mag_version",
 )
 
@@ -130,6 +132,13 @@ def load(path: str = LIB_PATH):
     lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,
                              ctypes.c_size_t, c_vp]
     lib.mag_diff.restype = ctypes.c_int
+    lib.mag_diff_batch_workspace_size.argtypes = [c_i64, ctypes.c_int32, c_i64,
+                                                  P(ctypes.c_size_t)]
+    lib.mag_diff_batch_workspace_size.restype = ctypes.c_int
+    # keysB: host array of device pointers; statsB / out: host arrays of structs
+    lib.mag_diff_batch.argtypes = [c_vp, P(KeyStats), ctypes.c_int32, c_vp, c_vp, c_i64, c_vp,
+                                   c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_diff_batch.restype = ctypes.c_int
     lib.mag_detect_workspace_size.argtypes = [c_i64, c_i64, c_i64, P(ctypes.c_size_t)]
     lib.mag_detect_workspace_size.restype = ctypes.c_int
     lib.mag_detect.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), P(DetectOpts), P(DetectOut),
@@ -164,6 +173,12 @@ def load(path: str = LIB_PATH):
     lib.mag_stream_state_export.restype = ctypes.c_int
     lib.mag_stream_state_import.argtypes = [c_vp, c_vp, ctypes.c_size_t]
     lib.mag_stream_state_import.restype = ctypes.c_int
+    lib.mag_stream_host_staging_size.argtypes = [c_i64, P(ctypes.c_size_t)]
+    lib.mag_stream_host_staging_size.restype = ctypes.c_int
+    lib.mag_stream_set_host_staging.argtypes = [c_vp, c_i64, c_vp, ctypes.c_size_t, c_vp]
+    lib.mag_stream_set_host_staging.restype = ctypes.c_int
+    lib.mag_stream_push_host.argtypes = [c_vp, c_vp, c_vp, c_i64]
+    lib.mag_stream_push_host.restype = ctypes.c_int
     lib.mag_strerror.argtypes = [ctypes.c_int]
     lib.mag_strerror.restype = ctypes.c_char_p
     lib.mag_last_error.argtypes = []

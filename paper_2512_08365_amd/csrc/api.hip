@@ -5,6 +5,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <memory>
 #include <new>
 #include <vector>
 
@@ -170,46 +171,77 @@ int check_opts(const mag_attr_opts* opts, int64_t m, int* S, uint32_t* flags, ma
 
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
-// optional HIP-event timing of a call's device work on its stream.  The events
-// belong to (thread, device, workspace) and are created once: a call made with
-// MAG_ASYNC reads them back in mag_attribute_finish, on the same thread.
+// Per-thread records of a call's timing events and of the pinned host buffer
+// its status block is copied into, one per (device, workspace).  A record
+// whose asynchronous call is not finished yet (events recorded but not read,
+// or a status copy in flight) is never handed to another workspace: idle
+// records are recycled, least recently used first, once TIMER_KEEP of them
+// exist, and the table grows when every record is busy (up to TIMER_MAX
+// unfinished asynchronous calls per thread).
 struct TimerSlot {
     int dev = -1;
     const void* ws = nullptr;
     hipEvent_t ev[4] = {nullptr, nullptr, nullptr, nullptr};
-    bool pending = false;  // recorded by an asynchronous call, not read yet
+    bool pending = false;          // events recorded by an asynchronous call, not read yet
     bool status_pending = false;   // an asynchronous call copied its status here
+    hipStream_t stream = nullptr;  // the stream that call was enqueued on
     mag::Status* host_status = nullptr;  // pinned host copy of the status block
+    uint64_t used = 0;             // last use, for the recycling order
+    bool busy() const { return pending || status_pending; }
 };
-constexpr int TIMER_SLOTS = 16;
-thread_local TimerSlot g_timers[TIMER_SLOTS];
-thread_local int g_timer_next = 0;
+constexpr size_t TIMER_KEEP = 16;
+constexpr size_t TIMER_MAX = 4096;
+thread_local std::vector<std::unique_ptr<TimerSlot>> g_timers;
+thread_local uint64_t g_timer_clock = 0;
 
 TimerSlot* timer_slot(const void* ws, bool create)
 {
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess) return nullptr;
     for (auto& t : g_timers)
-        if (t.dev == dev && t.ws == ws) return &t;
+        if (t->dev == dev && t->ws == ws) {
+            t->used = ++g_timer_clock;
+            return t.get();
+        }
     if (!create) return nullptr;
-    TimerSlot& t = g_timers[g_timer_next];
-    g_timer_next = (g_timer_next + 1) % TIMER_SLOTS;
-    for (auto& x : t.ev)
+    TimerSlot* t = nullptr;
+    if (g_timers.size() >= TIMER_KEEP)
+        for (auto& x : g_timers)
+            if (!x->busy() && (!t || x->used < t->used)) t = x.get();
+    if (!t) {
+        if (g_timers.size() >= TIMER_MAX) return nullptr;
+        std::unique_ptr<TimerSlot> fresh(new (std::nothrow) TimerSlot());
+        if (!fresh) return nullptr;
+        t = fresh.get();
+        g_timers.push_back(std::move(fresh));
+    }
+    for (auto& x : t->ev)
         if (x) (void)hipEventDestroy(x);
-    mag::Status* keep = t.host_status;  // the pinned buffer is reused
-    t = TimerSlot{};
-    t.host_status = keep;
-    for (auto& x : t.ev)
-        if (hipEventCreate(&x) != hipSuccess) return nullptr;
-    if (!t.host_status) {
+    mag::Status* keep = t->host_status;  // the pinned buffer is reused
+    *t = TimerSlot{};
+    t->host_status = keep;
+    t->used = ++g_timer_clock;
+    for (auto& x : t->ev)
+        if (hipEventCreate(&x) != hipSuccess) {
+            x = nullptr;
+            return nullptr;
+        }
+    if (!t->host_status) {
         void* h = nullptr;
         if (hipHostMalloc(&h, sizeof(mag::Status), hipHostMallocDefault) != hipSuccess)
             return nullptr;
-        t.host_status = static_cast<mag::Status*>(h);
+        t->host_status = static_cast<mag::Status*>(h);
     }
-    t.dev = dev;
-    t.ws = ws;
-    return &t;
+    t->dev = dev;
+    t->ws = ws;
+    return t;
+}
+
+// an asynchronous call on `ws` whose result has not been collected yet
+bool unfinished(const void* ws)
+{
+    const TimerSlot* t = timer_slot(ws, false);
+    return t && t->busy();
 }
 
 struct EventTimer {
@@ -373,6 +405,25 @@ int finish_status(const mag::Status* status, mag_key_stats* per_key, mag_summary
     const int rc = read_status(status, stream, &st);
     if (rc != MAG_OK) return rc;
     return interpret_status(st, per_key, summary);
+}
+
+// the end of an asynchronous call: its status block is copied to the pinned
+// buffer of the workspace's record on `stream`, and the record keeps that
+// stream (and the timing events, when timed) for mag_attribute_finish.
+// Without a record, finishing reads the status block from the device.
+int async_status(const void* workspace, const mag::Status* status, hipStream_t stream, bool timed)
+{
+    TimerSlot* t = timer_slot(workspace, true);
+    if (!t) return MAG_OK;
+    t->pending = timed;
+    t->stream = stream;
+    if (t->host_status) {
+        const hipError_t e = hipMemcpyAsync(t->host_status, status, sizeof(mag::Status),
+                                            hipMemcpyDeviceToHost, stream);
+        if (e != hipSuccess) return hip_fail(e, "status copy");
+        t->status_pending = true;
+    }
+    return MAG_OK;
 }
 
 struct Job {
@@ -609,6 +660,8 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
     if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
     if (!aligned(timestamps, 8) || !aligned(power, 4))
         return fail(MAG_E_ALIGN, "input array not aligned to its element size");
+    if (unfinished(workspace))
+        return fail(MAG_E_STATE, "an asynchronous call on this workspace is not finished");
     int rc;
     if (per_key && (rc = check_key_outputs(keys_out, per_key, opts ? opts->flags : 0u)) != MAG_OK)
         return rc;
@@ -636,20 +689,11 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         return hip_fail(e, "intervals_ready event");
     if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
     timer.mark(3);
-    if (job.flags & MAG_ASYNC) {
+    if (job.flags & MAG_ASYNC)
         // results, errors and timings come from mag_attribute_finish; the status
         // block is copied to pinned host memory now, so that finishing needs
         // no further device work
-        if (timer.on) timer.slot->pending = true;
-        TimerSlot* t = timer_slot(workspace, true);
-        if (t && t->host_status) {
-            if ((e = hipMemcpyAsync(t->host_status, job.w.status, sizeof(mag::Status),
-                                    hipMemcpyDeviceToHost, stream)) != hipSuccess)
-                return hip_fail(e, "status copy");
-            t->status_pending = true;
-        }
-        return MAG_OK;
-    }
+        return async_status(workspace, job.w.status, stream, timer.on);
     rc = job.conclude(per_key, summary);
     if (summary) {
         summary->tile_kernel_ms = timer.ms(1, 2);
@@ -683,6 +727,8 @@ int mag_attribute_counter(const double* timestamps, const double* counter, int64
     if (!aligned(timestamps, 8) || !aligned(counter, 8))
         return fail(MAG_E_ALIGN, "input array not aligned to its element size");
     if (!(delay - delay == 0.0)) return fail(MAG_E_TIMESTAMPS, "delay is not finite");
+    if (unfinished(workspace))
+        return fail(MAG_E_STATE, "an asynchronous call on this workspace is not finished");
     int rc;
     if (per_key && (rc = check_key_outputs(keys_out, per_key, flags)) != MAG_OK) return rc;
     Job job;
@@ -748,17 +794,7 @@ int mag_attribute_counter(const double* timestamps, const double* counter, int64
     if ((e = mag::launch_counter_fold(cp, stream)) != hipSuccess) return hip_fail(e, "fold kernel");
     if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
     timer.mark(3);
-    if (flags & MAG_ASYNC) {
-        if (timer.on) timer.slot->pending = true;
-        TimerSlot* t = timer_slot(workspace, true);
-        if (t && t->host_status) {
-            if ((e = hipMemcpyAsync(t->host_status, job.w.status, sizeof(mag::Status),
-                                    hipMemcpyDeviceToHost, stream)) != hipSuccess)
-                return hip_fail(e, "status copy");
-            t->status_pending = true;
-        }
-        return MAG_OK;
-    }
+    if (flags & MAG_ASYNC) return async_status(workspace, job.w.status, stream, timer.on);
     rc = job.conclude(per_key, summary);
     if (summary) {
         summary->tile_kernel_ms = timer.ms(1, 2);
@@ -777,10 +813,14 @@ int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summ
     TimerSlot* t = timer_slot(workspace, false);
     int rc;
     if (t && t->status_pending && t->host_status) {
-        // the call already copied its status to pinned memory on `stream`
+        // the call already copied its status to pinned memory on its own
+        // stream, which may differ from `stream`: that one is waited for
         t->status_pending = false;
         hipError_t e2;
-        if ((e2 = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e2, "synchronize");
+        if ((e2 = hipStreamSynchronize(t->stream)) != hipSuccess) {
+            t->pending = false;
+            return hip_fail(e2, "synchronize");
+        }
         rc = interpret_status(*t->host_status, per_key, summary);
     } else {
         rc = finish_status(static_cast<const mag::Status*>(workspace), per_key, summary, stream);
@@ -829,6 +869,26 @@ struct mag_stream {
     int64_t b_next = 0;    // first tile not yet run
     int64_t n_stage = 0;   // samples held in staging, from sample b_next * TILE on
     int failed = 0;        // a launch failed: the handle only accepts end/abort
+    // chunks pushed from host memory: two device halves of the caller's
+    // staging buffer, filled in turn on the copy stream
+    struct HostHalf {
+        double* t = nullptr;
+        float* P = nullptr;
+        hipEvent_t copied = nullptr;  // the half's copy is complete (copy stream)
+        hipEvent_t freed = nullptr;   // the half's samples are consumed (compute stream)
+        bool copied_rec = false;      // the events have been recorded at least once
+        bool freed_rec = false;
+    } half[2];
+    int64_t host_chunk = 0;   // most samples one host chunk may hold (0: no staging)
+    int next_half = 0;
+    hipStream_t copy_stream = nullptr;
+    ~mag_stream()
+    {
+        for (auto& x : half) {
+            if (x.copied) (void)hipEventDestroy(x.copied);
+            if (x.freed) (void)hipEventDestroy(x.freed);
+        }
+    }
 };
 
 namespace {
@@ -1011,6 +1071,97 @@ int mag_stream_push(mag_stream* h, const double* t_chunk, const float* p_chunk, 
     return MAG_OK;
 }
 
+int mag_stream_host_staging_size(int64_t max_chunk, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    if (max_chunk < 1) return fail(MAG_E_SIZE, "max_chunk must be >= 1");
+    if (max_chunk > MAG_MAX_SAMPLES) return fail(MAG_E_SIZE, "max_chunk exceeds MAG_MAX_SAMPLES");
+    Carver c;
+    for (int i = 0; i < 2; ++i) {
+        c.take<double>((size_t)max_chunk);
+        c.take<float>((size_t)max_chunk);
+    }
+    *bytes = c.off;
+    return MAG_OK;
+}
+
+int mag_stream_set_host_staging(mag_stream* h, int64_t max_chunk, void* staging,
+                                size_t staging_bytes, hipStream_t copy_stream)
+{
+    g_last_error[0] = 0;
+    if (!h || !staging) return fail(MAG_E_NULL, "handle/staging is NULL");
+    if (h->failed) return fail(MAG_E_STATE, "a previous call on this stream failed");
+    if (h->host_chunk > 0) return fail(MAG_E_STATE, "host staging is already set");
+    if (copy_stream == h->job.stream)
+        return fail(MAG_E_STATE, "the copy stream must differ from the stream's compute stream");
+    size_t need = 0;
+    int rc = mag_stream_host_staging_size(max_chunk, &need);
+    if (rc) return rc;
+    if (!aligned(staging, 256)) return fail(MAG_E_WORKSPACE, "staging must be 256-byte aligned");
+    if (staging_bytes < need) {
+        snprintf(g_last_error, sizeof(g_last_error), "staging needs %zu bytes, got %zu", need,
+                 staging_bytes);
+        return MAG_E_WORKSPACE;
+    }
+    Carver c;
+    c.base = static_cast<char*>(staging);
+    for (auto& x : h->half) {
+        x.t = c.take<double>((size_t)max_chunk);
+        x.P = c.take<float>((size_t)max_chunk);
+        hipError_t e;
+        if ((e = hipEventCreateWithFlags(&x.copied, hipEventDisableTiming)) != hipSuccess ||
+            (e = hipEventCreateWithFlags(&x.freed, hipEventDisableTiming)) != hipSuccess)
+            return hip_fail(e, "staging events");
+        x.copied_rec = x.freed_rec = false;
+    }
+    h->host_chunk = max_chunk;
+    h->next_half = 0;
+    h->copy_stream = copy_stream;
+    return MAG_OK;
+}
+
+int mag_stream_push_host(mag_stream* h, const double* t_host, const float* p_host, int64_t n_chunk)
+{
+    g_last_error[0] = 0;
+    if (!h) return fail(MAG_E_NULL, "handle is NULL");
+    if (h->failed) return fail(MAG_E_STATE, "a previous call on this stream failed");
+    if (h->host_chunk == 0) return fail(MAG_E_STATE, "no host staging set on this stream");
+    if (n_chunk < 0) return fail(MAG_E_SIZE, "n_chunk must be >= 0");
+    if (n_chunk > h->host_chunk) return fail(MAG_E_SIZE, "chunk larger than the staging holds");
+    if (n_chunk == 0) return MAG_OK;
+    if (!t_host || !p_host) return fail(MAG_E_NULL, "chunk pointer is NULL");
+    if (h->received + n_chunk > h->job.pl.n)
+        return fail(MAG_E_SIZE, "more samples pushed than max_samples");
+    auto& x = h->half[h->next_half];
+    hipError_t e;
+    auto bad = [&](const char* where) {
+        h->failed = 1;
+        return hip_fail(e, where);
+    };
+    // the host chunk copied into this half two pushes ago is complete, so the
+    // caller may reuse its memory once this call returns
+    if (x.copied_rec && (e = hipEventSynchronize(x.copied)) != hipSuccess)
+        return bad("staging wait");
+    // the half's previous samples have been consumed by the compute stream
+    if ((x.freed_rec && (e = hipStreamWaitEvent(h->copy_stream, x.freed, 0)) != hipSuccess) ||
+        (e = hipMemcpyAsync(x.t, t_host, sizeof(double) * (size_t)n_chunk, hipMemcpyHostToDevice,
+                            h->copy_stream)) != hipSuccess ||
+        (e = hipMemcpyAsync(x.P, p_host, sizeof(float) * (size_t)n_chunk, hipMemcpyHostToDevice,
+                            h->copy_stream)) != hipSuccess ||
+        (e = hipEventRecord(x.copied, h->copy_stream)) != hipSuccess)
+        return bad("staging copy");
+    x.copied_rec = true;
+    if ((e = hipStreamWaitEvent(h->job.stream, x.copied, 0)) != hipSuccess)
+        return bad("staging wait");
+    const int rc = mag_stream_push(h, x.t, x.P, n_chunk);
+    if (rc != MAG_OK) return rc;
+    if ((e = hipEventRecord(x.freed, h->job.stream)) != hipSuccess) return bad("staging event");
+    x.freed_rec = true;
+    h->next_half ^= 1;
+    return MAG_OK;
+}
+
 int mag_stream_end(mag_stream* h, uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary)
 {
     g_last_error[0] = 0;
@@ -1157,11 +1308,10 @@ int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_
 
 namespace {
 
-// the join and ranking shared by mag_diff and mag_detect; p's detection fields
-// are set by the caller; the status block is returned in *st
-int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
-             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p,
-             void* workspace, size_t workspace_bytes, hipStream_t stream, mag::Status* st)
+// the checks of one comparison and the parameters that do not depend on the
+// workspace; *na / *nb are the table sizes (upper bounds for device counts)
+int diff_params(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+                const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p)
 {
     if (!statsA || !statsB || !out) return fail(MAG_E_NULL, "statsA/statsB/out is NULL");
     // a negative n_keys: the count is read on the device, bounded by the capacity
@@ -1183,21 +1333,6 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
                           !out->count_a || !out->count_b ||
                           (p.detect && (!p.out_la || !p.out_lb || !p.out_verdict))))
         return fail(MAG_E_NULL, "output array is NULL");
-    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
-    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
-    size_t need = 0;
-    mag_diff_workspace_size(na, nb, k, &need);
-    if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
-
-    Carver c;
-    c.base = static_cast<char*>(workspace);
-    const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(na, k), 1);
-    p.status = c.take<mag::Status>(1);
-    p.cand_r = c.take<double>(nc);
-    p.cand_key = c.take<uint64_t>(nc);
-    p.cand_ia = c.take<int32_t>(nc);
-    p.cand_ib = c.take<int32_t>(nc);
-    p.cand_rank = c.take<uint32_t>(nc);
     p.ka = keysA;
     p.sa = statsA->sum;
     p.ca = statsA->count;
@@ -1219,20 +1354,73 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
         p.la = statsA->duration;
         p.lb = statsB->duration;
     }
+    return MAG_OK;
+}
+
+// the candidate arrays of one comparison
+void carve_candidates(Carver& c, int64_t na, int64_t k, mag::DiffParams* p)
+{
+    const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(na, k), 1);
+    double* r = c.take<double>(nc);
+    uint64_t* key = c.take<uint64_t>(nc);
+    int32_t* ia = c.take<int32_t>(nc);
+    int32_t* ib = c.take<int32_t>(nc);
+    uint32_t* rank = c.take<uint32_t>(nc);
+    if (p) {
+        p->cand_r = r;
+        p->cand_key = key;
+        p->cand_ia = ia;
+        p->cand_ib = ib;
+        p->cand_rank = rank;
+    }
+}
+
+// a comparison's result from its status block
+int conclude_diff(const mag::DiffParams& p, const mag::Status& st, mag_rank_out* out)
+{
+    if (st.err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
+    const bool dev = p.na_dev || p.nb_dev;
+    const int64_t ra = dev ? (int64_t)st.diff_na : p.na;
+    const int64_t rb = dev ? (int64_t)st.diff_nb : p.nb;
+    out->n_join = st.n_join;
+    out->n_out = std::min<int64_t>(p.k, st.n_join);
+    out->n_only_a = ra - st.n_join;
+    out->n_only_b = rb - st.n_join;
+    return MAG_OK;
+}
+
+// the join and ranking shared by mag_diff and mag_detect; p's detection fields
+// are set by the caller; the status block is returned in *st
+int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p,
+             void* workspace, size_t workspace_bytes, hipStream_t stream, mag::Status* st)
+{
+    int rc = diff_params(keysA, statsA, keysB, statsB, k, out, p);
+    if (rc != MAG_OK) return rc;
+    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    size_t need = 0;
+    mag_diff_workspace_size(p.na, p.nb, k, &need);
+    if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
+    Carver c;
+    c.base = static_cast<char*>(workspace);
+    p.status = c.take<mag::Status>(1);
+    carve_candidates(c, p.na, k, &p);
     hipError_t e;
     if ((e = mag::launch_init_status(p.status, nullptr, 0, stream)) != hipSuccess)
         return hip_fail(e, "init");
     if ((e = mag::launch_diff(p, stream)) != hipSuccess) return hip_fail(e, "diff kernels");
-    const int rc = read_status(p.status, stream, st);
+    rc = read_status(p.status, stream, st);
     if (rc != MAG_OK) return rc;
-    if (st->err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
-    const int64_t ra = (devA || devB) ? (int64_t)st->diff_na : na;
-    const int64_t rb = (devA || devB) ? (int64_t)st->diff_nb : nb;
-    out->n_join = st->n_join;
-    out->n_out = std::min<int64_t>(k, st->n_join);
-    out->n_only_a = ra - st->n_join;
-    out->n_only_b = rb - st->n_join;
-    return MAG_OK;
+    return conclude_diff(p, *st, out);
+}
+
+size_t diff_batch_bytes(int64_t na, int32_t n, int64_t k)
+{
+    Carver c;
+    c.take<mag::Status>((size_t)std::max(n, 1));
+    for (int32_t i = 0; i < n; ++i) carve_candidates(c, na, k, nullptr);
+    return c.off;
 }
 
 }  // namespace
@@ -1248,6 +1436,59 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     mag::Status st;
     return run_diff(keysA, statsA, keysB, statsB, k, out, p, workspace, workspace_bytes, stream,
                     &st);
+}
+
+int mag_diff_batch_workspace_size(int64_t n_keys_a, int32_t n_candidates, int64_t k,
+                                  size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    if (n_keys_a < 0 || k < 0 || n_candidates < 0 || n_candidates > MAG_DIFF_BATCH_MAX)
+        return fail(MAG_E_SIZE, "negative size or too many candidates");
+    *bytes = diff_batch_bytes(n_keys_a, n_candidates, k);
+    return MAG_OK;
+}
+
+int mag_diff_batch(const uint64_t* keysA, const mag_key_stats* statsA, int32_t n_candidates,
+                   const uint64_t* const* keysB, const mag_key_stats* statsB, int64_t k,
+                   mag_rank_out* out, void* workspace, size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (n_candidates < 0 || n_candidates > MAG_DIFF_BATCH_MAX)
+        return fail(MAG_E_SIZE, "n_candidates must be in [0, MAG_DIFF_BATCH_MAX]");
+    if (n_candidates == 0) return MAG_OK;
+    if (!keysB || !statsB || !out) return fail(MAG_E_NULL, "keysB/statsB/out is NULL");
+    std::vector<mag::DiffParams> ps((size_t)n_candidates);
+    for (int32_t c = 0; c < n_candidates; ++c) {
+        ps[c] = mag::DiffParams{};
+        const int rc = diff_params(keysA, statsA, keysB[c], &statsB[c], k, &out[c], ps[c]);
+        if (rc != MAG_OK) return rc;
+    }
+    if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
+    if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    const int64_t na = ps[0].na;
+    if (workspace_bytes < diff_batch_bytes(na, n_candidates, k))
+        return fail(MAG_E_WORKSPACE, "workspace too small");
+    Carver c;
+    c.base = static_cast<char*>(workspace);
+    mag::Status* status = c.take<mag::Status>((size_t)n_candidates);
+    for (int32_t i = 0; i < n_candidates; ++i) {
+        ps[i].status = status + i;
+        carve_candidates(c, na, k, &ps[i]);
+    }
+    hipError_t e;
+    if ((e = mag::launch_diff_batch(ps.data(), n_candidates, stream)) != hipSuccess)
+        return hip_fail(e, "diff kernels");
+    std::vector<mag::Status> st((size_t)n_candidates);
+    if ((e = hipMemcpyAsync(st.data(), status, sizeof(mag::Status) * (size_t)n_candidates,
+                            hipMemcpyDeviceToHost, stream)) != hipSuccess)
+        return hip_fail(e, "status copy");
+    if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    for (int32_t i = 0; i < n_candidates; ++i) {
+        const int rc = conclude_diff(ps[i], st[i], &out[i]);
+        if (rc != MAG_OK) return rc;
+    }
+    return MAG_OK;
 }
 
 int mag_detect_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t rows, size_t* bytes)

@@ -10,6 +10,10 @@
 // Stage 2 (k_diff_rank): every candidate's global rank is the number of
 // candidates ordered before it, counted in 256-candidate slices by many small
 // workgroups; ranks below k are written out (k_diff_write).
+// A batch (mag_diff_batch: one baseline against several candidates, the
+// sweep of Section 6.1's per-case comparisons) runs the same stages for up to
+// DIFF_BATCH candidates per launch, one candidate per blockIdx.z, with the
+// candidates' parameters in the kernel-argument segment.
 // Detection (Section 6.1) runs the same stages with k = the rows wanted: the
 // flagged keys (r >= threshold) are a prefix of the ranking, so the first
 // rows are the flagged ones; stage 1 also counts every flagged key and the
@@ -93,13 +97,47 @@ __device__ __forceinline__ void check_ascending(const DiffParams& p, int64_t na,
     if (bad) atomicOr(&p.status->err, ERR_KEYS);
 }
 
-__global__ __launch_bounds__(256) void k_diff_check(const DiffParams p)
+// the parameters of one comparison (blockIdx.z = 0), or of the candidate
+// blockIdx.z of a batch
+struct OneDiff {
+    DiffParams p;
+    __device__ __forceinline__ const DiffParams& get() const { return p; }
+    __host__ const DiffParams& get_host(int) const { return p; }
+};
+struct BatchDiff {
+    DiffParams p[DIFF_BATCH];
+    __device__ __forceinline__ const DiffParams& get() const { return p[blockIdx.z]; }
+    __host__ const DiffParams& get_host(int c) const { return p[c]; }
+};
+
+// counters of each candidate's status block cleared (batches only: a single
+// comparison clears its status with the attribution's init kernel)
+__global__ __launch_bounds__(64) void k_diff_init(const BatchDiff b, int n)
 {
+    const int c = threadIdx.x;
+    if (c < n) {
+        Status* st = b.p[c].status;
+        st->err = 0u;
+        st->n_cand = 0u;
+        st->n_join = 0u;
+        st->n_flag = 0u;
+        st->n_waste = 0u;
+        st->diff_na = 0u;
+        st->diff_nb = 0u;
+    }
+}
+
+template <class A>
+__global__ __launch_bounds__(256) void k_diff_check(const A a)
+{
+    const DiffParams& p = a.get();
     check_ascending(p, rows_a(p), rows_b(p));
 }
 
-__global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
+template <class A>
+__global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const A a)
 {
+    const DiffParams& p = a.get();
     __shared__ uint64_t bk[B_TILE];
     __shared__ double lr[JOIN_ROWS];
     __shared__ uint64_t lk[JOIN_ROWS];
@@ -191,8 +229,10 @@ __global__ __launch_bounds__(JOIN_ROWS) void k_diff_join(const DiffParams p)
 }
 
 // candidates [64 bx, 64 bx + 64) counted against the slice [256 by, 256 by + 256)
-__global__ __launch_bounds__(64) void k_diff_rank(const DiffParams p)
+template <class A>
+__global__ __launch_bounds__(64) void k_diff_rank(const A a)
 {
+    const DiffParams& p = a.get();
     __shared__ double tr[RANK_SLICE];
     __shared__ uint64_t tk[RANK_SLICE];
     const uint32_t nc = p.status->n_cand;
@@ -218,8 +258,10 @@ __global__ __launch_bounds__(64) void k_diff_rank(const DiffParams p)
     if (rank) atomicAdd(&p.cand_rank[c], rank);
 }
 
-__global__ __launch_bounds__(256) void k_diff_write(const DiffParams p)
+template <class A>
+__global__ __launch_bounds__(256) void k_diff_write(const A a)
 {
+    const DiffParams& p = a.get();
     const uint32_t nc = p.status->n_cand;
     const uint32_t c = blockIdx.x * blockDim.x + threadIdx.x;
     if (c >= nc) return;
@@ -246,24 +288,57 @@ int64_t diff_max_candidates(int64_t na, int64_t k)
     return min(na, groups * min(k, (int64_t)JOIN_ROWS));
 }
 
+namespace {
+
+// the stages of `n` comparisons that share table A (the single call: n = 1)
+template <class A>
+void launch_stages(const A& a, const DiffParams& p0, int n, hipStream_t stream)
+{
+    bool on_device = false;  // some sizes known on the device only
+    bool any_empty_b = false;
+    for (int c = 0; c < n; ++c) {
+        on_device |= a.get_host(c).na_dev || a.get_host(c).nb_dev;
+        any_empty_b |= (a.get_host(c).nb == 0);
+    }
+    if (!on_device && (p0.na == 0 || any_empty_b)) {
+        int64_t mx = p0.na;
+        for (int c = 0; c < n; ++c) mx = max(mx, a.get_host(c).nb);
+        const unsigned cb = (unsigned)max((int64_t)1, min((mx + 255) / 256, (int64_t)1024));
+        hipLaunchKernelGGL(k_diff_check<A>, dim3(cb, 1, n), dim3(256), 0, stream, a);
+    }
+    // an empty table B (known on the host) leaves no joined row: the join
+    // kernel then finds no partner for any row of A
+    if (p0.na > 0 && (on_device || n > 1 || p0.nb > 0)) {
+        const unsigned jb = (unsigned)((p0.na + JOIN_ROWS - 1) / JOIN_ROWS);
+        hipLaunchKernelGGL(k_diff_join<A>, dim3(jb, 1, n), dim3(JOIN_ROWS), 0, stream, a);
+        const int64_t mc = diff_max_candidates(p0.na, p0.k);
+        if (p0.k > 0 && mc > 0) {
+            const dim3 rg((unsigned)((mc + 63) / 64), (unsigned)((mc + RANK_SLICE - 1) / RANK_SLICE),
+                          n);
+            hipLaunchKernelGGL(k_diff_rank<A>, rg, dim3(64), 0, stream, a);
+            hipLaunchKernelGGL(k_diff_write<A>, dim3((unsigned)((mc + 255) / 256), 1, n), dim3(256),
+                               0, stream, a);
+        }
+    }
+}
+
+}  // namespace
+
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream)
 {
-    const bool on_device = p.na_dev || p.nb_dev;  // sizes known on the device only
-    if (!on_device && (p.na == 0 || p.nb == 0)) {
-        const int64_t mx = max(p.na, p.nb);
-        const unsigned cb = (unsigned)max((int64_t)1, min((mx + 255) / 256, (int64_t)1024));
-        hipLaunchKernelGGL(k_diff_check, dim3(cb), dim3(256), 0, stream, p);
-    }
-    if (on_device ? p.na > 0 : (p.na > 0 && p.nb > 0)) {
-        const unsigned jb = (unsigned)((p.na + JOIN_ROWS - 1) / JOIN_ROWS);
-        hipLaunchKernelGGL(k_diff_join, dim3(jb), dim3(JOIN_ROWS), 0, stream, p);
-        const int64_t mc = diff_max_candidates(p.na, p.k);
-        if (p.k > 0 && mc > 0) {
-            const dim3 rg((unsigned)((mc + 63) / 64), (unsigned)((mc + RANK_SLICE - 1) / RANK_SLICE));
-            hipLaunchKernelGGL(k_diff_rank, rg, dim3(64), 0, stream, p);
-            hipLaunchKernelGGL(k_diff_write, dim3((unsigned)((mc + 255) / 256)), dim3(256), 0,
-                               stream, p);
-        }
+    OneDiff a{p};
+    launch_stages(a, p, 1, stream);
+    return hipGetLastError();
+}
+
+hipError_t launch_diff_batch(const DiffParams* p, int n, hipStream_t stream)
+{
+    for (int c0 = 0; c0 < n; c0 += DIFF_BATCH) {
+        const int cnt = min(DIFF_BATCH, n - c0);
+        BatchDiff b{};
+        for (int c = 0; c < cnt; ++c) b.p[c] = p[c0 + c];
+        hipLaunchKernelGGL(k_diff_init, dim3(1), dim3(64), 0, stream, b, cnt);
+        launch_stages(b, p[c0], cnt, stream);
     }
     return hipGetLastError();
 }

@@ -282,6 +282,10 @@ hipError_t launch_counter(const CounterParams& p, hipStream_t stream, hipEvent_t
 hipError_t launch_counter_fold(const CounterParams& p, hipStream_t stream);
 hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream);
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream);
+// comparisons per launch of a batch (their parameters travel as kernel arguments)
+constexpr int DIFF_BATCH = 8;
+// n comparisons sharing table A (p[c].ka/sa/ca/na/na_dev and k equal for all c)
+hipError_t launch_diff_batch(const DiffParams* p, int n, hipStream_t stream);
 // upper bound of the diff's stage-1 candidates for n_keys_a rows and top k
 int64_t diff_max_candidates(int64_t na, int64_t k);
 

@@ -290,16 +290,71 @@ def test_workload_ab(cfg, k):
         _diff_and_compare(ra[5], rb[5], ra[1], rb[1], k, f"cfg{cfg} seed{seed}")
 
 
-def test_workload_multistream_100m():
-    A, B = synth.sides(3, 0)
-    ra = compare_attribution(A, label="cfg3 A")
-    rb = compare_attribution(B, label="cfg3 B")
-    _diff_and_compare(ra[5], rb[5], ra[1], rb[1], 100, "cfg3")
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_workload_multistream_100m(seed):
+    A, B = synth.sides(3, seed)
+    ra = compare_attribution(A, label=f"cfg3 A seed{seed}")
+    rb = compare_attribution(B, label=f"cfg3 B seed{seed}")
+    _diff_and_compare(ra[5], rb[5], ra[1], rb[1], 100, f"cfg3 seed{seed}")
 
 
 def test_workload_batched_sweep():
-    sides = synth.sides(4, 0, which=range(4))
+    """Baseline A against all eight candidates B1..B8: each candidate's
+    attribution against the oracle, each pair's top-100 by mag_diff, and the
+    eight rankings of one mag_diff_batch call against the oracle's."""
+    import paper_2512_08365_amd as mag
+    sides = synth.sides(4, 0)
+    assert len(sides) == 9
     base = compare_attribution(sides[0], label="cfg4 A")
+    dev_tabs, orc_tabs = [], []
     for b in range(1, len(sides)):
         rb = compare_attribution(sides[b], label=f"cfg4 B{b}")
         _diff_and_compare(base[5], rb[5], base[1], rb[1], 100, f"cfg4 B{b}")
+        dev_tabs.append(rb[5])
+        orc_tabs.append(rb[1])
+    got = mag.diff_batch(base[5], dev_tabs, 100)
+    assert len(got) == 8
+    for b, (d, og) in enumerate(zip(got, orc_tabs), start=1):
+        o = oracle.diff(base[1], og, 100)
+        label = f"cfg4 batch B{b}"
+        assert np.array_equal(d["key"].cpu().numpy().view(np.uint64), o["key"]), label
+        r = d["ratio"].cpu().numpy()
+        assert np.all(np.abs(r - o["ratio"]) <= 3e-9 * (1 + np.abs(o["ratio"]))), label
+        assert np.array_equal(d["count_a"].cpu().numpy(), o["count_a"]), label
+        assert np.array_equal(d["count_b"].cpu().numpy(), o["count_b"]), label
+        assert_energy_close(d["energy_a"].cpu().numpy(), o["energy_a"], label)
+        assert_energy_close(d["energy_b"].cpu().numpy(), o["energy_b"], label)
+        assert (d["n_only_a"], d["n_only_b"], d["n_join"]) == (o["n_only_a"], o["n_only_b"],
+                                                               o["n_join"]), label
+
+
+def test_diff_batch_matches_single_diffs():
+    """mag_diff_batch over more than one launch group (19 candidates), with
+    tables of different sizes, empty tables, k above the join and k = 0,
+    equals mag_diff candidate by candidate."""
+    import torch
+    import paper_2512_08365_amd as mag
+    rng = np.random.default_rng(11)
+
+    def table(n, vocab):
+        keys = np.sort(rng.choice(vocab, size=n, replace=False)).astype(np.uint64)
+        sums = rng.uniform(0.0, 10.0, n)
+        sums[rng.random(n) < 0.05] = 0.0
+        cnt = rng.integers(1, 50, n)
+        return {"keys": torch.from_numpy(keys.view(np.int64)).cuda(),
+                "sum": torch.from_numpy(sums).cuda(), "count": torch.from_numpy(cnt).cuda()}
+
+    vocab = np.unique(rng.integers(0, 2**63, 20000, dtype=np.int64).astype(np.uint64)
+                      | np.uint64(1 << 63))
+    a = table(3000, vocab)
+    bs = [table(int(n), vocab) for n in rng.integers(0, 6000, 17)] + [table(0, vocab),
+                                                                      table(1, vocab)]
+    for k in (0, 1, 37, 5000):
+        got = mag.diff_batch(a, bs, k)
+        for c, b in enumerate(bs):
+            want = mag.diff(a, b, k)
+            for f in ("key", "ratio", "energy_a", "energy_b", "count_a", "count_b"):
+                assert torch.equal(got[c][f], want[f]), (k, c, f)
+            for f in ("n_only_a", "n_only_b", "n_join"):
+                assert got[c][f] == want[f], (k, c, f)
+    assert mag.diff_batch(a, [], 10) == []

@@ -229,45 +229,86 @@ def test_stream_errors():
 
 
 @pytest.mark.slow
-def test_long_run_workload_streamed_in_32M_chunks():
-    """One side of the hour-long trace (360,000,000 samples at 100 kHz,
-    50,000,000 sequential intervals): streamed in 32,000,000-sample chunks it
-    equals the one-shot call bit for bit, and sampled intervals equal the
-    oracle's (sequential intervals do not interact, so a subset of them can be
-    checked on its own)."""
+def test_long_run_workload_both_sides_streamed_in_32M_chunks():
+    """The hour-long workload (360,000,000 samples at 100 kHz, 50,000,000
+    sequential intervals, 20,000 Zipf(1.05) keys), both sides drawn with
+    independent seeds.  Side A is pushed from device memory and side B from
+    pinned host memory (double-buffered copies on a copy stream), both in
+    32,000,000-sample chunks; side A also equals the one-shot call bit for bit.
+    Every one of the 50,000,000 energies and sample indices of each side is
+    compared with the oracle run on the whole, unchunked trace, the per-key
+    rows with the oracle's grouping of the oracle's energies, and the top-100
+    diff with the oracle's."""
     import torch
     import oracle
-    c = synth.trace(5, 0, 0)
+    import oracle_par
+    sides = synth.sides(5, 0)
+    tables, otables = [], []
+    for si, c in enumerate(sides):
+        label = "AB"[si]
+        n = c["t"].shape[0]
+        m = c["s"].shape[0]
+        log(f"[case] long-run side {label} n={n} m={m}")
+        sizes = [32_000_000] * (n // 32_000_000)
+        if n % 32_000_000:
+            sizes.append(n % 32_000_000)
+        off = [int(x) for x in c["offsets"]]
+        if si == 0:
+            d = to_gpu(c)
+            ref = _one_shot(d, off)
+            got = _streamed(d, off, sizes)
+            _assert_same(got, ref, "long-run A one-shot vs chunked")
+            del ref
+        else:
+            d = {"s": torch.from_numpy(c["s"]).cuda(), "e": torch.from_numpy(c["e"]).cuda(),
+                 "key": torch.from_numpy(c["key"].view(np.int64)).cuda()}
+            got = _streamed_host(c, d, off, sizes)
+        gi, gk, summ = _np(got)
+        tables.append(got[1])
+        del d
+        torch.cuda.empty_cache()
+        log(f"[oracle] long-run side {label}: whole trace, {oracle_par.workers()} interval slices")
+        r = oracle_par.attribute_one_stream(c["t"], c["P"], c["s"], c["e"])
+        assert np.array_equal(gi["start_idx"], r["start_idx"]), f"{label}: start_idx"
+        assert np.array_equal(gi["end_idx"], r["end_idx"]), f"{label}: end_idx"
+        assert_energy_close(gi["energy"], r["energy"], f"long-run {label}: energies")
+        W = r["trace_energy"]
+        assert abs(summ["trace_energy"] - W) <= 1e-12 * W
+        assert abs(summ["attributed_energy"] - r["attributed_energy"]) <= 1e-9 * W
+        assert abs(summ["idle_energy"] - r["idle_energy"]) <= 1e-9 * W
+        assert summ["n_clipped"] == r["n_clipped"]
+        g = oracle_par.groupby(c["key"], r["energy"])
+        otables.append(g)
+        assert np.array_equal(gk["keys"].view(np.uint64), g["keys"]), f"{label}: keys"
+        assert np.array_equal(gk["count"], g["count"]), f"{label}: counts"
+        assert_energy_close(gk["sum"], g["sum"], f"long-run {label}: key sums")
+        second = g["m2"] + g["sum"] ** 2 / np.maximum(g["count"], 1)
+        assert np.all(np.abs(gk["m2"] - g["m2"]) <= 1e-9 * second), f"{label}: m2"
+        del got, gi, r
+    import paper_2512_08365_amd as mag
+    d = mag.diff(tables[0], tables[1], 100)
+    o = oracle.diff(otables[0], otables[1], 100)
+    log(f"[diff] long-run: joined={o['n_join']} margin={o['margin']:.3g}")
+    assert o["margin"] > 1e-8, "near-tied ratios in the long-run workload"
+    assert np.array_equal(d["key"].cpu().numpy().view(np.uint64), o["key"])
+    r_ = d["ratio"].cpu().numpy()
+    assert np.all(np.abs(r_ - o["ratio"]) <= 3e-9 * (1 + np.abs(o["ratio"])))
+    assert np.array_equal(d["count_a"].cpu().numpy(), o["count_a"])
+    assert np.array_equal(d["count_b"].cpu().numpy(), o["count_b"])
+    assert (d["n_only_a"], d["n_only_b"], d["n_join"]) == (o["n_only_a"], o["n_only_b"], o["n_join"])
+
+
+def _streamed_host(c, d, off, sizes):
+    """Chunks pushed from pinned host memory through the library's copy stream."""
+    import torch
+    import paper_2512_08365_amd as mag
     n = c["t"].shape[0]
-    m = c["s"].shape[0]
-    log(f"[case] long-run trace n={n} m={m}")
-    d = to_gpu(c)
-    off = [int(x) for x in c["offsets"]]
-    ref = _one_shot(d, off)
-    sizes = [32_000_000] * (n // 32_000_000)
-    if n % 32_000_000:
-        sizes.append(n % 32_000_000)
-    got = _streamed(d, off, sizes)
-    _assert_same(got, ref, "long-run")
-    gi, gk, summ = _np(got)
-    del d, ref, got
-    torch.cuda.empty_cache()
-    # grouping of 50M intervals (chunks larger than one batch of loads per
-    # thread: the two-pass per-key path) against the oracle's grouping of the
-    # same energies
-    g = oracle.groupby(c["key"], gi["energy"])
-    assert np.array_equal(gk["keys"].view(np.uint64), g["keys"])
-    assert np.array_equal(gk["count"], g["count"])
-    assert_energy_close(gk["sum"], g["sum"], "long-run key sums")
-    second = g["m2"] + g["sum"] ** 2 / np.maximum(g["count"], 1)
-    assert np.all(np.abs(gk["m2"] - g["m2"]) <= 1e-9 * second)
-    rng = np.random.default_rng(0)
-    pick = np.sort(rng.choice(m, 20000, replace=False))
-    pick = np.concatenate([[0, 1, m - 2, m - 1], pick])
-    pick = np.unique(pick)
-    r = oracle.attribute(c["t"], c["P"], c["s"][pick], c["e"][pick], np.array([0, pick.size]),
-                         equal_split=True)
-    assert np.array_equal(gi["start_idx"][pick], r["start_idx"])
-    assert np.array_equal(gi["end_idx"][pick], r["end_idx"])
-    assert_energy_close(gi["energy"][pick], r["energy"], "long-run sampled energies")
-    assert abs(summ["trace_energy"] - r["trace_energy"]) <= 1e-12 * r["trace_energy"]
+    t_h = torch.from_numpy(c["t"]).pin_memory()
+    P_h = torch.from_numpy(c["P"]).pin_memory()
+    st = mag.Stream(n, d["s"], d["e"], d["key"], n_streams=len(off) - 1, stream_offsets=off,
+                    host_chunk=max(sizes))
+    pos = 0
+    for k in sizes:
+        st.push_host(t_h[pos:pos + k], P_h[pos:pos + k])
+        pos += k
+    return st.end()

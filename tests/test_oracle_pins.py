@@ -10,6 +10,8 @@ the relative difference, a wrong tie order, a wrong M2.
 from fractions import Fraction
 import os
 
+import math
+
 import numpy as np
 import pytest
 
@@ -370,6 +372,68 @@ def test_topk_order_and_join_counts():
         assert np.array_equal(d["ratio"], np.array([r for r, _ in rows]))
         assert d["n_only_a"] == len(set(ia) - set(ib))
         assert d["n_only_b"] == len(set(ib) - set(ia))
+
+
+def _margin_brute(ka, sa, kb, sb, k):
+    """Smallest gap r_p - r_{p+1} between adjacent rows among the first k+1
+    rows of the full ranking (by sorting every joined key); a pair of equal
+    infinite ratios (both baselines zero) has no numeric gap and is skipped;
+    infinity when no pair is compared."""
+    ib = {x: i for i, x in enumerate(kb.tolist())}
+    rows = []
+    for i, x in enumerate(ka.tolist()):
+        if x in ib:
+            a, b = float(sa[i]), float(sb[ib[x]])
+            r = (b - a) / a if a != 0.0 else (math.inf if b > 0.0 else 0.0)
+            rows.append((r, x))
+    rows.sort(key=lambda q: (-q[0], q[1]))
+    gaps = [rows[u][0] - rows[u + 1][0] for u in range(min(k, len(rows) - 1))]
+    gaps = [g for g in gaps if not math.isnan(g)]
+    return min(gaps) if gaps else math.inf
+
+
+def test_separation_margin_by_brute_force():
+    """The margin guards every top-k parity assertion: it must be the smallest
+    adjacent gap over exactly the first k+1 ranked rows."""
+    rng = np.random.default_rng(31)
+    ka = np.sort(rng.choice(2**40, 400, replace=False)).astype(np.uint64)
+    kb = np.unique(np.concatenate([ka[50:], rng.choice(2**40, 40).astype(np.uint64)]))
+    sa = rng.uniform(1, 100, ka.shape[0])
+    sa[:10] = 0.0  # zero baselines: ratios +inf (or 0) on the joined ones
+    sb = rng.uniform(1, 100, kb.shape[0])
+    sb[::17] = 0.0
+    ca = np.ones(ka.shape[0], np.int64)
+    cb = np.ones(kb.shape[0], np.int64)
+    nj = len(set(ka.tolist()) & set(kb.tolist()))
+    for k in (0, 1, 2, 7, 100, nj - 1, nj, nj + 25):
+        d = oracle.diff({"keys": ka, "sum": sa, "count": ca}, {"keys": kb, "sum": sb, "count": cb}, k)
+        assert d["margin"] == _margin_brute(ka, sa, kb, sb, k), k
+    # quantised ratios give exact ties: a zero margin once a tie is inside
+    sbq = np.array([sa[np.searchsorted(ka, x)] * (1 + rng.integers(-3, 4) / 4.0)
+                    if x in set(ka.tolist()) and sa[np.searchsorted(ka, x)] > 0 else 5.0
+                    for x in kb.tolist()])
+    for k in (3, 50, nj + 1):
+        d = oracle.diff({"keys": ka, "sum": sa, "count": ca}, {"keys": kb, "sum": sbq, "count": cb},
+                        k)
+        assert d["margin"] == _margin_brute(ka, sa, kb, sbq, k) == 0.0, k
+
+
+def test_separation_margin_worked_example():
+    """Ratios 3, 2.5, 2.25, 2, 1.999 on five keys (E_A = 1, E_B = 1 + r): the
+    gaps are 0.5, 0.25, 0.25, 0.001; only the first k+1 rows count."""
+    ka = np.array([10, 20, 30, 40, 50], np.uint64)
+    sa = np.ones(5)
+    sb = 1.0 + np.array([2.0, 1.999, 3.0, 2.25, 2.5])  # r of keys 10, 20, 30, 40, 50
+    c = np.ones(5, np.int64)
+    want = {0: math.inf, 1: 0.5, 2: 0.25, 3: 0.25, 4: 1.0 - 0.999, 5: 1.0 - 0.999, 9: 1.0 - 0.999}
+    for k, m in want.items():
+        d = oracle.diff({"keys": ka, "sum": sa, "count": c}, {"keys": ka, "sum": sb, "count": c}, k)
+        assert d["key"].tolist() == [30, 50, 40, 10, 20][:k], k
+        assert math.isclose(d["margin"], m, rel_tol=1e-12) or d["margin"] == m, (k, d["margin"])
+    # one joined key, or none: no pair, infinite margin
+    d = oracle.diff({"keys": ka[:1], "sum": sa[:1], "count": c[:1]},
+                    {"keys": ka[:1], "sum": sb[:1], "count": c[:1]}, 10)
+    assert d["margin"] == math.inf
 
 
 # ---------------------------------------------------------------------------
