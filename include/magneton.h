@@ -235,6 +235,32 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
                   size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * mag_attribute_static -- mag_attribute for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation): the same computation and results, with the
+ * workspace replaced by a scratch array that the library holds in device
+ * memory, MAG_STATIC_SCRATCH_BYTES (64 MiB) per GPU, for the life of the
+ * process.  The call allocates nothing: no hipMalloc / hipFree, no pinned
+ * host buffer, no events; the caller still provides every input and output.
+ *   Sizes: those whose mag_attribute_workspace_size exceeds
+ *   MAG_STATIC_SCRATCH_BYTES are rejected with MAG_E_WORKSPACE before any
+ *   device work (for example 20,000,000 samples with 1,000,000 intervals and
+ *   2,048 keys need 23 MiB and fit).
+ *   opts->flags must not contain MAG_ASYNC or MAG_TIME_KERNELS (MAG_E_STATE).
+ *   Every call on one GPU shares that GPU's scratch and leaves its contents
+ *   behind (every call initializes what it reads): calls that overlap on one
+ *   GPU (other host threads, or work still running on another stream) race
+ *   and give unspecified results.
+ * Synchronizes `stream`; returns what mag_attribute returns.
+ */
+#define MAG_STATIC_SCRATCH_BYTES (64LL << 20)
+int mag_attribute_static(const double* timestamps, const float* power, int64_t n_samples,
+                         const double* starts, const double* ends, const uint64_t* op_keys,
+                         int64_t n_intervals, const mag_attr_opts* opts,
+                         mag_interval_out* per_interval, uint64_t* keys_out,
+                         mag_key_stats* per_key, mag_summary* summary, hipStream_t stream);
+
+/*
  * mag_attribute_finish -- complete a mag_attribute (or mag_attribute_counter)
  * call made with MAG_ASYNC.
  * The paper's comparison is between two systems running the same workload

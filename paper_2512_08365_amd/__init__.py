@@ -14,7 +14,7 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "attribute_counter", "diff", "diff_batch", "detect", "invariants",
+__all__ = ["MagnetonError", "attribute", "attribute_static", "attribute_counter", "diff", "diff_batch", "detect", "invariants",
            "match", "match_subgraphs", "Stream", "workspace_size",
            "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
@@ -217,6 +217,53 @@ def counter_workspace_size(n_samples: int, n_intervals: int, key_capacity: int =
     _check(_lib().mag_counter_workspace_size(n_samples, n_intervals, key_capacity, flags,
                                              ctypes.byref(b)))
     return int(b.value)
+
+
+def attribute_static(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
+                     equal_split: bool = True, validate: bool = True,
+                     key_capacity: int | None = None, out=None, key_out=None):
+    """attribute() through mag_attribute_static: the library's own scratch
+    array (MAG_STATIC_SCRATCH_BYTES per GPU) replaces the workspace and the
+    call allocates nothing.  `out` / `key_out` may hold preallocated result
+    tensors (energy, start_idx, end_idx / keys, sum, m2, count) so that this
+    function allocates nothing either; missing ones are allocated here."""
+    lib = _lib()
+    n = int(t.shape[0])
+    m = int(s.shape[0])
+    dev = t.device
+    flags = (EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE)
+    o, keep = _opts(n_streams, stream_offsets, flags)
+    group = keys is not None
+    cap = int(key_capacity) if key_capacity is not None else max(1, m)
+    out = dict(out or {})
+    for name, dt in (("energy", torch.float64), ("start_idx", torch.int64),
+                     ("end_idx", torch.int64)):
+        if out.get(name) is None:
+            out[name] = torch.empty(m, dtype=dt, device=dev)
+    pio = N.IntervalOut(_dev_ptr(out["energy"], torch.float64, "energy"),
+                        _dev_ptr(out["start_idx"], torch.int64, "start_idx"),
+                        _dev_ptr(out["end_idx"], torch.int64, "end_idx"))
+    tab = ks = None
+    if group:
+        tab = dict(key_out or {})
+        for name, dt in (("keys", torch.int64), ("sum", torch.float64), ("m2", torch.float64),
+                         ("count", torch.int64)):
+            if tab.get(name) is None:
+                tab[name] = torch.empty(cap, dtype=dt, device=dev)
+        ks = N.KeyStats(tab["sum"].data_ptr(), tab["m2"].data_ptr(), tab["count"].data_ptr(), cap,
+                        0, None)
+    summ = N.Summary()
+    _check(lib.mag_attribute_static(
+        _dev_ptr(t, torch.float64, "t"), _dev_ptr(P, torch.float32, "P"), n,
+        _dev_ptr(s, torch.float64, "s"), _dev_ptr(e, torch.float64, "e"),
+        _dev_ptr(keys, torch.int64, "keys") if group else None, m, ctypes.byref(o),
+        ctypes.byref(pio), tab["keys"].data_ptr() if group else None,
+        ctypes.byref(ks) if group else None, ctypes.byref(summ), _stream_handle(dev)))
+    per_key = _key_rows(tab, ks) if group else None
+    summary = {"trace_energy": summ.trace_energy, "idle_energy": summ.idle_energy,
+               "attributed_energy": summ.attributed_energy, "n_clipped": int(summ.n_clipped),
+               "n_keys": int(summ.n_keys)}
+    return out, per_key, summary
 
 
 def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None,

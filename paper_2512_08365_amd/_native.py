@@ -34,10 +34,12 @@ MAG_KEY_LATENCY = 0x10
 MAG_WASTE = 1
 MAG_TRADEOFF = 2
 MAG_MAX_STREAMS = 32
+MAG_STATIC_SCRATCH_BYTES = 64 << 20
 
 # every symbol include/magneton.h declares
 EXPORTED = (
-    "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_finish",
+    "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_static",
+    "mag_attribute_finish",
     "mag_counter_workspace_size", "mag_attribute_counter",
     "mag_diff_workspace_size", "mag_diff", "mag_diff_batch_workspace_size", "mag_diff_batch",
     "mag_detect_workspace_size", "mag_detect",
@@ -118,6 +120,9 @@ def load(path: str = LIB_PATH):
                                   P(IntervalOut), c_vp, P(KeyStats), P(Summary), c_vp,
                                   ctypes.c_size_t, c_vp]
     lib.mag_attribute.restype = ctypes.c_int
+    lib.mag_attribute_static.argtypes = [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),
+                                         P(IntervalOut), c_vp, P(KeyStats), P(Summary), c_vp]
+    lib.mag_attribute_static.restype = ctypes.c_int
     lib.mag_attribute_finish.argtypes = [c_vp, P(KeyStats), P(Summary), c_vp]
     lib.mag_attribute_finish.restype = ctypes.c_int
     lib.mag_counter_workspace_size.argtypes = [c_i64, c_i64, c_i64, ctypes.c_uint32,

@@ -6,6 +6,7 @@
 
 #include <algorithm>
 #include <memory>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -650,18 +651,18 @@ int mag_attribute_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t
     return MAG_OK;
 }
 
-int mag_attribute(const double* timestamps, const float* power, int64_t n_samples,
-                  const double* starts, const double* ends, const uint64_t* op_keys,
-                  int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
-                  uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary, void* workspace,
-                  size_t workspace_bytes, hipStream_t stream)
+}  // extern "C"
+
+namespace {
+
+// mag_attribute and its allocation-free variant: with no_alloc the status
+// block is read back through a plain host copy (no pinned buffer, no events)
+int attribute_impl(const double* timestamps, const float* power, int64_t n_samples,
+                   const double* starts, const double* ends, const uint64_t* op_keys,
+                   int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
+                   uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary,
+                   void* workspace, size_t workspace_bytes, hipStream_t stream, bool no_alloc)
 {
-    g_last_error[0] = 0;
-    if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
-    if (!aligned(timestamps, 8) || !aligned(power, 4))
-        return fail(MAG_E_ALIGN, "input array not aligned to its element size");
-    if (unfinished(workspace))
-        return fail(MAG_E_STATE, "an asynchronous call on this workspace is not finished");
     int rc;
     if (per_key && (rc = check_key_outputs(keys_out, per_key, opts ? opts->flags : 0u)) != MAG_OK)
         return rc;
@@ -674,7 +675,7 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
     const int64_t NT = job.pl.NT;
     // timing (MAG_TIME_KERNELS): events 1 and 2 travel with the tile kernel's
     // dispatch, event 3 follows the call's last kernel
-    EventTimer timer((job.flags & MAG_TIME_KERNELS) != 0, stream, workspace);
+    EventTimer timer(!no_alloc && (job.flags & MAG_TIME_KERNELS) != 0, stream, workspace);
     if ((e = mag::launch_init(job.w.status, job.w.cnt_fin, (int64_t)job.pl.S * (NT + 1),
                               timestamps, n_samples, stream)) != hipSuccess)
         return hip_fail(e, "init");
@@ -689,6 +690,16 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         return hip_fail(e, "intervals_ready event");
     if ((e = job.grouping(keys_out, per_key)) != hipSuccess) return hip_fail(e, "group-by");
     timer.mark(3);
+    if (no_alloc) {
+        mag::Status st;
+        if ((e = hipMemcpyAsync(&st, job.w.status, sizeof(mag::Status), hipMemcpyDeviceToHost,
+                                stream)) != hipSuccess)
+            return hip_fail(e, "status copy");
+        if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
+        rc = interpret_status(st, per_key, summary);
+        if (summary) summary->tile_kernel_ms = summary->device_ms = 0.0;
+        return rc;
+    }
     if (job.flags & MAG_ASYNC)
         // results, errors and timings come from mag_attribute_finish; the status
         // block is copied to pinned host memory now, so that finishing needs
@@ -700,6 +711,87 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
         summary->device_ms = timer.ms(1, 3);
     }
     return rc;
+}
+
+// The allocation-free entry point's scratch memory: one copy per GPU, in the
+// library's code object, held until the process ends.  Host code never passes
+// this symbol itself to a kernel (in host code it names a host-side stand-in):
+// the device address of each GPU's copy is looked up once per device with
+// that device current, and only that address is used.
+constexpr size_t STATIC_SCRATCH_BYTES = (size_t)MAG_STATIC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[STATIC_SCRATCH_BYTES];
+
+constexpr int SCRATCH_DEVICES = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_addr[SCRATCH_DEVICES] = {};
+
+int scratch_address(void** out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= SCRATCH_DEVICES) return fail(MAG_E_STATE, "device index out of range");
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_addr[dev]) {
+        void* p = nullptr;
+        if ((e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) != hipSuccess)
+            return hip_fail(e, "scratch address");
+        if (!p || !aligned(p, 256)) return fail(MAG_E_STATE, "scratch address not 256-byte aligned");
+        g_scratch_addr[dev] = p;
+    }
+    *out = g_scratch_addr[dev];
+    return MAG_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mag_attribute(const double* timestamps, const float* power, int64_t n_samples,
+                  const double* starts, const double* ends, const uint64_t* op_keys,
+                  int64_t n_intervals, const mag_attr_opts* opts, mag_interval_out* per_interval,
+                  uint64_t* keys_out, mag_key_stats* per_key, mag_summary* summary, void* workspace,
+                  size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
+    if (!aligned(timestamps, 8) || !aligned(power, 4))
+        return fail(MAG_E_ALIGN, "input array not aligned to its element size");
+    if (unfinished(workspace))
+        return fail(MAG_E_STATE, "an asynchronous call on this workspace is not finished");
+    return attribute_impl(timestamps, power, n_samples, starts, ends, op_keys, n_intervals, opts,
+                          per_interval, keys_out, per_key, summary, workspace, workspace_bytes,
+                          stream, false);
+}
+
+int mag_attribute_static(const double* timestamps, const float* power, int64_t n_samples,
+                         const double* starts, const double* ends, const uint64_t* op_keys,
+                         int64_t n_intervals, const mag_attr_opts* opts,
+                         mag_interval_out* per_interval, uint64_t* keys_out,
+                         mag_key_stats* per_key, mag_summary* summary, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
+    if (!aligned(timestamps, 8) || !aligned(power, 4))
+        return fail(MAG_E_ALIGN, "input array not aligned to its element size");
+    if (opts && (opts->flags & (MAG_ASYNC | MAG_TIME_KERNELS)))
+        return fail(MAG_E_STATE, "MAG_ASYNC and MAG_TIME_KERNELS need host resources: not "
+                                 "accepted by the allocation-free entry point");
+    size_t need = 0;
+    int rc = mag_attribute_workspace_size(n_samples, n_intervals,
+                                          per_key ? per_key->capacity : 0, opts, &need);
+    if (rc != MAG_OK) return rc;
+    if (need > STATIC_SCRATCH_BYTES) {
+        snprintf(g_last_error, sizeof(g_last_error),
+                 "these sizes need %zu bytes of scratch; the allocation-free entry point has %zu",
+                 need, STATIC_SCRATCH_BYTES);
+        return MAG_E_WORKSPACE;
+    }
+    void* ws = nullptr;
+    if ((rc = scratch_address(&ws)) != MAG_OK) return rc;
+    return attribute_impl(timestamps, power, n_samples, starts, ends, op_keys, n_intervals, opts,
+                          per_interval, keys_out, per_key, summary, ws, STATIC_SCRATCH_BYTES,
+                          stream, true);
 }
 
 int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,
