@@ -12,8 +12,10 @@ stream (default priority) that waits for A's per-interval outputs (the
 does, and A's tile kernel has the device to itself.  Both attributions are
 enqueued asynchronously and leave their key counts on the device; the diff is
 enqueued behind both and its synchronization is the step's only host wait.
-Side A's tile kernel is timed with HIP events carried on its dispatch in every
-timed step; side B runs untimed.  Inputs are synthetic, seeded and resident in
+B's key map (distinct keys, ids, ranks: it depends on the keys only) is
+built on a third stream while A's trace is integrated.  Side A's tile kernel
+is timed with HIP events carried on its dispatch in every timed step; side B
+runs untimed.  Inputs are synthetic, seeded and resident in
 HBM before timing.
 
 --workload 1/2/3/4/5 times the other workloads the same way (2 and 4 fit in
@@ -133,7 +135,8 @@ def summarize_counters(tile_fetch, tile_write, copy_fetch, copy_write, copy_kern
 class Side:
     """Device copies of one side plus preallocated outputs and workspace."""
 
-    def __init__(self, c, lib, N, torch, k_cap, timed=True, ready_event=None):
+    def __init__(self, c, lib, N, torch, k_cap, timed=True, ready_event=None, tiles_wait=None,
+                 tiles_done=None, key_plan=False):
         import numpy as np
         self.n = int(c["t"].shape[0])
         self.m = int(c["s"].shape[0])
@@ -154,8 +157,20 @@ class Side:
         self.k_cap = k_cap
         self.offs = (ctypes.c_int64 * len(self.off))(*self.off)
         flags = N.MAG_EQUAL_SPLIT | N.MAG_ASYNC | (N.MAG_TIME_KERNELS if timed else 0)
+        self.plan = None
+        if key_plan:
+            # the key map is built on its own stream (build_plan), early in the
+            # step, and the grouping waits for it
+            b = ctypes.c_size_t(0)
+            assert lib.mag_key_plan_size(self.m, k_cap, ctypes.byref(b)) == 0
+            self.plan_buf = torch.empty(int(b.value), dtype=torch.uint8, device=dev)
+            self.plan_ready = torch.cuda.Event()
+            self.plan_ready.record()
+            self.plan = N.KeyPlan(self.plan_buf.data_ptr(), self.plan_buf.numel(), 0, 0,
+                                  ctypes.c_void_p(self.plan_ready.cuda_event))
         self.opts = N.AttrOpts(len(self.off) - 1, flags, ctypes.cast(self.offs, ctypes.c_void_p),
-                               ready_event)
+                               ready_event, ctypes.pointer(self.plan) if self.plan else None,
+                               tiles_wait, tiles_done)
         b = ctypes.c_size_t(0)
         rc = lib.mag_attribute_workspace_size(self.n, self.m, k_cap, ctypes.byref(self.opts),
                                               ctypes.byref(b))
@@ -170,6 +185,13 @@ class Side:
         self.ks_dev = N.KeyStats(self.ksum.data_ptr(), self.km2.data_ptr(), self.kcnt.data_ptr(),
                                  k_cap, -1, None, self.nkd.data_ptr())
         self.summ = N.Summary()
+
+    def build_plan(self, lib, stream):
+        """Enqueue this side's key map (mag_key_plan_build) on `stream`."""
+        rc = lib.mag_key_plan_build(self.key.data_ptr(), self.m, self.k_cap,
+                                    ctypes.byref(self.plan), stream)
+        if rc != 0:
+            raise RuntimeError(f"mag_key_plan_build failed {rc}: {lib.mag_last_error().decode()}")
 
     def attribute(self, lib, stream):
         """Enqueue this side's attribution (MAG_ASYNC: returns at once)."""
@@ -387,6 +409,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", type=int, default=WORKLOAD, choices=[1, 2, 3, 4, 5],
                     help="workload to time (default 3, the multi-stream 100M-sample trace)")
+    ap.add_argument("--timed-side", choices=["a", "b", "none"], default="a",
+                    help="which side's tile kernel carries the HIP timing events")
     ap.add_argument("--end-to-end", action="store_true",
                     help="workload 5 only: push the chunks from pinned host memory")
     ap.add_argument("--subgraphs", action="store_true",
@@ -524,14 +548,18 @@ def ab_bench(args, torch, mag, lib, N, synth):
     top = TOPK[cfg]
     s1 = torch.cuda.current_stream()
     s2 = torch.cuda.Stream()  # default priority
-    a_ready = torch.cuda.Event()
-    a_ready.record(s1)  # creates the HIP event
-    b_done = torch.cuda.Event()
-    sa = Side(A, lib, N, torch, k_cap, ready_event=ctypes.c_void_p(a_ready.cuda_event))
-    sb = Side(B, lib, N, torch, k_cap, timed=False)
+    a_tiles = torch.cuda.Event()
+    a_tiles.record(s1)  # creates the HIP event
+    a_done = torch.cuda.Event()
+    sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
+              tiles_done=ctypes.c_void_p(a_tiles.cuda_event))
+    sb = Side(B, lib, N, torch, k_cap, timed=args.timed_side == "b",
+              tiles_wait=ctypes.c_void_p(a_tiles.cuda_event), key_plan=True)
+    s3 = torch.cuda.Stream()  # default priority: B's key map
     torch.cuda.synchronize()
     stream = ctypes.c_void_p(s1.cuda_stream)
     stream_b = ctypes.c_void_p(s2.cuda_stream)
+    stream_k = ctypes.c_void_p(s3.cuda_stream)
     d_out = {k: torch.empty(top, dtype=dt, device="cuda") for k, dt in
              (("key", torch.int64), ("ratio", torch.float64), ("ea", torch.float64),
               ("eb", torch.float64), ("ca", torch.int64), ("cb", torch.int64))}
@@ -544,23 +572,28 @@ def ab_bench(args, torch, mag, lib, N, synth):
     tile_ms = []
 
     def step(record):
-        # B starts once A's per-interval outputs are complete; the diff reads
-        # both key counts on the device, behind both attributions; the diff's
-        # synchronization is the step's one host wait
+        # B's trace integration starts once A's is done (the two bandwidth-bound
+        # passes run back to back, each with the device to itself), everything
+        # else of each side overlaps the other; the diff reads both key counts
+        # on the device, behind both attributions, on B's stream (A finishes
+        # first); its synchronization is the step's one host wait
         sa.attribute(lib, stream)
-        s2.wait_event(a_ready)
+        a_done.record(s1)
+        # B's key map depends on B's keys only: built on a third stream while
+        # A's trace is integrated, so B's grouping after its own trace
+        # integration only aggregates
+        sb.build_plan(lib, stream_k)
         sb.attribute(lib, stream_b)
-        b_done.record(s2)
-        s1.wait_event(b_done)
+        s2.wait_event(a_done)
         rc = lib.mag_diff(sa.kout.data_ptr(), ctypes.byref(sa.ks_dev), sb.kout.data_ptr(),
                           ctypes.byref(sb.ks_dev), top, ctypes.byref(ro), d_ws.data_ptr(),
-                          d_ws.numel(), stream)
+                          d_ws.numel(), stream_b)
         if rc != 0:
             raise RuntimeError(f"mag_diff failed {rc}: {lib.mag_last_error().decode()}")
         ta = sa.finish(lib, stream)
-        sb.finish(lib, stream_b)
-        if record:
-            tile_ms.append(ta)
+        tb = sb.finish(lib, stream_b)
+        if record and args.timed_side != "none":
+            tile_ms.append(ta if args.timed_side == "a" else tb)
 
     flush = None
     if cfg == 2:
@@ -592,7 +625,9 @@ def ab_bench(args, torch, mag, lib, N, synth):
     sec_per_step = dt / args.steps
     log(f"[bench] {args.steps} steps in {dt:.4f} s -> {sec_per_step * 1e3:.4f} ms/step; "
         f"keys A={sa.ks.n_keys} B={sb.ks.n_keys} joined={ro.n_join}")
-    extra = {"timing": timing, "roofline": tile_roofline(tile_ms, sh["n"], sh["m"])}
+    extra = {"timing": timing}
+    if tile_ms:
+        extra["roofline"] = tile_roofline(tile_ms, sh["n"], sh["m"])
     res = result_line(args, cfg, sh, 2, sec_per_step, extra)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle on both sides ...")
@@ -602,8 +637,8 @@ def ab_bench(args, torch, mag, lib, N, synth):
 
 def sweep_bench(args, torch, mag, lib, N, synth):
     """One step = 9 attributions (baseline + 8 candidates, alternating two
-    streams, each tile kernel behind the previous side's per-interval outputs)
-    and one batched top-100 diff of the 8 candidates against the baseline."""
+    streams, each trace integration behind the previous side's) and one
+    batched top-100 diff of the 8 candidates against the baseline."""
     cfg = 4
     t0 = time.perf_counter()
     sides_h = synth.sides(cfg, args.seed)
@@ -612,12 +647,15 @@ def sweep_bench(args, torch, mag, lib, N, synth):
     k_cap = 4096
     top = TOPK[cfg]
     s = [torch.cuda.current_stream(), torch.cuda.Stream()]
-    ready = [torch.cuda.Event() for _ in sides_h]
-    for ev in ready:
-        ev.record(s[0])
+    tiles = [torch.cuda.Event() for _ in sides_h]
+    for ev in tiles:
+        ev.record(s[0])  # creates the HIP events
     last = torch.cuda.Event()
+    # each side's trace integration waits for the previous side's: the
+    # bandwidth-bound passes run back to back, the rest overlaps them
     sides = [Side(c, lib, N, torch, k_cap, timed=(i == 0),
-                  ready_event=ctypes.c_void_p(ready[i].cuda_event))
+                  tiles_wait=ctypes.c_void_p(tiles[i - 1].cuda_event) if i > 0 else None,
+                  tiles_done=ctypes.c_void_p(tiles[i].cuda_event))
              for i, c in enumerate(sides_h)]
     torch.cuda.synchronize()
     handles = [ctypes.c_void_p(x.cuda_stream) for x in s]
@@ -638,9 +676,6 @@ def sweep_bench(args, torch, mag, lib, N, synth):
 
     def step(record):
         for i, side in enumerate(sides):
-            st = s[i % 2]
-            if i > 0:
-                st.wait_event(ready[i - 1])
             side.attribute(lib, handles[i % 2])
         # the diff waits for every side's grouping: the sides on the second
         # stream are all behind this event

@@ -103,7 +103,47 @@ typedef struct mag_attr_opts {
                                     /* work on another stream (the other system's     */
                                     /* attribution, Section 3.2) can start while the  */
                                     /* grouping runs; the caller owns the event       */
+    const struct mag_key_plan* key_plan; /* mag_attribute only, may be NULL: host     */
+                                    /* struct of a key plan built by                  */
+                                    /* mag_key_plan_build for these op_keys (same     */
+                                    /* n_intervals and key capacity); the call then   */
+                                    /* groups with its key map instead of building    */
+                                    /* one, after waiting for key_plan->ready         */
+    hipEvent_t tiles_wait;          /* mag_attribute only, may be NULL: waited for on */
+                                    /* `stream` right before the power trace is       */
+                                    /* integrated (after the call's own set-up)       */
+    hipEvent_t tiles_done;          /* mag_attribute only, may be NULL: recorded on   */
+                                    /* `stream` right after the trace integration,    */
+                                    /* before the fix-ups and the grouping; with      */
+                                    /* tiles_wait it lets the bandwidth-bound passes  */
+                                    /* of two attributions run back to back while     */
+                                    /* the rest of each overlaps the other            */
 } mag_attr_opts;
+
+/*
+ * A key plan: the key map of a per-key grouping (the distinct operator keys,
+ * a dense id per key, each key's rank in ascending order, and every
+ * interval's id), which depends on the operator keys only, not on the power
+ * trace.  Built on its own (mag_key_plan_build) it can be made on another
+ * stream while the power trace is integrated, or once for several
+ * attributions of the same operator trace (Section 3.2 compares systems that
+ * run the same workload; Section 4.1 makes the operator the unit).
+ *   buffer        device memory, >= mag_key_plan_size(...) bytes, 256-byte
+ *                 aligned, caller-owned; holds the map until rebuilt
+ *   bytes         size of buffer
+ *   n_intervals, key_capacity   written by mag_key_plan_build; an attribution
+ *                 using the plan must pass the same values (else MAG_E_STATE)
+ *   ready         optional HIP event (caller-owned): recorded on the build's
+ *                 stream once the map is complete; an attribution using the
+ *                 plan waits for it on its own stream before grouping
+ */
+typedef struct mag_key_plan {
+    void* buffer;
+    size_t bytes;
+    int64_t n_intervals;
+    int64_t key_capacity;
+    hipEvent_t ready;
+} mag_key_plan;
 
 /* Per-interval outputs (device arrays of n_intervals entries; any may be NULL). */
 typedef struct mag_interval_out {
@@ -259,6 +299,20 @@ int mag_attribute_static(const double* timestamps, const float* power, int64_t n
                          int64_t n_intervals, const mag_attr_opts* opts,
                          mag_interval_out* per_interval, uint64_t* keys_out,
                          mag_key_stats* per_key, mag_summary* summary, hipStream_t stream);
+
+/*
+ * mag_key_plan_size -- device bytes of a key plan for n_intervals keys and a
+ * key capacity (>= 1).  Host only.  MAG_E_SIZE for a negative count or a
+ * capacity out of [1, MAG_MAX_KEYS].
+ * mag_key_plan_build -- build the key map of op_keys[n_intervals] (device,
+ * any uint64) into plan->buffer on `stream` (asynchronous; records
+ * plan->ready when given).  Distinct keys beyond the capacity are reported
+ * by the attribution that uses the plan (MAG_E_CAPACITY).  Errors:
+ * MAG_E_NULL, MAG_E_ALIGN, MAG_E_SIZE, MAG_E_WORKSPACE, MAG_E_HIP.
+ */
+int mag_key_plan_size(int64_t n_intervals, int64_t key_capacity, size_t* bytes);
+int mag_key_plan_build(const uint64_t* op_keys, int64_t n_intervals, int64_t key_capacity,
+                       mag_key_plan* plan, hipStream_t stream);
 
 /*
  * mag_attribute_finish -- complete a mag_attribute (or mag_attribute_counter)

@@ -14,7 +14,7 @@ import torch
 
 from . import _native as N
 
-__all__ = ["MagnetonError", "attribute", "attribute_static", "attribute_counter", "diff", "diff_batch", "detect", "invariants",
+__all__ = ["MagnetonError", "KeyPlan", "attribute", "attribute_static", "attribute_counter", "diff", "diff_batch", "detect", "invariants",
            "match", "match_subgraphs", "Stream", "workspace_size",
            "stream_workspace_size", "diff_workspace_size", "counter_workspace_size", "version", "EQUAL_SPLIT",
            "SKIP_VALIDATE"]
@@ -57,11 +57,16 @@ def _event_handle(ev):
     return ctypes.c_void_p(ev.cuda_event)
 
 
-def _opts(n_streams: int, stream_offsets, flags: int, intervals_ready=None):
+def _opts(n_streams: int, stream_offsets, flags: int, intervals_ready=None, key_plan=None,
+          tiles_wait=None, tiles_done=None):
     o = N.AttrOpts()
     o.n_streams = int(n_streams)
     o.flags = int(flags)
     o.intervals_ready = _event_handle(intervals_ready)
+    o.tiles_wait = _event_handle(tiles_wait)
+    o.tiles_done = _event_handle(tiles_done)
+    if key_plan is not None:
+        o.key_plan = ctypes.pointer(key_plan._kp)
     keep = None
     if stream_offsets is not None:
         keep = (ctypes.c_int64 * len(stream_offsets))(*[int(x) for x in stream_offsets])
@@ -82,8 +87,8 @@ def _dev_ptr(x, dtype, name):
 
 
 def workspace_size(n_samples: int, n_intervals: int, key_capacity: int = 0, n_streams: int = 1,
-                   stream_offsets=None, flags: int = EQUAL_SPLIT) -> int:
-    o, keep = _opts(n_streams, stream_offsets, flags)
+                   stream_offsets=None, flags: int = EQUAL_SPLIT, key_plan=None) -> int:
+    o, keep = _opts(n_streams, stream_offsets, flags, key_plan=key_plan)
     b = ctypes.c_size_t(0)
     _check(_lib().mag_attribute_workspace_size(n_samples, n_intervals, key_capacity,
                                                 ctypes.byref(o), ctypes.byref(b)))
@@ -143,13 +148,17 @@ class Pending:
 def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
               equal_split: bool = True, validate: bool = True, key_capacity: int | None = None,
               indices: bool = True, workspace=None, out=None, asynchronous: bool = False,
-              intervals_ready=None, latency: bool = False):
+              intervals_ready=None, latency: bool = False, key_plan=None, tiles_wait=None,
+              tiles_done=None):
     """Attribute the energy of a power trace to intervals and group it by key.
 
     t: float64 [n] timestamps (s), P: float32 [n] power (W), s/e: float64 [m]
     interval bounds, keys: int64 [m] (bits read as uint64) or None.
     intervals_ready: a torch.cuda.Event recorded on the current stream once the
     per-interval outputs are complete (before the grouping), or None.
+    key_plan: a KeyPlan of these keys (its key map is used instead of building
+    one; its capacity is the key capacity).  tiles_wait / tiles_done: events
+    waited for before / recorded after the trace integration.
     latency: also sum each key's interval durations (per_key["duration"]).
     Returns (per_interval, per_key, summary): dicts of tensors / numbers; with
     asynchronous=True a Pending whose finish() returns them once the work ran.
@@ -160,10 +169,14 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     dev = t.device
     flags = ((EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE) |
              (ASYNC if asynchronous else 0) | (KEY_LATENCY if latency and keys is not None else 0))
-    o, keep = _opts(n_streams, stream_offsets, flags, intervals_ready)
+    o, keep = _opts(n_streams, stream_offsets, flags, intervals_ready, key_plan, tiles_wait,
+                    tiles_done)
     group = keys is not None
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
-    ws_bytes = workspace_size(n, m, cap if group else 0, n_streams, stream_offsets, flags)
+    if key_plan is not None:
+        cap = key_plan.key_capacity
+    ws_bytes = workspace_size(n, m, cap if group else 0, n_streams, stream_offsets, flags,
+                              key_plan)
     if workspace is None or workspace.numel() < ws_bytes:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     out = out or {}
@@ -207,7 +220,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
 
     if asynchronous:
         # the inputs and the options stay referenced until finish()
-        return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys), sh)
+        return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys, key_plan), sh)
     return build()
 
 
@@ -217,6 +230,37 @@ def counter_workspace_size(n_samples: int, n_intervals: int, key_capacity: int =
     _check(_lib().mag_counter_workspace_size(n_samples, n_intervals, key_capacity, flags,
                                              ctypes.byref(b)))
     return int(b.value)
+
+
+class KeyPlan:
+    """The key map of a grouping (mag_key_plan_build): built from the
+    operator keys alone, on the current stream, so it can be made while the
+    power trace is integrated on another stream, or reused by several
+    attributions of the same keys.  `ready`: a torch.cuda.Event recorded when
+    the map is complete (attributions using the plan wait for it)."""
+
+    def __init__(self, keys, key_capacity: int | None = None, ready=None):
+        lib = _lib()
+        m = int(keys.shape[0])
+        cap = int(key_capacity) if key_capacity is not None else max(1, m)
+        b = ctypes.c_size_t(0)
+        _check(lib.mag_key_plan_size(m, cap, ctypes.byref(b)))
+        self.buffer = torch.empty(int(b.value), dtype=torch.uint8, device=keys.device)
+        self.keys = keys
+        self.ready = ready
+        self.key_capacity = cap
+        self._kp = N.KeyPlan(self.buffer.data_ptr(), self.buffer.numel(), 0, 0,
+                             _event_handle(ready) if ready is not None else None)
+        self.rebuild()
+
+    def rebuild(self):
+        """(Re)build the map from self.keys on the current stream."""
+        k = self.keys
+        if self.ready is not None:
+            self._kp.ready = _event_handle(self.ready)
+        _check(_lib().mag_key_plan_build(_dev_ptr(k, torch.int64, "keys"), int(k.shape[0]),
+                                         self.key_capacity, ctypes.byref(self._kp),
+                                         _stream_handle(k.device)))
 
 
 def attribute_static(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,

@@ -39,6 +39,7 @@ MAG_STATIC_SCRATCH_BYTES = 64 << 20
 # every symbol include/magneton.h declares
 EXPORTED = (
     "mag_attribute_workspace_size", "mag_attribute", "mag_attribute_static",
+    "mag_key_plan_size", "mag_key_plan_build",
     "mag_attribute_finish",
     "mag_counter_workspace_size", "mag_attribute_counter",
     "mag_diff_workspace_size", "mag_diff", "mag_diff_batch_workspace_size", "mag_diff_batch",
@@ -52,9 +53,15 @@ EXPORTED = (
 )
 
 
+class KeyPlan(ctypes.Structure):
+    _fields_ = [("buffer", c_vp), ("bytes", ctypes.c_size_t), ("n_intervals", c_i64),
+                ("key_capacity", c_i64), ("ready", c_vp)]
+
+
 class AttrOpts(ctypes.Structure):
     _fields_ = [("n_streams", ctypes.c_int32), ("flags", ctypes.c_uint32),
-                ("stream_offsets", c_vp), ("intervals_ready", c_vp)]
+                ("stream_offsets", c_vp), ("intervals_ready", c_vp),
+                ("key_plan", ctypes.POINTER(KeyPlan)), ("tiles_wait", c_vp), ("tiles_done", c_vp)]
 
 
 class IntervalOut(ctypes.Structure):
@@ -123,6 +130,10 @@ def load(path: str = LIB_PATH):
     lib.mag_attribute_static.argtypes = [c_vp, c_vp, c_i64, c_vp, c_vp, c_vp, c_i64, P(AttrOpts),
                                          P(IntervalOut), c_vp, P(KeyStats), P(Summary), c_vp]
     lib.mag_attribute_static.restype = ctypes.c_int
+    lib.mag_key_plan_size.argtypes = [c_i64, c_i64, P(ctypes.c_size_t)]
+    lib.mag_key_plan_size.restype = ctypes.c_int
+    lib.mag_key_plan_build.argtypes = [c_vp, c_i64, c_i64, P(KeyPlan), c_vp]
+    lib.mag_key_plan_build.restype = ctypes.c_int
     lib.mag_attribute_finish.argtypes = [c_vp, P(KeyStats), P(Summary), c_vp]
     lib.mag_attribute_finish.restype = ctypes.c_int
     lib.mag_counter_workspace_size.argtypes = [c_i64, c_i64, c_i64, ctypes.c_uint32,

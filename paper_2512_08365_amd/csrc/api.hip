@@ -61,10 +61,12 @@ struct Plan {
     int64_t chunk;
     bool staging;
     bool lat;  // per-key latency sums (MAG_KEY_LATENCY)
+    bool ext_keys;  // the key map comes from a key plan built beforehand
 };
 
 struct AttrWorkspace {
     mag::Status* status;
+    mag::Status* kstat;  // key state: status, or the key plan's header
     int64_t* cnt;
     int64_t* cnt_fin;
     double* head;
@@ -100,6 +102,7 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
     Carver c;
     c.base = static_cast<char*>(ws);
     w.status = c.take<mag::Status>(1);
+    w.kstat = w.status;
     w.cnt = c.take<int64_t>((size_t)pl.S * (pl.NT + 1));
     w.cnt_fin = c.take<int64_t>((size_t)pl.S * (pl.NT + 1));
     w.head = c.take<double>((size_t)pl.S * pl.NT);
@@ -120,6 +123,7 @@ size_t carve_counter(const Plan& pl, void* ws, AttrWorkspace& w)
     Carver c;
     c.base = static_cast<char*>(ws);
     w.status = c.take<mag::Status>(1);
+    w.kstat = w.status;
     w.part = c.take<double2>((size_t)pl.NT);
     w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
     carve_groupby(c, pl, w);
@@ -129,16 +133,33 @@ size_t carve_counter(const Plan& pl, void* ws, AttrWorkspace& w)
 void carve_groupby(Carver& c, const Plan& pl, AttrWorkspace& w)
 {
     if (pl.H > 0) {
-        w.table = c.take<unsigned long long>(2 * ((size_t)pl.H + 1));
-        w.slot = c.take<uint32_t>((size_t)std::max<int64_t>(pl.m, 1));
-        w.ukey = c.take<uint64_t>((size_t)pl.H + 1);
-        w.urank = c.take<uint32_t>((size_t)pl.H + 1);
+        if (!pl.ext_keys) {
+            w.table = c.take<unsigned long long>(2 * ((size_t)pl.H + 1));
+            w.slot = c.take<uint32_t>((size_t)std::max<int64_t>(pl.m, 1));
+            w.ukey = c.take<uint64_t>((size_t)pl.H + 1);
+            w.urank = c.take<uint32_t>((size_t)pl.H + 1);
+        }
         w.mean = c.take<double>((size_t)std::max<int64_t>(pl.cap, 1));
         w.pcnt = c.take<uint32_t>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.psum = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.pm2 = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         if (pl.lat) w.pdur = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
     }
+}
+
+// a key plan's buffer: header (a status block holding the key state), then
+// the key map of a grouping
+size_t carve_key_plan(int64_t m, int64_t cap, void* buf, AttrWorkspace& w)
+{
+    Carver c;
+    c.base = static_cast<char*>(buf);
+    const uint32_t H = hash_slots(cap);
+    w.kstat = c.take<mag::Status>(1);
+    w.table = c.take<unsigned long long>(2 * ((size_t)H + 1));
+    w.slot = c.take<uint32_t>((size_t)std::max<int64_t>(m, 1));
+    w.ukey = c.take<uint64_t>((size_t)H + 1);
+    w.urank = c.take<uint32_t>((size_t)H + 1);
+    return c.off;
 }
 
 int check_opts(const mag_attr_opts* opts, int64_t m, int* S, uint32_t* flags, mag::StreamSet* ss)
@@ -346,6 +367,7 @@ int plan_attribution(Plan& pl, int64_t n_samples, int64_t n_intervals, int64_t k
     pl.H = 0;
     pl.staging = streaming;
     pl.lat = key_capacity > 0 && (*flags & MAG_KEY_LATENCY) != 0;
+    pl.ext_keys = key_capacity > 0 && opts && opts->key_plan && !streaming;
     if (key_capacity > 0) plan_groupby(pl);
     return MAG_OK;
 }
@@ -436,6 +458,7 @@ struct Job {
     const double* e = nullptr;
     const uint64_t* keys = nullptr;
     const int32_t* reps = nullptr;  // counter mode: replays per window
+    hipEvent_t keys_ready = nullptr;  // a key plan's completion event (external key map)
     double* energy = nullptr;
     int64_t* start_idx = nullptr;
     int64_t* end_idx = nullptr;
@@ -502,7 +525,7 @@ struct Job {
         fp.status = w.status;
         fp.part = w.part;
         fp.validate = validate() ? 1 : 0;
-        if (grouping && pl.m > 0 && pl.H > 0) {
+        if (grouping && pl.m > 0 && pl.H > 0 && !pl.ext_keys) {
             fp.table = w.table;
             fp.H = pl.H;
             fp.urank = w.urank;
@@ -538,6 +561,7 @@ struct Job {
         gp.m2_out = per_key->m2;
         gp.count_out = per_key->count;
         gp.status = w.status;
+        gp.kstat = w.kstat;
         gp.n_keys_out = per_key->n_keys_device;
         if (pl.lat) {
             gp.s = s;
@@ -546,7 +570,12 @@ struct Job {
             gp.dur_out = per_key->duration;
             gp.pdur = w.pdur;
         }
-        return mag::launch_groupby(gp, stream);
+        if (!pl.ext_keys) return mag::launch_groupby(gp, stream);
+        if (keys_ready) {
+            const hipError_t e2 = hipStreamWaitEvent(stream, keys_ready, 0);
+            if (e2 != hipSuccess) return e2;
+        }
+        return mag::launch_aggregate(gp, stream);
     }
 
     // read the status block back and turn it into the call's result
@@ -597,6 +626,20 @@ int prepare(Job& job, int64_t n_samples, const double* starts, const double* end
         return MAG_E_WORKSPACE;
     }
     carve(job.pl, workspace, job.w);
+    if (job.pl.ext_keys) {
+        // the key map of a plan built beforehand for these keys and capacity
+        const mag_key_plan* kp = opts->key_plan;
+        if (!kp->buffer) return fail(MAG_E_NULL, "key_plan->buffer is NULL");
+        if (!aligned(kp->buffer, 256))
+            return fail(MAG_E_WORKSPACE, "key_plan->buffer must be 256-byte aligned");
+        if (kp->n_intervals != n_intervals || kp->key_capacity != key_capacity)
+            return fail(MAG_E_STATE, "key plan built for another interval count or key capacity");
+        AttrWorkspace pw{};
+        if (kp->bytes < carve_key_plan(n_intervals, key_capacity, nullptr, pw))
+            return fail(MAG_E_WORKSPACE, "key plan buffer too small");
+        carve_key_plan(n_intervals, key_capacity, kp->buffer, job.w);
+        job.keys_ready = kp->ready;
+    }
     job.s = starts;
     job.e = ends;
     job.keys = op_keys;
@@ -679,10 +722,14 @@ int attribute_impl(const double* timestamps, const float* power, int64_t n_sampl
     if ((e = mag::launch_init(job.w.status, job.w.cnt_fin, (int64_t)job.pl.S * (NT + 1),
                               timestamps, n_samples, stream)) != hipSuccess)
         return hip_fail(e, "init");
+    if (opts && opts->tiles_wait && (e = hipStreamWaitEvent(stream, opts->tiles_wait, 0)) != hipSuccess)
+        return hip_fail(e, "tiles_wait event");
     if ((e = job.run_tiles(timestamps, power, 0, 0, NT, n_samples - 1, NT,
                            timer.on ? timer.slot->ev[1] : nullptr,
                            timer.on ? timer.slot->ev[2] : nullptr)) != hipSuccess)
         return hip_fail(e, "tile kernel");
+    if (opts && opts->tiles_done && (e = hipEventRecord(opts->tiles_done, stream)) != hipSuccess)
+        return hip_fail(e, "tiles_done event");
     if ((e = job.fixups(n_samples, NT, per_key != nullptr)) != hipSuccess)
         return hip_fail(e, "fix-up kernels");
     if (opts && opts->intervals_ready &&
@@ -792,6 +839,56 @@ int mag_attribute_static(const double* timestamps, const float* power, int64_t n
     return attribute_impl(timestamps, power, n_samples, starts, ends, op_keys, n_intervals, opts,
                           per_interval, keys_out, per_key, summary, ws, STATIC_SCRATCH_BYTES,
                           stream, true);
+}
+
+int mag_key_plan_size(int64_t n_intervals, int64_t key_capacity, size_t* bytes)
+{
+    g_last_error[0] = 0;
+    if (!bytes) return fail(MAG_E_NULL, "bytes is NULL");
+    if (n_intervals < 0 || key_capacity < 1) return fail(MAG_E_SIZE, "n_intervals < 0 or key_capacity < 1");
+    if (key_capacity > MAG_MAX_KEYS) return fail(MAG_E_SIZE, "key_capacity exceeds MAG_MAX_KEYS");
+    AttrWorkspace w{};
+    *bytes = carve_key_plan(n_intervals, key_capacity, nullptr, w);
+    return MAG_OK;
+}
+
+int mag_key_plan_build(const uint64_t* op_keys, int64_t n_intervals, int64_t key_capacity,
+                       mag_key_plan* plan, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    if (!plan || !plan->buffer) return fail(MAG_E_NULL, "plan/plan->buffer is NULL");
+    if (n_intervals > 0 && !op_keys) return fail(MAG_E_NULL, "op_keys is NULL");
+    if (op_keys && !aligned(op_keys, 8)) return fail(MAG_E_ALIGN, "op_keys not 8-byte aligned");
+    if (!aligned(plan->buffer, 256))
+        return fail(MAG_E_WORKSPACE, "plan->buffer must be 256-byte aligned");
+    size_t need = 0;
+    int rc = mag_key_plan_size(n_intervals, key_capacity, &need);
+    if (rc) return rc;
+    if (plan->bytes < need) {
+        snprintf(g_last_error, sizeof(g_last_error), "key plan needs %zu bytes, got %zu", need,
+                 plan->bytes);
+        return MAG_E_WORKSPACE;
+    }
+    AttrWorkspace w{};
+    carve_key_plan(n_intervals, key_capacity, plan->buffer, w);
+    mag::GroupParams gp{};
+    gp.keys = op_keys;
+    gp.m = n_intervals;
+    gp.H = hash_slots(key_capacity);
+    gp.cap = key_capacity;
+    gp.table = w.table;
+    gp.slot = w.slot;
+    gp.ukey = w.ukey;
+    gp.urank = w.urank;
+    gp.status = w.kstat;
+    gp.kstat = w.kstat;
+    hipError_t e;
+    if ((e = mag::launch_key_map(gp, true, stream)) != hipSuccess) return hip_fail(e, "key map");
+    if (plan->ready && (e = hipEventRecord(plan->ready, stream)) != hipSuccess)
+        return hip_fail(e, "key plan event");
+    plan->n_intervals = n_intervals;
+    plan->key_capacity = key_capacity;
+    return MAG_OK;
 }
 
 int mag_counter_workspace_size(int64_t n_samples, int64_t n_intervals, int64_t key_capacity,

@@ -48,6 +48,9 @@
 
 #include <hip/hip_ext.h>
 
+#include <algorithm>
+#include <stdlib.h>
+
 #include "mag_internal.hpp"
 
 namespace mag {
@@ -60,6 +63,7 @@ constexpr int T = TILE;
 constexpr int NCOL = WAVE + 1;  // sample columns: the tile's last sample is row 0, column 64
 constexpr int WIN = 2 * WAVE;   // window entries, two per lane
 constexpr int SLOTS = WAVE - 1; // endpoints per round
+constexpr int64_t RUN_TILES = 32;  // most tiles one workgroup walks
 static_assert(T == WAVE * C && C == 8, "tile layout");
 
 __device__ __forceinline__ double endpoint_x(const double* s, const double* e, int64_t off,
@@ -796,8 +800,7 @@ hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream, hipEv
 {
     using K = decltype(&k_tile<SP>);
     const K kern = k_tile<SP>;
-    // persistent waves: as many as can be resident at once, each over a
-    // contiguous run of tiles
+    // resident waves per CU (the occupancy the runtime reports, capped by LDS)
     static int per_cu = 0;
     if (per_cu == 0) {
         int nb = 0;
@@ -815,8 +818,13 @@ hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream, hipEv
         }
         per_cu = nb;
     }
+    // runs of at most RUN_TILES tiles: many more workgroups than fit at once,
+    // so the hardware deals them out as slots free up -- workgroups of other
+    // kernels (another attribution's grouping) interleave with them, and no
+    // slot is left with a long run started late (measured: 32 tiles per run
+    // is as fast as one run per resident wave when the kernel runs alone)
     const int64_t waves = (int64_t)device_cu_count() * per_cu;
-    p.tiles_per_wg = (ntiles + waves - 1) / waves;
+    p.tiles_per_wg = std::min<int64_t>((ntiles + waves - 1) / waves, RUN_TILES);
     const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
     if (ev_start || ev_stop)
         // timing events travel with the dispatch: no marker packets around it

@@ -122,7 +122,7 @@ __global__ __launch_bounds__(INS_THREADS) void k_key_insert(const GroupParams p,
             h = (h + 1u) & (INS_SLOTS - 1);
         }
     }
-    if (special) atomicOr(&p.status->special, 1u);
+    if (special) atomicOr(&p.kstat->special, 1u);
     __syncthreads();
 
     const uint32_t mask = p.H - 1u;
@@ -162,7 +162,7 @@ __global__ __launch_bounds__(INS_THREADS) void k_key_insert(const GroupParams p,
                 h[u] = (h[u] + 1u) & mask;
         }
     }
-    if (pending) atomicOr(&p.status->overflow, 1u);
+    if (pending) atomicOr(&p.kstat->overflow, 1u);
 }
 
 // ids for the occupied slots that have none yet (slot H: the all-ones key);
@@ -177,7 +177,7 @@ __global__ __launch_bounds__(CMP_THREADS) void k_compact(const GroupParams p)
     __shared__ uint32_t wbase[CMP_THREADS / 64];
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int64_t b0 = (int64_t)blockIdx.x * CMP_THREADS * CMP_PER;
-    const bool special = p.status->special != 0u;
+    const bool special = p.kstat->special != 0u;
     unsigned long long key[CMP_PER];
     uint32_t cur[CMP_PER];
 #pragma unroll
@@ -211,7 +211,7 @@ __global__ __launch_bounds__(CMP_THREADS) void k_compact(const GroupParams p)
             wbase[w] = t;
             t += wtot[w];
         }
-        const uint32_t base = t ? atomicAdd(&p.status->n_unique, t) : 0u;
+        const uint32_t base = t ? atomicAdd(&p.kstat->n_unique, t) : 0u;
         for (int w = 0; w < CMP_THREADS / 64; ++w) wbase[w] += base;
     }
     __syncthreads();
@@ -288,8 +288,8 @@ __global__ __launch_bounds__(KM_THREADS) void k_keymap(const GroupParams p)
             if (i < p.m) p.slot[i] = id;
         }
     }
-    if (special && p.status->special == 0u) atomicOr(&p.status->special, 1u);
-    if (over) atomicOr(&p.status->overflow, 1u);
+    if (special && p.kstat->special == 0u) atomicOr(&p.kstat->special, 1u);
+    if (over) atomicOr(&p.kstat->overflow, 1u);
 }
 
 // rank = number of distinct keys smaller than this one: the pairs (x, y) of key
@@ -300,7 +300,7 @@ constexpr uint32_t RANK_TILE = 256u;
 __global__ __launch_bounds__(RANK_TILE) void k_rank(const GroupParams p)
 {
     __shared__ uint64_t tile[RANK_TILE];
-    const uint32_t nu = p.status->n_unique;
+    const uint32_t nu = p.kstat->n_unique;
     const uint32_t nt = (nu + RANK_TILE - 1) / RANK_TILE;
     const uint64_t pairs = (uint64_t)nt * nt;
     for (uint64_t pr = blockIdx.x; pr < pairs; pr += gridDim.x) {
@@ -335,7 +335,7 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
     __shared__ double lsum[AGG_IDS];
     const int c = blockIdx.x;
     const int64_t r0 = (int64_t)blockIdx.y * AGG_IDS;
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (r0 >= nk) return;  // uniform
     const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
@@ -376,6 +376,11 @@ constexpr int FIN_GROUPS = 16;
 
 __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupParams p)
 {
+    if (p.kstat != p.status && blockIdx.x == 0 && threadIdx.x == 0) {
+        // a key plan built beforehand: its counts become the call's
+        p.status->n_unique = p.kstat->n_unique;
+        if (p.kstat->overflow) p.status->overflow = 1u;
+    }
     __shared__ uint64_t qc[FIN_GROUPS][FIN_KEYS];
     __shared__ double qs[FIN_GROUPS][FIN_KEYS];
     const int kl = threadIdx.x % FIN_KEYS, grp = threadIdx.x / FIN_KEYS;
@@ -397,7 +402,7 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
         r = p.urank[id];
         key = p.ukey[id];
     }
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (p.n_keys_out && blockIdx.x == 0 && threadIdx.x == 0) *p.n_keys_out = nk;
     if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     qc[grp][kl] = cnt;
@@ -432,7 +437,7 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_m2(const GroupParams p)
     __shared__ double lmean[AGG_IDS];
     const int c = blockIdx.x;
     const int64_t r0 = (int64_t)blockIdx.y * AGG_IDS;
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (r0 >= nk) return;
     const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
@@ -478,7 +483,7 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_m2(const GroupPar
 #pragma unroll 16
         for (int c = grp; c < p.nchunks; c += FIN_GROUPS) du += p.pdur[(int64_t)c * p.cap + id];
     const uint32_t r = (grp == 0 && id < p.cap) ? p.urank[id] : 0xffffffffu;
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if ((int64_t)blockIdx.x * FIN_KEYS >= nk) return;  // uniform
     qs[grp][kl] = m2;
     qd[grp][kl] = du;
@@ -515,7 +520,7 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_one(const GroupParams p)
         sl[k] = (i < hi) ? p.slot[i] : NO_ID;
         en[k] = (i < hi) ? p.energy[i] : 0.0;
     }
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (r0 >= nk) return;  // uniform
     const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
@@ -574,7 +579,7 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_dur(const GroupParams p)
     __shared__ double ldur[AGG_IDS];
     const int c = blockIdx.x;
     const int64_t r0 = (int64_t)blockIdx.y * AGG_IDS;
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (r0 >= nk) return;
     const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) ldur[v] = 0.0;
@@ -608,6 +613,11 @@ constexpr int FO_KEYS = 32;
 constexpr int FO_GROUPS = 32;
 __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupParams p)
 {
+    if (p.kstat != p.status && blockIdx.x == 0 && threadIdx.x == 0) {
+        // a key plan built beforehand: its counts become the call's
+        p.status->n_unique = p.kstat->n_unique;
+        if (p.kstat->overflow) p.status->overflow = 1u;
+    }
     __shared__ uint64_t qc[FO_GROUPS][FO_KEYS];
     __shared__ double qs[FO_GROUPS][FO_KEYS];
     __shared__ double qmean[FO_KEYS];
@@ -633,7 +643,7 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
         r = p.urank[id];
         key = p.ukey[id];
     }
-    const int64_t nk = min((int64_t)p.status->n_unique, p.cap);
+    const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (p.n_keys_out && blockIdx.x == 0 && threadIdx.x == 0) *p.n_keys_out = nk;
     if ((int64_t)blockIdx.x * FO_KEYS >= nk) return;  // uniform
     qc[grp][kl] = cnt;
@@ -697,9 +707,30 @@ hipError_t launch_set_i64(int64_t* dst, int64_t v, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
+// clears the table, the rank counters and the key state (a key plan built
+// on its own; inside an attribution k_fix does this)
+__global__ __launch_bounds__(256) void k_plan_clear(const GroupParams p)
 {
-    if (p.m <= 0) return p.n_keys_out ? launch_set_i64(p.n_keys_out, 0, stream) : hipSuccess;
+    for (int64_t h = (int64_t)blockIdx.x * 256 + threadIdx.x; h <= (int64_t)p.H;
+         h += (int64_t)gridDim.x * 256) {
+        reinterpret_cast<ulonglong2*>(p.table)[h] = make_ulonglong2(~0ull, ~0ull);  // empty, no id
+        p.urank[h] = 0u;
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+        p.kstat->n_unique = 0u;
+        p.kstat->special = 0u;
+        p.kstat->overflow = 0u;
+        p.kstat->err = 0u;
+    }
+}
+
+hipError_t launch_key_map(const GroupParams& p, bool clear, hipStream_t stream)
+{
+    if (clear) {
+        const unsigned cb = (unsigned)min(((int64_t)p.H + 256) / 256, (int64_t)2048);
+        hipLaunchKernelGGL(k_plan_clear, dim3(cb), dim3(256), 0, stream, p);
+    }
+    if (p.m <= 0) return hipGetLastError();
     const int64_t n_ins = min(p.m, (int64_t)INS_CHUNK * INS_GROUPS);
     hipLaunchKernelGGL(k_key_insert, dim3((unsigned)((n_ins + INS_CHUNK - 1) / INS_CHUNK)),
                        dim3(INS_THREADS), 0, stream, p, n_ins);
@@ -718,6 +749,12 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
     const int64_t ntile = (nmax + RANK_TILE - 1) / RANK_TILE;
     hipLaunchKernelGGL(k_rank, dim3((unsigned)min(ntile * ntile, (int64_t)4096)), dim3(RANK_TILE),
                        0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_aggregate(const GroupParams& p, hipStream_t stream)
+{
+    if (p.m <= 0) return p.n_keys_out ? launch_set_i64(p.n_keys_out, 0, stream) : hipSuccess;
     const unsigned ranges = (unsigned)((p.cap + AGG_IDS - 1) / AGG_IDS);
     const unsigned kb = (unsigned)max((int64_t)1, (p.cap + FIN_KEYS - 1) / FIN_KEYS);
     if (ranges > 0 && p.chunk <= (int64_t)AGG_THREADS * AGG_BATCH) {
@@ -737,6 +774,14 @@ hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
         hipLaunchKernelGGL(k_fin_m2, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
     }
     return hipGetLastError();
+}
+
+hipError_t launch_groupby(const GroupParams& p, hipStream_t stream)
+{
+    if (p.m <= 0) return p.n_keys_out ? launch_set_i64(p.n_keys_out, 0, stream) : hipSuccess;
+    const hipError_t e = launch_key_map(p, false, stream);
+    if (e != hipSuccess) return e;
+    return launch_aggregate(p, stream);
 }
 
 }  // namespace mag

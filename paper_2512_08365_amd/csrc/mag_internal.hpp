@@ -144,6 +144,11 @@ struct GroupParams {
     double* dur_out;      // [cap]
     double* pdur;         // [nchunks][cap]
     int64_t* n_keys_out;  // device copy of the number of rows filled, or NULL
+    // the key state (distinct-key count, all-ones key seen, table overflow):
+    // the call's own status block when the call builds its key map, the
+    // header of a key plan built beforehand otherwise (the aggregation then
+    // copies the count and the overflow flag into the call's status)
+    Status* kstat;
 };
 
 // per-operator energy from a delayed cumulative energy counter
@@ -232,6 +237,13 @@ hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_st
                        hipEvent_t ev_stop = nullptr);
 // intervals spanning tiles, endpoints outside the trace, clearing of the group-by state
 hipError_t launch_fix(const FixParams& p, hipStream_t stream);
+// the key map of a grouping (distinct keys, their ids and ranks, every
+// interval's id): built into p.table / p.slot / p.ukey / p.urank / p.kstat;
+// clear: the table, ranks and key state are cleared first (else k_fix did)
+hipError_t launch_key_map(const GroupParams& p, bool clear, hipStream_t stream);
+// the per-key aggregation over a built key map (count, sum, M2, latency, rows
+// in key order)
+hipError_t launch_aggregate(const GroupParams& p, hipStream_t stream);
 // multi-mode SVD invariants (Section 4.2): one task per (tensor, unfolding)
 constexpr int SVD_MAX_RANK = 5;
 constexpr int SVD_MAX_K = 512;        // largest Gram side (min(M, N) of an unfolding)

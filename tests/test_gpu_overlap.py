@@ -163,3 +163,39 @@ def test_diff_enqueued_before_the_attributions_finish():
         nf = int(det.rank.n_out)
         assert torch.equal(o2["key"][:nf], dref["key"])
         assert torch.equal(o2["v"][:nf], dref["verdict"])
+
+
+def test_tile_events_serialize_the_trace_integrations():
+    """tiles_done on A and tiles_wait on B: B's set-up runs at once, its
+    trace integration after A's; both results equal the serial calls."""
+    import torch
+    import paper_2512_08365_amd as mag
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    cases = [synth.long_trace(seed, 300_000, 4, 20_000) for seed in (73, 74)]
+    devs = [to_gpu(c) for c in cases]
+
+    def run(d, c, **kw):
+        off = [int(x) for x in c["offsets"]]
+        return mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], n_streams=len(off) - 1,
+                             stream_offsets=off, **kw)
+
+    serial = [run(d, c) for d, c in zip(devs, cases)]
+    torch.cuda.synchronize()
+    s2 = torch.cuda.Stream()
+    a_tiles = torch.cuda.Event()
+    for rep in range(3):
+        log(f"[tile events] repetition {rep}")
+        pend_a = run(devs[0], cases[0], asynchronous=True, tiles_done=a_tiles)
+        with torch.cuda.stream(s2):
+            pend_b = run(devs[1], cases[1], asynchronous=True, tiles_wait=a_tiles)
+        res_b = pend_b.finish()
+        res_a = pend_a.finish()
+        torch.cuda.synchronize()
+        for got, want in ((res_a, serial[0]), (res_b, serial[1])):
+            for k in ("energy", "start_idx", "end_idx"):
+                assert torch.equal(got[0][k], want[0][k]), k
+            for k in ("keys", "count"):
+                assert torch.equal(got[1][k], want[1][k]), k
+            np.testing.assert_allclose(got[1]["sum"].cpu().numpy(), want[1]["sum"].cpu().numpy(),
+                                       rtol=1e-12)
