@@ -255,6 +255,116 @@ constexpr int log2_exact(int v) { return v <= 1 ? 0 : 1 + log2_exact(v >> 1); }
 
 }  // namespace
 
+namespace {
+
+// the samples of one tile in registers (lane k: local samples kC .. kC+C).
+// A whole tile of a 16-byte aligned trace is fetched one tile ahead and kept
+// in the vectors the loads produce until it is processed (unpacking them
+// earlier would wait for the loads right after their issue); a short tile or
+// an unaligned trace is read when its tile starts.
+struct SampleRegs {
+    double2 pt[C / 2];
+    float4 pp[C / 4];
+    double ptl;  // local sample kC + C: the next lane's first (lane 63: the tile's last)
+    float ppl;
+};
+
+__device__ __forceinline__ bool vector_tile(int b)
+{
+    const KArgs k = kargs();
+    return k->aligned16 && (int64_t)b * T + T <= k->nseg;
+}
+
+__device__ __forceinline__ void sample_prefetch(SampleRegs& r, int b, int lane)
+{
+    const KArgs k = kargs();
+    const int64_t g = (int64_t)b * T + (int64_t)lane * C - k->base;
+    const double2* t2 = reinterpret_cast<const double2*>(k->t + g);
+    const float4* P4 = reinterpret_cast<const float4*>(k->P + g);
+#pragma unroll
+    for (int u = 0; u < C / 2; ++u) r.pt[u] = t2[u];
+#pragma unroll
+    for (int u = 0; u < C / 4; ++u) r.pp[u] = P4[u];
+    r.ptl = k->t[g + C];
+    r.ppl = k->P[g + C];
+}
+
+// checks, segment energies S_j = (P_j + P_{j+1}) (t_{j+1} - t_j) / 2 and the
+// tile-local prefix F (a per-lane running sum plus a DPP scan of the lane
+// totals) of tile b (L segments), staged in LDS as {t, F} and P; returns the
+// tile's energy (uniform)
+__device__ __forceinline__ double sample_stage(const SampleRegs& r, int b, int L, int lane,
+                                               double2 (*tF)[NCOL], float (*Pl)[NCOL],
+                                               unsigned& err)
+{
+    const KArgs kk = kargs();
+    const int64_t j0 = (int64_t)b * T;
+    const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
+    double tv[C + 1];
+    float pv[C + 1];
+    if (vector_tile(b)) {
+#pragma unroll
+        for (int u = 0; u < C / 2; ++u) {
+            tv[2 * u] = r.pt[u].x;
+            tv[2 * u + 1] = r.pt[u].y;
+        }
+#pragma unroll
+        for (int u = 0; u < C / 4; ++u) {
+            pv[4 * u] = r.pp[u].x;
+            pv[4 * u + 1] = r.pp[u].y;
+            pv[4 * u + 2] = r.pp[u].z;
+            pv[4 * u + 3] = r.pp[u].w;
+        }
+        tv[C] = r.ptl;
+        pv[C] = r.ppl;
+    } else {
+        // a lane past the tile's last sample repeats the last one it has with
+        // zero power: missing segments have zero width and energy
+        const int64_t g = j0 + (int64_t)lane * C - kk->base;
+        const int have = min(max(L - lane * C, -1), C);  // last local sample of the lane
+        double tl = 0.0;
+#pragma unroll
+        for (int u = 0; u <= C; ++u) {
+            tv[u] = (u <= have) ? kk->t[g + u] : tl;
+            pv[u] = (u <= have) ? kk->P[g + u] : 0.0f;
+            tl = tv[u];
+        }
+    }
+    if (kk->validate) {
+        // every segment of the lane rises (the repeated last time of a short
+        // lane does not), and a strictly increasing run whose ends are finite
+        // is finite throughout (a NaN fails every comparison)
+        int rising = 0;
+#pragma unroll
+        for (int u = 0; u < C; ++u) rising += (tv[u + 1] > tv[u]) ? 1 : 0;
+        const bool t_ok = (rising == cs) & (fabs(tv[0]) < INFINITY) & (fabs(tv[C]) < INFINITY);
+        bool p_ok = true;
+#pragma unroll
+        for (int u = 0; u <= C; ++u) p_ok &= (pv[u] >= 0.0f) & (pv[u] < INFINITY);
+        err |= (t_ok ? 0u : ERR_TIMESTAMPS) | (p_ok ? 0u : ERR_POWER);
+    }
+    double f[C + 1];
+    f[0] = 0.0;
+#pragma unroll
+    for (int u = 0; u < C; ++u) f[u + 1] = f[u] + seg_energy(tv[u], tv[u + 1], pv[u], pv[u + 1]);
+    const double incl = scan_wave(f[C]);
+    // F at the lane's first sample: the exclusive scan (lane 0 reads 0)
+    const double base = dpp_f64<DPP_WAVE_SHR1, 0xf>(incl);
+#pragma unroll
+    for (int u = 0; u < C; ++u) {
+        tF[u][lane] = make_double2(tv[u], base + f[u]);
+        Pl[u][lane] = pv[u];
+    }
+    const double Wt = read_lane_f64(incl, WAVE - 1);
+    if (lane == WAVE - 1) {
+        tF[0][WAVE] = make_double2(tv[C], Wt);
+        Pl[0][WAVE] = pv[C];
+    }
+    return Wt;
+}
+
+}  // namespace
+
 // SP: the number of streams rounded up to a power of two (streams S .. SP-1
 // are treated as empty).  Lane a < SP holds stream a's state in registers.
 template <int SP>
@@ -335,33 +445,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     double ew0 = wload(bperm64(sq, wa0), wr0, woff0, wlen0, em0);
     double ew1 = wload(bperm64(sq, wa1), wr1, woff1, wlen1, em1);
 
-    // ---- samples of a tile into registers (lane k: local samples kC .. kC+C).
-    // A whole tile of a 16-byte aligned trace is fetched one tile ahead and
-    // kept in the vectors the loads produce until it is processed (unpacking
-    // them earlier would wait for the loads right after their issue); a short
-    // tile or an unaligned trace is read when its tile starts.
-    double2 pt[C / 2];
-    float4 pp[C / 4];
-    double ptl;  // local sample kC + C: the next lane's first (lane 63: the tile's last)
-    float ppl;
-    auto vector_tile = [&](int b) {
-        const KArgs k = kargs();
-        return k->aligned16 && (int64_t)b * T + T <= k->nseg;
-    };
-    auto prefetch = [&](int b) {
-        const KArgs k = kargs();
-        const int64_t g = (int64_t)b * T + (int64_t)lane * C - k->base;
-        const double2* t2 = reinterpret_cast<const double2*>(k->t + g);
-        const float4* P4 = reinterpret_cast<const float4*>(k->P + g);
-#pragma unroll
-        for (int u = 0; u < C / 2; ++u) pt[u] = t2[u];
-#pragma unroll
-        for (int u = 0; u < C / 4; ++u) pp[u] = P4[u];
-        ptl = k->t[g + C];
-        ppl = k->P[g + C];
-    };
-
-    if (vector_tile(b0)) prefetch(b0);
+    SampleRegs sr;
+    if (vector_tile(b0)) sample_prefetch(sr, b0, lane);
     // Outputs are written one round late, right after the next round's window
     // has arrived: loads complete in issue order, so a store issued between a
     // load and its use would make the use wait for the store as well.  Null:
@@ -392,74 +477,9 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         const KArgs kk = kargs();
         const int64_t j0 = (int64_t)b * T;
         const int L = (int)min((int64_t)T, kk->nseg - j0);
-        const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
 
         // ---- samples: checks, segment energies, tile-local prefix, staging
-        {
-            double tv[C + 1];
-            float pv[C + 1];
-            if (vector_tile(b)) {
-#pragma unroll
-                for (int u = 0; u < C / 2; ++u) {
-                    tv[2 * u] = pt[u].x;
-                    tv[2 * u + 1] = pt[u].y;
-                }
-#pragma unroll
-                for (int u = 0; u < C / 4; ++u) {
-                    pv[4 * u] = pp[u].x;
-                    pv[4 * u + 1] = pp[u].y;
-                    pv[4 * u + 2] = pp[u].z;
-                    pv[4 * u + 3] = pp[u].w;
-                }
-                tv[C] = ptl;
-                pv[C] = ppl;
-            } else {
-                // a lane past the tile's last sample repeats the last one it
-                // has with zero power: missing segments have zero width and energy
-                const int64_t g = j0 + (int64_t)lane * C - kk->base;
-                const int have = min(max(L - lane * C, -1), C);  // last local sample of the lane
-                double tl = 0.0;
-#pragma unroll
-                for (int u = 0; u <= C; ++u) {
-                    tv[u] = (u <= have) ? kk->t[g + u] : tl;
-                    pv[u] = (u <= have) ? kk->P[g + u] : 0.0f;
-                    tl = tv[u];
-                }
-            }
-            if (kk->validate) {
-                // every segment of the lane rises (the repeated last time of a
-                // short lane does not), and a strictly increasing run whose ends
-                // are finite is finite throughout (a NaN fails every comparison)
-                int rising = 0;
-#pragma unroll
-                for (int u = 0; u < C; ++u) rising += (tv[u + 1] > tv[u]) ? 1 : 0;
-                const bool t_ok =
-                    (rising == cs) & (fabs(tv[0]) < INFINITY) & (fabs(tv[C]) < INFINITY);
-                bool p_ok = true;
-#pragma unroll
-                for (int u = 0; u <= C; ++u) p_ok &= (pv[u] >= 0.0f) & (pv[u] < INFINITY);
-                err |= (t_ok ? 0u : ERR_TIMESTAMPS) | (p_ok ? 0u : ERR_POWER);
-            }
-            double f[C + 1];
-            f[0] = 0.0;
-#pragma unroll
-            for (int u = 0; u < C; ++u)
-                f[u + 1] = f[u] + seg_energy(tv[u], tv[u + 1], pv[u], pv[u + 1]);
-            const double incl = scan_wave(f[C]);
-            // F at the lane's first sample: the exclusive scan (lane 0 reads 0)
-            const double base = dpp_f64<DPP_WAVE_SHR1, 0xf>(incl);
-#pragma unroll
-            for (int u = 0; u < C; ++u) {
-                sm.tF[u][lane] = make_double2(tv[u], base + f[u]);
-                sm.P[u][lane] = pv[u];
-            }
-            const double Wt = read_lane_f64(incl, WAVE - 1);
-            if (lane == WAVE - 1) {
-                sm.tF[0][WAVE] = make_double2(tv[C], Wt);
-                sm.P[0][WAVE] = pv[C];
-            }
-            w_wave += Wt;
-        }
+        w_wave += sample_stage(sr, b, L, lane, sm.tF, sm.P, err);
         if (slane) {
             const KArgs k = kargs();
             pend_cnt = sreg(k->cnt) + ((int64_t)lane * (k->ld + 1) + b);
@@ -492,7 +512,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             // samples of the next tile, in flight during this tile's rounds;
             // issued after the window is read, so that the wait for the window
             // loads does not wait for them (loads complete in issue order)
-            if (first_round && b + 1 < b1 && vector_tile(b + 1)) prefetch(b + 1);
+            if (first_round && b + 1 < b1 && vector_tile(b + 1)) sample_prefetch(sr, b + 1, lane);
             first_round = false;
             const uint64_t mo0 = __ballot(em0), mo1 = __ballot(em1);
             const int tot = __popcll(in0) + __popcll(in1);
@@ -792,16 +812,233 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     }
 }
 
+// ---------------------------------------------------------------------------
+// One stream (sequential intervals): the endpoints of a stream are already in
+// time order, so a round needs no merge, no split and no per-round sums: the
+// gap ending at an endpoint runs from the endpoint one lane below (the round's
+// starting point for lane 0), and it is the energy of one interval (an end
+// endpoint: the stream was inside an interval) or idle energy (a start).  The
+// lane after the round's last endpoint takes the gap to the tile's end, the
+// piece of an interval still open there.  Same outputs as k_tile: energies,
+// sample indices, head/tail pieces, per-tile cursors, per-run trace and idle
+// energies.
+// ---------------------------------------------------------------------------
+struct SeqLds {
+    double2 tF[C][NCOL];
+    float P[C][NCOL];
+};
+
+__global__ __launch_bounds__(WAVE) void k_tile_seq(const TileParams p)
+{
+    __shared__ SeqLds sm;
+    const int lane = threadIdx.x;
+    const int b0 = (int)p.tile_begin + (int)blockIdx.x * (int)p.tiles_per_wg;
+    const int b1 = min(b0 + (int)p.tiles_per_wg, (int)p.tile_end);
+    if (b0 >= b1) return;
+    const int64_t len = 2 * (p.ss.off[1] - p.ss.off[0]);  // endpoints (off[0] = 0)
+
+    // cursor at the first tile: endpoints <= its start time (64-ary search)
+    int64_t sq;
+    {
+        const double tau0 = p.t[(int64_t)b0 * T - p.base];
+        int64_t lo = 0, hi = len;
+        while (hi - lo > WAVE) {
+            const int64_t step = (hi - lo + WAVE - 1) / WAVE;
+            const int64_t pr = lo + (int64_t)(lane + 1) * step - 1;
+            const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, 0, pr) <= tau0);
+            const int c = __popcll(__ballot(ok));
+            const int64_t nlo = lo + (int64_t)c * step;
+            const int64_t nhi = min(hi, lo + (int64_t)(c + 1) * step - 1);
+            lo = min(nlo, hi);
+            hi = max(nhi, lo);
+        }
+        const int64_t pr = lo + lane;
+        const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, 0, pr) <= tau0);
+        sq = lo + __popcll(__ballot(ok));
+    }
+    // the stream's last consumed endpoint (uniform)
+    double slastx = (sq > 0) ? endpoint_x(p.s, p.e, 0, sq - 1) : -INFINITY;
+
+    // window: lane l holds endpoint sq + l; past the stream's end it reads +inf
+    // from device memory, so the value needs no select after its load
+    auto wload = [&](int64_t cur) -> double {
+        const int64_t q = cur + lane;
+        const KArgs k = kargs();
+        const gptr<const double> pe = sreg(k->e), ps = sreg(k->s);
+        const gptr<const double> ptr =
+            (q < len) ? ((q & 1) ? pe : ps) + (q >> 1) : (gptr<const double>)&kPastEnd;
+        return *ptr;
+    };
+    double ew = wload(sq);
+
+    SampleRegs sr;
+    if (vector_tile(b0)) sample_prefetch(sr, b0, lane);
+    unsigned err = 0u;
+    double idle = 0.0;    // this lane's share of the idle energy
+    double w_wave = 0.0;  // the run's trace energy (uniform)
+
+    for (int b = b0; b < b1; ++b) {
+        const KArgs kk = kargs();
+        const int64_t j0 = (int64_t)b * T;
+        const int L = (int)min((int64_t)T, kk->nseg - j0);
+        w_wave += sample_stage(sr, b, L, lane, sm.tF, sm.P, err);
+        if (lane == 0) kk->cnt[b] = sq;
+        // the interval open at the tile's start began in an earlier tile
+        int started = 0;
+        wave_sync();
+        auto tF_at = [&](int i) -> double2 { return sm.tF[i & (C - 1)][i >> 3]; };
+        auto t_at = [&](int i) -> double { return sm.tF[i & (C - 1)][i >> 3].x; };
+        auto P_at = [&](int i) -> double { return (double)sm.P[i & (C - 1)][i >> 3]; };
+        const double t_begin = t_at(0);
+        const double tau_end = t_at(L);
+        const double inv_dt = (double)L * recip(tau_end - t_begin);
+        // where the round starts (uniform): the tile's first sample, later the
+        // previous round's last endpoint -- x, its interpolated power, the
+        // piece from x to the end of its segment, F at that end, its segment
+        double rs_x = t_begin, rs_ph = P_at(0), rs_right = 0.0, rs_Fn = 0.0;
+        int rs_j = -1;
+        bool first_round = true;
+        for (;;) {
+            const double xw = ew;
+            // the round: the window's leading entries inside the tile (63 at
+            // most when they are the tile's last, so that a lane is left for
+            // the gap to the tile's end)
+            const uint64_t inm = __ballot(xw <= tau_end);
+            const int lead = (inm == ~0ull) ? WAVE : (int)__builtin_ctzll(~inm);
+            const bool fin = lead < WAVE;
+            const int k = lead;
+            if (first_round && b + 1 < b1 && vector_tile(b + 1)) sample_prefetch(sr, b + 1, lane);
+            first_round = false;
+            const int64_t sqn = sq + k;
+            ew = wload(sqn);  // the next round's window
+
+            const bool real = lane < k;
+            const bool tail_lane = fin && lane == k;
+            const int64_t q = sq + lane;  // the tail lane: sqn
+            const double x = real ? xw : tau_end;
+            // an entry that is neither inside the tile nor after its end is
+            // not a number
+            if (tail_lane && kk->validate && q < len && !(xw > tau_end)) err |= ERR_INTERVAL;
+
+            // ---- segment j: t_j < x <= t_{j+1}; sample index j0 + j + 1
+            int j;
+            {
+                const int jg = (int)fmin(fmax((x - t_begin) * inv_dt, 0.0), (double)(L - 1));
+                const int c0 = max(0, min(jg - 1, L - 3));
+                const double u0 = t_at(c0), u1 = t_at(min(c0 + 1, L)), u2 = t_at(min(c0 + 2, L)),
+                             u3 = t_at(min(c0 + 3, L));
+                j = (u0 < x && x <= u1) ? c0
+                  : (c0 + 1 < L && u1 < x && x <= u2) ? c0 + 1
+                  : (c0 + 2 < L && u2 < x && x <= u3) ? c0 + 2 : -1;
+                if (!real) j = L;
+            }
+            if (__ballot(j < 0) != 0ull) {
+                if (j < 0) {
+                    int lo = 0, hi = L;
+                    while (lo < hi) {
+                        const int mid = (lo + hi) >> 1;
+                        if (t_at(mid) < x) lo = mid + 1; else hi = mid;
+                    }
+                    j = min(max(lo, 1), L) - 1;
+                }
+            }
+            const double2 A0 = tF_at(j), A1 = tF_at(min(j + 1, L));
+            const double pj = P_at(j), pj1 = P_at(min(j + 1, L));
+            const double rh = recip(A1.x - A0.x);
+            const double ph = !real ? pj : (x == A1.x) ? pj1 : pj + (pj1 - pj) * ((x - A0.x) * rh);
+            const double left = real ? ((pj + ph) * (x - A0.x)) * 0.5 : 0.0;
+            const double right = real ? ((ph + pj1) * (A1.x - x)) * 0.5 : 0.0;
+            const double Fj = A0.y;  // prefix at the start of segment j (the tile's end: F_L)
+            const int64_t gid = q >> 1;
+            if (real) {
+                int64_t* idx = (q & 1) ? kk->end_idx : kk->start_idx;
+                if (idx) idx[gid] = j0 + j + 1;
+            }
+
+            // ---- the gap ending here, from the endpoint one lane below
+            double px = dpp_f64<DPP_WAVE_SHR1, 0xf>(x);
+            double pph = dpp_f64<DPP_WAVE_SHR1, 0xf>(ph);
+            double pright = dpp_f64<DPP_WAVE_SHR1, 0xf>(right);
+            double pFn = dpp_f64<DPP_WAVE_SHR1, 0xf>(A1.y);
+            int pjx = dpp_i32<DPP_WAVE_SHR1, 0xf>(j);
+            if (lane == 0) {
+                px = rs_x;
+                pph = rs_ph;
+                pright = rs_right;
+                pFn = rs_Fn;
+                pjx = rs_j;
+            }
+            // finite and not before the stream's previous endpoint
+            if (real && kk->validate && (!(fabs(x) < INFINITY) || !(((lane == 0) ? slastx : px) <= x)))
+                err |= ERR_INTERVAL;
+            const bool has_gap = real || tail_lane;
+            const bool same = (pjx == j);
+            // both in segment j: the trapezoid of the two interpolated values
+            const double q_in = ((pph + ph) * (x - px)) * 0.5;
+            double whole = fmax(Fj - pFn, 0.0);
+            const bool ill = has_gap && !same && (j >= pjx + 2) && (whole < Fj * 0x1p-14);
+            if (__ballot(ill) != 0ull) {
+                if (ill) {
+                    // the whole segments summed directly
+                    double sum = 0.0;
+                    for (int i = pjx + 1; i < j; ++i)
+                        sum += seg_energy(t_at(i), t_at(i + 1), sm.P[i & 7][i >> 3],
+                                          sm.P[(i + 1) & 7][(i + 1) >> 3]);
+                    whole = sum;
+                }
+            }
+            const double Q = same ? q_in : (pright + whole) + left;
+            const bool open = (q & 1) != 0;  // the gap lies inside an interval
+            if (has_gap && !open) idle += Q;
+            if (has_gap && open) {
+                // an interval ending at this endpoint, or open at the tile's
+                // end: complete when it began in this tile, else its piece here
+                const bool began = (lane > 0) || started;
+                if (real)
+                    *(began ? &kk->energy[gid] : &kk->head[b]) = Q;
+                else
+                    *(began ? &kk->tail[b] : &kk->head[b]) = Q;
+            }
+            // ---- commit (uniform)
+            if (k > 0) {
+                const int ll = k - 1;
+                slastx = read_lane_f64(x, ll);
+                rs_x = slastx;
+                rs_ph = read_lane_f64(ph, ll);
+                rs_right = read_lane_f64(right, ll);
+                rs_Fn = read_lane_f64(A1.y, ll);
+                rs_j = __builtin_amdgcn_readlane(j, ll);
+                started = (sqn & 1) ? 1 : 0;  // the last endpoint was a start
+            }
+            sq = sqn;
+            if (fin) break;
+        }
+        wave_sync();
+    }
+
+    // the run's trace and idle energy, at its first tile (k_fix adds them up)
+    const double It = wave_sum(idle);
+    const KArgs k = kargs();
+    if (lane == 0) {
+        k->part[b0] = make_double2(w_wave, It);
+        // where this run stopped: the next run must start there
+        k->cnt_fin[b1] = sq;
+        if (b1 == (int)k->NT) k->cnt[b1] = sq;
+    }
+    if (__ballot(err != 0u)) {
+        unsigned e = err;
+        for (int off = 32; off > 0; off >>= 1) e |= __shfl_xor(e, off);
+        if (lane == 0) atomicOr(&k->status->err, e);
+    }
+}
+
 namespace {
 
-template <int SP>
-hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream, hipEvent_t ev_start,
-                         hipEvent_t ev_stop)
+template <class Lds>
+hipError_t launch_tile_kernel(void (*kern)(TileParams), int& per_cu, TileParams p, int64_t ntiles,
+                              hipStream_t stream, hipEvent_t ev_start, hipEvent_t ev_stop)
 {
-    using K = decltype(&k_tile<SP>);
-    const K kern = k_tile<SP>;
     // resident waves per CU (the occupancy the runtime reports, capped by LDS)
-    static int per_cu = 0;
     if (per_cu == 0) {
         int nb = 0;
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kern, WAVE, 0) != hipSuccess ||
@@ -813,7 +1050,7 @@ hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream, hipEv
             hipDeviceGetAttribute(&lds, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) ==
                 hipSuccess &&
             lds > 0) {
-            const int per_wave = (int)((sizeof(TileLds<SP>) + 2047) / 2048) * 2048;
+            const int per_wave = (int)((sizeof(Lds) + 2047) / 2048) * 2048;
             nb = max(1, min(nb, lds / per_wave));
         }
         per_cu = nb;
@@ -835,6 +1072,22 @@ hipError_t launch_tile_t(TileParams p, int64_t ntiles, hipStream_t stream, hipEv
     return hipGetLastError();
 }
 
+template <int SP>
+hipError_t launch_tile_t(const TileParams& p, int64_t ntiles, hipStream_t stream,
+                         hipEvent_t ev_start, hipEvent_t ev_stop)
+{
+    static int per_cu = 0;
+    return launch_tile_kernel<TileLds<SP>>(k_tile<SP>, per_cu, p, ntiles, stream, ev_start,
+                                           ev_stop);
+}
+
+hipError_t launch_tile_seq(const TileParams& p, int64_t ntiles, hipStream_t stream,
+                           hipEvent_t ev_start, hipEvent_t ev_stop)
+{
+    static int per_cu = 0;
+    return launch_tile_kernel<SeqLds>(k_tile_seq, per_cu, p, ntiles, stream, ev_start, ev_stop);
+}
+
 }  // namespace
 
 hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_start,
@@ -843,7 +1096,7 @@ hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_st
     const int64_t ntiles = p.tile_end - p.tile_begin;
     if (ntiles <= 0) return hipSuccess;
     const int S = p.ss.S;
-    if (S == 1) return launch_tile_t<1>(p, ntiles, stream, ev_start, ev_stop);
+    if (S == 1) return launch_tile_seq(p, ntiles, stream, ev_start, ev_stop);
     if (S == 2) return launch_tile_t<2>(p, ntiles, stream, ev_start, ev_stop);
     if (S <= 4) return launch_tile_t<4>(p, ntiles, stream, ev_start, ev_stop);
     if (S <= 8) return launch_tile_t<8>(p, ntiles, stream, ev_start, ev_stop);
