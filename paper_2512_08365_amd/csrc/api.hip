@@ -82,6 +82,8 @@ struct AttrWorkspace {
     double* psum;
     double* pm2;
     double* pdur;
+    double* ctot;    // per-chunk energy totals (the aggregation's)
+    double2* fold;   // k_fix's partial sums of the per-run trace and idle energies
     double* stage_t;
     float* stage_P;
 };
@@ -108,6 +110,7 @@ size_t carve(const Plan& pl, void* ws, AttrWorkspace& w)
     w.head = c.take<double>((size_t)pl.S * pl.NT);
     w.tail = c.take<double>((size_t)pl.S * pl.NT);
     w.part = c.take<double2>((size_t)pl.NT);
+    w.fold = c.take<double2>((size_t)mag::FOLD_BLOCKS);
     w.energy = c.take<double>((size_t)std::max<int64_t>(pl.m, 1));
     if (pl.staging) {
         w.stage_t = c.take<double>((size_t)mag::TILE + 1);
@@ -144,6 +147,7 @@ void carve_groupby(Carver& c, const Plan& pl, AttrWorkspace& w)
         w.psum = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         w.pm2 = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
         if (pl.lat) w.pdur = c.take<double>((size_t)pl.nchunks * std::max<int64_t>(pl.cap, 1));
+        w.ctot = c.take<double>((size_t)pl.nchunks);
     }
 }
 
@@ -524,6 +528,7 @@ struct Job {
         fp.end_idx = end_idx;
         fp.status = w.status;
         fp.part = w.part;
+        fp.fold = w.fold;
         fp.validate = validate() ? 1 : 0;
         if (grouping && pl.m > 0 && pl.H > 0 && !pl.ext_keys) {
             fp.table = w.table;
@@ -535,11 +540,14 @@ struct Job {
 
     hipError_t grouping(uint64_t* keys_out, mag_key_stats* per_key)
     {
-        if (pl.m == 0)
+        if (pl.m == 0 || !per_key) {
+            // no aggregation: one workgroup adds up the energies and the fold
+            const hipError_t e2 = mag::launch_energy_total(energy, pl.m, w.fold, w.status, stream);
+            if (e2 != hipSuccess || pl.m > 0) return e2;
             return (per_key && per_key->n_keys_device)
                        ? mag::launch_set_i64(per_key->n_keys_device, 0, stream)
                        : hipSuccess;
-        if (!per_key) return mag::launch_energy_total(energy, pl.m, w.status, stream);
+        }
         mag::GroupParams gp{};
         gp.keys = keys;
         gp.energy = energy;
@@ -562,6 +570,8 @@ struct Job {
         gp.count_out = per_key->count;
         gp.status = w.status;
         gp.kstat = w.kstat;
+        gp.ctot = w.ctot;
+        gp.fold = w.fold;  // NULL in the counter mode: its fold kernel sets those totals
         gp.n_keys_out = per_key->n_keys_device;
         if (pl.lat) {
             gp.s = s;
@@ -1130,6 +1140,34 @@ size_t state_bytes(const mag_stream* h)
 
 }  // namespace
 
+namespace {
+
+// the candidate slots and per-workgroup counts of one comparison
+void carve_candidates(Carver& c, int64_t na, int64_t k, mag::DiffParams* p)
+{
+    const int64_t groups = mag::diff_groups(na);
+    const int64_t slots = mag::diff_max_candidates(na, k);
+    const size_t nc = (size_t)std::max<int64_t>(slots, 1);
+    double* r = c.take<double>(nc);
+    uint64_t* key = c.take<uint64_t>(nc);
+    int32_t* ia = c.take<int32_t>(nc);
+    int32_t* ib = c.take<int32_t>(nc);
+    uint32_t* rank = c.take<uint32_t>(nc);
+    uint32_t* blk = c.take<uint32_t>(8 * (size_t)groups);
+    if (p) {
+        p->cand_r = r;
+        p->cand_key = key;
+        p->cand_ia = ia;
+        p->cand_ib = ib;
+        p->cand_rank = rank;
+        p->blk = blk;
+        p->n_groups = groups;
+        p->n_slots = slots;
+    }
+}
+
+}  // namespace
+
 extern "C" {
 
 int mag_stream_workspace_size(int64_t max_samples, int64_t n_intervals, int64_t key_capacity,
@@ -1483,12 +1521,7 @@ int mag_diff_workspace_size(int64_t n_keys_a, int64_t n_keys_b, int64_t k, size_
     if (n_keys_a < 0 || n_keys_b < 0 || k < 0) return fail(MAG_E_SIZE, "negative size");
     Carver c;
     c.take<mag::Status>(1);
-    const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(n_keys_a, k), 1);
-    c.take<double>(nc);
-    c.take<uint64_t>(nc);
-    c.take<int32_t>(nc);
-    c.take<int32_t>(nc);
-    c.take<uint32_t>(nc);
+    carve_candidates(c, n_keys_a, k, nullptr);
     *bytes = c.off;
     return MAG_OK;
 }
@@ -1546,23 +1579,6 @@ int diff_params(const uint64_t* keysA, const mag_key_stats* statsA, const uint64
     return MAG_OK;
 }
 
-// the candidate arrays of one comparison
-void carve_candidates(Carver& c, int64_t na, int64_t k, mag::DiffParams* p)
-{
-    const size_t nc = (size_t)std::max<int64_t>(mag::diff_max_candidates(na, k), 1);
-    double* r = c.take<double>(nc);
-    uint64_t* key = c.take<uint64_t>(nc);
-    int32_t* ia = c.take<int32_t>(nc);
-    int32_t* ib = c.take<int32_t>(nc);
-    uint32_t* rank = c.take<uint32_t>(nc);
-    if (p) {
-        p->cand_r = r;
-        p->cand_key = key;
-        p->cand_ia = ia;
-        p->cand_ib = ib;
-        p->cand_rank = rank;
-    }
-}
 
 // a comparison's result from its status block
 int conclude_diff(const mag::DiffParams& p, const mag::Status& st, mag_rank_out* out)
@@ -1596,8 +1612,7 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     p.status = c.take<mag::Status>(1);
     carve_candidates(c, p.na, k, &p);
     hipError_t e;
-    if ((e = mag::launch_init_status(p.status, nullptr, 0, stream)) != hipSuccess)
-        return hip_fail(e, "init");
+    // every field of the status block the call reads is written by its kernels
     if ((e = mag::launch_diff(p, stream)) != hipSuccess) return hip_fail(e, "diff kernels");
     rc = read_status(p.status, stream, st);
     if (rc != MAG_OK) return rc;

@@ -94,7 +94,6 @@ __device__ void fix_outside(const FixParams& p, int a, int64_t r, int64_t nthrea
 
 constexpr int FIX_THREADS = 256;
 constexpr int OUT_BLOCKS = 32;  // workgroups per stream for the outside endpoints
-constexpr int FOLD_BLOCKS = 256; // workgroups adding up the per-run trace and idle energies
 
 // the {trace, idle} energies the tile waves left at the first tile of their
 // runs; a run starts at tile 0 and at every tile where a wave stopped (its
@@ -126,8 +125,9 @@ __device__ void fold_parts(const FixParams& p, int blk)
             t.x += red[u].x;
             t.y += red[u].y;
         }
-        if (t.x != 0.0) atomicAdd(&p.status->trace_energy, t.x);
-        if (t.y != 0.0) atomicAdd(&p.status->idle_energy, t.y);
+        // a plain store: the call's last kernel adds the partial sums up (a
+        // same-address atomic from every workgroup would queue for microseconds)
+        p.fold[blk] = t;
     }
 }
 
@@ -191,19 +191,43 @@ __global__ __launch_bounds__(256) void k_init(Status* st, int64_t* cnt_fin, int6
     }
 }
 
-__global__ __launch_bounds__(1024) void k_energy_total(const double* energy, int64_t m, Status* st)
+__global__ __launch_bounds__(1024) void k_energy_total(const double* energy, int64_t m,
+                                                      const double2* fold, Status* st)
 {
     __shared__ double red[16];
+    __shared__ double2 redf[16];
     const int tid = threadIdx.x;
     double v = 0.0;
     for (int64_t i = tid; i < m; i += 1024) v += energy[i];
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    if ((tid & 63) == 0) red[tid >> 6] = v;
+    double2 f = make_double2(0.0, 0.0);
+    if (fold)
+        for (int b = tid; b < FOLD_BLOCKS; b += 1024) {
+            f.x += fold[b].x;
+            f.y += fold[b].y;
+        }
+    for (int off = 32; off > 0; off >>= 1) {
+        v += __shfl_xor(v, off);
+        f.x += __shfl_xor(f.x, off);
+        f.y += __shfl_xor(f.y, off);
+    }
+    if ((tid & 63) == 0) {
+        red[tid >> 6] = v;
+        redf[tid >> 6] = f;
+    }
     lds_barrier();
     if (tid == 0) {
         double s = 0.0;
-        for (int u = 0; u < 16; ++u) s += red[u];
+        double2 t = make_double2(0.0, 0.0);
+        for (int u = 0; u < 16; ++u) {
+            s += red[u];
+            t.x += redf[u].x;
+            t.y += redf[u].y;
+        }
         st->attributed_energy = s;
+        if (fold) {
+            st->trace_energy = t.x;
+            st->idle_energy = t.y;
+        }
     }
 }
 
@@ -236,9 +260,10 @@ hipError_t launch_fix(const FixParams& p, hipStream_t stream)
     return hipGetLastError();
 }
 
-hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream)
+hipError_t launch_energy_total(const double* energy, int64_t m, const double2* fold, Status* st,
+                               hipStream_t stream)
 {
-    hipLaunchKernelGGL(k_energy_total, dim3(1), dim3(1024), 0, stream, energy, m, st);
+    hipLaunchKernelGGL(k_energy_total, dim3(1), dim3(1024), 0, stream, energy, m, fold, st);
     return hipGetLastError();
 }
 

@@ -32,7 +32,7 @@ namespace {
 constexpr int WAVE = 64;
 constexpr int PER_LANE = CNT_BLOCK / WAVE;  // readings per lane and block
 constexpr int FOLD_THREADS = 256;
-constexpr int FOLD_BLOCKS = 64;
+constexpr int CFOLD_BLOCKS = 64;
 
 __device__ __forceinline__ bool finite(double x) { return fabs(x) < INFINITY; }
 
@@ -244,9 +244,9 @@ __global__ __launch_bounds__(FOLD_THREADS) void k_counter_fold(const CounterPara
                                                                int64_t nb_clear)
 {
     const int64_t blk = blockIdx.x;
-    if (blk < FOLD_BLOCKS) {
+    if (blk < CFOLD_BLOCKS) {
         __shared__ double2 red[FOLD_THREADS / WAVE];
-        const int64_t per = (p.nchunks + FOLD_BLOCKS - 1) / FOLD_BLOCKS;
+        const int64_t per = (p.nchunks + CFOLD_BLOCKS - 1) / CFOLD_BLOCKS;
         const int64_t lo = blk * per, hi = min(lo + per, p.nchunks);
         double inc = 0.0, clipped = 0.0;
         for (int64_t c = lo + threadIdx.x; c < hi; c += FOLD_THREADS) {
@@ -277,7 +277,7 @@ __global__ __launch_bounds__(FOLD_THREADS) void k_counter_fold(const CounterPara
         }
         return;
     }
-    const int64_t bc = blk - FOLD_BLOCKS;
+    const int64_t bc = blk - CFOLD_BLOCKS;
     for (int64_t h = bc * FOLD_THREADS + threadIdx.x; h <= (int64_t)p.H;
          h += nb_clear * FOLD_THREADS) {
         reinterpret_cast<ulonglong2*>(p.table)[h] = make_ulonglong2(~0ull, ~0ull);  // empty, no id
@@ -303,7 +303,7 @@ hipError_t launch_counter_fold(const CounterParams& p, hipStream_t stream)
 {
     int64_t nb_clear = p.table ? ((int64_t)p.H + FOLD_THREADS) / FOLD_THREADS : 0;
     if (nb_clear > 2048) nb_clear = 2048;
-    hipLaunchKernelGGL(k_counter_fold, dim3((unsigned)(FOLD_BLOCKS + nb_clear)), dim3(FOLD_THREADS),
+    hipLaunchKernelGGL(k_counter_fold, dim3((unsigned)(CFOLD_BLOCKS + nb_clear)), dim3(FOLD_THREADS),
                        0, stream, p, nb_clear);
     return hipGetLastError();
 }

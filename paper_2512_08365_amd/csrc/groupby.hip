@@ -81,6 +81,58 @@ __device__ __forceinline__ double interval_duration(const GroupParams& p, int64_
 
 }  // namespace
 
+// sum of v over a workgroup of nthreads (a multiple of 64) into thread 0's
+// return value; red holds one value per wave
+__device__ __forceinline__ double block_sum(double v, double* red, int nthreads)
+{
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    double t = 0.0;
+    if (threadIdx.x == 0)
+        for (int w = 0; w < nthreads / 64; ++w) t += red[w];
+    return t;
+}
+
+// the call's totals, by the first workgroup of its last kernel: attributed
+// energy from the chunk totals, trace and idle energy from k_fix's fold
+// partials (plain stores; no workgroup adds into a shared address)
+__device__ void write_totals(const GroupParams& p, double* red, int nthreads)
+{
+    double a = 0.0, w = 0.0, i = 0.0;
+    for (int c = threadIdx.x; c < p.nchunks; c += nthreads) a += p.ctot[c];
+    if (p.fold)
+        for (int b = threadIdx.x; b < FOLD_BLOCKS; b += nthreads) {
+            w += p.fold[b].x;
+            i += p.fold[b].y;
+        }
+    // the three sums reduced together: one pass over the waves
+    for (int off = 32; off > 0; off >>= 1) {
+        a += __shfl_xor(a, off);
+        w += __shfl_xor(w, off);
+        i += __shfl_xor(i, off);
+    }
+    if ((threadIdx.x & 63) == 0) {
+        red[3 * (threadIdx.x >> 6)] = a;
+        red[3 * (threadIdx.x >> 6) + 1] = w;
+        red[3 * (threadIdx.x >> 6) + 2] = i;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a = w = i = 0.0;
+        for (int v = 0; v < nthreads / 64; ++v) {
+            a += red[3 * v];
+            w += red[3 * v + 1];
+            i += red[3 * v + 2];
+        }
+        p.status->attributed_energy = a;
+        if (p.fold) {
+            p.status->trace_energy = w;
+            p.status->idle_energy = i;
+        }
+    }
+}
+
 // Insert the distinct keys of a prefix of the intervals.  Each workgroup first
 // de-duplicates its chunk in an LDS table; then every thread takes a few LDS
 // slots and inserts their keys into the global table, all of them side by side
@@ -344,6 +396,7 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
     }
     __syncthreads();
     const int64_t lo = (int64_t)c * p.chunk, hi = min(lo + p.chunk, p.m);
+    double ctot = 0.0;  // the chunk's total energy (all its intervals)
     for (int64_t i0 = lo + threadIdx.x; i0 < hi; i0 += (int64_t)AGG_BATCH * AGG_THREADS) {
         uint32_t sl[AGG_BATCH];
         double en[AGG_BATCH];
@@ -355,6 +408,7 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
         }
 #pragma unroll
         for (int k = 0; k < AGG_BATCH; ++k) {
+            ctot += en[k];
             const uint32_t id = resolve_id(p, sl[k]);
             const int64_t d = (id == NO_ID) ? -1 : (int64_t)id - r0;
             if (d < 0 || d >= nid) continue;
@@ -363,6 +417,11 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
         }
     }
     __syncthreads();
+    if (blockIdx.y == 0) {
+        __shared__ double red[AGG_THREADS / 64];
+        ctot = block_sum(ctot, red, AGG_THREADS);
+        if (threadIdx.x == 0) p.ctot[c] = ctot;
+    }
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
         p.pcnt[(int64_t)c * p.cap + r0 + v] = lcnt[v];
         p.psum[(int64_t)c * p.cap + r0 + v] = lsum[v];
@@ -376,6 +435,10 @@ constexpr int FIN_GROUPS = 16;
 
 __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupParams p)
 {
+    if (blockIdx.x == 0) {
+        __shared__ double red[3 * FIN_KEYS * FIN_GROUPS / 64];
+        write_totals(p, red, FIN_KEYS * FIN_GROUPS);
+    }
     if (p.kstat != p.status && blockIdx.x == 0 && threadIdx.x == 0) {
         // a key plan built beforehand: its counts become the call's
         p.status->n_unique = p.kstat->n_unique;
@@ -408,7 +471,6 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
     qc[grp][kl] = cnt;
     qs[grp][kl] = sum;
     __syncthreads();
-    double tot = 0.0;
     if (grp == 0 && id < nk) {
         cnt = 0;
         sum = 0.0;
@@ -422,12 +484,6 @@ __global__ __launch_bounds__(FIN_KEYS * FIN_GROUPS) void k_fin_sum(const GroupPa
             p.sum_out[r] = sum;
         }
         p.mean[id] = cnt ? sum / (double)cnt : 0.0;
-        tot = sum;
-    }
-    if (grp == 0) {
-        // this workgroup's rows, once into the attributed energy
-        for (int off = 32; off > 0; off >>= 1) tot += __shfl_xor(tot, off);
-        if (kl == 0 && tot != 0.0) atomicAdd(&p.status->attributed_energy, tot);
     }
 }
 
@@ -520,6 +576,15 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_one(const GroupParams p)
         sl[k] = (i < hi) ? p.slot[i] : NO_ID;
         en[k] = (i < hi) ? p.energy[i] : 0.0;
     }
+    if (blockIdx.y == 0) {
+        // the chunk's total energy (all its intervals, whatever their key)
+        __shared__ double red[AGG_THREADS / 64];
+        double v = 0.0;
+#pragma unroll
+        for (int k = 0; k < AGG_BATCH; ++k) v += en[k];
+        v = block_sum(v, red, AGG_THREADS);
+        if (threadIdx.x == 0) p.ctot[c] = v;
+    }
     const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (r0 >= nk) return;  // uniform
     const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
@@ -542,14 +607,19 @@ __global__ __launch_bounds__(AGG_THREADS) void k_agg_one(const GroupParams p)
         atomicAdd(&lsum[d[k]], en[k]);
     }
     __syncthreads();
+    // the chunk rows out; the table then holds each key's chunk mean, once
+    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
+        const uint32_t n = lcnt[v];
+        const double sm = lsum[v];
+        p.pcnt[(int64_t)c * p.cap + r0 + v] = n;
+        p.psum[(int64_t)c * p.cap + r0 + v] = sm;
+        lsum[v] = n ? sm / (double)n : 0.0;
+    }
+    __syncthreads();
     // each interval's deviation from its key's chunk mean
 #pragma unroll
     for (int k = 0; k < AGG_BATCH; ++k)
-        if (d[k] >= 0) en[k] -= lsum[d[k]] / (double)lcnt[d[k]];
-    for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
-        p.pcnt[(int64_t)c * p.cap + r0 + v] = lcnt[v];
-        p.psum[(int64_t)c * p.cap + r0 + v] = lsum[v];
-    }
+        if (d[k] >= 0) en[k] -= lsum[d[k]];
     __syncthreads();
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) lsum[v] = 0.0;
     __syncthreads();
@@ -613,6 +683,10 @@ constexpr int FO_KEYS = 32;
 constexpr int FO_GROUPS = 32;
 __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupParams p)
 {
+    if (blockIdx.x == 0) {
+        __shared__ double red[3 * FO_KEYS * FO_GROUPS / 64];
+        write_totals(p, red, FO_KEYS * FO_GROUPS);
+    }
     if (p.kstat != p.status && blockIdx.x == 0 && threadIdx.x == 0) {
         // a key plan built beforehand: its counts become the call's
         p.status->n_unique = p.kstat->n_unique;
@@ -650,7 +724,6 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
     qs[grp][kl] = sum;
     qdu[grp][kl] = du;
     __syncthreads();
-    double tot = 0.0;
     if (grp == 0) {
         cnt = 0;
         sum = 0.0;
@@ -668,11 +741,7 @@ __global__ __launch_bounds__(FO_KEYS * FO_GROUPS) void k_fin_one(const GroupPara
                 p.sum_out[r] = sum;
                 if (p.dur_out) p.dur_out[r] = du;
             }
-            tot = sum;
         }
-        // this workgroup's rows, once into the attributed energy
-        for (int off = FO_KEYS / 2; off > 0; off >>= 1) tot += __shfl_xor(tot, off);
-        if (kl == 0 && tot != 0.0) atomicAdd(&p.status->attributed_energy, tot);
     }
     __syncthreads();
     double m2 = 0.0;

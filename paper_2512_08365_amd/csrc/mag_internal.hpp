@@ -26,6 +26,10 @@ constexpr int AGG_THREADS = 1024;
 constexpr int AGG_IDS = 8192;       // key ids per LDS table (count u32 + sum f64)
 constexpr int AGG_MAX_CHUNKS = 256; // interval chunks (partial tables)
 
+// workgroups of k_fix that add up the per-run trace and idle energies; each
+// leaves its partial sum in a fold array that the call's last kernel adds up
+constexpr int FOLD_BLOCKS = 256;
+
 // cnt_fin entry that no workgroup wrote (no workgroup of any launch ended there)
 constexpr int64_t CNT_UNSET = -1;
 
@@ -109,6 +113,7 @@ struct FixParams {
     int64_t* end_idx;
     Status* status;
     const double2* part;  // per-run {trace, idle} energies (TileParams::part), added up here
+    double2* fold;        // [FOLD_BLOCKS] partial sums of part, one per fold workgroup
     int validate;
     // group-by state cleared for the grouping that follows (table NULL: none)
     unsigned long long* table;     // [2 (H+1)] {key, id} slots: all ones = empty / no id
@@ -149,6 +154,12 @@ struct GroupParams {
     // header of a key plan built beforehand otherwise (the aggregation then
     // copies the count and the overflow flag into the call's status)
     Status* kstat;
+    // the call's totals, written by its last kernel with plain stores:
+    // attributed energy = sum of ctot (one entry per interval chunk, written
+    // by the aggregation); trace and idle energy = sum of fold (NULL: set
+    // elsewhere)
+    double* ctot;         // [nchunks]
+    const double2* fold;  // [FOLD_BLOCKS] or NULL
 };
 
 // per-operator energy from a delayed cumulative energy counter
@@ -193,6 +204,10 @@ struct DiffParams {
     int32_t* cand_ia;
     int32_t* cand_ib;
     uint32_t* cand_rank;  // global rank of each candidate (counted by k_diff_rank)
+    uint32_t* blk;        // [n_groups][8] per join workgroup: joined, candidates, flagged,
+                          // waste, error bits
+    int64_t n_groups;     // join workgroups (diff_groups(na))
+    int64_t n_slots;      // candidate slots (diff_max_candidates(na, k))
     uint64_t* out_key;
     double* out_ratio;
     double* out_ea;
@@ -292,13 +307,18 @@ hipError_t launch_set_i64(int64_t* dst, int64_t v, hipStream_t stream);
 hipError_t launch_counter(const CounterParams& p, hipStream_t stream, hipEvent_t ev_start = nullptr,
                           hipEvent_t ev_stop = nullptr);
 hipError_t launch_counter_fold(const CounterParams& p, hipStream_t stream);
-hipError_t launch_energy_total(const double* energy, int64_t m, Status* st, hipStream_t stream);
+// attributed energy = sum of energy[m]; trace and idle energy from the fold
+// partials (fold NULL: left alone)
+hipError_t launch_energy_total(const double* energy, int64_t m, const double2* fold, Status* st,
+                               hipStream_t stream);
 hipError_t launch_diff(const DiffParams& p, hipStream_t stream);
 // comparisons per launch of a batch (their parameters travel as kernel arguments)
 constexpr int DIFF_BATCH = 8;
 // n comparisons sharing table A (p[c].ka/sa/ca/na/na_dev and k equal for all c)
 hipError_t launch_diff_batch(const DiffParams* p, int n, hipStream_t stream);
-// upper bound of the diff's stage-1 candidates for n_keys_a rows and top k
+// the diff's join workgroups for n_keys_a rows (at least one), and their
+// candidate slots for top k
+int64_t diff_groups(int64_t na);
 int64_t diff_max_candidates(int64_t na, int64_t k);
 
 int device_cu_count();
