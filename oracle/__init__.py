@@ -27,7 +27,8 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SO = os.path.join(_HERE, "_oracle.so")
+# MAG_ORACLE_SO: another build of oracle.c to load (the sanitizer runs in tests/)
+_SO = os.environ.get("MAG_ORACLE_SO") or os.path.join(_HERE, "_oracle.so")
 _lib = None
 
 
@@ -37,14 +38,16 @@ class OracleError(RuntimeError):
         self.code = code
 
 
-def build() -> str:
-    """Compile oracle.c into _oracle.so with gcc (always recompiles; IEEE fp64, no fast-math)."""
+def build(out: str | None = None, extra_flags=()) -> str:
+    """Compile oracle.c into _oracle.so (or `out`) with gcc (always recompiles;
+    IEEE fp64, no fast-math); extra_flags: e.g. sanitizer options."""
     src = os.path.join(_HERE, "oracle.c")
-    tmp = _SO + ".tmp"
+    so = out or _SO
+    tmp = so + ".tmp"
     subprocess.check_call(["gcc", "-O2", "-std=c99", "-fno-fast-math", "-ffp-contract=off",
-                           "-fPIC", "-shared", "-o", tmp, src, "-lm"])
-    os.replace(tmp, _SO)
-    return _SO
+                           *extra_flags, "-fPIC", "-shared", "-o", tmp, src, "-lm"])
+    os.replace(tmp, so)
+    return so
 
 
 def _load():

@@ -31,9 +31,21 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found: the HIP library cannot be built")
 
 
-def build(verbose: bool = False, jobs: int = 8) -> str:
+# host-side sanitizers (the device code is built as usual): each option right
+# after -Xarch_host, so that it applies to the host compilation only
+HOST_SANITIZE = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                 "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host",
+                 "-fno-omit-frame-pointer"]
+
+
+def build(verbose: bool = False, jobs: int = 8, out: str | None = None,
+          host_sanitize: bool = False) -> str:
+    """Build libmagneton.so (or `out`); host_sanitize: AddressSanitizer and
+    UndefinedBehaviorSanitizer on the host code (for the CPU test runs)."""
     cc = hipcc()
-    out_dir = os.path.join(ROOT, "_build")
+    lib = out or LIB
+    extra = HOST_SANITIZE if host_sanitize else []
+    out_dir = os.path.join(ROOT, "_build_san" if host_sanitize else "_build")
     os.makedirs(out_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(HERE, "csrc", "*.hip")))
     if not srcs:
@@ -41,7 +53,7 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
 
     def compile_one(src: str) -> str:
         obj = os.path.join(out_dir, os.path.basename(src) + ".o")
-        cmd = [cc, *COMMON, "-c", src, "-o", obj]
+        cmd = [cc, *COMMON, *extra, "-c", src, "-o", obj]
         if verbose:
             print(" ".join(cmd), flush=True)
         r = subprocess.run(cmd, capture_output=True, text=True)
@@ -51,13 +63,13 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
 
     with cf.ThreadPoolExecutor(max_workers=min(jobs, len(srcs))) as ex:
         objs = list(ex.map(compile_one, srcs))
-    tmp = LIB + ".tmp"
-    cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    tmp = lib + ".tmp"
+    cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *extra, "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

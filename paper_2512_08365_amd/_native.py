@@ -5,7 +5,9 @@ import ctypes
 import os
 
 HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(HERE, "libmagneton.so")
+# MAG_LIBRARY_SO: another build of the library to load (the host-sanitizer run
+# of the CPU tests); the default is the in-tree build
+LIB_PATH = os.environ.get("MAG_LIBRARY_SO") or os.path.join(HERE, "libmagneton.so")
 
 c_i64 = ctypes.c_int64
 c_vp = ctypes.c_void_p

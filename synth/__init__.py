@@ -15,18 +15,21 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SO = os.path.join(_HERE, "_synth.so")
+# MAG_SYNTH_SO: another build of synth.c to load (the sanitizer runs in tests/)
+_SO = os.environ.get("MAG_SYNTH_SO") or os.path.join(_HERE, "_synth.so")
 _lib = None
 
 
-def build() -> str:
-    """Compile synth.c into _synth.so with gcc (always recompiles)."""
+def build(out: str | None = None, extra_flags=()) -> str:
+    """Compile synth.c into _synth.so (or `out`) with gcc (always recompiles);
+    extra_flags: e.g. sanitizer options."""
     src = os.path.join(_HERE, "synth.c")
-    tmp = _SO + ".tmp"
-    subprocess.check_call(["gcc", "-O2", "-std=gnu99", "-fopenmp", "-fPIC", "-shared", "-o", tmp, src,
-                           "-lm"])
-    os.replace(tmp, _SO)
-    return _SO
+    so = out or _SO
+    tmp = so + ".tmp"
+    subprocess.check_call(["gcc", "-O2", "-std=gnu99", "-fopenmp", *extra_flags, "-fPIC", "-shared",
+                           "-o", tmp, src, "-lm"])
+    os.replace(tmp, so)
+    return so
 
 
 def _load():
