@@ -409,6 +409,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", type=int, default=WORKLOAD, choices=[1, 2, 3, 4, 5],
                     help="workload to time (default 3, the multi-stream 100M-sample trace)")
+    ap.add_argument("--schedule", choices=["overlap", "serial"], default="overlap",
+                    help="A/B workloads: overlap B's trace integration with A's grouping, or run "
+                         "A's whole call first (both with key maps built on a third stream)")
     ap.add_argument("--timed-side", choices=["a", "b", "none"], default="a",
                     help="which side's tile kernel carries the HIP timing events")
     ap.add_argument("--end-to-end", action="store_true",
@@ -551,10 +554,14 @@ def ab_bench(args, torch, mag, lib, N, synth):
     a_tiles = torch.cuda.Event()
     a_tiles.record(s1)  # creates the HIP event
     a_done = torch.cuda.Event()
+    a_done.record(s1)
+    serial = args.schedule == "serial"
     sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
-              tiles_done=ctypes.c_void_p(a_tiles.cuda_event))
+              tiles_done=ctypes.c_void_p(a_tiles.cuda_event), key_plan=serial)
+    # overlap: B's trace integration waits for A's; serial: for A's whole call
     sb = Side(B, lib, N, torch, k_cap, timed=args.timed_side == "b",
-              tiles_wait=ctypes.c_void_p(a_tiles.cuda_event), key_plan=True)
+              tiles_wait=ctypes.c_void_p((a_done if serial else a_tiles).cuda_event),
+              key_plan=True)
     s3 = torch.cuda.Stream()  # default priority: B's key map
     torch.cuda.synchronize()
     stream = ctypes.c_void_p(s1.cuda_stream)
@@ -577,6 +584,11 @@ def ab_bench(args, torch, mag, lib, N, synth):
         # else of each side overlaps the other; the diff reads both key counts
         # on the device, behind both attributions, on B's stream (A finishes
         # first); its synchronization is the step's one host wait
+        if serial:
+            # both key maps on the third stream, A's first, ahead of A's
+            # trace integration; each side's call then aggregates only, and
+            # B starts once A's call is complete
+            sa.build_plan(lib, stream_k)
         sa.attribute(lib, stream)
         a_done.record(s1)
         # B's key map depends on B's keys only: built on a third stream while
