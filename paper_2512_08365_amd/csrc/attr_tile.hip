@@ -300,9 +300,10 @@ __device__ __forceinline__ double sample_stage(const SampleRegs& r, int b, int L
     const KArgs kk = kargs();
     const int64_t j0 = (int64_t)b * T;
     const int cs = min(max(L - lane * C, 0), C);  // segments of this lane
+    const bool full = vector_tile(b);             // uniform: every lane has C segments
     double tv[C + 1];
     float pv[C + 1];
-    if (vector_tile(b)) {
+    if (full) {
 #pragma unroll
         for (int u = 0; u < C / 2; ++u) {
             tv[2 * u] = r.pt[u].x;
@@ -333,15 +334,24 @@ __device__ __forceinline__ double sample_stage(const SampleRegs& r, int b, int L
     if (kk->validate) {
         // every segment of the lane rises (the repeated last time of a short
         // lane does not), and a strictly increasing run whose ends are finite
-        // is finite throughout (a NaN fails every comparison)
-        int rising = 0;
+        // is finite throughout (a NaN fails every comparison).  The checks
+        // are collected as wave masks: the error bits are the wave's anyway
+        uint64_t tbad = __ballot(!(fabs(tv[0]) < INFINITY) || !(fabs(tv[C]) < INFINITY));
+        if (full) {
 #pragma unroll
-        for (int u = 0; u < C; ++u) rising += (tv[u + 1] > tv[u]) ? 1 : 0;
-        const bool t_ok = (rising == cs) & (fabs(tv[0]) < INFINITY) & (fabs(tv[C]) < INFINITY);
-        bool p_ok = true;
+            for (int u = 0; u < C; ++u) tbad |= __ballot(!(tv[u + 1] > tv[u]));
+        } else {
+            // rising as a positive difference (the same predicate, written
+            // apart from the whole-tile form above)
+            int rising = 0;
 #pragma unroll
-        for (int u = 0; u <= C; ++u) p_ok &= (pv[u] >= 0.0f) & (pv[u] < INFINITY);
-        err |= (t_ok ? 0u : ERR_TIMESTAMPS) | (p_ok ? 0u : ERR_POWER);
+            for (int u = 0; u < C; ++u) rising += (tv[u + 1] - tv[u] > 0.0) ? 1 : 0;
+            tbad |= __ballot(rising != cs);
+        }
+        uint64_t pbad = 0;
+#pragma unroll
+        for (int u = 0; u <= C; ++u) pbad |= __ballot(!((pv[u] >= 0.0f) & (pv[u] < INFINITY)));
+        err |= (tbad ? ERR_TIMESTAMPS : 0u) | (pbad ? ERR_POWER : 0u);
     }
     double f[C + 1];
     f[0] = 0.0;
@@ -392,31 +402,37 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     double sacc = 0.0;         // this tile's energy of the stream's open interval so far
     int sstarted = 0;          // the open interval started in this tile
     {
-        // cursor at the first tile: endpoints <= its start time (64-ary search,
-        // about four dependent loads per stream)
+        // cursor at the first tile: endpoints <= its start time.  Every stream
+        // is searched at once, each by its own group of GS = 64 / SP lanes (a
+        // GS-ary search: one dependent load per level for all streams)
+        constexpr int GS = WAVE / SP;
+        const int ga = lane / GS, gl = lane % GS;  // the lane's stream and rank in its group
         const double tau0 = p.t[(int64_t)b0 * T - p.base];
-        for (int a = 0; a < S; ++a) {
-            const int64_t off = p.ss.off[a];
-            const int64_t len = 2 * (p.ss.off[a + 1] - off);
-            int64_t lo = 0, hi = len;
-            while (hi - lo > WAVE) {
-                const int64_t step = (hi - lo + WAVE - 1) / WAVE;
-                const int64_t pr = lo + (int64_t)(lane + 1) * step - 1;
-                const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, off, pr) <= tau0);
-                const int c = __popcll(__ballot(ok));
+        const int64_t goff = (ga < S) ? p.ss.off[ga] : 0;
+        int64_t lo = 0, hi = (ga < S) ? 2 * (p.ss.off[ga + 1] - goff) : 0;
+        const uint64_t gmask = (GS == WAVE) ? ~0ull : ((1ull << (GS & 63)) - 1ull);
+        for (;;) {
+            const bool wide = hi - lo > GS;
+            if (__ballot(wide) == 0ull) break;
+            const int64_t step = wide ? (hi - lo + GS - 1) / GS : 1;
+            const int64_t pr = lo + (int64_t)(gl + 1) * step - 1;
+            const bool ok = wide && (pr < hi) && (endpoint_x(p.s, p.e, goff, pr) <= tau0);
+            const int c = __popcll((__ballot(ok) >> (ga * GS)) & gmask);
+            if (wide) {
                 const int64_t nlo = lo + (int64_t)c * step;
                 const int64_t nhi = min(hi, lo + (int64_t)(c + 1) * step - 1);
                 lo = min(nlo, hi);
                 hi = max(nhi, lo);
             }
-            const int64_t pr = lo + lane;
-            const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, off, pr) <= tau0);
-            const int c = __popcll(__ballot(ok));
-            const int64_t q = lo + c;
-            if (lane == a) {
-                sq = q;
-                slastx = (q > 0) ? endpoint_x(p.s, p.e, off, q - 1) : -INFINITY;
-            }
+        }
+        const int64_t pr = lo + gl;
+        const bool ok = (pr < hi) && (endpoint_x(p.s, p.e, goff, pr) <= tau0);
+        const int64_t q = lo + __popcll((__ballot(ok) >> (ga * GS)) & gmask);
+        // stream lane a takes group a's cursor, and the endpoint before it
+        const int64_t qa = bperm64(q, min(lane, SP - 1) * GS);
+        if (slane) {
+            sq = qa;
+            slastx = (qa > 0) ? endpoint_x(p.s, p.e, soff, qa - 1) : -INFINITY;
         }
     }
 
@@ -472,6 +488,9 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     unsigned err = 0u;
     double idle = 0.0;    // this lane's share of the idle energy
     double w_wave = 0.0;  // the wave's trace energy (uniform)
+    // 1 / lane: the equal share of a gap among mp active intervals is read
+    // from lane mp (mp <= S < 64)
+    const double inv_lane = (lane > 0) ? 1.0 / (double)lane : 0.0;
 
     for (int b = b0; b < b1; ++b) {
         const KArgs kk = kargs();
@@ -481,8 +500,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         // ---- samples: checks, segment energies, tile-local prefix, staging
         w_wave += sample_stage(sr, b, L, lane, sm.tF, sm.P, err);
         if (slane) {
-            const KArgs k = kargs();
-            pend_cnt = sreg(k->cnt) + ((int64_t)lane * (k->ld + 1) + b);
+            pend_cnt = sreg(kk->cnt) + ((int64_t)lane * (kk->ld + 1) + b);
             pend_cnt_v = sq;
         }
         sacc = 0.0;
@@ -713,7 +731,10 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
                 }
                 const double Q = same ? q_in : (pright + whole) + left;
                 const int mp = pe >> 16;
-                v = (has_gap && mp > 0) ? (kk->split ? Q * recip((double)mp) : Q) : 0.0;
+                // read with every lane active: a lane that is switched off
+                // cannot be read across lanes
+                const double inv_mp = bpermf(inv_lane, mp);
+                v = (has_gap && mp > 0) ? (kk->split ? Q * inv_mp : Q) : 0.0;
                 idle += (has_gap && mp == 0) ? Q : 0.0;
                 if (has_gap) sm.wx[pos] = v;
             }
