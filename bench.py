@@ -136,17 +136,22 @@ class Side:
     """Device copies of one side plus preallocated outputs and workspace."""
 
     def __init__(self, c, lib, N, torch, k_cap, timed=True, ready_event=None, tiles_wait=None,
-                 tiles_done=None, key_plan=False):
+                 tiles_done=None, key_plan=False, inputs=None):
         import numpy as np
         self.n = int(c["t"].shape[0])
         self.m = int(c["s"].shape[0])
         self.off = [int(x) for x in c["offsets"]]
         dev = "cuda"
-        self.t = torch.from_numpy(c["t"]).to(dev)
-        self.P = torch.from_numpy(c["P"]).to(dev)
-        self.s = torch.from_numpy(c["s"]).to(dev)
-        self.e = torch.from_numpy(c["e"]).to(dev)
-        self.key = torch.from_numpy(np.ascontiguousarray(c["key"]).view(np.int64)).to(dev)
+        if inputs is not None:
+            # another Side's device inputs (its own outputs and workspace)
+            self.t, self.P, self.s, self.e, self.key = (inputs.t, inputs.P, inputs.s, inputs.e,
+                                                        inputs.key)
+        else:
+            self.t = torch.from_numpy(c["t"]).to(dev)
+            self.P = torch.from_numpy(c["P"]).to(dev)
+            self.s = torch.from_numpy(c["s"]).to(dev)
+            self.e = torch.from_numpy(c["e"]).to(dev)
+            self.key = torch.from_numpy(np.ascontiguousarray(c["key"]).view(np.int64)).to(dev)
         self.energy = torch.empty(self.m, dtype=torch.float64, device=dev)
         self.si = torch.empty(self.m, dtype=torch.int64, device=dev)
         self.ei = torch.empty(self.m, dtype=torch.int64, device=dev)
@@ -409,6 +414,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", type=int, default=WORKLOAD, choices=[1, 2, 3, 4, 5],
                     help="workload to time (default 3, the multi-stream 100M-sample trace)")
+    ap.add_argument("--pipeline", type=int, default=1,
+                    help="A/B workloads: steps in flight (each on its own outputs and workspaces; "
+                         "1 = every step collected before the next is enqueued; deeper "
+                         "pipelines were measured slower: the next step's trace integration "
+                         "then shares the CUs with the previous step's short kernels)")
     ap.add_argument("--schedule", choices=["overlap", "serial"], default="overlap",
                     help="A/B workloads: overlap B's trace integration with A's grouping, or run "
                          "A's whole call first (both with key maps built on a third stream)")
@@ -541,7 +551,11 @@ def tile_roofline(tile_ms, n, m):
 
 
 def ab_bench(args, torch, mag, lib, N, synth):
-    """One step = attribute A, attribute B, top-k diff; one host wait per step."""
+    """One step = attribute A, attribute B, top-k diff.  Steps are pipelined
+    `--pipeline` deep: step i is enqueued (on its own set of outputs and
+    workspaces) before the host collects step i - depth + 1's results, so the
+    host's wait and the short kernels at a step's end overlap the next step's
+    work.  Every step's results are collected inside the timed region."""
     cfg = args.workload
     t0 = time.perf_counter()
     A, B = synth.sides(cfg, args.seed)
@@ -549,95 +563,149 @@ def ab_bench(args, torch, mag, lib, N, synth):
     sh = synth.shape(cfg)
     k_cap = 8192
     top = TOPK[cfg]
-    s1 = torch.cuda.current_stream()
-    s2 = torch.cuda.Stream()  # default priority
-    a_tiles = torch.cuda.Event()
-    a_tiles.record(s1)  # creates the HIP event
-    a_done = torch.cuda.Event()
-    a_done.record(s1)
-    serial = args.schedule == "serial"
-    sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
-              tiles_done=ctypes.c_void_p(a_tiles.cuda_event), key_plan=serial)
-    # overlap: B's trace integration waits for A's; serial: for A's whole call
-    sb = Side(B, lib, N, torch, k_cap, timed=args.timed_side == "b",
-              tiles_wait=ctypes.c_void_p((a_done if serial else a_tiles).cuda_event),
-              key_plan=True)
-    s3 = torch.cuda.Stream()  # default priority: B's key map
-    torch.cuda.synchronize()
-    stream = ctypes.c_void_p(s1.cuda_stream)
-    stream_b = ctypes.c_void_p(s2.cuda_stream)
-    stream_k = ctypes.c_void_p(s3.cuda_stream)
-    d_out = {k: torch.empty(top, dtype=dt, device="cuda") for k, dt in
-             (("key", torch.int64), ("ratio", torch.float64), ("ea", torch.float64),
-              ("eb", torch.float64), ("ca", torch.int64), ("cb", torch.int64))}
-    b = ctypes.c_size_t(0)
-    lib.mag_diff_workspace_size(k_cap, k_cap, top, ctypes.byref(b))
-    d_ws = torch.empty(int(b.value), dtype=torch.uint8, device="cuda")
-    ro = N.RankOut(d_out["key"].data_ptr(), d_out["ratio"].data_ptr(), d_out["ea"].data_ptr(),
-                   d_out["eb"].data_ptr(), d_out["ca"].data_ptr(), d_out["cb"].data_ptr(), top,
-                   0, 0, 0, 0)
-    tile_ms = []
-
-    def step(record):
-        # B's trace integration starts once A's is done (the two bandwidth-bound
-        # passes run back to back, each with the device to itself), everything
-        # else of each side overlaps the other; the diff reads both key counts
-        # on the device, behind both attributions, on B's stream (A finishes
-        # first); its synchronization is the step's one host wait
-        if serial:
-            # both key maps on the third stream, A's first, ahead of A's
-            # trace integration; each side's call then aggregates only, and
-            # B starts once A's call is complete
-            sa.build_plan(lib, stream_k)
-        sa.attribute(lib, stream)
-        a_done.record(s1)
-        # B's key map depends on B's keys only: built on a third stream while
-        # A's trace is integrated, so B's grouping after its own trace
-        # integration only aggregates
-        sb.build_plan(lib, stream_k)
-        sb.attribute(lib, stream_b)
-        s2.wait_event(a_done)
-        rc = lib.mag_diff(sa.kout.data_ptr(), ctypes.byref(sa.ks_dev), sb.kout.data_ptr(),
-                          ctypes.byref(sb.ks_dev), top, ctypes.byref(ro), d_ws.data_ptr(),
-                          d_ws.numel(), stream_b)
-        if rc != 0:
-            raise RuntimeError(f"mag_diff failed {rc}: {lib.mag_last_error().decode()}")
-        ta = sa.finish(lib, stream)
-        tb = sb.finish(lib, stream_b)
-        if record and args.timed_side != "none":
-            tile_ms.append(ta if args.timed_side == "a" else tb)
-
     flush = None
     if cfg == 2:
         flush_buf = torch.empty(MALL_FLUSH_BYTES // 4, dtype=torch.float32, device="cuda")
         flush = lambda: flush_buf.fill_(1.0)  # noqa: E731
-    for _ in range(args.warmup):
-        step(False)
+    # a cache flush before every step leaves nothing to overlap
+    depth = 1 if flush is not None else max(1, args.pipeline)
+    s1 = torch.cuda.current_stream()
+    s2 = torch.cuda.Stream()  # default priority
+    s3 = torch.cuda.Stream()  # default priority: B's key map
+    serial = args.schedule == "serial"
+    stream = ctypes.c_void_p(s1.cuda_stream)
+    stream_b = ctypes.c_void_p(s2.cuda_stream)
+    stream_k = ctypes.c_void_p(s3.cuda_stream)
+    b = ctypes.c_size_t(0)
+    lib.mag_diff_workspace_size(k_cap, k_cap, top, ctypes.byref(b))
+    d_bytes = int(b.value)
+
+    class Slot:
+        """One step's outputs, workspaces and events."""
+
+        def __init__(self):
+            self.a_tiles = torch.cuda.Event()
+            self.a_tiles.record(s1)  # creates the HIP event
+            self.a_done = torch.cuda.Event()
+            self.a_done.record(s1)
+            self.b_tiles = torch.cuda.Event()
+            self.b_tiles.record(s2)
+            self.d_out = {k: torch.empty(top, dtype=dt, device="cuda") for k, dt in
+                          (("key", torch.int64), ("ratio", torch.float64),
+                           ("ea", torch.float64), ("eb", torch.float64),
+                           ("ca", torch.int64), ("cb", torch.int64))}
+            self.d_ws = torch.empty(d_bytes, dtype=torch.uint8, device="cuda")
+            d = self.d_out
+            self.ro = N.RankOut(d["key"].data_ptr(), d["ratio"].data_ptr(), d["ea"].data_ptr(),
+                                d["eb"].data_ptr(), d["ca"].data_ptr(), d["cb"].data_ptr(), top,
+                                0, 0, 0, 0)
+            self.record = False
+
+        def sides(self, prev, first):
+            # the trace integrations never overlap: A's waits for the previous
+            # step's B, B's for this step's A (serial schedule: A's whole call)
+            self.sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
+                           tiles_wait=ctypes.c_void_p(prev.b_tiles.cuda_event),
+                           tiles_done=ctypes.c_void_p(self.a_tiles.cuda_event), key_plan=serial,
+                           inputs=first.sa if first else None)
+            self.sb = Side(B, lib, N, torch, k_cap, timed=args.timed_side == "b",
+                           tiles_wait=ctypes.c_void_p(
+                               (self.a_done if serial else self.a_tiles).cuda_event),
+                           tiles_done=ctypes.c_void_p(self.b_tiles.cuda_event),
+                           key_plan=True, inputs=first.sb if first else None)
+
+    slots = [Slot() for _ in range(depth)]
+    for j, x in enumerate(slots):
+        x.sides(slots[j - 1], slots[0] if j else None)
     torch.cuda.synchronize()
+    tile_ms = []
+
+    def enqueue(x, record):
+        # B's trace integration starts once A's is done (the two passes run
+        # back to back, each with the device to itself), everything else of
+        # each side overlaps the other; the diff reads both key counts on the
+        # device, behind both attributions, on B's stream (A finishes first)
+        if serial:
+            # both key maps on the third stream, A's first, ahead of A's
+            # trace integration; each side's call then aggregates only, and
+            # B starts once A's call is complete
+            x.sa.build_plan(lib, stream_k)
+        x.sa.attribute(lib, stream)
+        x.a_done.record(s1)
+        # B's key map depends on B's keys only: built on a third stream while
+        # A's trace is integrated, so B's grouping after its own trace
+        # integration only aggregates
+        x.sb.build_plan(lib, stream_k)
+        x.sb.attribute(lib, stream_b)
+        s2.wait_event(x.a_done)
+        rc = lib.mag_diff_async(x.sa.kout.data_ptr(), ctypes.byref(x.sa.ks_dev),
+                                x.sb.kout.data_ptr(), ctypes.byref(x.sb.ks_dev), top,
+                                ctypes.byref(x.ro), x.d_ws.data_ptr(), x.d_ws.numel(), stream_b)
+        if rc != 0:
+            raise RuntimeError(f"mag_diff_async failed {rc}: {lib.mag_last_error().decode()}")
+        x.record = record
+
+    def collect(x):
+        # the step's results on the host: key counts, errors, the ranking's counts
+        rc = lib.mag_diff_finish(x.d_ws.data_ptr(), ctypes.byref(x.ro))
+        if rc != 0:
+            raise RuntimeError(f"mag_diff_finish failed {rc}: {lib.mag_last_error().decode()}")
+        ta = x.sa.finish(lib, stream)
+        tb = x.sb.finish(lib, stream_b)
+        if x.record and args.timed_side != "none":
+            tile_ms.append(ta if args.timed_side == "a" else tb)
+
+    def run(n_steps, record, depth_):
+        inflight = []
+        for i in range(n_steps):
+            x = slots[i % depth_]
+            enqueue(x, record)
+            inflight.append(x)
+            if len(inflight) == depth_:
+                collect(inflight.pop(0))
+        while inflight:
+            collect(inflight.pop(0))
+
+    run(args.warmup, False, depth)
+    torch.cuda.synchronize()
+    extra = {"pipeline_depth": depth}
     if flush is None:
         t0 = time.perf_counter()
-        for _ in range(args.steps):
-            step(True)
+        run(args.steps, True, depth)
         torch.cuda.synchronize()
         dt = time.perf_counter() - t0
         timing = "wall clock over the timed steps"
+        if depth > 1:
+            # the same steps one at a time (each collected before the next is enqueued)
+            t1 = time.perf_counter()
+            run(args.steps, False, 1)
+            torch.cuda.synchronize()
+            extra["ms_per_step_unpipelined"] = (time.perf_counter() - t1) / args.steps * 1e3
     else:
         # the cache is flushed before every step, outside the timed region
         evs = []
+        x = slots[0]
         for _ in range(args.steps):
             flush()
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(s1)
-            step(True)
+            s2.wait_stream(s1)
+            s3.wait_stream(s1)
+            enqueue(x, True)
+            s1.wait_stream(s2)
             e1.record(s1)
+            collect(x)
             evs.append((e0, e1))
         torch.cuda.synchronize()
         dt = sum(a.elapsed_time(b_) for a, b_ in evs) * 1e-3
         timing = "HIP events around each step; a 512 MB write flushes the Infinity Cache before it"
     sec_per_step = dt / args.steps
-    log(f"[bench] {args.steps} steps in {dt:.4f} s -> {sec_per_step * 1e3:.4f} ms/step; "
-        f"keys A={sa.ks.n_keys} B={sb.ks.n_keys} joined={ro.n_join}")
-    extra = {"timing": timing}
+    x = slots[0]
+    log(f"[bench] {args.steps} steps in {dt:.4f} s -> {sec_per_step * 1e3:.4f} ms/step "
+        f"(pipeline depth {depth}); keys A={x.sa.ks.n_keys} B={x.sb.ks.n_keys} "
+        f"joined={x.ro.n_join}" + (f"; one step at a time {extra['ms_per_step_unpipelined']:.4f} ms"
+                                   if "ms_per_step_unpipelined" in extra else ""))
+    extra["timing"] = timing
     if tile_ms:
         extra["roofline"] = tile_roofline(tile_ms, sh["n"], sh["m"])
     res = result_line(args, cfg, sh, 2, sec_per_step, extra)

@@ -426,6 +426,30 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
              size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * mag_diff_async -- mag_diff without the wait (Section 6.1's comparison, for
+ * callers that keep several comparisons in flight): the arguments, checks and
+ * device outputs are mag_diff's, written in `stream` order; the call returns
+ * once the kernels and a copy of the call's status block are enqueued.  The
+ * host counts of *out (n_out, n_only_a, n_only_b, n_join) are filled by
+ * mag_diff_finish, which must be called before the workspace is used again
+ * (one unfinished call per workspace; another call on it returns
+ * MAG_E_STATE).  A device-detected error (MAG_E_KEYS) is returned by
+ * mag_diff_finish.  Errors: as mag_diff, and MAG_E_STATE.
+ */
+int mag_diff_async(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+                   const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream);
+
+/*
+ * mag_diff_finish -- waits for the mag_diff_async call on `workspace` (the
+ * stream it was enqueued on is synchronized) and fills the host counts of
+ * *out.  Must run on the host thread that made the call.  Errors: MAG_E_NULL,
+ * MAG_E_STATE (no unfinished mag_diff_async call on this workspace), MAG_E_KEYS,
+ * MAG_E_HIP.
+ */
+int mag_diff_finish(const void* workspace, mag_rank_out* out);
+
+/*
  * mag_diff_batch -- one baseline table A ranked against several candidate
  * tables B_0 .. B_{n-1} (Section 6.1 evaluates each case by comparing a
  * system against its more efficient counterparts, Table

@@ -380,9 +380,11 @@ def attribute_counter(t, C, s, e, keys=None, *, delay: float = 0.0, replays=None
     return build()
 
 
-def diff(a: dict, b: dict, k: int, workspace=None):
+def diff(a: dict, b: dict, k: int, workspace=None, asynchronous: bool = False):
     """Rank keys present in both per-key tables by (E_B - E_A)/E_A (descending,
-    ties by ascending key).  a/b: per-key dicts as returned by attribute()."""
+    ties by ascending key).  a/b: per-key dicts as returned by attribute().
+    asynchronous: enqueue only (mag_diff_async) and return a PendingDiff whose
+    result() waits (mag_diff_finish) and returns what diff() returns."""
     lib = _lib()
     dev = a["keys"].device
     na, nb = int(a["keys"].shape[0]), int(b["keys"].shape[0])
@@ -402,14 +404,36 @@ def diff(a: dict, b: dict, k: int, workspace=None):
                     _dev_ptr(b["count"], torch.int64, "b.count"), nb, nb)
     ro = N.RankOut(key.data_ptr(), ratio.data_ptr(), ea.data_ptr(), eb.data_ptr(), ca.data_ptr(),
                    cb.data_ptr(), cap, 0, 0, 0, 0)
-    rc = lib.mag_diff(_dev_ptr(a["keys"], torch.int64, "a.keys"), ctypes.byref(sa),
-                      _dev_ptr(b["keys"], torch.int64, "b.keys"), ctypes.byref(sb), int(k),
-                      ctypes.byref(ro), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
+    call = lib.mag_diff_async if asynchronous else lib.mag_diff
+    rc = call(_dev_ptr(a["keys"], torch.int64, "a.keys"), ctypes.byref(sa),
+              _dev_ptr(b["keys"], torch.int64, "b.keys"), ctypes.byref(sb), int(k),
+              ctypes.byref(ro), workspace.data_ptr(), workspace.numel(), _stream_handle(dev))
     _check(rc)
-    r = int(ro.n_out)
-    return {"key": key[:r], "ratio": ratio[:r], "energy_a": ea[:r], "energy_b": eb[:r],
-            "count_a": ca[:r], "count_b": cb[:r], "n_only_a": int(ro.n_only_a),
-            "n_only_b": int(ro.n_only_b), "n_join": int(ro.n_join)}
+
+    def collect():
+        r = int(ro.n_out)
+        return {"key": key[:r], "ratio": ratio[:r], "energy_a": ea[:r], "energy_b": eb[:r],
+                "count_a": ca[:r], "count_b": cb[:r], "n_only_a": int(ro.n_only_a),
+                "n_only_b": int(ro.n_only_b), "n_join": int(ro.n_join)}
+
+    if not asynchronous:
+        return collect()
+    return PendingDiff(lib, workspace, ro, collect)
+
+
+class PendingDiff:
+    """An enqueued comparison (diff(..., asynchronous=True)); result() waits
+    for it once (mag_diff_finish) and returns the ranking."""
+
+    def __init__(self, lib, workspace, ro, collect):
+        self._lib, self._ws, self._ro, self._collect = lib, workspace, ro, collect
+        self._done = None
+
+    def result(self) -> dict:
+        if self._done is None:
+            _check(self._lib.mag_diff_finish(self._ws.data_ptr(), ctypes.byref(self._ro)))
+            self._done = self._collect()
+        return self._done
 
 
 def diff_batch(a: dict, bs: list, k: int, workspace=None) -> list:

@@ -44,7 +44,8 @@ EXPORTED = (
     "mag_key_plan_size", "mag_key_plan_build",
     "mag_attribute_finish",
     "mag_counter_workspace_size", "mag_attribute_counter",
-    "mag_diff_workspace_size", "mag_diff", "mag_diff_batch_workspace_size", "mag_diff_batch",
+    "mag_diff_workspace_size", "mag_diff", "mag_diff_async", "mag_diff_finish",
+    "mag_diff_batch_workspace_size", "mag_diff_batch",
     "mag_detect_workspace_size", "mag_detect",
     "mag_invariant_count", "mag_invariants_workspace_size", "mag_invariants",
     "mag_match_workspace_size", "mag_match", "mag_match_subgraphs",
@@ -150,6 +151,10 @@ def load(path: str = LIB_PATH):
     lib.mag_diff.argtypes = [c_vp, P(KeyStats), c_vp, P(KeyStats), c_i64, P(RankOut), c_vp,
                              ctypes.c_size_t, c_vp]
     lib.mag_diff.restype = ctypes.c_int
+    lib.mag_diff_async.argtypes = lib.mag_diff.argtypes
+    lib.mag_diff_async.restype = ctypes.c_int
+    lib.mag_diff_finish.argtypes = [c_vp, P(RankOut)]
+    lib.mag_diff_finish.restype = ctypes.c_int
     lib.mag_diff_batch_workspace_size.argtypes = [c_i64, ctypes.c_int32, c_i64,
                                                   P(ctypes.c_size_t)]
     lib.mag_diff_batch_workspace_size.restype = ctypes.c_int

@@ -212,6 +212,11 @@ struct TimerSlot {
     bool status_pending = false;   // an asynchronous call copied its status here
     hipStream_t stream = nullptr;  // the stream that call was enqueued on
     mag::Status* host_status = nullptr;  // pinned host copy of the status block
+    // an asynchronous mag_diff on this workspace: what its conclusion needs
+    // besides the status block (table sizes or bounds, rows asked for, whether
+    // a size is read on the device)
+    bool diff = false, diff_dev = false;
+    int64_t diff_na = 0, diff_nb = 0, diff_k = 0;
     uint64_t used = 0;             // last use, for the recycling order
     bool busy() const { return pending || status_pending; }
 };
@@ -1580,30 +1585,37 @@ int diff_params(const uint64_t* keysA, const mag_key_stats* statsA, const uint64
 }
 
 
-// a comparison's result from its status block
-int conclude_diff(const mag::DiffParams& p, const mag::Status& st, mag_rank_out* out)
+// a comparison's result from its status block: na, nb the table sizes (or
+// their bounds when dev: sizes read on the device), k the rows asked for
+int conclude_diff(int64_t na, int64_t nb, int64_t k, bool dev, const mag::Status& st,
+                  mag_rank_out* out)
 {
     if (st.err & mag::ERR_KEYS) return fail(MAG_E_KEYS, "key table not strictly ascending");
-    const bool dev = p.na_dev || p.nb_dev;
-    const int64_t ra = dev ? (int64_t)st.diff_na : p.na;
-    const int64_t rb = dev ? (int64_t)st.diff_nb : p.nb;
+    const int64_t ra = dev ? (int64_t)st.diff_na : na;
+    const int64_t rb = dev ? (int64_t)st.diff_nb : nb;
     out->n_join = st.n_join;
-    out->n_out = std::min<int64_t>(p.k, st.n_join);
+    out->n_out = std::min<int64_t>(k, st.n_join);
     out->n_only_a = ra - st.n_join;
     out->n_only_b = rb - st.n_join;
     return MAG_OK;
 }
+int conclude_diff(const mag::DiffParams& p, const mag::Status& st, mag_rank_out* out)
+{
+    return conclude_diff(p.na, p.nb, p.k, p.na_dev || p.nb_dev, st, out);
+}
 
-// the join and ranking shared by mag_diff and mag_detect; p's detection fields
-// are set by the caller; the status block is returned in *st
-int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
-             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p,
-             void* workspace, size_t workspace_bytes, hipStream_t stream, mag::Status* st)
+// the checks and kernels of one comparison (mag_diff, mag_diff_async,
+// mag_detect; p's detection fields are set by the caller)
+int enqueue_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+                 const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p,
+                 void* workspace, size_t workspace_bytes, hipStream_t stream)
 {
     int rc = diff_params(keysA, statsA, keysB, statsB, k, out, p);
     if (rc != MAG_OK) return rc;
     if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
     if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
+    if (unfinished(workspace))
+        return fail(MAG_E_STATE, "an asynchronous call on this workspace is not finished");
     size_t need = 0;
     mag_diff_workspace_size(p.na, p.nb, k, &need);
     if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
@@ -1614,6 +1626,17 @@ int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     hipError_t e;
     // every field of the status block the call reads is written by its kernels
     if ((e = mag::launch_diff(p, stream)) != hipSuccess) return hip_fail(e, "diff kernels");
+    return MAG_OK;
+}
+
+// the join and ranking, waited for; the status block is returned in *st
+int run_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+             const mag_key_stats* statsB, int64_t k, mag_rank_out* out, mag::DiffParams& p,
+             void* workspace, size_t workspace_bytes, hipStream_t stream, mag::Status* st)
+{
+    int rc = enqueue_diff(keysA, statsA, keysB, statsB, k, out, p, workspace, workspace_bytes,
+                          stream);
+    if (rc != MAG_OK) return rc;
     rc = read_status(p.status, stream, st);
     if (rc != MAG_OK) return rc;
     return conclude_diff(p, *st, out);
@@ -1640,6 +1663,47 @@ int mag_diff(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t*
     mag::Status st;
     return run_diff(keysA, statsA, keysB, statsB, k, out, p, workspace, workspace_bytes, stream,
                     &st);
+}
+
+int mag_diff_async(const uint64_t* keysA, const mag_key_stats* statsA, const uint64_t* keysB,
+                   const mag_key_stats* statsB, int64_t k, mag_rank_out* out, void* workspace,
+                   size_t workspace_bytes, hipStream_t stream)
+{
+    g_last_error[0] = 0;
+    mag::DiffParams p{};
+    int rc = enqueue_diff(keysA, statsA, keysB, statsB, k, out, p, workspace, workspace_bytes,
+                          stream);
+    if (rc != MAG_OK) return rc;
+    // the status block (first in the workspace) goes to the pinned buffer of
+    // the workspace's record, in stream order
+    TimerSlot* t = timer_slot(workspace, true);
+    if (!t || !t->host_status)
+        return fail(MAG_E_HIP, "no host buffer for the status of an asynchronous call");
+    const hipError_t e =
+        hipMemcpyAsync(t->host_status, p.status, sizeof(mag::Status), hipMemcpyDeviceToHost, stream);
+    if (e != hipSuccess) return hip_fail(e, "status copy");
+    t->status_pending = true;
+    t->stream = stream;
+    t->diff = true;
+    t->diff_dev = p.na_dev || p.nb_dev;
+    t->diff_na = p.na;
+    t->diff_nb = p.nb;
+    t->diff_k = k;
+    return MAG_OK;
+}
+
+int mag_diff_finish(const void* workspace, mag_rank_out* out)
+{
+    g_last_error[0] = 0;
+    if (!workspace || !out) return fail(MAG_E_NULL, "workspace/out is NULL");
+    TimerSlot* t = timer_slot(workspace, false);
+    if (!t || !t->status_pending || !t->diff || !t->host_status)
+        return fail(MAG_E_STATE, "no unfinished mag_diff_async call on this workspace");
+    t->status_pending = false;
+    t->diff = false;
+    hipError_t e;
+    if ((e = hipStreamSynchronize(t->stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    return conclude_diff(t->diff_na, t->diff_nb, t->diff_k, t->diff_dev, *t->host_status, out);
 }
 
 int mag_diff_batch_workspace_size(int64_t n_keys_a, int32_t n_candidates, int64_t k,

@@ -58,12 +58,16 @@ __global__ void k_svd_clear(double* g, int64_t n)
 
 // One workgroup of 16 waves per (task, 64 x 64 block of the upper triangle,
 // chunk of GRAM_CHUNK columns).  Each 64-column step stages the block's 64
-// rows of each operand in LDS as fp64 (one global load per element, rows
-// fastest across threads, so a unit-stride row mode gives coalesced loads);
-// wave w then multiplies tile (w / 4, w % 4) from LDS with 16 MFMA steps.
+// rows of each operand in LDS as fp64, eight gathered elements per thread;
+// wave w then multiplies tile (w / 4, w % 4) from LDS with 16 MFMA steps
+// while the next step's elements are in flight.  The gather runs along
+// whichever side of the unfolding has unit stride (the rows when the K side's
+// last mode is the tensor's last, else the columns), so 64 neighbouring
+// threads read 256 contiguous bytes.
 constexpr int GB = 64;              // block side
 constexpr int GSTEP = 64;           // columns staged per step
 constexpr int GTHREADS = 1024;      // 16 waves: one per 16 x 16 tile of the block
+constexpr int GPER = 2 * GB * GSTEP / GTHREADS;  // staged elements per thread and step
 
 __global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_tasks,
                                                    int64_t n_items)
@@ -98,22 +102,42 @@ __global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_t
         const int64_t row = (int64_t)(side ? bj : bi) * GB + r;
         roff[side][r] = (row < t.K) ? mode_offset((uint32_t)row, t.nk, t.kdim, t.kstr) : -1;
     }
+    // neighbouring threads take neighbouring columns unless the rows are the
+    // unit-stride side (uniform)
+    const bool cols_fast = t.kstr[t.nk - 1] != 1;
     __syncthreads();
+    // staged element u of this thread: operand, row and column of the step
+    auto slot = [&](int u, int& side, int& rr, int& c) {
+        const int q = tid + u * GTHREADS;
+        side = q / (GB * GSTEP);
+        const int rem = q % (GB * GSTEP);
+        rr = cols_fast ? rem / GSTEP : rem % GB;
+        c = cols_fast ? rem % GSTEP : rem / GB;
+    };
+    float stage[GPER];
+    auto fetch = [&](int64_t s0) {
+        const int cols = (int)min((int64_t)GSTEP, b1 - s0);
+#pragma unroll
+        for (int u = 0; u < GPER; ++u) {
+            int side, rr, c;
+            slot(u, side, rr, c);
+            const int64_t ro = roff[side][rr];
+            stage[u] = (c < cols && ro >= 0) ? t.data[ro + loff[s0 - b0 + c]] : 0.0f;
+        }
+    };
     const int ti = wv / 4, tj = wv % 4;  // this wave's tile inside the block
     const int r = lane & 15, kq = lane >> 4;
     d4 acc = {0.0, 0.0, 0.0, 0.0};
+    fetch(b0);
     for (int64_t s0 = b0; s0 < b1; s0 += GSTEP) {
-        const int cols = (int)min((int64_t)GSTEP, b1 - s0);
-        // stage: element (row, column) of each operand; rows fastest
-        for (int q = tid; q < 2 * GB * GSTEP; q += GTHREADS) {
-            const int side = q / (GB * GSTEP), rem = q % (GB * GSTEP);
-            const int c = rem / GB, rr = rem % GB;
-            const int64_t ro = roff[side][rr];
-            double x = 0.0;
-            if (c < cols && ro >= 0) x = (double)t.data[ro + loff[s0 - b0 + c]];
-            (side ? xb : xa)[c][rr] = x;
+#pragma unroll
+        for (int u = 0; u < GPER; ++u) {
+            int side, rr, c;
+            slot(u, side, rr, c);
+            (side ? xb : xa)[c][rr] = (double)stage[u];  // fp32 widened exactly
         }
         __syncthreads();
+        if (s0 + GSTEP < b1) fetch(s0 + GSTEP);  // in flight during the products
 #pragma unroll 4
         for (int c = 0; c < GSTEP; c += 4) {
             const double a = xa[c + kq][ti * 16 + r];
@@ -134,14 +158,17 @@ __global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_t
     }
 }
 
-__device__ double block_sum(double v, double* red)
+// sum of v over the workgroup with one barrier: red holds two rows of
+// per-wave partials used alternately (flip selects the row, toggled here), so
+// a wave that is still reading one row cannot see the next call's writes
+__device__ double block_sum(double v, double (*red)[EIG_THREADS / 64], int& flip)
 {
     for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
-    __syncthreads();  // earlier readers of red are done
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    if ((threadIdx.x & 63) == 0) red[flip][threadIdx.x >> 6] = v;
     __syncthreads();
     double s = 0.0;
-    for (int u = 0; u < EIG_THREADS / 64; ++u) s += red[u];
+    for (int u = 0; u < EIG_THREADS / 64; ++u) s += red[flip][u];
+    flip ^= 1;
     return s;
 }
 
@@ -163,11 +190,17 @@ constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in 
 typedef __attribute__((address_space(3))) double lds_f64;
 
 template <class Ptr>
-__device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double (*w2)[EIG_THREADS / 2],
-                               double* d, double* e2, double* red)
+__device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* wp, double* d,
+                               double* e2, double (*red)[EIG_THREADS / 64])
 {
     const int tid = threadIdx.x;
+    int flip = 0;
     // Householder reduction: step k annihilates column k below the subdiagonal
+    // with H = I - beta u u^T, u = (x0 - alpha, x1, ..., x_{m-1}), and
+    // A_sub <- H A_sub H = A_sub - u w^T - w u^T, w = p - K u, p = beta A_sub u,
+    // K = beta (p . u) / 2.  u's first entry lives in a register (v[0] keeps
+    // x0), so a step has three barriers: after the column, after p, after
+    // the update
     for (int k = 0; k + 2 < n; ++k) {
         const int m = n - k - 1;
         double tail = 0.0;
@@ -176,33 +209,37 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double (*w2)[
             v[i] = x;
             if (i > 0) tail += x * x;
         }
-        tail = block_sum(tail, red);  // (its barriers publish v)
+        tail = block_sum(tail, red, flip);  // (its barrier publishes v)
         const double x0 = v[0];
         if (tid == 0) d[k] = A[(size_t)k * n + k];
         if (!(tail > 0.0)) {
             if (tid == 0) e2[k] = x0 * x0;
-            __syncthreads();
+            __syncthreads();  // every thread has read x0 before v is rewritten
             continue;
         }
+        // every thread derives the reflector's scalars itself
         const double alpha = (x0 >= 0.0) ? -sqrt(x0 * x0 + tail) : sqrt(x0 * x0 + tail);
-        const double v0 = x0 - alpha;
-        const double beta = 2.0 / (v0 * v0 + tail);
+        const double u0 = x0 - alpha;
+        const double beta = 2.0 / (u0 * u0 + tail);
         if (tid == 0) e2[k] = alpha * alpha;
-        __syncthreads();
-        if (tid == 0) v[0] = v0;
-        __syncthreads();
-        // p = beta A_sub v (columns by threads: row j of A is read across
-        // threads); with at most half as many columns as threads, two threads
-        // share a column, each taking half of the rows
-        const bool split = m <= EIG_THREADS / 2;
-        const int ci = split ? tid % (EIG_THREADS / 2) : tid;
-        const int hf = split ? tid / (EIG_THREADS / 2) : 0;
-        const int jlo = split ? hf * (m / 2) : 0, jhi = split ? (hf ? m : m / 2) : m;
+        // p = beta A_sub u, columns across threads (row j of A is read across
+        // neighbouring threads); with fewer columns than threads, tpc threads
+        // share a column, each taking a slice of its rows, and the slices'
+        // sums are added in slice order
+        int tpc = 1;  // uniform
+        while (tpc < 16 && 2 * tpc * m <= EIG_THREADS) tpc *= 2;
+        const int ncol = EIG_THREADS / tpc;
+        const int ci = tid % ncol, hf = tid / ncol;
+        const int jlo = hf * m / tpc, jhi = (hf + 1) * m / tpc;
         double pv = 0.0;
-        for (int i = ci; i < m; i += (split ? m + 1 : EIG_THREADS)) {
+        for (int i = ci; i < m; i += ncol) {
             const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
             double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
             int j = jlo;
+            if (j == 0 && j < jhi) {
+                s0 = col[0] * u0;
+                j = 1;
+            }
             for (; j + 4 <= jhi; j += 4) {  // four independent loads in flight
                 s0 += col[(size_t)j * n] * v[j];
                 s1 += col[(size_t)(j + 1) * n] * v[j + 1];
@@ -210,31 +247,41 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double (*w2)[
                 s3 += col[(size_t)(j + 3) * n] * v[j + 3];
             }
             for (; j < jhi; ++j) s0 += col[(size_t)j * n] * v[j];
-            const double part = beta * ((s0 + s1) + (s2 + s3));
-            if (split) {
-                w2[hf][i] = part;
+            const double part = (s0 + s1) + (s2 + s3);
+            if (tpc > 1) {
+                wp[hf * ncol + i] = part;
             } else {
-                w[i] = part;
-                pv += part * v[i];
+                w[i] = beta * part;
+                pv += beta * part * (i == 0 ? u0 : v[i]);
             }
         }
-        if (split) {
+        if (tpc > 1) {
             __syncthreads();
             if (hf == 0 && ci < m) {
-                w[ci] = w2[0][ci] + w2[1][ci];
-                pv = w[ci] * v[ci];
+                double sum = 0.0;
+                for (int h = 0; h < tpc; ++h) sum += wp[h * ncol + ci];
+                w[ci] = beta * sum;
+                pv = w[ci] * (ci == 0 ? u0 : v[ci]);
             }
         }
-        const double K2 = 0.5 * beta * block_sum(pv, red);
-        for (int i = tid; i < m; i += EIG_THREADS) w[i] -= K2 * v[i];
-        __syncthreads();
-        // A_sub -= v w^T + w v^T (each thread walks its columns down the rows;
-        // the rows of one column are independent, so the loop is unrolled)
-        for (int i = ci; i < m; i += (split ? m + 1 : EIG_THREADS)) {
+        const double K2 = 0.5 * beta * block_sum(pv, red, flip);  // (publishes p in w)
+        // A_sub -= u w^T + w u^T with w_j = p_j - K2 u_j formed as it is used
+        // (each thread walks its column slice down the rows; the rows of one
+        // column are independent, so the loop is unrolled)
+        for (int i = ci; i < m; i += ncol) {
             const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
-            const double vi = v[i], wi = w[i];
-#pragma unroll 8
-            for (int j = jlo; j < jhi; ++j) col[(size_t)j * n] -= v[j] * wi + w[j] * vi;
+            const double ui = (i == 0) ? u0 : v[i];
+            const double wi = w[i] - K2 * ui;
+            int j = jlo;
+            if (j == 0 && j < jhi) {
+                col[0] -= u0 * wi + (w[0] - K2 * u0) * ui;
+                j = 1;
+            }
+#pragma unroll 4
+            for (; j < jhi; ++j) {
+                const double uj = v[j];
+                col[(size_t)j * n] -= uj * wi + (w[j] - K2 * uj) * ui;
+            }
         }
         __syncthreads();
     }
@@ -253,18 +300,18 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
 {
     __shared__ double v[SVD_MAX_K], w[SVD_MAX_K];
     __shared__ double d[SVD_MAX_K], e2[SVD_MAX_K];
-    __shared__ double red[EIG_THREADS / 64];
+    __shared__ double red[2][EIG_THREADS / 64];
     __shared__ double As[EIG_LDS_K * EIG_LDS_K];
-    __shared__ double w2[2][EIG_THREADS / 2];
+    __shared__ double wp[EIG_THREADS];
     const SvdTask& t = tasks[blockIdx.x];
     const int n = (int)t.K;
     const int tid = threadIdx.x;
     if (n <= EIG_LDS_K) {
         for (int q = tid; q < n * n; q += EIG_THREADS) As[q] = t.gram[q];
         __syncthreads();
-        tridiagonalize((lds_f64*)As, n, v, w, w2, d, e2, red);  // ds_ instructions
+        tridiagonalize((lds_f64*)As, n, v, w, wp, d, e2, red);  // ds_ instructions
     } else {
-        tridiagonalize(t.gram, n, v, w, w2, d, e2, red);
+        tridiagonalize(t.gram, n, v, w, wp, d, e2, red);
     }
     // Gershgorin interval and the smallest pivot allowed in a Sturm count
     double glo = INFINITY, ghi = -INFINITY, emax = 0.0;
@@ -278,27 +325,36 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
     const double pivmin = 0x1p-1000 * fmax(1.0, emax);
     glo -= 2.0 * DBL_EPSILON * span + pivmin;
     ghi += 2.0 * DBL_EPSILON * span + pivmin;
-    for (int k = tid; k < n; k += EIG_THREADS) {
-        // the k-th smallest eigenvalue: count(lo) <= k < count(hi); each
-        // round counts at four interior points (four independent Sturm
-        // chains side by side) and keeps the fifth of the interval holding it
+    // G neighbouring threads per eigenvalue (G a power of two, uniform), each
+    // counting at four of the round's 4 G interior points.  The counts are
+    // bound by instruction issue (a reciprocal per step of each chain), so G
+    // grows only until about one wave per SIMD is busy: more threads per
+    // eigenvalue take fewer rounds but more work in all
+    int G = 1;
+    while (G < 8 && 2 * G * n <= 256) G *= 2;
+    const int g = tid % G;
+    for (int k = tid / G; k < n; k += EIG_THREADS / G) {
+        // the k-th smallest eigenvalue: count(lo) <= k < count(hi); a round
+        // keeps the one of its 4 G + 1 parts of the interval holding it (the
+        // group's threads agree on lo and hi after every round)
         double lo = glo, hi = ghi;
         for (int it = 0; it < 64; ++it) {
             if (!(hi - lo > 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin)) break;
-            const double h = (hi - lo) * 0.2;
+            const double h = (hi - lo) / (double)(4 * G + 1);
             double x[4], q[4];
             int c[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
-                x[u] = lo + h * (double)(u + 1);
+                x[u] = lo + h * (double)(4 * g + u + 1);
                 q[u] = d[0] - x[u];
                 if (fabs(q[u]) < pivmin) q[u] = -pivmin;
                 c[u] = q[u] < 0.0;
             }
             for (int i = 1; i < n; ++i) {
+                const double di = d[i], ei = e2[i - 1];
 #pragma unroll
                 for (int u = 0; u < 4; ++u) {
-                    q[u] = d[i] - x[u] - e2[i - 1] * recip_nr(q[u]);
+                    q[u] = di - x[u] - ei * recip_nr(q[u]);
                     if (fabs(q[u]) < pivmin) q[u] = -pivmin;
                     c[u] += q[u] < 0.0;
                 }
@@ -309,12 +365,16 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
                 if (c[u] <= k) nlo = fmax(nlo, x[u]);
                 else nhi = fmin(nhi, x[u]);
             }
+            for (int off = 1; off < G; off <<= 1) {
+                nlo = fmax(nlo, __shfl_xor(nlo, off));
+                nhi = fmin(nhi, __shfl_xor(nhi, off));
+            }
             if (nlo == lo && nhi == hi) break;  // no representable progress
             lo = nlo;
             hi = nhi;
         }
         const double lam = 0.5 * (lo + hi);
-        t.out[n - 1 - k] = sqrt(fmax(lam, 0.0));
+        if (g == 0) t.out[n - 1 - k] = sqrt(fmax(lam, 0.0));
     }
 }
 

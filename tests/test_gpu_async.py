@@ -7,6 +7,8 @@ their own key count, summary and errors; a call finished while another stream
 is current must wait for its own stream; a second call on a workspace whose
 asynchronous call is not finished is refused.
 """
+import ctypes
+
 import numpy as np
 import pytest
 
@@ -112,3 +114,59 @@ def test_second_call_on_an_unfinished_workspace_is_refused():
     # once finished the workspace takes calls again
     _same(_run(mag, d, c, workspace=ws), want, "workspace reused")
     torch.cuda.synchronize()
+
+
+def _same_rank(got, want, label):
+    import torch
+    for k in ("key", "ratio", "energy_a", "energy_b", "count_a", "count_b"):
+        assert torch.equal(got[k], want[k]), (label, k)
+    for k in ("n_only_a", "n_only_b", "n_join"):
+        assert got[k] == want[k], (label, k)
+
+
+def test_asynchronous_diffs_match_synchronous_ones():
+    """mag_diff_async / mag_diff_finish: several comparisons in flight on two
+    streams, each with its own workspace, give mag_diff's rows and counts; a
+    second call on a workspace whose asynchronous comparison is not finished
+    is refused, and so is finishing one twice."""
+    import torch
+    import paper_2512_08365_amd as mag
+    from paper_2512_08365_amd import _native as N
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    tabs = []
+    for i in range(7):
+        c = synth.tiny_case(1300 + i, n=6000, streams=2, per_stream=80)
+        c["key"] = (c["key"] % np.uint64(11 + 5 * i)).astype(np.uint64)
+        tabs.append(_run(mag, to_gpu(c), c)[1])
+    torch.cuda.synchronize()
+    want = [mag.diff(tabs[0], tabs[i], 7) for i in range(1, 7)]
+    s2 = torch.cuda.Stream()
+    for rep in range(2):
+        log(f"[async] 6 outstanding comparisons, repetition {rep}")
+        pend = []
+        for i in range(1, 7):
+            if i % 2:
+                with torch.cuda.stream(s2):
+                    pend.append(mag.diff(tabs[0], tabs[i], 7, asynchronous=True))
+            else:
+                pend.append(mag.diff(tabs[0], tabs[i], 7, asynchronous=True))
+        for i in reversed(range(6)):  # finished in another order than enqueued
+            _same_rank(pend[i].result(), want[i], f"comparison {i + 1}, repetition {rep}")
+    na, nb = int(tabs[0]["keys"].shape[0]), int(tabs[1]["keys"].shape[0])
+    ws = torch.empty(mag.diff_workspace_size(na, nb, 7), dtype=torch.uint8, device="cuda")
+    p1 = mag.diff(tabs[0], tabs[1], 7, workspace=ws, asynchronous=True)
+    with pytest.raises(mag.MagnetonError) as ei:
+        mag.diff(tabs[0], tabs[2], 7, workspace=ws)
+    assert ei.value.code == N.MAG_E_STATE
+    _same_rank(p1.result(), want[0], "after the refused call")
+    lib = mag._lib()
+    ro = N.RankOut()
+    assert lib.mag_diff_finish(ctypes_ptr(ws), ctypes.byref(ro)) == N.MAG_E_STATE
+    _same_rank(mag.diff(tabs[0], tabs[2], 7, workspace=ws), want[1], "workspace reused")
+    torch.cuda.synchronize()
+
+
+def ctypes_ptr(t):
+    import ctypes
+    return ctypes.c_void_p(t.data_ptr())
