@@ -414,14 +414,13 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", type=int, default=WORKLOAD, choices=[1, 2, 3, 4, 5],
                     help="workload to time (default 3, the multi-stream 100M-sample trace)")
-    ap.add_argument("--pipeline", type=int, default=1,
-                    help="A/B workloads: steps in flight (each on its own outputs and workspaces; "
-                         "1 = every step collected before the next is enqueued; deeper "
-                         "pipelines were measured slower: the next step's trace integration "
-                         "then shares the CUs with the previous step's short kernels)")
-    ap.add_argument("--schedule", choices=["overlap", "serial"], default="overlap",
-                    help="A/B workloads: overlap B's trace integration with A's grouping, or run "
-                         "A's whole call first (both with key maps built on a third stream)")
+    ap.add_argument("--pipeline", type=int, default=2,
+                    help="A/B workloads: steps in flight, each on its own outputs and "
+                         "workspaces (1 = every step collected before the next is enqueued)")
+    ap.add_argument("--schedule", choices=["overlap", "plans", "serial"], default="overlap",
+                    help="A/B workloads: B's trace integration waits for A's and overlaps A's "
+                         "grouping (overlap: B's key map built ahead on a third stream; plans: "
+                         "A's too), or waits for A's whole call (serial, both key maps ahead)")
     ap.add_argument("--timed-side", choices=["a", "b", "none"], default="a",
                     help="which side's tile kernel carries the HIP timing events")
     ap.add_argument("--end-to-end", action="store_true",
@@ -573,6 +572,7 @@ def ab_bench(args, torch, mag, lib, N, synth):
     s2 = torch.cuda.Stream()  # default priority
     s3 = torch.cuda.Stream()  # default priority: B's key map
     serial = args.schedule == "serial"
+    a_plan = args.schedule in ("serial", "plans")  # A's key map built ahead on the third stream
     stream = ctypes.c_void_p(s1.cuda_stream)
     stream_b = ctypes.c_void_p(s2.cuda_stream)
     stream_k = ctypes.c_void_p(s3.cuda_stream)
@@ -606,7 +606,7 @@ def ab_bench(args, torch, mag, lib, N, synth):
             # step's B, B's for this step's A (serial schedule: A's whole call)
             self.sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
                            tiles_wait=ctypes.c_void_p(prev.b_tiles.cuda_event),
-                           tiles_done=ctypes.c_void_p(self.a_tiles.cuda_event), key_plan=serial,
+                           tiles_done=ctypes.c_void_p(self.a_tiles.cuda_event), key_plan=a_plan,
                            inputs=first.sa if first else None)
             self.sb = Side(B, lib, N, torch, k_cap, timed=args.timed_side == "b",
                            tiles_wait=ctypes.c_void_p(
@@ -625,10 +625,10 @@ def ab_bench(args, torch, mag, lib, N, synth):
         # back to back, each with the device to itself), everything else of
         # each side overlaps the other; the diff reads both key counts on the
         # device, behind both attributions, on B's stream (A finishes first)
-        if serial:
+        if a_plan:
             # both key maps on the third stream, A's first, ahead of A's
-            # trace integration; each side's call then aggregates only, and
-            # B starts once A's call is complete
+            # trace integration; each side's call then aggregates only (and
+            # with the serial schedule B starts once A's call is complete)
             x.sa.build_plan(lib, stream_k)
         x.sa.attribute(lib, stream)
         x.a_done.record(s1)

@@ -327,9 +327,11 @@ int mag_key_plan_build(const uint64_t* op_keys, int64_t n_intervals, int64_t key
  *   summary    host struct, may be NULL: filled as by a synchronous call
  *              (tile_kernel_ms and device_ms when the call had MAG_TIME_KERNELS
  *              and is finished on the thread that made it)
- * Synchronizes the stream the call was enqueued on when it was made on this
- * thread (its status copy is in flight there), otherwise `stream`, which must
- * then be the call's stream; returns what the synchronous call would have
+ * Waits for the call itself when it was made on this thread (an event
+ * recorded after its status copy: work enqueued on its stream after the call
+ * is not waited for, so several calls can be kept in flight), otherwise
+ * synchronizes `stream`, which must then be the call's stream; returns what
+ * the synchronous call would have
  * returned for its device work: MAG_OK, MAG_E_TIMESTAMPS, MAG_E_POWER,
  * MAG_E_INTERVAL, MAG_E_CAPACITY or MAG_E_HIP; MAG_E_NULL or MAG_E_WORKSPACE
  * for a NULL or misaligned workspace.  A workspace that no asynchronous call
@@ -441,9 +443,10 @@ int mag_diff_async(const uint64_t* keysA, const mag_key_stats* statsA, const uin
                    size_t workspace_bytes, hipStream_t stream);
 
 /*
- * mag_diff_finish -- waits for the mag_diff_async call on `workspace` (the
- * stream it was enqueued on is synchronized) and fills the host counts of
- * *out.  Must run on the host thread that made the call.  Errors: MAG_E_NULL,
+ * mag_diff_finish -- waits for the mag_diff_async call on `workspace` (an
+ * event recorded after the call's status copy; later work on its stream is
+ * not waited for) and fills the host counts of *out.  Must run on the host
+ * thread that made the call.  Errors: MAG_E_NULL,
  * MAG_E_STATE (no unfinished mag_diff_async call on this workspace), MAG_E_KEYS,
  * MAG_E_HIP.
  */

@@ -211,6 +211,10 @@ struct TimerSlot {
     bool pending = false;          // events recorded by an asynchronous call, not read yet
     bool status_pending = false;   // an asynchronous call copied its status here
     hipStream_t stream = nullptr;  // the stream that call was enqueued on
+    // recorded right after that call's status copy: finishing waits for this
+    // call alone, not for later work on its stream (the next call of a
+    // caller that keeps several in flight)
+    hipEvent_t done = nullptr;
     mag::Status* host_status = nullptr;  // pinned host copy of the status block
     // an asynchronous mag_diff on this workspace: what its conclusion needs
     // besides the status block (table sizes or bounds, rows asked for, whether
@@ -248,9 +252,11 @@ TimerSlot* timer_slot(const void* ws, bool create)
     }
     for (auto& x : t->ev)
         if (x) (void)hipEventDestroy(x);
-    mag::Status* keep = t->host_status;  // the pinned buffer is reused
+    mag::Status* keep = t->host_status;  // the pinned buffer and the event are reused
+    hipEvent_t keep_done = t->done;
     *t = TimerSlot{};
     t->host_status = keep;
+    t->done = keep_done;
     t->used = ++g_timer_clock;
     for (auto& x : t->ev)
         if (hipEventCreate(&x) != hipSuccess) {
@@ -262,6 +268,10 @@ TimerSlot* timer_slot(const void* ws, bool create)
         if (hipHostMalloc(&h, sizeof(mag::Status), hipHostMallocDefault) != hipSuccess)
             return nullptr;
         t->host_status = static_cast<mag::Status*>(h);
+    }
+    if (!t->done && hipEventCreateWithFlags(&t->done, hipEventDisableTiming) != hipSuccess) {
+        t->done = nullptr;
+        return nullptr;
     }
     t->dev = dev;
     t->ws = ws;
@@ -450,9 +460,10 @@ int async_status(const void* workspace, const mag::Status* status, hipStream_t s
     t->pending = timed;
     t->stream = stream;
     if (t->host_status) {
-        const hipError_t e = hipMemcpyAsync(t->host_status, status, sizeof(mag::Status),
-                                            hipMemcpyDeviceToHost, stream);
+        hipError_t e = hipMemcpyAsync(t->host_status, status, sizeof(mag::Status),
+                                      hipMemcpyDeviceToHost, stream);
         if (e != hipSuccess) return hip_fail(e, "status copy");
+        if ((e = hipEventRecord(t->done, stream)) != hipSuccess) return hip_fail(e, "event record");
         t->status_pending = true;
     }
     return MAG_OK;
@@ -1021,7 +1032,7 @@ int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summ
         // stream, which may differ from `stream`: that one is waited for
         t->status_pending = false;
         hipError_t e2;
-        if ((e2 = hipStreamSynchronize(t->stream)) != hipSuccess) {
+        if ((e2 = hipEventSynchronize(t->done)) != hipSuccess) {
             t->pending = false;
             return hip_fail(e2, "synchronize");
         }
@@ -1679,9 +1690,10 @@ int mag_diff_async(const uint64_t* keysA, const mag_key_stats* statsA, const uin
     TimerSlot* t = timer_slot(workspace, true);
     if (!t || !t->host_status)
         return fail(MAG_E_HIP, "no host buffer for the status of an asynchronous call");
-    const hipError_t e =
+    hipError_t e =
         hipMemcpyAsync(t->host_status, p.status, sizeof(mag::Status), hipMemcpyDeviceToHost, stream);
     if (e != hipSuccess) return hip_fail(e, "status copy");
+    if ((e = hipEventRecord(t->done, stream)) != hipSuccess) return hip_fail(e, "event record");
     t->status_pending = true;
     t->stream = stream;
     t->diff = true;
@@ -1702,7 +1714,7 @@ int mag_diff_finish(const void* workspace, mag_rank_out* out)
     t->status_pending = false;
     t->diff = false;
     hipError_t e;
-    if ((e = hipStreamSynchronize(t->stream)) != hipSuccess) return hip_fail(e, "synchronize");
+    if ((e = hipEventSynchronize(t->done)) != hipSuccess) return hip_fail(e, "synchronize");
     return conclude_diff(t->diff_na, t->diff_nb, t->diff_k, t->diff_dev, *t->host_status, out);
 }
 
