@@ -7,16 +7,18 @@ streams x 1,000,000 operator intervals, 5,000 Zipf(1.2) keys): attribute side
 A, attribute side B (equal split of concurrent power, per-interval energies
 and sample indices, per-key count/sum/M2), then join and rank the top-100
 excess-energy keys.  Side A runs on the current stream; side B on a second
-stream (default priority) that waits for A's per-interval outputs (the
-`intervals_ready` event), so B's tile kernel runs while A's per-key grouping
-does, and A's tile kernel has the device to itself.  Both attributions are
-enqueued asynchronously and leave their key counts on the device; the diff is
-enqueued behind both and its synchronization is the step's only host wait.
-B's key map (distinct keys, ids, ranks: it depends on the keys only) is
-built on a third stream while A's trace is integrated.  Side A's tile kernel
-is timed with HIP events carried on its dispatch in every timed step; side B
-runs untimed.  Inputs are synthetic, seeded and resident in
-HBM before timing.
+stream (default priority) whose trace integration waits for A's (the
+`tiles_wait` / `tiles_done` events), so the two tile kernels run back to back
+while A's per-key grouping overlaps B's tile kernel.  Both attributions and
+the diff are enqueued asynchronously (key counts stay on the device) and
+collected with one host wait per step, on events of their own.  Two steps are
+kept in flight (`--pipeline`), each with its own outputs and workspaces:
+step i is enqueued before step i-1 is collected, and A's tile kernel of a
+step waits for B's of the step before.  B's key map (distinct keys, ids,
+ranks: it depends on the keys only) is built on a third stream while A's
+trace is integrated.  Side A's tile kernel is timed with HIP events carried
+on its dispatch in every timed step; side B runs untimed.  Inputs are
+synthetic, seeded and resident in HBM before timing.
 
 --workload 1/2/3/4/5 times the other workloads the same way (2 and 4 fit in
 or near the 256 MB Infinity Cache and are timed with a 512 MB flush before
@@ -136,7 +138,7 @@ class Side:
     """Device copies of one side plus preallocated outputs and workspace."""
 
     def __init__(self, c, lib, N, torch, k_cap, timed=True, ready_event=None, tiles_wait=None,
-                 tiles_done=None, key_plan=False, inputs=None):
+                 tiles_done=None, key_plan=False, inputs=None, group_stream=None):
         import numpy as np
         self.n = int(c["t"].shape[0])
         self.m = int(c["s"].shape[0])
@@ -175,7 +177,8 @@ class Side:
                                   ctypes.c_void_p(self.plan_ready.cuda_event))
         self.opts = N.AttrOpts(len(self.off) - 1, flags, ctypes.cast(self.offs, ctypes.c_void_p),
                                ready_event, ctypes.pointer(self.plan) if self.plan else None,
-                               tiles_wait, tiles_done)
+                               tiles_wait, tiles_done,
+                               ctypes.c_void_p(group_stream.cuda_stream) if group_stream else None)
         b = ctypes.c_size_t(0)
         rc = lib.mag_attribute_workspace_size(self.n, self.m, k_cap, ctypes.byref(self.opts),
                                               ctypes.byref(b))
@@ -417,10 +420,13 @@ def main():
     ap.add_argument("--pipeline", type=int, default=2,
                     help="A/B workloads: steps in flight, each on its own outputs and "
                          "workspaces (1 = every step collected before the next is enqueued)")
-    ap.add_argument("--schedule", choices=["overlap", "plans", "serial"], default="overlap",
+    ap.add_argument("--schedule", choices=["overlap", "plans", "serial", "tilestream"],
+                    default="overlap",
                     help="A/B workloads: B's trace integration waits for A's and overlaps A's "
                          "grouping (overlap: B's key map built ahead on a third stream; plans: "
-                         "A's too), or waits for A's whole call (serial, both key maps ahead)")
+                         "A's too), or waits for A's whole call (serial, both key maps ahead); "
+                         "tilestream: both trace integrations on one stream, each side's "
+                         "grouping on a stream of its own (group_stream), both key maps ahead")
     ap.add_argument("--timed-side", choices=["a", "b", "none"], default="a",
                     help="which side's tile kernel carries the HIP timing events")
     ap.add_argument("--end-to-end", action="store_true",
@@ -572,8 +578,12 @@ def ab_bench(args, torch, mag, lib, N, synth):
     s2 = torch.cuda.Stream()  # default priority
     s3 = torch.cuda.Stream()  # default priority: B's key map
     serial = args.schedule == "serial"
-    a_plan = args.schedule in ("serial", "plans")  # A's key map built ahead on the third stream
-    stream = ctypes.c_void_p(s1.cuda_stream)
+    # one stream for both sides' trace integrations, the groupings on their own
+    tilestream = args.schedule == "tilestream"
+    # A's key map built ahead on the third stream
+    a_plan = args.schedule in ("serial", "plans", "tilestream")
+    g_a = torch.cuda.Stream() if tilestream else None  # default priority: A's grouping
+    g_b = s2 if tilestream else None  # B's grouping and the diff
     stream_b = ctypes.c_void_p(s2.cuda_stream)
     stream_k = ctypes.c_void_p(s3.cuda_stream)
     b = ctypes.c_size_t(0)
@@ -581,13 +591,18 @@ def ab_bench(args, torch, mag, lib, N, synth):
     d_bytes = int(b.value)
 
     class Slot:
-        """One step's outputs, workspaces and events."""
+        """One step's outputs, workspaces, events and A's stream."""
 
-        def __init__(self):
+        def __init__(self, sa_stream):
+            # A's calls alternate between streams, so that a step's trace
+            # integration does not queue behind the previous step's grouping
+            # of A (B's next trace integration waits for A's anyway)
+            self.s_a = sa_stream
+            self.stream_a = ctypes.c_void_p(sa_stream.cuda_stream)
             self.a_tiles = torch.cuda.Event()
-            self.a_tiles.record(s1)  # creates the HIP event
+            self.a_tiles.record(sa_stream)  # creates the HIP event
             self.a_done = torch.cuda.Event()
-            self.a_done.record(s1)
+            self.a_done.record(sa_stream)
             self.b_tiles = torch.cuda.Event()
             self.b_tiles.record(s2)
             self.d_out = {k: torch.empty(top, dtype=dt, device="cuda") for k, dt in
@@ -602,6 +617,15 @@ def ab_bench(args, torch, mag, lib, N, synth):
             self.record = False
 
         def sides(self, prev, first):
+            if tilestream:
+                # the trace integrations queue on one stream, in call order
+                self.sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
+                               key_plan=True, inputs=first.sa if first else None,
+                               group_stream=g_a)
+                self.sb = Side(B, lib, N, torch, k_cap, timed=args.timed_side == "b",
+                               key_plan=True, inputs=first.sb if first else None,
+                               group_stream=g_b)
+                return
             # the trace integrations never overlap: A's waits for the previous
             # step's B, B's for this step's A (serial schedule: A's whole call)
             self.sa = Side(A, lib, N, torch, k_cap, timed=args.timed_side == "a",
@@ -614,7 +638,9 @@ def ab_bench(args, torch, mag, lib, N, synth):
                            tiles_done=ctypes.c_void_p(self.b_tiles.cuda_event),
                            key_plan=True, inputs=first.sb if first else None)
 
-    slots = [Slot() for _ in range(depth)]
+    a_streams = [s1] + [torch.cuda.Stream() for _ in range(min(depth, 2) - 1 if not tilestream
+                                                           else 0)]  # default priority
+    slots = [Slot(a_streams[j % len(a_streams)]) for j in range(depth)]
     for j, x in enumerate(slots):
         x.sides(slots[j - 1], slots[0] if j else None)
     torch.cuda.synchronize()
@@ -630,13 +656,13 @@ def ab_bench(args, torch, mag, lib, N, synth):
             # trace integration; each side's call then aggregates only (and
             # with the serial schedule B starts once A's call is complete)
             x.sa.build_plan(lib, stream_k)
-        x.sa.attribute(lib, stream)
-        x.a_done.record(s1)
+        x.sa.attribute(lib, x.stream_a)
+        x.a_done.record(g_a if tilestream else x.s_a)
         # B's key map depends on B's keys only: built on a third stream while
         # A's trace is integrated, so B's grouping after its own trace
         # integration only aggregates
         x.sb.build_plan(lib, stream_k)
-        x.sb.attribute(lib, stream_b)
+        x.sb.attribute(lib, x.stream_a if tilestream else stream_b)
         s2.wait_event(x.a_done)
         rc = lib.mag_diff_async(x.sa.kout.data_ptr(), ctypes.byref(x.sa.ks_dev),
                                 x.sb.kout.data_ptr(), ctypes.byref(x.sb.ks_dev), top,
@@ -650,7 +676,7 @@ def ab_bench(args, torch, mag, lib, N, synth):
         rc = lib.mag_diff_finish(x.d_ws.data_ptr(), ctypes.byref(x.ro))
         if rc != 0:
             raise RuntimeError(f"mag_diff_finish failed {rc}: {lib.mag_last_error().decode()}")
-        ta = x.sa.finish(lib, stream)
+        ta = x.sa.finish(lib, x.stream_a)
         tb = x.sb.finish(lib, stream_b)
         if x.record and args.timed_side != "none":
             tile_ms.append(ta if args.timed_side == "a" else tb)

@@ -118,6 +118,12 @@ typedef struct mag_attr_opts {
                                     /* tiles_wait it lets the bandwidth-bound passes  */
                                     /* of two attributions run back to back while     */
                                     /* the rest of each overlaps the other            */
+    hipStream_t group_stream;       /* mag_attribute only, may be NULL: the fix-ups,  */
+                                    /* grouping and status copy run on this stream,   */
+                                    /* which first waits for the trace integration    */
+                                    /* on `stream`; `stream` is then free for the next */
+                                    /* call's integration (a synchronous call waits   */
+                                    /* for group_stream; MAG_ASYNC finishes as usual) */
 } mag_attr_opts;
 
 /*
@@ -286,7 +292,8 @@ int mag_attribute(const double* timestamps, const float* power, int64_t n_sample
  *   MAG_STATIC_SCRATCH_BYTES are rejected with MAG_E_WORKSPACE before any
  *   device work (for example 20,000,000 samples with 1,000,000 intervals and
  *   2,048 keys need 23 MiB and fit).
- *   opts->flags must not contain MAG_ASYNC or MAG_TIME_KERNELS (MAG_E_STATE).
+ *   opts->flags must not contain MAG_ASYNC or MAG_TIME_KERNELS, and
+ *   opts->group_stream must be NULL (MAG_E_STATE).
  *   Every call on one GPU shares that GPU's scratch and leaves its contents
  *   behind (every call initializes what it reads): calls that overlap on one
  *   GPU (other host threads, or work still running on another stream) race

@@ -58,8 +58,10 @@ def _event_handle(ev):
 
 
 def _opts(n_streams: int, stream_offsets, flags: int, intervals_ready=None, key_plan=None,
-          tiles_wait=None, tiles_done=None):
+          tiles_wait=None, tiles_done=None, group_stream=None):
     o = N.AttrOpts()
+    if group_stream is not None:
+        o.group_stream = ctypes.c_void_p(group_stream.cuda_stream)
     o.n_streams = int(n_streams)
     o.flags = int(flags)
     o.intervals_ready = _event_handle(intervals_ready)
@@ -149,7 +151,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
               equal_split: bool = True, validate: bool = True, key_capacity: int | None = None,
               indices: bool = True, workspace=None, out=None, asynchronous: bool = False,
               intervals_ready=None, latency: bool = False, key_plan=None, tiles_wait=None,
-              tiles_done=None):
+              tiles_done=None, group_stream=None):
     """Attribute the energy of a power trace to intervals and group it by key.
 
     t: float64 [n] timestamps (s), P: float32 [n] power (W), s/e: float64 [m]
@@ -158,7 +160,9 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     per-interval outputs are complete (before the grouping), or None.
     key_plan: a KeyPlan of these keys (its key map is used instead of building
     one; its capacity is the key capacity).  tiles_wait / tiles_done: events
-    waited for before / recorded after the trace integration.
+    waited for before / recorded after the trace integration.  group_stream: a
+    torch.cuda.Stream that runs the fix-ups and grouping after the trace
+    integration (the current stream is then free for the next call's).
     latency: also sum each key's interval durations (per_key["duration"]).
     Returns (per_interval, per_key, summary): dicts of tensors / numbers; with
     asynchronous=True a Pending whose finish() returns them once the work ran.
@@ -170,7 +174,7 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
     flags = ((EQUAL_SPLIT if equal_split else 0) | (0 if validate else SKIP_VALIDATE) |
              (ASYNC if asynchronous else 0) | (KEY_LATENCY if latency and keys is not None else 0))
     o, keep = _opts(n_streams, stream_offsets, flags, intervals_ready, key_plan, tiles_wait,
-                    tiles_done)
+                    tiles_done, group_stream)
     group = keys is not None
     cap = int(key_capacity) if key_capacity is not None else max(1, m)
     if key_plan is not None:
@@ -220,7 +224,8 @@ def attribute(t, P, s, e, keys=None, *, n_streams: int = 1, stream_offsets=None,
 
     if asynchronous:
         # the inputs and the options stay referenced until finish()
-        return Pending(workspace, ks, summ, build, (keep, o, t, P, s, e, keys, key_plan), sh)
+        return Pending(workspace, ks, summ, build,
+                       (keep, o, t, P, s, e, keys, key_plan, group_stream), sh)
     return build()
 
 

@@ -64,7 +64,8 @@ class KeyPlan(ctypes.Structure):
 class AttrOpts(ctypes.Structure):
     _fields_ = [("n_streams", ctypes.c_int32), ("flags", ctypes.c_uint32),
                 ("stream_offsets", c_vp), ("intervals_ready", c_vp),
-                ("key_plan", ctypes.POINTER(KeyPlan)), ("tiles_wait", c_vp), ("tiles_done", c_vp)]
+                ("key_plan", ctypes.POINTER(KeyPlan)), ("tiles_wait", c_vp), ("tiles_done", c_vp),
+                ("group_stream", c_vp)]
 
 
 class IntervalOut(ctypes.Structure):

@@ -215,6 +215,9 @@ struct TimerSlot {
     // call alone, not for later work on its stream (the next call of a
     // caller that keeps several in flight)
     hipEvent_t done = nullptr;
+    // a call with a group stream: recorded after its trace integration, waited
+    // for by the group stream
+    hipEvent_t split = nullptr;
     mag::Status* host_status = nullptr;  // pinned host copy of the status block
     // an asynchronous mag_diff on this workspace: what its conclusion needs
     // besides the status block (table sizes or bounds, rows asked for, whether
@@ -253,10 +256,11 @@ TimerSlot* timer_slot(const void* ws, bool create)
     for (auto& x : t->ev)
         if (x) (void)hipEventDestroy(x);
     mag::Status* keep = t->host_status;  // the pinned buffer and the event are reused
-    hipEvent_t keep_done = t->done;
+    hipEvent_t keep_done = t->done, keep_split = t->split;
     *t = TimerSlot{};
     t->host_status = keep;
     t->done = keep_done;
+    t->split = keep_split;
     t->used = ++g_timer_clock;
     for (auto& x : t->ev)
         if (hipEventCreate(&x) != hipSuccess) {
@@ -271,6 +275,10 @@ TimerSlot* timer_slot(const void* ws, bool create)
     }
     if (!t->done && hipEventCreateWithFlags(&t->done, hipEventDisableTiming) != hipSuccess) {
         t->done = nullptr;
+        return nullptr;
+    }
+    if (!t->split && hipEventCreateWithFlags(&t->split, hipEventDisableTiming) != hipSuccess) {
+        t->split = nullptr;
         return nullptr;
     }
     t->dev = dev;
@@ -756,6 +764,18 @@ int attribute_impl(const double* timestamps, const float* power, int64_t n_sampl
         return hip_fail(e, "tile kernel");
     if (opts && opts->tiles_done && (e = hipEventRecord(opts->tiles_done, stream)) != hipSuccess)
         return hip_fail(e, "tiles_done event");
+    if (opts && opts->group_stream && opts->group_stream != stream) {
+        // everything after the trace integration moves to the group stream,
+        // which first waits for the integration
+        TimerSlot* ts = timer_slot(workspace, true);
+        if (!ts || !ts->split) return fail(MAG_E_HIP, "no event for the group stream");
+        if ((e = hipEventRecord(ts->split, stream)) != hipSuccess ||
+            (e = hipStreamWaitEvent(opts->group_stream, ts->split, 0)) != hipSuccess)
+            return hip_fail(e, "group stream event");
+        stream = opts->group_stream;
+        job.stream = stream;
+        timer.stream = stream;
+    }
     if ((e = job.fixups(n_samples, NT, per_key != nullptr)) != hipSuccess)
         return hip_fail(e, "fix-up kernels");
     if (opts && opts->intervals_ready &&
@@ -847,9 +867,9 @@ int mag_attribute_static(const double* timestamps, const float* power, int64_t n
     if (!timestamps || !power) return fail(MAG_E_NULL, "timestamps/power is NULL");
     if (!aligned(timestamps, 8) || !aligned(power, 4))
         return fail(MAG_E_ALIGN, "input array not aligned to its element size");
-    if (opts && (opts->flags & (MAG_ASYNC | MAG_TIME_KERNELS)))
-        return fail(MAG_E_STATE, "MAG_ASYNC and MAG_TIME_KERNELS need host resources: not "
-                                 "accepted by the allocation-free entry point");
+    if (opts && ((opts->flags & (MAG_ASYNC | MAG_TIME_KERNELS)) || opts->group_stream))
+        return fail(MAG_E_STATE, "MAG_ASYNC, MAG_TIME_KERNELS and group_stream need host "
+                                 "resources: not accepted by the allocation-free entry point");
     size_t need = 0;
     int rc = mag_attribute_workspace_size(n_samples, n_intervals,
                                           per_key ? per_key->capacity : 0, opts, &need);

@@ -199,3 +199,50 @@ def test_tile_events_serialize_the_trace_integrations():
                 assert torch.equal(got[1][k], want[1][k]), k
             np.testing.assert_allclose(got[1]["sum"].cpu().numpy(), want[1]["sum"].cpu().numpy(),
                                        rtol=1e-12)
+
+
+def test_group_stream_moves_the_grouping_off_the_tile_stream():
+    """mag_attr_opts.group_stream: the fix-ups, grouping and status copy run on
+    a second stream after the trace integration; results equal the one-stream
+    call's (synchronous and MAG_ASYNC), and the tile stream takes the next
+    call's trace integration while the first call still groups."""
+    import torch
+    import paper_2512_08365_amd as mag
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    cases = [synth.long_trace(seed, 200_000, 3, 15_000) for seed in (81, 82, 83)]
+    devs = [to_gpu(c) for c in cases]
+
+    def run(d, c, **kw):
+        off = [int(x) for x in c["offsets"]]
+        return mag.attribute(d["t"], d["P"], d["s"], d["e"], d["key"], n_streams=len(off) - 1,
+                             stream_offsets=off, **kw)
+
+    def same(got, want, label):
+        for k in ("energy", "start_idx", "end_idx"):
+            assert torch.equal(got[0][k], want[0][k]), (label, k)
+        for k in ("keys", "count"):
+            assert torch.equal(got[1][k], want[1][k]), (label, k)
+        # per-key sums and M2 are added through LDS atomics in no fixed order:
+        # equal up to rounding
+        for k in ("sum", "m2"):
+            np.testing.assert_allclose(got[1][k].cpu().numpy(), want[1][k].cpu().numpy(),
+                                       rtol=1e-12, err_msg=f"{label} {k}")
+        for k in ("n_keys", "n_clipped"):
+            assert got[2][k] == want[2][k], (label, k)
+        for k in ("trace_energy", "idle_energy", "attributed_energy"):
+            assert abs(got[2][k] - want[2][k]) <= 1e-12 * abs(want[2][k]), (label, k)
+
+    want = [run(d, c) for d, c in zip(devs, cases)]
+    torch.cuda.synchronize()
+    g = torch.cuda.Stream()
+    for rep in range(2):
+        log(f"[group stream] repetition {rep}")
+        for i, (d, c) in enumerate(zip(devs, cases)):
+            same(run(d, c, group_stream=g), want[i], f"synchronous {i}")
+        # three asynchronous calls back to back: their trace integrations queue
+        # on the current stream, their groupings on the group stream
+        pend = [run(d, c, asynchronous=True, group_stream=g) for d, c in zip(devs, cases)]
+        for i in reversed(range(3)):
+            same(pend[i].finish(), want[i], f"asynchronous {i}, repetition {rep}")
+    torch.cuda.synchronize()
