@@ -332,20 +332,26 @@ def counter_session(args, torch, mag):
 
 
 def invariants_bench(args, torch, mag):
-    """Multi-mode SVD invariants of a batch shaped like per-layer attention
-    K/V tensors (64 x fp32 [32 heads, 128 tokens, 128 head dims]) and the
-    all-pairs matching of the batch against a permuted copy; one JSON line."""
+    """Multi-mode SVD invariants of a batch of tensors (default: shaped like
+    per-layer attention K/V tensors, 64 x fp32 [32 heads, 128 tokens, 128 head
+    dims]; --inv-shape / --inv-count for others, e.g. one 4096 x 4096 weight)
+    and the all-pairs matching of the batch against a copy with its first two
+    modes swapped; one JSON line."""
     import numpy as np
     rng = np.random.default_rng(args.seed)
-    shape, count = (32, 128, 128), 64
+    shape = tuple(int(x) for x in args.inv_shape.split(","))
+    count = args.inv_count
+    r = len(shape)
     host = [rng.standard_normal(shape).astype(np.float32) for _ in range(count)]
     A = [torch.from_numpy(h).cuda() for h in host]
-    B = [x.permute(1, 0, 2).contiguous() for x in A]  # the other system's layout (NHD)
+    # the other system's layout: the first two modes swapped (NHD for attention K/V)
+    perm = (1, 0) + tuple(range(2, r)) if r >= 2 else (0,)
+    B = [x.permute(*perm).contiguous() for x in A]
     lay = mag.invariant_layout(A[0])
     # algorithmic work of the Gram products: K (K + 1) L flops per unfolding
     flops = 0
-    for g in range(1, 7, 2):
-        M = int(np.prod([shape[i] for i in range(3) if g >> i & 1]))
+    for g in range(1, (1 << r) - 1, 2):
+        M = int(np.prod([shape[i] for i in range(r) if g >> i & 1]))
         N = int(np.prod(shape)) // M
         K, L = min(M, N), max(M, N)
         flops += K * (K + 1) * L
@@ -368,17 +374,19 @@ def invariants_bench(args, torch, mag):
     res = {"mode": "tensor invariants", "tensors": count, "shape": list(shape),
            "spectrum_lengths": lay, "ms_per_batch": sec * 1e3, "tensors_per_s": count / sec,
            "gram_tflops_algorithmic_over_call": flops / sec / 1e12,
-           "match_ms_64x64": msec * 1e3, "matched_pairs": matched}
+           f"match_ms_{count}x{count}": msec * 1e3, "matched_pairs": matched}
     if not args.no_cpu_baseline:
         from threadpoolctl import threadpool_limits
         from oracle import spectra as S
+        ns = min(8, count)
         with threadpool_limits(1):
             t0 = time.perf_counter()
-            for h in host[:8]:
+            for h in host[:ns]:
                 S.invariants(h)
-            dt = (time.perf_counter() - t0) / 8
+            dt = (time.perf_counter() - t0) / ns
         res["cpu_baseline"] = {"value": 1.0 / dt, "unit": "tensors/s", "cores": 1,
-                               "kind": "oracle", "sample": "8 of the 64 tensors, numpy SVD",
+                               "kind": "oracle",
+                               "sample": f"{ns} of the {count} tensors, numpy SVD",
                                "seconds_per_tensor": round(dt, 4)}
     print(json.dumps(res), flush=True)
 
@@ -435,6 +443,9 @@ def main():
                     help="measure the host-side subgraph matching (Section 4.2) instead")
     ap.add_argument("--invariants", action="store_true",
                     help="measure the tensor invariants (Section 4.2) instead")
+    ap.add_argument("--inv-shape", default="32,128,128",
+                    help="--invariants: tensor shape (comma-separated)")
+    ap.add_argument("--inv-count", type=int, default=64, help="--invariants: tensors per batch")
     ap.add_argument("--counter-session", action="store_true",
                     help="measure the counter (software replay) attribution instead")
     ap.add_argument("--copy-calibration", action="store_true",

@@ -485,7 +485,7 @@ int mag_diff_batch(const uint64_t* keysA, const mag_key_stats* statsA, int32_t n
 
 /* ------------------------------------------------ tensor matching (4.2) */
 #define MAG_SVD_MAX_RANK 5
-#define MAG_SVD_MAX_K 512 /* largest min(M, N) of an unfolding this library handles */
+#define MAG_SVD_MAX_K 8192 /* largest min(M, N) of an unfolding this library handles */
 
 /* A dense tensor: fp32, row-major (the last mode fastest), on the device. */
 typedef struct mag_tensor {
@@ -518,6 +518,11 @@ int mag_invariant_count(const mag_tensor* tensor, int32_t* n_unfoldings, int64_t
  * exactly; MFMA products), reduced to tridiagonal form and bisected; an
  * eigenvalue is within about 1e-13 of the largest (relative), so a singular
  * value far below the largest carries an absolute error near 3e-7 of it.
+ * Gram sides up to 512 are reduced by one workgroup each, all unfoldings side
+ * by side; larger ones (up to MAG_SVD_MAX_K) one after another, each
+ * Householder step spread over the whole device (about 4 launches per row of
+ * the Gram matrix, so a side of n costs some 4 n launches; the workspace then
+ * also holds about (n / 256 + 4) n doubles of scratch).
  * Synchronizes `stream`.  Errors: MAG_E_NULL, MAG_E_SIZE, MAG_E_ALIGN,
  * MAG_E_WORKSPACE, MAG_E_HIP.
  */

@@ -90,7 +90,7 @@ class RankOut(ctypes.Structure):
 
 
 MAG_SVD_MAX_RANK = 5
-MAG_SVD_MAX_K = 512
+MAG_SVD_MAX_K = 8192
 
 
 class Tensor(ctypes.Structure):

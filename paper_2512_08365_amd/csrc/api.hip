@@ -1895,6 +1895,7 @@ int count_invariants(const mag_tensor* t, int32_t* n_unf, int64_t* n_values)
 struct InvPlan {
     std::vector<mag::SvdTask> tasks;
     int64_t gram_len = 0, n_items = 0;
+    int large_k = 0;  // largest Gram side above mag::SVD_SMALL_K (0: none)
 };
 
 int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
@@ -1913,18 +1914,23 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
             task.item0 = pl.n_items;
             pl.n_items += (int64_t)task.nt * (task.nt + 1) / 2 * task.nchunk;
             pl.gram_len += task.K * task.K;
+            if (task.K > mag::SVD_SMALL_K) pl.large_k = std::max(pl.large_k, (int)task.K);
             pl.tasks.push_back(task);
         }
     }
     return MAG_OK;
 }
 
-size_t carve_invariants(const InvPlan& pl, void* ws, mag::SvdTask** tasks, double** gram)
+size_t carve_invariants(const InvPlan& pl, void* ws, mag::SvdTask** tasks, double** gram,
+                        double** large)
 {
     Carver c;
     c.base = static_cast<char*>(ws);
     *tasks = c.take<mag::SvdTask>(std::max<size_t>(pl.tasks.size(), 1));
     *gram = c.take<double>((size_t)std::max<int64_t>(pl.gram_len, 1));
+    // scratch of the many-workgroup reduction, shared by the large unfoldings
+    // (they run one after another)
+    *large = pl.large_k ? c.take<double>((size_t)mag::svd_large_scratch(pl.large_k)) : nullptr;
     return c.off;
 }
 
@@ -1969,8 +1975,8 @@ int mag_invariants_workspace_size(const mag_tensor* tensors, int32_t n_tensors, 
     int rc = plan_invariants(tensors, n_tensors, pl);
     if (rc) return rc;
     mag::SvdTask* t;
-    double* g;
-    *bytes = carve_invariants(pl, nullptr, &t, &g);
+    double *g, *lg;
+    *bytes = carve_invariants(pl, nullptr, &t, &g, &lg);
     return MAG_OK;
 }
 
@@ -1991,10 +1997,10 @@ int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra
     if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
     if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
     mag::SvdTask* dtasks;
-    double* gram;
-    const size_t need = carve_invariants(pl, nullptr, &dtasks, &gram);
+    double *gram, *large;
+    const size_t need = carve_invariants(pl, nullptr, &dtasks, &gram, &large);
     if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
-    carve_invariants(pl, workspace, &dtasks, &gram);
+    carve_invariants(pl, workspace, &dtasks, &gram, &large);
     int64_t go = 0, so = 0;
     for (auto& t : pl.tasks) {
         t.gram = gram + go;
@@ -2009,6 +2015,10 @@ int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra
     if ((e = mag::launch_svd(dtasks, (int)pl.tasks.size(), pl.n_items, gram, pl.gram_len, stream)) !=
         hipSuccess)
         return hip_fail(e, "invariant kernels");
+    for (const auto& t : pl.tasks)
+        if (t.K > mag::SVD_SMALL_K &&
+            (e = mag::launch_svd_large(t.gram, (int)t.K, large, t.out, stream)) != hipSuccess)
+            return hip_fail(e, "large unfolding kernels");
     // (the task table on the host stays alive until the copy is done)
     if ((e = hipStreamSynchronize(stream)) != hipSuccess) return hip_fail(e, "synchronize");
     return MAG_OK;

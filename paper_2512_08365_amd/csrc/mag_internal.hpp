@@ -261,7 +261,8 @@ hipError_t launch_key_map(const GroupParams& p, bool clear, hipStream_t stream);
 hipError_t launch_aggregate(const GroupParams& p, hipStream_t stream);
 // multi-mode SVD invariants (Section 4.2): one task per (tensor, unfolding)
 constexpr int SVD_MAX_RANK = 5;
-constexpr int SVD_MAX_K = 512;        // largest Gram side (min(M, N) of an unfolding)
+constexpr int SVD_MAX_K = 8192;       // largest Gram side (min(M, N) of an unfolding)
+constexpr int SVD_SMALL_K = 512;      // Gram sides reduced by one workgroup (larger: many)
 constexpr int SVD_MAX_UNF = 15;       // unfoldings of a rank-5 tensor, complements folded
 constexpr int64_t GRAM_CHUNK = 2048;  // unfolding columns per Gram work item
 
@@ -286,9 +287,16 @@ struct SpecDesc {
     int64_t len[SVD_MAX_UNF];
 };
 
-// Gram matrices (zeroed, then accumulated), then the spectra
+// Gram matrices (zeroed, then accumulated), then the spectra of the tasks
+// with K <= SVD_SMALL_K
 hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double* gram,
                       int64_t gram_len, hipStream_t stream);
+// the spectrum of one n x n Gram matrix with n > SVD_SMALL_K (overwritten):
+// a Householder step is four launches over the whole device, then
+// multisection on Sturm counts; scratch of svd_large_scratch(n) doubles
+int64_t svd_large_scratch(int n);
+hipError_t launch_svd_large(double* gram, int n, double* scratch, double* out,
+                            hipStream_t stream);
 // match[i * nb + j] = 1 when tensor i of A and tensor j of B have matching invariants
 hipError_t launch_svd_match(const SpecDesc* da, int na, const double* sa, const SpecDesc* db,
                             int nb, const double* sb, double eps, uint8_t* match,

@@ -296,15 +296,85 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* wp, d
     __syncthreads();
 }
 
+// Gershgorin interval of the symmetric tridiagonal matrix (d, e2), widened
+// by two ulps of its span and the smallest pivot allowed in a Sturm count
+template <class Ptr>
+__device__ void gershgorin(Ptr d, Ptr e2, int n, double& glo, double& ghi, double& pivmin)
+{
+    glo = INFINITY;
+    ghi = -INFINITY;
+    double emax = 0.0;
+    for (int i = 0; i < n; ++i) {
+        const double r = (i > 0 ? sqrt(e2[i - 1]) : 0.0) + (i + 1 < n ? sqrt(e2[i]) : 0.0);
+        glo = fmin(glo, d[i] - r);
+        ghi = fmax(ghi, d[i] + r);
+        if (i + 1 < n) emax = fmax(emax, e2[i]);
+    }
+    const double span = fmax(fabs(glo), fabs(ghi));
+    pivmin = 0x1p-1000 * fmax(1.0, emax);
+    glo -= 2.0 * DBL_EPSILON * span + pivmin;
+    ghi += 2.0 * DBL_EPSILON * span + pivmin;
+}
+
+// the k-th smallest eigenvalue of (d, e2) by multisection on Sturm counts
+// (count(lo) <= k < count(hi)): the G neighbouring threads of eigenvalue k
+// (g = 0 .. G-1, G a power of two dividing 64) each count at four of a
+// round's 4 G interior points, four independent chains side by side, and the
+// round keeps the one of the interval's 4 G + 1 parts that holds the
+// eigenvalue (the group agrees on lo and hi after every round)
+template <class Ptr>
+__device__ double multisect(Ptr d, Ptr e2, int n, int k, int g, int G, double glo, double ghi,
+                            double pivmin)
+{
+    double lo = glo, hi = ghi;
+    for (int it = 0; it < 64; ++it) {
+        if (!(hi - lo > 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin)) break;
+        const double h = (hi - lo) / (double)(4 * G + 1);
+        double x[4], q[4];
+        int c[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            x[u] = lo + h * (double)(4 * g + u + 1);
+            q[u] = d[0] - x[u];
+            if (fabs(q[u]) < pivmin) q[u] = -pivmin;
+            c[u] = q[u] < 0.0;
+        }
+        for (int i = 1; i < n; ++i) {
+            const double di = d[i], ei = e2[i - 1];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                q[u] = di - x[u] - ei * recip_nr(q[u]);
+                if (fabs(q[u]) < pivmin) q[u] = -pivmin;
+                c[u] += q[u] < 0.0;
+            }
+        }
+        double nlo = lo, nhi = hi;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (c[u] <= k) nlo = fmax(nlo, x[u]);
+            else nhi = fmin(nhi, x[u]);
+        }
+        for (int off = 1; off < G; off <<= 1) {
+            nlo = fmax(nlo, __shfl_xor(nlo, off));
+            nhi = fmin(nhi, __shfl_xor(nhi, off));
+        }
+        if (nlo == lo && nhi == hi) break;  // no representable progress
+        lo = nlo;
+        hi = nhi;
+    }
+    return 0.5 * (lo + hi);
+}
+
 __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
 {
-    __shared__ double v[SVD_MAX_K], w[SVD_MAX_K];
-    __shared__ double d[SVD_MAX_K], e2[SVD_MAX_K];
+    __shared__ double v[SVD_SMALL_K], w[SVD_SMALL_K];
+    __shared__ double d[SVD_SMALL_K], e2[SVD_SMALL_K];
     __shared__ double red[2][EIG_THREADS / 64];
     __shared__ double As[EIG_LDS_K * EIG_LDS_K];
     __shared__ double wp[EIG_THREADS];
     const SvdTask& t = tasks[blockIdx.x];
     const int n = (int)t.K;
+    if (n > SVD_SMALL_K) return;  // (uniform) a larger matrix takes the many-workgroup path
     const int tid = threadIdx.x;
     if (n <= EIG_LDS_K) {
         for (int q = tid; q < n * n; q += EIG_THREADS) As[q] = t.gram[q];
@@ -313,69 +383,218 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
     } else {
         tridiagonalize(t.gram, n, v, w, wp, d, e2, red);
     }
-    // Gershgorin interval and the smallest pivot allowed in a Sturm count
-    double glo = INFINITY, ghi = -INFINITY, emax = 0.0;
-    for (int i = 0; i < n; ++i) {
-        const double r = (i > 0 ? sqrt(e2[i - 1]) : 0.0) + (i + 1 < n ? sqrt(e2[i]) : 0.0);
-        glo = fmin(glo, d[i] - r);
-        ghi = fmax(ghi, d[i] + r);
-        if (i + 1 < n) emax = fmax(emax, e2[i]);
-    }
-    const double span = fmax(fabs(glo), fabs(ghi));
-    const double pivmin = 0x1p-1000 * fmax(1.0, emax);
-    glo -= 2.0 * DBL_EPSILON * span + pivmin;
-    ghi += 2.0 * DBL_EPSILON * span + pivmin;
-    // G neighbouring threads per eigenvalue (G a power of two, uniform), each
-    // counting at four of the round's 4 G interior points.  The counts are
-    // bound by instruction issue (a reciprocal per step of each chain), so G
-    // grows only until about one wave per SIMD is busy: more threads per
-    // eigenvalue take fewer rounds but more work in all
+    double glo, ghi, pivmin;
+    const lds_f64* dl = (const lds_f64*)d;  // ds_ instructions in the counts
+    const lds_f64* el = (const lds_f64*)e2;
+    gershgorin(dl, el, n, glo, ghi, pivmin);
+    // the counts are bound by instruction issue (a reciprocal per step of
+    // each chain), so G grows only until about one wave per SIMD is busy:
+    // more threads per eigenvalue take fewer rounds but more work in all
     int G = 1;
     while (G < 8 && 2 * G * n <= 256) G *= 2;
     const int g = tid % G;
     for (int k = tid / G; k < n; k += EIG_THREADS / G) {
-        // the k-th smallest eigenvalue: count(lo) <= k < count(hi); a round
-        // keeps the one of its 4 G + 1 parts of the interval holding it (the
-        // group's threads agree on lo and hi after every round)
-        double lo = glo, hi = ghi;
-        for (int it = 0; it < 64; ++it) {
-            if (!(hi - lo > 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin)) break;
-            const double h = (hi - lo) / (double)(4 * G + 1);
-            double x[4], q[4];
-            int c[4];
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                x[u] = lo + h * (double)(4 * g + u + 1);
-                q[u] = d[0] - x[u];
-                if (fabs(q[u]) < pivmin) q[u] = -pivmin;
-                c[u] = q[u] < 0.0;
-            }
-            for (int i = 1; i < n; ++i) {
-                const double di = d[i], ei = e2[i - 1];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) {
-                    q[u] = di - x[u] - ei * recip_nr(q[u]);
-                    if (fabs(q[u]) < pivmin) q[u] = -pivmin;
-                    c[u] += q[u] < 0.0;
-                }
-            }
-            double nlo = lo, nhi = hi;
-#pragma unroll
-            for (int u = 0; u < 4; ++u) {
-                if (c[u] <= k) nlo = fmax(nlo, x[u]);
-                else nhi = fmin(nhi, x[u]);
-            }
-            for (int off = 1; off < G; off <<= 1) {
-                nlo = fmax(nlo, __shfl_xor(nlo, off));
-                nhi = fmin(nhi, __shfl_xor(nhi, off));
-            }
-            if (nlo == lo && nhi == hi) break;  // no representable progress
-            lo = nlo;
-            hi = nhi;
-        }
-        const double lam = 0.5 * (lo + hi);
+        const double lam = multisect(dl, el, n, k, g, G, glo, ghi, pivmin);
         if (g == 0) t.out[n - 1 - k] = sqrt(fmax(lam, 0.0));
     }
+}
+
+// ---------------------------------------------------------------------------
+// Gram matrices larger than SVD_SMALL_K: one Householder step is four
+// launches over the whole device (the reflector; the product p = beta A u in
+// 64-column x 256-row blocks; the blocks' partial sums added in block order,
+// with K = beta (p . u) / 2; the rank-two update in the same blocks), then the
+// tridiagonal matrix's eigenvalues by multisection with enough threads per
+// eigenvalue to fill the device.  The matrix stays in place in the workspace.
+// ---------------------------------------------------------------------------
+constexpr int HH_THREADS = 1024;  // one-workgroup kernels
+constexpr int HH_COLS = 64;       // columns per block (one per lane)
+constexpr int HH_ROWS = 256;      // rows per block (64 per wave)
+
+struct HhState {
+    double beta, K2;
+    double glo, ghi, pivmin;
+    int32_t skip;  // the step's column is already reduced
+};
+
+__device__ double sum_1024(double v, double* red)
+{
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    __syncthreads();
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = v;
+    __syncthreads();
+    double s = 0.0;
+    for (int u = 0; u < HH_THREADS / 64; ++u) s += red[u];
+    return s;
+}
+
+// step k: u = column k below the diagonal (read along row k, the same values
+// up to the rounding of the Gram matrix's accumulation), with u0 = x0 - alpha
+// in place of x0; d[k], e2[k] = alpha^2, beta
+__global__ __launch_bounds__(HH_THREADS) void k_hh_reflector(double* A, int n, int k, double* u,
+                                                             double* d, double* e2, HhState* hs)
+{
+    __shared__ double red[HH_THREADS / 64];
+    const int m = n - k - 1, tid = threadIdx.x;
+    const double* row = A + (size_t)k * n + (k + 1);
+    double tail = 0.0;
+    for (int i = tid; i < m; i += HH_THREADS) {
+        const double x = row[i];
+        u[i] = x;
+        if (i > 0) tail += x * x;
+    }
+    tail = sum_1024(tail, red);
+    if (tid == 0) {
+        const double x0 = row[0];
+        d[k] = A[(size_t)k * n + k];
+        if (!(tail > 0.0)) {
+            e2[k] = x0 * x0;
+            hs->skip = 1;
+        } else {
+            const double alpha = (x0 >= 0.0) ? -sqrt(x0 * x0 + tail) : sqrt(x0 * x0 + tail);
+            const double u0 = x0 - alpha;
+            e2[k] = alpha * alpha;
+            u[0] = u0;
+            hs->beta = 2.0 / (u0 * u0 + tail);
+            hs->skip = 0;
+        }
+    }
+}
+
+// partial sums of A_sub u: block (blockIdx.x, blockIdx.y) = 64 columns x 256
+// rows; wave w takes 64 rows, lane l one column (a row is read across lanes)
+__global__ __launch_bounds__(256) void k_hh_matvec(const double* A, int n, int k, const double* u,
+                                                   const HhState* hs, double* part)
+{
+    if (hs->skip) return;  // uniform
+    __shared__ double red[4][HH_COLS];
+    const int m = n - k - 1;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int i = blockIdx.x * HH_COLS + lane;
+    const int j0 = blockIdx.y * HH_ROWS + w * 64, j1 = min(j0 + 64, m);
+    double s0 = 0.0, s1 = 0.0, s2 = 0.0, s3 = 0.0;
+    if (i < m) {
+        const double* col = A + (size_t)(k + 1) * n + (k + 1 + i);
+        int j = j0;
+        for (; j + 4 <= j1; j += 4) {
+            s0 += col[(size_t)j * n] * u[j];
+            s1 += col[(size_t)(j + 1) * n] * u[j + 1];
+            s2 += col[(size_t)(j + 2) * n] * u[j + 2];
+            s3 += col[(size_t)(j + 3) * n] * u[j + 3];
+        }
+        for (; j < j1; ++j) s0 += col[(size_t)j * n] * u[j];
+    }
+    red[w][lane] = (s0 + s1) + (s2 + s3);
+    __syncthreads();
+    if (w == 0 && i < m)
+        part[(size_t)blockIdx.y * n + i] = (red[0][lane] + red[1][lane]) + (red[2][lane] + red[3][lane]);
+}
+
+// p = beta (the row blocks' partial sums, in block order); K2 = beta (p . u) / 2
+__global__ __launch_bounds__(HH_THREADS) void k_hh_combine(int n, int k, const double* u,
+                                                           const double* part, int R, double* p,
+                                                           HhState* hs)
+{
+    if (hs->skip) return;  // uniform
+    __shared__ double red[HH_THREADS / 64];
+    const int m = n - k - 1;
+    const double beta = hs->beta;
+    double dot = 0.0;
+    for (int i = threadIdx.x; i < m; i += HH_THREADS) {
+        double sum = 0.0;
+        for (int r = 0; r < R; ++r) sum += part[(size_t)r * n + i];
+        const double pi = beta * sum;
+        p[i] = pi;
+        dot += pi * u[i];
+    }
+    dot = sum_1024(dot, red);
+    if (threadIdx.x == 0) hs->K2 = 0.5 * beta * dot;
+}
+
+// A_sub -= u w^T + w u^T with w = p - K2 u, in the matvec's blocks
+__global__ __launch_bounds__(256) void k_hh_update(double* A, int n, int k, const double* u,
+                                                   const double* p, const HhState* hs)
+{
+    if (hs->skip) return;  // uniform
+    const int m = n - k - 1;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int i = blockIdx.x * HH_COLS + lane;
+    if (i >= m) return;  // (no barrier below)
+    const int j0 = blockIdx.y * HH_ROWS + w * 64, j1 = min(j0 + 64, m);
+    const double K2 = hs->K2;
+    const double ui = u[i], wi = fma(-K2, ui, p[i]);
+    double* col = A + (size_t)(k + 1) * n + (k + 1 + i);
+#pragma unroll 4
+    for (int j = j0; j < j1; ++j) {
+        const double uj = u[j], wj = fma(-K2, uj, p[j]);
+        col[(size_t)j * n] -= uj * wi + wj * ui;
+    }
+}
+
+// the last 2 x 2 corner; then the Gershgorin interval (one workgroup)
+__global__ __launch_bounds__(HH_THREADS) void k_hh_finish(const double* A, int n, double* d,
+                                                          double* e2, HhState* hs)
+{
+    __shared__ double red[3][HH_THREADS / 64];
+    __shared__ double de[2][3];
+    const int tid = threadIdx.x;
+    if (tid == 0) {
+        // d[n-2], e2[n-2], d[n-1] (n > SVD_SMALL_K >= 2)
+        de[0][0] = A[(size_t)(n - 2) * n + (n - 2)];
+        const double en = A[(size_t)(n - 1) * n + (n - 2)];
+        de[0][1] = en * en;
+        de[0][2] = A[(size_t)(n - 1) * n + (n - 1)];
+        d[n - 2] = de[0][0];
+        e2[n - 2] = de[0][1];
+        d[n - 1] = de[0][2];
+    }
+    __syncthreads();
+    // per-thread ranges of the Gershgorin bounds, then one reduction
+    double glo = INFINITY, ghi = -INFINITY, emax = 0.0;
+    for (int i = tid; i < n; i += HH_THREADS) {
+        const double di = (i == n - 2) ? de[0][0] : (i == n - 1) ? de[0][2] : d[i];
+        const double el = (i > 0) ? ((i - 1 == n - 2) ? de[0][1] : e2[i - 1]) : 0.0;
+        const double er = (i + 1 < n) ? ((i == n - 2) ? de[0][1] : e2[i]) : 0.0;
+        const double r = sqrt(el) + sqrt(er);
+        glo = fmin(glo, di - r);
+        ghi = fmax(ghi, di + r);
+        if (i + 1 < n) emax = fmax(emax, er);
+    }
+    for (int off = 32; off > 0; off >>= 1) {
+        glo = fmin(glo, __shfl_xor(glo, off));
+        ghi = fmax(ghi, __shfl_xor(ghi, off));
+        emax = fmax(emax, __shfl_xor(emax, off));
+    }
+    if ((tid & 63) == 0) {
+        red[0][tid >> 6] = glo;
+        red[1][tid >> 6] = ghi;
+        red[2][tid >> 6] = emax;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        for (int u = 1; u < HH_THREADS / 64; ++u) {
+            glo = fmin(glo, red[0][u]);
+            ghi = fmax(ghi, red[1][u]);
+            emax = fmax(emax, red[2][u]);
+        }
+        const double span = fmax(fabs(glo), fabs(ghi));
+        const double pivmin = 0x1p-1000 * fmax(1.0, emax);
+        hs->glo = glo - (2.0 * DBL_EPSILON * span + pivmin);
+        hs->ghi = ghi + (2.0 * DBL_EPSILON * span + pivmin);
+        hs->pivmin = pivmin;
+    }
+}
+
+// every eigenvalue, G threads each (the grid holds exactly n G threads,
+// rounded up to whole workgroups; whole groups leave together)
+__global__ __launch_bounds__(256) void k_hh_bisect(const double* d, const double* e2, int n, int G,
+                                                   const HhState* hs, double* out)
+{
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int k = (int)(t / G), g = (int)(t % G);
+    if (k >= n) return;
+    const double lam = multisect(d, e2, n, k, g, G, hs->glo, hs->ghi, hs->pivmin);
+    if (g == 0) out[n - 1 - k] = sqrt(fmax(lam, 0.0));
 }
 
 __global__ __launch_bounds__(64) void k_svd_match(const SpecDesc* da, int na, const double* sa,
@@ -459,6 +678,43 @@ hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double
         hipLaunchKernelGGL(k_gram, dim3((unsigned)n_items), dim3(GTHREADS), 0, stream, tasks,
                            n_tasks, n_items);
     hipLaunchKernelGGL(k_svd_eig, dim3((unsigned)n_tasks), dim3(EIG_THREADS), 0, stream, tasks);
+    return hipGetLastError();
+}
+
+int64_t svd_large_scratch(int n)
+{
+    const int64_t R = (n + HH_ROWS - 1) / HH_ROWS;
+    // u, p, d, e2, the row blocks' partial sums, the step state
+    return 4 * (int64_t)n + R * n + (int64_t)((sizeof(HhState) + 7) / 8);
+}
+
+hipError_t launch_svd_large(double* A, int n, double* scratch, double* out, hipStream_t stream)
+{
+    if (n <= SVD_SMALL_K) return hipErrorInvalidValue;
+    const int R = (n + HH_ROWS - 1) / HH_ROWS;
+    double* u = scratch;
+    double* p = u + n;
+    double* d = p + n;
+    double* e2 = d + n;
+    double* part = e2 + n;
+    HhState* hs = reinterpret_cast<HhState*>(part + (size_t)R * n);
+    for (int k = 0; k + 2 < n; ++k) {
+        const int m = n - k - 1;
+        const dim3 blocks((unsigned)((m + HH_COLS - 1) / HH_COLS), (unsigned)((m + HH_ROWS - 1) / HH_ROWS));
+        hipLaunchKernelGGL(k_hh_reflector, dim3(1), dim3(HH_THREADS), 0, stream, A, n, k, u, d, e2,
+                           hs);
+        hipLaunchKernelGGL(k_hh_matvec, blocks, dim3(256), 0, stream, A, n, k, u, hs, part);
+        hipLaunchKernelGGL(k_hh_combine, dim3(1), dim3(HH_THREADS), 0, stream, n, k, u, part,
+                           (int)blocks.y, p, hs);
+        hipLaunchKernelGGL(k_hh_update, blocks, dim3(256), 0, stream, A, n, k, u, p, hs);
+    }
+    hipLaunchKernelGGL(k_hh_finish, dim3(1), dim3(HH_THREADS), 0, stream, A, n, d, e2, hs);
+    // threads per eigenvalue: enough for about 32K threads in all
+    int G = 1;
+    while (G < 8 && (int64_t)G * n < 32768) G *= 2;
+    const int64_t threads = (int64_t)n * G;
+    hipLaunchKernelGGL(k_hh_bisect, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, stream,
+                       d, e2, n, G, hs, out);
     return hipGetLastError();
 }
 

@@ -57,7 +57,10 @@ def _assert_spectra(got, want, label):
 
 SHAPES = [(5,), (1, 1), (3, 7), (16, 16), (17, 33), (2, 3, 4), (4, 1, 9), (8, 64, 128),
           (3, 5, 2, 7), (2, 3, 2, 3, 2), (1, 4, 1, 5, 1), (100, 600), (511, 40), (512, 512),
-          (2, 256, 4096), (20, 25, 700)]
+          (2, 256, 4096), (20, 25, 700),
+          # Gram sides above 512: the many-workgroup reduction (one or two large
+          # unfoldings beside a small one, a side not a multiple of the blocks)
+          (600, 700), (2, 600, 700), (1030, 1100)]
 
 
 @pytest.mark.parametrize("shape", SHAPES)
@@ -125,7 +128,8 @@ def test_unsupported_shapes_are_rejected():
     import torch
     import paper_2512_08365_amd as mag
     with pytest.raises(mag.MagnetonError) as e:
-        mag.invariants([torch.zeros((600, 700), device="cuda")])  # min(M, N) = 600 > 512
+        # min(M, N) = 8193 > MAG_SVD_MAX_K (refused before any device work)
+        mag.invariants([torch.empty((8193, 8194), device="cuda")])
     assert e.value.code == -2
     with pytest.raises(mag.MagnetonError):
         mag.invariants([torch.zeros((2,) * 6, device="cuda")])  # rank 6
