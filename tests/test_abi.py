@@ -212,9 +212,14 @@ def test_invariants_host_side_errors_without_gpu():
     assert lib.mag_invariant_count(ctypes.byref(t), ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_SIZE
     t.rank, t.dims[1] = 3, 0
     assert lib.mag_invariant_count(ctypes.byref(t), ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_SIZE
-    big = N.Tensor(ctypes.c_void_p(256), 2, 0, (ctypes.c_int64 * 5)(600, 700, 0, 0, 0))
+    # a Gram side above 512 takes the many-workgroup path; above MAG_SVD_MAX_K it is refused
+    mid = N.Tensor(ctypes.c_void_p(256), 2, 0, (ctypes.c_int64 * 5)(600, 700, 0, 0, 0))
+    assert lib.mag_invariant_count(ctypes.byref(mid), ctypes.byref(u), ctypes.byref(v)) == 0
+    assert (u.value, v.value) == (1, 600)
+    big = N.Tensor(ctypes.c_void_p(256), 2, 0,
+                   (ctypes.c_int64 * 5)(N.MAG_SVD_MAX_K + 1, N.MAG_SVD_MAX_K + 2, 0, 0, 0))
     assert lib.mag_invariant_count(ctypes.byref(big), ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_SIZE
-    assert b"512" in lib.mag_last_error()
+    assert str(N.MAG_SVD_MAX_K).encode() in lib.mag_last_error()
     assert lib.mag_invariant_count(None, ctypes.byref(u), ctypes.byref(v)) == N.MAG_E_NULL
     b = ctypes.c_size_t(0)
     ok = N.Tensor(ctypes.c_void_p(256), 2, 0, (ctypes.c_int64 * 5)(30, 40, 0, 0, 0))
