@@ -1866,7 +1866,9 @@ void unfolding_task(const mag_tensor* t, int g, mag::SvdTask& task)
             task.lstr[task.nl++] = str[i];
         }
     }
-    task.nt = (int32_t)((task.K + 63) / 64);  // 64-row Gram blocks
+    // row blocks of the Gram product: 32-side blocks for a short side, else 64
+    const int64_t gb = task.K <= mag::GRAM_NARROW ? 32 : 64;
+    task.nt = (int32_t)((task.K + gb - 1) / gb);
     task.nchunk = (int32_t)((task.L + mag::GRAM_CHUNK - 1) / mag::GRAM_CHUNK);
 }
 
@@ -1893,8 +1895,13 @@ int count_invariants(const mag_tensor* t, int32_t* n_unf, int64_t* n_values)
 }
 
 struct InvPlan {
+    // tasks with K <= mag::GRAM_NARROW first (n_narrow of them, n_items_narrow
+    // work items), then the others (n_items work items); spec_off: each task's
+    // offset in the spectra array (the tensors' and unfoldings' order)
     std::vector<mag::SvdTask> tasks;
-    int64_t gram_len = 0, n_items = 0;
+    std::vector<int64_t> spec_off;
+    int n_narrow = 0;
+    int64_t gram_len = 0, n_items = 0, n_items_narrow = 0;
     int large_k = 0;  // largest Gram side above mag::SVD_SMALL_K (0: none)
 };
 
@@ -1903,6 +1910,9 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
     if (n < 0) return fail(MAG_E_SIZE, "n_tensors < 0");
     if (n > 0 && !ts) return fail(MAG_E_NULL, "tensors is NULL");
     pl = InvPlan{};
+    std::vector<mag::SvdTask> wide;
+    std::vector<int64_t> wide_off;
+    int64_t so = 0;
     for (int32_t i = 0; i < n; ++i) {
         int32_t u;
         int64_t v;
@@ -1911,13 +1921,26 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
         for (int g = 1; g < (1 << ts[i].rank) - 1; g += 2) {
             mag::SvdTask task;
             unfolding_task(&ts[i], g, task);
-            task.item0 = pl.n_items;
-            pl.n_items += (int64_t)task.nt * (task.nt + 1) / 2 * task.nchunk;
+            const int64_t items = (int64_t)task.nt * (task.nt + 1) / 2 * task.nchunk;
             pl.gram_len += task.K * task.K;
             if (task.K > mag::SVD_SMALL_K) pl.large_k = std::max(pl.large_k, (int)task.K);
-            pl.tasks.push_back(task);
+            if (task.K <= mag::GRAM_NARROW) {
+                task.item0 = pl.n_items_narrow;
+                pl.n_items_narrow += items;
+                pl.tasks.push_back(task);
+                pl.spec_off.push_back(so);
+            } else {
+                task.item0 = pl.n_items;
+                pl.n_items += items;
+                wide.push_back(task);
+                wide_off.push_back(so);
+            }
+            so += task.K;
         }
     }
+    pl.n_narrow = (int)pl.tasks.size();
+    pl.tasks.insert(pl.tasks.end(), wide.begin(), wide.end());
+    pl.spec_off.insert(pl.spec_off.end(), wide_off.begin(), wide_off.end());
     return MAG_OK;
 }
 
@@ -2001,19 +2024,19 @@ int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra
     const size_t need = carve_invariants(pl, nullptr, &dtasks, &gram, &large);
     if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
     carve_invariants(pl, workspace, &dtasks, &gram, &large);
-    int64_t go = 0, so = 0;
-    for (auto& t : pl.tasks) {
+    int64_t go = 0;
+    for (size_t i = 0; i < pl.tasks.size(); ++i) {
+        mag::SvdTask& t = pl.tasks[i];
         t.gram = gram + go;
-        t.out = spectra + so;
+        t.out = spectra + pl.spec_off[i];
         go += t.K * t.K;
-        so += t.K;
     }
     hipError_t e;
     if ((e = hipMemcpyAsync(dtasks, pl.tasks.data(), sizeof(mag::SvdTask) * pl.tasks.size(),
                             hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(e, "task copy");
-    if ((e = mag::launch_svd(dtasks, (int)pl.tasks.size(), pl.n_items, gram, pl.gram_len, stream)) !=
-        hipSuccess)
+    if ((e = mag::launch_svd(dtasks, (int)pl.tasks.size(), pl.n_narrow, pl.n_items_narrow,
+                             pl.n_items, gram, pl.gram_len, stream)) != hipSuccess)
         return hip_fail(e, "invariant kernels");
     for (const auto& t : pl.tasks)
         if (t.K > mag::SVD_SMALL_K &&

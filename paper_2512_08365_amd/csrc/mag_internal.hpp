@@ -265,6 +265,7 @@ constexpr int SVD_MAX_K = 8192;       // largest Gram side (min(M, N) of an unfo
 constexpr int SVD_SMALL_K = 512;      // Gram sides reduced by one workgroup (larger: many)
 constexpr int SVD_MAX_UNF = 15;       // unfoldings of a rank-5 tensor, complements folded
 constexpr int64_t GRAM_CHUNK = 2048;  // unfolding columns per Gram work item
+constexpr int GRAM_NARROW = 32;       // Gram sides up to this use 32-side blocks (else 64)
 
 struct SvdTask {
     const float* data;
@@ -274,8 +275,8 @@ struct SvdTask {
     int64_t ldim[SVD_MAX_RANK], lstr[SVD_MAX_RANK];
     double* gram;    // [K][K]
     double* out;     // [K] singular values, descending
-    int64_t item0;   // first Gram work item of this task
-    int32_t nt;      // 64-row blocks: ceil(K / 64)
+    int64_t item0;   // first Gram work item of this task (within its block size's launch)
+    int32_t nt;      // row blocks: ceil(K / 32) when K <= GRAM_NARROW, else ceil(K / 64)
     int32_t nchunk;  // column chunks: ceil(L / GRAM_CHUNK)
 };
 
@@ -288,9 +289,10 @@ struct SpecDesc {
 };
 
 // Gram matrices (zeroed, then accumulated), then the spectra of the tasks
-// with K <= SVD_SMALL_K
-hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double* gram,
-                      int64_t gram_len, hipStream_t stream);
+// with K <= SVD_SMALL_K; the first n_narrow tasks (K <= GRAM_NARROW) are
+// numbered by their own n_items_narrow work items, the others by n_items
+hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n_items_narrow,
+                      int64_t n_items, double* gram, int64_t gram_len, hipStream_t stream);
 // the spectrum of one n x n Gram matrix with n > SVD_SMALL_K (overwritten):
 // a Householder step is four launches over the whole device, then
 // multisection on Sturm counts; scratch of svd_large_scratch(n) doubles

@@ -56,23 +56,27 @@ __global__ void k_svd_clear(double* g, int64_t n)
         g[i] = 0.0;
 }
 
-// One workgroup of 16 waves per (task, 64 x 64 block of the upper triangle,
-// chunk of GRAM_CHUNK columns).  Each 64-column step stages the block's 64
-// rows of each operand in LDS as fp64, eight gathered elements per thread;
-// wave w then multiplies tile (w / 4, w % 4) from LDS with 16 MFMA steps
-// while the next step's elements are in flight.  The gather runs along
+// One workgroup per (task, GB x GB block of the upper triangle, chunk of
+// GRAM_CHUNK columns), one wave per 16 x 16 tile of the block (GB = 64: 16
+// waves; GB = 32, for unfoldings with at most 32 rows: 4 waves).  Each
+// 64-column step stages the block's GB rows of each operand in LDS as fp64,
+// GPER gathered elements per thread; wave w then multiplies tile
+// (w / (GB/16), w % (GB/16)) from LDS with 16 MFMA steps while the next step's
+// elements are in flight.  On a diagonal block the tiles below the diagonal
+// are mirrors of those above: their waves only stage.  The gather runs along
 // whichever side of the unfolding has unit stride (the rows when the K side's
 // last mode is the tensor's last, else the columns), so 64 neighbouring
 // threads read 256 contiguous bytes.
-constexpr int GB = 64;              // block side
-constexpr int GSTEP = 64;           // columns staged per step
-constexpr int GTHREADS = 1024;      // 16 waves: one per 16 x 16 tile of the block
-constexpr int GPER = 2 * GB * GSTEP / GTHREADS;  // staged elements per thread and step
+constexpr int GSTEP = 64;  // columns staged per step
 
-__global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_tasks,
-                                                   int64_t n_items)
+template <int GB>
+__global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int n_tasks,
+                                                      int64_t n_items)
 {
-    __shared__ double xa[GSTEP][GB + 1], xb[GSTEP][GB + 1];  // [column][row], padded
+    constexpr int TPB = GB / 16;              // tiles per block side
+    constexpr int THREADS = GB * GB / 4;      // one wave per tile
+    constexpr int GPER = 2 * GB * GSTEP / THREADS;  // staged elements per thread and step
+    __shared__ double xs[2][GSTEP][GB + 1];  // operand, [column][row], padded
     __shared__ int32_t loff[GRAM_CHUNK];
     __shared__ int64_t roff[2][GB];
     const int64_t item = blockIdx.x;
@@ -86,7 +90,7 @@ __global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_t
     const int64_t local = item - t.item0;
     const int64_t chunk = local % t.nchunk;
     int64_t pr = local / t.nchunk;
-    int bi = 0, rowlen = t.nt;  // nt counts 64-row blocks here
+    int bi = 0, rowlen = t.nt;  // nt counts GB-row blocks here
     while (pr >= rowlen && rowlen > 0) {
         pr -= rowlen;
         ++bi;
@@ -95,7 +99,7 @@ __global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_t
     const int bj = bi + (int)pr;
     const int tid = threadIdx.x, lane = tid % GW, wv = tid / GW;
     const int64_t b0 = chunk * GRAM_CHUNK, b1 = min(b0 + GRAM_CHUNK, t.L);
-    for (int64_t q = tid; q < b1 - b0; q += GTHREADS)
+    for (int64_t q = tid; q < b1 - b0; q += THREADS)
         loff[q] = (int32_t)mode_offset((uint32_t)(b0 + q), t.nl, t.ldim, t.lstr);
     if (tid < 2 * GB) {
         const int side = tid / GB, r = tid % GB;
@@ -108,44 +112,69 @@ __global__ __launch_bounds__(GTHREADS) void k_gram(const SvdTask* tasks, int n_t
     __syncthreads();
     // staged element u of this thread: operand, row and column of the step
     auto slot = [&](int u, int& side, int& rr, int& c) {
-        const int q = tid + u * GTHREADS;
+        const int q = tid + u * THREADS;
         side = q / (GB * GSTEP);
         const int rem = q % (GB * GSTEP);
         rr = cols_fast ? rem / GSTEP : rem % GB;
         c = cols_fast ? rem % GSTEP : rem / GB;
     };
+    // a diagonal block's two operands are the same rows: staged once (the
+    // first GPER / 2 elements of every thread are operand 0's).  Measured: a
+    // gain for 32-side blocks (99 -> 93 us on 64 tensors' 32 x 16384
+    // unfoldings), a loss for 64-side ones (286 -> 325 us: their fetch loop
+    // no longer issues its eight loads back to back), which stage both
+    const bool diag = GB == 32 && bi == bj;
     float stage[GPER];
+    // the tensor through a global-memory pointer (a generic one would make
+    // flat loads, which the LDS waits of the products also count)
+    typedef const __attribute__((address_space(1))) float* gfloat;
+    const gfloat data = (gfloat)t.data;
     auto fetch = [&](int64_t s0) {
         const int cols = (int)min((int64_t)GSTEP, b1 - s0);
 #pragma unroll
         for (int u = 0; u < GPER; ++u) {
+            if (diag && u >= GPER / 2) break;
             int side, rr, c;
             slot(u, side, rr, c);
             const int64_t ro = roff[side][rr];
-            stage[u] = (c < cols && ro >= 0) ? t.data[ro + loff[s0 - b0 + c]] : 0.0f;
+            stage[u] = (c < cols && ro >= 0) ? data[ro + loff[s0 - b0 + c]] : 0.0f;
         }
     };
-    const int ti = wv / 4, tj = wv % 4;  // this wave's tile inside the block
+    const int ti = wv / TPB, tj = wv % TPB;  // this wave's tile inside the block
+    // (uniform per wave) a tile below the diagonal of a diagonal block mirrors one above
+    const bool active = (bi != bj) || (ti <= tj);
     const int r = lane & 15, kq = lane >> 4;
     d4 acc = {0.0, 0.0, 0.0, 0.0};
     fetch(b0);
     for (int64_t s0 = b0; s0 < b1; s0 += GSTEP) {
 #pragma unroll
         for (int u = 0; u < GPER; ++u) {
+            if (diag && u >= GPER / 2) break;
             int side, rr, c;
             slot(u, side, rr, c);
-            (side ? xb : xa)[c][rr] = (double)stage[u];  // fp32 widened exactly
+            xs[side][c][rr] = (double)stage[u];  // fp32 widened exactly
         }
         __syncthreads();
         if (s0 + GSTEP < b1) fetch(s0 + GSTEP);  // in flight during the products
+        // (two loops, so that both operands' LDS addresses stay fixed offsets)
+        if (active && diag) {
 #pragma unroll 4
-        for (int c = 0; c < GSTEP; c += 4) {
-            const double a = xa[c + kq][ti * 16 + r];
-            const double b = xb[c + kq][tj * 16 + r];
-            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+            for (int c = 0; c < GSTEP; c += 4) {
+                const double a = xs[0][c + kq][ti * 16 + r];
+                const double b = xs[0][c + kq][tj * 16 + r];
+                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+            }
+        } else if (active) {
+#pragma unroll 4
+            for (int c = 0; c < GSTEP; c += 4) {
+                const double a = xs[0][c + kq][ti * 16 + r];
+                const double b = xs[1][c + kq][tj * 16 + r];
+                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+            }
         }
         __syncthreads();  // before the next step overwrites the staged rows
     }
+    if (!active) return;
     // register j of a lane holds row 4 j + lane/16, column lane%16 of the tile
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
@@ -381,7 +410,10 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
         __syncthreads();
         tridiagonalize((lds_f64*)As, n, v, w, wp, d, e2, red);  // ds_ instructions
     } else {
-        tridiagonalize(t.gram, n, v, w, wp, d, e2, red);
+        // global-memory instructions (generic ones would also count against
+        // the LDS waits)
+        typedef __attribute__((address_space(1))) double gdouble;
+        tridiagonalize((gdouble*)t.gram, n, v, w, wp, d, e2, red);
     }
     double glo, ghi, pivmin;
     const lds_f64* dl = (const lds_f64*)d;  // ds_ instructions in the counts
@@ -667,16 +699,21 @@ __global__ __launch_bounds__(64) void k_svd_match(const SpecDesc* da, int na, co
 
 }  // namespace
 
-hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int64_t n_items, double* gram,
-                      int64_t gram_len, hipStream_t stream)
+hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n_items_narrow,
+                      int64_t n_items, double* gram, int64_t gram_len, hipStream_t stream)
 {
     if (n_tasks <= 0) return hipSuccess;
     const int64_t cb = min((gram_len + 255) / 256, (int64_t)4096);
     hipLaunchKernelGGL(k_svd_clear, dim3((unsigned)max(cb, (int64_t)1)), dim3(256), 0, stream,
                        gram, gram_len);
-    if (n_items > 0)
-        hipLaunchKernelGGL(k_gram, dim3((unsigned)n_items), dim3(GTHREADS), 0, stream, tasks,
-                           n_tasks, n_items);
+    // tasks [0, n_narrow): K <= GRAM_NARROW, 32-side blocks; the rest 64-side
+    if (n_items_narrow > 0)
+        hipLaunchKernelGGL(k_gram<GRAM_NARROW>, dim3((unsigned)n_items_narrow),
+                           dim3(GRAM_NARROW * GRAM_NARROW / 4), 0, stream, tasks, n_narrow,
+                           n_items_narrow);
+    if (n_items > 0 && n_tasks > n_narrow)
+        hipLaunchKernelGGL(k_gram<64>, dim3((unsigned)n_items), dim3(64 * 64 / 4), 0, stream,
+                           tasks + n_narrow, n_tasks - n_narrow, n_items);
     hipLaunchKernelGGL(k_svd_eig, dim3((unsigned)n_tasks), dim3(EIG_THREADS), 0, stream, tasks);
     return hipGetLastError();
 }

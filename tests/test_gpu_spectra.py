@@ -133,3 +133,17 @@ def test_unsupported_shapes_are_rejected():
     assert e.value.code == -2
     with pytest.raises(mag.MagnetonError):
         mag.invariants([torch.zeros((2,) * 6, device="cuda")])  # rank 6
+
+
+def test_large_rank_deficient_unfolding():
+    """A Gram side above 512 whose matrix is rank-deficient (zero rows, and
+    rows repeated): Householder steps whose column is already reduced are
+    skipped, and the zero eigenvalues come out within the bound."""
+    rng = np.random.default_rng(12)
+    T = np.zeros((700, 800), np.float32)
+    T[:300] = rng.standard_normal((300, 800)).astype(np.float32)
+    T[300:350] = T[:50]  # repeated rows
+    T[:, :3] *= 40.0
+    log("[spectra] rank-deficient 700 x 800")
+    _, _, (got,) = _gpu_lists([T])
+    _assert_spectra(got, S.invariants(T), "rank-deficient 700 x 800")
