@@ -423,21 +423,24 @@ def diff(a: dict, b: dict, k: int, workspace=None, asynchronous: bool = False):
 
     if not asynchronous:
         return collect()
-    return PendingDiff(lib, workspace, ro, collect)
+    # the input tables stay referenced until result()
+    return PendingDiff(lib, workspace, ro, collect, (a, b))
 
 
 class PendingDiff:
     """An enqueued comparison (diff(..., asynchronous=True)); result() waits
     for it once (mag_diff_finish) and returns the ranking."""
 
-    def __init__(self, lib, workspace, ro, collect):
+    def __init__(self, lib, workspace, ro, collect, keep=None):
         self._lib, self._ws, self._ro, self._collect = lib, workspace, ro, collect
+        self._keep = keep
         self._done = None
 
     def result(self) -> dict:
         if self._done is None:
             _check(self._lib.mag_diff_finish(self._ws.data_ptr(), ctypes.byref(self._ro)))
             self._done = self._collect()
+            self._keep = None
         return self._done
 
 

@@ -1049,7 +1049,8 @@ int mag_attribute_finish(const void* workspace, mag_key_stats* per_key, mag_summ
     int rc;
     if (t && t->status_pending && t->host_status) {
         // the call already copied its status to pinned memory on its own
-        // stream, which may differ from `stream`: that one is waited for
+        // stream (which may differ from `stream`) and recorded an event
+        // after the copy: that event is waited for, not later work
         t->status_pending = false;
         hipError_t e2;
         if ((e2 = hipEventSynchronize(t->done)) != hipSuccess) {
