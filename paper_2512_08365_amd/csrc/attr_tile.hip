@@ -198,12 +198,16 @@ struct TileLds {
     double2 tF[C][NCOL];  // {t_i, F_i} of local sample i at [i % C][i / C]
     float P[C][NCOL];
     // endpoint window: stream a's entry r at a * WS + r; once the round's merged
-    // positions are known, wx[g] holds the value of gap g (ending at entry g):
-    // its energy per active interval
+    // positions are known, entry p of the round in time order leaves its x at
+    // wx[p] and the piece right of it at wx[64 + p] for the entry after it,
+    // and then wx[g] holds the value of gap g (ending at entry g): its energy
+    // per active interval
     double wx[WIN];
-    // inv[p]: the lane holding the round's p-th endpoint in time order; before
-    // the merge (more than 8 streams), inv[l] marks the round slot l of a
-    // stream's first endpoint: (stream + 1) << 8 | l
+    // F at the end of the segment of the round's entry p
+    double F1[WAVE];
+    // inv[p]: the entry's (segment + 1) | (intervals active after it) << 16 |
+    // (its lane) << 24; before the merge (more than 8 streams), inv[l] marks
+    // the round slot l of a stream's first endpoint: (stream + 1) << 8 | l
     int inv[WAVE];
 };
 
@@ -697,17 +701,25 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
                 if (real) pos = ps;
             }
             const int jm = (j + 1) | (m_after << 16);
-            if (has_gap) sm.inv[pos] = lane;
+            // each entry leaves what the entry after it in time order needs at
+            // its position (the merge's reads of the window are done: a wave's
+            // LDS operations complete in order)
+            if (has_gap) {
+                sm.wx[pos] = x;
+                sm.wx[WAVE + pos] = right;
+                sm.F1[pos] = A1.y;
+                sm.inv[pos] = jm | (lane << 24);
+            }
             wave_sync();
 
             // ---- gap ending at this lane's entry (from the entry before it)
             double v;
             {
-                // the entry before: another lane's (read across lanes), or the
+                // the entry before: the one at the position before, or the
                 // round's starting point
-                const int pl = sm.inv[max(pos - 1, 0)];
-                const double px = bpermf(x, pl), pr = bpermf(right, pl), pF = bpermf(A1.y, pl);
-                const int pjm = bperm(jm, pl);
+                const int pp = max(pos - 1, 0);
+                const double px = sm.wx[pp], pr = sm.wx[WAVE + pp], pF = sm.F1[pp];
+                const int pjm = sm.inv[pp] & 0xffffff;
                 const bool head_gap = (pos == 0);
                 const double xpv = head_gap ? rs_x : px;
                 const double pright = head_gap ? rs_right : pr;
@@ -780,7 +792,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const double vall = read_lane_f64(gpre, WAVE - 1);
             // the round's last entry is where the next round starts
             if (!fin) {
-                const int ll = __builtin_amdgcn_readfirstlane(sm.inv[Er - 1]);
+                const int ll = __builtin_amdgcn_readfirstlane(sm.inv[Er - 1] >> 24);
                 rs_x = read_lane_f64(x, ll);
                 rs_right = read_lane_f64(right, ll);
                 rs_Fn = read_lane_f64(A1.y, ll);
