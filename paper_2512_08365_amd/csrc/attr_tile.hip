@@ -74,6 +74,18 @@ __device__ __forceinline__ double endpoint_x(const double* s, const double* e, i
     return (q & 1) ? e[i] : s[i];
 }
 
+// the address of endpoint q of a stream whose starts begin at byte address
+// base (its ends at base + e_minus_s): s[i] for even q, e[i] for odd q, i = q/2.
+// Selecting between the arrays is a mask of the byte distance between them,
+// so no per-lane choice between two pointers is made
+__device__ __forceinline__ uint64_t endpoint_addr(uint64_t base, int64_t e_minus_s, int64_t q)
+{
+    const uint32_t odd = 0u - ((uint32_t)q & 1u);  // all ones for an end
+    const uint64_t d = (uint64_t)e_minus_s;
+    const uint64_t dsel = ((uint64_t)((uint32_t)(d >> 32) & odd) << 32) | ((uint32_t)d & odd);
+    return base + (((uint64_t)q << 2) & ~(uint64_t)7) + dsel;  // + 8 (q / 2) for q >= 0
+}
+
 // the kernel's arguments, read from the kernel-argument segment where used
 // (scalar loads through the constant cache; the compiler keeps or reloads
 // them as scalar-register pressure allows)
@@ -443,27 +455,27 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
     // the lane's two window entries: stream, rank, and that stream's extent
     const int wa0 = lane >> LW, wa1 = (lane + WAVE) >> LW;
     const int wr0 = lane & (WS - 1), wr1 = (lane + WAVE) & (WS - 1);
-    const int64_t woff0 = bperm64(soff, wa0), wlen0 = bperm64(slen, wa0);
-    const int64_t woff1 = bperm64(soff, wa1), wlen1 = bperm64(slen, wa1);
+    // byte address of the stream's first start (its ends lie e_minus_s further)
+    const int64_t e_minus_s = (int64_t)((const char*)p.e - (const char*)p.s);
+    const uint64_t wbase0 = (uint64_t)p.s + 8 * (uint64_t)bperm64(soff, wa0);
+    const uint64_t wbase1 = (uint64_t)p.s + 8 * (uint64_t)bperm64(soff, wa1);
+    const int64_t wlen0 = bperm64(slen, wa0), wlen1 = bperm64(slen, wa1);
     // window entry of rank r from cursor cur (+inf past the stream's end); `more`:
-    // the last entry of the stream's window, with endpoints after it.  An entry
-    // past the end loads the first sample of this wave's first tile instead (an
-    // address every launch reads), so the load needs no branch.
-    auto wload = [&](int64_t cur, int r, int64_t off, int64_t len, bool& more) -> double {
+    // the last entry of the stream's window, with endpoints after it
+    auto wload = [&](int64_t cur, int r, uint64_t base, int64_t len, bool& more) -> double {
         const int64_t q = cur + r;
         more = (r == WS - 1) && (q + 1 < len);
-        const KArgs k = kargs();
         // an entry past the stream's end reads +inf from device memory, so the
         // value needs no select after its load and is first waited for where
         // it is used
-        const gptr<const double> pe = sreg(k->e), ps = sreg(k->s);
-        const gptr<const double> ptr = (q < len) ? ((q & 1) ? pe : ps) + off + (q >> 1)
-                                                 : (gptr<const double>)&kPastEnd;
+        const gptr<const double> ptr = (q < len)
+            ? (gptr<const double>)endpoint_addr(base, e_minus_s, q)
+            : (gptr<const double>)&kPastEnd;
         return *ptr;
     };
     bool em0, em1;  // `more` flags of the prefetched window
-    double ew0 = wload(bperm64(sq, wa0), wr0, woff0, wlen0, em0);
-    double ew1 = wload(bperm64(sq, wa1), wr1, woff1, wlen1, em1);
+    double ew0 = wload(bperm64(sq, wa0), wr0, wbase0, wlen0, em0);
+    double ew1 = wload(bperm64(sq, wa1), wr1, wbase1, wlen1, em1);
 
     SampleRegs sr;
     if (vector_tile(b0)) sample_prefetch(sr, b0, lane);
@@ -578,8 +590,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             // the next round's window (this tile's next round, or the next
             // tile's first): both start at the cursors after this round
             const int64_t sqn = sq + ta;
-            ew0 = wload(bperm64(sqn, wa0), wr0, woff0, wlen0, em0);
-            ew1 = wload(bperm64(sqn, wa1), wr1, woff1, wlen1, em1);
+            ew0 = wload(bperm64(sqn, wa0), wr0, wbase0, wlen0, em0);
+            ew1 = wload(bperm64(sqn, wa1), wr1, wbase1, wlen1, em1);
 
             // ---- round slot of this lane: stream my_a, rank my_r (lane Er: the tile's end)
             const bool real = lane < Er;
@@ -894,12 +906,12 @@ __global__ __launch_bounds__(WAVE) void k_tile_seq(const TileParams p)
 
     // window: lane l holds endpoint sq + l; past the stream's end it reads +inf
     // from device memory, so the value needs no select after its load
+    const int64_t e_minus_s = (int64_t)((const char*)p.e - (const char*)p.s);
     auto wload = [&](int64_t cur) -> double {
         const int64_t q = cur + lane;
-        const KArgs k = kargs();
-        const gptr<const double> pe = sreg(k->e), ps = sreg(k->s);
-        const gptr<const double> ptr =
-            (q < len) ? ((q & 1) ? pe : ps) + (q >> 1) : (gptr<const double>)&kPastEnd;
+        const gptr<const double> ptr = (q < len)
+            ? (gptr<const double>)endpoint_addr((uint64_t)p.s, e_minus_s, q)
+            : (gptr<const double>)&kPastEnd;
         return *ptr;
     };
     double ew = wload(sq);
