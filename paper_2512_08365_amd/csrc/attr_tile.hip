@@ -63,7 +63,7 @@ constexpr int T = TILE;
 constexpr int NCOL = WAVE + 1;  // sample columns: the tile's last sample is row 0, column 64
 constexpr int WIN = 2 * WAVE;   // window entries, two per lane
 constexpr int SLOTS = WAVE - 1; // endpoints per round
-constexpr int64_t RUN_TILES = 32;  // most tiles one workgroup walks
+constexpr int64_t RUN_TILES = 16;  // most tiles one workgroup walks
 static_assert(T == WAVE * C && C == 8, "tile layout");
 
 __device__ __forceinline__ double endpoint_x(const double* s, const double* e, int64_t off,
@@ -1103,8 +1103,9 @@ hipError_t launch_tile_kernel(void (*kern)(TileParams), int& per_cu, TileParams 
     // runs of at most RUN_TILES tiles: many more workgroups than fit at once,
     // so the hardware deals them out as slots free up -- workgroups of other
     // kernels (another attribution's grouping) interleave with them, and no
-    // slot is left with a long run started late (measured: 32 tiles per run
-    // is as fast as one run per resident wave when the kernel runs alone)
+    // slot is left with a long run started late (measured on the A/B step of
+    // the multi-stream 100M-sample workload: 16 tiles per run 0.978 ms per
+    // step, 32 tiles 0.987 ms, 8 tiles no faster than 32)
     const int64_t waves = (int64_t)device_cu_count() * per_cu;
     p.tiles_per_wg = std::min<int64_t>((ntiles + waves - 1) / waves, RUN_TILES);
     const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
