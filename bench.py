@@ -31,7 +31,9 @@ Prints ONE JSON line.  `value` is operator intervals attributed per second
 (`pipeline_roofline`, at 12 B per sample and 48 B per interval).  `roofline`
 covers the dominant kernel (the interval-energy tile kernel), timed with HIP
 events on the call's stream; `cpu_baseline` is the CPU oracle timed on one
-pinned host core over sides of the same workload.
+pinned host core over sides of the same workload.  `copy_ceiling` is the
+achievable bandwidth of a trivial 1 GiB copy kernel measured in the same run;
+both rooflines also give their fraction of it (`frac_of_copy_ceiling`).
 """
 from __future__ import annotations
 
@@ -91,6 +93,37 @@ def copy_calibration():
         torch.mul(src, 1.0, out=dst)
     torch.cuda.synchronize()
     log(f"[calibration] copied {COPY_BYTES} bytes 3 times")
+
+
+# achievable HBM bandwidth on this device, measured once per run (copy_ceiling)
+CEILING = {}
+
+
+def copy_ceiling(torch):
+    """The achievable-bandwidth ceiling: a trivial streaming copy kernel
+    (torch's vectorized elementwise kernel computing dst = src * 1, the
+    calibration copy: COPY_BYTES read and COPY_BYTES written), the median of 10
+    launches timed with HIP events after 2 untimed ones.  (torch's copy_ goes
+    through the runtime's blit kernel, measured slower: 4.4-5.1 against
+    6.1-6.2 TB/s.)"""
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        torch.mul(src, 1.0, out=dst)
+    ev = []
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        torch.mul(src, 1.0, out=dst)
+        e1.record()
+        ev.append((e0, e1))
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in ev)[len(ev) // 2]
+    del src, dst
+    torch.cuda.empty_cache()
+    CEILING.update({"kernel": "elementwise dst = src * 1 over 1 GiB (1 GiB read + 1 GiB written)",
+                    "gbps": 2 * COPY_BYTES / (ms * 1e-3) / 1e9, "ms": ms})
+    log(f"[bench] copy ceiling {CEILING['gbps']:.0f} GB/s")
 
 
 def _counter_rows(path, kernel_substr, counter):
@@ -489,6 +522,7 @@ def main():
         return
     lib = N.load()
     log(f"[bench] {mag.version()} on {torch.cuda.get_device_name(0)}")
+    copy_ceiling(torch)
     if args.workload in (1, 2, 3):
         ab_bench(args, torch, mag, lib, N, synth)
     elif args.workload == 4:
@@ -544,7 +578,12 @@ def result_line(args, cfg, sh, sides, sec_per_step, extra):
                               "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
                               "algorithmic_bytes_per_step": bytes_step},
     }
+    if CEILING:
+        r["copy_ceiling"] = dict(CEILING)
+        r["pipeline_roofline"]["frac_of_copy_ceiling"] = gbs / CEILING["gbps"]
     r.update(extra)
+    if CEILING and "roofline" in r:
+        r["roofline"]["frac_of_copy_ceiling"] = r["roofline"]["achieved"] / CEILING["gbps"]
     return r
 
 

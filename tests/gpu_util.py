@@ -47,12 +47,26 @@ def run_oracle(c: dict, equal_split=True):
     return r, g
 
 
+def log_error_distribution(err, want, what):
+    """The relative-error distribution of one comparison (max, 99th percentile,
+    median over the nonzero expected values; the largest absolute error where
+    the expected value is zero), logged as an [err] line."""
+    nz = want != 0
+    rel = err[nz] / np.abs(want[nz])
+    zmax = float(err[~nz].max()) if (~nz).any() else 0.0
+    if rel.size:
+        log(f"[err] {what}: n={want.size} max_rel={rel.max():.3e} "
+            f"p99_rel={np.quantile(rel, 0.99):.3e} median_rel={np.median(rel):.3e} "
+            f"zero_expected={int((~nz).sum())} max_abs_there={zmax:.3e}")
+
+
 def assert_energy_close(got, want, what="energy"):
     got = np.asarray(got)
     want = np.asarray(want)
     assert got.shape == want.shape, what
     err = np.abs(got - want)
     bound = E_RTOL * np.abs(want)
+    log_error_distribution(err, want, what)
     bad = np.nonzero(err > bound)[0]
     assert bad.size == 0, (f"{what}: {bad.size} mismatches, first {bad[:5]}: got {got[bad[:5]]} "
                            f"want {want[bad[:5]]}")
