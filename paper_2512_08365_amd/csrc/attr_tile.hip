@@ -18,10 +18,12 @@
 //             the mean spacing, checked, binary search as the fallback), which
 //             is also its sample index; the interpolated power P^(x); the
 //             pieces of segment j left and right of x; its position in the
-//             time order of all streams (the number of endpoints of every
-//             stream that precede it, by searches of the streams' sorted
-//             windows) and the number of intervals active after it (a stream
-//             is inside an interval exactly when its cursor is odd);
+//             time order of all streams (the endpoints in earlier segments,
+//             from a count histogram over the tile's segments, plus those of
+//             its own segment ordered before it by direct comparison: a
+//             segment index never decreases with x) and, by a scan over the
+//             positions of the +1 / -1 each start / end makes, the number of
+//             intervals active before it;
 //   gaps      the lane of each endpoint integrates the gap from the endpoint
 //             before it in time order: within one segment the trapezoid of the
 //             two interpolated values; otherwise the right piece of the earlier
@@ -188,14 +190,6 @@ __device__ __forceinline__ double read_lane_f64(double v, int l)
     return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
 }
 
-// the smallest double above a finite x (so that y <= x  <=>  y < next_up(x))
-__device__ __forceinline__ double next_up(double x)
-{
-    const long long b = __double_as_longlong(x);
-    if (x == 0.0) return __longlong_as_double(1ll);
-    return __longlong_as_double(x > 0.0 ? b + 1 : b - 1);
-}
-
 // segment energy, one expression for every place that computes it
 __device__ __forceinline__ double seg_energy(double ta, double tb, float pa, float pb)
 {
@@ -209,17 +203,22 @@ template <int SP>
 struct TileLds {
     double2 tF[C][NCOL];  // {t_i, F_i} of local sample i at [i % C][i / C]
     float P[C][NCOL];
-    // endpoint window: stream a's entry r at a * WS + r; once the round's merged
-    // positions are known, entry p of the round in time order leaves its x at
-    // wx[p] and the piece right of it at wx[64 + p] for the entry after it,
-    // and then wx[g] holds the value of gap g (ending at entry g): its energy
-    // per active interval
+    // endpoint window: stream a's entry r at a * WS + r; once every slot lane
+    // has read its entry, the segment histogram of the merge (16-bit counts,
+    // then prefixes, two per word); once the round's merged positions are
+    // known, entry p of the round in time order leaves its x at wx[p] and the
+    // piece right of it at wx[64 + p] for the entry after it, and then wx[g]
+    // holds the value of gap g (ending at entry g): its energy per active
+    // interval
     double wx[WIN];
-    // F at the end of the segment of the round's entry p
+    // F at the end of the segment of the round's entry p (during the merge:
+    // the x of entries sharing a segment)
     double F1[WAVE];
-    // inv[p]: the entry's (segment + 1) | (intervals active after it) << 16 |
-    // (its lane) << 24; before the merge (more than 8 streams), inv[l] marks
-    // the round slot l of a stream's first endpoint: (stream + 1) << 8 | l
+    // inv[p]: the entry's (segment + 1) | (1 + the change it makes to the
+    // number of active intervals) << 16 | (its lane) << 24; before the merge
+    // (more than 8 streams), inv[l] marks the round slot l of a stream's first
+    // endpoint: (stream + 1) << 8 | l; during the merge, the (stream, rank) of
+    // entries sharing a segment
     int inv[WAVE];
 };
 
@@ -581,10 +580,6 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const int fa = incl - ta;
             const int Er = __builtin_amdgcn_readlane(incl, WAVE - 1);
             const int G = Er + (fin ? 1 : 0);  // gaps of the round
-            int top = 1;  // smallest power of two >= every stream's take
-#pragma unroll
-            for (int v = 1; v < WS; v <<= 1)
-                if (__ballot(ta > v) != 0ull) top = v << 1;
             if (SP > 8 && lane < SP && ta > 0) sm.inv[fa] = ((lane + 1) << 8) | fa;
             wave_sync();
             // the next round's window (this tile's next round, or the next
@@ -626,7 +621,6 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             const double acc_a = bpermf(sacc, my_a);
             const int st_a = bperm(sstarted, my_a);
             const double lx_a = bpermf(slastx, my_a);
-            const uint64_t qpar = __ballot(lane < SP && (sq & 1));
             const double x = real ? sm.wx[(my_a << LW) + my_r] : tau_end;
             const double xp = (my_r > 0) ? sm.wx[(my_a << LW) + max(my_r - 1, 0)] : lx_a;
 
@@ -676,53 +670,90 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
             // finite and not before the stream's previous endpoint
             if (real && kk->validate && (!(fabs(x) < INFINITY) || !(xp <= x))) err |= ERR_INTERVAL;
 
-            // ---- merged position and the number of intervals active after x
+            // ---- merged position: the round's entries in the order of (x, stream,
+            // rank).  A count histogram over the tile's segments (16-bit counts,
+            // two per word, in the window's LDS, which every slot lane has read)
+            // gives each entry the number of entries in earlier segments (a
+            // segment index never decreases with x); the few entries that share
+            // a segment order themselves by direct comparison.
             int pos = lane;
-            int m_after = (int)((q + 1) & 1);
-            if constexpr (SP > 1) {
-                // endpoints of every other stream before x (ties: the lower stream
-                // first): binary searches of the sorted windows, run side by side
-                const double xu = next_up(x);
-                constexpr int NO = SP > 1 ? SP - 1 : 1;  // other streams
-                int c[NO], wb[NO], tb[NO];
-                double thr[NO];
+            {
+                uint32_t* hist = reinterpret_cast<uint32_t*>(sm.wx);  // bin i: half i & 1 of word i >> 1
+                static_assert(sizeof(sm.wx) >= T * 2, "segment histogram fits the window");
+                wave_sync();  // every lane's reads of the window are done
+                reinterpret_cast<uint4*>(hist)[lane] = make_uint4(0u, 0u, 0u, 0u);
+                const int jj = real ? j : 0;  // the bin of a real entry (j < L <= T)
+                const int sh = 16 * (jj & 1);
+                uint32_t old = 0u;
+                wave_sync();
+                if (real) old = atomicAdd(&hist[jj >> 1], 1u << sh);
+                wave_sync();
+                // exclusive prefix over the bins: lane l holds bins 8l .. 8l + 7
+                const uint4 hw = reinterpret_cast<const uint4*>(hist)[lane];
+                const uint32_t hv[4] = {hw.x, hw.y, hw.z, hw.w};
+                int run = 0;
+                uint32_t pw[4];
 #pragma unroll
-                for (int d = 0; d < SP - 1; ++d) {
-                    const int bs = (my_a + d + 1) & (SP - 1);
-                    tb[d] = bperm(ta, bs);
-                    thr[d] = (bs < my_a) ? xu : x;
-                    wb[d] = bs << LW;
-                    c[d] = 0;
+                for (int u = 0; u < 4; ++u) {
+                    const int c0 = (int)(hv[u] & 0xffffu), c1 = (int)(hv[u] >> 16);
+                    pw[u] = (uint32_t)run | ((uint32_t)(run + c0) << 16);
+                    run += c0 + c1;
                 }
-#pragma unroll
-                for (int step = WS / 2; step > 0; step >>= 1) {
-                    if (step < top) {
-#pragma unroll
-                        for (int d = 0; d < SP - 1; ++d)
-                            c[d] += (sm.wx[wb[d] + c[d] + step - 1] < thr[d]) ? step : 0;
+                const int base = scan_add_i32(run) - run;
+                const uint32_t badd = (uint32_t)base | ((uint32_t)base << 16);
+                reinterpret_cast<uint4*>(hist)[lane] =
+                    make_uint4(pw[0] + badd, pw[1] + badd, pw[2] + badd, pw[3] + badd);
+                wave_sync();
+                // entries before my segment, and in it (the next bin's prefix, or
+                // the round's count after the last bin)
+                const int before = (int)((hist[jj >> 1] >> sh) & 0xffffu);
+                const int jn = min(jj + 1, T - 1);
+                const int after = (jj + 1 < T) ? (int)((hist[jn >> 1] >> (16 * (jn & 1))) & 0xffffu) : Er;
+                const int kj = after - before;
+                const int o = (int)((old >> sh) & 0xffffu);  // arrival order within the segment
+                const bool coll = real && kj > 1;
+                int w = 0;
+                if (__ballot(coll) != 0ull) {
+                    // the segment's entries leave x and (stream, rank) at
+                    // [before, after) of two scratch arrays, then count those
+                    // ordered before them
+                    const int key = (my_a << 8) | my_r;
+                    if (coll) {
+                        sm.F1[before + o] = x;
+                        sm.inv[before + o] = key;
                     }
+                    wave_sync();
+                    for (int i = 0; __ballot(coll && i < kj) != 0ull; ++i) {
+                        if (coll && i < kj && i != o) {
+                            const double y = sm.F1[before + i];
+                            const int ky = sm.inv[before + i];
+                            w += (y < x || (y == x && ky < key)) ? 1 : 0;
+                        }
+                    }
+                    wave_sync();
                 }
-                int ps = my_r;
-#pragma unroll
-                for (int d = 0; d < SP - 1; ++d) {
-                    const int bs = (my_a + d + 1) & (SP - 1);
-                    const int cc = min(c[d] + ((sm.wx[wb[d] + c[d]] < thr[d]) ? 1 : 0), tb[d]);
-                    ps += cc;
-                    m_after += (int)(((qpar >> bs) + (uint64_t)cc) & 1ull);
-                }
-                if (real) pos = ps;
+                if (real) pos = before + w;
             }
-            const int jm = (j + 1) | (m_after << 16);
+            // the entry's segment, and the change it makes to the number of active
+            // intervals (+1 a start, -1 an end, 0 the round's end) offset by 1
+            const int jd = (j + 1) | ((real ? ((q & 1) ? 0 : 2) : 1) << 16);
             // each entry leaves what the entry after it in time order needs at
-            // its position (the merge's reads of the window are done: a wave's
-            // LDS operations complete in order)
+            // its position (the merge's reads of LDS are done: a wave's LDS
+            // operations complete in order)
             if (has_gap) {
                 sm.wx[pos] = x;
                 sm.wx[WAVE + pos] = right;
                 sm.F1[pos] = A1.y;
-                sm.inv[pos] = jm | (lane << 24);
+                sm.inv[pos] = jd | (lane << 24);
             }
             wave_sync();
+            // intervals active after each position: the round's starting count
+            // plus a scan of the changes in time order (lane l: position l)
+            const int dl = (lane < G) ? (int)((sm.inv[lane] >> 16) & 0xff) - 1 : 0;
+            const int dincl = scan_add_i32(dl);
+            const int m0 = rs_jm >> 16;  // active at the round's start
+            // active in the gap ending at this lane's entry: after the position before it
+            const int m_gap = m0 + bperm(dincl - dl, pos);
 
             // ---- gap ending at this lane's entry (from the entry before it)
             double v;
@@ -754,7 +785,7 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
                     }
                 }
                 const double Q = same ? q_in : (pright + whole) + left;
-                const int mp = pe >> 16;
+                const int mp = m_gap;
                 // read with every lane active: a lane that is switched off
                 // cannot be read across lanes
                 const double inv_mp = bpermf(inv_lane, mp);
@@ -808,7 +839,8 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
                 rs_x = read_lane_f64(x, ll);
                 rs_right = read_lane_f64(right, ll);
                 rs_Fn = read_lane_f64(A1.y, ll);
-                rs_jm = __builtin_amdgcn_readlane(jm, ll);
+                rs_jm = (__builtin_amdgcn_readlane(j, ll) + 1) |
+                        ((m0 + __builtin_amdgcn_readlane(dincl, WAVE - 1)) << 16);
             }
             // ---- commit the round (stream lanes)
             {

@@ -30,13 +30,27 @@ def _gpu():
 # small randomized cases
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("streams", [1, 2, 3, 4, 7])
+@pytest.mark.parametrize("streams", [1, 2, 3, 4, 7, 12, 20])
 def test_tiny_fuzz(streams):
     for seed in range(25):
         c = synth.tiny_case(5000 * streams + seed, n=int(2 + (seed * 37) % 300), streams=streams,
                             per_stream=int(seed % 13))
         for split in (True, False):
             compare_attribution(c, equal_split=split, label=f"tiny s{streams} seed{seed}")
+
+
+def test_endpoints_shared_by_streams():
+    """Streams with identical endpoints (exact ties across streams, many in one
+    segment), on a dyadic grid, against the oracle: energies do not depend on
+    how equal times are ordered, indices and keys are exact."""
+    for streams, per in ((3, 40), (9, 12), (24, 6)):
+        base = synth.tiny_case(900 + streams, n=120, streams=1, per_stream=per, dyadic=True)
+        m = base["s"].shape[0]
+        c = {"t": base["t"], "P": base["P"], "s": np.tile(base["s"], streams),
+             "e": np.tile(base["e"], streams), "key": np.tile(base["key"], streams),
+             "offsets": np.arange(streams + 1, dtype=np.int64) * m}
+        for split in (True, False):
+            compare_attribution(c, equal_split=split, label=f"shared s{streams}")
 
 
 def test_dyadic_bit_exact():
