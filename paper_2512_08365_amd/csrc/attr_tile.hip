@@ -308,9 +308,14 @@ __device__ __forceinline__ void sample_prefetch(SampleRegs& r, int b, int lane)
 // tile-local prefix F (a per-lane running sum plus a DPP scan of the lane
 // totals) of tile b (L segments), staged in LDS as {t, F} and P; returns the
 // tile's energy (uniform)
+// NC = NCOL: the tile's last sample (local index T of a whole tile) goes to
+// column 64 of row 0; NC = WAVE: the arrays hold local samples 0 .. T - 1 only
+// and the last sample's time and power are returned in t_end / p_end (its F is
+// the returned total)
+template <int NC>
 __device__ __forceinline__ double sample_stage(const SampleRegs& r, int b, int L, int lane,
-                                               double2 (*tF)[NCOL], float (*Pl)[NCOL],
-                                               unsigned& err)
+                                               double2 (*tF)[NC], float (*Pl)[NC],
+                                               unsigned& err, double& t_end, float& p_end)
 {
     const KArgs kk = kargs();
     const int64_t j0 = (int64_t)b * T;
@@ -381,10 +386,14 @@ __device__ __forceinline__ double sample_stage(const SampleRegs& r, int b, int L
         Pl[u][lane] = pv[u];
     }
     const double Wt = read_lane_f64(incl, WAVE - 1);
-    if (lane == WAVE - 1) {
-        tF[0][WAVE] = make_double2(tv[C], Wt);
-        Pl[0][WAVE] = pv[C];
+    if constexpr (NC > WAVE) {
+        if (lane == WAVE - 1) {
+            tF[0][WAVE] = make_double2(tv[C], Wt);
+            Pl[0][WAVE] = pv[C];
+        }
     }
+    t_end = read_lane_f64(tv[C], WAVE - 1);
+    p_end = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(pv[C]), WAVE - 1));
     return Wt;
 }
 
@@ -513,7 +522,9 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
         const int L = (int)min((int64_t)T, kk->nseg - j0);
 
         // ---- samples: checks, segment energies, tile-local prefix, staging
-        w_wave += sample_stage(sr, b, L, lane, sm.tF, sm.P, err);
+        double t_end_unused;
+        float p_end_unused;
+        w_wave += sample_stage(sr, b, L, lane, sm.tF, sm.P, err, t_end_unused, p_end_unused);
         if (slane) {
             pend_cnt = sreg(kk->cnt) + ((int64_t)lane * (kk->ld + 1) + b);
             pend_cnt_v = sq;
@@ -901,9 +912,14 @@ __global__ __launch_bounds__(WAVE) void k_tile(const TileParams p)
 // energies.
 // ---------------------------------------------------------------------------
 struct SeqLds {
-    double2 tF[C][NCOL];
-    float P[C][NCOL];
+    // local samples 0 .. T - 1 ({t, F} and P at [i % C][i / C]); a whole
+    // tile's last sample (local index T) is kept in uniform registers, so
+    // that a wave's LDS is exactly 10 KiB (five 2 KiB allocation blocks:
+    // 16 waves per CU instead of 13)
+    double2 tF[C][WAVE];
+    float P[C][WAVE];
 };
+static_assert(sizeof(SeqLds) == 10240, "one-stream tile LDS");
 
 __global__ __launch_bounds__(WAVE) void k_tile_seq(const TileParams p)
 {
@@ -958,14 +974,28 @@ __global__ __launch_bounds__(WAVE) void k_tile_seq(const TileParams p)
         const KArgs kk = kargs();
         const int64_t j0 = (int64_t)b * T;
         const int L = (int)min((int64_t)T, kk->nseg - j0);
-        w_wave += sample_stage(sr, b, L, lane, sm.tF, sm.P, err);
+        double tT;  // a whole tile's last sample: time, power and prefix (uniform)
+        float pT;
+        const double FT = sample_stage(sr, b, L, lane, sm.tF, sm.P, err, tT, pT);
+        w_wave += FT;
         if (lane == 0) kk->cnt[b] = sq;
         // the interval open at the tile's start began in an earlier tile
         int started = 0;
         wave_sync();
-        auto tF_at = [&](int i) -> double2 { return sm.tF[i & (C - 1)][i >> 3]; };
-        auto t_at = [&](int i) -> double { return sm.tF[i & (C - 1)][i >> 3].x; };
-        auto P_at = [&](int i) -> double { return (double)sm.P[i & (C - 1)][i >> 3]; };
+        // local sample i <= L (i = T only for a whole tile; its column index
+        // is wrapped so that the LDS read stays inside the arrays)
+        auto tF_at = [&](int i) -> double2 {
+            const double2 v = sm.tF[i & (C - 1)][(i >> 3) & (WAVE - 1)];
+            return (i == T) ? make_double2(tT, FT) : v;
+        };
+        auto t_at = [&](int i) -> double {
+            const double v = sm.tF[i & (C - 1)][(i >> 3) & (WAVE - 1)].x;
+            return (i == T) ? tT : v;
+        };
+        auto P_at = [&](int i) -> double {
+            const float v = sm.P[i & (C - 1)][(i >> 3) & (WAVE - 1)];
+            return (double)((i == T) ? pT : v);
+        };
         const double t_begin = t_at(0);
         const double tau_end = t_at(L);
         const double inv_dt = (double)L * recip(tau_end - t_begin);
@@ -1059,8 +1089,7 @@ __global__ __launch_bounds__(WAVE) void k_tile_seq(const TileParams p)
                     // the whole segments summed directly
                     double sum = 0.0;
                     for (int i = pjx + 1; i < j; ++i)
-                        sum += seg_energy(t_at(i), t_at(i + 1), sm.P[i & 7][i >> 3],
-                                          sm.P[(i + 1) & 7][(i + 1) >> 3]);
+                        sum += seg_energy(t_at(i), t_at(i + 1), (float)P_at(i), (float)P_at(i + 1));
                     whole = sum;
                 }
             }
