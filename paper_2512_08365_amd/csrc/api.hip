@@ -1274,12 +1274,8 @@ int mag_stream_push(mag_stream* h, const double* t_chunk, const float* p_chunk, 
     };
     auto stage = [&](int64_t at, int64_t from, int64_t count) {
         // chunk samples [from, from + count) into staging slots [at, at + count)
-        hipError_t r = hipMemcpyAsync(job.w.stage_t + at, t_chunk + (from - g0),
-                                      sizeof(double) * count, hipMemcpyDeviceToDevice, st);
-        if (r == hipSuccess)
-            r = hipMemcpyAsync(job.w.stage_P + at, p_chunk + (from - g0), sizeof(float) * count,
-                               hipMemcpyDeviceToDevice, st);
-        return r;
+        return mag::launch_stage_copy(job.w.stage_t + at, t_chunk + (from - g0),
+                                      job.w.stage_P + at, p_chunk + (from - g0), count, st);
     };
     if (g0 == 0 &&
         (e = hipMemcpyAsync(&job.w.status->bounds[0], t_chunk, sizeof(double),
@@ -1310,10 +1306,8 @@ int mag_stream_push(mag_stream* h, const double* t_chunk, const float* p_chunk, 
             pos -= 1;
         } else {
             // its first sample is the staged tile's last one
-            if ((e = hipMemcpyAsync(job.w.stage_t, job.w.stage_t + T, sizeof(double),
-                                    hipMemcpyDeviceToDevice, st)) != hipSuccess ||
-                (e = hipMemcpyAsync(job.w.stage_P, job.w.stage_P + T, sizeof(float),
-                                    hipMemcpyDeviceToDevice, st)) != hipSuccess)
+            if ((e = mag::launch_stage_copy(job.w.stage_t, job.w.stage_t + T, job.w.stage_P,
+                                            job.w.stage_P + T, 1, st)) != hipSuccess)
                 return bad("staging copy");
             h->n_stage = 1;
         }

@@ -231,9 +231,31 @@ __global__ __launch_bounds__(1024) void k_energy_total(const double* energy, int
     }
 }
 
+// samples [0, n) of a time and a power array copied together (one launch
+// instead of two runtime copies, each of which costs a blit kernel)
+__global__ __launch_bounds__(256) void k_stage_copy(double* dst_t, const double* src_t,
+                                                    float* dst_P, const float* src_P, int64_t n)
+{
+    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x) {
+        dst_t[i] = src_t[i];
+        dst_P[i] = src_P[i];
+    }
+}
+
 // ---------------------------------------------------------------------------
 // launchers
 // ---------------------------------------------------------------------------
+hipError_t launch_stage_copy(double* dst_t, const double* src_t, float* dst_P, const float* src_P,
+                             int64_t n, hipStream_t stream)
+{
+    if (n <= 0) return hipSuccess;
+    const int64_t blocks = std::min<int64_t>((n + 255) / 256, 64);
+    hipLaunchKernelGGL(k_stage_copy, dim3((unsigned)blocks), dim3(256), 0, stream, dst_t, src_t,
+                       dst_P, src_P, n);
+    return hipGetLastError();
+}
+
 hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double* t, int64_t n,
                        hipStream_t stream)
 {

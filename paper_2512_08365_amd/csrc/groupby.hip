@@ -380,16 +380,19 @@ __global__ __launch_bounds__(RANK_TILE) void k_rank(const GroupParams p)
 // intervals per thread whose loads are requested together
 constexpr int AGG_BATCH = 16;
 
-// chunk of intervals -> LDS table over ids [r0, r0 + AGG_IDS) -> partial table row
+// chunk of intervals -> LDS table over ids [r0, r0 + SUM_IDS) -> partial table
+// row.  Its 12 bytes per id fit 12,288 ids in 144 KiB of LDS, so a chunk is
+// read once per 12,288 keys (the M2 pass, at 16 bytes per id, per 8,192)
+constexpr int SUM_IDS = 12288;
 __global__ __launch_bounds__(AGG_THREADS) void k_agg_sum(const GroupParams p)
 {
-    __shared__ uint32_t lcnt[AGG_IDS];
-    __shared__ double lsum[AGG_IDS];
+    __shared__ uint32_t lcnt[SUM_IDS];
+    __shared__ double lsum[SUM_IDS];
     const int c = blockIdx.x;
-    const int64_t r0 = (int64_t)blockIdx.y * AGG_IDS;
+    const int64_t r0 = (int64_t)blockIdx.y * SUM_IDS;
     const int64_t nk = min((int64_t)p.kstat->n_unique, p.cap);
     if (r0 >= nk) return;  // uniform
-    const int nid = (int)min((int64_t)AGG_IDS, nk - r0);
+    const int nid = (int)min((int64_t)SUM_IDS, nk - r0);
     for (int v = threadIdx.x; v < nid; v += AGG_THREADS) {
         lcnt[v] = 0u;
         lsum[v] = 0.0;
@@ -832,7 +835,8 @@ hipError_t launch_aggregate(const GroupParams& p, hipStream_t stream)
         const unsigned kb1 = (unsigned)max((int64_t)1, (p.cap + FO_KEYS - 1) / FO_KEYS);
         hipLaunchKernelGGL(k_fin_one, dim3(kb1), dim3(FO_KEYS * FO_GROUPS), 0, stream, p);
     } else if (ranges > 0) {
-        hipLaunchKernelGGL(k_agg_sum, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,
+        const unsigned ranges_sum = (unsigned)((p.cap + SUM_IDS - 1) / SUM_IDS);
+        hipLaunchKernelGGL(k_agg_sum, dim3((unsigned)p.nchunks, ranges_sum), dim3(AGG_THREADS), 0,
                            stream, p);
         hipLaunchKernelGGL(k_fin_sum, dim3(kb), dim3(FIN_KEYS * FIN_GROUPS), 0, stream, p);
         hipLaunchKernelGGL(k_agg_m2, dim3((unsigned)p.nchunks, ranges), dim3(AGG_THREADS), 0,

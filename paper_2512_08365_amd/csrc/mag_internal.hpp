@@ -246,6 +246,10 @@ __device__ __forceinline__ void lds_barrier()
 hipError_t launch_init(Status* st, int64_t* cnt_fin, int64_t n_fin, const double* t, int64_t n,
                        hipStream_t stream);
 hipError_t launch_init_status(Status* st, const double* t, int64_t n, hipStream_t stream);
+// n samples (time and power) copied in one launch: the staging of a streamed
+// tile that spans two chunks
+hipError_t launch_stage_copy(double* dst_t, const double* src_t, float* dst_P, const float* src_P,
+                             int64_t n, hipStream_t stream);
 // tiles [p.tile_begin, p.tile_end) on persistent waves (sets the launch shape);
 // ev_start / ev_stop (may be NULL) are recorded by the launch itself
 hipError_t launch_tile(const TileParams& p, hipStream_t stream, hipEvent_t ev_start = nullptr,
