@@ -16,8 +16,11 @@ kept in flight (`--pipeline`), each with its own outputs and workspaces:
 step i is enqueued before step i-1 is collected, and A's tile kernel of a
 step waits for B's of the step before.  B's key map (distinct keys, ids,
 ranks: it depends on the keys only) is built on a third stream while A's
-trace is integrated.  Side A's tile kernel is timed with HIP events carried
-on its dispatch in every timed step; side B runs untimed.  Inputs are
+trace is integrated.  The diff runs on A's stream of the step once B's call
+is complete (A's two streams alternate, so that stream is idle until the
+step after next), so B's next tile kernel does not queue behind it.  Side
+A's tile kernel is timed with HIP events carried on its dispatch in every
+timed step; side B runs untimed.  Inputs are
 synthetic, seeded and resident in HBM before timing.
 
 --workload 1/2/3/4/5 times the other workloads the same way (2 and 4 fit in
@@ -656,6 +659,7 @@ def ab_bench(args, torch, mag, lib, N, synth):
             self.a_done.record(sa_stream)
             self.b_tiles = torch.cuda.Event()
             self.b_tiles.record(s2)
+            self.b_done = torch.cuda.Event()
             self.d_out = {k: torch.empty(top, dtype=dt, device="cuda") for k, dt in
                           (("key", torch.int64), ("ratio", torch.float64),
                            ("ea", torch.float64), ("eb", torch.float64),
@@ -701,7 +705,7 @@ def ab_bench(args, torch, mag, lib, N, synth):
         # B's trace integration starts once A's is done (the two passes run
         # back to back, each with the device to itself), everything else of
         # each side overlaps the other; the diff reads both key counts on the
-        # device, behind both attributions, on B's stream (A finishes first)
+        # device, behind both attributions
         if a_plan:
             # both key maps on the third stream, A's first, ahead of A's
             # trace integration; each side's call then aggregates only (and
@@ -714,10 +718,19 @@ def ab_bench(args, torch, mag, lib, N, synth):
         # integration only aggregates
         x.sb.build_plan(lib, stream_k)
         x.sb.attribute(lib, x.stream_a if tilestream else stream_b)
-        s2.wait_event(x.a_done)
+        if tilestream:
+            s2.wait_event(x.a_done)
+            d_stream = stream_b
+        else:
+            # the diff runs on A's stream of this step (idle until the step
+            # after next) once B's call is complete, so that B's next trace
+            # integration does not queue behind it on B's stream
+            x.b_done.record(s2)
+            x.s_a.wait_event(x.b_done)
+            d_stream = x.stream_a
         rc = lib.mag_diff_async(x.sa.kout.data_ptr(), ctypes.byref(x.sa.ks_dev),
                                 x.sb.kout.data_ptr(), ctypes.byref(x.sb.ks_dev), top,
-                                ctypes.byref(x.ro), x.d_ws.data_ptr(), x.d_ws.numel(), stream_b)
+                                ctypes.byref(x.ro), x.d_ws.data_ptr(), x.d_ws.numel(), d_stream)
         if rc != 0:
             raise RuntimeError(f"mag_diff_async failed {rc}: {lib.mag_last_error().decode()}")
         x.record = record
