@@ -1864,7 +1864,8 @@ void unfolding_task(const mag_tensor* t, int g, mag::SvdTask& task)
     // row blocks of the Gram product: 32-side blocks for a short side, else 64
     const int64_t gb = task.K <= mag::GRAM_NARROW ? 32 : 64;
     task.nt = (int32_t)((task.K + gb - 1) / gb);
-    task.nchunk = (int32_t)((task.L + mag::GRAM_CHUNK - 1) / mag::GRAM_CHUNK);
+    const int64_t ch = task.K <= mag::GRAM_NARROW ? mag::GRAM_CHUNK_NARROW : mag::GRAM_CHUNK;
+    task.nchunk = (int32_t)((task.L + ch - 1) / ch);
 }
 
 int count_invariants(const mag_tensor* t, int32_t* n_unf, int64_t* n_values)

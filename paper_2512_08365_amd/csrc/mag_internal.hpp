@@ -269,6 +269,7 @@ constexpr int SVD_MAX_K = 8192;       // largest Gram side (min(M, N) of an unfo
 constexpr int SVD_SMALL_K = 512;      // Gram sides reduced by one workgroup (larger: many)
 constexpr int SVD_MAX_UNF = 15;       // unfoldings of a rank-5 tensor, complements folded
 constexpr int64_t GRAM_CHUNK = 2048;  // unfolding columns per Gram work item
+constexpr int64_t GRAM_CHUNK_NARROW = 1024;  // the same for K <= GRAM_NARROW (one 32-side block)
 constexpr int GRAM_NARROW = 32;       // Gram sides up to this use 32-side blocks (else 64)
 
 struct SvdTask {
@@ -281,7 +282,7 @@ struct SvdTask {
     double* out;     // [K] singular values, descending
     int64_t item0;   // first Gram work item of this task (within its block size's launch)
     int32_t nt;      // row blocks: ceil(K / 32) when K <= GRAM_NARROW, else ceil(K / 64)
-    int32_t nchunk;  // column chunks: ceil(L / GRAM_CHUNK)
+    int32_t nchunk;  // column chunks: ceil(L / GRAM_CHUNK), GRAM_CHUNK_NARROW when K <= GRAM_NARROW
 };
 
 // a tensor's invariant list inside a spectra array

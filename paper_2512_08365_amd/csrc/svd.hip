@@ -76,8 +76,13 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
     constexpr int TPB = GB / 16;              // tiles per block side
     constexpr int THREADS = GB * GB / 4;      // one wave per tile
     constexpr int GPER = 2 * GB * GSTEP / THREADS;  // staged elements per thread and step
-    __shared__ double xs[2][GSTEP][GB + 1];  // operand, [column][row], padded
-    __shared__ int32_t loff[GRAM_CHUNK];
+    // a 32-side block is the whole Gram matrix (K <= 32), its one diagonal
+    // block: one operand staged, half the LDS, shorter column chunks (more
+    // workgroups for the same unfoldings)
+    constexpr bool ONE_BLOCK = GB == GRAM_NARROW;
+    constexpr int64_t CH = ONE_BLOCK ? GRAM_CHUNK_NARROW : GRAM_CHUNK;
+    __shared__ double xs[ONE_BLOCK ? 1 : 2][GSTEP][GB + 1];  // operand, [column][row], padded
+    __shared__ int32_t loff[CH];
     __shared__ int64_t roff[2][GB];
     const int64_t item = blockIdx.x;
     if (item >= n_items) return;  // uniform
@@ -98,7 +103,7 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
     }
     const int bj = bi + (int)pr;
     const int tid = threadIdx.x, lane = tid % GW, wv = tid / GW;
-    const int64_t b0 = chunk * GRAM_CHUNK, b1 = min(b0 + GRAM_CHUNK, t.L);
+    const int64_t b0 = chunk * CH, b1 = min(b0 + CH, t.L);
     for (int64_t q = tid; q < b1 - b0; q += THREADS)
         loff[q] = (int32_t)mode_offset((uint32_t)(b0 + q), t.nl, t.ldim, t.lstr);
     if (tid < 2 * GB) {
@@ -123,7 +128,7 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
     // gain for 32-side blocks (99 -> 93 us on 64 tensors' 32 x 16384
     // unfoldings), a loss for 64-side ones (286 -> 325 us: their fetch loop
     // no longer issues its eight loads back to back), which stage both
-    const bool diag = GB == 32 && bi == bj;
+    constexpr bool diag = ONE_BLOCK;
     float stage[GPER];
     // the tensor through a global-memory pointer (a generic one would make
     // flat loads, which the LDS waits of the products also count)
@@ -152,17 +157,22 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
             if (diag && u >= GPER / 2) break;
             int side, rr, c;
             slot(u, side, rr, c);
-            xs[side][c][rr] = (double)stage[u];  // fp32 widened exactly
+            if constexpr (ONE_BLOCK)
+                xs[0][c][rr] = (double)stage[u];  // fp32 widened exactly
+            else
+                xs[side][c][rr] = (double)stage[u];
         }
         __syncthreads();
         if (s0 + GSTEP < b1) fetch(s0 + GSTEP);  // in flight during the products
         // (two loops, so that both operands' LDS addresses stay fixed offsets)
-        if (active && diag) {
+        if constexpr (ONE_BLOCK) {
+            if (active) {
 #pragma unroll 4
-            for (int c = 0; c < GSTEP; c += 4) {
-                const double a = xs[0][c + kq][ti * 16 + r];
-                const double b = xs[0][c + kq][tj * 16 + r];
-                acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+                for (int c = 0; c < GSTEP; c += 4) {
+                    const double a = xs[0][c + kq][ti * 16 + r];
+                    const double b = xs[0][c + kq][tj * 16 + r];
+                    acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+                }
             }
         } else if (active) {
 #pragma unroll 4
