@@ -1837,6 +1837,9 @@ int check_tensor(const mag_tensor* t)
     return MAG_OK;
 }
 
+// Gram sides whose product one workgroup makes whole
+bool gram_whole(int64_t K) { return K > 64 && K <= mag::GRAM_WHOLE; }
+
 // the unfolding of mask g as a Gram task (K side = the shorter side)
 void unfolding_task(const mag_tensor* t, int g, mag::SvdTask& task)
 {
@@ -1861,10 +1864,13 @@ void unfolding_task(const mag_tensor* t, int g, mag::SvdTask& task)
             task.lstr[task.nl++] = str[i];
         }
     }
-    // row blocks of the Gram product: 32-side blocks for a short side, else 64
+    // work items of the Gram product: one 32-side block for a short side, the
+    // whole triangle for a side in (64, GRAM_WHOLE], else pairs of 64-side blocks
     const int64_t gb = task.K <= mag::GRAM_NARROW ? 32 : 64;
-    task.nt = (int32_t)((task.K + gb - 1) / gb);
-    const int64_t ch = task.K <= mag::GRAM_NARROW ? mag::GRAM_CHUNK_NARROW : mag::GRAM_CHUNK;
+    task.nt = gram_whole(task.K) ? 1 : (int32_t)((task.K + gb - 1) / gb);
+    const int64_t ch = task.K <= mag::GRAM_NARROW ? mag::GRAM_CHUNK_NARROW
+                     : gram_whole(task.K)         ? mag::GRAM_CHUNK_WHOLE
+                                                  : mag::GRAM_CHUNK;
     task.nchunk = (int32_t)((task.L + ch - 1) / ch);
 }
 
@@ -1892,12 +1898,13 @@ int count_invariants(const mag_tensor* t, int32_t* n_unf, int64_t* n_values)
 
 struct InvPlan {
     // tasks with K <= mag::GRAM_NARROW first (n_narrow of them, n_items_narrow
-    // work items), then the others (n_items work items); spec_off: each task's
-    // offset in the spectra array (the tensors' and unfoldings' order)
+    // work items), then those made whole (n_whole, n_items_whole), then the
+    // others (n_items work items); spec_off: each task's offset in the spectra
+    // array (the tensors' and unfoldings' order)
     std::vector<mag::SvdTask> tasks;
     std::vector<int64_t> spec_off;
-    int n_narrow = 0;
-    int64_t gram_len = 0, n_items = 0, n_items_narrow = 0;
+    int n_narrow = 0, n_whole = 0;
+    int64_t gram_len = 0, n_items = 0, n_items_narrow = 0, n_items_whole = 0;
     int large_k = 0;  // largest Gram side above mag::SVD_SMALL_K (0: none)
 };
 
@@ -1906,8 +1913,8 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
     if (n < 0) return fail(MAG_E_SIZE, "n_tensors < 0");
     if (n > 0 && !ts) return fail(MAG_E_NULL, "tensors is NULL");
     pl = InvPlan{};
-    std::vector<mag::SvdTask> wide;
-    std::vector<int64_t> wide_off;
+    std::vector<mag::SvdTask> whole, wide;
+    std::vector<int64_t> whole_off, wide_off;
     int64_t so = 0;
     for (int32_t i = 0; i < n; ++i) {
         int32_t u;
@@ -1925,6 +1932,11 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
                 pl.n_items_narrow += items;
                 pl.tasks.push_back(task);
                 pl.spec_off.push_back(so);
+            } else if (gram_whole(task.K)) {
+                task.item0 = pl.n_items_whole;
+                pl.n_items_whole += items;
+                whole.push_back(task);
+                whole_off.push_back(so);
             } else {
                 task.item0 = pl.n_items;
                 pl.n_items += items;
@@ -1935,6 +1947,9 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
         }
     }
     pl.n_narrow = (int)pl.tasks.size();
+    pl.n_whole = (int)whole.size();
+    pl.tasks.insert(pl.tasks.end(), whole.begin(), whole.end());
+    pl.spec_off.insert(pl.spec_off.end(), whole_off.begin(), whole_off.end());
     pl.tasks.insert(pl.tasks.end(), wide.begin(), wide.end());
     pl.spec_off.insert(pl.spec_off.end(), wide_off.begin(), wide_off.end());
     return MAG_OK;
@@ -2032,7 +2047,8 @@ int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra
                             hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(e, "task copy");
     if ((e = mag::launch_svd(dtasks, (int)pl.tasks.size(), pl.n_narrow, pl.n_items_narrow,
-                             pl.n_items, gram, pl.gram_len, stream)) != hipSuccess)
+                             pl.n_whole, pl.n_items_whole, pl.n_items, gram, pl.gram_len,
+                             stream)) != hipSuccess)
         return hip_fail(e, "invariant kernels");
     for (const auto& t : pl.tasks)
         if (t.K > mag::SVD_SMALL_K &&

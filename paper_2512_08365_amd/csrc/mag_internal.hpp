@@ -271,6 +271,8 @@ constexpr int SVD_MAX_UNF = 15;       // unfoldings of a rank-5 tensor, compleme
 constexpr int64_t GRAM_CHUNK = 2048;  // unfolding columns per Gram work item
 constexpr int64_t GRAM_CHUNK_NARROW = 1024;  // the same for K <= GRAM_NARROW (one 32-side block)
 constexpr int GRAM_NARROW = 32;       // Gram sides up to this use 32-side blocks (else 64)
+constexpr int GRAM_WHOLE = 128;       // sides in (64, GRAM_WHOLE]: the whole triangle per item
+constexpr int64_t GRAM_CHUNK_WHOLE = 1024;  // unfolding columns per item for those sides
 
 struct SvdTask {
     const float* data;
@@ -281,8 +283,8 @@ struct SvdTask {
     double* gram;    // [K][K]
     double* out;     // [K] singular values, descending
     int64_t item0;   // first Gram work item of this task (within its block size's launch)
-    int32_t nt;      // row blocks: ceil(K / 32) when K <= GRAM_NARROW, else ceil(K / 64)
-    int32_t nchunk;  // column chunks: ceil(L / GRAM_CHUNK), GRAM_CHUNK_NARROW when K <= GRAM_NARROW
+    int32_t nt;      // row blocks: 1 when K <= GRAM_NARROW or 64 < K <= GRAM_WHOLE, else ceil(K / 64)
+    int32_t nchunk;  // column chunks of L: GRAM_CHUNK_NARROW, GRAM_CHUNK_WHOLE or GRAM_CHUNK columns
 };
 
 // a tensor's invariant list inside a spectra array
@@ -295,9 +297,11 @@ struct SpecDesc {
 
 // Gram matrices (zeroed, then accumulated), then the spectra of the tasks
 // with K <= SVD_SMALL_K; the first n_narrow tasks (K <= GRAM_NARROW) are
-// numbered by their own n_items_narrow work items, the others by n_items
+// numbered by their own n_items_narrow work items, the next n_whole (64 < K <=
+// GRAM_WHOLE) by n_items_whole, the others by n_items
 hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n_items_narrow,
-                      int64_t n_items, double* gram, int64_t gram_len, hipStream_t stream);
+                      int n_whole, int64_t n_items_whole, int64_t n_items, double* gram,
+                      int64_t gram_len, hipStream_t stream);
 // the spectrum of one n x n Gram matrix with n > SVD_SMALL_K (overwritten):
 // a Householder step is four launches over the whole device, then
 // multisection on Sturm counts; scratch of svd_large_scratch(n) doubles

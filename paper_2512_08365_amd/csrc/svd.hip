@@ -12,7 +12,8 @@
 //   of columns at a time and its 16 tiles are sums of fp64 16x16x4 MFMA
 //   products (fp32 data widened exactly), added into the Gram matrix (and its
 //   mirror) with fp64 atomics.  The elements of X are gathered through the
-//   unfolding's mixed-radix offsets.
+//   unfolding's mixed-radix offsets.  Sides up to 32: one 32-side block;
+//   sides in (64, 128]: k_gram_whole, the whole triangle per workgroup.
 // k_svd_eig: one workgroup per task: Householder reduction of the Gram
 //   matrix (in LDS up to side 128, else in place in global memory) to
 //   tridiagonal form, then every eigenvalue by multisection on Sturm counts
@@ -193,6 +194,182 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
         if (row < t.K && col < t.K && (bi != bj || row <= col)) {
             atomicAdd(&t.gram[row * t.K + col], acc[j]);
             if (row != col) atomicAdd(&t.gram[col * t.K + row], acc[j]);
+        }
+    }
+}
+
+// Gram sides in (64, GRAM_WHOLE]: one workgroup per (task, chunk of
+// GRAM_CHUNK_WHOLE columns) makes every tile of the upper triangle.  Each
+// step of WSTEP columns stages the chunk's K rows once (the blocked kernel stages every row
+// block once per block pair: three times for K = 128), and WHOLE_WAVES waves
+// take WHOLE_TILES tiles each: tiles w, w + WHOLE_WAVES, ... of the upper
+// triangle in row order, so that with K = 128 (36 tiles) every SIMD holds nine
+// (waves are dealt to the SIMDs in turn) and every MFMA issued is a tile of
+// the result; each wave's tiles are independent accumulations, interleaved.
+constexpr int WHOLE_WAVES = 12;
+constexpr int WHOLE_TILES = 3;
+constexpr int WSTEP = 48;  // columns staged per step
+constexpr int WHOLE_THREADS = WHOLE_WAVES * GW;
+constexpr int WHOLE_GPER = GRAM_WHOLE * WSTEP / WHOLE_THREADS;  // staged elements per thread
+static_assert(WHOLE_WAVES * WHOLE_TILES >= (GRAM_WHOLE / 16) * (GRAM_WHOLE / 16 + 1) / 2,
+              "every upper-triangle tile has a wave");
+static_assert(WHOLE_THREADS % WSTEP == 0 && WHOLE_THREADS % GRAM_WHOLE == 0 &&
+              GRAM_WHOLE * WSTEP % WHOLE_THREADS == 0, "staging layout");
+
+// the products of one staged step for a wave's WHOLE_TILES tiles: every
+// k-step's operands are read from LDS before the previous k-step's MFMAs
+// issue, so the reads' latency overlaps the products; the full unroll makes
+// every LDS address a fixed offset from one register per operand
+__device__ __forceinline__ void whole_products(const double (*xs)[GRAM_WHOLE + 1],
+                                               const int* ti, const int* tj, int r, int kq,
+                                               d4* acc)
+{
+    constexpr int NT = WHOLE_TILES;
+    const double* pa[NT];
+    const double* pb[NT];
+#pragma unroll
+    for (int k = 0; k < NT; ++k) {
+        pa[k] = &xs[kq][ti[k] * 16 + r];
+        pb[k] = &xs[kq][tj[k] * 16 + r];
+    }
+    double a[2][NT], b[2][NT];
+#pragma unroll
+    for (int k = 0; k < NT; ++k) {
+        a[0][k] = pa[k][0];
+        b[0][k] = pb[k][0];
+    }
+#pragma unroll
+    for (int s = 0; s < WSTEP / 4; ++s) {
+        const int cur = s & 1, nxt = cur ^ 1;
+        if (s + 1 < WSTEP / 4) {
+#pragma unroll
+            for (int k = 0; k < NT; ++k) {
+                a[nxt][k] = pa[k][(s + 1) * 4 * (GRAM_WHOLE + 1)];
+                b[nxt][k] = pb[k][(s + 1) * 4 * (GRAM_WHOLE + 1)];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < NT; ++k)
+            acc[k] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[cur][k], b[cur][k], acc[k], 0, 0, 0);
+    }
+}
+
+// the staging and products of k_gram_whole for one gather direction: with
+// COLS_FAST, 64 neighbouring threads take neighbouring columns of one row (the
+// rows are not the unit-stride side), else neighbouring rows of one column.
+// Thread tid stages elements u = 0..WHOLE_GPER-1 at row rr0 + u * RSTEP, column
+// c0 + u * CSTEP of each step, compile-time strides, so every per-element LDS
+// address is a fixed offset from one register.
+template <bool COLS_FAST>
+__device__ __forceinline__ void gram_whole_run(const SvdTask& t, int64_t b0, int64_t b1,
+                                               double (*xs)[GRAM_WHOLE + 1],
+                                               const int32_t* loff, const int32_t* roff,
+                                               const int* ti, const int* tj, d4* acc)
+{
+    constexpr int KB = GRAM_WHOLE;
+    constexpr int THREADS = WHOLE_THREADS;
+    constexpr int GPER = WHOLE_GPER;
+    constexpr int RSTEP = COLS_FAST ? THREADS / WSTEP : 0;
+    constexpr int CSTEP = COLS_FAST ? 0 : THREADS / KB;
+    const int tid = threadIdx.x, lane = tid % GW;
+    const int rr0 = COLS_FAST ? tid / WSTEP : tid % KB;
+    const int c0 = COLS_FAST ? tid % WSTEP : tid / KB;
+    typedef const __attribute__((address_space(1))) float* gfloat;
+    const gfloat data = (gfloat)t.data;
+    float stage[GPER];
+    auto fetch = [&](int64_t s0) {
+        const int cols = (int)min((int64_t)WSTEP, b1 - s0);
+        const int32_t* lo = loff + (s0 - b0);  // the step's columns (chunk-local)
+#pragma unroll
+        for (int u = 0; u < GPER; ++u) {
+            const int c = c0 + u * CSTEP;
+            const int ro = roff[rr0 + u * RSTEP];
+            const int lc = lo[c];  // in the chunk's table even past its last column
+            const bool ok = c < cols && ro >= 0;
+            const float v = data[ok ? ro + lc : 0];  // element 0: a valid read
+            stage[u] = ok ? v : 0.0f;
+        }
+    };
+    const int r = lane & 15, kq = lane >> 4;
+    fetch(b0);
+    for (int64_t s0 = b0; s0 < b1; s0 += WSTEP) {
+#pragma unroll
+        for (int u = 0; u < GPER; ++u)
+            xs[c0 + u * CSTEP][rr0 + u * RSTEP] = (double)stage[u];  // fp32 widened exactly
+        __syncthreads();
+        if (s0 + WSTEP < b1) fetch(s0 + WSTEP);  // in flight during the products
+        whole_products(xs, ti, tj, r, kq, acc);
+        __syncthreads();  // before the next step overwrites the staged rows
+    }
+}
+
+// (two workgroups per CU: registers for 2 WHOLE_WAVES / 4 waves per SIMD)
+__global__ __launch_bounds__(WHOLE_THREADS) __attribute__((amdgpu_waves_per_eu(WHOLE_WAVES / 2)))
+void k_gram_whole(const SvdTask* tasks, int n_tasks, int64_t n_items)
+{
+    constexpr int KB = GRAM_WHOLE;
+    constexpr int THREADS = WHOLE_THREADS;
+    __shared__ double xs[WSTEP][KB + 1];  // [column][row], padded
+    // column offsets of the chunk (one step's worth of slack: a step's reads
+    // stay inside even past the chunk's last column) and row offsets; element
+    // offsets, a tensor has fewer than 2^31
+    __shared__ int32_t loff[GRAM_CHUNK_WHOLE + WSTEP];
+    __shared__ int32_t roff[KB];
+    const int64_t item = blockIdx.x;
+    if (item >= n_items) return;  // uniform
+    int lo = 0, hi = n_tasks - 1;  // the last task whose first item is <= item
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tasks[mid].item0 <= item) lo = mid; else hi = mid - 1;
+    }
+    const SvdTask& t = tasks[lo];
+    const int64_t chunk = item - t.item0;  // one item per chunk
+    const int tid = threadIdx.x, lane = tid % GW;
+    const int wv = __builtin_amdgcn_readfirstlane(tid / GW);  // uniform: scalar tile indices
+    const int64_t b0 = chunk * GRAM_CHUNK_WHOLE, b1 = min(b0 + GRAM_CHUNK_WHOLE, t.L);
+    for (int64_t q = tid; q < GRAM_CHUNK_WHOLE + WSTEP; q += THREADS)
+        loff[q] = (q < b1 - b0) ? (int32_t)mode_offset((uint32_t)(b0 + q), t.nl, t.ldim, t.lstr)
+                                : 0;
+    if (tid < KB)
+        roff[tid] = (tid < t.K) ? (int32_t)mode_offset((uint32_t)tid, t.nk, t.kdim, t.kstr) : -1;
+    __syncthreads();
+    // this wave's tiles (uniform): (ti, tj), ti <= tj < ceil(K / 16); a slot
+    // past the triangle's last tile (K < GRAM_WHOLE) makes tile (0, 0) again
+    // and adds nothing
+    const int n16 = (int)((t.K + 15) / 16);
+    const int n_up = n16 * (n16 + 1) / 2;
+    int ti[WHOLE_TILES], tj[WHOLE_TILES];
+#pragma unroll
+    for (int k = 0; k < WHOLE_TILES; ++k) {
+        int idx = wv + k * WHOLE_WAVES, row = 0;
+        if (idx >= n_up) idx = 0;
+        while (idx >= n16 - row) {
+            idx -= n16 - row;
+            ++row;
+        }
+        ti[k] = row;
+        tj[k] = row + idx;
+    }
+    d4 acc[WHOLE_TILES];
+#pragma unroll
+    for (int k = 0; k < WHOLE_TILES; ++k) acc[k] = d4{0.0, 0.0, 0.0, 0.0};
+    if (t.kstr[t.nk - 1] != 1)  // uniform: the rows are not the unit-stride side
+        gram_whole_run<true>(t, b0, b1, xs, loff, roff, ti, tj, acc);
+    else
+        gram_whole_run<false>(t, b0, b1, xs, loff, roff, ti, tj, acc);
+    // register j of a lane holds row 4 j + lane/16, column lane%16 of a tile
+    const int r = lane & 15, kq = lane >> 4;
+#pragma unroll
+    for (int k = 0; k < WHOLE_TILES; ++k) {
+        if (wv + k * WHOLE_WAVES >= n_up) break;  // uniform
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t row = (int64_t)ti[k] * 16 + 4 * j + kq;
+            const int64_t col = (int64_t)tj[k] * 16 + r;
+            if (row < t.K && col < t.K && row <= col) {
+                atomicAdd(&t.gram[row * t.K + col], acc[k][j]);
+                if (row != col) atomicAdd(&t.gram[col * t.K + row], acc[k][j]);
+            }
         }
     }
 }
@@ -710,20 +887,27 @@ __global__ __launch_bounds__(64) void k_svd_match(const SpecDesc* da, int na, co
 }  // namespace
 
 hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n_items_narrow,
-                      int64_t n_items, double* gram, int64_t gram_len, hipStream_t stream)
+                      int n_whole, int64_t n_items_whole, int64_t n_items, double* gram,
+                      int64_t gram_len, hipStream_t stream)
 {
     if (n_tasks <= 0) return hipSuccess;
     const int64_t cb = min((gram_len + 255) / 256, (int64_t)4096);
     hipLaunchKernelGGL(k_svd_clear, dim3((unsigned)max(cb, (int64_t)1)), dim3(256), 0, stream,
                        gram, gram_len);
-    // tasks [0, n_narrow): K <= GRAM_NARROW, 32-side blocks; the rest 64-side
+    // tasks [0, n_narrow): K <= GRAM_NARROW, one 32-side block; then n_whole
+    // with K in (64, GRAM_WHOLE], the whole upper triangle per workgroup; the
+    // rest in 64-side blocks
     if (n_items_narrow > 0)
         hipLaunchKernelGGL(k_gram<GRAM_NARROW>, dim3((unsigned)n_items_narrow),
                            dim3(GRAM_NARROW * GRAM_NARROW / 4), 0, stream, tasks, n_narrow,
                            n_items_narrow);
-    if (n_items > 0 && n_tasks > n_narrow)
+    if (n_items_whole > 0 && n_whole > 0)
+        hipLaunchKernelGGL(k_gram_whole, dim3((unsigned)n_items_whole), dim3(WHOLE_THREADS),
+                           0, stream, tasks + n_narrow, n_whole, n_items_whole);
+    const int n_blocked = n_tasks - n_narrow - n_whole;
+    if (n_items > 0 && n_blocked > 0)
         hipLaunchKernelGGL(k_gram<64>, dim3((unsigned)n_items), dim3(64 * 64 / 4), 0, stream,
-                           tasks + n_narrow, n_tasks - n_narrow, n_items);
+                           tasks + n_narrow + n_whole, n_blocked, n_items);
     hipLaunchKernelGGL(k_svd_eig, dim3((unsigned)n_tasks), dim3(EIG_THREADS), 0, stream, tasks);
     return hipGetLastError();
 }

@@ -58,6 +58,10 @@ def _assert_spectra(got, want, label):
 SHAPES = [(5,), (1, 1), (3, 7), (16, 16), (17, 33), (2, 3, 4), (4, 1, 9), (8, 64, 128),
           (3, 5, 2, 7), (2, 3, 2, 3, 2), (1, 4, 1, 5, 1), (100, 600), (511, 40), (512, 512),
           (2, 256, 4096), (20, 25, 700),
+          # Gram sides in (64, 128], each made by one workgroup per column
+          # chunk: just above 64, ragged column chunks and steps, rows from two
+          # modes, both gather directions of the attention-shaped tensors
+          (65, 3000), (3, 40, 1100), (128, 2049), (32, 128, 128),
           # Gram sides above 512: the many-workgroup reduction (one or two large
           # unfoldings beside a small one, a side not a multiple of the blocks)
           (600, 700), (2, 600, 700), (1030, 1100)]
