@@ -1905,6 +1905,9 @@ struct InvPlan {
     std::vector<int64_t> spec_off;
     int n_narrow = 0, n_whole = 0;
     int64_t gram_len = 0, n_items = 0, n_items_narrow = 0, n_items_whole = 0;
+    // eigenvalue work items (tasks with K <= mag::SVD_SMALL_K, in task order)
+    // and the doubles of their tridiagonal forms (2 K + 3 each)
+    int64_t n_eig_items = 0, tri_len = 0;
     int large_k = 0;  // largest Gram side above mag::SVD_SMALL_K (0: none)
 };
 
@@ -1952,16 +1955,24 @@ int plan_invariants(const mag_tensor* ts, int32_t n, InvPlan& pl)
     pl.spec_off.insert(pl.spec_off.end(), whole_off.begin(), whole_off.end());
     pl.tasks.insert(pl.tasks.end(), wide.begin(), wide.end());
     pl.spec_off.insert(pl.spec_off.end(), wide_off.begin(), wide_off.end());
+    for (auto& t : pl.tasks) {
+        t.eig0 = pl.n_eig_items;
+        if (t.K <= mag::SVD_SMALL_K) {
+            pl.n_eig_items += (t.K + mag::EIG_PER_ITEM - 1) / mag::EIG_PER_ITEM;
+            pl.tri_len += 2 * t.K + 3;
+        }
+    }
     return MAG_OK;
 }
 
 size_t carve_invariants(const InvPlan& pl, void* ws, mag::SvdTask** tasks, double** gram,
-                        double** large)
+                        double** tri, double** large)
 {
     Carver c;
     c.base = static_cast<char*>(ws);
     *tasks = c.take<mag::SvdTask>(std::max<size_t>(pl.tasks.size(), 1));
     *gram = c.take<double>((size_t)std::max<int64_t>(pl.gram_len, 1));
+    *tri = c.take<double>((size_t)std::max<int64_t>(pl.tri_len, 1));
     // scratch of the many-workgroup reduction, shared by the large unfoldings
     // (they run one after another)
     *large = pl.large_k ? c.take<double>((size_t)mag::svd_large_scratch(pl.large_k)) : nullptr;
@@ -2009,8 +2020,8 @@ int mag_invariants_workspace_size(const mag_tensor* tensors, int32_t n_tensors, 
     int rc = plan_invariants(tensors, n_tensors, pl);
     if (rc) return rc;
     mag::SvdTask* t;
-    double *g, *lg;
-    *bytes = carve_invariants(pl, nullptr, &t, &g, &lg);
+    double *g, *tr, *lg;
+    *bytes = carve_invariants(pl, nullptr, &t, &g, &tr, &lg);
     return MAG_OK;
 }
 
@@ -2031,24 +2042,29 @@ int mag_invariants(const mag_tensor* tensors, int32_t n_tensors, double* spectra
     if (!workspace) return fail(MAG_E_NULL, "workspace is NULL");
     if (!aligned(workspace, 256)) return fail(MAG_E_WORKSPACE, "workspace must be 256-byte aligned");
     mag::SvdTask* dtasks;
-    double *gram, *large;
-    const size_t need = carve_invariants(pl, nullptr, &dtasks, &gram, &large);
+    double *gram, *tri, *large;
+    const size_t need = carve_invariants(pl, nullptr, &dtasks, &gram, &tri, &large);
     if (workspace_bytes < need) return fail(MAG_E_WORKSPACE, "workspace too small");
-    carve_invariants(pl, workspace, &dtasks, &gram, &large);
-    int64_t go = 0;
+    carve_invariants(pl, workspace, &dtasks, &gram, &tri, &large);
+    int64_t go = 0, to = 0;
     for (size_t i = 0; i < pl.tasks.size(); ++i) {
         mag::SvdTask& t = pl.tasks[i];
         t.gram = gram + go;
         t.out = spectra + pl.spec_off[i];
         go += t.K * t.K;
+        t.tri = nullptr;
+        if (t.K <= mag::SVD_SMALL_K) {
+            t.tri = tri + to;
+            to += 2 * t.K + 3;
+        }
     }
     hipError_t e;
     if ((e = hipMemcpyAsync(dtasks, pl.tasks.data(), sizeof(mag::SvdTask) * pl.tasks.size(),
                             hipMemcpyHostToDevice, stream)) != hipSuccess)
         return hip_fail(e, "task copy");
     if ((e = mag::launch_svd(dtasks, (int)pl.tasks.size(), pl.n_narrow, pl.n_items_narrow,
-                             pl.n_whole, pl.n_items_whole, pl.n_items, gram, pl.gram_len,
-                             stream)) != hipSuccess)
+                             pl.n_whole, pl.n_items_whole, pl.n_items, pl.n_eig_items, gram,
+                             pl.gram_len, stream)) != hipSuccess)
         return hip_fail(e, "invariant kernels");
     for (const auto& t : pl.tasks)
         if (t.K > mag::SVD_SMALL_K &&

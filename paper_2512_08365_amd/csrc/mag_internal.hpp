@@ -271,6 +271,7 @@ constexpr int SVD_MAX_UNF = 15;       // unfoldings of a rank-5 tensor, compleme
 constexpr int64_t GRAM_CHUNK = 2048;  // unfolding columns per Gram work item
 constexpr int64_t GRAM_CHUNK_NARROW = 1024;  // the same for K <= GRAM_NARROW (one 32-side block)
 constexpr int GRAM_NARROW = 32;       // Gram sides up to this use 32-side blocks (else 64)
+constexpr int EIG_PER_ITEM = 16;      // eigenvalues per work item of the Sturm counts
 constexpr int GRAM_WHOLE = 128;       // sides in (64, GRAM_WHOLE]: the whole triangle per item
 constexpr int64_t GRAM_CHUNK_WHOLE = 1024;  // unfolding columns per item for those sides
 
@@ -283,6 +284,8 @@ struct SvdTask {
     double* gram;    // [K][K]
     double* out;     // [K] singular values, descending
     int64_t item0;   // first Gram work item of this task (within its block size's launch)
+    double* tri;     // (K <= SVD_SMALL_K) the tridiagonal form: d[K], e2[K], glo, ghi, pivmin
+    int64_t eig0;    // (K <= SVD_SMALL_K) first eigenvalue work item, EIG_PER_ITEM values each
     int32_t nt;      // row blocks: 1 when K <= GRAM_NARROW or 64 < K <= GRAM_WHOLE, else ceil(K / 64)
     int32_t nchunk;  // column chunks of L: GRAM_CHUNK_NARROW, GRAM_CHUNK_WHOLE or GRAM_CHUNK columns
 };
@@ -298,10 +301,11 @@ struct SpecDesc {
 // Gram matrices (zeroed, then accumulated), then the spectra of the tasks
 // with K <= SVD_SMALL_K; the first n_narrow tasks (K <= GRAM_NARROW) are
 // numbered by their own n_items_narrow work items, the next n_whole (64 < K <=
-// GRAM_WHOLE) by n_items_whole, the others by n_items
+// GRAM_WHOLE) by n_items_whole, the others by n_items; the eigenvalue counts
+// by n_eig_items (each task's from its eig0, in task order)
 hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n_items_narrow,
-                      int n_whole, int64_t n_items_whole, int64_t n_items, double* gram,
-                      int64_t gram_len, hipStream_t stream);
+                      int n_whole, int64_t n_items_whole, int64_t n_items, int64_t n_eig_items,
+                      double* gram, int64_t gram_len, hipStream_t stream);
 // the spectrum of one n x n Gram matrix with n > SVD_SMALL_K (overwritten):
 // a Householder step is four launches over the whole device, then
 // multisection on Sturm counts; scratch of svd_large_scratch(n) doubles

@@ -16,9 +16,10 @@
 //   sides in (64, 128]: k_gram_whole, the whole triangle per workgroup.
 // k_svd_eig: one workgroup per task: Householder reduction of the Gram
 //   matrix (in LDS up to side 128, else in place in global memory) to
-//   tridiagonal form, then every eigenvalue by multisection on Sturm counts
-//   (the count of eigenvalues below x), sigma = sqrt(max(lambda, 0)), written
-//   in descending order.
+//   tridiagonal form and its Gershgorin bounds; k_svd_count: every
+//   eigenvalue by multisection on Sturm counts (the count of eigenvalues
+//   below x), a wave per 16 eigenvalues, sigma = sqrt(max(lambda, 0)),
+//   written in descending order.
 // k_svd_match: one workgroup per tensor pair: which spectra of the two lists
 //   are close, then a one-to-one pairing by augmenting paths.
 
@@ -31,7 +32,7 @@ namespace mag {
 namespace {
 
 constexpr int GW = 64;
-constexpr int EIG_THREADS = 256;
+constexpr int EIG_THREADS = 512;
 
 typedef double d4 __attribute__((ext_vector_type(4)));
 
@@ -374,12 +375,42 @@ void k_gram_whole(const SvdTask* tasks, int n_tasks, int64_t n_items)
     }
 }
 
+// a double moved between lanes by DPP (bound_ctrl: lanes without a source read 0)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ double dpp_move(double v)
+{
+    const uint64_t b = (uint64_t)__double_as_longlong(v);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)b, CTRL, ROWS, 0xf, true);
+    const uint32_t hi =
+        (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(b >> 32), CTRL, ROWS, 0xf, true);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
+// sum of v over the wave's 64 lanes, the same value in every lane: an
+// inclusive scan by DPP row shifts (1, 2, 4, 8) and row broadcasts (lane 15
+// into the next row, lane 31 into the upper half), then lane 63's total.
+// Register-to-register moves, where a butterfly of lane shuffles would make
+// six LDS round trips
+__device__ __forceinline__ double wave_total(double x)
+{
+    x += dpp_move<0x111, 0xf>(x);  // row_shr:1
+    x += dpp_move<0x112, 0xf>(x);  // row_shr:2
+    x += dpp_move<0x114, 0xf>(x);  // row_shr:4
+    x += dpp_move<0x118, 0xf>(x);  // row_shr:8
+    x += dpp_move<0x142, 0xa>(x);  // row_bcast:15 into rows 1 and 3
+    x += dpp_move<0x143, 0xc>(x);  // row_bcast:31 into rows 2 and 3
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)b, 63);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(b >> 32), 63);
+    return __longlong_as_double((long long)(((uint64_t)hi << 32) | lo));
+}
+
 // sum of v over the workgroup with one barrier: red holds two rows of
 // per-wave partials used alternately (flip selects the row, toggled here), so
 // a wave that is still reading one row cannot see the next call's writes
 __device__ double block_sum(double v, double (*red)[EIG_THREADS / 64], int& flip)
 {
-    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    v = wave_total(v);
     if ((threadIdx.x & 63) == 0) red[flip][threadIdx.x >> 6] = v;
     __syncthreads();
     double s = 0.0;
@@ -388,15 +419,16 @@ __device__ double block_sum(double v, double (*red)[EIG_THREADS / 64], int& flip
     return s;
 }
 
-// 1/q within about an ulp: the hardware estimate refined by two Newton steps
-// (the Sturm recurrence is a chain of these; a correctly rounded division
-// would lengthen every link)
+// 1/q to a relative error of about 2^-48: the hardware estimate (measured on
+// gfx950 to 2^-24.4 over 4M values spanning 2^+-300) refined by one Newton
+// step, which squares its error.  The Sturm recurrence is a chain of these; a
+// correctly rounded division would lengthen every link, and a count computed
+// with this reciprocal is exact for the tridiagonal matrix with each e2[i]
+// perturbed by about 2^-48 relative, far below the bisection's own tolerance
 __device__ __forceinline__ double recip_nr(double q)
 {
-    double r = __builtin_amdgcn_rcp(q);
-    r = fma(r, fma(-q, r, 1.0), r);
-    r = fma(r, fma(-q, r, 1.0), r);
-    return r;
+    const double r = __builtin_amdgcn_rcp(q);
+    return fma(r, fma(-q, r, 1.0), r);
 }
 
 constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in LDS
@@ -534,31 +566,38 @@ __device__ void gershgorin(Ptr d, Ptr e2, int n, double& glo, double& ghi, doubl
 
 // the k-th smallest eigenvalue of (d, e2) by multisection on Sturm counts
 // (count(lo) <= k < count(hi)): the G neighbouring threads of eigenvalue k
-// (g = 0 .. G-1, G a power of two dividing 64) each count at four of a
-// round's 4 G interior points, four independent chains side by side, and the
-// round keeps the one of the interval's 4 G + 1 parts that holds the
+// (g = 0 .. G-1, G a power of two dividing 64) each count at NC of a
+// round's NC G interior points, NC independent chains side by side, and the
+// round keeps the one of the interval's NC G + 1 parts that holds the
 // eigenvalue (the group agrees on lo and hi after every round)
-template <class Ptr>
+template <int NC, class Ptr>
 __device__ double multisect(Ptr d, Ptr e2, int n, int k, int g, int G, double glo, double ghi,
                             double pivmin)
 {
     double lo = glo, hi = ghi;
     for (int it = 0; it < 64; ++it) {
         if (!(hi - lo > 2.0 * DBL_EPSILON * fmax(fabs(lo), fabs(hi)) + pivmin)) break;
-        const double h = (hi - lo) / (double)(4 * G + 1);
-        double x[4], q[4];
-        int c[4];
+        const double h = (hi - lo) / (double)(NC * G + 1);
+        double x[NC], q[NC];
+        int c[NC];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-            x[u] = lo + h * (double)(4 * g + u + 1);
+        for (int u = 0; u < NC; ++u) {
+            x[u] = lo + h * (double)(NC * g + u + 1);
             q[u] = d[0] - x[u];
             if (fabs(q[u]) < pivmin) q[u] = -pivmin;
             c[u] = q[u] < 0.0;
         }
+        // the next step's coefficients are read a step ahead, so the LDS
+        // latency overlaps the current step's arithmetic
+        double dn = n > 1 ? d[1] : 0.0, en = n > 1 ? e2[0] : 0.0;
         for (int i = 1; i < n; ++i) {
-            const double di = d[i], ei = e2[i - 1];
+            const double di = dn, ei = en;
+            if (i + 1 < n) {
+                dn = d[i + 1];
+                en = e2[i];
+            }
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {
+            for (int u = 0; u < NC; ++u) {
                 q[u] = di - x[u] - ei * recip_nr(q[u]);
                 if (fabs(q[u]) < pivmin) q[u] = -pivmin;
                 c[u] += q[u] < 0.0;
@@ -566,7 +605,7 @@ __device__ double multisect(Ptr d, Ptr e2, int n, int k, int g, int G, double gl
         }
         double nlo = lo, nhi = hi;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
+        for (int u = 0; u < NC; ++u) {
             if (c[u] <= k) nlo = fmax(nlo, x[u]);
             else nhi = fmin(nhi, x[u]);
         }
@@ -602,20 +641,59 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
         typedef __attribute__((address_space(1))) double gdouble;
         tridiagonalize((gdouble*)t.gram, n, v, w, wp, d, e2, red);
     }
-    double glo, ghi, pivmin;
-    const lds_f64* dl = (const lds_f64*)d;  // ds_ instructions in the counts
-    const lds_f64* el = (const lds_f64*)e2;
-    gershgorin(dl, el, n, glo, ghi, pivmin);
-    // the counts are bound by instruction issue (a reciprocal per step of
-    // each chain), so G grows only until about one wave per SIMD is busy:
-    // more threads per eigenvalue take fewer rounds but more work in all
-    int G = 1;
-    while (G < 8 && 2 * G * n <= 256) G *= 2;
-    const int g = tid % G;
-    for (int k = tid / G; k < n; k += EIG_THREADS / G) {
-        const double lam = multisect(dl, el, n, k, g, G, glo, ghi, pivmin);
-        if (g == 0) t.out[n - 1 - k] = sqrt(fmax(lam, 0.0));
+    // the tridiagonal form and its bounds for k_svd_count
+    for (int i = tid; i < n; i += EIG_THREADS) {
+        t.tri[i] = d[i];
+        t.tri[n + i] = e2[i];
     }
+    if (tid == 0) {
+        double glo, ghi, pivmin;
+        gershgorin((const lds_f64*)d, (const lds_f64*)e2, n, glo, ghi, pivmin);
+        t.tri[2 * n] = glo;
+        t.tri[2 * n + 1] = ghi;
+        t.tri[2 * n + 2] = pivmin;
+    }
+}
+
+// every eigenvalue of the tridiagonal forms k_svd_eig wrote: one wave per
+// EIG_PER_ITEM eigenvalues of a task (work items numbered from the task's
+// eig0), COUNT_G threads per eigenvalue with COUNT_C chains each.  A count
+// is a chain of dependent steps, each bound by its reciprocal's latency more
+// than by issue, so two chains per thread and four threads per eigenvalue
+// (eight points a round, as four chains on two threads) spread the work of
+// a 128-side matrix over eight waves: about one wave per SIMD over the whole
+// device for 64 attention-shaped tensors, where one workgroup per matrix kept
+// half the CUs idle
+constexpr int COUNT_G = 4;
+constexpr int COUNT_C = 2;
+static_assert(EIG_PER_ITEM * COUNT_G == GW, "one wave per work item");
+
+__global__ __launch_bounds__(GW) void k_svd_count(const SvdTask* tasks, int n_tasks,
+                                                 int64_t n_items)
+{
+    __shared__ double ds[SVD_SMALL_K], es[SVD_SMALL_K];
+    const int64_t item = blockIdx.x;
+    if (item >= n_items) return;  // uniform
+    int lo = 0, hi = n_tasks - 1;  // the last task whose first item is <= item
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (tasks[mid].eig0 <= item) lo = mid; else hi = mid - 1;
+    }
+    const SvdTask& t = tasks[lo];
+    const int n = (int)t.K;
+    const int tid = threadIdx.x;
+    for (int i = tid; i < n; i += GW) {
+        ds[i] = t.tri[i];
+        es[i] = t.tri[n + i];
+    }
+    const double glo = t.tri[2 * n], ghi = t.tri[2 * n + 1], pivmin = t.tri[2 * n + 2];
+    __syncthreads();
+    // (whole groups of COUNT_G lanes share k and leave together)
+    const int k = (int)(item - t.eig0) * EIG_PER_ITEM + tid / COUNT_G, g = tid % COUNT_G;
+    if (k >= n) return;
+    const double lam = multisect<COUNT_C>((const lds_f64*)ds, (const lds_f64*)es, n, k, g,
+                                          COUNT_G, glo, ghi, pivmin);
+    if (g == 0) t.out[n - 1 - k] = sqrt(fmax(lam, 0.0));
 }
 
 // ---------------------------------------------------------------------------
@@ -812,7 +890,7 @@ __global__ __launch_bounds__(256) void k_hh_bisect(const double* d, const double
     const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int k = (int)(t / G), g = (int)(t % G);
     if (k >= n) return;
-    const double lam = multisect(d, e2, n, k, g, G, hs->glo, hs->ghi, hs->pivmin);
+    const double lam = multisect<4>(d, e2, n, k, g, G, hs->glo, hs->ghi, hs->pivmin);
     if (g == 0) out[n - 1 - k] = sqrt(fmax(lam, 0.0));
 }
 
@@ -887,8 +965,8 @@ __global__ __launch_bounds__(64) void k_svd_match(const SpecDesc* da, int na, co
 }  // namespace
 
 hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n_items_narrow,
-                      int n_whole, int64_t n_items_whole, int64_t n_items, double* gram,
-                      int64_t gram_len, hipStream_t stream)
+                      int n_whole, int64_t n_items_whole, int64_t n_items, int64_t n_eig_items,
+                      double* gram, int64_t gram_len, hipStream_t stream)
 {
     if (n_tasks <= 0) return hipSuccess;
     const int64_t cb = min((gram_len + 255) / 256, (int64_t)4096);
@@ -909,6 +987,9 @@ hipError_t launch_svd(const SvdTask* tasks, int n_tasks, int n_narrow, int64_t n
         hipLaunchKernelGGL(k_gram<64>, dim3((unsigned)n_items), dim3(64 * 64 / 4), 0, stream,
                            tasks + n_narrow + n_whole, n_blocked, n_items);
     hipLaunchKernelGGL(k_svd_eig, dim3((unsigned)n_tasks), dim3(EIG_THREADS), 0, stream, tasks);
+    if (n_eig_items > 0)
+        hipLaunchKernelGGL(k_svd_count, dim3((unsigned)n_eig_items), dim3(GW), 0, stream, tasks,
+                           n_tasks, n_eig_items);
     return hipGetLastError();
 }
 
