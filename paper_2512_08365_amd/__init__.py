@@ -9,6 +9,7 @@ raise.
 from __future__ import annotations
 
 import ctypes
+import functools
 
 import torch
 
@@ -540,28 +541,33 @@ def detect(a: dict, b: dict, threshold: float = 0.10, tolerance: float = 0.01,
 def _tensor_descs(tensors):
     arr = (N.Tensor * max(1, len(tensors)))()
     for i, x in enumerate(tensors):
-        if x.dim() < 1 or x.dim() > N.MAG_SVD_MAX_RANK:
-            raise MagnetonError(N.MAG_E_SIZE, f"tensor {i}: rank {x.dim()} out of range")
+        shape = tuple(x.shape)
+        if len(shape) < 1 or len(shape) > N.MAG_SVD_MAX_RANK:
+            raise MagnetonError(N.MAG_E_SIZE, f"tensor {i}: rank {len(shape)} out of range")
         arr[i].data = _dev_ptr(x, torch.float32, f"tensor {i}")
-        arr[i].rank = x.dim()
-        for d, n in enumerate(x.shape):
-            arr[i].dims[d] = int(n)
+        arr[i].rank = len(shape)
+        arr[i].dims[:len(shape)] = shape
     return arr
 
 
-def invariant_layout(tensor) -> list:
-    """Lengths of a tensor's spectra, in the order invariants() writes them."""
-    r = tensor.dim()
+@functools.lru_cache(maxsize=4096)
+def _layout_of_shape(shape: tuple) -> tuple:
+    r = len(shape)
     out = []
     for g in range(1, (1 << r) - 1, 2):
         M = N_ = 1
-        for i, n in enumerate(tensor.shape):
+        for i, n in enumerate(shape):
             if g >> i & 1:
                 M *= int(n)
             else:
                 N_ *= int(n)
         out.append(min(M, N_))
-    return out
+    return tuple(out)
+
+
+def invariant_layout(tensor) -> list:
+    """Lengths of a tensor's spectra, in the order invariants() writes them."""
+    return list(_layout_of_shape(tuple(tensor.shape)))
 
 
 def invariants(tensors, workspace=None):
@@ -574,11 +580,9 @@ def invariants(tensors, workspace=None):
     descs = _tensor_descs(tensors)
     n = len(tensors)
     dev = tensors[0].device if n else torch.device("cuda")
-    total = 0
-    for i in range(n):
-        u, v = ctypes.c_int32(0), ctypes.c_int64(0)
-        _check(lib.mag_invariant_count(ctypes.byref(descs[i]), ctypes.byref(u), ctypes.byref(v)))
-        total += int(v.value)
+    # (the library checks every tensor again while planning the workspace)
+    layouts = [_layout_of_shape(tuple(x.shape)) for x in tensors]
+    total = sum(sum(lay) for lay in layouts)
     b = ctypes.c_size_t(0)
     _check(lib.mag_invariants_workspace_size(descs, n, ctypes.byref(b)))
     if workspace is None or workspace.numel() < int(b.value):
@@ -586,7 +590,7 @@ def invariants(tensors, workspace=None):
     spectra = torch.empty(max(total, 1), dtype=torch.float64, device=dev)
     _check(lib.mag_invariants(descs, n, spectra.data_ptr(), workspace.data_ptr(), workspace.numel(),
                               _stream_handle(dev)))
-    return spectra[:total], [invariant_layout(x) for x in tensors]
+    return spectra[:total], [list(lay) for lay in layouts]
 
 
 def match(tensors_a, spectra_a, tensors_b, spectra_b, eps: float = 1e-5):

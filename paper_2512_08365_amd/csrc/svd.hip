@@ -438,7 +438,7 @@ constexpr int EIG_LDS_K = 128;  // Gram matrices up to this side are reduced in 
 typedef __attribute__((address_space(3))) double lds_f64;
 
 template <class Ptr>
-__device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* wp, double* d,
+__device__ void tridiagonalize(Ptr A, int n, double* v, double2* uw, double* wp, double* d,
                                double* e2, double (*red)[EIG_THREADS / 64])
 {
     const int tid = threadIdx.x;
@@ -499,8 +499,9 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* wp, d
             if (tpc > 1) {
                 wp[hf * ncol + i] = part;
             } else {
-                w[i] = beta * part;
-                pv += beta * part * (i == 0 ? u0 : v[i]);
+                const double ui = i == 0 ? u0 : v[i], wi = beta * part;
+                uw[i] = make_double2(ui, wi);
+                pv += wi * ui;
             }
         }
         if (tpc > 1) {
@@ -508,27 +509,24 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double* w, double* wp, d
             if (hf == 0 && ci < m) {
                 double sum = 0.0;
                 for (int h = 0; h < tpc; ++h) sum += wp[h * ncol + ci];
-                w[ci] = beta * sum;
-                pv = w[ci] * (ci == 0 ? u0 : v[ci]);
+                const double ui = ci == 0 ? u0 : v[ci], wi = beta * sum;
+                uw[ci] = make_double2(ui, wi);
+                pv = wi * ui;
             }
         }
-        const double K2 = 0.5 * beta * block_sum(pv, red, flip);  // (publishes p in w)
-        // A_sub -= u w^T + w u^T with w_j = p_j - K2 u_j formed as it is used
-        // (each thread walks its column slice down the rows; the rows of one
-        // column are independent, so the loop is unrolled)
+        const double K2 = 0.5 * beta * block_sum(pv, red, flip);  // (publishes p in w, uw)
+        // A_sub -= u w'^T + w' u^T with w' = p - K2 u: entry (j, i) loses
+        // u_j (w_i - 2 K2 u_i) + w_j u_i, two FMAs on the pair (u_j, w_j) read
+        // from LDS at once (each thread walks its column slice down the rows;
+        // the rows of one column are independent, so the loop is unrolled)
         for (int i = ci; i < m; i += ncol) {
             const auto col = A + (size_t)(k + 1) * n + (k + 1 + i);
-            const double ui = (i == 0) ? u0 : v[i];
-            const double wi = w[i] - K2 * ui;
-            int j = jlo;
-            if (j == 0 && j < jhi) {
-                col[0] -= u0 * wi + (w[0] - K2 * u0) * ui;
-                j = 1;
-            }
+            const double2 pi = uw[i];
+            const double ui = pi.x, ci2 = pi.y - 2.0 * K2 * pi.x;
 #pragma unroll 4
-            for (; j < jhi; ++j) {
-                const double uj = v[j];
-                col[(size_t)j * n] -= uj * wi + (w[j] - K2 * uj) * ui;
+            for (int j = jlo; j < jhi; ++j) {
+                const double2 pj = uw[j];
+                col[(size_t)j * n] -= fma(pj.x, ci2, pj.y * ui);
             }
         }
         __syncthreads();
@@ -622,7 +620,8 @@ __device__ double multisect(Ptr d, Ptr e2, int n, int k, int g, int G, double gl
 
 __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
 {
-    __shared__ double v[SVD_SMALL_K], w[SVD_SMALL_K];
+    __shared__ double v[SVD_SMALL_K];
+    __shared__ double2 uw[SVD_SMALL_K];
     __shared__ double d[SVD_SMALL_K], e2[SVD_SMALL_K];
     __shared__ double red[2][EIG_THREADS / 64];
     __shared__ double As[EIG_LDS_K * EIG_LDS_K];
@@ -634,12 +633,12 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
     if (n <= EIG_LDS_K) {
         for (int q = tid; q < n * n; q += EIG_THREADS) As[q] = t.gram[q];
         __syncthreads();
-        tridiagonalize((lds_f64*)As, n, v, w, wp, d, e2, red);  // ds_ instructions
+        tridiagonalize((lds_f64*)As, n, v, uw, wp, d, e2, red);  // ds_ instructions
     } else {
         // global-memory instructions (generic ones would also count against
         // the LDS waits)
         typedef __attribute__((address_space(1))) double gdouble;
-        tridiagonalize((gdouble*)t.gram, n, v, w, wp, d, e2, red);
+        tridiagonalize((gdouble*)t.gram, n, v, uw, wp, d, e2, red);
     }
     // the tridiagonal form and its bounds for k_svd_count
     for (int i = tid; i < n; i += EIG_THREADS) {
