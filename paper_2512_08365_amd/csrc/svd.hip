@@ -578,28 +578,36 @@ __device__ double multisect(Ptr d, Ptr e2, int n, int k, int g, int G, double gl
         const double h = (hi - lo) / (double)(NC * G + 1);
         double x[NC], q[NC];
         int c[NC];
+        // a pivot below pivmin in magnitude becomes -pivmin, so it is
+        // negative after that exactly when it was below pivmin: the count
+        // takes that test, beside the clamp rather than after it
+        auto step = [&](double di, double ei) {
+#pragma unroll
+            for (int u = 0; u < NC; ++u) {
+                q[u] = di - x[u] - ei * recip_nr(q[u]);
+                c[u] += q[u] < pivmin;
+                if (fabs(q[u]) < pivmin) q[u] = -pivmin;
+            }
+        };
 #pragma unroll
         for (int u = 0; u < NC; ++u) {
             x[u] = lo + h * (double)(NC * g + u + 1);
             q[u] = d[0] - x[u];
+            c[u] = q[u] < pivmin;
             if (fabs(q[u]) < pivmin) q[u] = -pivmin;
-            c[u] = q[u] < 0.0;
         }
         // the next step's coefficients are read a step ahead, so the LDS
-        // latency overlaps the current step's arithmetic
-        double dn = n > 1 ? d[1] : 0.0, en = n > 1 ? e2[0] : 0.0;
-        for (int i = 1; i < n; ++i) {
-            const double di = dn, ei = en;
-            if (i + 1 < n) {
+        // latency overlaps the current step's arithmetic (the last step
+        // peeled: no test inside the loop)
+        if (n > 1) {
+            double dn = d[1], en = e2[0];
+            for (int i = 1; i + 1 < n; ++i) {
+                const double di = dn, ei = en;
                 dn = d[i + 1];
                 en = e2[i];
+                step(di, ei);
             }
-#pragma unroll
-            for (int u = 0; u < NC; ++u) {
-                q[u] = di - x[u] - ei * recip_nr(q[u]);
-                if (fabs(q[u]) < pivmin) q[u] = -pivmin;
-                c[u] += q[u] < 0.0;
-            }
+            step(dn, en);
         }
         double nlo = lo, nhi = hi;
 #pragma unroll
@@ -656,15 +664,17 @@ __global__ __launch_bounds__(EIG_THREADS) void k_svd_eig(const SvdTask* tasks)
 
 // every eigenvalue of the tridiagonal forms k_svd_eig wrote: one wave per
 // EIG_PER_ITEM eigenvalues of a task (work items numbered from the task's
-// eig0), COUNT_G threads per eigenvalue with COUNT_C chains each.  A count
-// is a chain of dependent steps, each bound by its reciprocal's latency more
-// than by issue, so two chains per thread and four threads per eigenvalue
-// (eight points a round, as four chains on two threads) spread the work of
-// a 128-side matrix over eight waves: about one wave per SIMD over the whole
-// device for 64 attention-shaped tensors, where one workgroup per matrix kept
-// half the CUs idle
+// eig0), COUNT_G threads per eigenvalue with COUNT_C chains each.  The
+// counts are bound by instruction issue over the device as a whole (the
+// work is rounds x points per round, and fewer points per round cost fewer
+// instructions than the extra rounds add) and by each chain's latency within
+// a wave; four threads of one chain (four points a round, 22 rounds for 52
+// bits) spread a 128-side matrix over eight waves, about one wave per SIMD
+// over the whole device for 64 attention-shaped tensors.  Measured on those:
+// 0.15 ms; 2, 8 or 16 threads of one chain 0.21, 0.16, 0.22 ms; four threads
+// of two chains 0.19 ms, of four 0.27 ms
 constexpr int COUNT_G = 4;
-constexpr int COUNT_C = 2;
+constexpr int COUNT_C = 1;
 static_assert(EIG_PER_ITEM * COUNT_G == GW, "one wave per work item");
 
 __global__ __launch_bounds__(GW) void k_svd_count(const SvdTask* tasks, int n_tasks,
