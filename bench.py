@@ -72,15 +72,18 @@ COUNTERS_JSON = os.path.join(ROOT, "profiles", "tile_kernel_counters.json")
 COPY_BYTES = 1 << 30  # calibration copy: 1 GiB read + 1 GiB written
 
 
-def counters_traffic():
+def counters_traffic(algorithmic_bytes):
     """HBM bytes per launch of the tile kernel from the committed counter
-    summary, if it was taken on the current kernel source (else None)."""
+    summary, if it was taken on the current kernel source and on a launch of
+    the same algorithmic size, i.e. the same workload (else None)."""
     try:
         with open(COUNTERS_JSON) as f:
             d = json.load(f)
     except (OSError, ValueError):
         return None
     if d.get("source_hash") != source_hash():
+        return None
+    if d.get("algorithmic_bytes_per_launch") != algorithmic_bytes:
         return None
     return d.get("traffic_bytes_per_launch")
 
@@ -604,10 +607,11 @@ def tile_roofline(tile_ms, n, m):
     return {"kernel": "k_tile (interval energies)", "bound": "hbm",
             "achieved": b48 / (avg * 1e-3) / 1e9, "peak": HBM_PEAK_GBS, "unit": "GB/s",
             "frac": b48 / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS,
-            "traffic": counters_traffic(),
+            "traffic": counters_traffic(b48),
             "traffic_source": ("rocprofv3 FETCH_SIZE + WRITE_SIZE of this kernel source, scaled "
                                "by a 1 GiB copy (profiles/tile_kernel_counters.json); null when "
-                               "the source changed since"),
+                               "the source changed since or the counters were taken on another "
+                               "workload"),
             "algorithmic_bytes_per_launch": b48, "avg_launch_ms": avg,
             "achieved_at_40B_per_interval": b40 / (avg * 1e-3) / 1e9,
             "frac_at_40B_per_interval": b40 / (avg * 1e-3) / 1e9 / HBM_PEAK_GBS}

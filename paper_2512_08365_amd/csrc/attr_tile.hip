@@ -1161,14 +1161,18 @@ hipError_t launch_tile_kernel(void (*kern)(TileParams), int& per_cu, TileParams 
         }
         per_cu = nb;
     }
-    // runs of at most RUN_TILES tiles: many more workgroups than fit at once,
-    // so the hardware deals them out as slots free up -- workgroups of other
-    // kernels (another attribution's grouping) interleave with them, and no
-    // slot is left with a long run started late (measured on the A/B step of
-    // the multi-stream 100M-sample workload: 16 tiles per run 0.978 ms per
-    // step, 32 tiles 0.987 ms, 8 tiles no faster than 32)
+    // runs of at most RUN_TILES tiles, and at least two rounds of workgroups:
+    // more workgroups than fit at once, so the hardware deals them out as
+    // slots free up -- workgroups of other kernels (another attribution's
+    // grouping) interleave with them, and no slot is left with a long run
+    // started late (measured on the A/B step of the multi-stream 100M-sample
+    // workload: 16 tiles per run 0.978 ms per step, 32 tiles 0.987 ms, 8 tiles
+    // no faster than 32; on a 20M-sample one-stream trace, where 16 tiles
+    // would leave the chip part empty, two rounds of 5 tiles 0.117 ms per
+    // launch against 0.123 ms for one round of 10 and 0.117 ms for four of 3)
     const int64_t waves = (int64_t)device_cu_count() * per_cu;
-    p.tiles_per_wg = std::min<int64_t>((ntiles + waves - 1) / waves, RUN_TILES);
+    p.tiles_per_wg =
+        std::max<int64_t>(1, std::min<int64_t>((ntiles + 2 * waves - 1) / (2 * waves), RUN_TILES));
     const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
     if (ev_start || ev_stop)
         // timing events travel with the dispatch: no marker packets around it
