@@ -1161,18 +1161,22 @@ hipError_t launch_tile_kernel(void (*kern)(TileParams), int& per_cu, TileParams 
         }
         per_cu = nb;
     }
-    // runs of at most RUN_TILES tiles, and at least two rounds of workgroups:
-    // more workgroups than fit at once, so the hardware deals them out as
-    // slots free up -- workgroups of other kernels (another attribution's
-    // grouping) interleave with them, and no slot is left with a long run
-    // started late (measured on the A/B step of the multi-stream 100M-sample
-    // workload: 16 tiles per run 0.978 ms per step, 32 tiles 0.987 ms, 8 tiles
-    // no faster than 32; on a 20M-sample one-stream trace, where 16 tiles
-    // would leave the chip part empty, two rounds of 5 tiles 0.117 ms per
-    // launch against 0.123 ms for one round of 10 and 0.117 ms for four of 3)
+    // runs of at most RUN_TILES tiles: many more workgroups than fit at once,
+    // so the hardware deals them out as slots free up -- workgroups of other
+    // kernels (another attribution's grouping) interleave with them, and no
+    // slot is left with a long run started late (measured on the A/B step of
+    // the multi-stream 100M-sample workload: 16 tiles per run 0.978 ms per
+    // step, 32 tiles 0.987 ms, 8 tiles no faster than 32).  A launch whose one
+    // round of workgroups would take runs shorter than RUN_TILES is split in
+    // two rounds of half-length runs (a 20M-sample one-stream trace: two
+    // rounds of 5 tiles 0.116 ms per launch, one round of 10 0.123 ms; a
+    // 32M-sample chunk keeps its one round of 16: 6.01-6.03 ms per step of the
+    // long run against 6.04-6.13 ms with two rounds of 8)
     const int64_t waves = (int64_t)device_cu_count() * per_cu;
-    p.tiles_per_wg =
-        std::max<int64_t>(1, std::min<int64_t>((ntiles + 2 * waves - 1) / (2 * waves), RUN_TILES));
+    const int64_t one_round = (ntiles + waves - 1) / waves;
+    p.tiles_per_wg = one_round >= RUN_TILES
+                         ? RUN_TILES
+                         : std::max<int64_t>(1, (ntiles + 2 * waves - 1) / (2 * waves));
     const int64_t runs = (ntiles + p.tiles_per_wg - 1) / p.tiles_per_wg;
     if (ev_start || ev_stop)
         // timing events travel with the dispatch: no marker packets around it
