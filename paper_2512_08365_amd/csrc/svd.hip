@@ -452,8 +452,12 @@ __device__ void tridiagonalize(Ptr A, int n, double* v, double2* uw, double* wp,
     for (int k = 0; k + 2 < n; ++k) {
         const int m = n - k - 1;
         double tail = 0.0;
+        // column k below the diagonal, read as row k right of it (contiguous:
+        // no bank conflicts in LDS, coalesced in global memory); the two agree
+        // up to the rounding of the updates, which keep the matrix symmetric
+        // in exact arithmetic
         for (int i = tid; i < m; i += EIG_THREADS) {
-            const double x = A[(size_t)(k + 1 + i) * n + k];
+            const double x = A[(size_t)k * n + (k + 1 + i)];
             v[i] = x;
             if (i > 0) tail += x * x;
         }
