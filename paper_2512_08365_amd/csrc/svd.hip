@@ -201,7 +201,10 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
 
 // Gram sides in (64, GRAM_WHOLE]: one workgroup per (task, chunk of
 // GRAM_CHUNK_WHOLE columns) makes every tile of the upper triangle.  Each
-// step of WSTEP columns stages the chunk's K rows once (the blocked kernel stages every row
+// step of WSTEP columns (11 elements per thread, the last one of some threads
+// past the step and skipped; 48-column steps of 8 each: 0.223 against 0.216
+// ms for 128 [4096 x 128] unfoldings, fewer MFMAs per barrier) stages the
+// chunk's K rows once (the blocked kernel stages every row
 // block once per block pair: three times for K = 128), and WHOLE_WAVES waves
 // take WHOLE_TILES tiles each: tiles w, w + WHOLE_WAVES, ... of the upper
 // triangle in row order, so that with K = 128 (36 tiles) every SIMD holds nine
@@ -209,13 +212,12 @@ __global__ __launch_bounds__(GB * GB / 4) void k_gram(const SvdTask* tasks, int 
 // the result; each wave's tiles are independent accumulations, interleaved.
 constexpr int WHOLE_WAVES = 12;
 constexpr int WHOLE_TILES = 3;
-constexpr int WSTEP = 48;  // columns staged per step
+constexpr int WSTEP = 64;  // columns staged per step
 constexpr int WHOLE_THREADS = WHOLE_WAVES * GW;
-constexpr int WHOLE_GPER = GRAM_WHOLE * WSTEP / WHOLE_THREADS;  // staged elements per thread
+constexpr int WHOLE_GPER = (GRAM_WHOLE * WSTEP + WHOLE_THREADS - 1) / WHOLE_THREADS;
 static_assert(WHOLE_WAVES * WHOLE_TILES >= (GRAM_WHOLE / 16) * (GRAM_WHOLE / 16 + 1) / 2,
               "every upper-triangle tile has a wave");
-static_assert(WHOLE_THREADS % WSTEP == 0 && WHOLE_THREADS % GRAM_WHOLE == 0 &&
-              GRAM_WHOLE * WSTEP % WHOLE_THREADS == 0, "staging layout");
+static_assert(WHOLE_THREADS % WSTEP == 0 && WHOLE_THREADS % GRAM_WHOLE == 0, "staging layout");
 
 // the products of one staged step for a wave's WHOLE_TILES tiles: every
 // k-step's operands are read from LDS before the previous k-step's MFMAs
@@ -275,6 +277,8 @@ __device__ __forceinline__ void gram_whole_run(const SvdTask& t, int64_t b0, int
     const int tid = threadIdx.x, lane = tid % GW;
     const int rr0 = COLS_FAST ? tid / WSTEP : tid % KB;
     const int c0 = COLS_FAST ? tid % WSTEP : tid / KB;
+    // the last element of a thread may fall past the step (GPER rounded up)
+    const bool last_in = COLS_FAST ? rr0 + (GPER - 1) * RSTEP < KB : c0 + (GPER - 1) * CSTEP < WSTEP;
     typedef const __attribute__((address_space(1))) float* gfloat;
     const gfloat data = (gfloat)t.data;
     float stage[GPER];
@@ -283,10 +287,11 @@ __device__ __forceinline__ void gram_whole_run(const SvdTask& t, int64_t b0, int
         const int32_t* lo = loff + (s0 - b0);  // the step's columns (chunk-local)
 #pragma unroll
         for (int u = 0; u < GPER; ++u) {
-            const int c = c0 + u * CSTEP;
-            const int ro = roff[rr0 + u * RSTEP];
+            const bool in = u < GPER - 1 || last_in;
+            const int c = in ? c0 + u * CSTEP : 0;
+            const int ro = roff[in ? rr0 + u * RSTEP : 0];
             const int lc = lo[c];  // in the chunk's table even past its last column
-            const bool ok = c < cols && ro >= 0;
+            const bool ok = in && c < cols && ro >= 0;
             const float v = data[ok ? ro + lc : 0];  // element 0: a valid read
             stage[u] = ok ? v : 0.0f;
         }
@@ -296,7 +301,8 @@ __device__ __forceinline__ void gram_whole_run(const SvdTask& t, int64_t b0, int
     for (int64_t s0 = b0; s0 < b1; s0 += WSTEP) {
 #pragma unroll
         for (int u = 0; u < GPER; ++u)
-            xs[c0 + u * CSTEP][rr0 + u * RSTEP] = (double)stage[u];  // fp32 widened exactly
+            if (u < GPER - 1 || last_in)
+                xs[c0 + u * CSTEP][rr0 + u * RSTEP] = (double)stage[u];  // fp32 widened exactly
         __syncthreads();
         if (s0 + WSTEP < b1) fetch(s0 + WSTEP);  // in flight during the products
         whole_products(xs, ti, tj, r, kq, acc);
