@@ -219,9 +219,11 @@ static_assert(WHOLE_WAVES * WHOLE_TILES >= (GRAM_WHOLE / 16) * (GRAM_WHOLE / 16 
               "every upper-triangle tile has a wave");
 static_assert(WHOLE_THREADS % WSTEP == 0 && WHOLE_THREADS % GRAM_WHOLE == 0, "staging layout");
 
-// the products of one staged step for a wave's WHOLE_TILES tiles: every
-// k-step's operands are read from LDS before the previous k-step's MFMAs
-// issue, so the reads' latency overlaps the products; the full unroll makes
+// the products of one staged step for a wave's WHOLE_TILES tiles, written
+// with each k-step's operands read a step ahead (the compiler keeps a
+// k-step's six reads together ahead of its three MFMAs, reusing one set of
+// registers, and the SIMD's other waves cover their latency; the loop
+// written without it spilled 17 registers at the 80-VGPR limit); the full unroll makes
 // every LDS address a fixed offset from one register per operand
 __device__ __forceinline__ void whole_products(const double (*xs)[GRAM_WHOLE + 1],
                                                const int* ti, const int* tj, int r, int kq,
