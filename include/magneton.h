@@ -519,7 +519,9 @@ int mag_invariant_count(const mag_tensor* tensor, int32_t* n_unfoldings, int64_t
  * eigenvalue is within about 1e-13 of the largest (relative), so a singular
  * value far below the largest carries an absolute error near 3e-7 of it.
  * Gram sides up to 512 are reduced by one workgroup each, all unfoldings side
- * by side; larger ones (up to MAG_SVD_MAX_K) one after another, each
+ * by side, and their eigenvalues then bisected by waves spread over the whole
+ * device (the workspace holds each tridiagonal form between the two); larger
+ * ones (up to MAG_SVD_MAX_K) one after another, each
  * Householder step spread over the whole device (about 4 launches per row of
  * the Gram matrix, so a side of n costs some 4 n launches; the workspace then
  * also holds about (n / 256 + 4) n doubles of scratch).
