@@ -90,6 +90,29 @@ def test_closed_forms_on_the_gpu():
     assert np.allclose(h[S.canonical_masks(4).index(0b0011)], 1.0, atol=1e-7)
 
 
+@pytest.mark.parametrize("k,l", [(128, 600), (96, 257)])
+def test_clustered_spectra_whole_triangle_sides(k, l):
+    """Gram sides in (64, 128] (one workgroup per column chunk makes the whole
+    triangle) with repeated and clustered singular values, where bisection
+    has to separate equal eigenvalues: against the oracle on the same fp32
+    data, and against the singular values the matrix was built from (its
+    fp32 rounding moves them by about 1e-7 relative)."""
+    rng = np.random.default_rng(k + l)
+    q = rng.standard_normal((k, k))
+    u, _ = np.linalg.qr(q)
+    w, _ = np.linalg.qr(rng.standard_normal((l, k)))
+    parts = [np.full(k // 6, 10.0), np.full(k // 4, 5.0), 1.0 + 1e-6 * np.arange(k // 6),
+             np.linspace(1.5, 3.0, k // 6)]
+    sv = np.concatenate(parts)
+    sv = np.concatenate([sv, np.full(k - sv.size, 1e-3)])
+    X = ((u * sv) @ w.T).astype(np.float32)
+    log(f"[spectra] clustered {k} x {l}")
+    _, _, (got,) = _gpu_lists([X])
+    _assert_spectra(got, S.invariants(X), f"clustered {k} x {l}")
+    want = np.sort(sv)[::-1]
+    assert np.abs(got[0].astype(np.float64) - want).max() <= 1e-5 * want[0]
+
+
 def test_matching_planted_permutations():
     rng = np.random.default_rng(11)
     A = [rng.standard_normal(s).astype(np.float32) for s in
