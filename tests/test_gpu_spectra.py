@@ -113,6 +113,23 @@ def test_clustered_spectra_whole_triangle_sides(k, l):
     assert np.abs(got[0].astype(np.float64) - want).max() <= 1e-5 * want[0]
 
 
+def test_mixed_batch_in_one_call():
+    """One call over tensors of every Gram class (one 32-side block, the whole
+    triangle for sides in (64, 128], 64-side blocks, and sides above 512 on
+    the many-workgroup path), so the library's reordering of the unfoldings
+    by class and its numbering of the eigenvalue work items (large sides have
+    none) are checked against each tensor's own oracle lists, in input order."""
+    rng = np.random.default_rng(21)
+    shapes = [(5,), (100, 600), (600, 700), (3, 40, 1100), (17, 33), (2, 256, 4096), (65, 80),
+              (8, 64, 128), (1, 1)]
+    Ts = [rng.standard_normal(sh).astype(np.float32) for sh in shapes]
+    log(f"[spectra] mixed batch {shapes}")
+    _, _, got = _gpu_lists(Ts)
+    assert len(got) == len(Ts)
+    for T, g, sh in zip(Ts, got, shapes):
+        _assert_spectra(g, S.invariants(T), f"mixed {sh}")
+
+
 def test_matching_planted_permutations():
     rng = np.random.default_rng(11)
     A = [rng.standard_normal(s).astype(np.float32) for s in
